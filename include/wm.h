@@ -1,0 +1,204 @@
+/*
+ * wm.h - C ABI of the MI355X World-Model dream library (libwm.so).
+ *
+ * The library runs the data-parallel hot path of RLFlow's model-based agent
+ * (Parker, Alabed, Yoneki, arXiv 2205.01435):
+ *   - the batched "dream" rollout of the World Model: a controller picks an
+ *     action from [z_t, h_t] (section 3.4) among the valid ones (section
+ *     3.1.3), an LSTM core over [z_t, one-hot a_t] updates the hidden state,
+ *     and a mixture-density head samples z_{t+1} with temperature tau and
+ *     predicts reward and termination (section 3.3.2; the step returns next
+ *     state, reward and terminal flag as in section 3.1.1);
+ *   - the teacher-forced mixture negative log-likelihood pass that fits the
+ *     model (section 4.7, on random-agent data as in section 3.3.2);
+ *   - a single controller decision.
+ *
+ * Conventions (all entry points):
+ *   - Pointers are DEVICE pointers unless stated otherwise; `stream` is a
+ *     hipStream_t (NULL = the default stream).  Work is enqueued on that
+ *     stream and the call returns; the status covers argument checks and
+ *     launch errors only.
+ *   - The caller owns every buffer.  The library never allocates device
+ *     memory, keeps no pointer after the call returns and never
+ *     synchronises the stream.
+ *   - Matrices are row-major.  Time-major arrays are [T, B, ...].
+ *   - Dimensions: B trajectories / sequences, T steps, Z latent size (a
+ *     multiple of 8), H hidden size (a multiple of 16), A actions (1..2048),
+ *     K Gaussians per latent dimension (1..8).  Other values return
+ *     WM_ERR_UNSUPPORTED.
+ *   - Thread safety: calls may be made from several threads; calls that
+ *     share output or workspace buffers must be ordered by the caller.
+ *   - Random numbers: Philox4x32-10 (Salmon et al., SC'11) with key
+ *     (seed & 0xffffffff, seed >> 32) and counter (block, step, traj,
+ *     stream); uniform i of a stream is word i % 4 of block i / 4, mapped to
+ *     ((x >> 9) + 0.5) * 2^-23.  Streams: 0 controller Gumbel noise (index
+ *     = action), 1 component Gumbel noise (index = j*K + k), 2 Box-Muller
+ *     uniforms (index = latent dim), 3 done uniform (index 0).
+ */
+#ifndef WM_H
+#define WM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* hipStream_t without pulling in the HIP headers. */
+typedef struct ihipStream_t *wm_stream_t;
+
+typedef enum {
+  WM_OK = 0,
+  WM_ERR_INVALID_ARG = -1, /* null required pointer, bad size, tau <= 0, ...  */
+  WM_ERR_UNSUPPORTED = -2, /* dims outside the compiled kernels' range        */
+  WM_ERR_WORKSPACE = -3,   /* workspace smaller than wm_workspace_bytes()     */
+  WM_ERR_HIP = -4          /* a HIP call or launch failed; see wm_last_error  */
+} wm_status;
+
+typedef enum {
+  WM_FP32 = 0, /* fp32 weights and activations, fp32 accumulate            */
+  WM_BF16 = 1  /* bf16 weights and GEMM operands (z, h), fp32 accumulate,
+                  fp32 cell state and mixture arithmetic                    */
+} wm_dtype;
+
+enum {
+  WM_FLAG_DONE = 1u, /* sample the done head; else dones are 0 while live */
+  WM_FLAG_TRACE = 2u /* write h_trace / c_trace                            */
+};
+
+typedef struct {
+  int32_t Z, H, A, K;
+  int32_t dtype; /* wm_dtype */
+} wm_dims;
+
+/*
+ * Canonical weights, float32 device arrays (row-major [out, in]):
+ *   W_g [4H, Z+A+H]  LSTM gates, rows in blocks i | f | g | o, columns
+ *                    z | one-hot action | h; b_g [4H].
+ *   W_m [3ZK, H]     mixture head on h_{t+1}: row p*Z*K + j*K + k holds,
+ *                    for latent dim j and component k, the pi-logit (p=0),
+ *                    the mean (p=1) and log sigma (p=2); b_m [3ZK].
+ *   w_r [H], b_r [1] reward head on h_{t+1}.
+ *   w_d [H], b_d [1] done head on h_{t+1}: P(done) = sigmoid(w_d.h + b_d).
+ *   W_c [A, Z+H]     controller logits on [z_t, h_t] (section 3.4); b_c [A].
+ */
+typedef struct {
+  const float *W_g, *b_g;
+  const float *W_m, *b_m;
+  const float *w_r, *b_r;
+  const float *w_d, *b_d;
+  const float *W_c, *b_c;
+} wm_weights;
+
+/* Size in bytes of the packed (kernel-layout) weights for `dims`; 0 if the
+ * dims are invalid or unsupported. */
+size_t wm_packed_bytes(const wm_dims *dims);
+
+/* Convert canonical weights into the kernels' layout (gate-interleaved
+ * rows, one-hot block transposed for column gathers, mixture rows grouped
+ * per latent dimension, controller extended with the reward and done rows),
+ * rounding to bf16 (nearest, ties to even) when dims->dtype is WM_BF16.
+ * `packed` is a device buffer of at least wm_packed_bytes(dims) bytes.
+ * Enqueued on `stream`; the canonical arrays may be freed once it ran. */
+wm_status wm_pack_weights(const wm_dims *dims, const wm_weights *canon, void *packed,
+                          size_t packed_bytes, wm_stream_t stream);
+
+/* Workspace bytes needed by wm_rollout (which = 0) or wm_nll (which = 1)
+ * for B rows and T steps; wm_controller_step needs none.  0 on bad args. */
+size_t wm_workspace_bytes(const wm_dims *dims, int32_t B, int32_t T, int32_t which);
+
+/*
+ * One controller decision for B states (section 3.4, masked as in section
+ * 3.1.3): logits = W_c [q(z), q(h)] + b_c, where q rounds to bf16 on
+ * WM_BF16 and is the identity on WM_FP32.
+ *   z [B, Z], h [B, H]   float32 state.
+ *   valid_mask [B, A]    uint8, nonzero = action valid.
+ *   seed, step, traj0    Philox key and counter words; row b is trajectory
+ *                        traj0 + b.
+ *   probs [B, A]         nullable; softmax of the logits over the valid
+ *                        actions (exactly 0 on invalid ones; an all-invalid
+ *                        row is all 0).
+ *   action [B]           int32; argmax over valid a of logits_a - ln(-ln u_a)
+ *                        (a sample from `probs`), u_a uniform a of stream 0;
+ *                        ties go to the lowest index; -1 if none is valid.
+ */
+wm_status wm_controller_step(const wm_dims *dims, const void *packed, int32_t B,
+                             uint32_t traj0, const float *z, const float *h,
+                             const uint8_t *valid_mask, uint64_t seed, uint32_t step,
+                             float *probs, int32_t *action, wm_stream_t stream);
+
+/*
+ * B dream trajectories of T steps (sections 3.3.2 and 3.4).  Step t uses the
+ * absolute step s = step0 + t and trajectory traj0 + b in its counters.  For
+ * a live trajectory:
+ *   1. a_t = masked Gumbel-max of the controller logits on (z_t, h_t);
+ *   2. gates = W_z q(z_t) + W_h q(h_t) + W_g[:, Z + a_t] + b_g (the one-hot
+ *      product is a column gather), LSTM cell -> c_{t+1} (fp32) and
+ *      h_{t+1} (stored rounded to the dtype);
+ *   3. mixture parameters from h_{t+1}; for each latent dim j the component
+ *      k_j = argmax_k (pi_logit_jk / tau + Gumbel(stream 1, j*K + k));
+ *   4. z_{t+1,j} = mu_jk + exp(log_sigma_jk) * eps_j, eps from Box-Muller on
+ *      the stream-2 pair (2p, 2p+1) containing j (cos for even j, sin odd);
+ *   5. reward_t = w_r.h_{t+1} + b_r; done_t = sigmoid(w_d.h_{t+1} + b_d) > u
+ *      (stream 3) if WM_FLAG_DONE, else 0.
+ * A done trajectory is frozen for the remaining steps: action -1, reward 0,
+ * done 1, z copied, state unchanged.  A live trajectory with no valid action
+ * ends at that step with the same frozen outputs.
+ *
+ *   z0 [B, Z]            float32 initial latent.
+ *   h0, c0 [B, H]        float32 initial state, nullable (= 0).
+ *   done_io [B]          uint8, nullable: in = already done, out = done
+ *                        after the last step.
+ *   valid_mask [B, A]    uint8, constant over the rollout.
+ *   tau                  mixture temperature, finite and > 0.
+ *   z_out [T+1, B, Z]    float32; z_out[0] = z0.
+ *   actions [T, B]       int32.   rewards [T, B] float32.   dones [T, B] uint8.
+ *   h_T, c_T [B, H]      float32 final state, nullable.
+ *   h_trace, c_trace [T+1, B, H]  float32 state at the start of each step and
+ *                        after the last; required iff WM_FLAG_TRACE.
+ *   workspace            device buffer of wm_workspace_bytes(dims, B, T, 0).
+ * T = 0 is a no-op.  Results of trajectory b depend only on its own inputs,
+ * traj0 + b and the weights, not on B or the other rows.
+ */
+wm_status wm_rollout(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
+                     uint32_t traj0, uint32_t step0, const float *z0, const float *h0,
+                     const float *c0, uint8_t *done_io, const uint8_t *valid_mask,
+                     uint64_t seed, float tau, uint32_t flags, float *z_out,
+                     int32_t *actions, float *rewards, uint8_t *dones, float *h_T,
+                     float *c_T, float *h_trace, float *c_trace, void *workspace,
+                     size_t workspace_bytes, wm_stream_t stream);
+
+/*
+ * Teacher-forced MDN-RNN loss over B logged sequences of T steps (section
+ * 4.7; padding masked as in section 3.3.1).  With h_0 = c_0 = 0:
+ *   h_{t+1}, c_{t+1} = LSTM(W_z q(z_t) + W_h q(h_t) + W_g[:, Z + a_t] + b_g);
+ *   loglik[t,b]    = sum_j log sum_k pi_jk N(z_{t+1,j}; mu_jk, sigma_jk)
+ *                    (pi = softmax of the pi-logits, tau = 1);
+ *   reward_se[t,b] = (w_r.h_{t+1} + b_r - rewards[t,b])^2;
+ *   done_bce[t,b]  = softplus(rho) - dones[t,b] * rho, rho = w_d.h_{t+1} + b_d.
+ *   z [T+1, B, Z] float32; actions [T, B] int32 (outside [0, A) = no action,
+ *   a zero one-hot); rewards [T, B] float32; dones [T, B] uint8;
+ *   lengths [B] int32 nullable (= T): steps t >= lengths[b] output 0.
+ *   loglik, reward_se, done_bce [T, B] float32.
+ *   means [3] float32 nullable: (-sum loglik / (N Z), sum se / N,
+ *   sum bce / N) with N = sum of the clamped lengths (all 0 if N = 0).
+ *   workspace: wm_workspace_bytes(dims, B, T, 1) bytes.
+ */
+wm_status wm_nll(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
+                 const float *z, const int32_t *actions, const float *rewards,
+                 const uint8_t *dones, const int32_t *lengths, float *loglik,
+                 float *reward_se, float *done_bce, float *means, void *workspace,
+                 size_t workspace_bytes, wm_stream_t stream);
+
+/* Text of the last non-OK status on the calling thread ("" if none). */
+const char *wm_last_error(void);
+
+/* Library version string. */
+const char *wm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WM_H */

@@ -1,0 +1,220 @@
+"""ctypes binding of libwm.so: argument marshalling only.
+
+Every step of the hot path runs in the HIP library; this module turns torch
+device tensors into pointers, allocates caller-owned buffers with torch, and
+raises ``WmError`` on a non-OK status.  There is no fallback: if libwm.so is
+missing or fails to load, every entry point raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libwm.so")
+
+WM_OK, WM_ERR_INVALID_ARG, WM_ERR_UNSUPPORTED, WM_ERR_WORKSPACE, WM_ERR_HIP = 0, -1, -2, -3, -4
+WM_FP32, WM_BF16 = 0, 1
+WM_FLAG_DONE, WM_FLAG_TRACE = 1, 2
+_DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
+
+# Every symbol the C header declares.
+EXPORTS = ("wm_packed_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
+           "wm_rollout", "wm_nll", "wm_last_error", "wm_version")
+
+
+class WmError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"libwm status {status}: {msg}")
+        self.status = status
+
+
+class CDims(ctypes.Structure):
+    _fields_ = [("Z", ctypes.c_int32), ("H", ctypes.c_int32), ("A", ctypes.c_int32),
+                ("K", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class CWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("W_g", "b_g", "W_m", "b_m", "w_r", "b_r", "w_d", "b_d", "W_c", "b_c")]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libwm.so (once) and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise WmError(WM_ERR_UNSUPPORTED,
+                      f"{path} is missing: build it with `python -m paper_2205_01435_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, I32, U32, U64, F32, SZ = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32,
+                                 ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t)
+    pd = ctypes.POINTER(CDims)
+    lib.wm_packed_bytes.argtypes = [pd]
+    lib.wm_packed_bytes.restype = SZ
+    lib.wm_pack_weights.argtypes = [pd, ctypes.POINTER(CWeights), P, SZ, P]
+    lib.wm_pack_weights.restype = I32
+    lib.wm_workspace_bytes.argtypes = [pd, I32, I32, I32]
+    lib.wm_workspace_bytes.restype = SZ
+    lib.wm_controller_step.argtypes = [pd, P, I32, U32, P, P, P, U64, U32, P, P, P]
+    lib.wm_controller_step.restype = I32
+    lib.wm_rollout.argtypes = [pd, P, I32, I32, U32, U32, P, P, P, P, P, U64, F32, U32,
+                               P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.wm_rollout.restype = I32
+    lib.wm_nll.argtypes = [pd, P, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.wm_nll.restype = I32
+    lib.wm_last_error.argtypes = []
+    lib.wm_last_error.restype = ctypes.c_char_p
+    lib.wm_version.argtypes = []
+    lib.wm_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != WM_OK:
+        raise WmError(status, load().wm_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev_f32(x, device):
+    return torch.as_tensor(x, dtype=torch.float32).to(device).contiguous()
+
+
+@dataclass
+class Model:
+    """Packed weights on a device plus their dims."""
+
+    dims: CDims
+    packed: torch.Tensor
+    Z: int
+    H: int
+    A: int
+    K: int
+    dtype: str
+
+
+def make_dims(Z, H, A, K, dtype="fp32") -> CDims:
+    return CDims(Z, H, A, K, _DTYPES[dtype])
+
+
+def packed_bytes(dims: CDims) -> int:
+    return load().wm_packed_bytes(ctypes.byref(dims))
+
+
+def workspace_bytes(dims: CDims, B: int, T: int, which: int) -> int:
+    return load().wm_workspace_bytes(ctypes.byref(dims), B, T, which)
+
+
+def pack(weights: dict, Z: int, H: int, A: int, K: int, dtype: str = "fp32",
+         device="cuda") -> Model:
+    """Copy canonical float32 weights to the device and pack them."""
+    lib = load()
+    dims = make_dims(Z, H, A, K, dtype)
+    n = lib.wm_packed_bytes(ctypes.byref(dims))
+    if n == 0:
+        raise WmError(WM_ERR_UNSUPPORTED, lib.wm_last_error().decode())
+    canon = {k: _dev_f32(np_or_t, device).reshape(-1) for k, np_or_t in weights.items()}
+    packed = torch.empty(n, dtype=torch.uint8, device=device)
+    cw = CWeights(*[ctypes.c_void_p(canon[k].data_ptr()) for k in
+                    ("W_g", "b_g", "W_m", "b_m", "w_r", "b_r", "w_d", "b_d", "W_c", "b_c")])
+    _check(lib.wm_pack_weights(ctypes.byref(dims), ctypes.byref(cw), _ptr(packed), n, _stream()))
+    torch.cuda.current_stream().synchronize()  # canon tensors may be freed after return
+    return Model(dims, packed, Z, H, A, K, dtype)
+
+
+def controller_step(m: Model, z, h, mask, seed: int, step: int, traj0: int = 0,
+                    want_probs: bool = True):
+    """Returns (probs [B, A] or None, action [B] int32)."""
+    lib = load()
+    B = z.shape[0]
+    dev = m.packed.device
+    probs = torch.empty((B, m.A), dtype=torch.float32, device=dev) if want_probs else None
+    action = torch.empty(B, dtype=torch.int32, device=dev)
+    _check(lib.wm_controller_step(ctypes.byref(m.dims), _ptr(m.packed), B, traj0, _ptr(z),
+                                  _ptr(h), _ptr(mask), seed, step, _ptr(probs), _ptr(action),
+                                  _stream()))
+    return probs, action
+
+
+class RolloutBuffers:
+    """Caller-owned device buffers of one rollout shape (reusable across calls)."""
+
+    def __init__(self, m: Model, B: int, T: int, trace: bool = False, final_state: bool = True):
+        dev = m.packed.device
+        self.B, self.T = B, T
+        self.z_out = torch.empty((T + 1, B, m.Z), dtype=torch.float32, device=dev)
+        self.actions = torch.empty((T, B), dtype=torch.int32, device=dev)
+        self.rewards = torch.empty((T, B), dtype=torch.float32, device=dev)
+        self.dones = torch.empty((T, B), dtype=torch.uint8, device=dev)
+        self.h_T = torch.empty((B, m.H), dtype=torch.float32, device=dev) if final_state else None
+        self.c_T = torch.empty((B, m.H), dtype=torch.float32, device=dev) if final_state else None
+        self.h_trace = (torch.empty((T + 1, B, m.H), dtype=torch.float32, device=dev)
+                        if trace else None)
+        self.c_trace = (torch.empty((T + 1, B, m.H), dtype=torch.float32, device=dev)
+                        if trace else None)
+        nws = workspace_bytes(m.dims, B, T, 0)
+        self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+        self.ws_bytes = nws
+
+
+def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bool = True,
+            traj0: int = 0, step0: int = 0, h0=None, c0=None, done_io=None, trace: bool = False,
+            bufs: RolloutBuffers | None = None) -> RolloutBuffers:
+    """Launch wm_rollout on the current stream; returns the filled buffers."""
+    lib = load()
+    B = z0.shape[0]
+    if bufs is None:
+        bufs = RolloutBuffers(m, B, T, trace=trace)
+    flags = (WM_FLAG_DONE if done else 0) | (WM_FLAG_TRACE if trace else 0)
+    _check(lib.wm_rollout(
+        ctypes.byref(m.dims), _ptr(m.packed), B, T, traj0, step0, _ptr(z0), _ptr(h0), _ptr(c0),
+        _ptr(done_io), _ptr(mask), seed, tau, flags, _ptr(bufs.z_out), _ptr(bufs.actions),
+        _ptr(bufs.rewards), _ptr(bufs.dones), _ptr(bufs.h_T), _ptr(bufs.c_T),
+        _ptr(bufs.h_trace), _ptr(bufs.c_trace), _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
+    return bufs
+
+
+class NllBuffers:
+    def __init__(self, m: Model, B: int, T: int):
+        dev = m.packed.device
+        self.loglik = torch.empty((T, B), dtype=torch.float32, device=dev)
+        self.reward_se = torch.empty((T, B), dtype=torch.float32, device=dev)
+        self.done_bce = torch.empty((T, B), dtype=torch.float32, device=dev)
+        self.means = torch.empty(3, dtype=torch.float32, device=dev)
+        nws = workspace_bytes(m.dims, B, T, 1)
+        self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+        self.ws_bytes = nws
+
+
+def nll(m: Model, z, actions, rewards, dones, lengths=None,
+        bufs: NllBuffers | None = None) -> NllBuffers:
+    """Launch wm_nll on the current stream; returns the filled buffers."""
+    lib = load()
+    T, B = actions.shape
+    if bufs is None:
+        bufs = NllBuffers(m, B, T)
+    _check(lib.wm_nll(ctypes.byref(m.dims), _ptr(m.packed), B, T, _ptr(z), _ptr(actions),
+                      _ptr(rewards), _ptr(dones), _ptr(lengths), _ptr(bufs.loglik),
+                      _ptr(bufs.reward_se), _ptr(bufs.done_bce), _ptr(bufs.means),
+                      _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
+    return bufs
+
+
+def version() -> str:
+    return load().wm_version().decode()

@@ -1,0 +1,218 @@
+// C ABI of libwm: argument checks, workspace carving and dispatch to the HIP
+// launchers.  The semantics of each entry point are documented in
+// include/wm.h.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/wm.h"
+#include "wm_kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+wm_status fail(wm_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+wm_status ok() {
+  g_err.clear();
+  return WM_OK;
+}
+
+wm_status hip_fail(hipError_t e, const char* where) {
+  return fail(WM_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Checks the model dims; returns WM_OK and fills the layout.
+wm_status check_dims(const wm_dims* d, wm::Layout* L) {
+  if (!d) return fail(WM_ERR_INVALID_ARG, "dims is NULL");
+  if (d->Z <= 0 || d->H <= 0 || d->A <= 0 || d->K <= 0)
+    return fail(WM_ERR_INVALID_ARG, "dims must be positive (Z=%d H=%d A=%d K=%d)", d->Z, d->H,
+                d->A, d->K);
+  if (d->dtype != WM_FP32 && d->dtype != WM_BF16)
+    return fail(WM_ERR_INVALID_ARG, "unknown dtype %d", d->dtype);
+  if (d->Z % 8 != 0 || d->Z > 1024)
+    return fail(WM_ERR_UNSUPPORTED, "Z=%d: kernels need Z a multiple of 8, at most 1024", d->Z);
+  if (d->H % 16 != 0 || d->H > 8192)
+    return fail(WM_ERR_UNSUPPORTED, "H=%d: kernels need H a multiple of 16, at most 8192", d->H);
+  if (d->A > 2048) return fail(WM_ERR_UNSUPPORTED, "A=%d: at most 2048 actions", d->A);
+  if (d->K > 8) return fail(WM_ERR_UNSUPPORTED, "K=%d: at most 8 components", d->K);
+  *L = wm::make_layout(d->Z, d->H, d->A, d->K, d->dtype);
+  return WM_OK;
+}
+
+wm_status check_packed(const wm::Layout& L, const void* packed) {
+  if (!packed) return fail(WM_ERR_INVALID_ARG, "packed weights pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(packed) & 255u)
+    return fail(WM_ERR_INVALID_ARG, "packed weights must be 256-byte aligned");
+  (void)L;
+  return WM_OK;
+}
+
+uint32_t key_lo(uint64_t s) { return (uint32_t)(s & 0xffffffffu); }
+uint32_t key_hi(uint64_t s) { return (uint32_t)(s >> 32); }
+
+}  // namespace
+
+extern "C" {
+
+size_t wm_packed_bytes(const wm_dims* dims) {
+  wm::Layout L;
+  if (check_dims(dims, &L) != WM_OK) return 0;
+  return L.total;
+}
+
+size_t wm_workspace_bytes(const wm_dims* dims, int32_t B, int32_t T, int32_t which) {
+  wm::Layout L;
+  if (check_dims(dims, &L) != WM_OK || B <= 0 || T < 0) return 0;
+  if (which == 0) return wm::rollout_workspace_bytes(L, B);
+  if (which == 1) return wm::nll_workspace_bytes(L, B, T);
+  return 0;
+}
+
+wm_status wm_pack_weights(const wm_dims* dims, const wm_weights* c, void* packed,
+                          size_t packed_bytes, wm_stream_t stream) {
+  wm::Layout L;
+  wm_status st = check_dims(dims, &L);
+  if (st != WM_OK) return st;
+  if ((st = check_packed(L, packed)) != WM_OK) return st;
+  if (!c) return fail(WM_ERR_INVALID_ARG, "weights is NULL");
+  if (!c->W_g || !c->b_g || !c->W_m || !c->b_m || !c->w_r || !c->b_r || !c->w_d || !c->b_d ||
+      !c->W_c || !c->b_c)
+    return fail(WM_ERR_INVALID_ARG, "a canonical weight pointer is NULL");
+  if (packed_bytes < L.total)
+    return fail(WM_ERR_INVALID_ARG, "packed buffer has %zu bytes, needs %zu", packed_bytes, L.total);
+  wm::Packed P{L, packed};
+  hipError_t e = wm::launch_pack(P, packed, c->W_g, c->b_g, c->W_m, c->b_m, c->w_r, c->b_r, c->w_d,
+                                 c->b_d, c->W_c, c->b_c, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "wm_pack_weights");
+  return ok();
+}
+
+wm_status wm_controller_step(const wm_dims* dims, const void* packed, int32_t B, uint32_t traj0,
+                             const float* z, const float* h, const uint8_t* valid_mask,
+                             uint64_t seed, uint32_t step, float* probs, int32_t* action,
+                             wm_stream_t stream) {
+  wm::Layout L;
+  wm_status st = check_dims(dims, &L);
+  if (st != WM_OK) return st;
+  if ((st = check_packed(L, packed)) != WM_OK) return st;
+  if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
+  if (!z || !h || !valid_mask || !action)
+    return fail(WM_ERR_INVALID_ARG, "z, h, valid_mask and action are required");
+  if (!aligned16(z) || !aligned16(h)) return fail(WM_ERR_INVALID_ARG, "z and h must be 16-byte aligned");
+  wm::Packed P{L, packed};
+  hipError_t e = wm::launch_controller_step(P, B, traj0, z, h, valid_mask, key_lo(seed),
+                                            key_hi(seed), step, probs, action,
+                                            reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "wm_controller_step");
+  return ok();
+}
+
+wm_status wm_rollout(const wm_dims* dims, const void* packed, int32_t B, int32_t T,
+                     uint32_t traj0, uint32_t step0, const float* z0, const float* h0,
+                     const float* c0, uint8_t* done_io, const uint8_t* valid_mask, uint64_t seed,
+                     float tau, uint32_t flags, float* z_out, int32_t* actions, float* rewards,
+                     uint8_t* dones, float* h_T, float* c_T, float* h_trace, float* c_trace,
+                     void* workspace, size_t workspace_bytes, wm_stream_t stream) {
+  wm::Layout L;
+  wm_status st = check_dims(dims, &L);
+  if (st != WM_OK) return st;
+  if ((st = check_packed(L, packed)) != WM_OK) return st;
+  if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
+  if (T < 0) return fail(WM_ERR_INVALID_ARG, "T=%d must not be negative", T);
+  if (!(tau > 0.0f) || !isfinite(tau)) return fail(WM_ERR_INVALID_ARG, "tau must be finite and > 0");
+  if (flags & ~(uint32_t)(WM_FLAG_DONE | WM_FLAG_TRACE))
+    return fail(WM_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (!z0 || !valid_mask || !z_out || !actions || !rewards || !dones)
+    return fail(WM_ERR_INVALID_ARG, "z0, valid_mask, z_out, actions, rewards, dones are required");
+  if ((flags & WM_FLAG_TRACE) && (!h_trace || !c_trace))
+    return fail(WM_ERR_INVALID_ARG, "WM_FLAG_TRACE needs h_trace and c_trace");
+  if (!aligned16(z0) || !aligned16(z_out))
+    return fail(WM_ERR_INVALID_ARG, "z0 and z_out must be 16-byte aligned");
+  if ((int64_t)B * (T + 1) > (int64_t)1 << 30)
+    return fail(WM_ERR_UNSUPPORTED, "B*(T+1) too large");
+  if (T == 0) return ok();
+  const size_t need = wm::rollout_workspace_bytes(L, B);
+  if (!workspace || workspace_bytes < need)
+    return fail(WM_ERR_WORKSPACE, "rollout workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(WM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+
+  char* ws = reinterpret_cast<char*>(workspace);
+  wm::RolloutBufs R{};
+  R.B = B; R.T = T; R.traj0 = traj0; R.step0 = step0;
+  R.k0 = key_lo(seed); R.k1 = key_hi(seed);
+  R.tau = tau; R.flags = flags;
+  R.z0 = z0; R.h0 = h0; R.c0 = c0; R.done_io = done_io; R.mask = valid_mask;
+  R.z_out = z_out; R.actions = actions; R.rewards = rewards; R.dones = dones;
+  R.h_T = h_T; R.c_T = c_T; R.h_trace = h_trace; R.c_trace = c_trace;
+  size_t o = 0;
+  R.hbuf = ws + o; o = wm::wm_align256(o + (size_t)2 * B * L.H * L.esz);
+  R.c = reinterpret_cast<float*>(ws + o); o = wm::wm_align256(o + (size_t)B * L.H * 4);
+  R.done_state = reinterpret_cast<int32_t*>(ws + o);
+  wm::Packed P{L, packed};
+  hipError_t e = wm::launch_rollout(P, R, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "wm_rollout");
+  return ok();
+}
+
+wm_status wm_nll(const wm_dims* dims, const void* packed, int32_t B, int32_t T, const float* z,
+                 const int32_t* actions, const float* rewards, const uint8_t* dones,
+                 const int32_t* lengths, float* loglik, float* reward_se, float* done_bce,
+                 float* means, void* workspace, size_t workspace_bytes, wm_stream_t stream) {
+  wm::Layout L;
+  wm_status st = check_dims(dims, &L);
+  if (st != WM_OK) return st;
+  if ((st = check_packed(L, packed)) != WM_OK) return st;
+  if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
+  if (T < 0) return fail(WM_ERR_INVALID_ARG, "T=%d must not be negative", T);
+  if (!z || !actions || !rewards || !dones || !loglik || !reward_se || !done_bce)
+    return fail(WM_ERR_INVALID_ARG, "z, actions, rewards, dones and the three outputs are required");
+  if (!aligned16(z)) return fail(WM_ERR_INVALID_ARG, "z must be 16-byte aligned");
+  if ((int64_t)B * (T + 1) > (int64_t)1 << 30)
+    return fail(WM_ERR_UNSUPPORTED, "B*(T+1) too large");
+  if (T == 0) return ok();
+  const size_t need = wm::nll_workspace_bytes(L, B, T);
+  if (!workspace || workspace_bytes < need)
+    return fail(WM_ERR_WORKSPACE, "nll workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(WM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+
+  char* ws = reinterpret_cast<char*>(workspace);
+  const size_t M = (size_t)T * B;
+  wm::NllBufs N{};
+  N.B = B; N.T = T; N.z = z; N.actions = actions; N.rewards = rewards; N.dones = dones;
+  N.lengths = lengths; N.loglik = loglik; N.reward_se = reward_se; N.done_bce = done_bce;
+  N.means = means;
+  size_t o = 0;
+  N.trace = ws + o; o = wm::wm_align256(o + (size_t)(T + 1) * B * L.H * L.esz);
+  N.c = reinterpret_cast<float*>(ws + o); o = wm::wm_align256(o + (size_t)B * L.H * 4);
+  N.part = reinterpret_cast<float*>(ws + o); o = wm::wm_align256(o + M * (L.Z / 8) * 4);
+  N.head = reinterpret_cast<float*>(ws + o); o = wm::wm_align256(o + M * 2 * 4);
+  N.wgsum = reinterpret_cast<float*>(ws + o);
+  wm::Packed P{L, packed};
+  hipError_t e = wm::launch_nll(P, N, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "wm_nll");
+  return ok();
+}
+
+const char* wm_last_error(void) { return g_err.c_str(); }
+
+const char* wm_version(void) { return "libwm 0.1.0 (gfx950)"; }
+
+}  // extern "C"

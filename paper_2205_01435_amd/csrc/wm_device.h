@@ -1,0 +1,154 @@
+// Device helpers for the World-Model dream kernels (gfx950 / CDNA4).
+//
+// MFMA fragments: both GEMM operands are K-contiguous ([rows, K] row-major),
+// and every lane feeds 16 bytes per operand per step:
+//   fp32  v_mfma_f32_16x16x4_f32, four issues per 16-wide K slice; lane group
+//         g = lane / 16 owns k = 4g .. 4g+3 of the slice (one per issue);
+//   bf16  v_mfma_f32_16x16x32_bf16, one issue per 32-wide K slice; lane group
+//         g owns k = 8g .. 8g+7.
+// Any fixed assignment of k to (lane group, slot) gives the same dot product
+// as long as both operands use it, which they do.
+// Output block (16 x 16, fp32): lane l holds rows 4*(l/16) + v, v = 0..3, of
+// column l % 16.  Rows index output features (weights are the A operand) and
+// columns index batch rows, so each lane holds 4 consecutive features of one
+// batch row; the packed weight layouts put what an epilogue needs together
+// into those quartets.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wm {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t bf16_t;  // storage type of bfloat16 values
+
+// ---------------------------------------------------------------------------
+// bfloat16 storage: round to nearest, ties to even; NaN stays NaN.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t b = __float_as_uint(f);
+  if ((b & 0x7fffffffu) > 0x7f800000u) return (b >> 16) | 0x40u;
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return b >> 16;
+}
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+__device__ __forceinline__ float round_bf16(float f) { return bf16_bits_to_f32(f32_to_bf16_bits(f)); }
+
+__device__ __forceinline__ uint4 pack8_bf16(float4 a, float4 b) {
+  uint4 r;
+  r.x = f32_to_bf16_bits(a.x) | (f32_to_bf16_bits(a.y) << 16);
+  r.y = f32_to_bf16_bits(a.z) | (f32_to_bf16_bits(a.w) << 16);
+  r.z = f32_to_bf16_bits(b.x) | (f32_to_bf16_bits(b.y) << 16);
+  r.w = f32_to_bf16_bits(b.z) | (f32_to_bf16_bits(b.w) << 16);
+  return r;
+}
+
+template <typename DT> struct DType;
+template <> struct DType<float> {
+  static constexpr int VEC = 4;  // elements per 16 bytes
+  __device__ static float load(const float* p, long i) { return p[i]; }
+  __device__ static float round(float x) { return x; }
+  __device__ static void store(float* p, long i, float x) { p[i] = x; }
+};
+template <> struct DType<bf16_t> {
+  static constexpr int VEC = 8;
+  __device__ static float load(const bf16_t* p, long i) { return bf16_bits_to_f32(p[i]); }
+  __device__ static float round(float x) { return round_bf16(x); }
+  __device__ static void store(bf16_t* p, long i, float x) { p[i] = (bf16_t)f32_to_bf16_bits(x); }
+};
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 32x32->64 multiplies, high halves crossed with the other words and the key,
+// key bumped by the Weyl constants between rounds.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+  }
+  return c;
+}
+
+struct Rng {
+  uint32_t k0, k1;
+  __device__ __forceinline__ uint4 block(uint32_t blk, uint32_t step, uint32_t traj,
+                                         uint32_t stream) const {
+    return philox4x32_10(make_uint4(blk, step, traj, stream), k0, k1);
+  }
+};
+
+// ((x >> 9) + 1/2) * 2^-23: midpoint of one of 2^23 cells of (0, 1), exact.
+__device__ __forceinline__ float word_to_uniform(uint32_t x) {
+  return ((float)(x >> 9) + 0.5f) * 0x1p-23f;
+}
+__device__ __forceinline__ uint32_t word_of(uint4 w, int i) {
+  return i == 0 ? w.x : (i == 1 ? w.y : (i == 2 ? w.z : w.w));
+}
+__device__ __forceinline__ float gumbel(float u) { return -logf(-logf(u)); }
+__device__ __forceinline__ float sigmoidf(float x) { return 1.0f / (1.0f + expf(-x)); }
+
+enum : uint32_t { STREAM_CONTROLLER = 0, STREAM_COMPONENT = 1, STREAM_GAUSS = 2, STREAM_DONE = 3 };
+
+// ---------------------------------------------------------------------------
+// MFMA step on one 16-byte fragment per operand.
+// ---------------------------------------------------------------------------
+template <typename DT> struct Mfma;
+template <> struct Mfma<float> {
+  static constexpr int KSLICE = 16;
+  __device__ __forceinline__ static void step(f32x4& acc, uint4 a, uint4 b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+  }
+};
+template <> struct Mfma<bf16_t> {
+  static constexpr int KSLICE = 32;
+  __device__ __forceinline__ static void step(f32x4& acc, uint4 a, uint4 b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                  __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+  }
+};
+
+// 16 bytes of activations (row m, columns k .. k+VEC-1) converted to DT.
+// Columns [0, Kz) come from the float32 source xz, [Kz, Kz+Kh) from xh (SH
+// elements); anything else, and rows m >= M, read as zero.  Kz and Kh are
+// multiples of VEC, so a vector never straddles the two sources.
+template <typename DT, typename SH>
+__device__ __forceinline__ uint4 load_x16(const float* __restrict__ xz, long ldz, int Kz,
+                                          const SH* __restrict__ xh, long ldxh, int Kh,
+                                          int m, int M, int k) {
+  uint4 zero = make_uint4(0, 0, 0, 0);
+  if (m >= M) return zero;
+  if (k < Kz) {
+    const float* p = xz + (long)m * ldz + k;
+    if constexpr (sizeof(DT) == 4) {
+      return *reinterpret_cast<const uint4*>(p);
+    } else {
+      const float4* q = reinterpret_cast<const float4*>(p);
+      return pack8_bf16(q[0], q[1]);
+    }
+  }
+  k -= Kz;
+  if (k < Kh) {
+    const SH* p = xh + (long)m * ldxh + k;
+    if constexpr (sizeof(SH) == sizeof(DT)) {
+      return *reinterpret_cast<const uint4*>(p);
+    } else {
+      const float4* q = reinterpret_cast<const float4*>(p);
+      return pack8_bf16(q[0], q[1]);
+    }
+  }
+  return zero;
+}
+
+}  // namespace wm

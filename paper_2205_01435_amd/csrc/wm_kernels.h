@@ -1,0 +1,67 @@
+// Launch interface between the C ABI (wm_api.cpp) and the HIP kernels
+// (wm_kernels.hip).  Internal to libwm.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "wm_layout.h"
+
+namespace wm {
+
+// Arguments shared by every kernel: the packed weights and their layout.
+struct Packed {
+  Layout L;
+  const void* base;  // device pointer to the packed buffer
+};
+
+struct RolloutBufs {
+  int B, T;
+  uint32_t traj0, step0, k0, k1;  // k0, k1: Philox key words
+  float tau;
+  uint32_t flags;
+  const float *z0, *h0, *c0;
+  uint8_t* done_io;
+  const uint8_t* mask;
+  float* z_out;
+  int32_t* actions;
+  float* rewards;
+  uint8_t* dones;
+  float *h_T, *c_T, *h_trace, *c_trace;
+  void* hbuf;          // [2, B, H] dtype
+  float* c;            // [B, H]
+  int32_t* done_state; // [B]
+};
+
+struct NllBufs {
+  int B, T;
+  const float* z;
+  const int32_t* actions;
+  const float* rewards;
+  const uint8_t* dones;
+  const int32_t* lengths;
+  float *loglik, *reward_se, *done_bce, *means;
+  void* trace;   // [T+1, B, H] dtype
+  float* c;      // [B, H]
+  float* part;   // [T*B, NTd]
+  float* head;   // [T*B, 2]
+  float* wgsum;  // [nwg, 4]
+};
+
+size_t nll_workspace_bytes(const Layout& L, int B, int T);
+size_t rollout_workspace_bytes(const Layout& L, int B);
+
+hipError_t launch_pack(const Packed& P, void* packed, const float* W_g, const float* b_g,
+                       const float* W_m, const float* b_m, const float* w_r, const float* b_r,
+                       const float* w_d, const float* b_d, const float* W_c, const float* b_c,
+                       hipStream_t s);
+
+hipError_t launch_controller_step(const Packed& P, int B, uint32_t traj0, const float* z,
+                                  const float* h, const uint8_t* mask, uint32_t k0, uint32_t k1,
+                                  uint32_t step, float* probs, int32_t* action, hipStream_t s);
+
+hipError_t launch_rollout(const Packed& P, const RolloutBufs& R, hipStream_t s);
+
+hipError_t launch_nll(const Packed& P, const NllBufs& N, hipStream_t s);
+
+}  // namespace wm

@@ -1,0 +1,1107 @@
+// HIP kernels of libwm for gfx950 (MI355X).
+//
+// The dream rollout runs three kernels per step, each a GEMM on the MFMA
+// units with the step's arithmetic fused into its epilogue:
+//   k_ctrl   controller logits W_c [z_t, h_t] (+ reward/done rows on h_t),
+//            masked Gumbel-max action, resolution of the previous
+//            transition's reward and done flag;
+//   k_gates  gate GEMM [z_t, h_t] x W^T plus the gathered one-hot column,
+//            LSTM cell, state commit (frozen rows copy their state);
+//   k_mdn    mixture head on h_{t+1}, Gumbel-max component pick per latent
+//            dim, Box-Muller draw, z_{t+1} commit.
+// The NLL pass runs k_gates once per step (teacher-forced), then one k_mdn
+// over all T*B rows with a log-likelihood epilogue, then a deterministic
+// reduction.  Nothing here allocates memory.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "wm_device.h"
+#include "wm_kernels.h"
+
+namespace wm {
+
+static constexpr float kHalfLn2Pi = 0.91893853320467274178f;
+
+// ===========================================================================
+// Packing (one-time): canonical fp32 -> kernel layout, rounded to DT.
+// ===========================================================================
+template <typename DT>
+__global__ void k_pack(const Layout L, char* base, const float* __restrict__ W_g,
+                       const float* __restrict__ b_g, const float* __restrict__ W_m,
+                       const float* __restrict__ b_m, const float* __restrict__ w_r,
+                       const float* __restrict__ b_r, const float* __restrict__ w_d,
+                       const float* __restrict__ b_d, const float* __restrict__ W_c,
+                       const float* __restrict__ b_c) {
+  const int Z = L.Z, H = L.H, A = L.A, K = L.K, Q = L.Q;
+  const long cg = Z + A + H;  // canonical W_g row length
+  const int section = blockIdx.y;
+  const long stride = (long)gridDim.x * blockDim.x;
+  const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  DT* Wg = reinterpret_cast<DT*>(base + L.off_Wg);
+  DT* WaT = reinterpret_cast<DT*>(base + L.off_WaT);
+  float* bg = reinterpret_cast<float*>(base + L.off_bg);
+  DT* Wm = reinterpret_cast<DT*>(base + L.off_Wm);
+  float* bm = reinterpret_cast<float*>(base + L.off_bm);
+  DT* Wc = reinterpret_cast<DT*>(base + L.off_Wc);
+  float* bc = reinterpret_cast<float*>(base + L.off_bc);
+  const int head0 = 16 * Q * (Z / 4);
+  if (section == 0) {
+    for (long idx = i0; idx < (long)4 * H * L.ldk; idx += stride) {
+      const int r = (int)(idx / L.ldk), col = (int)(idx % L.ldk);
+      const long crow = (long)(r % 4) * H + r / 4;
+      float v = 0.f;
+      if (col < Z) v = W_g[crow * cg + col];
+      else if (col < Z + H) v = W_g[crow * cg + A + col];
+      DType<DT>::store(Wg, idx, v);
+    }
+  } else if (section == 1) {
+    for (long idx = i0; idx < (long)A * 4 * H; idx += stride) {
+      const int a = (int)(idx / (4 * H)), r = (int)(idx % (4 * H));
+      const long crow = (long)(r % 4) * H + r / 4;
+      DType<DT>::store(WaT, idx, W_g[crow * cg + Z + a]);
+    }
+  } else if (section == 2) {
+    for (long idx = i0; idx < 4 * H; idx += stride) bg[idx] = b_g[(idx % 4) * H + idx / 4];
+  } else if (section == 3 || section == 4) {
+    const long n = section == 3 ? (long)L.Nm * L.ldh : (long)L.Nm;
+    for (long idx = i0; idx < n; idx += stride) {
+      const int row = section == 3 ? (int)(idx / L.ldh) : (int)idx;
+      const int col = section == 3 ? (int)(idx % L.ldh) : 0;
+      float v = 0.f;
+      if (col < H) {
+        if (row >= head0) {
+          const int hr = row - head0;
+          if (section == 3) v = hr == 0 ? w_r[col] : (hr == 1 ? w_d[col] : 0.f);
+          else v = hr == 0 ? b_r[0] : (hr == 1 ? b_d[0] : 0.f);
+        } else {
+          const int J = row / (16 * Q), rem = row % (16 * Q);
+          const int q = rem / 16, g = (rem % 16) / 4, vv = rem % 4;
+          const int j = 4 * J + g, f = 4 * q + vv;
+          long canon = -1;
+          if (f < K) canon = (long)j * K + f;
+          else if (f < 2 * K) canon = (long)Z * K + (long)j * K + (f - K);
+          else if (f < 3 * K) canon = 2L * Z * K + (long)j * K + (f - 2 * K);
+          if (canon >= 0) v = section == 3 ? W_m[canon * H + col] : b_m[canon];
+        }
+      }
+      if (section == 3) DType<DT>::store(Wm, idx, v);
+      else bm[idx] = v;
+    }
+  } else if (section == 5) {
+    for (long idx = i0; idx < (long)L.Nc * L.ldk; idx += stride) {
+      const int row = (int)(idx / L.ldk), col = (int)(idx % L.ldk);
+      float v = 0.f;
+      if (col < Z + H) {
+        if (row < A) v = W_c[(long)row * (Z + H) + col];
+        else if (row == A && col >= Z) v = w_r[col - Z];
+        else if (row == A + 1 && col >= Z) v = w_d[col - Z];
+      }
+      DType<DT>::store(Wc, idx, v);
+    }
+  } else {
+    for (long idx = i0; idx < L.Nc; idx += stride)
+      bc[idx] = idx < A ? b_c[idx] : (idx == A ? b_r[0] : (idx == A + 1 ? b_d[0] : 0.f));
+  }
+}
+
+// ===========================================================================
+// GEMM tile, both operands staged through LDS (double buffered).
+//   acc[i][j] = W[n0 + (wn*NBW + i)*16 .. +16, :] . X[m0 + (wm*MBW + j)*16 .. +16, :]^T
+// W: [Nrows, ldw] DT (rows >= Nrows read as 0), K padded to Kpad.
+// X: columns [0, Kz) from xz (fp32), [Kz, Kz+Kh) from xh (SH), rows < M.
+// ===========================================================================
+template <typename DT, int NBW, int MBW, int WAVES_N, int WAVES_M, int BK>
+struct TileLds {
+  static constexpr int VEC = DType<DT>::VEC;
+  static constexpr int NT = 64 * WAVES_N * WAVES_M;
+  static constexpr int BN = 16 * NBW * WAVES_N;
+  static constexpr int BM = 16 * MBW * WAVES_M;
+  static constexpr int LDL = BK + VEC;  // padded LDS row (elements)
+  static constexpr int KV = BK / VEC;   // 16-byte vectors per row chunk
+  static constexpr int WV = BN * KV;
+  static constexpr int XV = BM * KV;
+  static constexpr int WIT = (WV + NT - 1) / NT;
+  static constexpr int XIT = (XV + NT - 1) / NT;
+  static constexpr int BUF = (BN + BM) * LDL;  // elements per stage
+  static constexpr int LDS_BYTES = 2 * BUF * (int)sizeof(DT);
+  static_assert(BK % Mfma<DT>::KSLICE == 0, "BK must be a multiple of the MFMA K slice");
+
+  template <typename SH>
+  __device__ __forceinline__ static void run(f32x4 (&acc)[NBW][MBW], const DT* __restrict__ W,
+                                             long ldw, int n0, int Nrows, int Kpad,
+                                             const float* __restrict__ xz, long ldz, int Kz,
+                                             const SH* __restrict__ xh, long ldxh, int Kh,
+                                             int m0, int M, DT* lds) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wn = wave % WAVES_N, wmi = wave / WAVES_N;
+    const int g = lane >> 4, r16 = lane & 15;
+#pragma unroll
+    for (int i = 0; i < NBW; ++i)
+#pragma unroll
+      for (int j = 0; j < MBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    uint4 wr[WIT], xr[XIT];
+    auto gload = [&](int k0) {
+#pragma unroll
+      for (int it = 0; it < WIT; ++it) {
+        const int v = tid + it * NT;
+        if (v < WV) {
+          const int r = v / KV, kv = v % KV, n = n0 + r;
+          wr[it] = n < Nrows ? *reinterpret_cast<const uint4*>(W + (long)n * ldw + k0 + kv * VEC)
+                             : make_uint4(0, 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int it = 0; it < XIT; ++it) {
+        const int v = tid + it * NT;
+        if (v < XV) {
+          const int r = v / KV, kv = v % KV;
+          xr[it] = load_x16<DT, SH>(xz, ldz, Kz, xh, ldxh, Kh, m0 + r, M, k0 + kv * VEC);
+        }
+      }
+    };
+    auto sstore = [&](int buf) {
+      DT* Wl = lds + buf * BUF;
+      DT* Xl = Wl + BN * LDL;
+#pragma unroll
+      for (int it = 0; it < WIT; ++it) {
+        const int v = tid + it * NT;
+        if (v < WV) *reinterpret_cast<uint4*>(Wl + (v / KV) * LDL + (v % KV) * VEC) = wr[it];
+      }
+#pragma unroll
+      for (int it = 0; it < XIT; ++it) {
+        const int v = tid + it * NT;
+        if (v < XV) *reinterpret_cast<uint4*>(Xl + (v / KV) * LDL + (v % KV) * VEC) = xr[it];
+      }
+    };
+
+    const int nk = Kpad / BK;
+    gload(0);
+    sstore(0);
+    __syncthreads();
+    for (int kc = 0; kc < nk; ++kc) {
+      const int cur = kc & 1;
+      if (kc + 1 < nk) gload((kc + 1) * BK);
+      const DT* Wl = lds + cur * BUF;
+      const DT* Xl = Wl + BN * LDL;
+#pragma unroll
+      for (int ks = 0; ks < BK; ks += Mfma<DT>::KSLICE) {
+        uint4 a[NBW], b[MBW];
+#pragma unroll
+        for (int i = 0; i < NBW; ++i)
+          a[i] = *reinterpret_cast<const uint4*>(Wl + ((wn * NBW + i) * 16 + r16) * LDL + ks + g * VEC);
+#pragma unroll
+        for (int j = 0; j < MBW; ++j)
+          b[j] = *reinterpret_cast<const uint4*>(Xl + ((wmi * MBW + j) * 16 + r16) * LDL + ks + g * VEC);
+#pragma unroll
+        for (int i = 0; i < NBW; ++i)
+#pragma unroll
+          for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], a[i], b[j]);
+      }
+      if (kc + 1 < nk) sstore(cur ^ 1);
+      __syncthreads();
+    }
+  }
+};
+
+// ===========================================================================
+// k_gates: g = W [z | h]^T + WaT[a] + b, LSTM cell, commit.
+// Rollout mode: a < 0 marks a frozen row, whose state is copied forward.
+// NLL mode: every row is live; a outside [0, A) adds no column.
+// ===========================================================================
+struct GatesArgs {
+  const void* Wg;
+  const void* WaT;
+  const float* bg;
+  long ldk;
+  int H, A, Z, M;
+  const float* xz;  // [M, Z] fp32
+  long ldz;
+  const void* h_in;  // [M, H] DT
+  void* h_out;       // [M, H] DT
+  float* c;          // [M, H] fp32, updated in place
+  const int32_t* act;
+  float* h_trace;  // [M, H] fp32 or null
+  float* c_trace;
+  int nll_mode;
+};
+
+template <typename DT, int NBW, int MBW, int WAVES_N, int WAVES_M, int BK>
+__global__ void __launch_bounds__(64 * WAVES_N * WAVES_M)
+    k_gates(const GatesArgs p) {
+  using Tl = TileLds<DT, NBW, MBW, WAVES_N, WAVES_M, BK>;
+  __shared__ __attribute__((aligned(16))) DT lds[Tl::LDS_BYTES / sizeof(DT)];
+  const int n0 = blockIdx.y * Tl::BN, m0 = blockIdx.x * Tl::BM;
+  f32x4 acc[NBW][MBW];
+  const DT* h_in = reinterpret_cast<const DT*>(p.h_in);
+  Tl::template run<DT>(acc, reinterpret_cast<const DT*>(p.Wg), p.ldk, n0, 4 * p.H, (int)p.ldk,
+                       p.xz, p.ldz, p.Z, h_in, p.H, p.H, m0, p.M, lds);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wn = wave % WAVES_N, wmi = wave / WAVES_N;
+  const int H = p.H;
+  DT* h_out = reinterpret_cast<DT*>(p.h_out);
+  const DT* WaT = reinterpret_cast<const DT*>(p.WaT);
+#pragma unroll
+  for (int j = 0; j < MBW; ++j) {
+    const int m = m0 + (wmi * MBW + j) * 16 + (lane & 15);
+    if (m >= p.M) continue;
+    const int a = p.act[m];
+    const bool live = p.nll_mode || a >= 0;
+    const bool gather = a >= 0 && a < p.A;
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) {
+      const int u = (n0 + (wn * NBW + i) * 16) / 4 + (lane >> 4);
+      if (u >= H) continue;
+      const long e = (long)m * H + u;
+      float hv, cv;
+      if (!live) {
+        hv = DType<DT>::load(h_in, e);
+        cv = p.c[e];
+        DType<DT>::store(h_out, e, hv);
+      } else {
+        const float4 bias = *reinterpret_cast<const float4*>(p.bg + 4 * u);
+        float wa0 = 0.f, wa1 = 0.f, wa2 = 0.f, wa3 = 0.f;
+        if (gather) {
+          const long o = (long)a * 4 * H + 4 * u;
+          wa0 = DType<DT>::load(WaT, o);
+          wa1 = DType<DT>::load(WaT, o + 1);
+          wa2 = DType<DT>::load(WaT, o + 2);
+          wa3 = DType<DT>::load(WaT, o + 3);
+        }
+        const float gi = acc[i][j][0] + bias.x + wa0;
+        const float gf = acc[i][j][1] + bias.y + wa1;
+        const float gg = acc[i][j][2] + bias.z + wa2;
+        const float go = acc[i][j][3] + bias.w + wa3;
+        cv = sigmoidf(gf) * p.c[e] + sigmoidf(gi) * tanhf(gg);
+        hv = DType<DT>::round(sigmoidf(go) * tanhf(cv));
+        p.c[e] = cv;
+        DType<DT>::store(h_out, e, hv);
+      }
+      if (p.h_trace) {
+        p.h_trace[e] = hv;
+        p.c_trace[e] = cv;
+      }
+    }
+  }
+}
+
+// ===========================================================================
+// k_mdn: mixture head on h_{t+1}.  Each wave owns one group of four latent
+// dims (Q output blocks), so each lane holds all features of one dim.
+// Rollout epilogue: component pick + Box-Muller + z commit.
+// NLL epilogue: per-dim log-likelihood, summed over the tile's dims; the
+// extra last tile column computes the reward / done logits.
+// ===========================================================================
+struct MdnArgs {
+  const void* Wm;
+  const float* bm;
+  long ldh;
+  int H, Z, K, Nm, M;
+  const void* h;  // [M, H] DT
+  // rollout
+  const int32_t* act;
+  const float* z_prev;  // [M, Z]
+  float* z_next;        // [M, Z]
+  uint32_t k0, k1, step, traj0;
+  float tau;
+  // nll
+  const float* z_tgt;  // [M, Z]
+  float* part;         // [M, ntd]
+  float* head;         // [M, 2]
+  int ntd;
+  int nll_mode;
+};
+
+template <typename DT, int Q, int MBW, int BK>
+__global__ void __launch_bounds__(256) k_mdn(const MdnArgs p) {
+  constexpr int WAVES_N = 2, WAVES_M = 2;
+  using Tl = TileLds<DT, Q, MBW, WAVES_N, WAVES_M, BK>;
+  __shared__ __attribute__((aligned(16))) DT lds[Tl::LDS_BYTES / sizeof(DT)];
+  __shared__ float red[WAVES_M][MBW * 16];
+  const int ntile = blockIdx.y;
+  const int n0 = ntile * Tl::BN, m0 = blockIdx.x * Tl::BM;
+  f32x4 acc[Q][MBW];
+  Tl::template run<DT>(acc, reinterpret_cast<const DT*>(p.Wm), p.ldh, n0, p.Nm, (int)p.ldh,
+                       nullptr, 0, 0, reinterpret_cast<const DT*>(p.h), p.H, p.H, m0, p.M, lds);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wn = wave % WAVES_N, wmi = wave / WAVES_N;
+  const int g = lane >> 4;
+  const int Z = p.Z, K = p.K;
+  const int J = ntile * WAVES_N + wn;  // dim group of this wave
+  const int j = 4 * J + g;             // latent dim of this lane
+  const bool head_tile = p.nll_mode && ntile == p.ntd;
+
+  if (head_tile) {
+    // Rows 0 and 1 of the block are the reward and done logits.
+    if (wn == 0 && g == 0) {
+#pragma unroll
+      for (int jj = 0; jj < MBW; ++jj) {
+        const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
+        if (m < p.M) {
+          p.head[2 * (long)m] = acc[0][jj][0] + p.bm[n0];
+          p.head[2 * (long)m + 1] = acc[0][jj][1] + p.bm[n0 + 1];
+        }
+      }
+    }
+    return;
+  }
+
+  // features f = 4q + v of dim j: acc[q][.][v] + bias
+  float bias[4 * Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const float4 b4 = *reinterpret_cast<const float4*>(p.bm + J * 16 * Q + 16 * q + 4 * g);
+    bias[4 * q] = b4.x; bias[4 * q + 1] = b4.y; bias[4 * q + 2] = b4.z; bias[4 * q + 3] = b4.w;
+  }
+
+  if (!p.nll_mode) {
+    const Rng rng{p.k0, p.k1};
+#pragma unroll
+    for (int jj = 0; jj < MBW; ++jj) {
+      const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
+      if (m >= p.M || j >= Z) continue;
+      const long e = (long)m * Z + j;
+      if (p.act[m] < 0) {
+        p.z_next[e] = p.z_prev[e];
+        continue;
+      }
+      float feat[4 * Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) feat[4 * q + v] = acc[q][jj][v] + bias[4 * q + v];
+      const uint32_t traj = p.traj0 + (uint32_t)m;
+      // Gumbel-max over k of logit/tau + G (stream 1, uniform j*K + k)
+      float best = -INFINITY;
+      int kbest = 0;
+      uint32_t cur = 0xffffffffu;
+      uint4 w = make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int f = 0; f < 4 * Q; ++f) {
+        if (f < K) {
+          const uint32_t idx = (uint32_t)j * K + f;
+          if ((idx >> 2) != cur) {
+            cur = idx >> 2;
+            w = rng.block(cur, p.step, traj, STREAM_COMPONENT);
+          }
+          const float s = feat[f] / p.tau + gumbel(word_to_uniform(word_of(w, idx & 3)));
+          if (s > best) { best = s; kbest = f; }
+        }
+      }
+      float mu = 0.f, ls = 0.f;
+#pragma unroll
+      for (int f = 0; f < 4 * Q; ++f) {
+        if (f == K + kbest) mu = feat[f];
+        if (f == 2 * K + kbest) ls = feat[f];
+      }
+      // Box-Muller on the pair (2p, 2p+1) of stream 2 that contains j
+      const uint4 wg = rng.block((uint32_t)j >> 2, p.step, traj, STREAM_GAUSS);
+      const float u1 = word_to_uniform(word_of(wg, j & 2));
+      const float u2 = word_to_uniform(word_of(wg, (j & 2) + 1));
+      const float r = sqrtf(-2.0f * logf(u1));
+      float sn, cs;
+      sincospif(2.0f * u2, &sn, &cs);
+      const float eps = (j & 1) ? r * sn : r * cs;
+      p.z_next[e] = mu + expf(ls) * eps;
+    }
+  } else {
+#pragma unroll
+    for (int jj = 0; jj < MBW; ++jj) {
+      const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
+      float ll = 0.f;
+      if (m < p.M && j < Z) {
+        float feat[4 * Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) feat[4 * q + v] = acc[q][jj][v] + bias[4 * q + v];
+        const float x = p.z_tgt[(long)m * Z + j];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int f = 0; f < 4 * Q; ++f)
+          if (f < K) mx = fmaxf(mx, feat[f]);
+        float se = 0.f;
+#pragma unroll
+        for (int f = 0; f < 4 * Q; ++f)
+          if (f < K) se += expf(feat[f] - mx);
+        const float lse_pi = mx + logf(se);
+        float terms[4 * Q];
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int f = 0; f < 4 * Q; ++f) {
+          terms[f] = -INFINITY;
+          if (f < K) {
+            float mu = 0.f, ls = 0.f;
+#pragma unroll
+            for (int f2 = 0; f2 < 4 * Q; ++f2) {
+              if (f2 == K + f) mu = feat[f2];
+              if (f2 == 2 * K + f) ls = feat[f2];
+            }
+            const float d = (x - mu) * expf(-ls);
+            terms[f] = (feat[f] - lse_pi) - 0.5f * d * d - ls - kHalfLn2Pi;
+            tmax = fmaxf(tmax, terms[f]);
+          }
+        }
+        float st = 0.f;
+#pragma unroll
+        for (int f = 0; f < 4 * Q; ++f)
+          if (f < K) st += expf(terms[f] - tmax);
+        ll = tmax + logf(st);
+      }
+      // sum over the four dims of the group (lane groups), then the two waves
+      ll += __shfl_xor(ll, 16);
+      ll += __shfl_xor(ll, 32);
+      if (wn == 1 && g == 0) red[wmi][jj * 16 + (lane & 15)] = ll;
+      __syncthreads();
+      if (wn == 0 && g == 0 && m < p.M)
+        p.part[(long)m * p.ntd + ntile] = ll + red[wmi][jj * 16 + (lane & 15)];
+      __syncthreads();
+    }
+  }
+}
+
+// ===========================================================================
+// k_ctrl: controller logits for BM = 16*MBW rows (all Nc outputs in one
+// block; four waves take interleaved 16-output slices), weights read
+// straight from global memory, activations staged through LDS in K chunks.
+//   mode 0: controller step (probs + action)
+//   mode 1: rollout step t: resolve transition t-1, choose a_t
+//   mode 2: rollout tail: resolve transition T-1 only
+// ===========================================================================
+struct CtrlArgs {
+  const void* Wc;
+  const float* bc;
+  long ldk;
+  int Z, H, A, Nc, M;
+  const float* z;  // [M, Z] fp32
+  long ldz;
+  const void* h;  // [M, H] SH
+  const uint8_t* mask;
+  uint32_t k0, k1, step, traj0;
+  int mode;
+  // mode 0
+  float* probs;
+  int32_t* action;
+  // mode 1/2
+  int32_t* act_t;       // [M]
+  const int32_t* act_prev;  // [M] or null (t == 0)
+  float* rew_prev;
+  uint8_t* done_prev;
+  float* rew_t;
+  uint8_t* done_t;
+  int32_t* done_state;
+  int use_done;
+};
+
+template <typename DT, typename SH, int NBW, int MBW, int BKC>
+__global__ void __launch_bounds__(256) k_ctrl(const CtrlArgs p) {
+  constexpr int VEC = DType<DT>::VEC;
+  constexpr int BM = 16 * MBW;
+  constexpr int LDL = BKC + VEC;
+  __shared__ __attribute__((aligned(16))) DT xl[BM * LDL];
+  __shared__ float s_best[4][BM];
+  __shared__ int s_idx[4][BM];
+  __shared__ float s_max[4][BM];
+  __shared__ float s_rho[BM][2];
+  __shared__ float s_fin[BM][2];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int m0 = blockIdx.x * BM;
+  const int nbtot = p.Nc / 16;
+  const DT* W = reinterpret_cast<const DT*>(p.Wc);
+  const SH* hsrc = reinterpret_cast<const SH*>(p.h);
+
+  f32x4 acc[NBW][MBW];
+#pragma unroll
+  for (int i = 0; i < NBW; ++i)
+#pragma unroll
+    for (int j = 0; j < MBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int kc = 0; kc < (int)p.ldk; kc += BKC) {
+    __syncthreads();
+    for (int v = tid; v < BM * (BKC / VEC); v += 256) {
+      const int r = v / (BKC / VEC), kv = v % (BKC / VEC);
+      *reinterpret_cast<uint4*>(xl + r * LDL + kv * VEC) =
+          load_x16<DT, SH>(p.z, p.ldz, p.Z, hsrc, p.H, p.H, m0 + r, p.M, kc + kv * VEC);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < BKC; ks += Mfma<DT>::KSLICE) {
+      if (kc + ks >= (int)p.ldk) break;  // last chunk may overhang the padded K
+      uint4 b[MBW];
+#pragma unroll
+      for (int j = 0; j < MBW; ++j)
+        b[j] = *reinterpret_cast<const uint4*>(xl + (j * 16 + r16) * LDL + ks + g * VEC);
+#pragma unroll
+      for (int i = 0; i < NBW; ++i) {
+        const int nb = wave + 4 * i;
+        if (nb < nbtot) {
+          const uint4 a = *reinterpret_cast<const uint4*>(W + (long)(nb * 16 + r16) * p.ldk + kc + ks + g * VEC);
+#pragma unroll
+          for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], a, b[j]);
+        }
+      }
+    }
+  }
+
+  // ---- epilogue ----
+  const Rng rng{p.k0, p.k1};
+  const int A = p.A;
+  const bool want_action = p.mode != 2;
+#pragma unroll
+  for (int j = 0; j < MBW; ++j) {
+    const int ml = j * 16 + r16;
+    const int m = m0 + ml;
+    float best = -INFINITY, mx = -INFINITY;
+    int bidx = -1;
+    if (m < p.M) {
+#pragma unroll
+      for (int i = 0; i < NBW; ++i) {
+        const int nb = wave + 4 * i;
+        if (nb >= nbtot) continue;
+        const int n = nb * 16 + 4 * g;
+        const float4 b4 = *reinterpret_cast<const float4*>(p.bc + n);
+        const float lg[4] = {acc[i][j][0] + b4.x, acc[i][j][1] + b4.y, acc[i][j][2] + b4.z,
+                             acc[i][j][3] + b4.w};
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          if (n + v == A) s_rho[ml][0] = lg[v];
+          if (n + v == A + 1) s_rho[ml][1] = lg[v];
+        }
+        if (want_action && n < A) {
+          const uint4 w = rng.block((uint32_t)(n >> 2), p.step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            if (n + v < A && p.mask[(long)m * A + n + v]) {
+              mx = fmaxf(mx, lg[v]);
+              const float s = lg[v] + gumbel(word_to_uniform(word_of(w, v)));
+              if (s > best) { best = s; bidx = n + v; }
+            }
+          }
+        }
+      }
+    }
+    // reduce over the four lane groups (same row), lowest index on ties
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float ob = __shfl_xor(best, off);
+      const int oi = __shfl_xor(bidx, off);
+      const float om = __shfl_xor(mx, off);
+      if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
+      mx = fmaxf(mx, om);
+    }
+    if (g == 0) {
+      s_best[wave][ml] = best;
+      s_idx[wave][ml] = bidx;
+      s_max[wave][ml] = mx;
+    }
+  }
+  __syncthreads();
+
+  if (p.mode == 0) {
+    // combine waves; then probabilities
+    if (tid < BM) {
+      float best = -INFINITY, mx = -INFINITY;
+      int bidx = -1;
+      for (int w = 0; w < 4; ++w) {
+        const float ob = s_best[w][tid];
+        const int oi = s_idx[w][tid];
+        if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
+        mx = fmaxf(mx, s_max[w][tid]);
+      }
+      s_fin[tid][0] = mx;
+      const int m = m0 + tid;
+      if (m < p.M) p.action[m] = bidx;
+    }
+    __syncthreads();
+    if (p.probs) {
+      // sum of exp(l - max) over valid actions
+#pragma unroll
+      for (int j = 0; j < MBW; ++j) {
+        const int ml = j * 16 + r16;
+        const int m = m0 + ml;
+        float se = 0.f;
+        if (m < p.M) {
+          const float mx = s_fin[ml][0];
+#pragma unroll
+          for (int i = 0; i < NBW; ++i) {
+            const int nb = wave + 4 * i;
+            if (nb >= nbtot) continue;
+            const int n = nb * 16 + 4 * g;
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+              if (n + v < A && p.mask[(long)m * A + n + v]) se += expf(acc[i][j][v] + p.bc[n + v] - mx);
+          }
+        }
+        se += __shfl_xor(se, 16);
+        se += __shfl_xor(se, 32);
+        if (g == 0) s_best[wave][ml] = se;
+      }
+      __syncthreads();
+      if (tid < BM) s_fin[tid][1] = s_best[0][tid] + s_best[1][tid] + s_best[2][tid] + s_best[3][tid];
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < MBW; ++j) {
+        const int ml = j * 16 + r16;
+        const int m = m0 + ml;
+        if (m >= p.M) continue;
+        const float mx = s_fin[ml][0], inv = s_fin[ml][1] > 0.f ? 1.0f / s_fin[ml][1] : 0.f;
+#pragma unroll
+        for (int i = 0; i < NBW; ++i) {
+          const int nb = wave + 4 * i;
+          if (nb >= nbtot) continue;
+          const int n = nb * 16 + 4 * g;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            if (n + v < A) {
+              const bool ok = p.mask[(long)m * A + n + v] != 0;
+              p.probs[(long)m * A + n + v] = ok ? expf(acc[i][j][v] + p.bc[n + v] - mx) * inv : 0.f;
+            }
+          }
+        }
+      }
+    }
+    return;
+  }
+
+  // rollout modes: one thread per row
+  if (tid < BM) {
+    const int m = m0 + tid;
+    if (m < p.M) {
+      int ds = p.done_state[m];
+      if (p.act_prev && p.act_prev[m] >= 0) {
+        // resolve transition t-1: reward and done head on h_t
+        const float rr = s_rho[tid][0], rd = s_rho[tid][1];
+        p.rew_prev[m] = rr;
+        int d = 0;
+        if (p.use_done) {
+          const uint4 w = rng.block(0, p.step - 1u, p.traj0 + (uint32_t)m, STREAM_DONE);
+          d = sigmoidf(rd) > word_to_uniform(w.x);
+        }
+        p.done_prev[m] = (uint8_t)d;
+        if (d) ds = 1;
+      }
+      if (p.mode == 1) {
+        int a = -1;
+        if (!ds) {
+          float best = -INFINITY;
+          for (int w = 0; w < 4; ++w) {
+            const float ob = s_best[w][tid];
+            const int oi = s_idx[w][tid];
+            if (oi >= 0 && (a < 0 || ob > best || (ob == best && oi < a))) { best = ob; a = oi; }
+          }
+          if (a < 0) ds = 1;  // no valid action: the trajectory ends here
+        }
+        p.act_t[m] = a;
+        if (a < 0) {
+          p.rew_t[m] = 0.f;
+          p.done_t[m] = 1;
+        }
+      }
+      p.done_state[m] = ds;
+    }
+  }
+}
+
+// ===========================================================================
+// small element-wise kernels
+// ===========================================================================
+template <typename DT>
+__global__ void k_rollout_init(int B, int Z, int H, const float* __restrict__ z0,
+                               const float* __restrict__ h0, const float* __restrict__ c0,
+                               const uint8_t* __restrict__ done_io, float* __restrict__ z_out,
+                               DT* __restrict__ hbuf, float* __restrict__ c,
+                               int32_t* __restrict__ done_state, float* __restrict__ h_trace,
+                               float* __restrict__ c_trace) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  for (long i = i0; i < (long)B * Z; i += stride) z_out[i] = z0[i];
+  for (long i = i0; i < (long)B * H; i += stride) {
+    const float hv = DType<DT>::round(h0 ? h0[i] : 0.f);
+    const float cv = c0 ? c0[i] : 0.f;
+    DType<DT>::store(hbuf, i, hv);
+    c[i] = cv;
+    if (h_trace) {
+      h_trace[i] = hv;
+      c_trace[i] = cv;
+    }
+  }
+  for (long i = i0; i < B; i += stride) done_state[i] = done_io ? (done_io[i] != 0) : 0;
+}
+
+template <typename DT>
+__global__ void k_rollout_finish(int B, int H, const DT* __restrict__ hbuf,
+                                 const float* __restrict__ c, const int32_t* __restrict__ done_state,
+                                 float* __restrict__ h_T, float* __restrict__ c_T,
+                                 uint8_t* __restrict__ done_io) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  for (long i = i0; i < (long)B * H; i += stride) {
+    if (h_T) h_T[i] = DType<DT>::load(hbuf, i);
+    if (c_T) c_T[i] = c[i];
+  }
+  if (done_io)
+    for (long i = i0; i < B; i += stride) done_io[i] = (uint8_t)done_state[i];
+}
+
+template <typename DT>
+__global__ void k_nll_init(long n, DT* __restrict__ trace0, float* __restrict__ c) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    DType<DT>::store(trace0, i, 0.f);
+    c[i] = 0.f;
+  }
+}
+
+// Per (t, b): sum the dim-tile partials, reward SE and done BCE from the head
+// logits, padding mask; one partial sum per block for the means.
+__global__ void __launch_bounds__(256)
+    k_nll_reduce(int T, int B, int ntd, const float* __restrict__ part,
+                 const float* __restrict__ head, const float* __restrict__ rewards,
+                 const uint8_t* __restrict__ dones, const int32_t* __restrict__ lengths,
+                 float* __restrict__ loglik, float* __restrict__ reward_se,
+                 float* __restrict__ done_bce, float* __restrict__ wgsum) {
+  __shared__ float s[4][256];
+  const long M = (long)T * B;
+  const long m = (long)blockIdx.x * 256 + threadIdx.x;
+  float ll = 0.f, se = 0.f, bce = 0.f, cnt = 0.f;
+  if (m < M) {
+    const int t = (int)(m / B), b = (int)(m % B);
+    int len = lengths ? lengths[b] : T;
+    len = len < 0 ? 0 : (len > T ? T : len);
+    if (t < len) {
+      for (int k = 0; k < ntd; ++k) ll += part[m * ntd + k];
+      const float rr = head[2 * m], rd = head[2 * m + 1];
+      const float dr = rr - rewards[m];
+      se = dr * dr;
+      bce = fmaxf(rd, 0.f) + log1pf(expf(-fabsf(rd))) - (dones[m] ? rd : 0.f);
+      cnt = 1.f;
+    }
+    loglik[m] = ll;
+    reward_se[m] = se;
+    done_bce[m] = bce;
+  }
+  s[0][threadIdx.x] = ll;
+  s[1][threadIdx.x] = se;
+  s[2][threadIdx.x] = bce;
+  s[3][threadIdx.x] = cnt;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w)
+      for (int k = 0; k < 4; ++k) s[k][threadIdx.x] += s[k][threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x < 4) wgsum[(long)blockIdx.x * 4 + threadIdx.x] = s[threadIdx.x][0];
+}
+
+__global__ void __launch_bounds__(256)
+    k_nll_means(int nwg, int Z, const float* __restrict__ wgsum, float* __restrict__ means) {
+  __shared__ double s[4][256];
+  double acc[4] = {0, 0, 0, 0};
+  for (int i = threadIdx.x; i < nwg; i += 256)
+    for (int k = 0; k < 4; ++k) acc[k] += wgsum[(long)i * 4 + k];
+  for (int k = 0; k < 4; ++k) s[k][threadIdx.x] = acc[k];
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w)
+      for (int k = 0; k < 4; ++k) s[k][threadIdx.x] += s[k][threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double n = s[3][0];
+    means[0] = n > 0 ? (float)(-s[0][0] / (n * Z)) : 0.f;
+    means[1] = n > 0 ? (float)(s[1][0] / n) : 0.f;
+    means[2] = n > 0 ? (float)(s[2][0] / n) : 0.f;
+  }
+}
+
+// ===========================================================================
+// host-side launch logic
+// ===========================================================================
+namespace {
+
+// fp32: 64 x 32 tiles (K slice 32); bf16: 128 x 128 tiles (K slice 64).
+template <typename DT> struct GatesCfg;
+template <> struct GatesCfg<float> {
+  static constexpr int NBW = 2, MBW = 1, WN = 2, WMv = 2, BK = 32;
+};
+template <> struct GatesCfg<bf16_t> {
+  static constexpr int NBW = 4, MBW = 4, WN = 2, WMv = 2, BK = 64;
+};
+template <typename DT> struct MdnCfg;
+template <> struct MdnCfg<float> { static constexpr int MBW = 1, BK = 32; };
+template <> struct MdnCfg<bf16_t> { static constexpr int MBW = 2, BK = 64; };
+template <typename DT> struct CtrlCfg;
+template <> struct CtrlCfg<float> { static constexpr int BKC = 64; };
+template <> struct CtrlCfg<bf16_t> { static constexpr int BKC = 128; };
+
+template <typename DT>
+hipError_t launch_gates(const GatesArgs& a, hipStream_t s) {
+  using C = GatesCfg<DT>;
+  using Tl = TileLds<DT, C::NBW, C::MBW, C::WN, C::WMv, C::BK>;
+  dim3 grid((a.M + Tl::BM - 1) / Tl::BM, (4 * a.H + Tl::BN - 1) / Tl::BN);
+  hipLaunchKernelGGL((k_gates<DT, C::NBW, C::MBW, C::WN, C::WMv, C::BK>), grid, dim3(Tl::NT), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename DT, int Q>
+hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
+  using C = MdnCfg<DT>;
+  using Tl = TileLds<DT, Q, C::MBW, 2, 2, C::BK>;
+  dim3 grid((a.M + Tl::BM - 1) / Tl::BM, ntiles);
+  hipLaunchKernelGGL((k_mdn<DT, Q, C::MBW, C::BK>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename DT>
+hipError_t launch_mdn(const MdnArgs& a, int Q, int ntiles, hipStream_t s) {
+  switch (Q) {
+    case 1: return launch_mdn_q<DT, 1>(a, ntiles, s);
+    case 2: return launch_mdn_q<DT, 2>(a, ntiles, s);
+    case 3: return launch_mdn_q<DT, 3>(a, ntiles, s);
+    case 4: return launch_mdn_q<DT, 4>(a, ntiles, s);
+    case 5: return launch_mdn_q<DT, 5>(a, ntiles, s);
+    case 6: return launch_mdn_q<DT, 6>(a, ntiles, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename DT, typename SH, int NBW, int MBW>
+hipError_t launch_ctrl_nb(const CtrlArgs& a, hipStream_t s) {
+  constexpr int BM = 16 * MBW;
+  dim3 grid((a.M + BM - 1) / BM);
+  hipLaunchKernelGGL((k_ctrl<DT, SH, NBW, MBW, CtrlCfg<DT>::BKC>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename DT, typename SH>
+hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
+  const int nb = (a.Nc / 16 + 3) / 4;  // output blocks per wave
+  if (nb <= 1) return launch_ctrl_nb<DT, SH, 1, 4>(a, s);
+  if (nb <= 2) return launch_ctrl_nb<DT, SH, 2, 4>(a, s);
+  if (nb <= 3) return launch_ctrl_nb<DT, SH, 3, 4>(a, s);
+  if (nb <= 5) return launch_ctrl_nb<DT, SH, 5, 4>(a, s);
+  if (nb <= 8) return launch_ctrl_nb<DT, SH, 8, 2>(a, s);
+  if (nb <= 12) return launch_ctrl_nb<DT, SH, 12, 2>(a, s);
+  if (nb <= 17) return launch_ctrl_nb<DT, SH, 17, 1>(a, s);
+  if (nb <= 24) return launch_ctrl_nb<DT, SH, 24, 1>(a, s);
+  if (nb <= 33) return launch_ctrl_nb<DT, SH, 33, 1>(a, s);
+  return hipErrorInvalidValue;
+}
+
+unsigned elem_grid(long n) {
+  long g = (n + 255) / 256;
+  if (g < 1) g = 1;
+  if (g > 4096) g = 4096;
+  return (unsigned)g;
+}
+
+template <typename DT>
+hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
+  const Layout& L = P.L;
+  const char* base = reinterpret_cast<const char*>(P.base);
+  const int B = R.B, T = R.T, Z = L.Z, H = L.H;
+  DT* hb = reinterpret_cast<DT*>(R.hbuf);
+  const long BH = (long)B * H, BZ = (long)B * Z;
+  const bool trace = (R.flags & 2u) != 0;
+  hipLaunchKernelGGL((k_rollout_init<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, R.z0,
+                     R.h0, R.c0, R.done_io, R.z_out, hb, R.c, R.done_state,
+                     trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  CtrlArgs ca{};
+  ca.Wc = base + L.off_Wc;
+  ca.bc = reinterpret_cast<const float*>(base + L.off_bc);
+  ca.ldk = L.ldk;
+  ca.Z = Z; ca.H = H; ca.A = L.A; ca.Nc = L.Nc; ca.M = B;
+  ca.ldz = Z;
+  ca.mask = R.mask;
+  ca.k0 = R.k0; ca.k1 = R.k1; ca.traj0 = R.traj0;
+  ca.done_state = R.done_state;
+  ca.use_done = (R.flags & 1u) != 0;
+
+  GatesArgs ga{};
+  ga.Wg = base + L.off_Wg;
+  ga.WaT = base + L.off_WaT;
+  ga.bg = reinterpret_cast<const float*>(base + L.off_bg);
+  ga.ldk = L.ldk;
+  ga.H = H; ga.A = L.A; ga.Z = Z; ga.M = B;
+  ga.ldz = Z;
+  ga.nll_mode = 0;
+  ga.c = R.c;
+
+  MdnArgs ma{};
+  ma.Wm = base + L.off_Wm;
+  ma.bm = reinterpret_cast<const float*>(base + L.off_bm);
+  ma.ldh = L.ldh;
+  ma.H = H; ma.Z = Z; ma.K = L.K; ma.Nm = L.Nm; ma.M = B;
+  ma.k0 = R.k0; ma.k1 = R.k1; ma.traj0 = R.traj0; ma.tau = R.tau;
+  ma.nll_mode = 0;
+  const int mdn_tiles = Z / 8;
+
+  for (int t = 0; t <= T; ++t) {
+    const uint32_t step = R.step0 + (uint32_t)t;
+    const DT* hcur = hb + (long)(t & 1) * BH;
+    ca.z = R.z_out + (long)t * BZ;
+    ca.h = hcur;
+    ca.step = step;
+    ca.mode = t < T ? 1 : 2;
+    ca.act_t = t < T ? R.actions + (long)t * B : nullptr;
+    ca.rew_t = t < T ? R.rewards + (long)t * B : nullptr;
+    ca.done_t = t < T ? R.dones + (long)t * B : nullptr;
+    ca.act_prev = t > 0 ? R.actions + (long)(t - 1) * B : nullptr;
+    ca.rew_prev = t > 0 ? R.rewards + (long)(t - 1) * B : nullptr;
+    ca.done_prev = t > 0 ? R.dones + (long)(t - 1) * B : nullptr;
+    e = launch_ctrl<DT, DT>(ca, s);
+    if (e != hipSuccess) return e;
+    if (t == T) break;
+
+    DT* hnext = hb + (long)((t + 1) & 1) * BH;
+    ga.xz = R.z_out + (long)t * BZ;
+    ga.h_in = hcur;
+    ga.h_out = hnext;
+    ga.act = R.actions + (long)t * B;
+    ga.h_trace = trace ? R.h_trace + (long)(t + 1) * BH : nullptr;
+    ga.c_trace = trace ? R.c_trace + (long)(t + 1) * BH : nullptr;
+    e = launch_gates<DT>(ga, s);
+    if (e != hipSuccess) return e;
+
+    ma.h = hnext;
+    ma.act = R.actions + (long)t * B;
+    ma.z_prev = R.z_out + (long)t * BZ;
+    ma.z_next = R.z_out + (long)(t + 1) * BZ;
+    ma.step = step;
+    e = launch_mdn<DT>(ma, L.Q, mdn_tiles, s);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((k_rollout_finish<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, H,
+                     hb + (long)(T & 1) * BH, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
+  return hipGetLastError();
+}
+
+template <typename DT>
+hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
+  const Layout& L = P.L;
+  const char* base = reinterpret_cast<const char*>(P.base);
+  const int B = N.B, T = N.T, Z = L.Z, H = L.H;
+  const long BH = (long)B * H, BZ = (long)B * Z, M = (long)T * B;
+  DT* tr = reinterpret_cast<DT*>(N.trace);
+  hipLaunchKernelGGL((k_nll_init<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, BH, tr, N.c);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  GatesArgs ga{};
+  ga.Wg = base + L.off_Wg;
+  ga.WaT = base + L.off_WaT;
+  ga.bg = reinterpret_cast<const float*>(base + L.off_bg);
+  ga.ldk = L.ldk;
+  ga.H = H; ga.A = L.A; ga.Z = Z; ga.M = B;
+  ga.ldz = Z;
+  ga.nll_mode = 1;
+  ga.c = N.c;
+  for (int t = 0; t < T; ++t) {
+    ga.xz = N.z + (long)t * BZ;
+    ga.h_in = tr + (long)t * BH;
+    ga.h_out = tr + (long)(t + 1) * BH;
+    ga.act = N.actions + (long)t * B;
+    e = launch_gates<DT>(ga, s);
+    if (e != hipSuccess) return e;
+  }
+
+  const int ntd = Z / 8;
+  MdnArgs ma{};
+  ma.Wm = base + L.off_Wm;
+  ma.bm = reinterpret_cast<const float*>(base + L.off_bm);
+  ma.ldh = L.ldh;
+  ma.H = H; ma.Z = Z; ma.K = L.K; ma.Nm = L.Nm; ma.M = (int)M;
+  ma.h = tr + BH;
+  ma.z_tgt = N.z + BZ;
+  ma.part = N.part;
+  ma.head = N.head;
+  ma.ntd = ntd;
+  ma.nll_mode = 1;
+  e = launch_mdn<DT>(ma, L.Q, ntd + 1, s);
+  if (e != hipSuccess) return e;
+
+  const int nwg = (int)((M + 255) / 256);
+  hipLaunchKernelGGL(k_nll_reduce, dim3(nwg), dim3(256), 0, s, T, B, ntd, N.part, N.head,
+                     N.rewards, N.dones, N.lengths, N.loglik, N.reward_se, N.done_bce, N.wgsum);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (N.means) {
+    hipLaunchKernelGGL(k_nll_means, dim3(1), dim3(256), 0, s, nwg, Z, N.wgsum, N.means);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+}  // namespace
+
+size_t rollout_workspace_bytes(const Layout& L, int B) {
+  size_t o = 0;
+  o = wm_align256(o + (size_t)2 * B * L.H * L.esz);  // h ping-pong
+  o = wm_align256(o + (size_t)B * L.H * 4);          // c
+  o = wm_align256(o + (size_t)B * 4);                // done state
+  return o;
+}
+
+size_t nll_workspace_bytes(const Layout& L, int B, int T) {
+  const size_t M = (size_t)T * B;
+  size_t o = 0;
+  o = wm_align256(o + (size_t)(T + 1) * B * L.H * L.esz);  // h trace
+  o = wm_align256(o + (size_t)B * L.H * 4);                // c
+  o = wm_align256(o + M * (L.Z / 8) * 4);                  // dim-tile partials
+  o = wm_align256(o + M * 2 * 4);                          // reward / done logits
+  o = wm_align256(o + ((M + 255) / 256) * 4 * 4);          // block sums
+  return o;
+}
+
+hipError_t launch_pack(const Packed& P, void* packed, const float* W_g, const float* b_g,
+                       const float* W_m, const float* b_m, const float* w_r, const float* b_r,
+                       const float* w_d, const float* b_d, const float* W_c, const float* b_c,
+                       hipStream_t s) {
+  dim3 grid(1024, 7);
+  if (P.L.dt == 0)
+    hipLaunchKernelGGL(k_pack<float>, grid, dim3(256), 0, s, P.L, reinterpret_cast<char*>(packed),
+                       W_g, b_g, W_m, b_m, w_r, b_r, w_d, b_d, W_c, b_c);
+  else
+    hipLaunchKernelGGL(k_pack<bf16_t>, grid, dim3(256), 0, s, P.L, reinterpret_cast<char*>(packed),
+                       W_g, b_g, W_m, b_m, w_r, b_r, w_d, b_d, W_c, b_c);
+  return hipGetLastError();
+}
+
+hipError_t launch_controller_step(const Packed& P, int B, uint32_t traj0, const float* z,
+                                  const float* h, const uint8_t* mask, uint32_t k0, uint32_t k1,
+                                  uint32_t step, float* probs, int32_t* action, hipStream_t s) {
+  const Layout& L = P.L;
+  const char* base = reinterpret_cast<const char*>(P.base);
+  CtrlArgs ca{};
+  ca.Wc = base + L.off_Wc;
+  ca.bc = reinterpret_cast<const float*>(base + L.off_bc);
+  ca.ldk = L.ldk;
+  ca.Z = L.Z; ca.H = L.H; ca.A = L.A; ca.Nc = L.Nc; ca.M = B;
+  ca.z = z; ca.ldz = L.Z;
+  ca.h = h;
+  ca.mask = mask;
+  ca.k0 = k0; ca.k1 = k1; ca.step = step; ca.traj0 = traj0;
+  ca.mode = 0;
+  ca.probs = probs;
+  ca.action = action;
+  if (L.dt == 0) return launch_ctrl<float, float>(ca, s);
+  return launch_ctrl<bf16_t, float>(ca, s);
+}
+
+hipError_t launch_rollout(const Packed& P, const RolloutBufs& R, hipStream_t s) {
+  return P.L.dt == 0 ? rollout_impl<float>(P, R, s) : rollout_impl<bf16_t>(P, R, s);
+}
+
+hipError_t launch_nll(const Packed& P, const NllBufs& N, hipStream_t s) {
+  return P.L.dt == 0 ? nll_impl<float>(P, N, s) : nll_impl<bf16_t>(P, N, s);
+}
+
+}  // namespace wm
