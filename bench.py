@@ -1,0 +1,285 @@
+#!/usr/bin/env python3
+"""Throughput of the World-Model dream hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+  * a dream rollout of B = 256 trajectories x T = 50 steps (Z = 64, H = 512,
+    A = 64, K = 5, fp32): controller, LSTM core, mixture sampling, reward and
+    done heads, freeze/commit;
+  * a teacher-forced mixture-NLL pass over B = 256 logged sequences of T = 50
+    steps with the same model (random-agent data: AR(1) latents, uniform valid
+    actions, N(0, 0.1^2) rewards, Bernoulli(1/T) dones).
+value = B * T / seconds per step (each transition is both dreamed and
+scored).  Inputs are resident in HBM before the timed region; weights are
+packed once, outside it.
+
+Prints ONE JSON line (rank 0, N = 1).  --gpus above 1 exits with a message:
+this build measures one GPU.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "imagined transitions/sec (B×T) + MDN-NLL tokens/sec; % of MFMA/HBM peak"
+PEAK = {"fp32": 157.3e12, "bf16": 2516.6e12}  # dense MFMA, FLOP/s
+HBM_PEAK = 8.0e12  # B/s
+
+
+def flops_per_transition(w) -> float:
+    """Algorithmic flops of one dream transition (the one-hot product is a
+    column gather and is not counted)."""
+    Z, H, A, K = w.Z, w.H, w.A, w.K
+    return 2.0 * (4 * H * (Z + H) + 3 * Z * K * H + A * (Z + H) + 2 * H)
+
+
+def flops_per_token(w) -> float:
+    Z, H, K = w.Z, w.H, w.K
+    return 2.0 * (4 * H * (Z + H) + 3 * Z * K * H + 2 * H)
+
+
+def kernel_flops_per_launch(name: str, w, B: int, T: int) -> float:
+    """Algorithmic flops of one launch of a kernel class in the bench step."""
+    Z, H, A, K = w.Z, w.H, w.A, w.K
+    if name == "gates":
+        return 2.0 * B * 4 * H * (Z + H)
+    if name == "ctrl":
+        return 2.0 * B * (A * (Z + H) + 2 * H)
+    if name == "mdn":
+        raise ValueError("mdn launches differ between rollout and NLL")
+    return 0.0
+
+
+def weight_stream_bytes_per_step(w) -> float:
+    """Bytes of weights a step must move if nothing stays on chip (all
+    matrices at their precision + fp32 biases + min(B, A) gathered columns)."""
+    esz = 4 if w.dtype == "fp32" else 2
+    Z, H, A, K = w.Z, w.H, w.A, w.K
+    mats = 4 * H * (Z + H) + 3 * Z * K * H + 2 * H + A * (Z + H)
+    gathered = min(w.B, A) * 4 * H
+    biases = 4 * H + 3 * Z * K + 2 + A
+    return mats * esz + gathered * esz + biases * 4
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
+    ap.add_argument("--no-workloads", action="store_true", help="skip the per-workload table")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle sample budget")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} (WORLD_SIZE {world}) is not "
+              "supported: the rollout shards by trajectory with no exchange, so N GPUs run N "
+              "independent copies of this benchmark.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2205_01435_amd import _lib as wmlib
+    from paper_2205_01435_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wmlib.load()
+    dev = torch.device("cuda:0")
+
+    def cuda(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    w = wl.WORKLOADS["medium_rollout"]
+    B, T = w.B, w.T
+    roll_in = wl.make_rollout_inputs(w)
+    nll_in = wl.make_nll_inputs(w.replace(kind="nll"))
+    model = wmlib.pack(roll_in["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+    z0, mask = cuda(roll_in["z0"]), cuda(roll_in["mask"])
+    nz, na = cuda(nll_in["z"]), cuda(nll_in["actions"])
+    nr, nd = cuda(nll_in["rewards"]), cuda(nll_in["dones"])
+    rbufs = wmlib.RolloutBuffers(model, B, T, trace=False)
+    nbufs = wmlib.NllBuffers(model, B, T)
+
+    def step(i):
+        wmlib.rollout(model, z0, mask, T=T, seed=w.seed + i, tau=w.tau, done=w.done, bufs=rbufs)
+        wmlib.nll(model, nz, na, nr, nd, bufs=nbufs)
+
+    # warmup, with every kernel class timed to find the dominant one
+    wmlib.profile_reset()
+    wmlib.profile_enable("")
+    for i in range(max(args.warmup, 1)):
+        step(i)
+    torch.cuda.synchronize()
+    classes = ["ctrl", "gates", "mdn", "init", "finish", "nll_init", "nll_reduce", "nll_means"]
+    warm = {c: wmlib.profile_read(c) for c in classes}
+    dominant = max(classes, key=lambda c: warm[c][0])
+    wmlib.profile_enable(None)
+    wmlib.profile_reset()
+
+    # timed region: K steps; the dominant kernel's launches are bracketed by
+    # HIP events on the stream they run on (the current torch stream)
+    wmlib.profile_enable(dominant)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    ev0.record()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    ev1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_total = ev0.elapsed_time(ev1)
+    k_ms, k_n = wmlib.profile_read(dominant)
+    wmlib.profile_enable(None)
+    wmlib.profile_reset()
+    ms_step = ms_total / args.steps
+    value = B * T / (ms_step / 1e3)
+
+    # per-call breakdown (clean: no per-kernel events)
+    def time_calls(fn, reps):
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(reps):
+            fn(i)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    ms_roll = time_calls(lambda i: wmlib.rollout(model, z0, mask, T=T, seed=w.seed + i, tau=w.tau,
+                                                done=w.done, bufs=rbufs), 10)
+    ms_nll = time_calls(lambda i: wmlib.nll(model, nz, na, nr, nd, bufs=nbufs), 10)
+    live = int((rbufs.actions >= 0).sum().item())
+
+    # roofline of the dominant kernel
+    avg_ms = k_ms / max(k_n, 1)
+    if dominant == "mdn":
+        # mixed: rollout launches (B rows) and one NLL launch (B*T rows + head)
+        per_step = T * 2.0 * B * 3 * w.Z * w.K * w.H + 2.0 * B * T * (3 * w.Z * w.K + 2) * w.H
+        launches_per_step = T + 1
+        flops_launch = per_step / launches_per_step
+    elif dominant == "gates":
+        flops_launch = kernel_flops_per_launch("gates", w, B, T)
+    elif dominant == "ctrl":
+        flops_launch = 2.0 * B * (w.A * (w.Z + w.H) + 2 * w.H)
+    else:
+        flops_launch = 0.0
+    achieved = flops_launch / (avg_ms / 1e3) if avg_ms > 0 else 0.0
+    roofline = {"kernel": dominant, "bound": "mfma", "achieved": achieved / 1e12,
+                "peak": PEAK[w.dtype] / 1e12, "unit": "TFLOP/s",
+                "frac": achieved / PEAK[w.dtype], "traffic": None,
+                "avg_launch_us": avg_ms * 1e3, "launches": k_n,
+                "flops_per_launch": flops_launch}
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "transitions/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded; Xavier-uniform weights, N(0,1) latents, Bernoulli(0.3) masks)",
+        "config": {"workload": "medium_rollout: dream rollout B=256 T=50 Z=64 H=512 A=64 K=5 fp32 "
+                               "+ teacher-forced NLL over B=256 x T=50 logged sequences",
+                   "B": B, "T": T, "Z": w.Z, "H": w.H, "A": w.A, "K": w.K, "tau": w.tau},
+        "breakdown": {"rollout_ms": ms_roll, "nll_ms": ms_nll,
+                      "rollout_transitions_per_s": B * T / (ms_roll / 1e3),
+                      "nll_tokens_per_s": B * T / (ms_nll / 1e3),
+                      "live_transitions_last_rollout": live,
+                      "step_tflops": (B * T * (flops_per_transition(w) + flops_per_token(w)))
+                      / (ms_step / 1e3) / 1e12,
+                      "warmup_kernel_ms": {c: round(warm[c][0], 4) for c in classes},
+                      "wall_s_timed_region": t_wall},
+        "roofline": roofline,
+    }
+
+    if not args.no_workloads:
+        out["workloads"] = workload_table(wmlib, wl, torch, cuda)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, roll_in, nll_in, args.cpu_seconds)
+
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def workload_table(wmlib, wl, torch, cuda) -> dict:
+    """Whole-call timing of every workload (median of a few calls)."""
+    res = {}
+    for name, w in wl.WORKLOADS.items():
+        if w.kind == "rollout":
+            inp = wl.make_rollout_inputs(w)
+            m = wmlib.pack(inp["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+            z0, mask = cuda(inp["z0"]), cuda(inp["mask"])
+            bufs = wmlib.RolloutBuffers(m, w.B, w.T)
+            fn = lambda i: wmlib.rollout(m, z0, mask, T=w.T, seed=w.seed + i, tau=w.tau,  # noqa: E731
+                                         done=w.done, bufs=bufs)
+            fl = flops_per_transition(w)
+        else:
+            d = wl.make_nll_inputs(w)
+            m = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+            args = [cuda(d[k]) for k in ("z", "actions", "rewards", "dones")]
+            bufs = wmlib.NllBuffers(m, w.B, w.T)
+            fn = lambda i: wmlib.nll(m, *args, bufs=bufs)  # noqa: E731
+            fl = flops_per_token(w)
+        fn(0)
+        torch.cuda.synchronize()
+        times = []
+        for i in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn(i + 1)
+            b.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        ms = float(np.median(times))
+        n = w.B * w.T
+        row = {"ms": ms, "per_s": n / (ms / 1e3), "unit": "transitions/s" if w.kind == "rollout"
+               else "tokens/s", "tflops": n * fl / (ms / 1e3) / 1e12,
+               "frac_mfma_peak": n * fl / (ms / 1e3) / PEAK[w.dtype]}
+        if name == "tiny_rollout":
+            gb = weight_stream_bytes_per_step(w) * w.T
+            row["weight_stream_GBps"] = gb / (ms / 1e3) / 1e9
+            row["frac_hbm_peak"] = gb / (ms / 1e3) / HBM_PEAK
+        res[name] = row
+        del bufs, m
+        torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(w, roll_in, nll_in, budget_s: float) -> dict:
+    """The oracle as it stands, timed on this host's cores on the same batch."""
+    from oracle import wm as owm
+
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        threads = int(blas[0]["num_threads"]) if blas else 1
+    except Exception:  # noqa: BLE001
+        threads = 1
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        owm.rollout(roll_in["weights"], w.dims, roll_in["z0"], roll_in["mask"], T=w.T,
+                    seed=w.seed + reps, tau=w.tau, done_flag=w.done, dtype=w.dtype)
+        owm.nll(roll_in["weights"], w.dims, nll_in["z"], nll_in["actions"], nll_in["rewards"],
+                nll_in["dones"], dtype=w.dtype)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 50:
+            break
+    return {"value": w.B * w.T * reps / el, "unit": "transitions/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"full step (rollout + NLL, B={w.B}, T={w.T}) x {reps} in {el:.1f} s, "
+                      f"float64 numpy, {threads} BLAS threads, "
+                      f"{len(os.sched_getaffinity(0))} cores visible"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -191,6 +191,20 @@ wm_status wm_nll(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
                  float *reward_se, float *done_bce, float *means, void *workspace,
                  size_t workspace_bytes, wm_stream_t stream);
 
+/*
+ * Measurement aid (no counterpart in the paper).  While a prefix is set, every
+ * kernel launch of the library whose name starts with it is bracketed by HIP
+ * events on its stream.  Kernel names: "ctrl", "gates", "mdn", "init",
+ * "finish", "nll_init", "nll_reduce", "nll_means", "pack"; "" selects all,
+ * NULL turns timing off.  wm_profile_read waits for the recorded events and
+ * returns the summed duration (ms) and count of the launches whose name
+ * starts with `prefix` (NULL = all); wm_profile_reset forgets them.  Timing
+ * adds host work per launch; leave it off outside measurement runs.
+ */
+wm_status wm_profile_enable(const char *prefix);
+wm_status wm_profile_read(const char *prefix, double *total_ms, int64_t *launches);
+wm_status wm_profile_reset(void);
+
 /* Text of the last non-OK status on the calling thread ("" if none). */
 const char *wm_last_error(void);
 

@@ -24,7 +24,8 @@ _DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
 
 # Every symbol the C header declares.
 EXPORTS = ("wm_packed_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
-           "wm_rollout", "wm_nll", "wm_last_error", "wm_version")
+           "wm_rollout", "wm_nll", "wm_profile_enable", "wm_profile_read", "wm_profile_reset",
+           "wm_last_error", "wm_version")
 
 
 class WmError(RuntimeError):
@@ -71,6 +72,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_rollout.restype = I32
     lib.wm_nll.argtypes = [pd, P, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.wm_nll.restype = I32
+    lib.wm_profile_enable.argtypes = [ctypes.c_char_p]
+    lib.wm_profile_enable.restype = I32
+    lib.wm_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(ctypes.c_int64)]
+    lib.wm_profile_read.restype = I32
+    lib.wm_profile_reset.argtypes = []
+    lib.wm_profile_reset.restype = I32
     lib.wm_last_error.argtypes = []
     lib.wm_last_error.restype = ctypes.c_char_p
     lib.wm_version.argtypes = []
@@ -214,6 +222,24 @@ def nll(m: Model, z, actions, rewards, dones, lengths=None,
                       _ptr(bufs.reward_se), _ptr(bufs.done_bce), _ptr(bufs.means),
                       _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
     return bufs
+
+
+def profile_enable(prefix: str | None):
+    """Bracket launches of kernels whose name starts with ``prefix`` with HIP
+    events (None turns it off)."""
+    _check(load().wm_profile_enable(None if prefix is None else prefix.encode()))
+
+
+def profile_read(prefix: str | None = None) -> tuple[float, int]:
+    """(summed milliseconds, launch count) of the recorded launches."""
+    ms, n = ctypes.c_double(), ctypes.c_int64()
+    _check(load().wm_profile_read(None if prefix is None else prefix.encode(), ctypes.byref(ms),
+                                  ctypes.byref(n)))
+    return ms.value, n.value
+
+
+def profile_reset():
+    _check(load().wm_profile_reset())
 
 
 def version() -> str:

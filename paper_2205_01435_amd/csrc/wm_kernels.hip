@@ -18,6 +18,7 @@
 
 #include "wm_device.h"
 #include "wm_kernels.h"
+#include "wm_profile.h"
 
 namespace wm {
 
@@ -844,6 +845,7 @@ hipError_t launch_gates(const GatesArgs& a, hipStream_t s) {
   using C = GatesCfg<DT>;
   using Tl = TileLds<DT, C::NBW, C::MBW, C::WN, C::WMv, C::BK>;
   dim3 grid((a.M + Tl::BM - 1) / Tl::BM, (4 * a.H + Tl::BN - 1) / Tl::BN);
+  KTimer kt("gates", s);
   hipLaunchKernelGGL((k_gates<DT, C::NBW, C::MBW, C::WN, C::WMv, C::BK>), grid, dim3(Tl::NT), 0, s, a);
   return hipGetLastError();
 }
@@ -853,6 +855,7 @@ hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
   using C = MdnCfg<DT>;
   using Tl = TileLds<DT, Q, C::MBW, 2, 2, C::BK>;
   dim3 grid((a.M + Tl::BM - 1) / Tl::BM, ntiles);
+  KTimer kt("mdn", s);
   hipLaunchKernelGGL((k_mdn<DT, Q, C::MBW, C::BK>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -874,6 +877,7 @@ template <typename DT, typename SH, int NBW, int MBW>
 hipError_t launch_ctrl_nb(const CtrlArgs& a, hipStream_t s) {
   constexpr int BM = 16 * MBW;
   dim3 grid((a.M + BM - 1) / BM);
+  KTimer kt("ctrl", s);
   hipLaunchKernelGGL((k_ctrl<DT, SH, NBW, MBW, CtrlCfg<DT>::BKC>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -908,10 +912,14 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   DT* hb = reinterpret_cast<DT*>(R.hbuf);
   const long BH = (long)B * H, BZ = (long)B * Z;
   const bool trace = (R.flags & 2u) != 0;
-  hipLaunchKernelGGL((k_rollout_init<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, R.z0,
-                     R.h0, R.c0, R.done_io, R.z_out, hb, R.c, R.done_state,
-                     trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr);
-  hipError_t e = hipGetLastError();
+  hipError_t e;
+  {
+    KTimer kt("init", s);
+    hipLaunchKernelGGL((k_rollout_init<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, R.z0,
+                       R.h0, R.c0, R.done_io, R.z_out, hb, R.c, R.done_state,
+                       trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess) return e;
 
   CtrlArgs ca{};
@@ -979,6 +987,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
     e = launch_mdn<DT>(ma, L.Q, mdn_tiles, s);
     if (e != hipSuccess) return e;
   }
+  KTimer kt("finish", s);
   hipLaunchKernelGGL((k_rollout_finish<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, H,
                      hb + (long)(T & 1) * BH, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
   return hipGetLastError();
@@ -991,8 +1000,12 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   const int B = N.B, T = N.T, Z = L.Z, H = L.H;
   const long BH = (long)B * H, BZ = (long)B * Z, M = (long)T * B;
   DT* tr = reinterpret_cast<DT*>(N.trace);
-  hipLaunchKernelGGL((k_nll_init<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, BH, tr, N.c);
-  hipError_t e = hipGetLastError();
+  hipError_t e;
+  {
+    KTimer kt("nll_init", s);
+    hipLaunchKernelGGL((k_nll_init<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, BH, tr, N.c);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess) return e;
 
   GatesArgs ga{};
@@ -1029,11 +1042,15 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   if (e != hipSuccess) return e;
 
   const int nwg = (int)((M + 255) / 256);
-  hipLaunchKernelGGL(k_nll_reduce, dim3(nwg), dim3(256), 0, s, T, B, ntd, N.part, N.head,
-                     N.rewards, N.dones, N.lengths, N.loglik, N.reward_se, N.done_bce, N.wgsum);
-  e = hipGetLastError();
+  {
+    KTimer kt("nll_reduce", s);
+    hipLaunchKernelGGL(k_nll_reduce, dim3(nwg), dim3(256), 0, s, T, B, ntd, N.part, N.head,
+                       N.rewards, N.dones, N.lengths, N.loglik, N.reward_se, N.done_bce, N.wgsum);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess) return e;
   if (N.means) {
+    KTimer kt("nll_means", s);
     hipLaunchKernelGGL(k_nll_means, dim3(1), dim3(256), 0, s, nwg, Z, N.wgsum, N.means);
     e = hipGetLastError();
   }
@@ -1066,6 +1083,7 @@ hipError_t launch_pack(const Packed& P, void* packed, const float* W_g, const fl
                        const float* w_d, const float* b_d, const float* W_c, const float* b_c,
                        hipStream_t s) {
   dim3 grid(1024, 7);
+  KTimer kt("pack", s);
   if (P.L.dt == 0)
     hipLaunchKernelGGL(k_pack<float>, grid, dim3(256), 0, s, P.L, reinterpret_cast<char*>(packed),
                        W_g, b_g, W_m, b_m, w_r, b_r, w_d, b_d, W_c, b_c);
