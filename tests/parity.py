@@ -133,8 +133,10 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
         na = ~ok
         if na.any():
             assert np.all(g["dones"][t][sel][na] == 1) and np.all(g["rewards"][t][sel][na] == 0)
+        done_now = np.zeros(idx.size, bool)
+        done_now[ok] = dg
         new_live = live.copy()
-        new_live[idx] = ok & ~dg
+        new_live[idx] = ok & ~done_now
         live = new_live
     ties.check()
     return ties, n_live_steps
