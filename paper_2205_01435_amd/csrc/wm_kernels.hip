@@ -107,15 +107,26 @@ __global__ void k_pack(const Layout L, char* base, const float* __restrict__ W_g
 }
 
 // ===========================================================================
-// GEMM tile, both operands staged through LDS (double buffered).
+// GEMM core: a WG tile of BN weight rows x BM activation rows, both operands
+// staged through two LDS buffers, with global loads issued STAGES chunks
+// ahead into a ring of register stages so their latency overlaps the MFMAs.
+// Waves are laid out WAVES_M x WAVES_N x KSPLIT; the KSPLIT waves of one
+// (wm, wn) position take interleaved MFMA K slices of every chunk and are
+// summed through LDS at the end, so that only waves with kw == 0 hold the
+// result.
 //   acc[i][j] = W[n0 + (wn*NBW + i)*16 .. +16, :] . X[m0 + (wm*MBW + j)*16 .. +16, :]^T
 // W: [Nrows, ldw] DT (rows >= Nrows read as 0), K padded to Kpad.
 // X: columns [0, Kz) from xz (fp32), [Kz, Kz+Kh) from xh (SH), rows < M.
 // ===========================================================================
-template <typename DT, int NBW, int MBW, int WAVES_N, int WAVES_M, int BK>
-struct TileLds {
+template <typename DT_, int NBW_, int MBW_, int WAVES_N_, int WAVES_M_, int KSPLIT_, int BK_,
+          int STAGES_>
+struct Gemm {
+  using DT = DT_;
+  static constexpr int NBW = NBW_, MBW = MBW_, WAVES_N = WAVES_N_, WAVES_M = WAVES_M_;
+  static constexpr int KSPLIT = KSPLIT_, BK = BK_, STAGES = STAGES_;
   static constexpr int VEC = DType<DT>::VEC;
-  static constexpr int NT = 64 * WAVES_N * WAVES_M;
+  static constexpr int NWAVES = WAVES_N * WAVES_M * KSPLIT;
+  static constexpr int NT = 64 * NWAVES;
   static constexpr int BN = 16 * NBW * WAVES_N;
   static constexpr int BM = 16 * MBW * WAVES_M;
   static constexpr int LDL = BK + VEC;  // padded LDS row (elements)
@@ -124,9 +135,81 @@ struct TileLds {
   static constexpr int XV = BM * KV;
   static constexpr int WIT = (WV + NT - 1) / NT;
   static constexpr int XIT = (XV + NT - 1) / NT;
-  static constexpr int BUF = (BN + BM) * LDL;  // elements per stage
-  static constexpr int LDS_BYTES = 2 * BUF * (int)sizeof(DT);
+  static constexpr int BUF = (BN + BM) * LDL;  // elements per LDS buffer
+  static constexpr int NSLICE = BK / Mfma<DT>::KSLICE;
+  static constexpr int RED_BYTES = (KSPLIT - 1) * WAVES_N * WAVES_M * NBW * MBW * 64 * 16;
+  static constexpr int PIPE_BYTES = 2 * BUF * (int)sizeof(DT);
+  static constexpr int LDS_BYTES = PIPE_BYTES > RED_BYTES ? PIPE_BYTES : RED_BYTES;
   static_assert(BK % Mfma<DT>::KSLICE == 0, "BK must be a multiple of the MFMA K slice");
+  static_assert(NSLICE % KSPLIT == 0, "K slices must split evenly over the K waves");
+
+  __device__ static int kw() { return (threadIdx.x >> 6) % KSPLIT; }
+  __device__ static int wn() { return ((threadIdx.x >> 6) / KSPLIT) % WAVES_N; }
+  __device__ static int wm() { return (threadIdx.x >> 6) / (KSPLIT * WAVES_N); }
+
+  template <typename SH>
+  __device__ __forceinline__ static void gload(uint4 (&wr)[WIT], uint4 (&xr)[XIT],
+                                               const DT* __restrict__ W, long ldw, int n0,
+                                               int Nrows, int Kpad, const float* __restrict__ xz,
+                                               long ldz, int Kz, const SH* __restrict__ xh,
+                                               long ldxh, int Kh, int m0, int M, int k0) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int it = 0; it < WIT; ++it) {
+      const int v = tid + it * NT;
+      if (v < WV) {
+        const int r = v / KV, k = k0 + (v % KV) * VEC, n = n0 + r;
+        // the last chunk may overhang the padded K when BK does not divide it
+        wr[it] = (n < Nrows && k < Kpad) ? *reinterpret_cast<const uint4*>(W + (long)n * ldw + k)
+                                         : make_uint4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < XIT; ++it) {
+      const int v = tid + it * NT;
+      if (v < XV) {
+        const int r = v / KV, kv = v % KV;
+        xr[it] = load_x16<DT, SH>(xz, ldz, Kz, xh, ldxh, Kh, m0 + r, M, k0 + kv * VEC);
+      }
+    }
+  }
+
+  __device__ __forceinline__ static void sstore(const uint4 (&wr)[WIT], const uint4 (&xr)[XIT],
+                                                DT* buf) {
+    const int tid = threadIdx.x;
+    DT* Xl = buf + BN * LDL;
+#pragma unroll
+    for (int it = 0; it < WIT; ++it) {
+      const int v = tid + it * NT;
+      if (v < WV) *reinterpret_cast<uint4*>(buf + (v / KV) * LDL + (v % KV) * VEC) = wr[it];
+    }
+#pragma unroll
+    for (int it = 0; it < XIT; ++it) {
+      const int v = tid + it * NT;
+      if (v < XV) *reinterpret_cast<uint4*>(Xl + (v / KV) * LDL + (v % KV) * VEC) = xr[it];
+    }
+  }
+
+  __device__ __forceinline__ static void compute(f32x4 (&acc)[NBW][MBW], const DT* buf) {
+    const int lane = threadIdx.x & 63;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int wni = wn(), wmi = wm();
+    const DT* Xl = buf + BN * LDL;
+    for (int sl = kw(); sl < NSLICE; sl += KSPLIT) {
+      const int ks = sl * Mfma<DT>::KSLICE;
+      uint4 a[NBW], b[MBW];
+#pragma unroll
+      for (int i = 0; i < NBW; ++i)
+        a[i] = *reinterpret_cast<const uint4*>(buf + ((wni * NBW + i) * 16 + r16) * LDL + ks + g * VEC);
+#pragma unroll
+      for (int j = 0; j < MBW; ++j)
+        b[j] = *reinterpret_cast<const uint4*>(Xl + ((wmi * MBW + j) * 16 + r16) * LDL + ks + g * VEC);
+#pragma unroll
+      for (int i = 0; i < NBW; ++i)
+#pragma unroll
+        for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], a[i], b[j]);
+    }
+  }
 
   template <typename SH>
   __device__ __forceinline__ static void run(f32x4 (&acc)[NBW][MBW], const DT* __restrict__ W,
@@ -134,77 +217,82 @@ struct TileLds {
                                              const float* __restrict__ xz, long ldz, int Kz,
                                              const SH* __restrict__ xh, long ldxh, int Kh,
                                              int m0, int M, DT* lds) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wn = wave % WAVES_N, wmi = wave / WAVES_N;
-    const int g = lane >> 4, r16 = lane & 15;
 #pragma unroll
     for (int i = 0; i < NBW; ++i)
 #pragma unroll
       for (int j = 0; j < MBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    uint4 wr[WIT], xr[XIT];
-    auto gload = [&](int k0) {
+    uint4 wr[STAGES][WIT], xr[STAGES][XIT];
+    const int nk = (Kpad + BK - 1) / BK;
 #pragma unroll
-      for (int it = 0; it < WIT; ++it) {
-        const int v = tid + it * NT;
-        if (v < WV) {
-          const int r = v / KV, kv = v % KV, n = n0 + r;
-          wr[it] = n < Nrows ? *reinterpret_cast<const uint4*>(W + (long)n * ldw + k0 + kv * VEC)
-                             : make_uint4(0, 0, 0, 0);
-        }
-      }
-#pragma unroll
-      for (int it = 0; it < XIT; ++it) {
-        const int v = tid + it * NT;
-        if (v < XV) {
-          const int r = v / KV, kv = v % KV;
-          xr[it] = load_x16<DT, SH>(xz, ldz, Kz, xh, ldxh, Kh, m0 + r, M, k0 + kv * VEC);
-        }
-      }
-    };
-    auto sstore = [&](int buf) {
-      DT* Wl = lds + buf * BUF;
-      DT* Xl = Wl + BN * LDL;
-#pragma unroll
-      for (int it = 0; it < WIT; ++it) {
-        const int v = tid + it * NT;
-        if (v < WV) *reinterpret_cast<uint4*>(Wl + (v / KV) * LDL + (v % KV) * VEC) = wr[it];
-      }
-#pragma unroll
-      for (int it = 0; it < XIT; ++it) {
-        const int v = tid + it * NT;
-        if (v < XV) *reinterpret_cast<uint4*>(Xl + (v / KV) * LDL + (v % KV) * VEC) = xr[it];
-      }
-    };
-
-    const int nk = Kpad / BK;
-    gload(0);
-    sstore(0);
+    for (int s = 0; s < STAGES; ++s)
+      if (s < nk)
+        gload<SH>(wr[s], xr[s], W, ldw, n0, Nrows, Kpad, xz, ldz, Kz, xh, ldxh, Kh, m0, M, s * BK);
+    sstore(wr[0], xr[0], lds);
     __syncthreads();
-    for (int kc = 0; kc < nk; ++kc) {
-      const int cur = kc & 1;
-      if (kc + 1 < nk) gload((kc + 1) * BK);
-      const DT* Wl = lds + cur * BUF;
-      const DT* Xl = Wl + BN * LDL;
+    for (int kc0 = 0; kc0 < nk; kc0 += STAGES) {
 #pragma unroll
-      for (int ks = 0; ks < BK; ks += Mfma<DT>::KSLICE) {
-        uint4 a[NBW], b[MBW];
-#pragma unroll
-        for (int i = 0; i < NBW; ++i)
-          a[i] = *reinterpret_cast<const uint4*>(Wl + ((wn * NBW + i) * 16 + r16) * LDL + ks + g * VEC);
-#pragma unroll
-        for (int j = 0; j < MBW; ++j)
-          b[j] = *reinterpret_cast<const uint4*>(Xl + ((wmi * MBW + j) * 16 + r16) * LDL + ks + g * VEC);
-#pragma unroll
-        for (int i = 0; i < NBW; ++i)
-#pragma unroll
-          for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], a[i], b[j]);
+      for (int s = 0; s < STAGES; ++s) {
+        const int kc = kc0 + s;
+        if (kc < nk) {
+          compute(acc, lds + (kc & 1) * BUF);
+          if (kc + 1 < nk) sstore(wr[(s + 1) % STAGES], xr[(s + 1) % STAGES], lds + ((kc + 1) & 1) * BUF);
+          if (kc + STAGES < nk)
+            gload<SH>(wr[s], xr[s], W, ldw, n0, Nrows, Kpad, xz, ldz, Kz, xh, ldxh, Kh, m0, M,
+                      (kc + STAGES) * BK);
+          __syncthreads();
+        }
       }
-      if (kc + 1 < nk) sstore(cur ^ 1);
+    }
+    if constexpr (KSPLIT > 1) {
+      // sum the K partials into the kw == 0 waves (LDS is free after the loop)
+      f32x4* red = reinterpret_cast<f32x4*>(lds);
+      const int lane = threadIdx.x & 63;
+      const int pos = wm() * WAVES_N + wn();
+      const int k = kw();
+      if (k > 0) {
+#pragma unroll
+        for (int i = 0; i < NBW; ++i)
+#pragma unroll
+          for (int j = 0; j < MBW; ++j)
+            red[((((k - 1) * WAVES_N * WAVES_M + pos) * NBW + i) * MBW + j) * 64 + lane] = acc[i][j];
+      }
+      __syncthreads();
+      if (k == 0) {
+        for (int kk = 1; kk < KSPLIT; ++kk)
+#pragma unroll
+          for (int i = 0; i < NBW; ++i)
+#pragma unroll
+            for (int j = 0; j < MBW; ++j)
+              acc[i][j] += red[((((kk - 1) * WAVES_N * WAVES_M + pos) * NBW + i) * MBW + j) * 64 + lane];
+      }
       __syncthreads();
     }
   }
 };
+
+// Work-group -> tile mapping.  Work-groups are dispatched round-robin over
+// the eight XCDs (each with its own L2); when there are at least eight
+// weight-row tiles, each XCD gets the work-groups of a fixed subset of them
+// (tile n on XCD n % 8), so every XCD streams only its slice of the weights
+// and keeps it in its L2 across calls.  Returns false for padding groups.
+__device__ __forceinline__ bool tile_of(int nt_count, int mt_count, int& nt, int& mt) {
+  const int L = blockIdx.x;
+  if (nt_count >= 8) {
+    const int xcd = L & 7, r = L >> 3;
+    nt = xcd + 8 * (r / mt_count);
+    mt = r % mt_count;
+    return nt < nt_count;
+  }
+  nt = L / mt_count;
+  mt = L % mt_count;
+  return nt < nt_count;
+}
+
+static inline unsigned grid_of(int nt_count, int mt_count) {
+  if (nt_count >= 8) return (unsigned)(8 * ((nt_count + 7) / 8) * mt_count);
+  return (unsigned)(nt_count * mt_count);
+}
 
 // ===========================================================================
 // k_gates: g = W [z | h]^T + WaT[a] + b, LSTM cell, commit.
@@ -228,19 +316,23 @@ struct GatesArgs {
   int nll_mode;
 };
 
-template <typename DT, int NBW, int MBW, int WAVES_N, int WAVES_M, int BK>
-__global__ void __launch_bounds__(64 * WAVES_N * WAVES_M)
-    k_gates(const GatesArgs p) {
-  using Tl = TileLds<DT, NBW, MBW, WAVES_N, WAVES_M, BK>;
-  __shared__ __attribute__((aligned(16))) DT lds[Tl::LDS_BYTES / sizeof(DT)];
-  const int n0 = blockIdx.y * Tl::BN, m0 = blockIdx.x * Tl::BM;
+template <class C>
+__global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
+  using DT = typename C::DT;
+  constexpr int NBW = C::NBW, MBW = C::MBW;
+  __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
+  DT* lds = reinterpret_cast<DT*>(lds_raw);
+  int nt, mt;
+  if (!tile_of((4 * p.H + C::BN - 1) / C::BN, (p.M + C::BM - 1) / C::BM, nt, mt)) return;
+  const int n0 = nt * C::BN, m0 = mt * C::BM;
   f32x4 acc[NBW][MBW];
   const DT* h_in = reinterpret_cast<const DT*>(p.h_in);
-  Tl::template run<DT>(acc, reinterpret_cast<const DT*>(p.Wg), p.ldk, n0, 4 * p.H, (int)p.ldk,
-                       p.xz, p.ldz, p.Z, h_in, p.H, p.H, m0, p.M, lds);
+  C::template run<DT>(acc, reinterpret_cast<const DT*>(p.Wg), p.ldk, n0, 4 * p.H, (int)p.ldk,
+                      p.xz, p.ldz, p.Z, h_in, p.H, p.H, m0, p.M, lds);
+  if (C::kw() != 0) return;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wn = wave % WAVES_N, wmi = wave / WAVES_N;
+  const int lane = threadIdx.x & 63;
+  const int wn = C::wn(), wmi = C::wm();
   const int H = p.H;
   DT* h_out = reinterpret_cast<DT*>(p.h_out);
   const DT* WaT = reinterpret_cast<const DT*>(p.WaT);
@@ -312,23 +404,28 @@ struct MdnArgs {
   float* part;         // [M, ntd]
   float* head;         // [M, 2]
   int ntd;
+  int ntiles;          // weight-row tiles in the grid
   int nll_mode;
 };
 
-template <typename DT, int Q, int MBW, int BK>
-__global__ void __launch_bounds__(256) k_mdn(const MdnArgs p) {
-  constexpr int WAVES_N = 2, WAVES_M = 2;
-  using Tl = TileLds<DT, Q, MBW, WAVES_N, WAVES_M, BK>;
-  __shared__ __attribute__((aligned(16))) DT lds[Tl::LDS_BYTES / sizeof(DT)];
+template <class C>
+__global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
+  using DT = typename C::DT;
+  constexpr int Q = C::NBW, MBW = C::MBW, WAVES_N = C::WAVES_N, WAVES_M = C::WAVES_M;
+  static_assert(WAVES_N == 2, "the NLL epilogue sums two dim groups per work-group");
+  __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
+  DT* lds = reinterpret_cast<DT*>(lds_raw);
   __shared__ float red[WAVES_M][MBW * 16];
-  const int ntile = blockIdx.y;
-  const int n0 = ntile * Tl::BN, m0 = blockIdx.x * Tl::BM;
+  int ntile, mt;
+  if (!tile_of(p.ntiles, (p.M + C::BM - 1) / C::BM, ntile, mt)) return;
+  const int n0 = ntile * C::BN, m0 = mt * C::BM;
   f32x4 acc[Q][MBW];
-  Tl::template run<DT>(acc, reinterpret_cast<const DT*>(p.Wm), p.ldh, n0, p.Nm, (int)p.ldh,
-                       nullptr, 0, 0, reinterpret_cast<const DT*>(p.h), p.H, p.H, m0, p.M, lds);
+  C::template run<DT>(acc, reinterpret_cast<const DT*>(p.Wm), p.ldh, n0, p.Nm, (int)p.ldh,
+                      nullptr, 0, 0, reinterpret_cast<const DT*>(p.h), p.H, p.H, m0, p.M, lds);
+  const bool owner = C::kw() == 0;  // holds the summed tile
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wn = wave % WAVES_N, wmi = wave / WAVES_N;
+  const int lane = threadIdx.x & 63;
+  const int wn = C::wn(), wmi = C::wm();
   const int g = lane >> 4;
   const int Z = p.Z, K = p.K;
   const int J = ntile * WAVES_N + wn;  // dim group of this wave
@@ -337,7 +434,7 @@ __global__ void __launch_bounds__(256) k_mdn(const MdnArgs p) {
 
   if (head_tile) {
     // Rows 0 and 1 of the block are the reward and done logits.
-    if (wn == 0 && g == 0) {
+    if (owner && wn == 0 && g == 0) {
 #pragma unroll
       for (int jj = 0; jj < MBW; ++jj) {
         const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
@@ -359,6 +456,7 @@ __global__ void __launch_bounds__(256) k_mdn(const MdnArgs p) {
   }
 
   if (!p.nll_mode) {
+    if (!owner) return;  // no barrier below
     const Rng rng{p.k0, p.k1};
 #pragma unroll
     for (int jj = 0; jj < MBW; ++jj) {
@@ -413,7 +511,7 @@ __global__ void __launch_bounds__(256) k_mdn(const MdnArgs p) {
     for (int jj = 0; jj < MBW; ++jj) {
       const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
       float ll = 0.f;
-      if (m < p.M && j < Z) {
+      if (owner && m < p.M && j < Z) {
         float feat[4 * Q];
 #pragma unroll
         for (int q = 0; q < Q; ++q)
@@ -455,9 +553,9 @@ __global__ void __launch_bounds__(256) k_mdn(const MdnArgs p) {
       // sum over the four dims of the group (lane groups), then the two waves
       ll += __shfl_xor(ll, 16);
       ll += __shfl_xor(ll, 32);
-      if (wn == 1 && g == 0) red[wmi][jj * 16 + (lane & 15)] = ll;
+      if (owner && wn == 1 && g == 0) red[wmi][jj * 16 + (lane & 15)] = ll;
       __syncthreads();
-      if (wn == 0 && g == 0 && m < p.M)
+      if (owner && wn == 0 && g == 0 && m < p.M)
         p.part[(long)m * p.ntd + ntile] = ll + red[wmi][jj * 16 + (lane & 15)];
       __syncthreads();
     }
@@ -498,7 +596,7 @@ struct CtrlArgs {
 };
 
 template <typename DT, typename SH, int NBW, int MBW, int BKC>
-__global__ void __launch_bounds__(256) k_ctrl(const CtrlArgs p) {
+__global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
   constexpr int VEC = DType<DT>::VEC;
   constexpr int BM = 16 * MBW;
   constexpr int LDL = BKC + VEC;
@@ -708,6 +806,199 @@ __global__ void __launch_bounds__(256) k_ctrl(const CtrlArgs p) {
   }
 }
 
+// k_ctrl: the same controller epilogue on the pipelined GEMM core, for
+// A + 2 <= 64 * NBW outputs: all Nc weight rows of a row block are staged
+// through LDS once per K chunk.  Waves with kw != 0 only help with the K
+// loop.  (k_ctrl_wide above reads the weights straight from global memory and
+// covers larger action counts.)
+template <class C, typename SH>
+__global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
+  using DT = typename C::DT;
+  constexpr int NBW = C::NBW, MBW = C::MBW, WN = C::WAVES_N, BM = C::BM;
+  __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
+  __shared__ float s_best[WN][BM];
+  __shared__ int s_idx[WN][BM];
+  __shared__ float s_max[WN][BM];
+  __shared__ float s_rho[BM][2];
+  __shared__ float s_fin[BM][2];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int m0 = blockIdx.x * BM;
+  const int nbtot = p.Nc / 16;
+  f32x4 acc[NBW][MBW];
+  C::template run<SH>(acc, reinterpret_cast<const DT*>(p.Wc), p.ldk, 0, p.Nc, (int)p.ldk, p.z,
+                      p.ldz, p.Z, reinterpret_cast<const SH*>(p.h), p.H, p.H, m0, p.M,
+                      reinterpret_cast<DT*>(lds_raw));
+  const bool owner = C::kw() == 0;
+  const int wn = C::wn(), wmi = C::wm();
+
+  const Rng rng{p.k0, p.k1};
+  const int A = p.A;
+  const bool want_action = p.mode != 2;
+  if (owner) {
+#pragma unroll
+    for (int j = 0; j < MBW; ++j) {
+      const int ml = (wmi * MBW + j) * 16 + r16;
+      const int m = m0 + ml;
+      float best = -INFINITY, mx = -INFINITY;
+      int bidx = -1;
+      if (m < p.M) {
+#pragma unroll
+        for (int i = 0; i < NBW; ++i) {
+          const int nb = wn * NBW + i;
+          if (nb >= nbtot) continue;
+          const int n = nb * 16 + 4 * g;
+          const float4 b4 = *reinterpret_cast<const float4*>(p.bc + n);
+          const float lg[4] = {acc[i][j][0] + b4.x, acc[i][j][1] + b4.y, acc[i][j][2] + b4.z,
+                               acc[i][j][3] + b4.w};
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            if (n + v == A) s_rho[ml][0] = lg[v];
+            if (n + v == A + 1) s_rho[ml][1] = lg[v];
+          }
+          if (want_action && n < A) {
+            const uint4 w = rng.block((uint32_t)(n >> 2), p.step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              if (n + v < A && p.mask[(long)m * A + n + v]) {
+                mx = fmaxf(mx, lg[v]);
+                const float sc = lg[v] + gumbel(word_to_uniform(word_of(w, v)));
+                if (sc > best) { best = sc; bidx = n + v; }
+              }
+            }
+          }
+        }
+      }
+      // reduce over the four lane groups (same row), lowest index on ties
+#pragma unroll
+      for (int off = 16; off <= 32; off <<= 1) {
+        const float ob = __shfl_xor(best, off);
+        const int oi = __shfl_xor(bidx, off);
+        const float om = __shfl_xor(mx, off);
+        if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
+        mx = fmaxf(mx, om);
+      }
+      if (g == 0) {
+        s_best[wn][ml] = best;
+        s_idx[wn][ml] = bidx;
+        s_max[wn][ml] = mx;
+      }
+    }
+  }
+  __syncthreads();
+
+  if (p.mode == 0) {
+    if (tid < BM) {
+      float best = -INFINITY, mx = -INFINITY;
+      int bidx = -1;
+      for (int w = 0; w < WN; ++w) {
+        const float ob = s_best[w][tid];
+        const int oi = s_idx[w][tid];
+        if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
+        mx = fmaxf(mx, s_max[w][tid]);
+      }
+      s_fin[tid][0] = mx;
+      const int m = m0 + tid;
+      if (m < p.M) p.action[m] = bidx;
+    }
+    __syncthreads();
+    if (p.probs) {
+      if (owner) {
+#pragma unroll
+        for (int j = 0; j < MBW; ++j) {
+          const int ml = (wmi * MBW + j) * 16 + r16;
+          const int m = m0 + ml;
+          float se = 0.f;
+          if (m < p.M) {
+            const float mx = s_fin[ml][0];
+#pragma unroll
+            for (int i = 0; i < NBW; ++i) {
+              const int nb = wn * NBW + i;
+              if (nb >= nbtot) continue;
+              const int n = nb * 16 + 4 * g;
+#pragma unroll
+              for (int v = 0; v < 4; ++v)
+                if (n + v < A && p.mask[(long)m * A + n + v]) se += expf(acc[i][j][v] + p.bc[n + v] - mx);
+            }
+          }
+          se += __shfl_xor(se, 16);
+          se += __shfl_xor(se, 32);
+          if (g == 0) s_best[wn][ml] = se;
+        }
+      }
+      __syncthreads();
+      if (tid < BM) {
+        float tot = 0.f;
+        for (int w = 0; w < WN; ++w) tot += s_best[w][tid];
+        s_fin[tid][1] = tot;
+      }
+      __syncthreads();
+      if (owner) {
+#pragma unroll
+        for (int j = 0; j < MBW; ++j) {
+          const int ml = (wmi * MBW + j) * 16 + r16;
+          const int m = m0 + ml;
+          if (m >= p.M) continue;
+          const float mx = s_fin[ml][0], inv = s_fin[ml][1] > 0.f ? 1.0f / s_fin[ml][1] : 0.f;
+#pragma unroll
+          for (int i = 0; i < NBW; ++i) {
+            const int nb = wn * NBW + i;
+            if (nb >= nbtot) continue;
+            const int n = nb * 16 + 4 * g;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              if (n + v < A) {
+                const bool ok = p.mask[(long)m * A + n + v] != 0;
+                p.probs[(long)m * A + n + v] = ok ? expf(acc[i][j][v] + p.bc[n + v] - mx) * inv : 0.f;
+              }
+            }
+          }
+        }
+      }
+    }
+    return;
+  }
+
+  // rollout modes: one thread per row
+  if (tid < BM) {
+    const int m = m0 + tid;
+    if (m < p.M) {
+      int ds = p.done_state[m];
+      if (p.act_prev && p.act_prev[m] >= 0) {
+        // resolve transition t-1: reward and done head on h_t
+        const float rr = s_rho[tid][0], rd = s_rho[tid][1];
+        p.rew_prev[m] = rr;
+        int d = 0;
+        if (p.use_done) {
+          const uint4 w = rng.block(0, p.step - 1u, p.traj0 + (uint32_t)m, STREAM_DONE);
+          d = sigmoidf(rd) > word_to_uniform(w.x);
+        }
+        p.done_prev[m] = (uint8_t)d;
+        if (d) ds = 1;
+      }
+      if (p.mode == 1) {
+        int a = -1;
+        if (!ds) {
+          float best = -INFINITY;
+          for (int w = 0; w < WN; ++w) {
+            const float ob = s_best[w][tid];
+            const int oi = s_idx[w][tid];
+            if (oi >= 0 && (a < 0 || ob > best || (ob == best && oi < a))) { best = ob; a = oi; }
+          }
+          if (a < 0) ds = 1;  // no valid action: the trajectory ends here
+        }
+        p.act_t[m] = a;
+        if (a < 0) {
+          p.rew_t[m] = 0.f;
+          p.done_t[m] = 1;
+        }
+      }
+      p.done_state[m] = ds;
+    }
+  }
+}
+
 // ===========================================================================
 // small element-wise kernels
 // ===========================================================================
@@ -825,39 +1116,59 @@ __global__ void __launch_bounds__(256)
 // ===========================================================================
 namespace {
 
-// fp32: 64 x 32 tiles (K slice 32); bf16: 128 x 128 tiles (K slice 64).
-template <typename DT> struct GatesCfg;
-template <> struct GatesCfg<float> {
-  static constexpr int NBW = 2, MBW = 1, WN = 2, WMv = 2, BK = 32;
+// Tile configurations by dtype and call size.  "Small" tiles serve calls
+// with up to kSmallRows rows (latency-bound: many work-groups, deep
+// prefetch, K split across waves); "Large" tiles serve the big batches
+// (MFMA-bound: more reuse per LDS byte).
+constexpr int kSmallRows = 2048;
+
+template <typename DT> struct Cfgs;
+template <> struct Cfgs<float> {
+  using GatesSmall = Gemm<float, 2, 1, 2, 2, 1, 32, 4>;  // 64 x 32
+  using GatesLarge = Gemm<float, 4, 2, 2, 2, 1, 32, 3>;  // 128 x 64
+  template <int Q> using MdnSmall = Gemm<float, Q, 1, 2, 1, 2, 32, 4>;  // 32Q x 16, K split 2
+  template <int Q> using MdnLarge = Gemm<float, Q, 2, 2, 2, 1, 32, 3>;  // 32Q x 64
+  template <int NB> using CtrlSmall = Gemm<float, NB, 1, 1, 1, 4, 64, 3>;  // 16NB x 16, K split 4
+  template <int NB> using CtrlLarge = Gemm<float, NB, 4, 4, 1, 1, 32, 3>;  // 64NB x 64
+  static constexpr int WIDE_BKC = 64;
 };
-template <> struct GatesCfg<bf16_t> {
-  static constexpr int NBW = 4, MBW = 4, WN = 2, WMv = 2, BK = 64;
+template <> struct Cfgs<bf16_t> {
+  using GatesSmall = Gemm<bf16_t, 2, 1, 2, 2, 1, 64, 4>;
+  using GatesLarge = Gemm<bf16_t, 4, 4, 2, 2, 1, 64, 2>;  // 128 x 128
+  template <int Q> using MdnSmall = Gemm<bf16_t, Q, 1, 2, 1, 2, 64, 4>;
+  template <int Q> using MdnLarge = Gemm<bf16_t, Q, 2, 2, 2, 1, 64, 2>;
+  template <int NB> using CtrlSmall = Gemm<bf16_t, NB, 1, 1, 1, 4, 128, 3>;
+  template <int NB> using CtrlLarge = Gemm<bf16_t, NB, 4, 4, 1, 1, 64, 2>;
+  static constexpr int WIDE_BKC = 128;
 };
-template <typename DT> struct MdnCfg;
-template <> struct MdnCfg<float> { static constexpr int MBW = 1, BK = 32; };
-template <> struct MdnCfg<bf16_t> { static constexpr int MBW = 2, BK = 64; };
-template <typename DT> struct CtrlCfg;
-template <> struct CtrlCfg<float> { static constexpr int BKC = 64; };
-template <> struct CtrlCfg<bf16_t> { static constexpr int BKC = 128; };
+
+template <class C>
+hipError_t launch_gates_cfg(const GatesArgs& a, hipStream_t s) {
+  const int nt = (4 * a.H + C::BN - 1) / C::BN, mt = (a.M + C::BM - 1) / C::BM;
+  KTimer kt("gates", s);
+  hipLaunchKernelGGL((k_gates<C>), dim3(grid_of(nt, mt)), dim3(C::NT), 0, s, a);
+  return hipGetLastError();
+}
 
 template <typename DT>
 hipError_t launch_gates(const GatesArgs& a, hipStream_t s) {
-  using C = GatesCfg<DT>;
-  using Tl = TileLds<DT, C::NBW, C::MBW, C::WN, C::WMv, C::BK>;
-  dim3 grid((a.M + Tl::BM - 1) / Tl::BM, (4 * a.H + Tl::BN - 1) / Tl::BN);
-  KTimer kt("gates", s);
-  hipLaunchKernelGGL((k_gates<DT, C::NBW, C::MBW, C::WN, C::WMv, C::BK>), grid, dim3(Tl::NT), 0, s, a);
+  if (a.M <= kSmallRows) return launch_gates_cfg<typename Cfgs<DT>::GatesSmall>(a, s);
+  return launch_gates_cfg<typename Cfgs<DT>::GatesLarge>(a, s);
+}
+
+template <class C>
+hipError_t launch_mdn_cfg(MdnArgs a, int ntiles, hipStream_t s) {
+  a.ntiles = ntiles;
+  const int mt = (a.M + C::BM - 1) / C::BM;
+  KTimer kt("mdn", s);
+  hipLaunchKernelGGL((k_mdn<C>), dim3(grid_of(ntiles, mt)), dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
 template <typename DT, int Q>
 hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
-  using C = MdnCfg<DT>;
-  using Tl = TileLds<DT, Q, C::MBW, 2, 2, C::BK>;
-  dim3 grid((a.M + Tl::BM - 1) / Tl::BM, ntiles);
-  KTimer kt("mdn", s);
-  hipLaunchKernelGGL((k_mdn<DT, Q, C::MBW, C::BK>), grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  if (a.M <= kSmallRows) return launch_mdn_cfg<typename Cfgs<DT>::template MdnSmall<Q>>(a, ntiles, s);
+  return launch_mdn_cfg<typename Cfgs<DT>::template MdnLarge<Q>>(a, ntiles, s);
 }
 
 template <typename DT>
@@ -873,27 +1184,43 @@ hipError_t launch_mdn(const MdnArgs& a, int Q, int ntiles, hipStream_t s) {
   }
 }
 
-template <typename DT, typename SH, int NBW, int MBW>
-hipError_t launch_ctrl_nb(const CtrlArgs& a, hipStream_t s) {
-  constexpr int BM = 16 * MBW;
-  dim3 grid((a.M + BM - 1) / BM);
+template <class C, typename SH>
+hipError_t launch_ctrl_cfg(const CtrlArgs& a, hipStream_t s) {
   KTimer kt("ctrl", s);
-  hipLaunchKernelGGL((k_ctrl<DT, SH, NBW, MBW, CtrlCfg<DT>::BKC>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_ctrl<C, SH>), dim3((a.M + C::BM - 1) / C::BM), dim3(C::NT), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename DT, typename SH, int NBW, int MBW>
+hipError_t launch_ctrl_wide(const CtrlArgs& a, hipStream_t s) {
+  constexpr int BM = 16 * MBW;
+  KTimer kt("ctrl", s);
+  hipLaunchKernelGGL((k_ctrl_wide<DT, SH, NBW, MBW, Cfgs<DT>::WIDE_BKC>), dim3((a.M + BM - 1) / BM),
+                     dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 template <typename DT, typename SH>
 hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
-  const int nb = (a.Nc / 16 + 3) / 4;  // output blocks per wave
-  if (nb <= 1) return launch_ctrl_nb<DT, SH, 1, 4>(a, s);
-  if (nb <= 2) return launch_ctrl_nb<DT, SH, 2, 4>(a, s);
-  if (nb <= 3) return launch_ctrl_nb<DT, SH, 3, 4>(a, s);
-  if (nb <= 5) return launch_ctrl_nb<DT, SH, 5, 4>(a, s);
-  if (nb <= 8) return launch_ctrl_nb<DT, SH, 8, 2>(a, s);
-  if (nb <= 12) return launch_ctrl_nb<DT, SH, 12, 2>(a, s);
-  if (nb <= 17) return launch_ctrl_nb<DT, SH, 17, 1>(a, s);
-  if (nb <= 24) return launch_ctrl_nb<DT, SH, 24, 1>(a, s);
-  if (nb <= 33) return launch_ctrl_nb<DT, SH, 33, 1>(a, s);
+  using Cf = Cfgs<DT>;
+  const int nbtot = a.Nc / 16;
+  if (a.M <= kSmallRows && nbtot <= 9) {
+    if (nbtot <= 1) return launch_ctrl_cfg<typename Cf::template CtrlSmall<1>, SH>(a, s);
+    if (nbtot <= 2) return launch_ctrl_cfg<typename Cf::template CtrlSmall<2>, SH>(a, s);
+    if (nbtot <= 3) return launch_ctrl_cfg<typename Cf::template CtrlSmall<3>, SH>(a, s);
+    if (nbtot <= 5) return launch_ctrl_cfg<typename Cf::template CtrlSmall<5>, SH>(a, s);
+    return launch_ctrl_cfg<typename Cf::template CtrlSmall<9>, SH>(a, s);
+  }
+  const int nb = (nbtot + 3) / 4;  // output blocks per wave over four waves
+  if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLarge<1>, SH>(a, s);
+  if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlLarge<2>, SH>(a, s);
+  if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlLarge<3>, SH>(a, s);
+  if (nb <= 5) return launch_ctrl_cfg<typename Cf::template CtrlLarge<5>, SH>(a, s);
+  if (nb <= 8) return launch_ctrl_wide<DT, SH, 8, 2>(a, s);
+  if (nb <= 12) return launch_ctrl_wide<DT, SH, 12, 2>(a, s);
+  if (nb <= 17) return launch_ctrl_wide<DT, SH, 17, 1>(a, s);
+  if (nb <= 24) return launch_ctrl_wide<DT, SH, 24, 1>(a, s);
+  if (nb <= 33) return launch_ctrl_wide<DT, SH, 33, 1>(a, s);
   return hipErrorInvalidValue;
 }
 
