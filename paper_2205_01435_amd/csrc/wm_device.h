@@ -119,6 +119,41 @@ template <> struct Mfma<bf16_t> {
   }
 };
 
+// ---------------------------------------------------------------------------
+// Buffer (range-checked) loads: a 16-byte load at a byte offset at or beyond
+// the resource's size returns zeros without touching memory, which replaces
+// per-load bounds branches and 64-bit address arithmetic.  Offsets are 32-bit
+// (resources are at most 2^31 bytes); kOffNone addresses nothing.
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOffNone = 0x80000000u;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ uint4 operator|(uint4 a, uint4 b) {
+  return make_uint4(a.x | b.x, a.y | b.y, a.z | b.z, a.w | b.w);
+}
+
+// 16 bytes of DT activations from a source of element type S at byte offset
+// `off` (fp32 sources are converted to DT: two 16-byte loads when DT is bf16).
+template <typename DT, typename S>
+__device__ __forceinline__ uint4 bload_x16(rsrc_t r, uint32_t off) {
+  if constexpr (sizeof(S) == sizeof(DT)) {
+    return bload16(r, off);
+  } else {
+    const uint4 a = bload16(r, off);
+    const uint4 b = bload16(r, off == kOffNone ? kOffNone : off + 16u);
+    return pack8_bf16(make_float4(__uint_as_float(a.x), __uint_as_float(a.y), __uint_as_float(a.z),
+                                  __uint_as_float(a.w)),
+                      make_float4(__uint_as_float(b.x), __uint_as_float(b.y), __uint_as_float(b.z),
+                                  __uint_as_float(b.w)));
+  }
+}
+
 // 16 bytes of activations (row m, columns k .. k+VEC-1) converted to DT.
 // Columns [0, Kz) come from the float32 source xz, [Kz, Kz+Kh) from xh (SH
 // elements); anything else, and rows m >= M, read as zero.  Kz and Kh are

@@ -22,6 +22,21 @@
 
 namespace wm {
 
+#ifdef WM_PHASE_TIMING
+// Debug builds only: per-wave wall-clock stamps of kernel phases.
+__device__ unsigned long long wm_phase_t[1 << 20];
+#define WM_STAMP(slot)                                                                    \
+  do {                                                                                    \
+    if ((threadIdx.x & 63) == 0)                                                          \
+      wm_phase_t[((blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 8 + (slot)) &   \
+                 ((1 << 20) - 1)] = wall_clock64();                                       \
+  } while (0)
+#else
+#define WM_STAMP(slot) \
+  do {                 \
+  } while (0)
+#endif
+
 static constexpr float kHalfLn2Pi = 0.91893853320467274178f;
 
 // ===========================================================================
@@ -316,6 +331,65 @@ struct GatesArgs {
   int nll_mode;
 };
 
+// LSTM cell and state commit of hidden unit u of row m.  gates_pre loads
+// everything that does not depend on the GEMM (action, bias plus gathered
+// one-hot column, cell state), so that callers can issue it early;
+// gates_fin adds the GEMM part (W [z | h]) of the four gate pre-activations
+// i, f, g, o and commits.  A frozen rollout row copies its state.
+struct GatePre {
+  long e;        // element index m * H + u
+  bool live;
+  float4 add;    // bias + one-hot column, per gate
+  float c;       // cell state c_t
+};
+
+template <typename DT>
+__device__ __forceinline__ GatePre gates_pre(const GatesArgs& p, int m, int u) {
+  GatePre q;
+  const int H = p.H;
+  const int a = p.act[m];
+  q.live = p.nll_mode || a >= 0;
+  q.e = (long)m * H + u;
+  q.add = *reinterpret_cast<const float4*>(p.bg + 4 * u);
+  if (a >= 0 && a < p.A) {
+    const DT* WaT = reinterpret_cast<const DT*>(p.WaT);
+    const long o = (long)a * 4 * H + 4 * u;
+    q.add.x += DType<DT>::load(WaT, o);
+    q.add.y += DType<DT>::load(WaT, o + 1);
+    q.add.z += DType<DT>::load(WaT, o + 2);
+    q.add.w += DType<DT>::load(WaT, o + 3);
+  }
+  q.c = p.c[q.e];
+  return q;
+}
+
+template <typename DT>
+__device__ __forceinline__ void gates_fin(const GatesArgs& p, const GatePre& q, float pi, float pf,
+                                          float pg, float po) {
+  DT* h_out = reinterpret_cast<DT*>(p.h_out);
+  float hv, cv;
+  if (!q.live) {
+    hv = DType<DT>::load(reinterpret_cast<const DT*>(p.h_in), q.e);
+    cv = q.c;
+    DType<DT>::store(h_out, q.e, hv);
+  } else {
+    cv = sigmoidf(pf + q.add.y) * q.c + sigmoidf(pi + q.add.x) * tanhf(pg + q.add.z);
+    hv = DType<DT>::round(sigmoidf(po + q.add.w) * tanhf(cv));
+    p.c[q.e] = cv;
+    DType<DT>::store(h_out, q.e, hv);
+  }
+  if (p.h_trace) {
+    p.h_trace[q.e] = hv;
+    p.c_trace[q.e] = cv;
+  }
+}
+
+template <typename DT>
+__device__ __forceinline__ void gates_commit(const GatesArgs& p, int m, int u, float pi, float pf,
+                                             float pg, float po) {
+  gates_fin<DT>(p, gates_pre<DT>(p, m, u), pi, pf, pg, po);
+}
+
 template <class C>
 __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
   using DT = typename C::DT;
@@ -333,49 +407,14 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
 
   const int lane = threadIdx.x & 63;
   const int wn = C::wn(), wmi = C::wm();
-  const int H = p.H;
-  DT* h_out = reinterpret_cast<DT*>(p.h_out);
-  const DT* WaT = reinterpret_cast<const DT*>(p.WaT);
 #pragma unroll
   for (int j = 0; j < MBW; ++j) {
     const int m = m0 + (wmi * MBW + j) * 16 + (lane & 15);
     if (m >= p.M) continue;
-    const int a = p.act[m];
-    const bool live = p.nll_mode || a >= 0;
-    const bool gather = a >= 0 && a < p.A;
 #pragma unroll
     for (int i = 0; i < NBW; ++i) {
       const int u = (n0 + (wn * NBW + i) * 16) / 4 + (lane >> 4);
-      if (u >= H) continue;
-      const long e = (long)m * H + u;
-      float hv, cv;
-      if (!live) {
-        hv = DType<DT>::load(h_in, e);
-        cv = p.c[e];
-        DType<DT>::store(h_out, e, hv);
-      } else {
-        const float4 bias = *reinterpret_cast<const float4*>(p.bg + 4 * u);
-        float wa0 = 0.f, wa1 = 0.f, wa2 = 0.f, wa3 = 0.f;
-        if (gather) {
-          const long o = (long)a * 4 * H + 4 * u;
-          wa0 = DType<DT>::load(WaT, o);
-          wa1 = DType<DT>::load(WaT, o + 1);
-          wa2 = DType<DT>::load(WaT, o + 2);
-          wa3 = DType<DT>::load(WaT, o + 3);
-        }
-        const float gi = acc[i][j][0] + bias.x + wa0;
-        const float gf = acc[i][j][1] + bias.y + wa1;
-        const float gg = acc[i][j][2] + bias.z + wa2;
-        const float go = acc[i][j][3] + bias.w + wa3;
-        cv = sigmoidf(gf) * p.c[e] + sigmoidf(gi) * tanhf(gg);
-        hv = DType<DT>::round(sigmoidf(go) * tanhf(cv));
-        p.c[e] = cv;
-        DType<DT>::store(h_out, e, hv);
-      }
-      if (p.h_trace) {
-        p.h_trace[e] = hv;
-        p.c_trace[e] = cv;
-      }
+      if (u < p.H) gates_commit<DT>(p, m, u, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
   }
 }
@@ -407,6 +446,110 @@ struct MdnArgs {
   int ntiles;          // weight-row tiles in the grid
   int nll_mode;
 };
+
+// z_{t+1,j} of row m: Gumbel-max component pick on pi-logit / tau (stream 1,
+// uniform j*K + k), then mu + exp(log sigma) * eps with eps from Box-Muller on
+// the stream-2 pair (2p, 2p+1) that contains j.  mdn_noise draws the random
+// part (independent of the GEMM, so callers can issue it early); mdn_pick
+// finishes from the dim's features f = 0 .. 4Q-1 (pi-logits, means, log
+// sigmas, padding), biased.
+struct MdnNoise {
+  float g[8];  // Gumbel noise of components 0 .. K-1 (K <= 8)
+  float eps;   // standard normal of dim j
+};
+
+__device__ __forceinline__ MdnNoise mdn_noise(const MdnArgs& p, const Rng& rng, int m, int j) {
+  MdnNoise n;
+  const int K = p.K;
+  const uint32_t traj = p.traj0 + (uint32_t)m;
+  uint32_t cur = 0xffffffffu;
+  uint4 w = make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    n.g[k] = 0.f;
+    if (k < K) {
+      const uint32_t idx = (uint32_t)j * K + k;
+      if ((idx >> 2) != cur) {
+        cur = idx >> 2;
+        w = rng.block(cur, p.step, traj, STREAM_COMPONENT);
+      }
+      n.g[k] = gumbel(word_to_uniform(word_of(w, idx & 3)));
+    }
+  }
+  const uint4 wg = rng.block((uint32_t)j >> 2, p.step, traj, STREAM_GAUSS);
+  const float u1 = word_to_uniform(word_of(wg, j & 2));
+  const float u2 = word_to_uniform(word_of(wg, (j & 2) + 1));
+  const float r = sqrtf(-2.0f * logf(u1));
+  float sn, cs;
+  sincospif(2.0f * u2, &sn, &cs);
+  n.eps = (j & 1) ? r * sn : r * cs;
+  return n;
+}
+
+template <int Q>
+__device__ __forceinline__ float mdn_pick(const MdnArgs& p, const MdnNoise& n,
+                                          const float (&feat)[4 * Q]) {
+  const int K = p.K;
+  float best = -INFINITY;
+  int kbest = 0;
+#pragma unroll
+  for (int f = 0; f < 4 * Q && f < 8; ++f) {
+    if (f < K) {
+      const float sc = feat[f] / p.tau + n.g[f];
+      if (sc > best) { best = sc; kbest = f; }
+    }
+  }
+  float mu = 0.f, ls = 0.f;
+#pragma unroll
+  for (int f = 0; f < 4 * Q; ++f) {
+    if (f == K + kbest) mu = feat[f];
+    if (f == 2 * K + kbest) ls = feat[f];
+  }
+  return mu + expf(ls) * n.eps;
+}
+
+template <int Q>
+__device__ __forceinline__ float mdn_draw(const MdnArgs& p, const Rng& rng, int m, int j,
+                                          const float (&feat)[4 * Q]) {
+  return mdn_pick<Q>(p, mdn_noise(p, rng, m, j), feat);
+}
+
+// log sum_k pi_k N(x; mu_k, sigma_k) of one latent dim (pi at tau = 1).
+template <int Q>
+__device__ __forceinline__ float mdn_loglik(const MdnArgs& p, float x, const float (&feat)[4 * Q]) {
+  const int K = p.K;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int f = 0; f < 4 * Q; ++f)
+    if (f < K) mx = fmaxf(mx, feat[f]);
+  float se = 0.f;
+#pragma unroll
+  for (int f = 0; f < 4 * Q; ++f)
+    if (f < K) se += expf(feat[f] - mx);
+  const float lse_pi = mx + logf(se);
+  float terms[4 * Q];
+  float tmax = -INFINITY;
+#pragma unroll
+  for (int f = 0; f < 4 * Q; ++f) {
+    terms[f] = -INFINITY;
+    if (f < K) {
+      float mu = 0.f, ls = 0.f;
+#pragma unroll
+      for (int f2 = 0; f2 < 4 * Q; ++f2) {
+        if (f2 == K + f) mu = feat[f2];
+        if (f2 == 2 * K + f) ls = feat[f2];
+      }
+      const float d = (x - mu) * expf(-ls);
+      terms[f] = (feat[f] - lse_pi) - 0.5f * d * d - ls - kHalfLn2Pi;
+      tmax = fmaxf(tmax, terms[f]);
+    }
+  }
+  float st = 0.f;
+#pragma unroll
+  for (int f = 0; f < 4 * Q; ++f)
+    if (f < K) st += expf(terms[f] - tmax);
+  return tmax + logf(st);
+}
 
 template <class C>
 __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
@@ -472,39 +615,7 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
       for (int q = 0; q < Q; ++q)
 #pragma unroll
         for (int v = 0; v < 4; ++v) feat[4 * q + v] = acc[q][jj][v] + bias[4 * q + v];
-      const uint32_t traj = p.traj0 + (uint32_t)m;
-      // Gumbel-max over k of logit/tau + G (stream 1, uniform j*K + k)
-      float best = -INFINITY;
-      int kbest = 0;
-      uint32_t cur = 0xffffffffu;
-      uint4 w = make_uint4(0, 0, 0, 0);
-#pragma unroll
-      for (int f = 0; f < 4 * Q; ++f) {
-        if (f < K) {
-          const uint32_t idx = (uint32_t)j * K + f;
-          if ((idx >> 2) != cur) {
-            cur = idx >> 2;
-            w = rng.block(cur, p.step, traj, STREAM_COMPONENT);
-          }
-          const float s = feat[f] / p.tau + gumbel(word_to_uniform(word_of(w, idx & 3)));
-          if (s > best) { best = s; kbest = f; }
-        }
-      }
-      float mu = 0.f, ls = 0.f;
-#pragma unroll
-      for (int f = 0; f < 4 * Q; ++f) {
-        if (f == K + kbest) mu = feat[f];
-        if (f == 2 * K + kbest) ls = feat[f];
-      }
-      // Box-Muller on the pair (2p, 2p+1) of stream 2 that contains j
-      const uint4 wg = rng.block((uint32_t)j >> 2, p.step, traj, STREAM_GAUSS);
-      const float u1 = word_to_uniform(word_of(wg, j & 2));
-      const float u2 = word_to_uniform(word_of(wg, (j & 2) + 1));
-      const float r = sqrtf(-2.0f * logf(u1));
-      float sn, cs;
-      sincospif(2.0f * u2, &sn, &cs);
-      const float eps = (j & 1) ? r * sn : r * cs;
-      p.z_next[e] = mu + expf(ls) * eps;
+      p.z_next[e] = mdn_draw<Q>(p, rng, m, j, feat);
     }
   } else {
 #pragma unroll
@@ -517,38 +628,7 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
         for (int q = 0; q < Q; ++q)
 #pragma unroll
           for (int v = 0; v < 4; ++v) feat[4 * q + v] = acc[q][jj][v] + bias[4 * q + v];
-        const float x = p.z_tgt[(long)m * Z + j];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int f = 0; f < 4 * Q; ++f)
-          if (f < K) mx = fmaxf(mx, feat[f]);
-        float se = 0.f;
-#pragma unroll
-        for (int f = 0; f < 4 * Q; ++f)
-          if (f < K) se += expf(feat[f] - mx);
-        const float lse_pi = mx + logf(se);
-        float terms[4 * Q];
-        float tmax = -INFINITY;
-#pragma unroll
-        for (int f = 0; f < 4 * Q; ++f) {
-          terms[f] = -INFINITY;
-          if (f < K) {
-            float mu = 0.f, ls = 0.f;
-#pragma unroll
-            for (int f2 = 0; f2 < 4 * Q; ++f2) {
-              if (f2 == K + f) mu = feat[f2];
-              if (f2 == 2 * K + f) ls = feat[f2];
-            }
-            const float d = (x - mu) * expf(-ls);
-            terms[f] = (feat[f] - lse_pi) - 0.5f * d * d - ls - kHalfLn2Pi;
-            tmax = fmaxf(tmax, terms[f]);
-          }
-        }
-        float st = 0.f;
-#pragma unroll
-        for (int f = 0; f < 4 * Q; ++f)
-          if (f < K) st += expf(terms[f] - tmax);
-        ll = tmax + logf(st);
+        ll = mdn_loglik<Q>(p, p.z_tgt[(long)m * Z + j], feat);
       }
       // sum over the four dims of the group (lane groups), then the two waves
       ll += __shfl_xor(ll, 16);
@@ -594,6 +674,37 @@ struct CtrlArgs {
   int32_t* done_state;
   int use_done;
 };
+
+// Rollout bookkeeping of row m at step t (modes 1 and 2 of the controller
+// kernels).  First the previous transition t-1 is resolved if the row was
+// live then: its reward is the reward head on h_t and it is done when
+// sigmoid(done head) exceeds the stream-3 uniform of step t-1.  Then (mode 1)
+// the row takes action `a` (the masked Gumbel-max, -1 if no action is valid)
+// or, if done, the frozen outputs; a row without a valid action ends here.
+__device__ __forceinline__ void ctrl_row_commit(const CtrlArgs& p, const Rng& rng, int m, int a,
+                                                float rr, float rd) {
+  int ds = p.done_state[m];
+  if (p.act_prev && p.act_prev[m] >= 0) {
+    p.rew_prev[m] = rr;
+    int d = 0;
+    if (p.use_done) {
+      const uint4 w = rng.block(0, p.step - 1u, p.traj0 + (uint32_t)m, STREAM_DONE);
+      d = sigmoidf(rd) > word_to_uniform(w.x);
+    }
+    p.done_prev[m] = (uint8_t)d;
+    if (d) ds = 1;
+  }
+  if (p.mode == 1) {
+    if (ds) a = -1;
+    else if (a < 0) ds = 1;
+    p.act_t[m] = a;
+    if (a < 0) {
+      p.rew_t[m] = 0.f;
+      p.done_t[m] = 1;
+    }
+  }
+  p.done_state[m] = ds;
+}
 
 template <typename DT, typename SH, int NBW, int MBW, int BKC>
 __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
@@ -771,37 +882,14 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
   if (tid < BM) {
     const int m = m0 + tid;
     if (m < p.M) {
-      int ds = p.done_state[m];
-      if (p.act_prev && p.act_prev[m] >= 0) {
-        // resolve transition t-1: reward and done head on h_t
-        const float rr = s_rho[tid][0], rd = s_rho[tid][1];
-        p.rew_prev[m] = rr;
-        int d = 0;
-        if (p.use_done) {
-          const uint4 w = rng.block(0, p.step - 1u, p.traj0 + (uint32_t)m, STREAM_DONE);
-          d = sigmoidf(rd) > word_to_uniform(w.x);
-        }
-        p.done_prev[m] = (uint8_t)d;
-        if (d) ds = 1;
+      float best = -INFINITY;
+      int a = -1;
+      for (int w = 0; w < 4; ++w) {
+        const float ob = s_best[w][tid];
+        const int oi = s_idx[w][tid];
+        if (oi >= 0 && (a < 0 || ob > best || (ob == best && oi < a))) { best = ob; a = oi; }
       }
-      if (p.mode == 1) {
-        int a = -1;
-        if (!ds) {
-          float best = -INFINITY;
-          for (int w = 0; w < 4; ++w) {
-            const float ob = s_best[w][tid];
-            const int oi = s_idx[w][tid];
-            if (oi >= 0 && (a < 0 || ob > best || (ob == best && oi < a))) { best = ob; a = oi; }
-          }
-          if (a < 0) ds = 1;  // no valid action: the trajectory ends here
-        }
-        p.act_t[m] = a;
-        if (a < 0) {
-          p.rew_t[m] = 0.f;
-          p.done_t[m] = 1;
-        }
-      }
-      p.done_state[m] = ds;
+      ctrl_row_commit(p, rng, m, a, s_rho[tid][0], s_rho[tid][1]);
     }
   }
 }
@@ -964,39 +1052,285 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
   if (tid < BM) {
     const int m = m0 + tid;
     if (m < p.M) {
-      int ds = p.done_state[m];
-      if (p.act_prev && p.act_prev[m] >= 0) {
-        // resolve transition t-1: reward and done head on h_t
-        const float rr = s_rho[tid][0], rd = s_rho[tid][1];
-        p.rew_prev[m] = rr;
-        int d = 0;
-        if (p.use_done) {
-          const uint4 w = rng.block(0, p.step - 1u, p.traj0 + (uint32_t)m, STREAM_DONE);
-          d = sigmoidf(rd) > word_to_uniform(w.x);
-        }
-        p.done_prev[m] = (uint8_t)d;
-        if (d) ds = 1;
+      float best = -INFINITY;
+      int a = -1;
+      for (int w = 0; w < WN; ++w) {
+        const float ob = s_best[w][tid];
+        const int oi = s_idx[w][tid];
+        if (oi >= 0 && (a < 0 || ob > best || (ob == best && oi < a))) { best = ob; a = oi; }
       }
-      if (p.mode == 1) {
-        int a = -1;
-        if (!ds) {
-          float best = -INFINITY;
-          for (int w = 0; w < WN; ++w) {
-            const float ob = s_best[w][tid];
-            const int oi = s_idx[w][tid];
-            if (oi >= 0 && (a < 0 || ob > best || (ob == best && oi < a))) { best = ob; a = oi; }
-          }
-          if (a < 0) ds = 1;  // no valid action: the trajectory ends here
-        }
-        p.act_t[m] = a;
-        if (a < 0) {
-          p.rew_t[m] = 0.f;
-          p.done_t[m] = 1;
-        }
-      }
-      p.done_state[m] = ds;
+      ctrl_row_commit(p, rng, m, a, s_rho[tid][0], s_rho[tid][1]);
     }
   }
+}
+
+// ===========================================================================
+// Register-direct split-K GEMM for calls with few rows.  Every wave takes a
+// contiguous run of at most SMAX MFMA K slices and loads all of its operand
+// fragments for the whole tile straight from global memory into registers in
+// one round trip (no LDS staging, no barrier inside the K loop), then runs
+// its MFMAs.  The per-wave partial tiles meet in LDS and are summed in a
+// fixed wave order, so results are deterministic; the sum lands in
+// E[m][n] (tile rows m, features n, fp32) for an epilogue with any thread
+// mapping.  The block has nwaves = blockDim.x / 64 waves, chosen by the host
+// so that ceil(K slices / nwaves) <= SMAX.
+// ===========================================================================
+template <typename DT_, int NBW_, int MBW_, int SMAX_, int MAXT_>
+struct GemmRD {
+  using DT = DT_;
+  static constexpr int NBW = NBW_, MBW = MBW_, SMAX = SMAX_;
+  static constexpr int MAXT = MAXT_;  // largest block the kernels are compiled for
+  static constexpr int KSLICE = Mfma<DT>::KSLICE, VEC = DType<DT>::VEC;
+  static constexpr int BN = 16 * NBW, BM = 16 * MBW;
+  static constexpr int TILE = BN * BM;  // floats per partial tile
+  static constexpr int ELD = BN + 4;    // row stride of E (floats)
+
+  static size_t lds_bytes(int nwaves) {
+    return (size_t)nwaves * TILE * 4 + (size_t)BM * ELD * 4;
+  }
+  __device__ static float* E(float* lds) { return lds + (blockDim.x >> 6) * TILE; }
+
+  template <typename SH>
+  __device__ __forceinline__ static void run(float* lds, const DT* __restrict__ W, long ldw, int n0,
+                                             int Nrows, int Kpad, const float* __restrict__ xz,
+                                             long ldz, int Kz, const SH* __restrict__ xh, long ldxh,
+                                             int Kh, int m0, int M) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int nsl = (Kpad + KSLICE - 1) / KSLICE;
+    const int per = (nsl + nw - 1) / nw;
+    WM_STAMP(1);
+    const int s0 = wave * per;
+    const int Kx = Kz + Kh;
+    // resources over the tile's valid rows: rows past them read as zero
+    const int nval = max(0, min(BN, Nrows - n0)), mval = max(0, min(BM, M - m0));
+    const rsrc_t rw = make_rsrc(W + (long)n0 * ldw, (uint32_t)(nval * ldw * (long)sizeof(DT)));
+    const rsrc_t rz = make_rsrc(xz ? xz + (long)m0 * ldz : xz, xz ? (uint32_t)(mval * ldz * 4L) : 0u);
+    const rsrc_t rh = make_rsrc(xh + (long)m0 * ldxh, (uint32_t)(mval * ldxh * (long)sizeof(SH)));
+    uint32_t wo[NBW], zo[MBW], ho[MBW];
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) wo[i] = (uint32_t)((i * 16 + r16) * ldw * sizeof(DT));
+#pragma unroll
+    for (int j = 0; j < MBW; ++j) {
+      zo[j] = (uint32_t)((j * 16 + r16) * ldz * 4);
+      ho[j] = (uint32_t)((j * 16 + r16) * ldxh * sizeof(SH));
+    }
+    uint4 wf[NBW][SMAX], xf[MBW][SMAX];
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s) {
+      const int sl = s0 + s;
+      const int kb = sl * KSLICE;             // first column of the slice (uniform)
+      const int kl = kb + g * VEC;            // first column of this lane's vector
+      if (s < per && sl < nsl) {
+#pragma unroll
+        for (int i = 0; i < NBW; ++i) wf[i][s] = bload16(rw, wo[i] + (uint32_t)(kl * sizeof(DT)));
+        if (kb + KSLICE <= Kz) {              // slice inside the z columns
+#pragma unroll
+          for (int j = 0; j < MBW; ++j) xf[j][s] = bload_x16<DT, float>(rz, zo[j] + (uint32_t)(kl * 4));
+        } else if (kb >= Kz && kb + KSLICE <= Kx) {  // inside the h columns
+#pragma unroll
+          for (int j = 0; j < MBW; ++j)
+            xf[j][s] = bload_x16<DT, SH>(rh, ho[j] + (uint32_t)((kl - Kz) * sizeof(SH)));
+        } else {                              // straddles a boundary: per-lane source
+          const bool inz = kl < Kz, inh = kl >= Kz && kl < Kx;
+#pragma unroll
+          for (int j = 0; j < MBW; ++j)
+            xf[j][s] = bload_x16<DT, float>(rz, inz ? zo[j] + (uint32_t)(kl * 4) : kOffNone) |
+                       bload_x16<DT, SH>(rh, inh ? ho[j] + (uint32_t)((kl - Kz) * sizeof(SH)) : kOffNone);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NBW; ++i) wf[i][s] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < MBW; ++j) xf[j][s] = make_uint4(0, 0, 0, 0);
+      }
+    }
+    f32x4 acc[NBW][MBW];
+#pragma unroll
+    for (int i = 0; i < NBW; ++i)
+#pragma unroll
+      for (int j = 0; j < MBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    WM_STAMP(2);
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s) {
+      if (s < per && s0 + s < nsl) {
+#pragma unroll
+        for (int i = 0; i < NBW; ++i)
+#pragma unroll
+          for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], wf[i][s], xf[j][s]);
+      }
+    }
+    WM_STAMP(3);
+    float* P = lds + wave * TILE;
+#pragma unroll
+    for (int i = 0; i < NBW; ++i)
+#pragma unroll
+      for (int j = 0; j < MBW; ++j)
+        *reinterpret_cast<f32x4*>(P + ((i * MBW + j) * 64 + lane) * 4) = acc[i][j];
+    __syncthreads();
+    WM_STAMP(4);
+    float* Et = E(lds);
+    for (int e = threadIdx.x; e < TILE; e += blockDim.x) {
+      float sum = 0.f;
+      for (int w = 0; w < nw; ++w) sum += lds[w * TILE + e];
+      const int v = e & 3, l = (e >> 2) & 63, ij = e >> 8;
+      const int j = ij % MBW, i = ij / MBW;
+      Et[(j * 16 + (l & 15)) * ELD + i * 16 + 4 * (l >> 4) + v] = sum;
+    }
+    __syncthreads();
+    WM_STAMP(5);
+  }
+};
+
+// Gates on the register-direct core: tiles of 8 hidden units (32 gate rows)
+// x 32 rows.  Each of the first 256 threads owns one (unit, row) of the
+// epilogue and loads its inputs before the GEMM.
+template <class R>
+__global__ void __launch_bounds__(R::MAXT) k_gates_rd(const GatesArgs p) {
+  using DT = typename R::DT;
+  extern __shared__ __attribute__((aligned(16))) float lds_dyn[];
+  int nt, mt;
+  if (!tile_of((4 * p.H + R::BN - 1) / R::BN, (p.M + R::BM - 1) / R::BM, nt, mt)) return;
+  const int n0 = nt * R::BN, m0 = mt * R::BM;
+  constexpr int UPT = R::BN / 4;  // hidden units per tile
+  static_assert(UPT * R::BM <= 256, "one epilogue element per thread of the first four waves");
+  const int t = threadIdx.x;
+  const int ul = t % UPT, ml = t / UPT;
+  const int m = m0 + ml, u = n0 / 4 + ul;
+  const bool mine = t < UPT * R::BM && m < p.M && u < p.H;
+  WM_STAMP(0);
+  GatePre pre{};
+  if (mine) pre = gates_pre<DT>(p, m, u);
+  R::template run<DT>(lds_dyn, reinterpret_cast<const DT*>(p.Wg), p.ldk, n0, 4 * p.H, (int)p.ldk,
+                      p.xz, p.ldz, p.Z, reinterpret_cast<const DT*>(p.h_in), p.H, p.H, m0, p.M);
+  if (mine) {
+    const float4 g4 = *reinterpret_cast<const float4*>(R::E(lds_dyn) + ml * R::ELD + 4 * ul);
+    gates_fin<DT>(p, pre, g4.x, g4.y, g4.z, g4.w);
+  }
+  WM_STAMP(6);
+}
+
+// Rollout mixture head on the register-direct core: one group of four
+// latent dims (16Q feature rows) x 32 rows per tile.  Each of the first 128
+// threads owns one (dim, row) and draws its noise before the GEMM.
+template <class R>
+__global__ void __launch_bounds__(R::MAXT) k_mdn_rd(const MdnArgs p) {
+  using DT = typename R::DT;
+  constexpr int Q = R::NBW;
+  extern __shared__ __attribute__((aligned(16))) float lds_dyn[];
+  int J, mt;
+  if (!tile_of(p.ntiles, (p.M + R::BM - 1) / R::BM, J, mt)) return;
+  const int n0 = J * R::BN, m0 = mt * R::BM;
+  const int t = threadIdx.x;
+  const int d = t & 3, ml = t >> 2;
+  const int m = m0 + ml, j = 4 * J + d;
+  const bool mine = t < 4 * R::BM && m < p.M && j < p.Z;
+  const Rng rng{p.k0, p.k1};
+  bool live = false;
+  float zprev = 0.f;
+  MdnNoise noise{};
+  if (mine) {
+    live = p.act[m] >= 0;
+    if (live) noise = mdn_noise(p, rng, m, j);
+    else zprev = p.z_prev[(long)m * p.Z + j];
+  }
+  R::template run<DT>(lds_dyn, reinterpret_cast<const DT*>(p.Wm), p.ldh, n0, p.Nm, (int)p.ldh,
+                      nullptr, 0, 0, reinterpret_cast<const DT*>(p.h), p.H, p.H, m0, p.M);
+  if (!mine) return;
+  const long e = (long)m * p.Z + j;
+  if (!live) {
+    p.z_next[e] = zprev;
+    return;
+  }
+  const float* E = R::E(lds_dyn);
+  float feat[4 * Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int r = 16 * q + 4 * d + v;
+      feat[4 * q + v] = E[ml * R::ELD + r] + p.bm[n0 + r];
+    }
+  p.z_next[e] = mdn_pick<Q>(p, noise, feat);
+}
+
+// Controller on the register-direct core: all Nc outputs x 16 rows.  Each row
+// is handled by 16 lanes of one wave (four waves, four rows per wave), each
+// lane taking the action blocks sub + 16 h, h < 4 (four actions and one
+// Philox block each); their Gumbel noise and mask bits are drawn before the
+// GEMM.  Requires A <= 256.
+template <class R, typename SH>
+__global__ void __launch_bounds__(R::MAXT) k_ctrl_rd(const CtrlArgs p) {
+  using DT = typename R::DT;
+  extern __shared__ __attribute__((aligned(16))) float lds_dyn[];
+  const int m0 = blockIdx.x * R::BM;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int ml = 4 * wave + (lane >> 4), sub = lane & 15;
+  const int m = m0 + ml;
+  const bool row_ok = wave < 4 && m < p.M;
+  const int A = p.A;
+  const Rng rng{p.k0, p.k1};
+  float gn[16];
+  unsigned valid = 0;
+  if (row_ok && p.mode != 2) {
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const int b = sub + 16 * h;
+      if (4 * b < A) {
+        const uint4 w = rng.block((uint32_t)b, p.step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int a = 4 * b + v;
+          gn[4 * h + v] = gumbel(word_to_uniform(word_of(w, v)));
+          if (a < A && p.mask[(long)m * A + a]) valid |= 1u << (4 * h + v);
+        }
+      }
+    }
+  }
+  R::template run<SH>(lds_dyn, reinterpret_cast<const DT*>(p.Wc), p.ldk, 0, p.Nc, (int)p.ldk, p.z,
+                      p.ldz, p.Z, reinterpret_cast<const SH*>(p.h), p.H, p.H, m0, p.M);
+  if (wave >= 4) return;  // rows live in the first four waves; no barrier below
+  const float* lg = R::E(lds_dyn) + ml * R::ELD;
+  float best = -INFINITY, mx = -INFINITY;
+  int bidx = -1;
+#pragma unroll
+  for (int h = 0; h < 4; ++h)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      if (valid & (1u << (4 * h + v))) {
+        const int a = 4 * (sub + 16 * h) + v;
+        const float l = lg[a] + p.bc[a];
+        mx = fmaxf(mx, l);
+        const float sc = l + gn[4 * h + v];
+        if (sc > best) { best = sc; bidx = a; }
+      }
+    }
+  // reduce over the 16 lanes of the row, lowest index on ties
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) {
+    const float ob = __shfl_xor(best, off);
+    const int oi = __shfl_xor(bidx, off);
+    const float om = __shfl_xor(mx, off);
+    if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
+    mx = fmaxf(mx, om);
+  }
+  if (p.mode == 0) {
+    if (row_ok && sub == 0) p.action[m] = bidx;
+    if (p.probs) {
+      float se = 0.f;
+      if (row_ok)
+        for (int a = sub; a < A; a += 16)
+          if (p.mask[(long)m * A + a]) se += expf(lg[a] + p.bc[a] - mx);
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) se += __shfl_xor(se, off);
+      const float inv = se > 0.f ? 1.0f / se : 0.f;
+      if (row_ok)
+        for (int a = sub; a < A; a += 16)
+          p.probs[(long)m * A + a] = p.mask[(long)m * A + a] ? expf(lg[a] + p.bc[a] - mx) * inv : 0.f;
+    }
+    return;
+  }
+  if (row_ok && sub == 0) ctrl_row_commit(p, rng, m, bidx, lg[A] + p.bc[A], lg[A + 1] + p.bc[A + 1]);
 }
 
 // ===========================================================================
@@ -1150,8 +1484,38 @@ hipError_t launch_gates_cfg(const GatesArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Register-direct kernels serve calls with at most kRdRows rows when the K
+// slices fit SMAX per wave on the compiled block size.
+constexpr int kRdRows = 1024;
+constexpr size_t kRdLdsMax = 64 * 1024;
+
+inline int rd_waves(int Kpad, int kslice, int smax, int min_waves) {
+  const int nsl = (Kpad + kslice - 1) / kslice;
+  int nw = (nsl + smax - 1) / smax;
+  return nw < min_waves ? min_waves : nw;
+}
+
+// Dynamic LDS above the default needs the kernel attribute raised once.
+template <typename F>
+hipError_t allow_lds(F* kernel, size_t bytes) {
+  if (bytes <= 64 * 1024) return hipSuccess;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
 template <typename DT>
 hipError_t launch_gates(const GatesArgs& a, hipStream_t s) {
+  using R = GemmRD<DT, 2, 2, 8, 512>;
+  const int nw = rd_waves((int)a.ldk, R::KSLICE, R::SMAX, 4);
+  const size_t lds = R::lds_bytes(nw);
+  if (a.M <= kRdRows && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
+    hipError_t e = allow_lds(k_gates_rd<R>, lds);
+    if (e != hipSuccess) return e;
+    const int nt = (4 * a.H + R::BN - 1) / R::BN, mt = (a.M + R::BM - 1) / R::BM;
+    KTimer kt("gates", s);
+    hipLaunchKernelGGL((k_gates_rd<R>), dim3(grid_of(nt, mt)), dim3(64 * nw), lds, s, a);
+    return hipGetLastError();
+  }
   if (a.M <= kSmallRows) return launch_gates_cfg<typename Cfgs<DT>::GatesSmall>(a, s);
   return launch_gates_cfg<typename Cfgs<DT>::GatesLarge>(a, s);
 }
@@ -1167,6 +1531,21 @@ hipError_t launch_mdn_cfg(MdnArgs a, int ntiles, hipStream_t s) {
 
 template <typename DT, int Q>
 hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
+  if (!a.nll_mode) {
+    using R = GemmRD<DT, Q, 2, (Q <= 4 ? 8 : 4), 512>;
+    const int nw = rd_waves((int)a.ldh, R::KSLICE, R::SMAX, 4);
+    const size_t lds = R::lds_bytes(nw);
+    if (a.M <= kRdRows && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
+      hipError_t e = allow_lds(k_mdn_rd<R>, lds);
+      if (e != hipSuccess) return e;
+      MdnArgs b = a;
+      b.ntiles = a.Z / 4;  // one dim group per tile
+      const int mt = (a.M + R::BM - 1) / R::BM;
+      KTimer kt("mdn", s);
+      hipLaunchKernelGGL((k_mdn_rd<R>), dim3(grid_of(b.ntiles, mt)), dim3(64 * nw), lds, s, b);
+      return hipGetLastError();
+    }
+  }
   if (a.M <= kSmallRows) return launch_mdn_cfg<typename Cfgs<DT>::template MdnSmall<Q>>(a, ntiles, s);
   return launch_mdn_cfg<typename Cfgs<DT>::template MdnLarge<Q>>(a, ntiles, s);
 }
@@ -1200,16 +1579,33 @@ hipError_t launch_ctrl_wide(const CtrlArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <class R, typename SH>
+hipError_t launch_ctrl_rd(const CtrlArgs& a, int nw, hipStream_t s) {
+  const size_t lds = R::lds_bytes(nw);
+  hipError_t e = allow_lds(k_ctrl_rd<R, SH>, lds);
+  if (e != hipSuccess) return e;
+  KTimer kt("ctrl", s);
+  hipLaunchKernelGGL((k_ctrl_rd<R, SH>), dim3((a.M + R::BM - 1) / R::BM), dim3(64 * nw), lds, s, a);
+  return hipGetLastError();
+}
+
 template <typename DT, typename SH>
 hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
   using Cf = Cfgs<DT>;
   const int nbtot = a.Nc / 16;
-  if (a.M <= kSmallRows && nbtot <= 9) {
-    if (nbtot <= 1) return launch_ctrl_cfg<typename Cf::template CtrlSmall<1>, SH>(a, s);
-    if (nbtot <= 2) return launch_ctrl_cfg<typename Cf::template CtrlSmall<2>, SH>(a, s);
-    if (nbtot <= 3) return launch_ctrl_cfg<typename Cf::template CtrlSmall<3>, SH>(a, s);
-    if (nbtot <= 5) return launch_ctrl_cfg<typename Cf::template CtrlSmall<5>, SH>(a, s);
-    return launch_ctrl_cfg<typename Cf::template CtrlSmall<9>, SH>(a, s);
+  if (a.M <= kRdRows && nbtot <= 9) {
+    const int nb = nbtot <= 1 ? 1 : nbtot <= 2 ? 2 : nbtot <= 3 ? 3 : nbtot <= 5 ? 5 : 9;
+    const int smax = nb <= 5 ? 8 : 4;  // register budget
+    const int nw = rd_waves((int)a.ldk, Mfma<DT>::KSLICE, smax, 4);
+    if (nw <= 8 && GemmRD<DT, 9, 1, 4, 512>::lds_bytes(nw) <= kRdLdsMax) {
+      switch (nb) {
+        case 1: return launch_ctrl_rd<GemmRD<DT, 1, 1, 8, 512>, SH>(a, nw, s);
+        case 2: return launch_ctrl_rd<GemmRD<DT, 2, 1, 8, 512>, SH>(a, nw, s);
+        case 3: return launch_ctrl_rd<GemmRD<DT, 3, 1, 8, 512>, SH>(a, nw, s);
+        case 5: return launch_ctrl_rd<GemmRD<DT, 5, 1, 8, 512>, SH>(a, nw, s);
+        default: return launch_ctrl_rd<GemmRD<DT, 9, 1, 4, 512>, SH>(a, nw, s);
+      }
+    }
   }
   const int nb = (nbtot + 3) / 4;  // output blocks per wave over four waves
   if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLarge<1>, SH>(a, s);
@@ -1385,6 +1781,12 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
 }
 
 }  // namespace
+
+#ifdef WM_PHASE_TIMING
+extern "C" int wm_debug_phase_copy(void* host, size_t bytes) {
+  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(wm_phase_t), bytes, 0, hipMemcpyDeviceToHost);
+}
+#endif
 
 size_t rollout_workspace_bytes(const Layout& L, int B) {
   size_t o = 0;
