@@ -79,8 +79,8 @@ size_t wm_packed_bytes(const wm_dims* dims) {
 size_t wm_workspace_bytes(const wm_dims* dims, int32_t B, int32_t T, int32_t which) {
   wm::Layout L;
   if (check_dims(dims, &L) != WM_OK || B <= 0 || T < 0) return 0;
-  if (which == 0) return wm::rollout_workspace_bytes(L, B);
-  if (which == 1) return wm::nll_workspace_bytes(L, B, T);
+  if (which == 0) return wm::rollout_workspace(L, B, nullptr, nullptr);
+  if (which == 1) return wm::nll_workspace(L, B, T, nullptr, nullptr);
   return 0;
 }
 
@@ -147,7 +147,7 @@ wm_status wm_rollout(const wm_dims* dims, const void* packed, int32_t B, int32_t
   if ((int64_t)B * (T + 1) > (int64_t)1 << 30)
     return fail(WM_ERR_UNSUPPORTED, "B*(T+1) too large");
   if (T == 0) return ok();
-  const size_t need = wm::rollout_workspace_bytes(L, B);
+  const size_t need = wm::rollout_workspace(L, B, nullptr, nullptr);
   if (!workspace || workspace_bytes < need)
     return fail(WM_ERR_WORKSPACE, "rollout workspace needs %zu bytes, got %zu", need, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
@@ -161,10 +161,7 @@ wm_status wm_rollout(const wm_dims* dims, const void* packed, int32_t B, int32_t
   R.z0 = z0; R.h0 = h0; R.c0 = c0; R.done_io = done_io; R.mask = valid_mask;
   R.z_out = z_out; R.actions = actions; R.rewards = rewards; R.dones = dones;
   R.h_T = h_T; R.c_T = c_T; R.h_trace = h_trace; R.c_trace = c_trace;
-  size_t o = 0;
-  R.hbuf = ws + o; o = wm::wm_align256(o + (size_t)2 * B * L.H * L.esz);
-  R.c = reinterpret_cast<float*>(ws + o); o = wm::wm_align256(o + (size_t)B * L.H * 4);
-  R.done_state = reinterpret_cast<int32_t*>(ws + o);
+  wm::rollout_workspace(L, B, ws, &R);
   wm::Packed P{L, packed};
   hipError_t e = wm::launch_rollout(P, R, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "wm_rollout");
@@ -187,24 +184,18 @@ wm_status wm_nll(const wm_dims* dims, const void* packed, int32_t B, int32_t T, 
   if ((int64_t)B * (T + 1) > (int64_t)1 << 30)
     return fail(WM_ERR_UNSUPPORTED, "B*(T+1) too large");
   if (T == 0) return ok();
-  const size_t need = wm::nll_workspace_bytes(L, B, T);
+  const size_t need = wm::nll_workspace(L, B, T, nullptr, nullptr);
   if (!workspace || workspace_bytes < need)
     return fail(WM_ERR_WORKSPACE, "nll workspace needs %zu bytes, got %zu", need, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(WM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
 
   char* ws = reinterpret_cast<char*>(workspace);
-  const size_t M = (size_t)T * B;
   wm::NllBufs N{};
   N.B = B; N.T = T; N.z = z; N.actions = actions; N.rewards = rewards; N.dones = dones;
   N.lengths = lengths; N.loglik = loglik; N.reward_se = reward_se; N.done_bce = done_bce;
   N.means = means;
-  size_t o = 0;
-  N.trace = ws + o; o = wm::wm_align256(o + (size_t)(T + 1) * B * L.H * L.esz);
-  N.c = reinterpret_cast<float*>(ws + o); o = wm::wm_align256(o + (size_t)B * L.H * 4);
-  N.part = reinterpret_cast<float*>(ws + o); o = wm::wm_align256(o + M * (L.Z / 8) * 4);
-  N.head = reinterpret_cast<float*>(ws + o); o = wm::wm_align256(o + M * 2 * 4);
-  N.wgsum = reinterpret_cast<float*>(ws + o);
+  wm::nll_workspace(L, B, T, ws, &N);
   wm::Packed P{L, packed};
   hipError_t e = wm::launch_nll(P, N, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "wm_nll");

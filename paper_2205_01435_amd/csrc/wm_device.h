@@ -154,36 +154,59 @@ __device__ __forceinline__ uint4 bload_x16(rsrc_t r, uint32_t off) {
   }
 }
 
-// 16 bytes of activations (row m, columns k .. k+VEC-1) converted to DT.
-// Columns [0, Kz) come from the float32 source xz, [Kz, Kz+Kh) from xh (SH
-// elements); anything else, and rows m >= M, read as zero.  Kz and Kh are
-// multiples of VEC, so a vector never straddles the two sources.
-template <typename DT, typename SH>
-__device__ __forceinline__ uint4 load_x16(const float* __restrict__ xz, long ldz, int Kz,
-                                          const SH* __restrict__ xh, long ldxh, int Kh,
-                                          int m, int M, int k) {
-  uint4 zero = make_uint4(0, 0, 0, 0);
-  if (m >= M) return zero;
-  if (k < Kz) {
-    const float* p = xz + (long)m * ldz + k;
-    if constexpr (sizeof(DT) == 4) {
-      return *reinterpret_cast<const uint4*>(p);
-    } else {
-      const float4* q = reinterpret_cast<const float4*>(p);
-      return pack8_bf16(q[0], q[1]);
-    }
+// ---------------------------------------------------------------------------
+// GEMM operand sources.  Each addresses the rows of one work-group tile
+// through a buffer resource, so that rows past the valid ones and columns at
+// or past Kpad read as zero, with straight-line code.  row(i) gives the
+// per-row part of the byte offset, load(row, k, Kpad) the 16 bytes of
+// columns k .. k+VEC-1 (k a multiple of VEC).
+//   SrcX   one row-major DT matrix with a row stride of ld elements (the
+//          weights, and the activation matrix [q(z) | h | 0]);
+//   SrcZH  float32 z [M, Z] followed by float32 h [M, H], converted to DT
+//          (the standalone controller step, whose inputs are two tensors).
+// ---------------------------------------------------------------------------
+template <typename DT_>
+struct SrcX {
+  using DT = DT_;
+  using Row = uint32_t;
+  static constexpr bool kTwo = false;
+  rsrc_t r;
+  uint32_t ldb;  // row stride in bytes
+  // rows m0 .. m0+rows-1 of x, clipped to M; `span` readable columns per row
+  __device__ SrcX(const DT* x, long ld, long span, int m0, int rows, int M) {
+    const long mval = max(0, min(rows, M - m0));
+    ldb = (uint32_t)(ld * (long)sizeof(DT));
+    r = make_rsrc(x + (long)m0 * ld, mval ? (uint32_t)(((mval - 1) * ld + span) * (long)sizeof(DT)) : 0u);
   }
-  k -= Kz;
-  if (k < Kh) {
-    const SH* p = xh + (long)m * ldxh + k;
-    if constexpr (sizeof(SH) == sizeof(DT)) {
-      return *reinterpret_cast<const uint4*>(p);
-    } else {
-      const float4* q = reinterpret_cast<const float4*>(p);
-      return pack8_bf16(q[0], q[1]);
-    }
+  __device__ Row row(int i) const { return (uint32_t)i * ldb; }
+  __device__ uint4 load(Row ro, int k, int Kpad) const {
+    return bload16(r, k < Kpad ? ro + (uint32_t)k * (uint32_t)sizeof(DT) : kOffNone);
   }
-  return zero;
-}
+};
+
+template <typename DT_>
+struct SrcZH {
+  using DT = DT_;
+  using Row = uint2;
+  static constexpr bool kTwo = true;
+  rsrc_t rz, rh;
+  int Z, Kx;
+  uint32_t zb, hb;  // row strides in bytes
+  __device__ SrcZH(const float* z, const float* h, int Z_, int H, int m0, int rows, int M) {
+    const long mval = max(0, min(rows, M - m0));
+    Z = Z_;
+    Kx = Z_ + H;
+    zb = (uint32_t)Z_ * 4u;
+    hb = (uint32_t)H * 4u;
+    rz = make_rsrc(z + (long)m0 * Z_, (uint32_t)(mval * Z_ * 4));
+    rh = make_rsrc(h + (long)m0 * H, (uint32_t)(mval * H * 4));
+  }
+  __device__ Row row(int i) const { return make_uint2((uint32_t)i * zb, (uint32_t)i * hb); }
+  __device__ uint4 load(Row ro, int k, int /*Kpad*/) const {
+    const bool inz = k < Z, inh = k >= Z && k < Kx;
+    return bload_x16<DT, float>(rz, inz ? ro.x + (uint32_t)k * 4u : kOffNone) |
+           bload_x16<DT, float>(rh, inh ? ro.y + (uint32_t)(k - Z) * 4u : kOffNone);
+  }
+};
 
 }  // namespace wm

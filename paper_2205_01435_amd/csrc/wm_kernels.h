@@ -28,7 +28,8 @@ struct RolloutBufs {
   float* rewards;
   uint8_t* dones;
   float *h_T, *c_T, *h_trace, *c_trace;
-  void* hbuf;          // [2, B, H] dtype
+  // workspace
+  void* x;             // [2, B, ldx] dtype: activation matrices X_t, X_t+1
   float* c;            // [B, H]
   int32_t* done_state; // [B]
 };
@@ -41,15 +42,18 @@ struct NllBufs {
   const uint8_t* dones;
   const int32_t* lengths;
   float *loglik, *reward_se, *done_bce, *means;
-  void* trace;   // [T+1, B, H] dtype
+  // workspace
+  void* x;       // [T+1, B, ldx] dtype: activation matrices X_0 .. X_T
   float* c;      // [B, H]
   float* part;   // [T*B, NTd]
   float* head;   // [T*B, 2]
   float* wgsum;  // [nwg, 4]
 };
 
-size_t nll_workspace_bytes(const Layout& L, int B, int T);
-size_t rollout_workspace_bytes(const Layout& L, int B);
+// Workspace sizes; with a non-null `ws` the workspace pointers of the
+// buffer struct are also set (ws must be 256-byte aligned).
+size_t rollout_workspace(const Layout& L, int B, char* ws, RolloutBufs* R);
+size_t nll_workspace(const Layout& L, int B, int T, char* ws, NllBufs* N);
 
 hipError_t launch_pack(const Packed& P, void* packed, const float* W_g, const float* b_g,
                        const float* W_m, const float* b_m, const float* w_r, const float* b_r,

@@ -9,6 +9,11 @@
 //            LSTM cell, state commit (frozen rows copy their state);
 //   k_mdn    mixture head on h_{t+1}, Gumbel-max component pick per latent
 //            dim, Box-Muller draw, z_{t+1} commit.
+// The activations of step t are one matrix X_t = [q(z_t) | h_t | 0] in the
+// compute type (q: round to the compute type), so every GEMM streams a
+// single K-contiguous operand: the gate and controller GEMMs read X_t from
+// column 0, the mixture head reads X_{t+1} from column Z, k_gates writes h_{t+1}
+// and k_mdn q(z_{t+1}) into X_{t+1}.
 // The NLL pass runs k_gates once per step (teacher-forced), then one k_mdn
 // over all T*B rows with a log-likelihood epilogue, then a deterministic
 // reduction.  Nothing here allocates memory.
@@ -21,21 +26,6 @@
 #include "wm_profile.h"
 
 namespace wm {
-
-#ifdef WM_PHASE_TIMING
-// Debug builds only: per-wave wall-clock stamps of kernel phases.
-__device__ unsigned long long wm_phase_t[1 << 20];
-#define WM_STAMP(slot)                                                                    \
-  do {                                                                                    \
-    if ((threadIdx.x & 63) == 0)                                                          \
-      wm_phase_t[((blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 8 + (slot)) &   \
-                 ((1 << 20) - 1)] = wall_clock64();                                       \
-  } while (0)
-#else
-#define WM_STAMP(slot) \
-  do {                 \
-  } while (0)
-#endif
 
 static constexpr float kHalfLn2Pi = 0.91893853320467274178f;
 
@@ -130,8 +120,7 @@ __global__ void k_pack(const Layout L, char* base, const float* __restrict__ W_g
 // summed through LDS at the end, so that only waves with kw == 0 hold the
 // result.
 //   acc[i][j] = W[n0 + (wn*NBW + i)*16 .. +16, :] . X[m0 + (wm*MBW + j)*16 .. +16, :]^T
-// W: [Nrows, ldw] DT (rows >= Nrows read as 0), K padded to Kpad.
-// X: columns [0, Kz) from xz (fp32), [Kz, Kz+Kh) from xh (SH), rows < M.
+// over K = Kpad columns; both sources address the tile's rows only.
 // ===========================================================================
 template <typename DT_, int NBW_, int MBW_, int WAVES_N_, int WAVES_M_, int KSPLIT_, int BK_,
           int STAGES_>
@@ -162,30 +151,19 @@ struct Gemm {
   __device__ static int wn() { return ((threadIdx.x >> 6) / KSPLIT) % WAVES_N; }
   __device__ static int wm() { return (threadIdx.x >> 6) / (KSPLIT * WAVES_N); }
 
-  template <typename SH>
+  template <class S>
   __device__ __forceinline__ static void gload(uint4 (&wr)[WIT], uint4 (&xr)[XIT],
-                                               const DT* __restrict__ W, long ldw, int n0,
-                                               int Nrows, int Kpad, const float* __restrict__ xz,
-                                               long ldz, int Kz, const SH* __restrict__ xh,
-                                               long ldxh, int Kh, int m0, int M, int k0) {
+                                               const SrcX<DT>& w, const S& x, int Kpad, int k0) {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int it = 0; it < WIT; ++it) {
       const int v = tid + it * NT;
-      if (v < WV) {
-        const int r = v / KV, k = k0 + (v % KV) * VEC, n = n0 + r;
-        // the last chunk may overhang the padded K when BK does not divide it
-        wr[it] = (n < Nrows && k < Kpad) ? *reinterpret_cast<const uint4*>(W + (long)n * ldw + k)
-                                         : make_uint4(0, 0, 0, 0);
-      }
+      if (WV % NT == 0 || v < WV) wr[it] = w.load(w.row(v / KV), k0 + (v % KV) * VEC, Kpad);
     }
 #pragma unroll
     for (int it = 0; it < XIT; ++it) {
       const int v = tid + it * NT;
-      if (v < XV) {
-        const int r = v / KV, kv = v % KV;
-        xr[it] = load_x16<DT, SH>(xz, ldz, Kz, xh, ldxh, Kh, m0 + r, M, k0 + kv * VEC);
-      }
+      if (XV % NT == 0 || v < XV) xr[it] = x.load(x.row(v / KV), k0 + (v % KV) * VEC, Kpad);
     }
   }
 
@@ -196,12 +174,14 @@ struct Gemm {
 #pragma unroll
     for (int it = 0; it < WIT; ++it) {
       const int v = tid + it * NT;
-      if (v < WV) *reinterpret_cast<uint4*>(buf + (v / KV) * LDL + (v % KV) * VEC) = wr[it];
+      if (WV % NT == 0 || v < WV)
+        *reinterpret_cast<uint4*>(buf + (v / KV) * LDL + (v % KV) * VEC) = wr[it];
     }
 #pragma unroll
     for (int it = 0; it < XIT; ++it) {
       const int v = tid + it * NT;
-      if (v < XV) *reinterpret_cast<uint4*>(Xl + (v / KV) * LDL + (v % KV) * VEC) = xr[it];
+      if (XV % NT == 0 || v < XV)
+        *reinterpret_cast<uint4*>(Xl + (v / KV) * LDL + (v % KV) * VEC) = xr[it];
     }
   }
 
@@ -226,12 +206,10 @@ struct Gemm {
     }
   }
 
-  template <typename SH>
-  __device__ __forceinline__ static void run(f32x4 (&acc)[NBW][MBW], const DT* __restrict__ W,
-                                             long ldw, int n0, int Nrows, int Kpad,
-                                             const float* __restrict__ xz, long ldz, int Kz,
-                                             const SH* __restrict__ xh, long ldxh, int Kh,
-                                             int m0, int M, DT* lds) {
+  // w: weight rows n0 .. n0+BN-1; x: activation rows m0 .. m0+BM-1.
+  template <class S>
+  __device__ __forceinline__ static void run(f32x4 (&acc)[NBW][MBW], const SrcX<DT>& w, const S& x,
+                                             int Kpad, DT* lds) {
 #pragma unroll
     for (int i = 0; i < NBW; ++i)
 #pragma unroll
@@ -241,8 +219,7 @@ struct Gemm {
     const int nk = (Kpad + BK - 1) / BK;
 #pragma unroll
     for (int s = 0; s < STAGES; ++s)
-      if (s < nk)
-        gload<SH>(wr[s], xr[s], W, ldw, n0, Nrows, Kpad, xz, ldz, Kz, xh, ldxh, Kh, m0, M, s * BK);
+      if (s < nk) gload(wr[s], xr[s], w, x, Kpad, s * BK);
     sstore(wr[0], xr[0], lds);
     __syncthreads();
     for (int kc0 = 0; kc0 < nk; kc0 += STAGES) {
@@ -252,9 +229,7 @@ struct Gemm {
         if (kc < nk) {
           compute(acc, lds + (kc & 1) * BUF);
           if (kc + 1 < nk) sstore(wr[(s + 1) % STAGES], xr[(s + 1) % STAGES], lds + ((kc + 1) & 1) * BUF);
-          if (kc + STAGES < nk)
-            gload<SH>(wr[s], xr[s], W, ldw, n0, Nrows, Kpad, xz, ldz, Kz, xh, ldxh, Kh, m0, M,
-                      (kc + STAGES) * BK);
+          if (kc + STAGES < nk) gload(wr[s], xr[s], w, x, Kpad, (kc + STAGES) * BK);
           __syncthreads();
         }
       }
@@ -310,7 +285,7 @@ static inline unsigned grid_of(int nt_count, int mt_count) {
 }
 
 // ===========================================================================
-// k_gates: g = W [z | h]^T + WaT[a] + b, LSTM cell, commit.
+// k_gates: g = W [q(z) | h]^T + WaT[a] + b, LSTM cell, commit.
 // Rollout mode: a < 0 marks a frozen row, whose state is copied forward.
 // NLL mode: every row is live; a outside [0, A) adds no column.
 // ===========================================================================
@@ -318,12 +293,10 @@ struct GatesArgs {
   const void* Wg;
   const void* WaT;
   const float* bg;
-  long ldk;
+  long ldk, ldx;
   int H, A, Z, M;
-  const float* xz;  // [M, Z] fp32
-  long ldz;
-  const void* h_in;  // [M, H] DT
-  void* h_out;       // [M, H] DT
+  const void* x_in;  // X_t [M, ldx] DT
+  void* x_out;       // X_t+1 [M, ldx] DT: h_t+1 goes to columns Z .. Z+H-1
   float* c;          // [M, H] fp32, updated in place
   const int32_t* act;
   float* h_trace;  // [M, H] fp32 or null
@@ -334,10 +307,12 @@ struct GatesArgs {
 // LSTM cell and state commit of hidden unit u of row m.  gates_pre loads
 // everything that does not depend on the GEMM (action, bias plus gathered
 // one-hot column, cell state), so that callers can issue it early;
-// gates_fin adds the GEMM part (W [z | h]) of the four gate pre-activations
-// i, f, g, o and commits.  A frozen rollout row copies its state.
+// gates_fin adds the GEMM part (W [q(z) | h]) of the four gate
+// pre-activations i, f, g, o and commits.  A frozen rollout row copies its
+// state.
 struct GatePre {
-  long e;        // element index m * H + u
+  long e;        // m * H + u (cell state, traces)
+  long xe;       // m * ldx + Z + u (h in X)
   bool live;
   float4 add;    // bias + one-hot column, per gate
   float c;       // cell state c_t
@@ -350,6 +325,7 @@ __device__ __forceinline__ GatePre gates_pre(const GatesArgs& p, int m, int u) {
   const int a = p.act[m];
   q.live = p.nll_mode || a >= 0;
   q.e = (long)m * H + u;
+  q.xe = (long)m * p.ldx + p.Z + u;
   q.add = *reinterpret_cast<const float4*>(p.bg + 4 * u);
   if (a >= 0 && a < p.A) {
     const DT* WaT = reinterpret_cast<const DT*>(p.WaT);
@@ -366,28 +342,21 @@ __device__ __forceinline__ GatePre gates_pre(const GatesArgs& p, int m, int u) {
 template <typename DT>
 __device__ __forceinline__ void gates_fin(const GatesArgs& p, const GatePre& q, float pi, float pf,
                                           float pg, float po) {
-  DT* h_out = reinterpret_cast<DT*>(p.h_out);
+  DT* x_out = reinterpret_cast<DT*>(p.x_out);
   float hv, cv;
   if (!q.live) {
-    hv = DType<DT>::load(reinterpret_cast<const DT*>(p.h_in), q.e);
+    hv = DType<DT>::load(reinterpret_cast<const DT*>(p.x_in), q.xe);
     cv = q.c;
-    DType<DT>::store(h_out, q.e, hv);
   } else {
     cv = sigmoidf(pf + q.add.y) * q.c + sigmoidf(pi + q.add.x) * tanhf(pg + q.add.z);
     hv = DType<DT>::round(sigmoidf(po + q.add.w) * tanhf(cv));
     p.c[q.e] = cv;
-    DType<DT>::store(h_out, q.e, hv);
   }
+  DType<DT>::store(x_out, q.xe, hv);
   if (p.h_trace) {
     p.h_trace[q.e] = hv;
     p.c_trace[q.e] = cv;
   }
-}
-
-template <typename DT>
-__device__ __forceinline__ void gates_commit(const GatesArgs& p, int m, int u, float pi, float pf,
-                                             float pg, float po) {
-  gates_fin<DT>(p, gates_pre<DT>(p, m, u), pi, pf, pg, po);
 }
 
 template <class C>
@@ -395,14 +364,13 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
   using DT = typename C::DT;
   constexpr int NBW = C::NBW, MBW = C::MBW;
   __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
-  DT* lds = reinterpret_cast<DT*>(lds_raw);
   int nt, mt;
   if (!tile_of((4 * p.H + C::BN - 1) / C::BN, (p.M + C::BM - 1) / C::BM, nt, mt)) return;
   const int n0 = nt * C::BN, m0 = mt * C::BM;
+  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wg), p.ldk, p.ldk, n0, C::BN, 4 * p.H);
+  const SrcX<DT> x(reinterpret_cast<const DT*>(p.x_in), p.ldx, p.ldx, m0, C::BM, p.M);
   f32x4 acc[NBW][MBW];
-  const DT* h_in = reinterpret_cast<const DT*>(p.h_in);
-  C::template run<DT>(acc, reinterpret_cast<const DT*>(p.Wg), p.ldk, n0, 4 * p.H, (int)p.ldk,
-                      p.xz, p.ldz, p.Z, h_in, p.H, p.H, m0, p.M, lds);
+  C::run(acc, w, x, (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
   if (C::kw() != 0) return;
 
   const int lane = threadIdx.x & 63;
@@ -414,7 +382,8 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
 #pragma unroll
     for (int i = 0; i < NBW; ++i) {
       const int u = (n0 + (wn * NBW + i) * 16) / 4 + (lane >> 4);
-      if (u < p.H) gates_commit<DT>(p, m, u, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      if (u < p.H)
+        gates_fin<DT>(p, gates_pre<DT>(p, m, u), acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
   }
 }
@@ -429,9 +398,11 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
 struct MdnArgs {
   const void* Wm;
   const float* bm;
-  long ldh;
+  long ldh, ldx;
   int H, Z, K, Nm, M;
-  const void* h;  // [M, H] DT
+  // [M, ldx] DT activation rows: the head reads h at columns Z ..; the
+  // rollout writes q(z_t+1) to columns 0 .. Z-1
+  void* x;
   // rollout
   const int32_t* act;
   const float* z_prev;  // [M, Z]
@@ -551,26 +522,33 @@ __device__ __forceinline__ float mdn_loglik(const MdnArgs& p, float x, const flo
   return tmax + logf(st);
 }
 
+// z_{t+1,j} of row m goes to the fp32 output and, rounded, to X_{t+1}.
+template <typename DT>
+__device__ __forceinline__ void mdn_commit(const MdnArgs& p, int m, int j, float z) {
+  p.z_next[(long)m * p.Z + j] = z;
+  DType<DT>::store(reinterpret_cast<DT*>(p.x), (long)m * p.ldx + j, z);
+}
+
 template <class C>
 __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
   using DT = typename C::DT;
   constexpr int Q = C::NBW, MBW = C::MBW, WAVES_N = C::WAVES_N, WAVES_M = C::WAVES_M;
   static_assert(WAVES_N == 2, "the NLL epilogue sums two dim groups per work-group");
   __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
-  DT* lds = reinterpret_cast<DT*>(lds_raw);
   __shared__ float red[WAVES_M][MBW * 16];
   int ntile, mt;
   if (!tile_of(p.ntiles, (p.M + C::BM - 1) / C::BM, ntile, mt)) return;
   const int n0 = ntile * C::BN, m0 = mt * C::BM;
+  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wm), p.ldh, p.ldh, n0, C::BN, p.Nm);
+  const SrcX<DT> x(reinterpret_cast<const DT*>(p.x) + p.Z, p.ldx, p.ldx - p.Z, m0, C::BM, p.M);
   f32x4 acc[Q][MBW];
-  C::template run<DT>(acc, reinterpret_cast<const DT*>(p.Wm), p.ldh, n0, p.Nm, (int)p.ldh,
-                      nullptr, 0, 0, reinterpret_cast<const DT*>(p.h), p.H, p.H, m0, p.M, lds);
+  C::run(acc, w, x, (int)p.ldh, reinterpret_cast<DT*>(lds_raw));
   const bool owner = C::kw() == 0;  // holds the summed tile
 
   const int lane = threadIdx.x & 63;
   const int wn = C::wn(), wmi = C::wm();
   const int g = lane >> 4;
-  const int Z = p.Z, K = p.K;
+  const int Z = p.Z;
   const int J = ntile * WAVES_N + wn;  // dim group of this wave
   const int j = 4 * J + g;             // latent dim of this lane
   const bool head_tile = p.nll_mode && ntile == p.ntd;
@@ -605,9 +583,8 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
     for (int jj = 0; jj < MBW; ++jj) {
       const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
       if (m >= p.M || j >= Z) continue;
-      const long e = (long)m * Z + j;
       if (p.act[m] < 0) {
-        p.z_next[e] = p.z_prev[e];
+        mdn_commit<DT>(p, m, j, p.z_prev[(long)m * Z + j]);
         continue;
       }
       float feat[4 * Q];
@@ -615,7 +592,7 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
       for (int q = 0; q < Q; ++q)
 #pragma unroll
         for (int v = 0; v < 4; ++v) feat[4 * q + v] = acc[q][jj][v] + bias[4 * q + v];
-      p.z_next[e] = mdn_draw<Q>(p, rng, m, j, feat);
+      mdn_commit<DT>(p, m, j, mdn_draw<Q>(p, rng, m, j, feat));
     }
   } else {
 #pragma unroll
@@ -655,9 +632,10 @@ struct CtrlArgs {
   const float* bc;
   long ldk;
   int Z, H, A, Nc, M;
-  const float* z;  // [M, Z] fp32
-  long ldz;
-  const void* h;  // [M, H] SH
+  const void* x;   // rollout: X_t [M, ldx] DT
+  long ldx;
+  const float* z;  // controller step: z [M, Z] and h [M, H], fp32
+  const float* h;
   const uint8_t* mask;
   uint32_t k0, k1, step, traj0;
   int mode;
@@ -706,8 +684,17 @@ __device__ __forceinline__ void ctrl_row_commit(const CtrlArgs& p, const Rng& rn
   p.done_state[m] = ds;
 }
 
-template <typename DT, typename SH, int NBW, int MBW, int BKC>
+// Activation source of the controller kernels for rows m0 .. m0+rows-1.
+template <class S>
+__device__ __forceinline__ S ctrl_src(const CtrlArgs& p, int m0, int rows) {
+  using DT = typename S::DT;
+  if constexpr (S::kTwo) return S(p.z, p.h, p.Z, p.H, m0, rows, p.M);
+  else return S(reinterpret_cast<const DT*>(p.x), p.ldx, p.ldx, m0, rows, p.M);
+}
+
+template <class S, int NBW, int MBW, int BKC>
 __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
+  using DT = typename S::DT;
   constexpr int VEC = DType<DT>::VEC;
   constexpr int BM = 16 * MBW;
   constexpr int LDL = BKC + VEC;
@@ -723,7 +710,7 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
   const int m0 = blockIdx.x * BM;
   const int nbtot = p.Nc / 16;
   const DT* W = reinterpret_cast<const DT*>(p.Wc);
-  const SH* hsrc = reinterpret_cast<const SH*>(p.h);
+  const S src = ctrl_src<S>(p, m0, BM);
 
   f32x4 acc[NBW][MBW];
 #pragma unroll
@@ -735,8 +722,7 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
     __syncthreads();
     for (int v = tid; v < BM * (BKC / VEC); v += 256) {
       const int r = v / (BKC / VEC), kv = v % (BKC / VEC);
-      *reinterpret_cast<uint4*>(xl + r * LDL + kv * VEC) =
-          load_x16<DT, SH>(p.z, p.ldz, p.Z, hsrc, p.H, p.H, m0 + r, p.M, kc + kv * VEC);
+      *reinterpret_cast<uint4*>(xl + r * LDL + kv * VEC) = src.load(src.row(r), kc + kv * VEC, (int)p.ldk);
     }
     __syncthreads();
 #pragma unroll
@@ -899,7 +885,7 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
 // through LDS once per K chunk.  Waves with kw != 0 only help with the K
 // loop.  (k_ctrl_wide above reads the weights straight from global memory and
 // covers larger action counts.)
-template <class C, typename SH>
+template <class C, class S>
 __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
   using DT = typename C::DT;
   constexpr int NBW = C::NBW, MBW = C::MBW, WN = C::WAVES_N, BM = C::BM;
@@ -915,9 +901,8 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
   const int m0 = blockIdx.x * BM;
   const int nbtot = p.Nc / 16;
   f32x4 acc[NBW][MBW];
-  C::template run<SH>(acc, reinterpret_cast<const DT*>(p.Wc), p.ldk, 0, p.Nc, (int)p.ldk, p.z,
-                      p.ldz, p.Z, reinterpret_cast<const SH*>(p.h), p.H, p.H, m0, p.M,
-                      reinterpret_cast<DT*>(lds_raw));
+  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wc), p.ldk, p.ldk, 0, p.Nc, p.Nc);
+  C::run(acc, w, ctrl_src<S>(p, m0, BM), (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
   const bool owner = C::kw() == 0;
   const int wn = C::wn(), wmi = C::wm();
 
@@ -1090,54 +1075,30 @@ struct GemmRD {
   }
   __device__ static float* E(float* lds) { return lds + (blockDim.x >> 6) * TILE; }
 
-  template <typename SH>
-  __device__ __forceinline__ static void run(float* lds, const DT* __restrict__ W, long ldw, int n0,
-                                             int Nrows, int Kpad, const float* __restrict__ xz,
-                                             long ldz, int Kz, const SH* __restrict__ xh, long ldxh,
-                                             int Kh, int m0, int M) {
+  // w: weight rows n0 .. n0+BN-1; x: activation rows m0 .. m0+BM-1.
+  template <class S>
+  __device__ __forceinline__ static void run(float* lds, const SrcX<DT>& w, const S& x, int Kpad) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     const int g = lane >> 4, r16 = lane & 15;
     const int nsl = (Kpad + KSLICE - 1) / KSLICE;
     const int per = (nsl + nw - 1) / nw;
-    WM_STAMP(1);
     const int s0 = wave * per;
-    const int Kx = Kz + Kh;
-    // resources over the tile's valid rows: rows past them read as zero
-    const int nval = max(0, min(BN, Nrows - n0)), mval = max(0, min(BM, M - m0));
-    const rsrc_t rw = make_rsrc(W + (long)n0 * ldw, (uint32_t)(nval * ldw * (long)sizeof(DT)));
-    const rsrc_t rz = make_rsrc(xz ? xz + (long)m0 * ldz : xz, xz ? (uint32_t)(mval * ldz * 4L) : 0u);
-    const rsrc_t rh = make_rsrc(xh + (long)m0 * ldxh, (uint32_t)(mval * ldxh * (long)sizeof(SH)));
-    uint32_t wo[NBW], zo[MBW], ho[MBW];
+    typename SrcX<DT>::Row wo[NBW];
+    typename S::Row xo[MBW];
 #pragma unroll
-    for (int i = 0; i < NBW; ++i) wo[i] = (uint32_t)((i * 16 + r16) * ldw * sizeof(DT));
+    for (int i = 0; i < NBW; ++i) wo[i] = w.row(i * 16 + r16);
 #pragma unroll
-    for (int j = 0; j < MBW; ++j) {
-      zo[j] = (uint32_t)((j * 16 + r16) * ldz * 4);
-      ho[j] = (uint32_t)((j * 16 + r16) * ldxh * sizeof(SH));
-    }
+    for (int j = 0; j < MBW; ++j) xo[j] = x.row(j * 16 + r16);
     uint4 wf[NBW][SMAX], xf[MBW][SMAX];
 #pragma unroll
     for (int s = 0; s < SMAX; ++s) {
       const int sl = s0 + s;
-      const int kb = sl * KSLICE;             // first column of the slice (uniform)
-      const int kl = kb + g * VEC;            // first column of this lane's vector
       if (s < per && sl < nsl) {
+        const int kl = sl * KSLICE + g * VEC;  // first column of this lane's vector
 #pragma unroll
-        for (int i = 0; i < NBW; ++i) wf[i][s] = bload16(rw, wo[i] + (uint32_t)(kl * sizeof(DT)));
-        if (kb + KSLICE <= Kz) {              // slice inside the z columns
+        for (int i = 0; i < NBW; ++i) wf[i][s] = w.load(wo[i], kl, Kpad);
 #pragma unroll
-          for (int j = 0; j < MBW; ++j) xf[j][s] = bload_x16<DT, float>(rz, zo[j] + (uint32_t)(kl * 4));
-        } else if (kb >= Kz && kb + KSLICE <= Kx) {  // inside the h columns
-#pragma unroll
-          for (int j = 0; j < MBW; ++j)
-            xf[j][s] = bload_x16<DT, SH>(rh, ho[j] + (uint32_t)((kl - Kz) * sizeof(SH)));
-        } else {                              // straddles a boundary: per-lane source
-          const bool inz = kl < Kz, inh = kl >= Kz && kl < Kx;
-#pragma unroll
-          for (int j = 0; j < MBW; ++j)
-            xf[j][s] = bload_x16<DT, float>(rz, inz ? zo[j] + (uint32_t)(kl * 4) : kOffNone) |
-                       bload_x16<DT, SH>(rh, inh ? ho[j] + (uint32_t)((kl - Kz) * sizeof(SH)) : kOffNone);
-        }
+        for (int j = 0; j < MBW; ++j) xf[j][s] = x.load(xo[j], kl, Kpad);
       } else {
 #pragma unroll
         for (int i = 0; i < NBW; ++i) wf[i][s] = make_uint4(0, 0, 0, 0);
@@ -1150,7 +1111,6 @@ struct GemmRD {
     for (int i = 0; i < NBW; ++i)
 #pragma unroll
       for (int j = 0; j < MBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    WM_STAMP(2);
 #pragma unroll
     for (int s = 0; s < SMAX; ++s) {
       if (s < per && s0 + s < nsl) {
@@ -1160,7 +1120,6 @@ struct GemmRD {
           for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], wf[i][s], xf[j][s]);
       }
     }
-    WM_STAMP(3);
     float* P = lds + wave * TILE;
 #pragma unroll
     for (int i = 0; i < NBW; ++i)
@@ -1168,23 +1127,21 @@ struct GemmRD {
       for (int j = 0; j < MBW; ++j)
         *reinterpret_cast<f32x4*>(P + ((i * MBW + j) * 64 + lane) * 4) = acc[i][j];
     __syncthreads();
-    WM_STAMP(4);
     float* Et = E(lds);
     for (int e = threadIdx.x; e < TILE; e += blockDim.x) {
       float sum = 0.f;
-      for (int w = 0; w < nw; ++w) sum += lds[w * TILE + e];
+      for (int w2 = 0; w2 < nw; ++w2) sum += lds[w2 * TILE + e];
       const int v = e & 3, l = (e >> 2) & 63, ij = e >> 8;
       const int j = ij % MBW, i = ij / MBW;
       Et[(j * 16 + (l & 15)) * ELD + i * 16 + 4 * (l >> 4) + v] = sum;
     }
     __syncthreads();
-    WM_STAMP(5);
   }
 };
 
-// Gates on the register-direct core: tiles of 8 hidden units (32 gate rows)
-// x 32 rows.  Each of the first 256 threads owns one (unit, row) of the
-// epilogue and loads its inputs before the GEMM.
+// Gates on the register-direct core: tiles of BN/4 hidden units x BM rows.
+// Each of the first threads owns one (unit, row) of the epilogue and loads
+// its inputs before the GEMM.
 template <class R>
 __global__ void __launch_bounds__(R::MAXT) k_gates_rd(const GatesArgs p) {
   using DT = typename R::DT;
@@ -1198,20 +1155,19 @@ __global__ void __launch_bounds__(R::MAXT) k_gates_rd(const GatesArgs p) {
   const int ul = t % UPT, ml = t / UPT;
   const int m = m0 + ml, u = n0 / 4 + ul;
   const bool mine = t < UPT * R::BM && m < p.M && u < p.H;
-  WM_STAMP(0);
   GatePre pre{};
   if (mine) pre = gates_pre<DT>(p, m, u);
-  R::template run<DT>(lds_dyn, reinterpret_cast<const DT*>(p.Wg), p.ldk, n0, 4 * p.H, (int)p.ldk,
-                      p.xz, p.ldz, p.Z, reinterpret_cast<const DT*>(p.h_in), p.H, p.H, m0, p.M);
+  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wg), p.ldk, p.ldk, n0, R::BN, 4 * p.H);
+  const SrcX<DT> x(reinterpret_cast<const DT*>(p.x_in), p.ldx, p.ldx, m0, R::BM, p.M);
+  R::run(lds_dyn, w, x, (int)p.ldk);
   if (mine) {
     const float4 g4 = *reinterpret_cast<const float4*>(R::E(lds_dyn) + ml * R::ELD + 4 * ul);
     gates_fin<DT>(p, pre, g4.x, g4.y, g4.z, g4.w);
   }
-  WM_STAMP(6);
 }
 
 // Rollout mixture head on the register-direct core: one group of four
-// latent dims (16Q feature rows) x 32 rows per tile.  Each of the first 128
+// latent dims (16Q feature rows) x BM rows per tile.  Each of the first
 // threads owns one (dim, row) and draws its noise before the GEMM.
 template <class R>
 __global__ void __launch_bounds__(R::MAXT) k_mdn_rd(const MdnArgs p) {
@@ -1234,12 +1190,12 @@ __global__ void __launch_bounds__(R::MAXT) k_mdn_rd(const MdnArgs p) {
     if (live) noise = mdn_noise(p, rng, m, j);
     else zprev = p.z_prev[(long)m * p.Z + j];
   }
-  R::template run<DT>(lds_dyn, reinterpret_cast<const DT*>(p.Wm), p.ldh, n0, p.Nm, (int)p.ldh,
-                      nullptr, 0, 0, reinterpret_cast<const DT*>(p.h), p.H, p.H, m0, p.M);
+  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wm), p.ldh, p.ldh, n0, R::BN, p.Nm);
+  const SrcX<DT> x(reinterpret_cast<const DT*>(p.x) + p.Z, p.ldx, p.ldx - p.Z, m0, R::BM, p.M);
+  R::run(lds_dyn, w, x, (int)p.ldh);
   if (!mine) return;
-  const long e = (long)m * p.Z + j;
   if (!live) {
-    p.z_next[e] = zprev;
+    mdn_commit<DT>(p, m, j, zprev);
     return;
   }
   const float* E = R::E(lds_dyn);
@@ -1251,7 +1207,7 @@ __global__ void __launch_bounds__(R::MAXT) k_mdn_rd(const MdnArgs p) {
       const int r = 16 * q + 4 * d + v;
       feat[4 * q + v] = E[ml * R::ELD + r] + p.bm[n0 + r];
     }
-  p.z_next[e] = mdn_pick<Q>(p, noise, feat);
+  mdn_commit<DT>(p, m, j, mdn_pick<Q>(p, noise, feat));
 }
 
 // Controller on the register-direct core: all Nc outputs x 16 rows.  Each row
@@ -1259,7 +1215,7 @@ __global__ void __launch_bounds__(R::MAXT) k_mdn_rd(const MdnArgs p) {
 // lane taking the action blocks sub + 16 h, h < 4 (four actions and one
 // Philox block each); their Gumbel noise and mask bits are drawn before the
 // GEMM.  Requires A <= 256.
-template <class R, typename SH>
+template <class R, class S>
 __global__ void __launch_bounds__(R::MAXT) k_ctrl_rd(const CtrlArgs p) {
   using DT = typename R::DT;
   extern __shared__ __attribute__((aligned(16))) float lds_dyn[];
@@ -1287,8 +1243,8 @@ __global__ void __launch_bounds__(R::MAXT) k_ctrl_rd(const CtrlArgs p) {
       }
     }
   }
-  R::template run<SH>(lds_dyn, reinterpret_cast<const DT*>(p.Wc), p.ldk, 0, p.Nc, (int)p.ldk, p.z,
-                      p.ldz, p.Z, reinterpret_cast<const SH*>(p.h), p.H, p.H, m0, p.M);
+  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wc), p.ldk, p.ldk, 0, R::BN, p.Nc);
+  R::run(lds_dyn, w, ctrl_src<S>(p, m0, R::BM), (int)p.ldk);
   if (wave >= 4) return;  // rows live in the first four waves; no barrier below
   const float* lg = R::E(lds_dyn) + ml * R::ELD;
   float best = -INFINITY, mx = -INFINITY;
@@ -1336,23 +1292,32 @@ __global__ void __launch_bounds__(R::MAXT) k_ctrl_rd(const CtrlArgs p) {
 // ===========================================================================
 // small element-wise kernels
 // ===========================================================================
+// X_0 = [q(z0) | q(h0) | 0], zero padding columns of X_1, z_out[0] = z0,
+// c = c0, done state, traces of step 0.
 template <typename DT>
-__global__ void k_rollout_init(int B, int Z, int H, const float* __restrict__ z0,
+__global__ void k_rollout_init(int B, int Z, int H, int ldx, const float* __restrict__ z0,
                                const float* __restrict__ h0, const float* __restrict__ c0,
                                const uint8_t* __restrict__ done_io, float* __restrict__ z_out,
-                               DT* __restrict__ hbuf, float* __restrict__ c,
+                               DT* __restrict__ X0, DT* __restrict__ X1, float* __restrict__ c,
                                int32_t* __restrict__ done_state, float* __restrict__ h_trace,
                                float* __restrict__ c_trace) {
   const long stride = (long)gridDim.x * blockDim.x;
   const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  for (long i = i0; i < (long)B * ldx; i += stride) {
+    const long b = i / ldx;
+    const int col = (int)(i % ldx);
+    float v = 0.f;
+    if (col < Z) v = z0[b * Z + col];
+    else if (col < Z + H) v = h0 ? h0[b * H + col - Z] : 0.f;
+    DType<DT>::store(X0, i, v);
+    if (col >= Z + H) DType<DT>::store(X1, i, 0.f);
+  }
   for (long i = i0; i < (long)B * Z; i += stride) z_out[i] = z0[i];
   for (long i = i0; i < (long)B * H; i += stride) {
-    const float hv = DType<DT>::round(h0 ? h0[i] : 0.f);
     const float cv = c0 ? c0[i] : 0.f;
-    DType<DT>::store(hbuf, i, hv);
     c[i] = cv;
     if (h_trace) {
-      h_trace[i] = hv;
+      h_trace[i] = DType<DT>::round(h0 ? h0[i] : 0.f);
       c_trace[i] = cv;
     }
   }
@@ -1360,25 +1325,35 @@ __global__ void k_rollout_init(int B, int Z, int H, const float* __restrict__ z0
 }
 
 template <typename DT>
-__global__ void k_rollout_finish(int B, int H, const DT* __restrict__ hbuf,
+__global__ void k_rollout_finish(int B, int Z, int H, int ldx, const DT* __restrict__ XT,
                                  const float* __restrict__ c, const int32_t* __restrict__ done_state,
                                  float* __restrict__ h_T, float* __restrict__ c_T,
                                  uint8_t* __restrict__ done_io) {
   const long stride = (long)gridDim.x * blockDim.x;
   const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
   for (long i = i0; i < (long)B * H; i += stride) {
-    if (h_T) h_T[i] = DType<DT>::load(hbuf, i);
+    if (h_T) h_T[i] = DType<DT>::load(XT, (i / H) * ldx + Z + i % H);
     if (c_T) c_T[i] = c[i];
   }
   if (done_io)
     for (long i = i0; i < B; i += stride) done_io[i] = (uint8_t)done_state[i];
 }
 
+// X_t[:, 0:Z] = q(z_t) for t = 0..T, padding columns zero, h_0 = c_0 = 0.
 template <typename DT>
-__global__ void k_nll_init(long n, DT* __restrict__ trace0, float* __restrict__ c) {
+__global__ void k_nll_init(int T, int B, int Z, int H, int ldx, const float* __restrict__ z,
+                           DT* __restrict__ X, float* __restrict__ c) {
   const long stride = (long)gridDim.x * blockDim.x;
-  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-    DType<DT>::store(trace0, i, 0.f);
+  const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const int ncol = ldx - H;  // z columns, then padding columns
+  for (long i = i0; i < (long)(T + 1) * B * ncol; i += stride) {
+    const long r = i / ncol;
+    const int cc = (int)(i % ncol);
+    if (cc < Z) DType<DT>::store(X, r * ldx + cc, z[r * Z + cc]);
+    else DType<DT>::store(X, r * ldx + H + cc, 0.f);
+  }
+  for (long i = i0; i < (long)B * H; i += stride) {
+    DType<DT>::store(X, (i / H) * ldx + Z + i % H, 0.f);
     c[i] = 0.f;
   }
 }
@@ -1456,13 +1431,16 @@ namespace {
 // (MFMA-bound: more reuse per LDS byte).
 constexpr int kSmallRows = 2048;
 
+#ifndef WM_MDN_LARGE_F32_MBW
+#define WM_MDN_LARGE_F32_MBW 1
+#endif
+
 template <typename DT> struct Cfgs;
 template <> struct Cfgs<float> {
   using GatesSmall = Gemm<float, 2, 1, 2, 2, 1, 32, 4>;  // 64 x 32
   using GatesLarge = Gemm<float, 4, 2, 2, 2, 1, 32, 3>;  // 128 x 64
   template <int Q> using MdnSmall = Gemm<float, Q, 1, 2, 1, 2, 32, 4>;  // 32Q x 16, K split 2
-  template <int Q> using MdnLarge = Gemm<float, Q, 2, 2, 2, 1, 32, 3>;  // 32Q x 64
-  template <int NB> using CtrlSmall = Gemm<float, NB, 1, 1, 1, 4, 64, 3>;  // 16NB x 16, K split 4
+  template <int Q> using MdnLarge = Gemm<float, Q, WM_MDN_LARGE_F32_MBW, 2, 2, 1, 32, 3>;
   template <int NB> using CtrlLarge = Gemm<float, NB, 4, 4, 1, 1, 32, 3>;  // 64NB x 64
   static constexpr int WIDE_BKC = 64;
 };
@@ -1471,22 +1449,21 @@ template <> struct Cfgs<bf16_t> {
   using GatesLarge = Gemm<bf16_t, 4, 4, 2, 2, 1, 64, 2>;  // 128 x 128
   template <int Q> using MdnSmall = Gemm<bf16_t, Q, 1, 2, 1, 2, 64, 4>;
   template <int Q> using MdnLarge = Gemm<bf16_t, Q, 2, 2, 2, 1, 64, 2>;
-  template <int NB> using CtrlSmall = Gemm<bf16_t, NB, 1, 1, 1, 4, 128, 3>;
   template <int NB> using CtrlLarge = Gemm<bf16_t, NB, 4, 4, 1, 1, 64, 2>;
   static constexpr int WIDE_BKC = 128;
 };
 
-template <class C>
-hipError_t launch_gates_cfg(const GatesArgs& a, hipStream_t s) {
-  const int nt = (4 * a.H + C::BN - 1) / C::BN, mt = (a.M + C::BM - 1) / C::BM;
-  KTimer kt("gates", s);
-  hipLaunchKernelGGL((k_gates<C>), dim3(grid_of(nt, mt)), dim3(C::NT), 0, s, a);
-  return hipGetLastError();
-}
-
-// Register-direct kernels serve calls with at most kRdRows rows when the K
-// slices fit SMAX per wave on the compiled block size.
-constexpr int kRdRows = 1024;
+// Register-direct kernels serve calls with at most this many rows, when the
+// K slices fit SMAX per wave on the compiled block size.
+#ifndef WM_RD_GATES_ROWS
+#define WM_RD_GATES_ROWS 256
+#endif
+#ifndef WM_RD_MDN_ROWS
+#define WM_RD_MDN_ROWS 1024
+#endif
+#ifndef WM_RD_CTRL_ROWS
+#define WM_RD_CTRL_ROWS 1024
+#endif
 constexpr size_t kRdLdsMax = 64 * 1024;
 
 inline int rd_waves(int Kpad, int kslice, int smax, int min_waves) {
@@ -1503,12 +1480,20 @@ hipError_t allow_lds(F* kernel, size_t bytes) {
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
+template <class C>
+hipError_t launch_gates_cfg(const GatesArgs& a, hipStream_t s) {
+  const int nt = (4 * a.H + C::BN - 1) / C::BN, mt = (a.M + C::BM - 1) / C::BM;
+  KTimer kt("gates", s);
+  hipLaunchKernelGGL((k_gates<C>), dim3(grid_of(nt, mt)), dim3(C::NT), 0, s, a);
+  return hipGetLastError();
+}
+
 template <typename DT>
 hipError_t launch_gates(const GatesArgs& a, hipStream_t s) {
   using R = GemmRD<DT, 2, 2, 8, 512>;
   const int nw = rd_waves((int)a.ldk, R::KSLICE, R::SMAX, 4);
   const size_t lds = R::lds_bytes(nw);
-  if (a.M <= kRdRows && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
+  if (a.M <= WM_RD_GATES_ROWS && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
     hipError_t e = allow_lds(k_gates_rd<R>, lds);
     if (e != hipSuccess) return e;
     const int nt = (4 * a.H + R::BN - 1) / R::BN, mt = (a.M + R::BM - 1) / R::BM;
@@ -1535,7 +1520,7 @@ hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
     using R = GemmRD<DT, Q, 2, (Q <= 4 ? 8 : 4), 512>;
     const int nw = rd_waves((int)a.ldh, R::KSLICE, R::SMAX, 4);
     const size_t lds = R::lds_bytes(nw);
-    if (a.M <= kRdRows && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
+    if (a.M <= WM_RD_MDN_ROWS && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
       hipError_t e = allow_lds(k_mdn_rd<R>, lds);
       if (e != hipSuccess) return e;
       MdnArgs b = a;
@@ -1563,60 +1548,62 @@ hipError_t launch_mdn(const MdnArgs& a, int Q, int ntiles, hipStream_t s) {
   }
 }
 
-template <class C, typename SH>
+template <class C, class S>
 hipError_t launch_ctrl_cfg(const CtrlArgs& a, hipStream_t s) {
   KTimer kt("ctrl", s);
-  hipLaunchKernelGGL((k_ctrl<C, SH>), dim3((a.M + C::BM - 1) / C::BM), dim3(C::NT), 0, s, a);
+  hipLaunchKernelGGL((k_ctrl<C, S>), dim3((a.M + C::BM - 1) / C::BM), dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
-template <typename DT, typename SH, int NBW, int MBW>
+template <class S, int NBW, int MBW>
 hipError_t launch_ctrl_wide(const CtrlArgs& a, hipStream_t s) {
   constexpr int BM = 16 * MBW;
   KTimer kt("ctrl", s);
-  hipLaunchKernelGGL((k_ctrl_wide<DT, SH, NBW, MBW, Cfgs<DT>::WIDE_BKC>), dim3((a.M + BM - 1) / BM),
-                     dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_ctrl_wide<S, NBW, MBW, Cfgs<typename S::DT>::WIDE_BKC>),
+                     dim3((a.M + BM - 1) / BM), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-template <class R, typename SH>
+template <class R, class S>
 hipError_t launch_ctrl_rd(const CtrlArgs& a, int nw, hipStream_t s) {
   const size_t lds = R::lds_bytes(nw);
-  hipError_t e = allow_lds(k_ctrl_rd<R, SH>, lds);
+  hipError_t e = allow_lds(k_ctrl_rd<R, S>, lds);
   if (e != hipSuccess) return e;
   KTimer kt("ctrl", s);
-  hipLaunchKernelGGL((k_ctrl_rd<R, SH>), dim3((a.M + R::BM - 1) / R::BM), dim3(64 * nw), lds, s, a);
+  hipLaunchKernelGGL((k_ctrl_rd<R, S>), dim3((a.M + R::BM - 1) / R::BM), dim3(64 * nw), lds, s, a);
   return hipGetLastError();
 }
 
-template <typename DT, typename SH>
+// S: activation source (SrcX for the rollout's X_t, SrcZH for the step).
+template <class S>
 hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
+  using DT = typename S::DT;
   using Cf = Cfgs<DT>;
   const int nbtot = a.Nc / 16;
-  if (a.M <= kRdRows && nbtot <= 9) {
+  if (a.M <= WM_RD_CTRL_ROWS && nbtot <= 9) {
     const int nb = nbtot <= 1 ? 1 : nbtot <= 2 ? 2 : nbtot <= 3 ? 3 : nbtot <= 5 ? 5 : 9;
     const int smax = nb <= 5 ? 8 : 4;  // register budget
     const int nw = rd_waves((int)a.ldk, Mfma<DT>::KSLICE, smax, 4);
     if (nw <= 8 && GemmRD<DT, 9, 1, 4, 512>::lds_bytes(nw) <= kRdLdsMax) {
       switch (nb) {
-        case 1: return launch_ctrl_rd<GemmRD<DT, 1, 1, 8, 512>, SH>(a, nw, s);
-        case 2: return launch_ctrl_rd<GemmRD<DT, 2, 1, 8, 512>, SH>(a, nw, s);
-        case 3: return launch_ctrl_rd<GemmRD<DT, 3, 1, 8, 512>, SH>(a, nw, s);
-        case 5: return launch_ctrl_rd<GemmRD<DT, 5, 1, 8, 512>, SH>(a, nw, s);
-        default: return launch_ctrl_rd<GemmRD<DT, 9, 1, 4, 512>, SH>(a, nw, s);
+        case 1: return launch_ctrl_rd<GemmRD<DT, 1, 1, 8, 512>, S>(a, nw, s);
+        case 2: return launch_ctrl_rd<GemmRD<DT, 2, 1, 8, 512>, S>(a, nw, s);
+        case 3: return launch_ctrl_rd<GemmRD<DT, 3, 1, 8, 512>, S>(a, nw, s);
+        case 5: return launch_ctrl_rd<GemmRD<DT, 5, 1, 8, 512>, S>(a, nw, s);
+        default: return launch_ctrl_rd<GemmRD<DT, 9, 1, 4, 512>, S>(a, nw, s);
       }
     }
   }
   const int nb = (nbtot + 3) / 4;  // output blocks per wave over four waves
-  if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLarge<1>, SH>(a, s);
-  if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlLarge<2>, SH>(a, s);
-  if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlLarge<3>, SH>(a, s);
-  if (nb <= 5) return launch_ctrl_cfg<typename Cf::template CtrlLarge<5>, SH>(a, s);
-  if (nb <= 8) return launch_ctrl_wide<DT, SH, 8, 2>(a, s);
-  if (nb <= 12) return launch_ctrl_wide<DT, SH, 12, 2>(a, s);
-  if (nb <= 17) return launch_ctrl_wide<DT, SH, 17, 1>(a, s);
-  if (nb <= 24) return launch_ctrl_wide<DT, SH, 24, 1>(a, s);
-  if (nb <= 33) return launch_ctrl_wide<DT, SH, 33, 1>(a, s);
+  if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLarge<1>, S>(a, s);
+  if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlLarge<2>, S>(a, s);
+  if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlLarge<3>, S>(a, s);
+  if (nb <= 5) return launch_ctrl_cfg<typename Cf::template CtrlLarge<5>, S>(a, s);
+  if (nb <= 8) return launch_ctrl_wide<S, 8, 2>(a, s);
+  if (nb <= 12) return launch_ctrl_wide<S, 12, 2>(a, s);
+  if (nb <= 17) return launch_ctrl_wide<S, 17, 1>(a, s);
+  if (nb <= 24) return launch_ctrl_wide<S, 24, 1>(a, s);
+  if (nb <= 33) return launch_ctrl_wide<S, 33, 1>(a, s);
   return hipErrorInvalidValue;
 }
 
@@ -1632,14 +1619,14 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   const Layout& L = P.L;
   const char* base = reinterpret_cast<const char*>(P.base);
   const int B = R.B, T = R.T, Z = L.Z, H = L.H;
-  DT* hb = reinterpret_cast<DT*>(R.hbuf);
-  const long BH = (long)B * H, BZ = (long)B * Z;
+  DT* X = reinterpret_cast<DT*>(R.x);
+  const long BX = (long)B * L.ldx, BH = (long)B * H, BZ = (long)B * Z;
   const bool trace = (R.flags & 2u) != 0;
   hipError_t e;
   {
     KTimer kt("init", s);
-    hipLaunchKernelGGL((k_rollout_init<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, R.z0,
-                       R.h0, R.c0, R.done_io, R.z_out, hb, R.c, R.done_state,
+    hipLaunchKernelGGL((k_rollout_init<DT>), dim3(elem_grid(BX)), dim3(256), 0, s, B, Z, H, L.ldx,
+                       R.z0, R.h0, R.c0, R.done_io, R.z_out, X, X + BX, R.c, R.done_state,
                        trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr);
     e = hipGetLastError();
   }
@@ -1650,7 +1637,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ca.bc = reinterpret_cast<const float*>(base + L.off_bc);
   ca.ldk = L.ldk;
   ca.Z = Z; ca.H = H; ca.A = L.A; ca.Nc = L.Nc; ca.M = B;
-  ca.ldz = Z;
+  ca.ldx = L.ldx;
   ca.mask = R.mask;
   ca.k0 = R.k0; ca.k1 = R.k1; ca.traj0 = R.traj0;
   ca.done_state = R.done_state;
@@ -1661,8 +1648,8 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ga.WaT = base + L.off_WaT;
   ga.bg = reinterpret_cast<const float*>(base + L.off_bg);
   ga.ldk = L.ldk;
+  ga.ldx = L.ldx;
   ga.H = H; ga.A = L.A; ga.Z = Z; ga.M = B;
-  ga.ldz = Z;
   ga.nll_mode = 0;
   ga.c = R.c;
 
@@ -1670,6 +1657,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ma.Wm = base + L.off_Wm;
   ma.bm = reinterpret_cast<const float*>(base + L.off_bm);
   ma.ldh = L.ldh;
+  ma.ldx = L.ldx;
   ma.H = H; ma.Z = Z; ma.K = L.K; ma.Nm = L.Nm; ma.M = B;
   ma.k0 = R.k0; ma.k1 = R.k1; ma.traj0 = R.traj0; ma.tau = R.tau;
   ma.nll_mode = 0;
@@ -1677,9 +1665,9 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
 
   for (int t = 0; t <= T; ++t) {
     const uint32_t step = R.step0 + (uint32_t)t;
-    const DT* hcur = hb + (long)(t & 1) * BH;
-    ca.z = R.z_out + (long)t * BZ;
-    ca.h = hcur;
+    DT* Xt = X + (long)(t & 1) * BX;
+    DT* Xn = X + (long)((t + 1) & 1) * BX;
+    ca.x = Xt;
     ca.step = step;
     ca.mode = t < T ? 1 : 2;
     ca.act_t = t < T ? R.actions + (long)t * B : nullptr;
@@ -1688,21 +1676,19 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
     ca.act_prev = t > 0 ? R.actions + (long)(t - 1) * B : nullptr;
     ca.rew_prev = t > 0 ? R.rewards + (long)(t - 1) * B : nullptr;
     ca.done_prev = t > 0 ? R.dones + (long)(t - 1) * B : nullptr;
-    e = launch_ctrl<DT, DT>(ca, s);
+    e = launch_ctrl<SrcX<DT>>(ca, s);
     if (e != hipSuccess) return e;
     if (t == T) break;
 
-    DT* hnext = hb + (long)((t + 1) & 1) * BH;
-    ga.xz = R.z_out + (long)t * BZ;
-    ga.h_in = hcur;
-    ga.h_out = hnext;
+    ga.x_in = Xt;
+    ga.x_out = Xn;
     ga.act = R.actions + (long)t * B;
     ga.h_trace = trace ? R.h_trace + (long)(t + 1) * BH : nullptr;
     ga.c_trace = trace ? R.c_trace + (long)(t + 1) * BH : nullptr;
     e = launch_gates<DT>(ga, s);
     if (e != hipSuccess) return e;
 
-    ma.h = hnext;
+    ma.x = Xn;
     ma.act = R.actions + (long)t * B;
     ma.z_prev = R.z_out + (long)t * BZ;
     ma.z_next = R.z_out + (long)(t + 1) * BZ;
@@ -1711,8 +1697,8 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
   KTimer kt("finish", s);
-  hipLaunchKernelGGL((k_rollout_finish<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, H,
-                     hb + (long)(T & 1) * BH, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
+  hipLaunchKernelGGL((k_rollout_finish<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, L.ldx,
+                     X + (long)(T & 1) * BX, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
   return hipGetLastError();
 }
 
@@ -1721,12 +1707,13 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   const Layout& L = P.L;
   const char* base = reinterpret_cast<const char*>(P.base);
   const int B = N.B, T = N.T, Z = L.Z, H = L.H;
-  const long BH = (long)B * H, BZ = (long)B * Z, M = (long)T * B;
-  DT* tr = reinterpret_cast<DT*>(N.trace);
+  const long BX = (long)B * L.ldx, BZ = (long)B * Z, M = (long)T * B;
+  DT* X = reinterpret_cast<DT*>(N.x);
   hipError_t e;
   {
     KTimer kt("nll_init", s);
-    hipLaunchKernelGGL((k_nll_init<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, BH, tr, N.c);
+    hipLaunchKernelGGL((k_nll_init<DT>), dim3(elem_grid((long)(T + 1) * B * (L.ldx - H))), dim3(256),
+                       0, s, T, B, Z, H, L.ldx, N.z, X, N.c);
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;
@@ -1736,14 +1723,13 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   ga.WaT = base + L.off_WaT;
   ga.bg = reinterpret_cast<const float*>(base + L.off_bg);
   ga.ldk = L.ldk;
+  ga.ldx = L.ldx;
   ga.H = H; ga.A = L.A; ga.Z = Z; ga.M = B;
-  ga.ldz = Z;
   ga.nll_mode = 1;
   ga.c = N.c;
   for (int t = 0; t < T; ++t) {
-    ga.xz = N.z + (long)t * BZ;
-    ga.h_in = tr + (long)t * BH;
-    ga.h_out = tr + (long)(t + 1) * BH;
+    ga.x_in = X + (long)t * BX;
+    ga.x_out = X + (long)(t + 1) * BX;
     ga.act = N.actions + (long)t * B;
     e = launch_gates<DT>(ga, s);
     if (e != hipSuccess) return e;
@@ -1754,8 +1740,9 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   ma.Wm = base + L.off_Wm;
   ma.bm = reinterpret_cast<const float*>(base + L.off_bm);
   ma.ldh = L.ldh;
+  ma.ldx = L.ldx;
   ma.H = H; ma.Z = Z; ma.K = L.K; ma.Nm = L.Nm; ma.M = (int)M;
-  ma.h = tr + BH;
+  ma.x = X + BX;  // rows of X_1 .. X_T
   ma.z_tgt = N.z + BZ;
   ma.part = N.part;
   ma.head = N.head;
@@ -1782,28 +1769,42 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
 
 }  // namespace
 
-#ifdef WM_PHASE_TIMING
-extern "C" int wm_debug_phase_copy(void* host, size_t bytes) {
-  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(wm_phase_t), bytes, 0, hipMemcpyDeviceToHost);
-}
-#endif
-
-size_t rollout_workspace_bytes(const Layout& L, int B) {
+size_t rollout_workspace(const Layout& L, int B, char* ws, RolloutBufs* R) {
   size_t o = 0;
-  o = wm_align256(o + (size_t)2 * B * L.H * L.esz);  // h ping-pong
-  o = wm_align256(o + (size_t)B * L.H * 4);          // c
-  o = wm_align256(o + (size_t)B * 4);                // done state
+  const size_t ox = o;
+  o = wm_align256(o + (size_t)2 * B * L.ldx * L.esz);  // X_t, X_t+1
+  const size_t oc = o;
+  o = wm_align256(o + (size_t)B * L.H * 4);  // c
+  const size_t od = o;
+  o = wm_align256(o + (size_t)B * 4);  // done state
+  if (ws && R) {
+    R->x = ws + ox;
+    R->c = reinterpret_cast<float*>(ws + oc);
+    R->done_state = reinterpret_cast<int32_t*>(ws + od);
+  }
   return o;
 }
 
-size_t nll_workspace_bytes(const Layout& L, int B, int T) {
+size_t nll_workspace(const Layout& L, int B, int T, char* ws, NllBufs* N) {
   const size_t M = (size_t)T * B;
   size_t o = 0;
-  o = wm_align256(o + (size_t)(T + 1) * B * L.H * L.esz);  // h trace
-  o = wm_align256(o + (size_t)B * L.H * 4);                // c
-  o = wm_align256(o + M * (L.Z / 8) * 4);                  // dim-tile partials
-  o = wm_align256(o + M * 2 * 4);                          // reward / done logits
-  o = wm_align256(o + ((M + 255) / 256) * 4 * 4);          // block sums
+  const size_t ox = o;
+  o = wm_align256(o + (size_t)(T + 1) * B * L.ldx * L.esz);  // X_0 .. X_T
+  const size_t oc = o;
+  o = wm_align256(o + (size_t)B * L.H * 4);  // c
+  const size_t op = o;
+  o = wm_align256(o + M * (L.Z / 8) * 4);  // dim-tile partials
+  const size_t oh = o;
+  o = wm_align256(o + M * 2 * 4);  // reward / done logits
+  const size_t og = o;
+  o = wm_align256(o + ((M + 255) / 256) * 4 * 4);  // block sums
+  if (ws && N) {
+    N->x = ws + ox;
+    N->c = reinterpret_cast<float*>(ws + oc);
+    N->part = reinterpret_cast<float*>(ws + op);
+    N->head = reinterpret_cast<float*>(ws + oh);
+    N->wgsum = reinterpret_cast<float*>(ws + og);
+  }
   return o;
 }
 
@@ -1832,15 +1833,15 @@ hipError_t launch_controller_step(const Packed& P, int B, uint32_t traj0, const 
   ca.bc = reinterpret_cast<const float*>(base + L.off_bc);
   ca.ldk = L.ldk;
   ca.Z = L.Z; ca.H = L.H; ca.A = L.A; ca.Nc = L.Nc; ca.M = B;
-  ca.z = z; ca.ldz = L.Z;
+  ca.z = z;
   ca.h = h;
   ca.mask = mask;
   ca.k0 = k0; ca.k1 = k1; ca.step = step; ca.traj0 = traj0;
   ca.mode = 0;
   ca.probs = probs;
   ca.action = action;
-  if (L.dt == 0) return launch_ctrl<float, float>(ca, s);
-  return launch_ctrl<bf16_t, float>(ca, s);
+  if (L.dt == 0) return launch_ctrl<SrcZH<float>>(ca, s);
+  return launch_ctrl<SrcZH<bf16_t>>(ca, s);
 }
 
 hipError_t launch_rollout(const Packed& P, const RolloutBufs& R, hipStream_t s) {

@@ -20,6 +20,11 @@
 //   Wc  [Nc, ldk]  controller rows 0..A-1 (columns z | h), row A = [0 | w_r],
 //                  row A+1 = [0 | w_d], zero rows up to Nc = roundup(A+2, 16).
 //   bc  [Nc]       fp32: b_c, b_r, b_d, zeros.
+//
+// Activations live in one matrix per step, X [rows, ldx] in the same element
+// type: columns 0..Z-1 hold q(z), Z..Z+H-1 hold h, the rest zero, so that the
+// gate and controller GEMMs read X from column 0 (K = ldk <= ldx) and the
+// mixture head reads it from column Z (K = ldh <= ldx - Z).
 #pragma once
 
 #include <stddef.h>
@@ -33,6 +38,7 @@ struct Layout {
   int Kx;              // Z + H
   int ldk;             // roundup(Kx, 64)
   int ldh;             // roundup(H, 64)
+  int ldx;             // roundup(Z + ldh, 64): row stride of the activation matrix
   int Q;               // ceil(3K / 4)
   int Nm;              // 16 Q (Z / 4) + 16
   int Nc;              // roundup(A + 2, 16)
@@ -49,6 +55,7 @@ static inline Layout make_layout(int Z, int H, int A, int K, int dt) {
   L.Kx = Z + H;
   L.ldk = wm_roundup(L.Kx, 64);
   L.ldh = wm_roundup(H, 64);
+  L.ldx = wm_roundup(Z + L.ldh, 64);
   L.Q = (3 * K + 3) / 4;
   L.Nm = 16 * L.Q * (Z / 4) + 16;
   L.Nc = wm_roundup(A + 2, 16);

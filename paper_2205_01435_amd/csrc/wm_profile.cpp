@@ -46,14 +46,22 @@ KTimer::KTimer(const char* name, hipStream_t s) : name_(name), s_(s) {
   if (!g_on || std::strncmp(name, g_prefix.c_str(), g_prefix.size()) != 0) return;
   a_ = take_event();
   b_ = take_event();
-  if (a_ && b_) hipEventRecord(a_, s_);
+  if (a_ && b_ && hipEventRecord(a_, s_) == hipSuccess) return;
+  if (a_) g_pool.push_back(a_);
+  if (b_) g_pool.push_back(b_);
+  a_ = b_ = nullptr;
 }
 
 KTimer::~KTimer() {
   if (!a_ || !b_) return;
-  hipEventRecord(b_, s_);
+  const bool ok = hipEventRecord(b_, s_) == hipSuccess;
   std::lock_guard<std::mutex> lk(g_mu);
-  g_recs.push_back(Rec{name_, a_, b_});
+  if (ok) {
+    g_recs.push_back(Rec{name_, a_, b_});
+  } else {
+    g_pool.push_back(a_);
+    g_pool.push_back(b_);
+  }
 }
 
 }  // namespace wm
@@ -88,7 +96,7 @@ wm_status wm_profile_read(const char* prefix, double* total_ms, int64_t* launche
 wm_status wm_profile_reset(void) {
   std::lock_guard<std::mutex> lk(wm::g_mu);
   for (const wm::Rec& r : wm::g_recs) {
-    hipEventSynchronize(r.b);
+    (void)hipEventSynchronize(r.b);
     wm::g_pool.push_back(r.a);
     wm::g_pool.push_back(r.b);
   }
