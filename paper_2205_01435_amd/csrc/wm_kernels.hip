@@ -262,26 +262,25 @@ struct Gemm {
 };
 
 // Work-group -> tile mapping.  Work-groups are dispatched round-robin over
-// the eight XCDs (each with its own L2); when there are at least eight
-// weight-row tiles, each XCD gets the work-groups of a fixed subset of them
-// (tile n on XCD n % 8), so every XCD streams only its slice of the weights
-// and keeps it in its L2 across calls.  Returns false for padding groups.
-__device__ __forceinline__ bool tile_of(int nt_count, int mt_count, int& nt, int& mt) {
-  const int L = blockIdx.x;
-  if (nt_count >= 8) {
-    const int xcd = L & 7, r = L >> 3;
-    nt = xcd + 8 * (r / mt_count);
-    mt = r % mt_count;
-    return nt < nt_count;
-  }
-  nt = L / mt_count;
-  mt = L % mt_count;
-  return nt < nt_count;
-}
+// the eight XCDs, each with its own L2.  The XCDs form a gn x (8 / gn) grid
+// over (weight-row tiles, activation-row tiles): XCD x owns a contiguous
+// range of nper weight tiles, so that its slice of the weights stays in its
+// L2 across calls, and a range of mper activation tiles, which it walks
+// with the weight tile fastest, so that an activation tile it has fetched
+// is reused by all of its weight tiles while still in L2.  The host picks
+// gn (tile_map below).  Returns false for padding work-groups.
+struct TileMap {
+  int nt, mt;      // weight-row tiles, activation-row tiles
+  int gn;          // XCD groups along the weight tiles (1, 2, 4 or 8)
+  int nper, mper;  // tiles of each kind per XCD
+};
 
-static inline unsigned grid_of(int nt_count, int mt_count) {
-  if (nt_count >= 8) return (unsigned)(8 * ((nt_count + 7) / 8) * mt_count);
-  return (unsigned)(nt_count * mt_count);
+__device__ __forceinline__ bool tile_of(const TileMap& t, int& n, int& m) {
+  const int x = blockIdx.x & 7, r = blockIdx.x >> 3;
+  const int nl = r % t.nper, ml = r / t.nper;
+  n = (x % t.gn) * t.nper + nl;
+  m = (x / t.gn) * t.mper + ml;
+  return n < t.nt && m < t.mt;
 }
 
 // ===========================================================================
@@ -302,6 +301,7 @@ struct GatesArgs {
   float* h_trace;  // [M, H] fp32 or null
   float* c_trace;
   int nll_mode;
+  TileMap map;
 };
 
 // LSTM cell and state commit of hidden unit u of row m.  gates_pre loads
@@ -365,7 +365,7 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
   constexpr int NBW = C::NBW, MBW = C::MBW;
   __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
   int nt, mt;
-  if (!tile_of((4 * p.H + C::BN - 1) / C::BN, (p.M + C::BM - 1) / C::BM, nt, mt)) return;
+  if (!tile_of(p.map, nt, mt)) return;
   const int n0 = nt * C::BN, m0 = mt * C::BM;
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wg), p.ldk, p.ldk, n0, C::BN, 4 * p.H);
   const SrcX<DT> x(reinterpret_cast<const DT*>(p.x_in), p.ldx, p.ldx, m0, C::BM, p.M);
@@ -414,8 +414,8 @@ struct MdnArgs {
   float* part;         // [M, ntd]
   float* head;         // [M, 2]
   int ntd;
-  int ntiles;          // weight-row tiles in the grid
   int nll_mode;
+  TileMap map;
 };
 
 // z_{t+1,j} of row m: Gumbel-max component pick on pi-logit / tau (stream 1,
@@ -537,7 +537,7 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
   __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
   __shared__ float red[WAVES_M][MBW * 16];
   int ntile, mt;
-  if (!tile_of(p.ntiles, (p.M + C::BM - 1) / C::BM, ntile, mt)) return;
+  if (!tile_of(p.map, ntile, mt)) return;
   const int n0 = ntile * C::BN, m0 = mt * C::BM;
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wm), p.ldh, p.ldh, n0, C::BN, p.Nm);
   const SrcX<DT> x(reinterpret_cast<const DT*>(p.x) + p.Z, p.ldx, p.ldx - p.Z, m0, C::BM, p.M);
@@ -1147,7 +1147,7 @@ __global__ void __launch_bounds__(R::MAXT) k_gates_rd(const GatesArgs p) {
   using DT = typename R::DT;
   extern __shared__ __attribute__((aligned(16))) float lds_dyn[];
   int nt, mt;
-  if (!tile_of((4 * p.H + R::BN - 1) / R::BN, (p.M + R::BM - 1) / R::BM, nt, mt)) return;
+  if (!tile_of(p.map, nt, mt)) return;
   const int n0 = nt * R::BN, m0 = mt * R::BM;
   constexpr int UPT = R::BN / 4;  // hidden units per tile
   static_assert(UPT * R::BM <= 256, "one epilogue element per thread of the first four waves");
@@ -1175,7 +1175,7 @@ __global__ void __launch_bounds__(R::MAXT) k_mdn_rd(const MdnArgs p) {
   constexpr int Q = R::NBW;
   extern __shared__ __attribute__((aligned(16))) float lds_dyn[];
   int J, mt;
-  if (!tile_of(p.ntiles, (p.M + R::BM - 1) / R::BM, J, mt)) return;
+  if (!tile_of(p.map, J, mt)) return;
   const int n0 = J * R::BN, m0 = mt * R::BM;
   const int t = threadIdx.x;
   const int d = t & 3, ml = t >> 2;
@@ -1480,37 +1480,67 @@ hipError_t allow_lds(F* kernel, size_t bytes) {
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
-template <class C>
-hipError_t launch_gates_cfg(const GatesArgs& a, hipStream_t s) {
-  const int nt = (4 * a.H + C::BN - 1) / C::BN, mt = (a.M + C::BM - 1) / C::BM;
+// Weight bytes an XCD should keep in its L2 (4 MB) while activations stream.
+#ifndef WM_L2_BUDGET
+#define WM_L2_BUDGET (2560 * 1024)
+#endif
+constexpr size_t kL2Budget = WM_L2_BUDGET;
+
+// Picks gn for nt x mt tiles over `wbytes` of weights: the weights' per-XCD
+// slice fits the L2 budget if possible, then the busiest XCD gets the fewest
+// tiles, then the activations are re-read by the fewest XCD groups.
+TileMap tile_map(int nt, int mt, size_t wbytes) {
+  TileMap best{};
+  bool best_fits = false;
+  long best_tiles = 0;
+  for (int gn = 1; gn <= 8; gn *= 2) {
+    if (gn > 1 && gn > nt) break;
+    TileMap t{nt, mt, gn, (nt + gn - 1) / gn, (mt + 8 / gn - 1) / (8 / gn)};
+    const bool fits = wbytes / gn <= kL2Budget;
+    const long tiles = (long)t.nper * t.mper;
+    if (gn == 1 || (fits && !best_fits) || (fits == best_fits && tiles < best_tiles)) {
+      best = t;
+      best_fits = fits;
+      best_tiles = tiles;
+    }
+  }
+  return best;
+}
+
+unsigned grid_of(const TileMap& t) { return (unsigned)(8 * t.nper * t.mper); }
+
+template <class C, typename DT>
+hipError_t launch_gates_cfg(GatesArgs a, hipStream_t s) {
+  a.map = tile_map((4 * a.H + C::BN - 1) / C::BN, (a.M + C::BM - 1) / C::BM,
+                   (size_t)4 * a.H * a.ldk * sizeof(DT));
   KTimer kt("gates", s);
-  hipLaunchKernelGGL((k_gates<C>), dim3(grid_of(nt, mt)), dim3(C::NT), 0, s, a);
+  hipLaunchKernelGGL((k_gates<C>), dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
 template <typename DT>
-hipError_t launch_gates(const GatesArgs& a, hipStream_t s) {
+hipError_t launch_gates(GatesArgs a, hipStream_t s) {
   using R = GemmRD<DT, 2, 2, 8, 512>;
   const int nw = rd_waves((int)a.ldk, R::KSLICE, R::SMAX, 4);
   const size_t lds = R::lds_bytes(nw);
   if (a.M <= WM_RD_GATES_ROWS && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
     hipError_t e = allow_lds(k_gates_rd<R>, lds);
     if (e != hipSuccess) return e;
-    const int nt = (4 * a.H + R::BN - 1) / R::BN, mt = (a.M + R::BM - 1) / R::BM;
+    a.map = tile_map((4 * a.H + R::BN - 1) / R::BN, (a.M + R::BM - 1) / R::BM,
+                     (size_t)4 * a.H * a.ldk * sizeof(DT));
     KTimer kt("gates", s);
-    hipLaunchKernelGGL((k_gates_rd<R>), dim3(grid_of(nt, mt)), dim3(64 * nw), lds, s, a);
+    hipLaunchKernelGGL((k_gates_rd<R>), dim3(grid_of(a.map)), dim3(64 * nw), lds, s, a);
     return hipGetLastError();
   }
-  if (a.M <= kSmallRows) return launch_gates_cfg<typename Cfgs<DT>::GatesSmall>(a, s);
-  return launch_gates_cfg<typename Cfgs<DT>::GatesLarge>(a, s);
+  if (a.M <= kSmallRows) return launch_gates_cfg<typename Cfgs<DT>::GatesSmall, DT>(a, s);
+  return launch_gates_cfg<typename Cfgs<DT>::GatesLarge, DT>(a, s);
 }
 
-template <class C>
+template <class C, typename DT>
 hipError_t launch_mdn_cfg(MdnArgs a, int ntiles, hipStream_t s) {
-  a.ntiles = ntiles;
-  const int mt = (a.M + C::BM - 1) / C::BM;
+  a.map = tile_map(ntiles, (a.M + C::BM - 1) / C::BM, (size_t)a.Nm * a.ldh * sizeof(DT));
   KTimer kt("mdn", s);
-  hipLaunchKernelGGL((k_mdn<C>), dim3(grid_of(ntiles, mt)), dim3(C::NT), 0, s, a);
+  hipLaunchKernelGGL((k_mdn<C>), dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1524,15 +1554,15 @@ hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
       hipError_t e = allow_lds(k_mdn_rd<R>, lds);
       if (e != hipSuccess) return e;
       MdnArgs b = a;
-      b.ntiles = a.Z / 4;  // one dim group per tile
-      const int mt = (a.M + R::BM - 1) / R::BM;
+      // one dim group per tile
+      b.map = tile_map(a.Z / 4, (a.M + R::BM - 1) / R::BM, (size_t)a.Nm * a.ldh * sizeof(DT));
       KTimer kt("mdn", s);
-      hipLaunchKernelGGL((k_mdn_rd<R>), dim3(grid_of(b.ntiles, mt)), dim3(64 * nw), lds, s, b);
+      hipLaunchKernelGGL((k_mdn_rd<R>), dim3(grid_of(b.map)), dim3(64 * nw), lds, s, b);
       return hipGetLastError();
     }
   }
-  if (a.M <= kSmallRows) return launch_mdn_cfg<typename Cfgs<DT>::template MdnSmall<Q>>(a, ntiles, s);
-  return launch_mdn_cfg<typename Cfgs<DT>::template MdnLarge<Q>>(a, ntiles, s);
+  if (a.M <= kSmallRows) return launch_mdn_cfg<typename Cfgs<DT>::template MdnSmall<Q>, DT>(a, ntiles, s);
+  return launch_mdn_cfg<typename Cfgs<DT>::template MdnLarge<Q>, DT>(a, ntiles, s);
 }
 
 template <typename DT>
