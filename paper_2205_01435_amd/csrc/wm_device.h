@@ -96,6 +96,22 @@ __device__ __forceinline__ uint32_t word_of(uint4 w, int i) {
 __device__ __forceinline__ float gumbel(float u) { return -logf(-logf(u)); }
 __device__ __forceinline__ float sigmoidf(float x) { return 1.0f / (1.0f + expf(-x)); }
 
+// Fast LSTM nonlinearities on the hardware base-2 exponential and reciprocal
+// (v_exp_f32, v_rcp_f32, about 1 ulp each): relative error below 1e-6 for
+// |x| <= 20.  tanh switches to its odd Taylor polynomial for |x| < 1/8,
+// where 1 - exp(-2|x|) would cancel (truncation error below 2e-9).
+__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
+__device__ __forceinline__ float frcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ float fsigmoid(float x) { return frcp(1.0f + fexp(-x)); }
+__device__ __forceinline__ float ftanh(float x) {
+  const float ax = fabsf(x);
+  const float t = fexp(-2.0f * ax);
+  const float big = (1.0f - t) * frcp(1.0f + t);
+  const float x2 = x * x;
+  const float small = ax * (1.0f + x2 * (-1.0f / 3.0f + x2 * (2.0f / 15.0f + x2 * (-17.0f / 315.0f))));
+  return copysignf(ax < 0.125f ? small : big, x);
+}
+
 enum : uint32_t { STREAM_CONTROLLER = 0, STREAM_COMPONENT = 1, STREAM_GAUSS = 2, STREAM_DONE = 3 };
 
 // ---------------------------------------------------------------------------
@@ -133,6 +149,22 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
 }
 __device__ __forceinline__ uint4 bload16(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ uint2 bload8(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ uint32_t bload4(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ uint32_t bload2(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+}
+// Stores at an offset at or beyond the resource's size are dropped.
+__device__ __forceinline__ void bstore4(rsrc_t r, uint32_t off, uint32_t v) {
+  __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore2(rsrc_t r, uint32_t off, uint32_t v) {
+  __builtin_amdgcn_raw_buffer_store_b16((unsigned short)v, r, (int)off, 0, 0);
 }
 __device__ __forceinline__ uint4 operator|(uint4 a, uint4 b) {
   return make_uint4(a.x | b.x, a.y | b.y, a.z | b.z, a.w | b.w);

@@ -304,60 +304,87 @@ struct GatesArgs {
   TileMap map;
 };
 
-// LSTM cell and state commit of hidden unit u of row m.  gates_pre loads
-// everything that does not depend on the GEMM (action, bias plus gathered
-// one-hot column, cell state), so that callers can issue it early;
-// gates_fin adds the GEMM part (W [q(z) | h]) of the four gate
-// pre-activations i, f, g, o and commits.  A frozen rollout row copies its
-// state.
-struct GatePre {
-  long e;        // m * H + u (cell state, traces)
-  long xe;       // m * ldx + Z + u (h in X)
+// Element-wise side of the gate kernels for rows m0 .. m0+rows-1 of a tile.
+// Every access goes through a range-checked buffer resource and elements
+// that must not be touched get the offset kOffNone, so that the loads are
+// straight-line code issued together, before any of their values is used.
+// load() fetches what the cell needs besides the GEMM (bias plus the
+// gathered one-hot column, cell state, and for a frozen row its h);
+// commit() runs the LSTM cell on the four gate pre-activations i, f, g, o
+// and stores h_t+1 into X_t+1 and c (a frozen rollout row keeps its state).
+struct GateIn {
+  float4 add;  // bias + one-hot column, per gate
+  float c;     // cell state c_t
+  float hprev; // h_t (frozen rows only)
   bool live;
-  float4 add;    // bias + one-hot column, per gate
-  float c;       // cell state c_t
 };
 
 template <typename DT>
-__device__ __forceinline__ GatePre gates_pre(const GatesArgs& p, int m, int u) {
-  GatePre q;
-  const int H = p.H;
-  const int a = p.act[m];
-  q.live = p.nll_mode || a >= 0;
-  q.e = (long)m * H + u;
-  q.xe = (long)m * p.ldx + p.Z + u;
-  q.add = *reinterpret_cast<const float4*>(p.bg + 4 * u);
-  if (a >= 0 && a < p.A) {
-    const DT* WaT = reinterpret_cast<const DT*>(p.WaT);
-    const long o = (long)a * 4 * H + 4 * u;
-    q.add.x += DType<DT>::load(WaT, o);
-    q.add.y += DType<DT>::load(WaT, o + 1);
-    q.add.z += DType<DT>::load(WaT, o + 2);
-    q.add.w += DType<DT>::load(WaT, o + 3);
-  }
-  q.c = p.c[q.e];
-  return q;
-}
+struct GateIO {
+  rsrc_t rc, rxi, rxo, rw, rb, rht, rct;
+  int H, A;
+  uint32_t ldxb;  // X row stride in bytes
+  bool nll;
 
-template <typename DT>
-__device__ __forceinline__ void gates_fin(const GatesArgs& p, const GatePre& q, float pi, float pf,
-                                          float pg, float po) {
-  DT* x_out = reinterpret_cast<DT*>(p.x_out);
-  float hv, cv;
-  if (!q.live) {
-    hv = DType<DT>::load(reinterpret_cast<const DT*>(p.x_in), q.xe);
-    cv = q.c;
-  } else {
-    cv = sigmoidf(pf + q.add.y) * q.c + sigmoidf(pi + q.add.x) * tanhf(pg + q.add.z);
-    hv = DType<DT>::round(sigmoidf(po + q.add.w) * tanhf(cv));
-    p.c[q.e] = cv;
+  __device__ GateIO(const GatesArgs& p, int m0, int rows) {
+    H = p.H;
+    A = p.A;
+    nll = p.nll_mode != 0;
+    const long mval = max(0, min(rows, p.M - m0));
+    const uint32_t hb = (uint32_t)(mval * H * 4);
+    ldxb = (uint32_t)(p.ldx * (long)sizeof(DT));
+    const uint32_t xb = mval ? (uint32_t)(((mval - 1) * p.ldx + H) * (long)sizeof(DT)) : 0u;
+    rc = make_rsrc(p.c + (long)m0 * H, hb);
+    rxi = make_rsrc(reinterpret_cast<const DT*>(p.x_in) + (long)m0 * p.ldx + p.Z, xb);
+    rxo = make_rsrc(reinterpret_cast<DT*>(p.x_out) + (long)m0 * p.ldx + p.Z, xb);
+    rw = make_rsrc(p.WaT, (uint32_t)((long)A * 4 * H * (long)sizeof(DT)));
+    rb = make_rsrc(p.bg, (uint32_t)(16 * H));
+    rht = make_rsrc(p.h_trace ? p.h_trace + (long)m0 * H : nullptr, p.h_trace ? hb : 0u);
+    rct = make_rsrc(p.c_trace ? p.c_trace + (long)m0 * H : nullptr, p.c_trace ? hb : 0u);
   }
-  DType<DT>::store(x_out, q.xe, hv);
-  if (p.h_trace) {
-    p.h_trace[q.e] = hv;
-    p.c_trace[q.e] = cv;
+
+  // tile row ml, hidden unit u, action a of the row; ok: inside the call
+  __device__ __forceinline__ GateIn load(int ml, int u, int a, bool ok) const {
+    GateIn in;
+    in.live = nll || a >= 0;
+    const uint32_t ec = ((uint32_t)ml * H + u) * 4u;
+    const uint4 b = bload16(rb, ok ? (uint32_t)u * 16u : kOffNone);
+    const bool gather = ok && a >= 0 && a < A;
+    const uint32_t ew = ((uint32_t)a * 4u * H + 4u * u) * (uint32_t)sizeof(DT);
+    float4 w;
+    if constexpr (sizeof(DT) == 4) {
+      const uint4 v = bload16(rw, gather ? ew : kOffNone);
+      w = make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
+    } else {
+      const uint2 v = bload8(rw, gather ? ew : kOffNone);
+      w = make_float4(bf16_bits_to_f32(v.x & 0xffffu), bf16_bits_to_f32(v.x >> 16),
+                      bf16_bits_to_f32(v.y & 0xffffu), bf16_bits_to_f32(v.y >> 16));
+    }
+    in.add = make_float4(__uint_as_float(b.x) + w.x, __uint_as_float(b.y) + w.y,
+                         __uint_as_float(b.z) + w.z, __uint_as_float(b.w) + w.w);
+    in.c = __uint_as_float(bload4(rc, ok ? ec : kOffNone));
+    const uint32_t ex = (uint32_t)ml * ldxb + (uint32_t)u * (uint32_t)sizeof(DT);
+    const uint32_t ox = ok && !in.live ? ex : kOffNone;
+    if constexpr (sizeof(DT) == 4) in.hprev = __uint_as_float(bload4(rxi, ox));
+    else in.hprev = bf16_bits_to_f32(bload2(rxi, ox));
+    return in;
   }
-}
+
+  __device__ __forceinline__ void commit(int ml, int u, bool ok, const GateIn& in, float pi, float pf,
+                                         float pg, float po) const {
+    const float cn = fsigmoid(pf + in.add.y) * in.c + fsigmoid(pi + in.add.x) * ftanh(pg + in.add.z);
+    const float hn = DType<DT>::round(fsigmoid(po + in.add.w) * ftanh(cn));
+    const float cv = in.live ? cn : in.c;
+    const float hv = in.live ? hn : in.hprev;
+    const uint32_t ec = ((uint32_t)ml * H + u) * 4u;
+    const uint32_t ex = (uint32_t)ml * ldxb + (uint32_t)u * (uint32_t)sizeof(DT);
+    bstore4(rc, ok && in.live ? ec : kOffNone, __float_as_uint(cv));
+    if constexpr (sizeof(DT) == 4) bstore4(rxo, ok ? ex : kOffNone, __float_as_uint(hv));
+    else bstore2(rxo, ok ? ex : kOffNone, f32_to_bf16_bits(hv));
+    bstore4(rht, ok ? ec : kOffNone, __float_as_uint(hv));  // dropped without traces
+    bstore4(rct, ok ? ec : kOffNone, __float_as_uint(cv));
+  }
+};
 
 template <class C>
 __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
@@ -367,23 +394,36 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
   int nt, mt;
   if (!tile_of(p.map, nt, mt)) return;
   const int n0 = nt * C::BN, m0 = mt * C::BM;
+  const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+  const int wn = C::wn(), wmi = C::wm();
+  // actions of this lane's rows, fetched ahead of the GEMM
+  int act[MBW];
+#pragma unroll
+  for (int j = 0; j < MBW; ++j) {
+    const int m = m0 + (wmi * MBW + j) * 16 + r16;
+    act[j] = m < p.M ? p.act[m] : -1;
+  }
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wg), p.ldk, p.ldk, n0, C::BN, 4 * p.H);
   const SrcX<DT> x(reinterpret_cast<const DT*>(p.x_in), p.ldx, p.ldx, m0, C::BM, p.M);
   f32x4 acc[NBW][MBW];
   C::run(acc, w, x, (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
   if (C::kw() != 0) return;
 
-  const int lane = threadIdx.x & 63;
-  const int wn = C::wn(), wmi = C::wm();
+  const GateIO<DT> io(p, m0, C::BM);
 #pragma unroll
   for (int j = 0; j < MBW; ++j) {
-    const int m = m0 + (wmi * MBW + j) * 16 + (lane & 15);
-    if (m >= p.M) continue;
+    const int ml = (wmi * MBW + j) * 16 + r16;
+    GateIn in[NBW];
 #pragma unroll
     for (int i = 0; i < NBW; ++i) {
-      const int u = (n0 + (wn * NBW + i) * 16) / 4 + (lane >> 4);
-      if (u < p.H)
-        gates_fin<DT>(p, gates_pre<DT>(p, m, u), acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      const int u = (n0 + (wn * NBW + i) * 16) / 4 + g;
+      in[i] = io.load(ml, u, act[j], m0 + ml < p.M && u < p.H);
+    }
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) {
+      const int u = (n0 + (wn * NBW + i) * 16) / 4 + g;
+      io.commit(ml, u, m0 + ml < p.M && u < p.H, in[i], acc[i][j][0], acc[i][j][1], acc[i][j][2],
+                acc[i][j][3]);
     }
   }
 }
@@ -1140,8 +1180,8 @@ struct GemmRD {
 };
 
 // Gates on the register-direct core: tiles of BN/4 hidden units x BM rows.
-// Each of the first threads owns one (unit, row) of the epilogue and loads
-// its inputs before the GEMM.
+// Each of the first threads owns one (unit, row) of the epilogue and issues
+// its loads before the GEMM.
 template <class R>
 __global__ void __launch_bounds__(R::MAXT) k_gates_rd(const GatesArgs p) {
   using DT = typename R::DT;
@@ -1154,15 +1194,17 @@ __global__ void __launch_bounds__(R::MAXT) k_gates_rd(const GatesArgs p) {
   const int t = threadIdx.x;
   const int ul = t % UPT, ml = t / UPT;
   const int m = m0 + ml, u = n0 / 4 + ul;
-  const bool mine = t < UPT * R::BM && m < p.M && u < p.H;
-  GatePre pre{};
-  if (mine) pre = gates_pre<DT>(p, m, u);
+  const bool mine = t < UPT * R::BM;
+  const bool ok = mine && m < p.M && u < p.H;
+  const GateIO<DT> io(p, m0, R::BM);
+  GateIn in{};
+  if (mine) in = io.load(ml, u, ok ? p.act[m] : -1, ok);
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wg), p.ldk, p.ldk, n0, R::BN, 4 * p.H);
   const SrcX<DT> x(reinterpret_cast<const DT*>(p.x_in), p.ldx, p.ldx, m0, R::BM, p.M);
   R::run(lds_dyn, w, x, (int)p.ldk);
   if (mine) {
     const float4 g4 = *reinterpret_cast<const float4*>(R::E(lds_dyn) + ml * R::ELD + 4 * ul);
-    gates_fin<DT>(p, pre, g4.x, g4.y, g4.z, g4.w);
+    io.commit(ml, u, ok, in, g4.x, g4.y, g4.z, g4.w);
   }
 }
 
