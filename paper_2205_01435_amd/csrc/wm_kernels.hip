@@ -133,7 +133,9 @@ struct Gemm {
   static constexpr int NT = 64 * NWAVES;
   static constexpr int BN = 16 * NBW * WAVES_N;
   static constexpr int BM = 16 * MBW * WAVES_M;
-  static constexpr int LDL = BK + VEC;  // padded LDS row (elements)
+  // LDS rows padded by 32 bytes: 16-byte fragment reads of 16 rows at a
+  // 160-byte stride run conflict-free on gfx950 (144 bytes: two-way conflicts)
+  static constexpr int LDL = BK + 2 * VEC;
   static constexpr int KV = BK / VEC;   // 16-byte vectors per row chunk
   static constexpr int WV = BN * KV;
   static constexpr int XV = BM * KV;
@@ -575,7 +577,10 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
   constexpr int Q = C::NBW, MBW = C::MBW, WAVES_N = C::WAVES_N, WAVES_M = C::WAVES_M;
   static_assert(WAVES_N == 2, "the NLL epilogue sums two dim groups per work-group");
   __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
-  __shared__ float red[WAVES_M][MBW * 16];
+  // NLL partial sums of the second dim group; reuses the GEMM's LDS, which
+  // is free once run() has returned
+  float(*red)[MBW * 16] = reinterpret_cast<float(*)[MBW * 16]>(lds_raw);
+  static_assert(WAVES_M * MBW * 16 * 4 <= C::LDS_BYTES, "partial sums fit the GEMM's LDS");
   int ntile, mt;
   if (!tile_of(p.map, ntile, mt)) return;
   const int n0 = ntile * C::BN, m0 = mt * C::BM;
@@ -737,7 +742,7 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
   using DT = typename S::DT;
   constexpr int VEC = DType<DT>::VEC;
   constexpr int BM = 16 * MBW;
-  constexpr int LDL = BKC + VEC;
+  constexpr int LDL = BKC + 2 * VEC;
   __shared__ __attribute__((aligned(16))) DT xl[BM * LDL];
   __shared__ float s_best[4][BM];
   __shared__ int s_idx[4][BM];
