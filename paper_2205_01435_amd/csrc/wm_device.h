@@ -203,12 +203,16 @@ struct SrcX {
   using Row = uint32_t;
   static constexpr bool kTwo = false;
   rsrc_t r;
-  uint32_t ldb;  // row stride in bytes
+  const DT* base;  // first row of the tile
+  uint32_t bytes;  // readable bytes from base
+  uint32_t ldb;    // row stride in bytes
   // rows m0 .. m0+rows-1 of x, clipped to M; `span` readable columns per row
   __device__ SrcX(const DT* x, long ld, long span, int m0, int rows, int M) {
     const long mval = max(0, min(rows, M - m0));
     ldb = (uint32_t)(ld * (long)sizeof(DT));
-    r = make_rsrc(x + (long)m0 * ld, mval ? (uint32_t)(((mval - 1) * ld + span) * (long)sizeof(DT)) : 0u);
+    base = x + (long)m0 * ld;
+    bytes = mval ? (uint32_t)(((mval - 1) * ld + span) * (long)sizeof(DT)) : 0u;
+    r = make_rsrc(base, bytes);
   }
   __device__ Row row(int i) const { return (uint32_t)i * ldb; }
   __device__ uint4 load(Row ro, int k, int Kpad) const {

@@ -263,6 +263,158 @@ struct Gemm {
   }
 };
 
+// ===========================================================================
+// GEMM core for large row counts: operands go from global memory straight
+// into LDS (buffer loads with the LDS-DMA modifier, no staging registers and
+// no LDS store instructions, which on gfx950 run at about a third of the
+// LDS read rate), through a ring of STAGES buffers so that the loads of
+// chunk k + STAGES - 1 fly while chunk k is multiplied.  A chunk is 128 bytes
+// of K per row (64 bf16 or 32 fp32 values, two MFMA K slices); rows are
+// stored unpadded with their 16-byte pieces permuted, piece c of row r at
+// slot c ^ ((r >> 1) & 7), which keeps the 16-row fragment reads free of
+// bank conflicts.  One LDS-DMA instruction fills 8 rows (1 KB): lane l
+// loads piece (l & 7) ^ ((row >> 1) & 7) of row 8q + (l >> 3).
+// Same interface as Gemm (without a K split); Kpad must be a multiple of
+// the chunk.
+// ===========================================================================
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource words for inline assembly (same fields as make_rsrc).
+__device__ __forceinline__ u32x4 rsrc_words(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  u32x4 r;
+  r.x = (uint32_t)a;
+  r.y = (uint32_t)(a >> 32) & 0xffffu;
+  r.z = bytes;
+  r.w = 0x00020000u;
+  return r;
+}
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// 16 bytes per lane from the buffer at byte offset voff into LDS at
+// lds + 16 * lane (lds is wave-uniform).  Out-of-range offsets load zeros.
+// Issued as inline assembly so that the compiler does not wait for these
+// loads before every LDS read; callers wait with vm_wait<N>() instead.
+__device__ __forceinline__ void dma16(u32x4 rs, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rs)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+template <typename DT_, int NBW_, int MBW_, int WAVES_N_, int WAVES_M_, int STAGES_>
+struct GemmD {
+  using DT = DT_;
+  static constexpr int NBW = NBW_, MBW = MBW_, WAVES_N = WAVES_N_, WAVES_M = WAVES_M_;
+  static constexpr int STAGES = STAGES_, KSPLIT = 1;
+  static constexpr int VEC = DType<DT>::VEC;
+  static constexpr int BK = 128 / (int)sizeof(DT);  // K per chunk
+  static constexpr int NWAVES = WAVES_N * WAVES_M;
+  static constexpr int NT = 64 * NWAVES;
+  static constexpr int BN = 16 * NBW * WAVES_N;
+  static constexpr int BM = 16 * MBW * WAVES_M;
+  static constexpr int ROWS = BN + BM;
+  static constexpr int STAGE_BYTES = ROWS * 128;
+  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
+  static constexpr int NQ = ROWS / 8;        // DMA instructions per chunk
+  static constexpr int QW = NQ / NWAVES;     // ... per wave
+  static_assert(NQ % NWAVES == 0 && BN % 8 == 0, "whole DMA instructions per wave");
+  static_assert(STAGES >= 2 && (STAGES - 2) * QW < 64, "vmcnt range");
+  static_assert(2 * Mfma<DT>::KSLICE == BK, "two MFMA K slices per chunk");
+
+  __device__ static int kw() { return 0; }
+  __device__ static int wn() { return (threadIdx.x >> 6) % WAVES_N; }
+  __device__ static int wm() { return (threadIdx.x >> 6) / WAVES_N; }
+
+  // this wave's chunks are in LDS once at most `young` later chunks are in flight
+  __device__ __forceinline__ static void wait_chunks(int young) {
+    if constexpr (STAGES >= 4) {
+      if (young >= 2) { vm_wait<2 * QW>(); return; }
+    }
+    if constexpr (STAGES >= 3) {
+      if (young >= 1) { vm_wait<QW>(); return; }
+    }
+    vm_wait<0>();
+  }
+
+  template <class S>
+  __device__ __forceinline__ static void run(f32x4 (&acc)[NBW][MBW], const SrcX<DT>& w, const S& x,
+                                             int Kpad, DT* lds) {
+    static_assert(!S::kTwo, "the direct core reads one activation matrix");
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = lane >> 4, r16 = lane & 15;
+    const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(
+        (__attribute__((address_space(3))) char*)reinterpret_cast<char*>(lds));
+#pragma unroll
+    for (int i = 0; i < NBW; ++i)
+#pragma unroll
+      for (int j = 0; j < MBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // per-lane source offsets of this wave's DMA instructions (chunk 0)
+    u32x4 rs[QW];
+    uint32_t off[QW];
+#pragma unroll
+    for (int t = 0; t < QW; ++t) {
+      const int q = wave * QW + t;  // uniform
+      const int row = 8 * q + (lane >> 3);
+      const int c = (lane & 7) ^ ((row >> 1) & 7);
+      if (q < BN / 8) {
+        rs[t] = rsrc_words(w.base, w.bytes);
+        off[t] = w.row(row) + 16u * c;
+      } else {
+        rs[t] = rsrc_words(x.base, x.bytes);
+        off[t] = x.row(row - BN) + 16u * c;
+      }
+    }
+    const int nk = Kpad / BK;
+    auto issue = [&](int kc) {
+      const uint32_t base = lds0 + (uint32_t)(kc % STAGES) * STAGE_BYTES + (uint32_t)wave * QW * 1024u;
+#pragma unroll
+      for (int t = 0; t < QW; ++t) dma16(rs[t], off[t] + 128u * (uint32_t)kc, base + 1024u * t);
+    };
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < nk) issue(s);
+
+    const int wni = wn(), wmi = wm();
+    const int sw = (r16 >> 1) & 7;
+    const uint32_t col0 = (uint32_t)((g ^ sw) << 4), col1 = (uint32_t)(((4 + g) ^ sw) << 4);
+    for (int kc = 0; kc < nk; ++kc) {
+      wait_chunks(min(STAGES - 2, nk - 1 - kc));
+      __builtin_amdgcn_s_barrier();  // no fence: it would wait for every load in flight
+      asm volatile("" : : : "memory");
+      if (kc + STAGES - 1 < nk) issue(kc + STAGES - 1);
+      const char* buf = reinterpret_cast<const char*>(lds) + (kc % STAGES) * STAGE_BYTES;
+#pragma unroll
+      for (int sl = 0; sl < 2; ++sl) {
+        const uint32_t col = sl ? col1 : col0;
+        uint4 a[NBW], b[MBW];
+#pragma unroll
+        for (int i = 0; i < NBW; ++i)
+          a[i] = *reinterpret_cast<const uint4*>(buf + ((wni * NBW + i) * 16 + r16) * 128 + col);
+#pragma unroll
+        for (int j = 0; j < MBW; ++j)
+          b[j] = *reinterpret_cast<const uint4*>(buf + (BN + (wmi * MBW + j) * 16 + r16) * 128 + col);
+#pragma unroll
+        for (int i = 0; i < NBW; ++i)
+#pragma unroll
+          for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], a[i], b[j]);
+      }
+    }
+    __syncthreads();  // LDS free for the caller's epilogue
+  }
+};
+
 // Work-group -> tile mapping.  Work-groups are dispatched round-robin over
 // the eight XCDs, each with its own L2.  The XCDs form a gn x (8 / gn) grid
 // over (weight-row tiles, activation-row tiles): XCD x owns a contiguous
@@ -1493,7 +1645,7 @@ template <> struct Cfgs<float> {
 };
 template <> struct Cfgs<bf16_t> {
   using GatesSmall = Gemm<bf16_t, 2, 1, 2, 2, 1, 64, 4>;
-  using GatesLarge = Gemm<bf16_t, 4, 4, 2, 2, 1, 64, 2>;  // 128 x 128
+  using GatesLarge = GemmD<bf16_t, 4, 4, 2, 2, 2>;  // 128 x 128
   template <int Q> using MdnSmall = Gemm<bf16_t, Q, 1, 2, 1, 2, 64, 4>;
   template <int Q> using MdnLarge = Gemm<bf16_t, Q, 2, 2, 2, 1, 64, 2>;
   template <int NB> using CtrlLarge = Gemm<bf16_t, NB, 4, 4, 1, 1, 64, 2>;
