@@ -540,45 +540,179 @@ struct GateIO {
   }
 };
 
+// Element-wise side of the pipelined gate kernels for four consecutive hidden
+// units u0 .. u0+3 of one tile row, so that cell state, h, traces and the
+// gathered one-hot columns move in 16-byte (8-byte for bf16 h) pieces.
+// Same masking scheme as GateIO: range-checked buffer accesses, kOffNone for
+// elements that must not be touched.
+struct Gate4In {
+  float4 add[4];  // bias + one-hot column of unit u0 + t, per gate
+  float4 c;       // cell states of the four units
+  float4 hprev;   // h_t of the four units (frozen rows only)
+  bool live;
+};
+
+template <typename DT>
+struct Gate4IO {
+  rsrc_t rc, rxi, rxo, rw, rb, rht, rct;
+  int H, A;
+  uint32_t ldxb;
+  bool nll;
+
+  __device__ Gate4IO(const GatesArgs& p, int m0, int rows) {
+    H = p.H;
+    A = p.A;
+    nll = p.nll_mode != 0;
+    const long mval = max(0, min(rows, p.M - m0));
+    const uint32_t hb = (uint32_t)(mval * H * 4);
+    ldxb = (uint32_t)(p.ldx * (long)sizeof(DT));
+    const uint32_t xb = mval ? (uint32_t)(((mval - 1) * p.ldx + H) * (long)sizeof(DT)) : 0u;
+    rc = make_rsrc(p.c + (long)m0 * H, hb);
+    rxi = make_rsrc(reinterpret_cast<const DT*>(p.x_in) + (long)m0 * p.ldx + p.Z, xb);
+    rxo = make_rsrc(reinterpret_cast<DT*>(p.x_out) + (long)m0 * p.ldx + p.Z, xb);
+    rw = make_rsrc(p.WaT, (uint32_t)((long)A * 4 * H * (long)sizeof(DT)));
+    rb = make_rsrc(p.bg, (uint32_t)(16 * H));
+    rht = make_rsrc(p.h_trace ? p.h_trace + (long)m0 * H : nullptr, p.h_trace ? hb : 0u);
+    rct = make_rsrc(p.c_trace ? p.c_trace + (long)m0 * H : nullptr, p.c_trace ? hb : 0u);
+  }
+
+  // biases of units u0 .. u0+3 (gate order i, f, g, o)
+  __device__ __forceinline__ void bias(int u0, bool ok, float4 (&b)[4]) const {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) b[t] = as_float4(bload16(rb, ok ? (uint32_t)(u0 + t) * 16u : kOffNone));
+  }
+
+  // four 16-byte pieces of DT: units u0 .. u0+3 x 4 gates from WaT row a
+  __device__ __forceinline__ void gather(uint32_t off, float4 (&w)[4]) const {
+    if constexpr (sizeof(DT) == 4) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) w[t] = as_float4(bload16(rw, off == kOffNone ? kOffNone : off + 16u * t));
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint4 v = bload16(rw, off == kOffNone ? kOffNone : off + 16u * h);
+        w[2 * h] = make_float4(bf16_bits_to_f32(v.x & 0xffffu), bf16_bits_to_f32(v.x >> 16),
+                               bf16_bits_to_f32(v.y & 0xffffu), bf16_bits_to_f32(v.y >> 16));
+        w[2 * h + 1] = make_float4(bf16_bits_to_f32(v.z & 0xffffu), bf16_bits_to_f32(v.z >> 16),
+                                   bf16_bits_to_f32(v.w & 0xffffu), bf16_bits_to_f32(v.w >> 16));
+      }
+    }
+  }
+
+  __device__ __forceinline__ Gate4In load(int ml, int u0, int a, bool ok, const float4 (&b)[4]) const {
+    Gate4In in;
+    in.live = nll || a >= 0;
+    const bool gok = ok && a >= 0 && a < A;
+    float4 w[4];
+    gather(gok ? ((uint32_t)a * 4u * H + 4u * u0) * (uint32_t)sizeof(DT) : kOffNone, w);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      in.add[t] = make_float4(b[t].x + w[t].x, b[t].y + w[t].y, b[t].z + w[t].z, b[t].w + w[t].w);
+    in.c = as_float4(bload16(rc, ok ? ((uint32_t)ml * H + u0) * 4u : kOffNone));
+    const uint32_t ox = ok && !in.live ? (uint32_t)ml * ldxb + (uint32_t)u0 * (uint32_t)sizeof(DT) : kOffNone;
+    if constexpr (sizeof(DT) == 4) {
+      in.hprev = as_float4(bload16(rxi, ox));
+    } else {
+      const uint2 v = bload8(rxi, ox);
+      in.hprev = make_float4(bf16_bits_to_f32(v.x & 0xffffu), bf16_bits_to_f32(v.x >> 16),
+                             bf16_bits_to_f32(v.y & 0xffffu), bf16_bits_to_f32(v.y >> 16));
+    }
+    return in;
+  }
+
+  // g[t]: GEMM part of the gates (i, f, g, o) of unit u0 + t
+  __device__ __forceinline__ void commit(int ml, int u0, bool ok, const Gate4In& in, const float4 (&g)[4]) const {
+    float cv[4], hv[4];
+    const float cin[4] = {in.c.x, in.c.y, in.c.z, in.c.w};
+    const float hin[4] = {in.hprev.x, in.hprev.y, in.hprev.z, in.hprev.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const float cn = fsigmoid(g[t].y + in.add[t].y) * cin[t] +
+                       fsigmoid(g[t].x + in.add[t].x) * ftanh(g[t].z + in.add[t].z);
+      const float hn = DType<DT>::round(fsigmoid(g[t].w + in.add[t].w) * ftanh(cn));
+      cv[t] = in.live ? cn : cin[t];
+      hv[t] = in.live ? hn : hin[t];
+    }
+    const uint32_t ec = ((uint32_t)ml * H + u0) * 4u;
+    const uint32_t ex = (uint32_t)ml * ldxb + (uint32_t)u0 * (uint32_t)sizeof(DT);
+    const float4 c4 = make_float4(cv[0], cv[1], cv[2], cv[3]);
+    const float4 h4 = make_float4(hv[0], hv[1], hv[2], hv[3]);
+    bstore16(rc, ok && in.live ? ec : kOffNone, as_uint4(c4));
+    if constexpr (sizeof(DT) == 4) {
+      bstore16(rxo, ok ? ex : kOffNone, as_uint4(h4));
+    } else {
+      bstore8(rxo, ok ? ex : kOffNone,
+              make_uint2(f32_to_bf16_bits(hv[0]) | (f32_to_bf16_bits(hv[1]) << 16),
+                         f32_to_bf16_bits(hv[2]) | (f32_to_bf16_bits(hv[3]) << 16)));
+    }
+    bstore16(rht, ok ? ec : kOffNone, as_uint4(h4));  // dropped without traces
+    bstore16(rct, ok ? ec : kOffNone, as_uint4(c4));
+  }
+};
+
+// Gate kernel on the pipelined cores.  The GEMM tile is staged through LDS
+// as E[row][feature] (fp32) and the epilogue then runs with thread t on the
+// four-unit group t % GPR of rows t / GPR, t / GPR + RSTEP, ...
 template <class C>
 __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
   using DT = typename C::DT;
   constexpr int NBW = C::NBW, MBW = C::MBW;
-  __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
+  constexpr int GPR = C::BN / 16;          // groups of four units per tile row
+  constexpr int RSTEP = C::NT / GPR;       // rows per pass of the block
+  constexpr int IPT = (C::BM + RSTEP - 1) / RSTEP;
+  constexpr int ELD = C::BN + 4;           // staged row stride (floats)
+  constexpr int E_BYTES = C::BM * ELD * 4;
+  constexpr int LDS = C::LDS_BYTES > E_BYTES ? C::LDS_BYTES : E_BYTES;
+  static_assert(C::NT % GPR == 0, "whole groups per block");
+  __shared__ __attribute__((aligned(16))) char lds_raw[LDS];
   int nt, mt;
   if (!tile_of(p.map, nt, mt)) return;
   const int n0 = nt * C::BN, m0 = mt * C::BM;
-  const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
-  const int wn = C::wn(), wmi = C::wm();
-  // actions of this lane's rows, fetched ahead of the GEMM
-  int act[MBW];
+  const int grp = threadIdx.x % GPR, r0 = threadIdx.x / GPR;
+  const int u0 = n0 / 4 + 4 * grp;
+  // actions of this thread's epilogue rows, fetched ahead of the GEMM
+  int act[IPT];
 #pragma unroll
-  for (int j = 0; j < MBW; ++j) {
-    const int m = m0 + (wmi * MBW + j) * 16 + r16;
-    act[j] = m < p.M ? p.act[m] : -1;
+  for (int k = 0; k < IPT; ++k) {
+    const int r = r0 + k * RSTEP, m = m0 + r;
+    act[k] = (r < C::BM && m < p.M) ? p.act[m] : -1;
   }
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wg), p.ldk, p.ldk, n0, C::BN, 4 * p.H);
   const SrcX<DT> x(reinterpret_cast<const DT*>(p.x_in), p.ldx, p.ldx, m0, C::BM, p.M);
   f32x4 acc[NBW][MBW];
   C::run(acc, w, x, (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
-  if (C::kw() != 0) return;
 
-  const GateIO<DT> io(p, m0, C::BM);
+  float* E = reinterpret_cast<float*>(lds_raw);
+  if (C::kw() == 0) {
+    const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+    const int wn = C::wn(), wmi = C::wm();
 #pragma unroll
-  for (int j = 0; j < MBW; ++j) {
-    const int ml = (wmi * MBW + j) * 16 + r16;
-    GateIn in[NBW];
+    for (int j = 0; j < MBW; ++j)
 #pragma unroll
-    for (int i = 0; i < NBW; ++i) {
-      const int u = (n0 + (wn * NBW + i) * 16) / 4 + g;
-      in[i] = io.load(ml, u, act[j], m0 + ml < p.M && u < p.H);
-    }
+      for (int i = 0; i < NBW; ++i)
+        *reinterpret_cast<f32x4*>(E + ((wmi * MBW + j) * 16 + r16) * ELD + (wn * NBW + i) * 16 + 4 * g) =
+            acc[i][j];
+  }
+  __syncthreads();
+
+  const Gate4IO<DT> io(p, m0, C::BM);
+  const bool uok = u0 < p.H;  // H % 16 == 0: the whole group is inside
+  float4 b[4];
+  io.bias(u0, uok, b);
+  Gate4In in[IPT];
 #pragma unroll
-    for (int i = 0; i < NBW; ++i) {
-      const int u = (n0 + (wn * NBW + i) * 16) / 4 + g;
-      io.commit(ml, u, m0 + ml < p.M && u < p.H, in[i], acc[i][j][0], acc[i][j][1], acc[i][j][2],
-                acc[i][j][3]);
-    }
+  for (int k = 0; k < IPT; ++k) {
+    const int r = r0 + k * RSTEP;
+    in[k] = io.load(r, u0, act[k], uok && r < C::BM && m0 + r < p.M, b);
+  }
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const int r = r0 + k * RSTEP;
+    if (r >= C::BM) continue;
+    float4 gsum[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) gsum[t] = *reinterpret_cast<const float4*>(E + r * ELD + 16 * grp + 4 * t);
+    io.commit(r, u0, uok && m0 + r < p.M, in[k], gsum);
   }
 }
 
@@ -1637,9 +1771,9 @@ constexpr int kSmallRows = 2048;
 template <typename DT> struct Cfgs;
 template <> struct Cfgs<float> {
   using GatesSmall = Gemm<float, 2, 1, 2, 2, 1, 32, 4>;  // 64 x 32
-  using GatesLarge = Gemm<float, 4, 2, 2, 2, 1, 32, 3>;  // 128 x 64
+  using GatesLarge = GemmD<float, 4, 2, 2, 2, 2>;  // 128 x 64
   template <int Q> using MdnSmall = Gemm<float, Q, 1, 2, 1, 2, 32, 4>;  // 32Q x 16, K split 2
-  template <int Q> using MdnLarge = Gemm<float, Q, WM_MDN_LARGE_F32_MBW, 2, 2, 1, 32, 3>;
+  template <int Q> using MdnLarge = GemmD<float, Q, WM_MDN_LARGE_F32_MBW, 2, 2, 2>;
   template <int NB> using CtrlLarge = Gemm<float, NB, 4, 4, 1, 1, 32, 3>;  // 64NB x 64
   static constexpr int WIDE_BKC = 64;
 };
@@ -1647,7 +1781,7 @@ template <> struct Cfgs<bf16_t> {
   using GatesSmall = Gemm<bf16_t, 2, 1, 2, 2, 1, 64, 4>;
   using GatesLarge = GemmD<bf16_t, 4, 4, 2, 2, 2>;  // 128 x 128
   template <int Q> using MdnSmall = Gemm<bf16_t, Q, 1, 2, 1, 2, 64, 4>;
-  template <int Q> using MdnLarge = Gemm<bf16_t, Q, 2, 2, 2, 1, 64, 2>;
+  template <int Q> using MdnLarge = GemmD<bf16_t, Q, 2, 2, 2, 2>;
   template <int NB> using CtrlLarge = Gemm<bf16_t, NB, 4, 4, 1, 1, 64, 2>;
   static constexpr int WIDE_BKC = 128;
 };
