@@ -1211,173 +1211,128 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
   }
 }
 
-// k_ctrl: the same controller epilogue on the pipelined GEMM core, for
-// A + 2 <= 64 * NBW outputs: all Nc weight rows of a row block are staged
-// through LDS once per K chunk.  Waves with kw != 0 only help with the K
-// loop.  (k_ctrl_wide above reads the weights straight from global memory and
-// covers larger action counts.)
+// k_ctrl: controller on the pipelined GEMM core for A + 2 <= 64 * NBW
+// outputs (all Nc weight rows of a row block in one tile).  The logit tile
+// is staged through LDS as E[row][output]; each row is then handled by TPR
+// adjacent threads, thread q taking the contiguous actions
+// [q * APT, (q + 1) * APT) (APT a multiple of 4: one Philox block per four
+// actions).  The mask bytes of those actions are fetched as 32-bit words
+// before the GEMM when A % 4 == 0 (byte loads otherwise).
 template <class C, class S>
 __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
   using DT = typename C::DT;
-  constexpr int NBW = C::NBW, MBW = C::MBW, WN = C::WAVES_N, BM = C::BM;
-  __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
-  __shared__ float s_best[WN][BM];
-  __shared__ int s_idx[WN][BM];
-  __shared__ float s_max[WN][BM];
-  __shared__ float s_rho[BM][2];
-  __shared__ float s_fin[BM][2];
+  constexpr int NBW = C::NBW, MBW = C::MBW, BM = C::BM;
+  constexpr int TPR = C::NT / BM;               // threads per row
+  constexpr int MAXB = (C::BN / TPR + 3) / 4;  // Philox blocks per thread
+  constexpr int ELD = C::BN + 4;
+  constexpr int E_BYTES = BM * ELD * 4;
+  constexpr int LDS = C::LDS_BYTES > E_BYTES ? C::LDS_BYTES : E_BYTES;
+  static_assert(C::NT % BM == 0 && (TPR & (TPR - 1)) == 0 && TPR <= 16, "row groups inside a wave");
+  __shared__ __attribute__((aligned(16))) char lds_raw[LDS];
 
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int g = lane >> 4, r16 = lane & 15;
   const int m0 = blockIdx.x * BM;
-  const int nbtot = p.Nc / 16;
+  const int r = threadIdx.x / TPR, q = threadIdx.x % TPR;
+  const int m = m0 + r;
+  const bool row_ok = m < p.M;
+  const int A = p.A;
+  const int apt = (A + 4 * TPR - 1) / (4 * TPR) * 4;  // actions per thread
+  const int a0 = q * apt;
+  const bool want_action = p.mode != 2;
+
+  // mask words of this thread's actions, ahead of the GEMM
+  uint32_t mk[MAXB];
+  const rsrc_t rmask = make_rsrc(p.mask + (long)m0 * A, (uint32_t)(max(0, min(BM, p.M - m0)) * A));
+  const bool words = (A & 3) == 0 && (reinterpret_cast<uintptr_t>(p.mask) & 3) == 0;
+#pragma unroll
+  for (int b = 0; b < MAXB; ++b) {
+    const int a = a0 + 4 * b;
+    const bool ok = want_action && row_ok && 4 * b < apt && a < A;
+    const uint32_t off = (uint32_t)(r * A + a);
+    if (words) {
+      mk[b] = bload4(rmask, ok ? off : kOffNone);
+    } else {
+      mk[b] = 0;
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        mk[b] |= bload1(rmask, ok && a + v < A ? off + v : kOffNone) << (8 * v);
+    }
+  }
+
   f32x4 acc[NBW][MBW];
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wc), p.ldk, p.ldk, 0, p.Nc, p.Nc);
   C::run(acc, w, ctrl_src<S>(p, m0, BM), (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
-  const bool owner = C::kw() == 0;
-  const int wn = C::wn(), wmi = C::wm();
-
-  const Rng rng{p.k0, p.k1};
-  const int A = p.A;
-  const bool want_action = p.mode != 2;
-  if (owner) {
+  float* E = reinterpret_cast<float*>(lds_raw);
+  if (C::kw() == 0) {
+    const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+    const int wn = C::wn(), wmi = C::wm();
 #pragma unroll
-    for (int j = 0; j < MBW; ++j) {
-      const int ml = (wmi * MBW + j) * 16 + r16;
-      const int m = m0 + ml;
-      float best = -INFINITY, mx = -INFINITY;
-      int bidx = -1;
-      if (m < p.M) {
+    for (int j = 0; j < MBW; ++j)
 #pragma unroll
-        for (int i = 0; i < NBW; ++i) {
-          const int nb = wn * NBW + i;
-          if (nb >= nbtot) continue;
-          const int n = nb * 16 + 4 * g;
-          const float4 b4 = *reinterpret_cast<const float4*>(p.bc + n);
-          const float lg[4] = {acc[i][j][0] + b4.x, acc[i][j][1] + b4.y, acc[i][j][2] + b4.z,
-                               acc[i][j][3] + b4.w};
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            if (n + v == A) s_rho[ml][0] = lg[v];
-            if (n + v == A + 1) s_rho[ml][1] = lg[v];
-          }
-          if (want_action && n < A) {
-            const uint4 w = rng.block((uint32_t)(n >> 2), p.step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              if (n + v < A && p.mask[(long)m * A + n + v]) {
-                mx = fmaxf(mx, lg[v]);
-                const float sc = lg[v] + gumbel(word_to_uniform(word_of(w, v)));
-                if (sc > best) { best = sc; bidx = n + v; }
-              }
-            }
-          }
-        }
-      }
-      // reduce over the four lane groups (same row), lowest index on ties
-#pragma unroll
-      for (int off = 16; off <= 32; off <<= 1) {
-        const float ob = __shfl_xor(best, off);
-        const int oi = __shfl_xor(bidx, off);
-        const float om = __shfl_xor(mx, off);
-        if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
-        mx = fmaxf(mx, om);
-      }
-      if (g == 0) {
-        s_best[wn][ml] = best;
-        s_idx[wn][ml] = bidx;
-        s_max[wn][ml] = mx;
-      }
-    }
+      for (int i = 0; i < NBW; ++i)
+        *reinterpret_cast<f32x4*>(E + ((wmi * MBW + j) * 16 + r16) * ELD + (wn * NBW + i) * 16 + 4 * g) =
+            acc[i][j];
   }
   __syncthreads();
 
-  if (p.mode == 0) {
-    if (tid < BM) {
-      float best = -INFINITY, mx = -INFINITY;
-      int bidx = -1;
-      for (int w = 0; w < WN; ++w) {
-        const float ob = s_best[w][tid];
-        const int oi = s_idx[w][tid];
-        if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
-        mx = fmaxf(mx, s_max[w][tid]);
+  const float* lg = E + r * ELD;
+  const Rng rng{p.k0, p.k1};
+  const uint32_t traj = p.traj0 + (uint32_t)m;
+  float best = -INFINITY, mx = -INFINITY;
+  int bidx = -1;
+  if (want_action && row_ok) {
+#pragma unroll
+    for (int b = 0; b < MAXB; ++b) {
+      if (mk[b] == 0) continue;  // no valid action in the block (or outside the range)
+      const int a = a0 + 4 * b;
+      const uint4 wd = rng.block((uint32_t)(a >> 2), p.step, traj, STREAM_CONTROLLER);
+      const float4 l4 = *reinterpret_cast<const float4*>(lg + a);
+      const float4 b4 = *reinterpret_cast<const float4*>(p.bc + a);
+      const float lv[4] = {l4.x + b4.x, l4.y + b4.y, l4.z + b4.z, l4.w + b4.w};
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        if ((mk[b] >> (8 * v)) & 0xffu) {
+          mx = fmaxf(mx, lv[v]);
+          const float sc = lv[v] + gumbel(word_to_uniform(word_of(wd, v)));
+          if (sc > best) { best = sc; bidx = a + v; }
+        }
       }
-      s_fin[tid][0] = mx;
-      const int m = m0 + tid;
-      if (m < p.M) p.action[m] = bidx;
     }
-    __syncthreads();
+  }
+  // reduce over the TPR threads of the row, lowest index on ties
+#pragma unroll
+  for (int off = 1; off < TPR; off <<= 1) {
+    const float ob = __shfl_xor(best, off);
+    const int oi = __shfl_xor(bidx, off);
+    const float om = __shfl_xor(mx, off);
+    if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
+    mx = fmaxf(mx, om);
+  }
+  if (p.mode == 0) {
+    if (row_ok && q == 0) p.action[m] = bidx;
     if (p.probs) {
-      if (owner) {
+      float se = 0.f;
 #pragma unroll
-        for (int j = 0; j < MBW; ++j) {
-          const int ml = (wmi * MBW + j) * 16 + r16;
-          const int m = m0 + ml;
-          float se = 0.f;
-          if (m < p.M) {
-            const float mx = s_fin[ml][0];
+      for (int b = 0; b < MAXB; ++b)
 #pragma unroll
-            for (int i = 0; i < NBW; ++i) {
-              const int nb = wn * NBW + i;
-              if (nb >= nbtot) continue;
-              const int n = nb * 16 + 4 * g;
+        for (int v = 0; v < 4; ++v)
+          if ((mk[b] >> (8 * v)) & 0xffu) se += expf(lg[a0 + 4 * b + v] + p.bc[a0 + 4 * b + v] - mx);
 #pragma unroll
-              for (int v = 0; v < 4; ++v)
-                if (n + v < A && p.mask[(long)m * A + n + v]) se += expf(acc[i][j][v] + p.bc[n + v] - mx);
-            }
+      for (int off = 1; off < TPR; off <<= 1) se += __shfl_xor(se, off);
+      const float inv = se > 0.f ? 1.0f / se : 0.f;
+      if (row_ok) {
+#pragma unroll
+        for (int b = 0; b < MAXB; ++b)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int a = a0 + 4 * b + v;
+            if (4 * b + v < apt && a < A)
+              p.probs[(long)m * A + a] = ((mk[b] >> (8 * v)) & 0xffu) ? expf(lg[a] + p.bc[a] - mx) * inv : 0.f;
           }
-          se += __shfl_xor(se, 16);
-          se += __shfl_xor(se, 32);
-          if (g == 0) s_best[wn][ml] = se;
-        }
-      }
-      __syncthreads();
-      if (tid < BM) {
-        float tot = 0.f;
-        for (int w = 0; w < WN; ++w) tot += s_best[w][tid];
-        s_fin[tid][1] = tot;
-      }
-      __syncthreads();
-      if (owner) {
-#pragma unroll
-        for (int j = 0; j < MBW; ++j) {
-          const int ml = (wmi * MBW + j) * 16 + r16;
-          const int m = m0 + ml;
-          if (m >= p.M) continue;
-          const float mx = s_fin[ml][0], inv = s_fin[ml][1] > 0.f ? 1.0f / s_fin[ml][1] : 0.f;
-#pragma unroll
-          for (int i = 0; i < NBW; ++i) {
-            const int nb = wn * NBW + i;
-            if (nb >= nbtot) continue;
-            const int n = nb * 16 + 4 * g;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              if (n + v < A) {
-                const bool ok = p.mask[(long)m * A + n + v] != 0;
-                p.probs[(long)m * A + n + v] = ok ? expf(acc[i][j][v] + p.bc[n + v] - mx) * inv : 0.f;
-              }
-            }
-          }
-        }
       }
     }
     return;
   }
-
-  // rollout modes: one thread per row
-  if (tid < BM) {
-    const int m = m0 + tid;
-    if (m < p.M) {
-      float best = -INFINITY;
-      int a = -1;
-      for (int w = 0; w < WN; ++w) {
-        const float ob = s_best[w][tid];
-        const int oi = s_idx[w][tid];
-        if (oi >= 0 && (a < 0 || ob > best || (ob == best && oi < a))) { best = ob; a = oi; }
-      }
-      ctrl_row_commit(p, rng, m, a, s_rho[tid][0], s_rho[tid][1]);
-    }
-  }
+  if (row_ok && q == 0) ctrl_row_commit(p, rng, m, bidx, lg[A] + p.bc[A], lg[A + 1] + p.bc[A + 1]);
 }
 
 // ===========================================================================
