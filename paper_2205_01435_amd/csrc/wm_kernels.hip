@@ -1730,6 +1730,7 @@ template <> struct Cfgs<float> {
   template <int Q> using MdnSmall = Gemm<float, Q, 1, 2, 1, 2, 32, 4>;  // 32Q x 16, K split 2
   template <int Q> using MdnLarge = GemmD<float, Q, WM_MDN_LARGE_F32_MBW, 2, 2, 2>;
   template <int NB> using CtrlLarge = Gemm<float, NB, 4, 4, 1, 1, 32, 3>;  // 64NB x 64
+  template <int NB> using CtrlLargeX = GemmD<float, NB, 2, 4, 1, 3>;      // 64NB x 32
   static constexpr int WIDE_BKC = 64;
 };
 template <> struct Cfgs<bf16_t> {
@@ -1738,6 +1739,7 @@ template <> struct Cfgs<bf16_t> {
   template <int Q> using MdnSmall = Gemm<bf16_t, Q, 1, 2, 1, 2, 64, 4>;
   template <int Q> using MdnLarge = GemmD<bf16_t, Q, 2, 2, 2, 2>;
   template <int NB> using CtrlLarge = Gemm<bf16_t, NB, 4, 4, 1, 1, 64, 2>;
+  template <int NB> using CtrlLargeX = GemmD<bf16_t, NB, 2, 4, 1, 3>;
   static constexpr int WIDE_BKC = 128;
 };
 
@@ -1913,10 +1915,17 @@ hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
     }
   }
   const int nb = (nbtot + 3) / 4;  // output blocks per wave over four waves
-  if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLarge<1>, S>(a, s);
-  if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlLarge<2>, S>(a, s);
-  if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlLarge<3>, S>(a, s);
-  if (nb <= 5) return launch_ctrl_cfg<typename Cf::template CtrlLarge<5>, S>(a, s);
+  if constexpr (S::kTwo) {
+    if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLarge<1>, S>(a, s);
+    if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlLarge<2>, S>(a, s);
+    if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlLarge<3>, S>(a, s);
+    if (nb <= 5) return launch_ctrl_cfg<typename Cf::template CtrlLarge<5>, S>(a, s);
+  } else {
+    if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLargeX<1>, S>(a, s);
+    if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlLargeX<2>, S>(a, s);
+    if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlLargeX<3>, S>(a, s);
+    if (nb <= 5) return launch_ctrl_cfg<typename Cf::template CtrlLargeX<5>, S>(a, s);
+  }
   if (nb <= 8) return launch_ctrl_wide<S, 8, 2>(a, s);
   if (nb <= 12) return launch_ctrl_wide<S, 12, 2>(a, s);
   if (nb <= 17) return launch_ctrl_wide<S, 17, 1>(a, s);
