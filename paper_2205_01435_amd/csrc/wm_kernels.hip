@@ -1803,9 +1803,7 @@ template <class C, typename DT>
 hipError_t launch_gates_cfg(GatesArgs a, hipStream_t s) {
   a.map = tile_map((4 * a.H + C::BN - 1) / C::BN, (a.M + C::BM - 1) / C::BM,
                    (size_t)4 * a.H * a.ldk * sizeof(DT));
-  KTimer kt("gates", s);
-  hipLaunchKernelGGL((k_gates<C>), dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
-  return hipGetLastError();
+  return launch("gates", k_gates<C>, dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
 }
 
 template <typename DT>
@@ -1818,9 +1816,7 @@ hipError_t launch_gates(GatesArgs a, hipStream_t s) {
     if (e != hipSuccess) return e;
     a.map = tile_map((4 * a.H + R::BN - 1) / R::BN, (a.M + R::BM - 1) / R::BM,
                      (size_t)4 * a.H * a.ldk * sizeof(DT));
-    KTimer kt("gates", s);
-    hipLaunchKernelGGL((k_gates_rd<R>), dim3(grid_of(a.map)), dim3(64 * nw), lds, s, a);
-    return hipGetLastError();
+    return launch("gates", k_gates_rd<R>, dim3(grid_of(a.map)), dim3(64 * nw), lds, s, a);
   }
   if (a.M <= kSmallRows) return launch_gates_cfg<typename Cfgs<DT>::GatesSmall, DT>(a, s);
   return launch_gates_cfg<typename Cfgs<DT>::GatesLarge, DT>(a, s);
@@ -1829,9 +1825,7 @@ hipError_t launch_gates(GatesArgs a, hipStream_t s) {
 template <class C, typename DT>
 hipError_t launch_mdn_cfg(MdnArgs a, int ntiles, hipStream_t s) {
   a.map = tile_map(ntiles, (a.M + C::BM - 1) / C::BM, (size_t)a.Nm * a.ldh * sizeof(DT));
-  KTimer kt("mdn", s);
-  hipLaunchKernelGGL((k_mdn<C>), dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
-  return hipGetLastError();
+  return launch("mdn", k_mdn<C>, dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
 }
 
 template <typename DT, int Q>
@@ -1846,9 +1840,7 @@ hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
       MdnArgs b = a;
       // one dim group per tile
       b.map = tile_map(a.Z / 4, (a.M + R::BM - 1) / R::BM, (size_t)a.Nm * a.ldh * sizeof(DT));
-      KTimer kt("mdn", s);
-      hipLaunchKernelGGL((k_mdn_rd<R>), dim3(grid_of(b.map)), dim3(64 * nw), lds, s, b);
-      return hipGetLastError();
+      return launch("mdn", k_mdn_rd<R>, dim3(grid_of(b.map)), dim3(64 * nw), lds, s, b);
     }
   }
   if (a.M <= kSmallRows) return launch_mdn_cfg<typename Cfgs<DT>::template MdnSmall<Q>, DT>(a, ntiles, s);
@@ -1870,18 +1862,14 @@ hipError_t launch_mdn(const MdnArgs& a, int Q, int ntiles, hipStream_t s) {
 
 template <class C, class S>
 hipError_t launch_ctrl_cfg(const CtrlArgs& a, hipStream_t s) {
-  KTimer kt("ctrl", s);
-  hipLaunchKernelGGL((k_ctrl<C, S>), dim3((a.M + C::BM - 1) / C::BM), dim3(C::NT), 0, s, a);
-  return hipGetLastError();
+  return launch("ctrl", k_ctrl<C, S>, dim3((a.M + C::BM - 1) / C::BM), dim3(C::NT), 0, s, a);
 }
 
 template <class S, int NBW, int MBW>
 hipError_t launch_ctrl_wide(const CtrlArgs& a, hipStream_t s) {
   constexpr int BM = 16 * MBW;
-  KTimer kt("ctrl", s);
-  hipLaunchKernelGGL((k_ctrl_wide<S, NBW, MBW, Cfgs<typename S::DT>::WIDE_BKC>),
-                     dim3((a.M + BM - 1) / BM), dim3(256), 0, s, a);
-  return hipGetLastError();
+  return launch("ctrl", k_ctrl_wide<S, NBW, MBW, Cfgs<typename S::DT>::WIDE_BKC>,
+                dim3((a.M + BM - 1) / BM), dim3(256), 0, s, a);
 }
 
 template <class R, class S>
@@ -1889,9 +1877,7 @@ hipError_t launch_ctrl_rd(const CtrlArgs& a, int nw, hipStream_t s) {
   const size_t lds = R::lds_bytes(nw);
   hipError_t e = allow_lds(k_ctrl_rd<R, S>, lds);
   if (e != hipSuccess) return e;
-  KTimer kt("ctrl", s);
-  hipLaunchKernelGGL((k_ctrl_rd<R, S>), dim3((a.M + R::BM - 1) / R::BM), dim3(64 * nw), lds, s, a);
-  return hipGetLastError();
+  return launch("ctrl", k_ctrl_rd<R, S>, dim3((a.M + R::BM - 1) / R::BM), dim3(64 * nw), lds, s, a);
 }
 
 // S: activation source (SrcX for the rollout's X_t, SrcZH for the step).
@@ -1949,14 +1935,9 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   DT* X = reinterpret_cast<DT*>(R.x);
   const long BX = (long)B * L.ldx, BH = (long)B * H, BZ = (long)B * Z;
   const bool trace = (R.flags & 2u) != 0;
-  hipError_t e;
-  {
-    KTimer kt("init", s);
-    hipLaunchKernelGGL((k_rollout_init<DT>), dim3(elem_grid(BX)), dim3(256), 0, s, B, Z, H, L.ldx,
-                       R.z0, R.h0, R.c0, R.done_io, R.z_out, X, X + BX, R.c, R.done_state,
-                       trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr);
-    e = hipGetLastError();
-  }
+  hipError_t e = launch("init", k_rollout_init<DT>, dim3(elem_grid(BX)), dim3(256), 0, s, B, Z, H,
+                        L.ldx, R.z0, R.h0, R.c0, R.done_io, R.z_out, X, X + BX, R.c, R.done_state,
+                        trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr);
   if (e != hipSuccess) return e;
 
   CtrlArgs ca{};
@@ -2023,10 +2004,8 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
     e = launch_mdn<DT>(ma, L.Q, mdn_tiles, s);
     if (e != hipSuccess) return e;
   }
-  KTimer kt("finish", s);
-  hipLaunchKernelGGL((k_rollout_finish<DT>), dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, L.ldx,
-                     X + (long)(T & 1) * BX, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
-  return hipGetLastError();
+  return launch("finish", k_rollout_finish<DT>, dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, L.ldx,
+                X + (long)(T & 1) * BX, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
 }
 
 template <typename DT>
@@ -2036,13 +2015,8 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   const int B = N.B, T = N.T, Z = L.Z, H = L.H;
   const long BX = (long)B * L.ldx, BZ = (long)B * Z, M = (long)T * B;
   DT* X = reinterpret_cast<DT*>(N.x);
-  hipError_t e;
-  {
-    KTimer kt("nll_init", s);
-    hipLaunchKernelGGL((k_nll_init<DT>), dim3(elem_grid((long)(T + 1) * B * (L.ldx - H))), dim3(256),
-                       0, s, T, B, Z, H, L.ldx, N.z, X, N.c);
-    e = hipGetLastError();
-  }
+  hipError_t e = launch("nll_init", k_nll_init<DT>, dim3(elem_grid((long)(T + 1) * B * (L.ldx - H))),
+                        dim3(256), 0, s, T, B, Z, H, L.ldx, N.z, X, N.c);
   if (e != hipSuccess) return e;
 
   GatesArgs ga{};
@@ -2079,19 +2053,10 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   if (e != hipSuccess) return e;
 
   const int nwg = (int)((M + 255) / 256);
-  {
-    KTimer kt("nll_reduce", s);
-    hipLaunchKernelGGL(k_nll_reduce, dim3(nwg), dim3(256), 0, s, T, B, ntd, N.part, N.head,
-                       N.rewards, N.dones, N.lengths, N.loglik, N.reward_se, N.done_bce, N.wgsum);
-    e = hipGetLastError();
-  }
-  if (e != hipSuccess) return e;
-  if (N.means) {
-    KTimer kt("nll_means", s);
-    hipLaunchKernelGGL(k_nll_means, dim3(1), dim3(256), 0, s, nwg, Z, N.wgsum, N.means);
-    e = hipGetLastError();
-  }
-  return e;
+  e = launch("nll_reduce", k_nll_reduce, dim3(nwg), dim3(256), 0, s, T, B, ntd, N.part, N.head,
+             N.rewards, N.dones, N.lengths, N.loglik, N.reward_se, N.done_bce, N.wgsum);
+  if (e != hipSuccess || !N.means) return e;
+  return launch("nll_means", k_nll_means, dim3(1), dim3(256), 0, s, nwg, Z, N.wgsum, N.means);
 }
 
 }  // namespace
@@ -2140,14 +2105,12 @@ hipError_t launch_pack(const Packed& P, void* packed, const float* W_g, const fl
                        const float* w_d, const float* b_d, const float* W_c, const float* b_c,
                        hipStream_t s) {
   dim3 grid(1024, 7);
-  KTimer kt("pack", s);
+  char* out = reinterpret_cast<char*>(packed);
   if (P.L.dt == 0)
-    hipLaunchKernelGGL(k_pack<float>, grid, dim3(256), 0, s, P.L, reinterpret_cast<char*>(packed),
-                       W_g, b_g, W_m, b_m, w_r, b_r, w_d, b_d, W_c, b_c);
-  else
-    hipLaunchKernelGGL(k_pack<bf16_t>, grid, dim3(256), 0, s, P.L, reinterpret_cast<char*>(packed),
-                       W_g, b_g, W_m, b_m, w_r, b_r, w_d, b_d, W_c, b_c);
-  return hipGetLastError();
+    return launch("pack", k_pack<float>, grid, dim3(256), 0, s, P.L, out, W_g, b_g, W_m, b_m, w_r, b_r,
+                  w_d, b_d, W_c, b_c);
+  return launch("pack", k_pack<bf16_t>, grid, dim3(256), 0, s, P.L, out, W_g, b_g, W_m, b_m, w_r, b_r,
+                w_d, b_d, W_c, b_c);
 }
 
 hipError_t launch_controller_step(const Packed& P, int B, uint32_t traj0, const float* z,

@@ -1,4 +1,5 @@
-// Per-kernel HIP-event timing for measurement runs (wm_profile_* entry points).
+// Per-kernel timing for measurement runs (wm_profile_* entry points): event
+// pairs stamped by the kernel dispatches (see launch() in wm_profile.h).
 #include "wm_profile.h"
 
 #include <stdint.h>
@@ -41,27 +42,29 @@ bool starts_with(const std::string& s, const char* p) {
 
 }  // namespace
 
-KTimer::KTimer(const char* name, hipStream_t s) : name_(name), s_(s) {
+KTimer::KTimer(const char* name) : name_(name) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on || std::strncmp(name, g_prefix.c_str(), g_prefix.size()) != 0) return;
   a_ = take_event();
   b_ = take_event();
-  if (a_ && b_ && hipEventRecord(a_, s_) == hipSuccess) return;
+  if (a_ && b_) return;
   if (a_) g_pool.push_back(a_);
   if (b_) g_pool.push_back(b_);
   a_ = b_ = nullptr;
 }
 
-KTimer::~KTimer() {
+void KTimer::commit() {
   if (!a_ || !b_) return;
-  const bool ok = hipEventRecord(b_, s_) == hipSuccess;
   std::lock_guard<std::mutex> lk(g_mu);
-  if (ok) {
-    g_recs.push_back(Rec{name_, a_, b_});
-  } else {
-    g_pool.push_back(a_);
-    g_pool.push_back(b_);
-  }
+  g_recs.push_back(Rec{name_, a_, b_});
+  a_ = b_ = nullptr;
+}
+
+KTimer::~KTimer() {
+  if (!a_ && !b_) return;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (a_) g_pool.push_back(a_);
+  if (b_) g_pool.push_back(b_);
 }
 
 }  // namespace wm
