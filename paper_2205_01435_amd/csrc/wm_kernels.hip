@@ -1806,17 +1806,27 @@ hipError_t launch_gates_cfg(GatesArgs a, hipStream_t s) {
   return launch("gates", k_gates<C>, dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
 }
 
-template <typename DT>
-hipError_t launch_gates(GatesArgs a, hipStream_t s) {
-  using R = GemmRD<DT, 2, 2, 8, 512>;
+// Register-direct gate launch with tile R; returns hipErrorNotSupported
+// when the K slices do not fit the compiled block size or the LDS budget.
+template <class R, typename DT>
+hipError_t launch_gates_rd(GatesArgs a, hipStream_t s) {
   const int nw = rd_waves((int)a.ldk, R::KSLICE, R::SMAX, 4);
   const size_t lds = R::lds_bytes(nw);
-  if (a.M <= WM_RD_GATES_ROWS && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
-    hipError_t e = allow_lds(k_gates_rd<R>, lds);
-    if (e != hipSuccess) return e;
-    a.map = tile_map((4 * a.H + R::BN - 1) / R::BN, (a.M + R::BM - 1) / R::BM,
-                     (size_t)4 * a.H * a.ldk * sizeof(DT));
-    return launch("gates", k_gates_rd<R>, dim3(grid_of(a.map)), dim3(64 * nw), lds, s, a);
+  if (64 * nw > R::MAXT || lds > kRdLdsMax) return hipErrorNotSupported;
+  hipError_t e = allow_lds(k_gates_rd<R>, lds);
+  if (e != hipSuccess) return e;
+  a.map = tile_map((4 * a.H + R::BN - 1) / R::BN, (a.M + R::BM - 1) / R::BM,
+                   (size_t)4 * a.H * a.ldk * sizeof(DT));
+  return launch("gates", k_gates_rd<R>, dim3(grid_of(a.map)), dim3(64 * nw), lds, s, a);
+}
+
+template <typename DT>
+hipError_t launch_gates(GatesArgs a, hipStream_t s) {
+  if (a.M <= WM_RD_GATES_ROWS) {
+    // 16-row tiles for a single row block, 32-row tiles above
+    const hipError_t e = a.M <= 16 ? launch_gates_rd<GemmRD<DT, 2, 1, 4, 640>, DT>(a, s)
+                                   : launch_gates_rd<GemmRD<DT, 2, 2, 4, 640>, DT>(a, s);
+    if (e != hipErrorNotSupported) return e;
   }
   if (a.M <= kSmallRows) return launch_gates_cfg<typename Cfgs<DT>::GatesSmall, DT>(a, s);
   return launch_gates_cfg<typename Cfgs<DT>::GatesLarge, DT>(a, s);
@@ -1831,7 +1841,7 @@ hipError_t launch_mdn_cfg(MdnArgs a, int ntiles, hipStream_t s) {
 template <typename DT, int Q>
 hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
   if (!a.nll_mode) {
-    using R = GemmRD<DT, Q, 2, (Q <= 4 ? 8 : 4), 512>;
+    using R = GemmRD<DT, Q, 1, 4, 640>;  // 16-row tiles: more work-groups
     const int nw = rd_waves((int)a.ldh, R::KSLICE, R::SMAX, 4);
     const size_t lds = R::lds_bytes(nw);
     if (a.M <= WM_RD_MDN_ROWS && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
