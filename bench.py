@@ -47,15 +47,28 @@ def flops_per_token(w) -> float:
     return 2.0 * (4 * H * (Z + H) + 3 * Z * K * H + 2 * H)
 
 
-def kernel_flops_per_launch(name: str, w, B: int, T: int) -> float:
-    """Algorithmic flops of one launch of a kernel class in the bench step."""
+def kernel_flops_per_launch(name: str, w, B: int, T: int, mdn_launches_per_step: int = 1) -> float:
+    """Algorithmic flops of one launch of a kernel class in the bench step.
+    persist: one whole dream rollout (every phase of every step);
+    nll_persist: the NLL pass's recurrence (gate GEMMs of all T steps);
+    gates / ctrl: one dream step of the multi-launch path;
+    mdn: the NLL head over all T*B rows, plus, on the multi-launch path, T
+    rollout launches of B rows (averaged over the launches)."""
     Z, H, A, K = w.Z, w.H, w.A, w.K
+    if name == "persist":
+        return B * T * flops_per_transition(w)
+    if name == "nll_persist":
+        return 2.0 * B * T * 4 * H * (Z + H)
     if name == "gates":
         return 2.0 * B * 4 * H * (Z + H)
     if name == "ctrl":
         return 2.0 * B * (A * (Z + H) + 2 * H)
     if name == "mdn":
-        raise ValueError("mdn launches differ between rollout and NLL")
+        head = 2.0 * B * T * (3 * Z * K + 2) * H
+        if mdn_launches_per_step == 1:
+            return head
+        rollout = T * 2.0 * B * 3 * Z * K * H
+        return (head + rollout) / mdn_launches_per_step
     return 0.0
 
 
@@ -121,7 +134,9 @@ def main() -> int:
     for i in range(max(args.warmup, 1)):
         step(i)
     torch.cuda.synchronize()
-    classes = ["ctrl", "gates", "mdn", "init", "finish", "nll_init", "nll_reduce", "nll_means"]
+    classes = ["persist", "nll_persist", "ctrl", "gates", "mdn", "init", "finish", "nll_init",
+               "nll_reduce", "nll_means"]
+    nwarm = max(args.warmup, 1)
     warm = {c: wmlib.profile_read(c) for c in classes}
     dominant = max(classes, key=lambda c: warm[c][0])
     wmlib.profile_enable(None)
@@ -173,17 +188,8 @@ def main() -> int:
 
     # roofline of the dominant kernel
     avg_ms = k_ms / max(k_n, 1)
-    if dominant == "mdn":
-        # mixed: rollout launches (B rows) and one NLL launch (B*T rows + head)
-        per_step = T * 2.0 * B * 3 * w.Z * w.K * w.H + 2.0 * B * T * (3 * w.Z * w.K + 2) * w.H
-        launches_per_step = T + 1
-        flops_launch = per_step / launches_per_step
-    elif dominant == "gates":
-        flops_launch = kernel_flops_per_launch("gates", w, B, T)
-    elif dominant == "ctrl":
-        flops_launch = 2.0 * B * (w.A * (w.Z + w.H) + 2 * w.H)
-    else:
-        flops_launch = 0.0
+    mdn_per_step = max(1, round(warm["mdn"][1] / nwarm))
+    flops_launch = kernel_flops_per_launch(dominant, w, B, T, mdn_per_step)
     achieved = flops_launch / (avg_ms / 1e3) if avg_ms > 0 else 0.0
     traffic = read_summary(os.path.join(ROOT, "profiles", f"traffic_{dominant}_medium_rollout_nll_fp32.md"))
     roofline = {"kernel": dominant, "bound": "mfma", "achieved": achieved / 1e12,

@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libwm.so")
-SOURCES = ["wm_kernels.hip", "wm_api.cpp", "wm_profile.cpp"]
+SOURCES = ["wm_kernels.hip", "wm_persist.hip", "wm_api.cpp", "wm_profile.cpp"]
 HEADERS = ["wm_device.h", "wm_kernels.h", "wm_layout.h", "wm_profile.h"]
 ARCH = "gfx950"
 
@@ -37,22 +37,26 @@ def compile_flags() -> list[str]:
 
 
 def build_library(verbose: bool = False) -> str:
-    """Compile every source and link ``libwm.so`` next to this file."""
+    """Compile every source (in parallel) and link ``libwm.so`` next to this file."""
+    from concurrent.futures import ThreadPoolExecutor
+
     cc = hipcc()
-    objs = []
     build_dir = os.path.join(PKG, "_build")
     os.makedirs(build_dir, exist_ok=True)
-    for src in SOURCES:
+
+    def compile_one(src):
         obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
-        lang = ["-x", "hip"]
-        cmd = [cc, *lang, *compile_flags(), "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [cc, "-x", "hip", *compile_flags(), "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         res = subprocess.run(cmd, capture_output=True, text=True)
         if res.returncode != 0:
             sys.stderr.write(res.stdout + res.stderr)
             raise RuntimeError(f"hipcc failed on {src}")
-        objs.append(obj)
+        return obj
+
+    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
+        objs = list(ex.map(compile_one, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)

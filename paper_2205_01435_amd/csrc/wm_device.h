@@ -262,4 +262,121 @@ struct SrcZH {
   }
 };
 
+
+// ---------------------------------------------------------------------------
+// Mixture sampling of one latent dim j of one trajectory at one step:
+// Gumbel-max component pick on pi-logit / tau (stream 1, uniform j*K + k),
+// then mu + exp(log sigma) * eps with eps from Box-Muller on the stream-2 pair
+// (2p, 2p+1) that contains j (cos for even j, sin for odd j).
+// mixture_noise draws the random part (independent of the head GEMM, so it
+// can be issued early); mixture_pick finishes from the dim's features
+// f = 0 .. 4Q-1 (pi-logits, means, log sigmas, padding), biased.
+// ---------------------------------------------------------------------------
+struct MdnNoise {
+  float g[8];  // Gumbel noise of components 0 .. K-1 (K <= 8)
+  float eps;   // standard normal of dim j
+};
+
+__device__ __forceinline__ MdnNoise mixture_noise(const Rng& rng, int K, uint32_t step, uint32_t traj,
+                                                  int j) {
+  MdnNoise n;
+  uint32_t cur = 0xffffffffu;
+  uint4 w = make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    n.g[k] = 0.f;
+    if (k < K) {
+      const uint32_t idx = (uint32_t)j * K + k;
+      if ((idx >> 2) != cur) {
+        cur = idx >> 2;
+        w = rng.block(cur, step, traj, STREAM_COMPONENT);
+      }
+      n.g[k] = gumbel(word_to_uniform(word_of(w, idx & 3)));
+    }
+  }
+  const uint4 wg = rng.block((uint32_t)j >> 2, step, traj, STREAM_GAUSS);
+  const float u1 = word_to_uniform(word_of(wg, j & 2));
+  const float u2 = word_to_uniform(word_of(wg, (j & 2) + 1));
+  const float r = sqrtf(-2.0f * logf(u1));
+  float sn, cs;
+  sincospif(2.0f * u2, &sn, &cs);
+  n.eps = (j & 1) ? r * sn : r * cs;
+  return n;
+}
+
+template <int Q>
+__device__ __forceinline__ float mixture_pick(int K, float tau, const MdnNoise& n,
+                                              const float (&feat)[4 * Q]) {
+  float best = -INFINITY;
+  int kbest = 0;
+#pragma unroll
+  for (int f = 0; f < 4 * Q && f < 8; ++f) {
+    if (f < K) {
+      const float sc = feat[f] / tau + n.g[f];
+      if (sc > best) { best = sc; kbest = f; }
+    }
+  }
+  float mu = 0.f, ls = 0.f;
+#pragma unroll
+  for (int f = 0; f < 4 * Q; ++f) {
+    if (f == K + kbest) mu = feat[f];
+    if (f == 2 * K + kbest) ls = feat[f];
+  }
+  return mu + expf(ls) * n.eps;
+}
+
+// ---------------------------------------------------------------------------
+// LDS-DMA: buffer loads that write straight into LDS (no staging registers,
+// no LDS store instructions).
+// ---------------------------------------------------------------------------
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource words for inline assembly (same fields as make_rsrc).
+__device__ __forceinline__ u32x4 rsrc_words(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  u32x4 r;
+  r.x = (uint32_t)a;
+  r.y = (uint32_t)(a >> 32) & 0xffffu;
+  r.z = bytes;
+  r.w = 0x00020000u;
+  return r;
+}
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// 16 bytes per lane from the buffer at byte offset voff into LDS at
+// lds + 16 * lane (lds is wave-uniform).  Out-of-range offsets load zeros.
+// Issued as inline assembly so that the compiler does not wait for these
+// loads before every LDS read; callers wait with vm_wait<N>() instead.
+__device__ __forceinline__ void dma16(u32x4 rs, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rs)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+// vm_wait with a run-time bound (clamped to 0 .. 63).
+__device__ __forceinline__ void vm_wait_n(int n) {
+  switch (n <= 0 ? 0 : (n >= 63 ? 63 : n)) {
+#define WM_VMW(k) case k: vm_wait<k>(); break;
+    WM_VMW(0) WM_VMW(1) WM_VMW(2) WM_VMW(3) WM_VMW(4) WM_VMW(5) WM_VMW(6) WM_VMW(7)
+    WM_VMW(8) WM_VMW(9) WM_VMW(10) WM_VMW(11) WM_VMW(12) WM_VMW(13) WM_VMW(14) WM_VMW(15)
+    WM_VMW(16) WM_VMW(17) WM_VMW(18) WM_VMW(19) WM_VMW(20) WM_VMW(21) WM_VMW(22) WM_VMW(23)
+    WM_VMW(24) WM_VMW(25) WM_VMW(26) WM_VMW(27) WM_VMW(28) WM_VMW(29) WM_VMW(30) WM_VMW(31)
+    WM_VMW(32) WM_VMW(33) WM_VMW(34) WM_VMW(35) WM_VMW(36) WM_VMW(37) WM_VMW(38) WM_VMW(39)
+    WM_VMW(40) WM_VMW(41) WM_VMW(42) WM_VMW(43) WM_VMW(44) WM_VMW(45) WM_VMW(46) WM_VMW(47)
+    WM_VMW(48) WM_VMW(49) WM_VMW(50) WM_VMW(51) WM_VMW(52) WM_VMW(53) WM_VMW(54) WM_VMW(55)
+    WM_VMW(56) WM_VMW(57) WM_VMW(58) WM_VMW(59) WM_VMW(60) WM_VMW(61) WM_VMW(62) WM_VMW(63)
+#undef WM_VMW
+  }
+}
+
 }  // namespace wm

@@ -32,6 +32,8 @@ struct RolloutBufs {
   void* x;             // [2, B, ldx] dtype: activation matrices X_t, X_t+1
   float* c;            // [B, H]
   int32_t* done_state; // [B]
+  float* P;            // [32, B, Nc] controller partial logits (persistent kernel) or null
+  unsigned* sync;      // kSyncWords barrier words (persistent kernel)
 };
 
 struct NllBufs {
@@ -48,7 +50,11 @@ struct NllBufs {
   float* part;   // [T*B, NTd]
   float* head;   // [T*B, 2]
   float* wgsum;  // [nwg, 4]
+  unsigned* sync;  // kSyncWords barrier words (persistent kernel)
 };
+
+// Barrier words of the persistent kernels (zeroed by the init kernels).
+constexpr int kSyncWords = 64 * 17;
 
 // Workspace sizes; with a non-null `ws` the workspace pointers of the
 // buffer struct are also set (ws must be 256-byte aligned).
@@ -67,5 +73,13 @@ hipError_t launch_controller_step(const Packed& P, int B, uint32_t traj0, const 
 hipError_t launch_rollout(const Packed& P, const RolloutBufs& R, hipStream_t s);
 
 hipError_t launch_nll(const Packed& P, const NllBufs& N, hipStream_t s);
+
+// Persistent single-launch kernels (wm_persist.hip) for small fp32 batches.
+// The launchers return hipErrorNotSupported when the dims, the batch or the
+// device are outside what they serve (or WM_PERSISTENT=0 is set).
+size_t persist_partial_bytes(const Layout& L, int B);  // 0 if not served
+bool persist_usable(const Layout& L, int B, bool nll);
+hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStream_t s);
+hipError_t launch_nll_persist(const Packed& P, const NllBufs& N, hipStream_t s);
 
 }  // namespace wm

@@ -277,40 +277,6 @@ struct Gemm {
 // Same interface as Gemm (without a K split); Kpad must be a multiple of
 // the chunk.
 // ===========================================================================
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-
-// Buffer resource words for inline assembly (same fields as make_rsrc).
-__device__ __forceinline__ u32x4 rsrc_words(const void* p, uint32_t bytes) {
-  const uint64_t a = reinterpret_cast<uint64_t>(p);
-  u32x4 r;
-  r.x = (uint32_t)a;
-  r.y = (uint32_t)(a >> 32) & 0xffffu;
-  r.z = bytes;
-  r.w = 0x00020000u;
-  return r;
-}
-
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-// 16 bytes per lane from the buffer at byte offset voff into LDS at
-// lds + 16 * lane (lds is wave-uniform).  Out-of-range offsets load zeros.
-// Issued as inline assembly so that the compiler does not wait for these
-// loads before every LDS read; callers wait with vm_wait<N>() instead.
-__device__ __forceinline__ void dma16(u32x4 rs, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :
-               : "s"(lds), "v"(voff), "s"(rs)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-// Wait until at most N vector-memory operations of this wave are in flight.
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
-}
-
 template <typename DT_, int NBW_, int MBW_, int WAVES_N_, int WAVES_M_, int STAGES_>
 struct GemmD {
   using DT = DT_;
@@ -746,65 +712,16 @@ struct MdnArgs {
   TileMap map;
 };
 
-// z_{t+1,j} of row m: Gumbel-max component pick on pi-logit / tau (stream 1,
-// uniform j*K + k), then mu + exp(log sigma) * eps with eps from Box-Muller on
-// the stream-2 pair (2p, 2p+1) that contains j.  mdn_noise draws the random
-// part (independent of the GEMM, so callers can issue it early); mdn_pick
-// finishes from the dim's features f = 0 .. 4Q-1 (pi-logits, means, log
-// sigmas, padding), biased.
-struct MdnNoise {
-  float g[8];  // Gumbel noise of components 0 .. K-1 (K <= 8)
-  float eps;   // standard normal of dim j
-};
-
+// z_{t+1,j} of row m (mixture_noise / mixture_pick with the call's step,
+// temperature and trajectory index).
 __device__ __forceinline__ MdnNoise mdn_noise(const MdnArgs& p, const Rng& rng, int m, int j) {
-  MdnNoise n;
-  const int K = p.K;
-  const uint32_t traj = p.traj0 + (uint32_t)m;
-  uint32_t cur = 0xffffffffu;
-  uint4 w = make_uint4(0, 0, 0, 0);
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    n.g[k] = 0.f;
-    if (k < K) {
-      const uint32_t idx = (uint32_t)j * K + k;
-      if ((idx >> 2) != cur) {
-        cur = idx >> 2;
-        w = rng.block(cur, p.step, traj, STREAM_COMPONENT);
-      }
-      n.g[k] = gumbel(word_to_uniform(word_of(w, idx & 3)));
-    }
-  }
-  const uint4 wg = rng.block((uint32_t)j >> 2, p.step, traj, STREAM_GAUSS);
-  const float u1 = word_to_uniform(word_of(wg, j & 2));
-  const float u2 = word_to_uniform(word_of(wg, (j & 2) + 1));
-  const float r = sqrtf(-2.0f * logf(u1));
-  float sn, cs;
-  sincospif(2.0f * u2, &sn, &cs);
-  n.eps = (j & 1) ? r * sn : r * cs;
-  return n;
+  return mixture_noise(rng, p.K, p.step, p.traj0 + (uint32_t)m, j);
 }
 
 template <int Q>
 __device__ __forceinline__ float mdn_pick(const MdnArgs& p, const MdnNoise& n,
                                           const float (&feat)[4 * Q]) {
-  const int K = p.K;
-  float best = -INFINITY;
-  int kbest = 0;
-#pragma unroll
-  for (int f = 0; f < 4 * Q && f < 8; ++f) {
-    if (f < K) {
-      const float sc = feat[f] / p.tau + n.g[f];
-      if (sc > best) { best = sc; kbest = f; }
-    }
-  }
-  float mu = 0.f, ls = 0.f;
-#pragma unroll
-  for (int f = 0; f < 4 * Q; ++f) {
-    if (f == K + kbest) mu = feat[f];
-    if (f == 2 * K + kbest) ls = feat[f];
-  }
-  return mu + expf(ls) * n.eps;
+  return mixture_pick<Q>(p.K, p.tau, n, feat);
 }
 
 template <int Q>
@@ -1588,9 +1505,11 @@ __global__ void k_rollout_init(int B, int Z, int H, int ldx, const float* __rest
                                const uint8_t* __restrict__ done_io, float* __restrict__ z_out,
                                DT* __restrict__ X0, DT* __restrict__ X1, float* __restrict__ c,
                                int32_t* __restrict__ done_state, float* __restrict__ h_trace,
-                               float* __restrict__ c_trace) {
+                               float* __restrict__ c_trace, unsigned* __restrict__ sync) {
   const long stride = (long)gridDim.x * blockDim.x;
   const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (sync)
+    for (long i = i0; i < kSyncWords; i += stride) sync[i] = 0u;
   for (long i = i0; i < (long)B * ldx; i += stride) {
     const long b = i / ldx;
     const int col = (int)(i % ldx);
@@ -1630,9 +1549,11 @@ __global__ void k_rollout_finish(int B, int Z, int H, int ldx, const DT* __restr
 // X_t[:, 0:Z] = q(z_t) for t = 0..T, padding columns zero, h_0 = c_0 = 0.
 template <typename DT>
 __global__ void k_nll_init(int T, int B, int Z, int H, int ldx, const float* __restrict__ z,
-                           DT* __restrict__ X, float* __restrict__ c) {
+                           DT* __restrict__ X, float* __restrict__ c, unsigned* __restrict__ sync) {
   const long stride = (long)gridDim.x * blockDim.x;
   const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (sync)
+    for (long i = i0; i < kSyncWords; i += stride) sync[i] = 0u;
   const int ncol = ldx - H;  // z columns, then padding columns
   for (long i = i0; i < (long)(T + 1) * B * ncol; i += stride) {
     const long r = i / ncol;
@@ -1947,8 +1868,16 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   const bool trace = (R.flags & 2u) != 0;
   hipError_t e = launch("init", k_rollout_init<DT>, dim3(elem_grid(BX)), dim3(256), 0, s, B, Z, H,
                         L.ldx, R.z0, R.h0, R.c0, R.done_io, R.z_out, X, X + BX, R.c, R.done_state,
-                        trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr);
+                        trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr, R.sync);
   if (e != hipSuccess) return e;
+  if (T > 0) {
+    // one persistent launch for every step when the batch and dims allow it
+    e = launch_rollout_persist(P, R, s);
+    if (e == hipSuccess)
+      return launch("finish", k_rollout_finish<DT>, dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, L.ldx,
+                    X + (long)(T & 1) * BX, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
+    if (e != hipErrorNotSupported) return e;
+  }
 
   CtrlArgs ca{};
   ca.Wc = base + L.off_Wc;
@@ -2026,7 +1955,7 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   const long BX = (long)B * L.ldx, BZ = (long)B * Z, M = (long)T * B;
   DT* X = reinterpret_cast<DT*>(N.x);
   hipError_t e = launch("nll_init", k_nll_init<DT>, dim3(elem_grid((long)(T + 1) * B * (L.ldx - H))),
-                        dim3(256), 0, s, T, B, Z, H, L.ldx, N.z, X, N.c);
+                        dim3(256), 0, s, T, B, Z, H, L.ldx, N.z, X, N.c, N.sync);
   if (e != hipSuccess) return e;
 
   GatesArgs ga{};
@@ -2038,12 +1967,15 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
   ga.H = H; ga.A = L.A; ga.Z = Z; ga.M = B;
   ga.nll_mode = 1;
   ga.c = N.c;
-  for (int t = 0; t < T; ++t) {
+  // the recurrence: one persistent launch when the batch and dims allow it
+  e = launch_nll_persist(P, N, s);
+  if (e != hipSuccess && e != hipErrorNotSupported) return e;
+  for (int t = 0; e == hipErrorNotSupported && t < T; ++t) {
     ga.x_in = X + (long)t * BX;
     ga.x_out = X + (long)(t + 1) * BX;
     ga.act = N.actions + (long)t * B;
-    e = launch_gates<DT>(ga, s);
-    if (e != hipSuccess) return e;
+    const hipError_t eg = launch_gates<DT>(ga, s);
+    if (eg != hipSuccess) return eg;
   }
 
   const int ntd = Z / 8;
@@ -2079,10 +2011,17 @@ size_t rollout_workspace(const Layout& L, int B, char* ws, RolloutBufs* R) {
   o = wm_align256(o + (size_t)B * L.H * 4);  // c
   const size_t od = o;
   o = wm_align256(o + (size_t)B * 4);  // done state
+  const size_t os = o;
+  o = wm_align256(o + (size_t)kSyncWords * 4);  // persistent-kernel barriers
+  const size_t pb = persist_partial_bytes(L, B);
+  const size_t op = o;
+  o = wm_align256(o + pb);  // persistent-kernel controller partials
   if (ws && R) {
     R->x = ws + ox;
     R->c = reinterpret_cast<float*>(ws + oc);
     R->done_state = reinterpret_cast<int32_t*>(ws + od);
+    R->sync = reinterpret_cast<unsigned*>(ws + os);
+    R->P = pb ? reinterpret_cast<float*>(ws + op) : nullptr;
   }
   return o;
 }
@@ -2100,7 +2039,10 @@ size_t nll_workspace(const Layout& L, int B, int T, char* ws, NllBufs* N) {
   o = wm_align256(o + M * 2 * 4);  // reward / done logits
   const size_t og = o;
   o = wm_align256(o + ((M + 255) / 256) * 4 * 4);  // block sums
+  const size_t os = o;
+  o = wm_align256(o + (size_t)kSyncWords * 4);  // persistent-kernel barriers
   if (ws && N) {
+    N->sync = reinterpret_cast<unsigned*>(ws + os);
     N->x = ws + ox;
     N->c = reinterpret_cast<float*>(ws + oc);
     N->part = reinterpret_cast<float*>(ws + op);

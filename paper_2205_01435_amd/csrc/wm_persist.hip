@@ -1,0 +1,873 @@
+// Persistent kernels of libwm for small batches (fp32) on gfx950 (MI355X):
+// one launch runs every step of a dream rollout, or every step of the NLL
+// pass's teacher-forced recurrence.
+//
+// Rows are split over the eight XCDs: XCD x owns rows [x*Bx, (x+1)*Bx) and
+// its 32 work-groups (one per CU; blockIdx % 8 selects the XCD) step those
+// trajectories together.  Trajectories of different XCDs never exchange
+// data, so every barrier is local to one XCD: a counter in that XCD's L2,
+// producers wait for their stores to reach the L2 (vmcnt), and everything a
+// work-group reads that another one wrote during the call is read with
+// device-coherent loads (sc1: past the CU's L1, served by the shared L2), so
+// no cache has to be invalidated and the weights stay in the L2.  That costs
+// about 0.9 us per barrier on the MI355X, where a kernel boundary costs
+// about 4.5 us and a barrier with agent-scope fences 4-7 us.  Each
+// work-group checks its hardware XCD id at the start; if any member of a
+// group is not on the group's XCD, the group uses agent-scope fences
+// instead, so results never depend on the placement.
+//
+// Each work-group owns NBC blocks of four hidden units (16 gate rows each).
+// The gate weights of those rows stay in registers for the whole call (the
+// A operand of the MFMAs), and each lane keeps the cell state of the
+// (unit, row) pairs it owns in registers.  Per dream step t, three phases
+// separated by XCD barriers:
+//   ctrl(t)   one row per work-group: logits = b_c + W_c,z q(z_t) + the sum
+//             of the 32 work-groups' h-part partials (from gates(t-1); the
+//             full product at t = 0), masked Gumbel-max action, resolution
+//             of transition t-1 (reward, done), freeze logic;
+//   gates(t)  X_t of the XCD's rows staged in LDS (LDS-DMA, four chunks so
+//             that the MFMAs start on the first), gate GEMM against the
+//             register weights, LSTM cell, h_{t+1} into X_{t+1}, and this
+//             work-group's partial W_c,h h_{t+1} of the next controller
+//             logits (rows A and A+1 of W_c are the reward and done heads);
+//   mdn(t)    (group of four latent dims, 16-row block) tiles, K split over
+//             the four waves and summed in LDS, component pick, Box-Muller
+//             draw, z_{t+1} to z_out and X_{t+1}.
+// The NLL recurrence runs gates(t) only, one barrier per step; the mixture
+// head then runs once over all T*B rows (wm_kernels.hip).
+// Every wait is bounded: a wait that times out raises an error word that
+// every other wait polls, and all work-groups leave.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <cstdlib>
+#include <cstring>
+
+#include "wm_device.h"
+#include "wm_kernels.h"
+#include "wm_layout.h"
+#include "wm_profile.h"
+
+namespace wm {
+namespace {
+
+constexpr int kGroups = 8;     // XCDs
+constexpr int kMembers = 32;   // work-groups (CUs) per XCD
+constexpr int kGrid = kGroups * kMembers;
+constexpr int kMaxS = 36;      // register-resident MFMA K slices per wave (4 chunks of 9)
+constexpr int kMaxQ = 6;       // mixture output blocks per latent-dim group (K <= 8)
+constexpr int kMaxMS = 8;      // mixture-head K slices per wave (H <= 512)
+constexpr unsigned kSpinLimit = 1u << 22;
+
+struct PArgs {
+  const float *Wg, *WaT, *bg, *Wm, *bm, *Wc, *bc;
+  int Z, H, A, K, Q, Nc, ldk, ldh, ldx;
+  int B, T, Bx;
+  uint32_t k0, k1, traj0, step0;
+  float tau;
+  int use_done, wat_lds;
+  float* X;             // rollout [2, B, ldx]; NLL [T+1, B, ldx]
+  float* c;             // [B, H]: initial cell state in, final state out (rollout)
+  int32_t* done_state;  // [B]
+  float* P;             // [32, B, Nc] controller partial logits (rollout)
+  unsigned* sync;       // kSyncWords words, zero at launch
+  const uint8_t* mask;  // [B, A]
+  float* z_out;         // [T+1, B, Z]
+  int32_t* actions;     // [T, B]: rollout output, NLL input
+  float* rewards;
+  uint8_t* dones;
+  float *h_trace, *c_trace;  // [T+1, B, H] or null
+  // LDS carve-up (bytes)
+  int off_red, off_hb, off_wat, off_mdn, off_ctl;
+};
+
+// sync words: group counters at 64*x, placement flags at 64*(8+x), error at 64*16
+__device__ __forceinline__ unsigned* sync_ctr(const PArgs& p, int x) { return p.sync + 64 * x; }
+__device__ __forceinline__ unsigned* sync_flag(const PArgs& p, int x) { return p.sync + 64 * (8 + x); }
+__device__ __forceinline__ unsigned* sync_err(const PArgs& p) { return p.sync + 64 * 16; }
+
+__device__ __forceinline__ unsigned xcc_id() { return __builtin_amdgcn_s_getreg((3 << 11) | 20) & 15u; }
+
+struct GroupSync {
+  unsigned* ctr;
+  unsigned* err;
+  unsigned n;  // barriers passed
+  bool agent;  // members not all on one XCD: agent-scope fences
+};
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// Barrier of the 32 work-groups of one XCD.  Returns false if the group must
+// stop (a wait timed out here or elsewhere).
+__device__ __forceinline__ bool group_sync(GroupSync& gs, volatile int* flag) {
+  if (gs.agent) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  else asm volatile("s_waitcnt vmcnt(0)" : : : "memory");  // this wave's stores reached L2
+  __syncthreads();
+  ++gs.n;
+  if (threadIdx.x == 0) {
+    int ok = 1;
+    __hip_atomic_fetch_add(gs.ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned target = gs.n * kMembers;
+    unsigned spins = 0;
+    while ((int)(__hip_atomic_load(gs.ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+      if ((++spins & 63u) == 0) {
+        if (__hip_atomic_load(gs.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+          ok = 0;
+          break;
+        }
+        if (spins >= kSpinLimit) {
+          __hip_atomic_fetch_or(gs.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ok = 0;
+          break;
+        }
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (gs.agent) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    *flag = ok;
+  }
+  __syncthreads();
+  return *flag != 0;
+}
+#pragma clang diagnostic pop
+
+// Device-coherent (sc1) reads of data other work-groups wrote during the
+// call: they bypass this CU's L1, which may still hold an older copy of the
+// line, and are served by the XCD's L2.
+__device__ __forceinline__ uint32_t cload4(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 16);
+}
+__device__ __forceinline__ uint4 cload16(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 16));
+}
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// dma16 with the device-coherent policy
+__device__ __forceinline__ void cdma16(u32x4 rs, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen sc1 lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rs)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Issue v (0..3) of a 16-wide fp32 K slice (the four issues of Mfma<float>::step).
+__device__ __forceinline__ void mfma4(f32x4& acc, const uint4& a, const uint4& b, int v) {
+  const uint32_t av = v == 0 ? a.x : v == 1 ? a.y : v == 2 ? a.z : a.w;
+  const uint32_t bv = v == 0 ? b.x : v == 1 ? b.y : v == 2 ? b.z : b.w;
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(av), __uint_as_float(bv), acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char*)p);
+}
+
+// ---------------------------------------------------------------------------
+// Per-work-group state that lives across steps.
+// ---------------------------------------------------------------------------
+template <int RB, int NBC>
+struct GateState {
+  static constexpr int KSPLIT = 4 / NBC;
+  uint4 wr[kMaxS];  // gate weights: rows 16 blk + r16, K slices sl0 .. sl0+nper-1
+  uint4 wc[2];      // controller h-part weights of this CU's units (rollout)
+  float4 bias;      // b_g of this lane's unit (owner waves)
+  float cst[RB];    // cell state of (unit, row 16 rb + r16) (owner waves)
+};
+
+// This work-group's share of the next controller logits from the h block in
+// LDS (its units, all rows of the XCD):
+// P[s][m][a] = sum over its units u of W_c[a][Z + u] h[m][u].
+template <int RB, int NBC>
+__device__ __forceinline__ void ctrl_partials(const PArgs& p, const GateState<RB, NBC>& st, char* lds,
+                                              int r0, int nrows) {
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int s = blockIdx.x >> 3;
+  const int B = p.B;
+  const int rbv = (nrows + 15) >> 4;
+  const float* hb = reinterpret_cast<const float*>(lds + p.off_hb);
+  {
+    __syncthreads();
+    const rsrc_t rp = make_rsrc(p.P + ((long)s * B + r0) * p.Nc, (uint32_t)(nrows * p.Nc * 4));
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int nbk = wave + 4 * j;
+      if (16 * nbk >= p.Nc) break;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        if (rb >= rbv) break;
+        const uint4 hf = *reinterpret_cast<const uint4*>(hb + (16 * rb + r16) * 16 + 4 * g);
+        f32x4 pc = f32x4{0.f, 0.f, 0.f, 0.f};
+        Mfma<float>::step(pc, st.wc[j], hf);
+        const int ml = 16 * rb + r16;
+        const uint32_t op = ml < nrows ? (uint32_t)(ml * p.Nc + 16 * nbk + 4 * g) * 4u : kOffNone;
+        bstore16(rp, op, make_uint4(__float_as_uint(pc[0]), __float_as_uint(pc[1]), __float_as_uint(pc[2]),
+                                    __float_as_uint(pc[3])));
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// gates(t): X_in -> h_{t+1} into X_out (+ the controller partials)
+// ---------------------------------------------------------------------------
+template <int RB, int NBC, bool NLL>
+__device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& st, char* lds, int t,
+                                            const float* Xin, float* Xout, int r0, int nrows) {
+  constexpr int KSPLIT = GateState<RB, NBC>::KSPLIT;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
+  const int s = blockIdx.x >> 3;
+  const int wb = wave % NBC, kp = wave / NBC;
+  const int blk = s * NBC + wb;
+  const int unit = 4 * blk + g;
+  const bool owner = kp == 0;
+  const int nks = p.ldk >> 4;
+  const int nper = (nks + KSPLIT - 1) / KSPLIT;
+  const int sl0 = kp * nper;
+  const int B = p.B, H = p.H, A = p.A;
+
+  // epilogue inputs issued first (older than the staging loads)
+  const rsrc_t ra = make_rsrc(p.actions + (long)t * B + r0, (uint32_t)nrows * 4u);
+  int act[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int ml = 16 * rb + r16;
+    act[rb] = owner && ml < nrows ? (int)cload4(ra, (uint32_t)ml * 4u) : -1;
+  }
+
+  // stage X_in rows [r0, r0 + nrows), columns [0, ldk) into LDS as
+  // [slice][row block][16 rows][16 floats]; instruction order: chunk, K part,
+  // slice, row block, dealt round-robin to the waves
+  const u32x4 rsx = rsrc_words(Xin + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
+  const uint32_t lds0 = lds_addr(lds);
+  const uint32_t ldxb = (uint32_t)p.ldx * 4u;
+  const int rbv = (nrows + 15) >> 4;  // row blocks holding valid rows
+  int mine[4] = {0, 0, 0, 0};
+  int jj = 0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    // the 32 work-groups of an XCD read the same rows: each starts its chunk
+    // at a different slice so that they do not all hit the same L2 lines
+    const int len = min(9, nper - 9 * c);
+    for (int kq = 0; kq < KSPLIT; ++kq) {
+      for (int ii = 0; ii < len; ++ii) {
+        const int i = 9 * c + (ii + s) % len;
+        const int sl = kq * nper + i;
+        if (sl >= nks) continue;
+        for (int rb = 0; rb < rbv; ++rb, ++jj) {
+          if ((jj & 3) != wave) continue;
+          const uint32_t voff = (uint32_t)(16 * rb + (lane >> 2)) * ldxb + (uint32_t)sl * 64u + (uint32_t)(lane & 3) * 16u;
+          cdma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
+          ++mine[c];
+        }
+      }
+    }
+  }
+
+  // two accumulator sets (even and odd K slices) and RB row blocks give
+  // 2 RB independent MFMA chains, issued interleaved
+  f32x4 acc2[2][RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) acc2[0][rb] = acc2[1][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int later = mine[0] + mine[1] + mine[2] + mine[3];
+  const int nval = min(nper, nks - sl0);  // this wave's valid K slices (uniform)
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    later -= mine[c];
+    vm_wait_n(later);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" : : : "memory");
+    const char* sb0 = lds + sl0 * RB * 1024 + 64 * r16 + 16 * g;
+    if (9 * c + 9 <= nval && rbv == RB) {
+      // whole chunk, every row block: straight-line MFMAs, slices in pairs
+#pragma unroll
+      for (int i = 9 * c; i < 9 * c + 9; i += 2) {
+        const bool two = i + 1 < 9 * c + 9;
+        uint4 b0[RB], b1[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          b0[rb] = *reinterpret_cast<const uint4*>(sb0 + (i * RB + rb) * 1024);
+          if (two) b1[rb] = *reinterpret_cast<const uint4*>(sb0 + ((i + 1) * RB + rb) * 1024);
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            mfma4(acc2[i & 1][rb], st.wr[i], b0[rb], v);
+            if (two) mfma4(acc2[(i + 1) & 1][rb], st.wr[i + 1], b1[rb], v);
+          }
+      }
+    } else {
+#pragma unroll
+      for (int i = 9 * c; i < 9 * c + 9; ++i) {
+        if (i < nval) {
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            if (rb < rbv)
+              Mfma<float>::step(acc2[i & 1][rb], st.wr[i], *reinterpret_cast<const uint4*>(sb0 + (i * RB + rb) * 1024));
+        }
+      }
+    }
+  }
+  f32x4 acc[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) acc[rb] = acc2[0][rb] + acc2[1][rb];
+
+  // K-split partials meet in LDS (waves of the same gate block)
+  if constexpr (KSPLIT > 1) {
+    f32x4* red = reinterpret_cast<f32x4*>(lds + p.off_red);
+    if (!owner) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) red[(((kp - 1) * NBC + wb) * RB + rb) * 64 + lane] = acc[rb];
+    }
+    __syncthreads();
+    if (owner) {
+#pragma unroll
+      for (int k2 = 1; k2 < KSPLIT; ++k2)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) acc[rb] += red[(((k2 - 1) * NBC + wb) * RB + rb) * 64 + lane];
+    }
+  }
+
+  float* hb = reinterpret_cast<float*>(lds + p.off_hb);  // [16 RB rows][16 units]
+  if (owner) {
+    const rsrc_t rxo = make_rsrc(Xout + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
+    const rsrc_t rw = make_rsrc(p.WaT, (uint32_t)(A * 4 * H * 4));
+    const bool tr = p.h_trace != nullptr;
+    const rsrc_t rht = make_rsrc(tr ? p.h_trace + ((long)(t + 1) * B + r0) * H : nullptr, tr ? (uint32_t)(nrows * H * 4) : 0u);
+    const rsrc_t rct = make_rsrc(tr ? p.c_trace + ((long)(t + 1) * B + r0) * H : nullptr, tr ? (uint32_t)(nrows * H * 4) : 0u);
+    const int hcol = p.Z + unit;  // X column of this lane's h
+    const float* wat = reinterpret_cast<const float*>(lds + p.off_wat);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int ml = 16 * rb + r16;
+      const bool ok = ml < nrows;
+      const int a = act[rb];
+      const bool live = NLL || a >= 0;
+      const bool gather = ok && a >= 0 && a < A;
+      float4 add;
+      if (p.wat_lds) {
+        add = gather ? *reinterpret_cast<const float4*>(wat + (a * NBC * 4 + 4 * wb + g) * 4)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {
+        add = as_float4(bload16(rw, gather ? (uint32_t)((a * 4 * H + 4 * unit) * 4) : kOffNone));
+      }
+      const float pi = acc[rb][0] + st.bias.x + add.x, pf = acc[rb][1] + st.bias.y + add.y;
+      const float pg = acc[rb][2] + st.bias.z + add.z, po = acc[rb][3] + st.bias.w + add.w;
+      float cn = fsigmoid(pf) * st.cst[rb] + fsigmoid(pi) * ftanh(pg);
+      float hn = fsigmoid(po) * ftanh(cn);
+      if (!live) {
+        cn = st.cst[rb];
+        hn = *reinterpret_cast<const float*>(lds + ((hcol >> 4) * RB + rb) * 1024 + 64 * r16 + 4 * (hcol & 15));
+      }
+      if (ok) st.cst[rb] = cn;
+      const uint32_t ox = ok ? (uint32_t)ml * ldxb + (uint32_t)hcol * 4u : kOffNone;
+      bstore4(rxo, ox, __float_as_uint(hn));
+      const uint32_t oh = ok ? (uint32_t)(ml * H + unit) * 4u : kOffNone;
+      bstore4(rht, oh, __float_as_uint(hn));  // dropped without traces
+      bstore4(rct, oh, __float_as_uint(cn));
+      if constexpr (!NLL) hb[ml * 16 + 4 * wb + g] = hn;
+    }
+  }
+
+  if constexpr (!NLL) ctrl_partials<RB, NBC>(p, st, lds, r0, nrows);
+}
+
+// ---------------------------------------------------------------------------
+// mdn(t): mixture head on h_{t+1} (X_out columns Z ..), z_{t+1}
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void mdn_phase(const PArgs& p, char* lds, int t, float* Xout, int r0, int nrows) {
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
+  const int s = blockIdx.x >> 3;
+  const int B = p.B, Z = p.Z, H = p.H, Q = p.Q;
+  const int rbv = (nrows + 15) >> 4;
+  const int ntiles = (Z >> 2) * rbv;
+  const int nsl = H >> 4;
+  const int per = (nsl + 3) >> 2;  // K slices per wave (<= kMaxMS)
+  const int s0 = wave * per;
+  const Rng rng{p.k0, p.k1};
+  const uint32_t step = p.step0 + (uint32_t)t;
+  const uint32_t ldxb = (uint32_t)p.ldx * 4u;
+  const rsrc_t rwm = make_rsrc(p.Wm, (uint32_t)((16 * Q * (Z >> 2) + 16) * p.ldh * 4));
+  const rsrc_t rx = make_rsrc(Xout + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
+  const rsrc_t ra = make_rsrc(p.actions + (long)t * B + r0, (uint32_t)nrows * 4u);
+  const rsrc_t rzp = make_rsrc(p.z_out + ((long)t * B + r0) * Z, (uint32_t)(nrows * Z * 4));
+  const rsrc_t rzn = make_rsrc(p.z_out + ((long)(t + 1) * B + r0) * Z, (uint32_t)(nrows * Z * 4));
+  f32x4* red = reinterpret_cast<f32x4*>(lds + p.off_mdn);  // [4 waves][Q][64 lanes]
+
+  for (int ti = s; ti < ntiles; ti += kMembers) {
+    const int J = ti / rbv, rb = ti % rbv;
+    const int ml = 16 * rb + r16, j = 4 * J + g;
+    const bool ok = ml < nrows;
+    // wave 0 owns the epilogue: liveness, noise or the frozen latent
+    bool live = false;
+    float zprev = 0.f;
+    MdnNoise nz{};
+    if (wave == 0) {
+      const int a = (int)cload4(ra, ok ? (uint32_t)ml * 4u : kOffNone);
+      live = ok && a >= 0;
+      if (live) nz = mixture_noise(rng, p.K, step, p.traj0 + (uint32_t)(r0 + ml), j);
+      zprev = __uint_as_float(cload4(rzp, ok && !live ? (uint32_t)(ml * Z + j) * 4u : kOffNone));
+    }
+    f32x4 acc[kMaxQ];
+#pragma unroll
+    for (int q = 0; q < kMaxQ; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // slice i's fragments are fetched three slices ahead of their MFMAs; the
+    // scheduling barriers keep the compiler from hoisting every fetch (which
+    // would not fit the registers next to the resident gate weights)
+    uint4 af[kMaxMS][kMaxQ], bf[kMaxMS];
+#pragma unroll
+    for (int i = 0; i < kMaxMS + 3; ++i) {
+      if (i < kMaxMS) {
+        const int sl = s0 + i;
+        const bool kin = i < per && sl < nsl;
+        const uint32_t kb = (uint32_t)(sl * 16 + 4 * g) * 4u;
+        bf[i] = cload16(rx, kin && ok ? (uint32_t)ml * ldxb + (uint32_t)Z * 4u + kb : kOffNone);
+#pragma unroll
+        for (int q = 0; q < kMaxQ; ++q)
+          if (q < Q)
+            af[i][q] = bload16(rwm, kin ? (uint32_t)((16 * Q * J + 16 * q + r16) * p.ldh) * 4u + kb : kOffNone);
+      }
+      if (i >= 3 && i - 3 < per && s0 + i - 3 < nsl) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+          for (int q = 0; q < kMaxQ; ++q)
+            if (q < Q) mfma4(acc[q], af[i - 3][q], bf[i - 3], v);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q = 0; q < kMaxQ; ++q)
+      if (q < Q) red[(wave * Q + q) * 64 + lane] = acc[q];
+    __syncthreads();
+    if (wave == 0 && ok) {
+      float z = zprev;
+      if (live) {
+        float feat[4 * kMaxQ];
+#pragma unroll
+        for (int q = 0; q < kMaxQ; ++q) {
+          f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (q < Q) {
+            v = red[q * 64 + lane] + red[(Q + q) * 64 + lane] + red[(2 * Q + q) * 64 + lane] +
+                red[(3 * Q + q) * 64 + lane];
+            const float4 b4 = *reinterpret_cast<const float4*>(p.bm + 16 * Q * J + 16 * q + 4 * g);
+            v += f32x4{b4.x, b4.y, b4.z, b4.w};
+          }
+          feat[4 * q] = v[0]; feat[4 * q + 1] = v[1]; feat[4 * q + 2] = v[2]; feat[4 * q + 3] = v[3];
+        }
+        z = mixture_pick<kMaxQ>(p.K, p.tau, nz, feat);
+      }
+      bstore4(rzn, (uint32_t)(ml * Z + j) * 4u, __float_as_uint(z));
+      bstore4(rx, (uint32_t)ml * ldxb + (uint32_t)j * 4u, __float_as_uint(z));
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// ctrl(t): action a_t of each row (mode 1) and resolution of transition t-1
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void ctrl_phase(const PArgs& p, char* lds, int t, const float* Xt, int r0,
+                                           int nrows) {
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int s = blockIdx.x >> 3;
+  const int B = p.B, Z = p.Z, A = p.A, Nc = p.Nc;
+  const int k = __builtin_amdgcn_readfirstlane(tid >> 7), a = tid & 127;  // k: wave-uniform
+  const int ml = s + kMembers * k;
+  const bool rowok = ml < nrows;
+  const int m = r0 + ml;
+  const bool tail = t == p.T;
+  const uint32_t step = p.step0 + (uint32_t)t;
+  const Rng rng{p.k0, p.k1};
+  float* lg = reinterpret_cast<float*>(lds + p.off_ctl);  // [2][128] logits
+  float* wbest = lg + 256;                                // [4] best score per wave
+  int* widx = reinterpret_cast<int*>(wbest + 4);           // [4] its action
+  float* xz = lg + 272;                                   // [2][Z] q(z_t) of the two rows
+
+  // z_t of this work-group's rows (written by mdn(t-1) elsewhere on the XCD)
+  {
+    const int zq = Z >> 2;  // 16-byte pieces per row
+    for (int e = tid; e < 2 * zq; e += 256) {
+      const int kk = e / zq, pc = e % zq;
+      const int mr = s + kMembers * kk;
+      const rsrc_t rxt = make_rsrc(Xt + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
+      const uint4 v = cload16(rxt, mr < nrows ? (uint32_t)(mr * p.ldx + 4 * pc) * 4u : kOffNone);
+      *reinterpret_cast<uint4*>(xz + kk * Z + 4 * pc) = v;
+    }
+  }
+  // this lane's share of the partial logits (issued before the barrier)
+  float ps = 0.f;
+  if (rowok && a < Nc) {
+    const rsrc_t rp = make_rsrc(p.P, (uint32_t)((long)kMembers * B * Nc * 4));
+    float pv[kMembers];
+#pragma unroll
+    for (int s2 = 0; s2 < kMembers; ++s2)
+      pv[s2] = __uint_as_float(cload4(rp, (uint32_t)(((long)s2 * B + m) * Nc + a) * 4u));
+#pragma unroll
+    for (int s2 = 0; s2 < kMembers; ++s2) ps += pv[s2];
+  }
+  __syncthreads();
+
+  float l = 0.f;
+  if (rowok && a < Nc) {
+    // logit a = b_c + W_c[a, 0:Z] . q(z_t) + (the h part, summed above)
+    const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(Nc * p.ldk * 4));  // uniform resource
+    const uint32_t wrow = (uint32_t)(a * p.ldk) * 4u;
+    const float* zr = xz + k * Z;
+    float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+    for (int kk = 0; kk < Z; kk += 4) {
+      const float4 w = as_float4(bload16(rwc, wrow + (uint32_t)kk * 4u));
+      const float4 xv = *reinterpret_cast<const float4*>(zr + kk);
+      s4.x = fmaf(w.x, xv.x, s4.x);
+      s4.y = fmaf(w.y, xv.y, s4.y);
+      s4.z = fmaf(w.z, xv.z, s4.z);
+      s4.w = fmaf(w.w, xv.w, s4.w);
+    }
+    l = (s4.x + s4.y) + (s4.z + s4.w) + ps + p.bc[a];
+  }
+  lg[k * 128 + a] = l;
+
+  // masked Gumbel-max over the valid actions, lowest index on ties
+  float best = -INFINITY;
+  int bidx = -1;
+  if (!tail && rowok && a < A && p.mask[(long)m * A + a]) {
+    const uint4 w = rng.block((uint32_t)a >> 2, step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
+    best = l + gumbel(word_to_uniform(word_of(w, a & 3)));
+    bidx = a;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ob = __shfl_xor(best, off);
+    const int oi = __shfl_xor(bidx, off);
+    if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) {
+      best = ob;
+      bidx = oi;
+    }
+  }
+  if (lane == 0) {
+    wbest[wave] = best;
+    widx[wave] = bidx;
+  }
+  __syncthreads();
+  if (a == 0 && rowok) {
+    const float ob = wbest[2 * k + 1];
+    const int oi = widx[2 * k + 1];
+    best = wbest[2 * k];
+    bidx = widx[2 * k];
+    if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) bidx = oi;
+    // commit (rows are owned by this work-group for the whole call)
+    const rsrc_t rds = make_rsrc(p.done_state, (uint32_t)B * 4u);
+    int ds = (int)cload4(rds, (uint32_t)m * 4u);
+    if (t > 0) {
+      const rsrc_t rap = make_rsrc(p.actions + (long)(t - 1) * B, (uint32_t)B * 4u);
+      if ((int)cload4(rap, (uint32_t)m * 4u) >= 0) {
+        p.rewards[(long)(t - 1) * B + m] = lg[k * 128 + A];
+        int d = 0;
+        if (p.use_done) {
+          const uint4 w = rng.block(0, step - 1u, p.traj0 + (uint32_t)m, STREAM_DONE);
+          d = sigmoidf(lg[k * 128 + A + 1]) > word_to_uniform(w.x);
+        }
+        p.dones[(long)(t - 1) * B + m] = (uint8_t)d;
+        if (d) ds = 1;
+      }
+    }
+    if (!tail) {
+      int act = bidx;
+      if (ds) act = -1;
+      else if (act < 0) ds = 1;
+      p.actions[(long)t * B + m] = act;
+      if (act < 0) {
+        p.rewards[(long)t * B + m] = 0.f;
+        p.dones[(long)t * B + m] = 1;
+      }
+    }
+    p.done_state[m] = ds;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The kernel.
+// ---------------------------------------------------------------------------
+template <int RB, int NBC, bool NLL>
+__global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  __shared__ int s_flag, s_agent;
+  constexpr int KSPLIT = 4 / NBC;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
+  const int x = blockIdx.x & 7, s = blockIdx.x >> 3;
+  const int r0 = x * p.Bx;
+  const int nrows = min(p.Bx, p.B - r0);
+  if (nrows <= 0) return;  // the whole group leaves
+
+  GroupSync gs{sync_ctr(p, x), sync_err(p), 0u, false};
+  // placement check, settled by the first barrier
+  if (tid == 0 && xcc_id() != (unsigned)x)
+    __hip_atomic_fetch_or(sync_flag(p, x), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  // register-resident weights and state
+  GateState<RB, NBC> st;
+  const int wb = wave % NBC, kp = wave / NBC;
+  const int blk = s * NBC + wb;
+  const int unit = 4 * blk + g;
+  const bool owner = kp == 0;
+  const int nks = p.ldk >> 4;
+  const int nper = (nks + KSPLIT - 1) / KSPLIT;
+  const int sl0 = kp * nper;
+  {
+    const rsrc_t rwg = make_rsrc(p.Wg, (uint32_t)(4 * p.H * p.ldk * 4));
+    const uint32_t rowb = (uint32_t)((16 * blk + r16) * p.ldk) * 4u;
+#pragma unroll
+    for (int i = 0; i < kMaxS; ++i) {
+      const bool ok = i < nper && sl0 + i < nks;
+      st.wr[i] = bload16(rwg, ok ? rowb + (uint32_t)((sl0 + i) * 16 + 4 * g) * 4u : kOffNone);
+    }
+    const rsrc_t rb4 = make_rsrc(p.bg, (uint32_t)(16 * p.H));
+    st.bias = as_float4(bload16(rb4, owner ? (uint32_t)unit * 16u : kOffNone));
+    const rsrc_t rc = make_rsrc(p.c + (long)r0 * p.H, (uint32_t)(nrows * p.H * 4));
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int ml = 16 * rb + r16;
+      st.cst[rb] = __uint_as_float(bload4(rc, owner && ml < nrows ? (uint32_t)(ml * p.H + unit) * 4u : kOffNone));
+    }
+    const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(p.Nc * p.ldk * 4));
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int nbk = wave + 4 * j;
+      const bool ok = !NLL && 16 * nbk < p.Nc && g < NBC;
+      st.wc[j] = bload16(rwc, ok ? (uint32_t)((16 * nbk + r16) * p.ldk + p.Z + 4 * NBC * s + 4 * g) * 4u : kOffNone);
+    }
+  }
+  if constexpr (!NLL) {
+    // unused units of the h block read as zero in the partial-logit MFMA
+    float* hb = reinterpret_cast<float*>(lds + p.off_hb);
+    for (int i = tid; i < 16 * RB * 16; i += 256) hb[i] = 0.f;
+  }
+  if (p.wat_lds) {
+    // this work-group's columns of the one-hot block: [A][NBC blocks][4 units][4 gates]
+    float* wat = reinterpret_cast<float*>(lds + p.off_wat);
+    const int per_a = 16 * NBC;
+    for (int i = tid; i < p.A * per_a; i += 256) {
+      const int aa = i / per_a, r = i % per_a;
+      wat[i] = p.WaT[(long)aa * 4 * p.H + 16 * NBC * s + r];
+    }
+  }
+
+  if (!group_sync(gs, &s_flag)) return;
+  if (tid == 0) s_agent = __hip_atomic_load(sync_flag(p, x), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+  __syncthreads();
+  gs.agent = s_agent != 0;
+
+  if constexpr (!NLL) {
+    // the h part of the step-0 controller logits, from h_0 (X_0, written
+    // before the launch), like every later step's from gates(t-1)
+    if (owner) {
+      float* hb = reinterpret_cast<float*>(lds + p.off_hb);
+      const rsrc_t rx0 = make_rsrc(p.X + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int ml = 16 * rb + r16;
+        if (ml < nrows) hb[ml * 16 + 4 * wb + g] = __uint_as_float(bload4(rx0, (uint32_t)(ml * p.ldx + p.Z + unit) * 4u));
+      }
+    }
+    ctrl_partials<RB, NBC>(p, st, lds, r0, nrows);
+    if (!group_sync(gs, &s_flag)) return;
+  }
+
+  const long BX = (long)p.B * p.ldx;
+  if constexpr (NLL) {
+    for (int t = 0; t < p.T; ++t) {
+      gates_phase<RB, NBC, true>(p, st, lds, t, p.X + (long)t * BX, p.X + (long)(t + 1) * BX, r0, nrows);
+      if (t + 1 < p.T && !group_sync(gs, &s_flag)) return;
+    }
+  } else {
+    for (int t = 0;; ++t) {
+      float* Xt = p.X + (long)(t & 1) * BX;
+      float* Xn = p.X + (long)((t + 1) & 1) * BX;
+      ctrl_phase(p, lds, t, Xt, r0, nrows);
+      if (t == p.T) break;
+      if (!group_sync(gs, &s_flag)) return;
+      gates_phase<RB, NBC, false>(p, st, lds, t, Xt, Xn, r0, nrows);
+      if (!group_sync(gs, &s_flag)) return;
+      mdn_phase(p, lds, t, Xn, r0, nrows);
+      if (!group_sync(gs, &s_flag)) return;
+    }
+    // final cell state for k_rollout_finish
+    if (owner) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int ml = 16 * rb + r16;
+        if (ml < nrows) p.c[(long)(r0 + ml) * p.H + unit] = st.cst[rb];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+constexpr size_t kLdsMax = 160 * 1024 - 64;  // dynamic LDS budget (static flags take the rest)
+constexpr size_t kLdsMin = 81 * 1024;        // above half the CU's LDS: one work-group per CU
+
+bool persist_enabled() {
+  const char* e = std::getenv("WM_PERSISTENT");
+  return !(e && e[0] == '0');
+}
+
+// Row blocks per XCD for B rows (0 = not served by the persistent kernels).
+int persist_rb(int B) {
+  const int bx = (B + kGroups - 1) / kGroups;
+  return bx <= 16 ? 1 : bx <= 32 ? 2 : bx <= 64 ? 4 : 0;
+}
+
+struct PPlan {
+  int rb = 0, nbc = 0;
+  size_t lds = 0;
+  int off_red = 0, off_hb = 0, off_wat = 0, off_mdn = 0, off_ctl = 0, wat_lds = 0;
+};
+
+// The grid must be co-resident with one work-group per CU: 8 XCDs x 32 CUs.
+bool device_fits() {
+  static int cached[64];  // 0 unknown, 1 fits, 2 does not
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+  if (cached[dev] == 0) {
+    int cus = 0;
+    const bool ok = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                    cus == kGrid;
+    cached[dev] = ok ? 1 : 2;
+  }
+  return cached[dev] == 1;
+}
+
+bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
+  if (L.dt != 0) return false;
+  if (L.H != 256 && L.H != 512) return false;
+  if (L.Nc > 128 || L.K > 8) return false;
+  const int rb = persist_rb(B);
+  if (rb == 0) return false;
+  const int nbc = L.H / 128;
+  const int nks = L.ldk / 16;
+  const int nper = (nks + 4 / nbc - 1) / (4 / nbc);
+  if (nper > kMaxS || (L.H / 16 + 3) / 4 > kMaxMS || L.Q > kMaxQ) return false;
+  pl.rb = rb;
+  pl.nbc = nbc;
+  // the mixture-head partial sums and the controller scratch live in other
+  // phases than the gate staging and share its bytes; the h block (zero
+  // padded once) and the one-hot columns persist
+  size_t o = (size_t)nks * rb * 1024;  // staging
+  pl.off_red = (int)o;
+  o += (size_t)(4 - nbc) * rb * 1024;   // K-split partial sums
+  pl.off_mdn = 0;
+  pl.off_ctl = 0;
+  if (!nll) {
+    o = o > (size_t)4 * L.Q * 1024 ? o : (size_t)4 * L.Q * 1024;
+    const size_t ctl = 1088 + (size_t)8 * L.Z;  // logits, wave bests, two latent rows
+    o = o > ctl ? o : ctl;
+  }
+  pl.off_hb = (int)o;
+  if (!nll) o += (size_t)rb * 1024;
+  o = (o + 15) & ~(size_t)15;
+  pl.off_wat = (int)o;
+  const size_t wat = (size_t)L.A * 64 * nbc;
+  if (o + wat <= kLdsMax) {
+    pl.wat_lds = 1;
+    o += wat;
+  }
+  if (o > kLdsMax) return false;
+  pl.lds = o < kLdsMin ? kLdsMin : o;
+  return true;
+}
+
+template <int RB, int NBC, bool NLL>
+hipError_t launch_k(const PArgs& a, size_t lds, hipStream_t s) {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_persist<RB, NBC, NLL>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  return launch(NLL ? "nll_persist" : "persist", k_persist<RB, NBC, NLL>, dim3(kGrid), dim3(256), lds, s, a);
+}
+
+template <bool NLL>
+hipError_t launch_plan(const PArgs& a, const PPlan& pl, hipStream_t s) {
+  switch (pl.rb * 8 + pl.nbc) {
+    case 1 * 8 + 2: return launch_k<1, 2, NLL>(a, pl.lds, s);
+    case 1 * 8 + 4: return launch_k<1, 4, NLL>(a, pl.lds, s);
+    case 2 * 8 + 2: return launch_k<2, 2, NLL>(a, pl.lds, s);
+    case 2 * 8 + 4: return launch_k<2, 4, NLL>(a, pl.lds, s);
+    case 4 * 8 + 2: return launch_k<4, 2, NLL>(a, pl.lds, s);
+    case 4 * 8 + 4: return launch_k<4, 4, NLL>(a, pl.lds, s);
+    default: return hipErrorNotSupported;
+  }
+}
+
+PArgs base_args(const Packed& P, const PPlan& pl, int B, int T) {
+  const Layout& L = P.L;
+  const char* base = reinterpret_cast<const char*>(P.base);
+  PArgs a{};
+  a.Wg = reinterpret_cast<const float*>(base + L.off_Wg);
+  a.WaT = reinterpret_cast<const float*>(base + L.off_WaT);
+  a.bg = reinterpret_cast<const float*>(base + L.off_bg);
+  a.Wm = reinterpret_cast<const float*>(base + L.off_Wm);
+  a.bm = reinterpret_cast<const float*>(base + L.off_bm);
+  a.Wc = reinterpret_cast<const float*>(base + L.off_Wc);
+  a.bc = reinterpret_cast<const float*>(base + L.off_bc);
+  a.Z = L.Z; a.H = L.H; a.A = L.A; a.K = L.K; a.Q = L.Q; a.Nc = L.Nc;
+  a.ldk = L.ldk; a.ldh = L.ldh; a.ldx = L.ldx;
+  a.B = B; a.T = T; a.Bx = (B + kGroups - 1) / kGroups;
+  a.wat_lds = pl.wat_lds;
+  a.off_red = pl.off_red; a.off_hb = pl.off_hb; a.off_wat = pl.off_wat;
+  a.off_mdn = pl.off_mdn; a.off_ctl = pl.off_ctl;
+  return a;
+}
+
+}  // namespace
+
+size_t persist_partial_bytes(const Layout& L, int B) {
+  PPlan pl;
+  if (!plan(L, B, false, pl)) return 0;
+  return (size_t)kMembers * B * L.Nc * 4;
+}
+
+bool persist_usable(const Layout& L, int B, bool nll) {
+  PPlan pl;
+  return persist_enabled() && plan(L, B, nll, pl) && device_fits();
+}
+
+hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStream_t s) {
+  PPlan pl;
+  if (!persist_enabled() || !plan(P.L, R.B, false, pl) || !R.P || !R.sync || !device_fits())
+    return hipErrorNotSupported;
+  PArgs a = base_args(P, pl, R.B, R.T);
+  a.k0 = R.k0; a.k1 = R.k1; a.traj0 = R.traj0; a.step0 = R.step0;
+  a.tau = R.tau;
+  a.use_done = (R.flags & 1u) != 0;
+  a.X = reinterpret_cast<float*>(R.x);
+  a.c = R.c;
+  a.done_state = R.done_state;
+  a.P = R.P;
+  a.sync = R.sync;
+  a.mask = R.mask;
+  a.z_out = R.z_out;
+  a.actions = R.actions;
+  a.rewards = R.rewards;
+  a.dones = R.dones;
+  const bool trace = (R.flags & 2u) != 0;
+  a.h_trace = trace ? R.h_trace : nullptr;
+  a.c_trace = trace ? R.c_trace : nullptr;
+  return launch_plan<false>(a, pl, s);
+}
+
+hipError_t launch_nll_persist(const Packed& P, const NllBufs& N, hipStream_t s) {
+  PPlan pl;
+  if (!persist_enabled() || !plan(P.L, N.B, true, pl) || !N.sync || !device_fits())
+    return hipErrorNotSupported;
+  PArgs a = base_args(P, pl, N.B, N.T);
+  a.X = reinterpret_cast<float*>(N.x);
+  a.c = N.c;
+  a.sync = N.sync;
+  a.actions = const_cast<int32_t*>(N.actions);
+  return launch_plan<true>(a, pl, s);
+}
+
+}  // namespace wm

@@ -30,7 +30,7 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-KERNEL_SOURCES = ["wm_kernels.hip", "wm_device.h", "wm_kernels.h", "wm_layout.h"]
+KERNEL_SOURCES = ["wm_kernels.hip", "wm_persist.hip", "wm_device.h", "wm_kernels.h", "wm_layout.h"]
 CALIB_BYTES = 256 << 20
 
 

@@ -1,0 +1,260 @@
+"""GPU parity of the persistent single-launch kernels (fp32, H of 256 or 512,
+up to 512 rows) against the oracle, and against the multi-launch path.
+
+The library takes the persistent path by itself when the dims and the batch
+allow it; WM_PERSISTENT=0 in the environment switches it off, which these
+tests use to run both paths on the same inputs in one process.  Cases cover
+ragged batches (rows per XCD from 1 to 64, XCD groups without rows), one and
+two K parts per gate block, K = 1 .. 8 (one to six mixture output blocks),
+A = 1 .. 126, frozen and resumed rows, empty masks, traces and the NLL
+recurrence with padding and out-of-range actions.
+"""
+
+import os
+import sys
+from contextlib import contextmanager
+
+import numpy as np
+import pytest
+import torch
+
+import parity
+from oracle import wm as owm
+from paper_2205_01435_amd import _lib as wmlib
+from paper_2205_01435_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+KEYS = ("z_out", "actions", "rewards", "dones", "h_T", "c_T", "h_trace", "c_trace")
+
+
+def say(*a):
+    print("[gpu-persist]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    wmlib.load()
+    yield
+
+
+@contextmanager
+def launch_path():
+    """Run the multi-launch path (persistent kernels off)."""
+    old = os.environ.get("WM_PERSISTENT")
+    os.environ["WM_PERSISTENT"] = "0"
+    try:
+        yield
+    finally:
+        if old is None:
+            del os.environ["WM_PERSISTENT"]
+        else:
+            os.environ["WM_PERSISTENT"] = old
+
+
+def _t(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def _np(b, extra=None):
+    out = {k: getattr(b, k).cpu().numpy() for k in KEYS if getattr(b, k) is not None}
+    return out
+
+
+def _case(B, Z, H, A, K, seed, mask_p=0.4):
+    w = wl.Workload("p", "rollout", B=B, T=4, Z=Z, H=H, A=A, K=K, dtype="fp32", seed=seed,
+                    mask_p=mask_p)
+    inp = wl.make_rollout_inputs(w)
+    rng = np.random.default_rng(seed)
+    for k in ("b_g", "b_m", "b_c"):
+        inp["weights"][k] = (0.3 * rng.standard_normal(inp["weights"][k].shape)).astype(np.float32)
+    return w, inp
+
+
+def _persist_launches(fn):
+    wmlib.profile_reset()
+    wmlib.profile_enable("")
+    try:
+        out = fn()
+        torch.cuda.synchronize()
+        _, n = wmlib.profile_read("persist")
+        _, n_nll = wmlib.profile_read("nll_persist")
+    finally:
+        wmlib.profile_enable(None)
+        wmlib.profile_reset()
+    return out, n, n_nll
+
+
+# (B, T, Z, H, A, K): rows per XCD 1 .. 64, ldk up to 576 (36 K slices)
+ROLL = [
+    (5, 3, 8, 256, 1, 1),      # 1 row per XCD, three XCDs without rows, one action
+    (16, 6, 32, 256, 32, 5),   # the tiny workload's dims
+    (37, 5, 24, 512, 37, 3),
+    (100, 4, 64, 256, 126, 8),  # A + 2 = 128 controller rows, six mixture blocks
+    (257, 3, 64, 512, 64, 5),  # 33 rows per XCD: four row blocks
+    (300, 3, 32, 256, 20, 2),  # two K parts per gate block, four row blocks
+    (512, 3, 64, 512, 64, 5),  # the largest batch served
+]
+
+
+@pytest.mark.parametrize("B,T,Z,H,A,K", ROLL)
+def test_persistent_rollout_vs_oracle_and_launch_path(B, T, Z, H, A, K):
+    say("rollout", B, T, Z, H, A, K)
+    w, inp = _case(B, Z, H, A, K, seed=B + 3)
+    mask = inp["mask"].copy()
+    mask[B // 2] = 0  # a row without a valid action
+    m = wmlib.pack(inp["weights"], Z, H, A, K, "fp32")
+    args = dict(T=T, seed=17, tau=1.3, done=True, trace=True, step0=2, traj0=11)
+    b, n, _ = _persist_launches(lambda: wmlib.rollout(m, _t(inp["z0"]), _t(mask), **args))
+    assert n == 1, "the persistent kernel did not run"
+    g = _np(b)
+    with launch_path():
+        r, n2, _ = _persist_launches(lambda: wmlib.rollout(m, _t(inp["z0"]), _t(mask), **args))
+    assert n2 == 0
+    gl = _np(r)
+    ties, live = parity.reanchored(w.dims, inp["weights"], mask, g, seed=17, tau=1.3,
+                                   done_flag=True, dtype="fp32", traj=11 + np.arange(B), step0=2)
+    say("ties", ties.mismatches, "of", ties.draws, "live", live)
+    ref = owm.rollout(inp["weights"], w.dims, inp["z0"], mask, T=T, seed=17, tau=1.3,
+                      done_flag=True, dtype="fp32", step0=2, traj0=11)
+    assert parity.free_run(ref, g, "fp32", T) <= max(1, 1e-3 * B * T * (Z + 2))
+    assert g["actions"][0, B // 2] == -1 and np.all(g["dones"][:, B // 2] == 1)
+    # the two device paths agree except where the oracle's own free run diverges
+    same = np.all(g["actions"] == gl["actions"], axis=0)
+    assert same.mean() >= 0.99
+    parity.close(g["z_out"][:, same], gl["z_out"][:, same], 1e-4, "z_out vs launch path")
+    parity.close(g["h_T"][same], gl["h_T"][same], 1e-4, "h_T vs launch path")
+
+
+def test_persistent_rollout_workloads_match_launch_path():
+    """tiny and medium workloads: both device paths against each other."""
+    for name in ("tiny_rollout", "medium_rollout"):
+        w = wl.WORKLOADS[name]
+        inp = wl.make_rollout_inputs(w)
+        m = wmlib.pack(inp["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+        run = lambda: _np(wmlib.rollout(m, _t(inp["z0"]), _t(inp["mask"]), T=w.T,  # noqa: E731
+                                        seed=w.seed, tau=w.tau, done=w.done))
+        (g, n, _) = _persist_launches(run)
+        assert n == 1
+        with launch_path():
+            gl = run()
+        same = np.all(g["actions"] == gl["actions"], axis=0)
+        say(name, "trajectories identical on both paths:", same.mean())
+        assert same.mean() >= 0.99
+        parity.close(g["z_out"][:, same], gl["z_out"][:, same], 1e-4, name + " z_out")
+
+
+def test_persistent_resume_state_inputs_and_determinism():
+    """rollout(T1) + rollout(T2, step0 = T1, state) == rollout(T1 + T2), with
+    initial state and done flags given, run to run bit-exact, batch subsets."""
+    w, inp = _case(120, 32, 256, 24, 4, seed=5)
+    m = wmlib.pack(inp["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+    rng = np.random.default_rng(3)
+    h0 = np.tanh(rng.standard_normal((120, 256))).astype(np.float32)
+    c0 = rng.standard_normal((120, 256)).astype(np.float32)
+    done0 = (rng.random(120) < 0.2).astype(np.uint8)
+    z0, mask = _t(inp["z0"]), _t(inp["mask"])
+
+    def full_run():
+        dio = _t(done0)
+        b = wmlib.rollout(m, z0, mask, T=7, seed=4, done=True, h0=_t(h0), c0=_t(c0), done_io=dio,
+                          step0=1, traj0=9)
+        torch.cuda.synchronize()
+        return _np(b), dio.cpu().numpy()
+
+    full, dfull = full_run()
+    again, _ = full_run()
+    for k in full:
+        np.testing.assert_array_equal(full[k], again[k], err_msg=f"run-to-run {k}")
+    dio = _t(done0)
+    a = wmlib.rollout(m, z0, mask, T=3, seed=4, done=True, h0=_t(h0), c0=_t(c0), done_io=dio,
+                      step0=1, traj0=9)
+    torch.cuda.synchronize()
+    na = _np(a)
+    b = wmlib.rollout(m, a.z_out[3].contiguous(), mask, T=4, seed=4, done=True, step0=4, traj0=9,
+                      h0=a.h_T, c0=a.c_T, done_io=dio)
+    torch.cuda.synchronize()
+    nb = _np(b)
+    for k in ("actions", "rewards", "dones"):
+        np.testing.assert_array_equal(np.concatenate([na[k], nb[k]]), full[k], err_msg=k)
+    np.testing.assert_array_equal(np.concatenate([na["z_out"], nb["z_out"][1:]]), full["z_out"])
+    np.testing.assert_array_equal(nb["h_T"], full["h_T"])
+    np.testing.assert_array_equal(nb["c_T"], full["c_T"])
+    np.testing.assert_array_equal(dio.cpu().numpy(), dfull)
+    pre = done0 != 0
+    assert np.all(full["actions"][:, pre] == -1) and np.all(full["dones"][:, pre] == 1)
+    np.testing.assert_array_equal(full["h_T"][pre], h0[pre])
+    np.testing.assert_array_equal(full["c_T"][pre], c0[pre])
+    ref = owm.rollout(inp["weights"], w.dims, inp["z0"], inp["mask"], T=7, seed=4, done_flag=True,
+                      h0=h0, c0=c0, done0=done0, step0=1, traj0=9)
+    assert parity.free_run(ref, full, "fp32", 7) <= 1
+    # a row subset with its trajectory offset reproduces those rows
+    lo, hi = 17, 83
+    sub = _np(wmlib.rollout(m, _t(inp["z0"][lo:hi]), _t(inp["mask"][lo:hi]), T=7, seed=4,
+                            done=True, h0=_t(h0[lo:hi]), c0=_t(c0[lo:hi]), done_io=_t(done0[lo:hi]),
+                            step0=1, traj0=9 + lo))
+    for k in ("actions", "dones", "rewards", "z_out"):
+        np.testing.assert_array_equal(sub[k], full[k][:, lo:hi], err_msg=f"subset {k}")
+
+
+def test_persistent_no_done_flag():
+    w, inp = _case(64, 16, 256, 9, 2, seed=8)
+    mask = inp["mask"].copy()
+    mask[[0, 40]] = 0
+    m = wmlib.pack(inp["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+    g, n, _ = _persist_launches(lambda: _np(wmlib.rollout(m, _t(inp["z0"]), _t(mask), T=5, seed=2,
+                                                          done=False)))
+    assert n == 1
+    live = np.ones(64, bool)
+    live[[0, 40]] = False
+    assert np.all(g["dones"][:, live] == 0) and np.all(g["actions"][:, live] >= 0)
+    assert np.all(g["actions"][:, ~live] == -1) and np.all(g["dones"][:, ~live] == 1)
+    ref = owm.rollout(inp["weights"], w.dims, inp["z0"], mask, T=5, seed=2, done_flag=False)
+    assert parity.free_run(ref, g, "fp32", 5) <= 1
+
+
+# (B, T, Z, H, A, K)
+NLL = [
+    (5, 7, 8, 256, 3, 1),
+    (45, 9, 24, 512, 13, 3),
+    (300, 6, 64, 256, 64, 5),
+    (512, 4, 64, 512, 64, 5),
+]
+
+
+@pytest.mark.parametrize("B,T,Z,H,A,K", NLL)
+def test_persistent_nll_recurrence(B, T, Z, H, A, K):
+    say("nll", B, T, Z, H, A, K)
+    w = wl.Workload("n", "nll", B=B, T=T, Z=Z, H=H, A=A, K=K, dtype="fp32", seed=B)
+    d = wl.make_nll_inputs(w)
+    acts = d["actions"].copy()
+    acts[0, :3] = [-1, A, 10 ** 6]  # outside [0, A): zero one-hot
+    lengths = np.random.default_rng(1).integers(0, T + 1, size=B).astype(np.int32)
+    lengths[:3] = [0, T, T + 5]
+    m = wmlib.pack(d["weights"], Z, H, A, K, "fp32")
+    run = lambda: wmlib.nll(m, _t(d["z"]), _t(acts), _t(d["rewards"]), _t(d["dones"]),  # noqa: E731
+                            lengths=_t(lengths))
+    b, _, n = _persist_launches(run)
+    assert n == 1, "the persistent recurrence did not run"
+    ref = owm.nll(d["weights"], w.dims, d["z"], acts, d["rewards"], d["dones"], lengths=lengths)
+    for k in ("loglik", "reward_se", "done_bce"):
+        parity.close(getattr(b, k).cpu().numpy(), ref[k], 1e-4, k)
+    parity.close(b.means.cpu().numpy(), ref["means"], 1e-4, "means")
+    with launch_path():
+        bl, _, n2 = _persist_launches(run)
+    assert n2 == 0
+    parity.close(b.loglik.cpu().numpy(), bl.loglik.cpu().numpy(), 1e-4, "loglik vs launch path")
+
+
+def test_persistent_not_taken_outside_its_range():
+    """bf16, H outside {256, 512}, more than 512 rows or more than 36 K slices
+    per wave run on the multi-launch path."""
+    for (B, Z, H, A, K, dt) in [(64, 16, 256, 8, 2, "bf16"), (64, 16, 128, 8, 2, "fp32"),
+                                (520, 16, 256, 8, 2, "fp32"), (32, 72, 512, 8, 2, "fp32")]:
+        w, inp = _case(B, Z, H, A, K, seed=1)
+        m = wmlib.pack(inp["weights"], Z, H, A, K, dt)
+        _, n, _ = _persist_launches(lambda: wmlib.rollout(m, _t(inp["z0"]), _t(inp["mask"]), T=2,
+                                                          seed=1))
+        assert n == 0, (B, Z, H, dt)
