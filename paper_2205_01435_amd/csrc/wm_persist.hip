@@ -65,7 +65,7 @@ struct PArgs {
   int B, T, Bx;
   uint32_t k0, k1, traj0, step0;
   float tau;
-  int use_done, wat_lds;
+  int use_done, wat_lds, wcz_lds;
   float* X;             // rollout [2, B, ldx]; NLL [T+1, B, ldx]
   float* c;             // [B, H]: initial cell state in, final state out (rollout)
   int32_t* done_state;  // [B]
@@ -78,7 +78,7 @@ struct PArgs {
   uint8_t* dones;
   float *h_trace, *c_trace;  // [T+1, B, H] or null
   // LDS carve-up (bytes)
-  int off_red, off_hb, off_wat, off_mdn, off_ctl;
+  int off_red, off_hb, off_wat, off_wcz, off_mdn, off_ctl, off_flags;
 };
 
 // sync words: group counters at 64*x, placement flags at 64*(8+x), error at 64*16
@@ -236,32 +236,36 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   }
 
   // stage X_in rows [r0, r0 + nrows), columns [0, ldk) into LDS as
-  // [slice][row block][16 rows][16 floats]; instruction order: chunk, K part,
-  // slice, row block, dealt round-robin to the waves
+  // [slice][row block][16 rows][16 floats], in four chunks of local K slices.
+  // Chunk c's LDS-DMA instructions, ordered (K part, slice, row block), are
+  // dealt round-robin to the waves.  Chunk 0 goes out first; the loads of
+  // chunk c+1 are then spread between the MFMAs of chunk c, so that the MFMA
+  // pipe keeps running while they stream in.
+  static_assert(KSPLIT <= 2, "one or two K parts per gate block");
   const u32x4 rsx = rsrc_words(Xin + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
   const uint32_t lds0 = lds_addr(lds);
   const uint32_t ldxb = (uint32_t)p.ldx * 4u;
   const int rbv = (nrows + 15) >> 4;  // row blocks holding valid rows
-  int mine[4] = {0, 0, 0, 0};
-  int jj = 0;
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    // the 32 work-groups of an XCD read the same rows: each starts its chunk
-    // at a different slice so that they do not all hit the same L2 lines
-    const int len = min(9, nper - 9 * c);
-    for (int kq = 0; kq < KSPLIT; ++kq) {
-      for (int ii = 0; ii < len; ++ii) {
-        const int i = 9 * c + (ii + s) % len;
-        const int sl = kq * nper + i;
-        if (sl >= nks) continue;
-        for (int rb = 0; rb < rbv; ++rb, ++jj) {
-          if ((jj & 3) != wave) continue;
-          const uint32_t voff = (uint32_t)(16 * rb + (lane >> 2)) * ldxb + (uint32_t)sl * 64u + (uint32_t)(lane & 3) * 16u;
-          cdma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
-          ++mine[c];
-        }
-      }
+  auto valid_in = [&](int c, int kq) { return max(0, min(min(9, nper - 9 * c), nks - kq * nper - 9 * c)); };
+  auto wave_count = [&](int c) {
+    int n = valid_in(c, 0) * rbv;
+    if (KSPLIT > 1) n += valid_in(c, 1) * rbv;
+    return n > wave ? (n - wave + 3) >> 2 : 0;
+  };
+  auto issue = [&](int c, int k) {
+    int r = wave + 4 * k, kq = 0;
+    const int n0 = valid_in(c, 0) * rbv;
+    if (KSPLIT > 1 && r >= n0) {
+      kq = 1;
+      r -= n0;
     }
+    const int sl = kq * nper + 9 * c + r / rbv, rb = r % rbv;
+    const uint32_t voff = (uint32_t)(16 * rb + (lane >> 2)) * ldxb + (uint32_t)sl * 64u + (uint32_t)(lane & 3) * 16u;
+    cdma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
+  };
+  {
+    const int n0 = wave_count(0);
+    for (int k = 0; k < n0; ++k) issue(0, k);
   }
 
   // two accumulator sets (even and odd K slices) and RB row blocks give
@@ -269,14 +273,14 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   f32x4 acc2[2][RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) acc2[0][rb] = acc2[1][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  int later = mine[0] + mine[1] + mine[2] + mine[3];
   const int nval = min(nper, nks - sl0);  // this wave's valid K slices (uniform)
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
-    later -= mine[c];
-    vm_wait_n(later);
+    vm_wait<0>();  // this wave's loads of chunk c (the only ones in flight)
     __builtin_amdgcn_s_barrier();
     asm volatile("" : : : "memory");
+    const int nn = c < 3 ? wave_count(c + 1) : 0;
+    int kk = 0;  // next load of chunk c+1 to issue
     const char* sb0 = lds + sl0 * RB * 1024 + 64 * r16 + 16 * g;
     if (9 * c + 9 <= nval && rbv == RB) {
       // whole chunk, every row block: straight-line MFMAs, slices in pairs
@@ -296,6 +300,8 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
             mfma4(acc2[i & 1][rb], st.wr[i], b0[rb], v);
             if (two) mfma4(acc2[(i + 1) & 1][rb], st.wr[i + 1], b1[rb], v);
           }
+        const int upto = ((i - 9 * c + (two ? 2 : 1)) * nn + 8) / 9;
+        for (; kk < upto; ++kk) issue(c + 1, kk);
       }
     } else {
 #pragma unroll
@@ -306,6 +312,8 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
             if (rb < rbv)
               Mfma<float>::step(acc2[i & 1][rb], st.wr[i], *reinterpret_cast<const uint4*>(sb0 + (i * RB + rb) * 1024));
         }
+        const int upto = ((i - 9 * c + 1) * nn + 8) / 9;
+        for (; kk < upto; ++kk) issue(c + 1, kk);
       }
     }
   }
@@ -512,18 +520,32 @@ __device__ __forceinline__ void ctrl_phase(const PArgs& p, char* lds, int t, con
   float l = 0.f;
   if (rowok && a < Nc) {
     // logit a = b_c + W_c[a, 0:Z] . q(z_t) + (the h part, summed above)
-    const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(Nc * p.ldk * 4));  // uniform resource
-    const uint32_t wrow = (uint32_t)(a * p.ldk) * 4u;
     const float* zr = xz + k * Z;
     float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (p.wcz_lds) {
+      // W_c[:, 0:Z] resident in LDS as [Z/4][Nc][4]
+      const float4* wz = reinterpret_cast<const float4*>(lds + p.off_wcz);
 #pragma unroll 8
-    for (int kk = 0; kk < Z; kk += 4) {
-      const float4 w = as_float4(bload16(rwc, wrow + (uint32_t)kk * 4u));
-      const float4 xv = *reinterpret_cast<const float4*>(zr + kk);
-      s4.x = fmaf(w.x, xv.x, s4.x);
-      s4.y = fmaf(w.y, xv.y, s4.y);
-      s4.z = fmaf(w.z, xv.z, s4.z);
-      s4.w = fmaf(w.w, xv.w, s4.w);
+      for (int kk = 0; kk < Z; kk += 4) {
+        const float4 w = wz[(kk >> 2) * Nc + a];
+        const float4 xv = *reinterpret_cast<const float4*>(zr + kk);
+        s4.x = fmaf(w.x, xv.x, s4.x);
+        s4.y = fmaf(w.y, xv.y, s4.y);
+        s4.z = fmaf(w.z, xv.z, s4.z);
+        s4.w = fmaf(w.w, xv.w, s4.w);
+      }
+    } else {
+      const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(Nc * p.ldk * 4));  // uniform resource
+      const uint32_t wrow = (uint32_t)(a * p.ldk) * 4u;
+#pragma unroll 8
+      for (int kk = 0; kk < Z; kk += 4) {
+        const float4 w = as_float4(bload16(rwc, wrow + (uint32_t)kk * 4u));
+        const float4 xv = *reinterpret_cast<const float4*>(zr + kk);
+        s4.x = fmaf(w.x, xv.x, s4.x);
+        s4.y = fmaf(w.y, xv.y, s4.y);
+        s4.z = fmaf(w.z, xv.z, s4.z);
+        s4.w = fmaf(w.w, xv.w, s4.w);
+      }
     }
     l = (s4.x + s4.y) + (s4.z + s4.w) + ps + p.bc[a];
   }
@@ -592,8 +614,12 @@ __device__ __forceinline__ void ctrl_phase(const PArgs& p, char* lds, int t, con
 // ---------------------------------------------------------------------------
 template <int RB, int NBC, bool NLL>
 __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
-  extern __shared__ __attribute__((aligned(16))) char lds[];
-  __shared__ int s_flag, s_agent;
+  // no static LDS: the dynamic region starts at LDS address 0, so that the
+  // 1 KB LDS-DMA destinations are 1 KB aligned (misaligned ones run several
+  // times slower); the two flags live in the last 64 bytes of the region
+  extern __shared__ __attribute__((aligned(1024))) char lds[];
+  int& s_flag = *reinterpret_cast<int*>(lds + p.off_flags);
+  int& s_agent = *reinterpret_cast<int*>(lds + p.off_flags + 4);
   constexpr int KSPLIT = 4 / NBC;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
   const int x = blockIdx.x & 7, s = blockIdx.x >> 3;
@@ -643,6 +669,14 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
     // unused units of the h block read as zero in the partial-logit MFMA
     float* hb = reinterpret_cast<float*>(lds + p.off_hb);
     for (int i = tid; i < 16 * RB * 16; i += 256) hb[i] = 0.f;
+  }
+  if (!NLL && p.wcz_lds) {
+    // the controller's z columns, W_c[:, 0:Z], as [Z/4][Nc][4]
+    float4* wz = reinterpret_cast<float4*>(lds + p.off_wcz);
+    for (int i = tid; i < (p.Z >> 2) * p.Nc; i += 256) {
+      const int q4 = i / p.Nc, aa = i % p.Nc;
+      wz[i] = *reinterpret_cast<const float4*>(p.Wc + (long)aa * p.ldk + 4 * q4);
+    }
   }
   if (p.wat_lds) {
     // this work-group's columns of the one-hot block: [A][NBC blocks][4 units][4 gates]
@@ -707,7 +741,7 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-constexpr size_t kLdsMax = 160 * 1024 - 64;  // dynamic LDS budget (static flags take the rest)
+constexpr size_t kLdsMax = 160 * 1024 - 64;  // LDS budget below the flags
 constexpr size_t kLdsMin = 81 * 1024;        // above half the CU's LDS: one work-group per CU
 
 bool persist_enabled() {
@@ -724,7 +758,8 @@ int persist_rb(int B) {
 struct PPlan {
   int rb = 0, nbc = 0;
   size_t lds = 0;
-  int off_red = 0, off_hb = 0, off_wat = 0, off_mdn = 0, off_ctl = 0, wat_lds = 0;
+  int off_red = 0, off_hb = 0, off_wat = 0, off_wcz = 0, off_mdn = 0, off_ctl = 0, off_flags = 0;
+  int wat_lds = 0, wcz_lds = 0;
 };
 
 // The grid must be co-resident with one work-group per CU: 8 XCDs x 32 CUs.
@@ -775,8 +810,17 @@ bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
     pl.wat_lds = 1;
     o += wat;
   }
+  o = (o + 15) & ~(size_t)15;
+  pl.off_wcz = (int)o;
+  const size_t wcz = (size_t)L.Nc * L.Z * 4;
+  if (!nll && o + wcz <= kLdsMax) {
+    pl.wcz_lds = 1;
+    o += wcz;
+  }
   if (o > kLdsMax) return false;
-  pl.lds = o < kLdsMin ? kLdsMin : o;
+  o = o < kLdsMin ? kLdsMin : o;
+  pl.off_flags = (int)((o + 15) & ~(size_t)15);
+  pl.lds = (size_t)pl.off_flags + 64;
   return true;
 }
 
@@ -816,8 +860,10 @@ PArgs base_args(const Packed& P, const PPlan& pl, int B, int T) {
   a.ldk = L.ldk; a.ldh = L.ldh; a.ldx = L.ldx;
   a.B = B; a.T = T; a.Bx = (B + kGroups - 1) / kGroups;
   a.wat_lds = pl.wat_lds;
+  a.wcz_lds = pl.wcz_lds;
+  a.off_wcz = pl.off_wcz;
   a.off_red = pl.off_red; a.off_hb = pl.off_hb; a.off_wat = pl.off_wat;
-  a.off_mdn = pl.off_mdn; a.off_ctl = pl.off_ctl;
+  a.off_mdn = pl.off_mdn; a.off_ctl = pl.off_ctl; a.off_flags = pl.off_flags;
   return a;
 }
 
