@@ -21,6 +21,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "wm_device.h"
 #include "wm_kernels.h"
 #include "wm_profile.h"
@@ -381,6 +383,9 @@ struct GemmD {
   }
 };
 
+// Static LDS a work-group may hold on gfx950 (160 KB per CU).
+constexpr int kLdsStatic = 160 * 1024;
+
 // Work-group -> tile mapping.  Work-groups are dispatched round-robin over
 // the eight XCDs, each with its own L2.  The XCDs form a gn x (8 / gn) grid
 // over (weight-row tiles, activation-row tiles): XCD x owns a contiguous
@@ -618,18 +623,23 @@ struct Gate4IO {
 
 // Gate kernel on the pipelined cores.  The GEMM tile is staged through LDS
 // as E[row][feature] (fp32) and the epilogue then runs with thread t on the
-// four-unit group t % GPR of rows t / GPR, t / GPR + RSTEP, ...
+// four-unit group t % GPR of rows t / GPR, t / GPR + RSTEP, ...  A tile
+// whose fp32 copy does not fit the LDS is staged in NPASS passes, one row of
+// waves (PROWS tile rows) at a time.
 template <class C>
 __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
   using DT = typename C::DT;
   constexpr int NBW = C::NBW, MBW = C::MBW;
   constexpr int GPR = C::BN / 16;          // groups of four units per tile row
   constexpr int RSTEP = C::NT / GPR;       // rows per pass of the block
-  constexpr int IPT = (C::BM + RSTEP - 1) / RSTEP;
   constexpr int ELD = C::BN + 4;           // staged row stride (floats)
-  constexpr int E_BYTES = C::BM * ELD * 4;
+  constexpr int NPASS = C::BM * ELD * 4 <= kLdsStatic ? 1 : C::WAVES_M;
+  constexpr int PROWS = C::BM / NPASS;     // tile rows staged per pass
+  constexpr int IPT = (PROWS + RSTEP - 1) / RSTEP;
+  constexpr int E_BYTES = PROWS * ELD * 4;
   constexpr int LDS = C::LDS_BYTES > E_BYTES ? C::LDS_BYTES : E_BYTES;
   static_assert(C::NT % GPR == 0, "whole groups per block");
+  static_assert(NPASS == 1 || (E_BYTES <= kLdsStatic && C::KSPLIT == 1), "staged passes");
   __shared__ __attribute__((aligned(16))) char lds_raw[LDS];
   int nt, mt;
   if (!tile_of(p.map, nt, mt)) return;
@@ -637,48 +647,55 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
   const int grp = threadIdx.x % GPR, r0 = threadIdx.x / GPR;
   const int u0 = n0 / 4 + 4 * grp;
   // actions of this thread's epilogue rows, fetched ahead of the GEMM
-  int act[IPT];
+  int act[NPASS][IPT];
 #pragma unroll
-  for (int k = 0; k < IPT; ++k) {
-    const int r = r0 + k * RSTEP, m = m0 + r;
-    act[k] = (r < C::BM && m < p.M) ? p.act[m] : -1;
-  }
+  for (int ps = 0; ps < NPASS; ++ps)
+#pragma unroll
+    for (int k = 0; k < IPT; ++k) {
+      const int r = r0 + k * RSTEP, m = m0 + ps * PROWS + r;
+      act[ps][k] = (r < PROWS && m < p.M) ? p.act[m] : -1;
+    }
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wg), p.ldk, p.ldk, n0, C::BN, 4 * p.H);
   const SrcX<DT> x(reinterpret_cast<const DT*>(p.x_in), p.ldx, p.ldx, m0, C::BM, p.M);
   f32x4 acc[NBW][MBW];
   C::run(acc, w, x, (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
 
   float* E = reinterpret_cast<float*>(lds_raw);
-  if (C::kw() == 0) {
-    const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
-    const int wn = C::wn(), wmi = C::wm();
-#pragma unroll
-    for (int j = 0; j < MBW; ++j)
-#pragma unroll
-      for (int i = 0; i < NBW; ++i)
-        *reinterpret_cast<f32x4*>(E + ((wmi * MBW + j) * 16 + r16) * ELD + (wn * NBW + i) * 16 + 4 * g) =
-            acc[i][j];
-  }
-  __syncthreads();
-
   const Gate4IO<DT> io(p, m0, C::BM);
   const bool uok = u0 < p.H;  // H % 16 == 0: the whole group is inside
   float4 b[4];
   io.bias(u0, uok, b);
-  Gate4In in[IPT];
 #pragma unroll
-  for (int k = 0; k < IPT; ++k) {
-    const int r = r0 + k * RSTEP;
-    in[k] = io.load(r, u0, act[k], uok && r < C::BM && m0 + r < p.M, b);
-  }
+  for (int ps = 0; ps < NPASS; ++ps) {
+    if (ps > 0) __syncthreads();  // the previous pass has read E
+    if (C::kw() == 0 && (NPASS == 1 || C::wm() == ps)) {
+      const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+      const int wn = C::wn(), wmi = NPASS == 1 ? C::wm() : 0;
 #pragma unroll
-  for (int k = 0; k < IPT; ++k) {
-    const int r = r0 + k * RSTEP;
-    if (r >= C::BM) continue;
-    float4 gsum[4];
+      for (int j = 0; j < MBW; ++j)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) gsum[t] = *reinterpret_cast<const float4*>(E + r * ELD + 16 * grp + 4 * t);
-    io.commit(r, u0, uok && m0 + r < p.M, in[k], gsum);
+        for (int i = 0; i < NBW; ++i)
+          *reinterpret_cast<f32x4*>(E + ((wmi * MBW + j) * 16 + r16) * ELD + (wn * NBW + i) * 16 + 4 * g) =
+              acc[i][j];
+    }
+    __syncthreads();
+
+    const int rp = ps * PROWS;  // first tile row of the pass
+    Gate4In in[IPT];
+#pragma unroll
+    for (int k = 0; k < IPT; ++k) {
+      const int r = r0 + k * RSTEP;
+      in[k] = io.load(rp + r, u0, act[ps][k], uok && r < PROWS && m0 + rp + r < p.M, b);
+    }
+#pragma unroll
+    for (int k = 0; k < IPT; ++k) {
+      const int r = r0 + k * RSTEP;
+      if (r >= PROWS) continue;
+      float4 gsum[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) gsum[t] = *reinterpret_cast<const float4*>(E + r * ELD + 16 * grp + 4 * t);
+      io.commit(rp + r, u0, uok && m0 + rp + r < p.M, in[k], gsum);
+    }
   }
 }
 
@@ -1648,10 +1665,14 @@ template <typename DT> struct Cfgs;
 template <> struct Cfgs<float> {
   using GatesSmall = Gemm<float, 2, 1, 2, 2, 1, 32, 4>;  // 64 x 32
   using GatesLarge = GemmD<float, 4, 2, 2, 2, 2>;  // 128 x 64
+  using GatesXL = GatesLarge;
+  template <int Q> using MdnXL = GemmD<float, Q, WM_MDN_LARGE_F32_MBW, 2, 2, 2>;
+  static constexpr bool kXL = false;  // fp32 calls this large take the 128 x 64 tiles
   template <int Q> using MdnSmall = Gemm<float, Q, 1, 2, 1, 2, 32, 4>;  // 32Q x 16, K split 2
   template <int Q> using MdnLarge = GemmD<float, Q, WM_MDN_LARGE_F32_MBW, 2, 2, 2>;
   template <int NB> using CtrlLarge = Gemm<float, NB, 4, 4, 1, 1, 32, 3>;  // 64NB x 64
   template <int NB> using CtrlLargeX = GemmD<float, NB, 2, 4, 1, 3>;      // 64NB x 32
+  template <int NB> using CtrlXL = CtrlLargeX<NB>;
   static constexpr int WIDE_BKC = 64;
 };
 template <> struct Cfgs<bf16_t> {
@@ -1659,10 +1680,25 @@ template <> struct Cfgs<bf16_t> {
   using GatesLarge = GemmD<bf16_t, 4, 4, 2, 2, 2>;  // 128 x 128
   template <int Q> using MdnSmall = Gemm<bf16_t, Q, 1, 2, 1, 2, 64, 4>;
   template <int Q> using MdnLarge = GemmD<bf16_t, Q, 2, 2, 2, 2>;
+  // many-tile calls: 256 x 256 gate tiles and 32Q x 256 mixture tiles on
+  // eight waves halve the L2 -> LDS bytes per MFMA of the 128-wide tiles
+  using GatesXL = GemmD<bf16_t, 4, 8, 4, 2, 2>;
+  // (odd Q: 32Q + 256 rows do not deal evenly to eight waves' DMA loads)
+  template <int Q> using MdnXL = std::conditional_t<Q % 2 == 0, GemmD<bf16_t, Q, 4, 2, 4, 2>, MdnLarge<Q>>;
+  static constexpr bool kXL = true;
   template <int NB> using CtrlLarge = Gemm<bf16_t, NB, 4, 4, 1, 1, 64, 2>;
   template <int NB> using CtrlLargeX = GemmD<bf16_t, NB, 2, 4, 1, 3>;
+  // 64-row controller tiles on eight waves, three stages: half the
+  // weight re-reads of the 32-row tiles
+  template <int NB> using CtrlXL = GemmD<bf16_t, NB, 2, 4, 2, 3>;
   static constexpr int WIDE_BKC = 128;
 };
+
+// The 256-row tiles serve calls that still give every CU at least one tile.
+#ifndef WM_XL_TILES
+#define WM_XL_TILES 256
+#endif
+constexpr long kXLTiles = WM_XL_TILES;
 
 // Register-direct kernels serve calls with at most this many rows, when the
 // K slices fit SMAX per wave on the compiled block size.
@@ -1750,6 +1786,9 @@ hipError_t launch_gates(GatesArgs a, hipStream_t s) {
     if (e != hipErrorNotSupported) return e;
   }
   if (a.M <= kSmallRows) return launch_gates_cfg<typename Cfgs<DT>::GatesSmall, DT>(a, s);
+  using XL = typename Cfgs<DT>::GatesXL;
+  if (Cfgs<DT>::kXL && (long)((4 * a.H + XL::BN - 1) / XL::BN) * ((a.M + XL::BM - 1) / XL::BM) >= kXLTiles)
+    return launch_gates_cfg<XL, DT>(a, s);
   return launch_gates_cfg<typename Cfgs<DT>::GatesLarge, DT>(a, s);
 }
 
@@ -1775,6 +1814,9 @@ hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
     }
   }
   if (a.M <= kSmallRows) return launch_mdn_cfg<typename Cfgs<DT>::template MdnSmall<Q>, DT>(a, ntiles, s);
+  using XL = typename Cfgs<DT>::template MdnXL<Q>;
+  if (Cfgs<DT>::kXL && (long)ntiles * ((a.M + XL::BM - 1) / XL::BM) >= kXLTiles)
+    return launch_mdn_cfg<XL, DT>(a, ntiles, s);
   return launch_mdn_cfg<typename Cfgs<DT>::template MdnLarge<Q>, DT>(a, ntiles, s);
 }
 
@@ -1838,6 +1880,13 @@ hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
     if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlLarge<3>, S>(a, s);
     if (nb <= 5) return launch_ctrl_cfg<typename Cf::template CtrlLarge<5>, S>(a, s);
   } else {
+    // 64-row tiles once they still give every CU one, 32-row tiles below
+    if (Cf::kXL && (long)(a.M + 63) / 64 >= kXLTiles) {
+      if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlXL<1>, S>(a, s);
+      if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlXL<2>, S>(a, s);
+      if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlXL<3>, S>(a, s);
+      if (nb <= 5) return launch_ctrl_cfg<typename Cf::template CtrlXL<5>, S>(a, s);
+    }
     if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLargeX<1>, S>(a, s);
     if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlLargeX<2>, S>(a, s);
     if (nb <= 3) return launch_ctrl_cfg<typename Cf::template CtrlLargeX<3>, S>(a, s);

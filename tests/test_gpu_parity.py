@@ -157,3 +157,28 @@ def test_rollout_bf16_workloads_reanchored(name, nrows):
     for t in range(w.T):
         after = t > first_done
         assert np.all(acts[t, after] == -1) and np.all(dones[t, after] == 1)
+
+
+def test_rollout_bf16_ragged_wide_tiles():
+    """A bf16 batch just past a multiple of the 256-row gate / mixture tiles
+    and the 64-row controller tiles (the many-tile configurations), with the
+    ragged last tiles among the re-anchored rows."""
+    w = wl.WORKLOADS["xlarge_rollout"].replace(B=16384 + 6, T=3)
+    say("rollout ragged", w.B, "x", w.T)
+    inp = wl.make_rollout_inputs(w)
+    m = wmlib.pack(inp["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+    b = wmlib.rollout(m, _t(inp["z0"]), _t(inp["mask"]), T=w.T, seed=w.seed, tau=w.tau,
+                      done=w.done, trace=True)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.linspace(0, w.B - 1, 40).astype(np.int64),
+                                     np.arange(16384 - 3, w.B), [255, 256, 16383 - 63, 16384 - 64]]))
+    ri = torch.from_numpy(rows).cuda()
+    g = {k: getattr(b, k)[:, ri].cpu().numpy()
+         for k in ("z_out", "actions", "rewards", "dones", "h_trace", "c_trace")}
+    del b
+    torch.cuda.empty_cache()
+    say("ragged: oracle re-anchored on", rows.size, "rows")
+    ties, live = parity.reanchored(w.dims, inp["weights"], inp["mask"][rows], g, seed=w.seed,
+                                   tau=w.tau, done_flag=w.done, dtype=w.dtype, traj=rows)
+    say("ragged: tie mismatches", ties.mismatches, "of", ties.draws, "live", live)
+    assert live > 0
