@@ -15,8 +15,9 @@ TCC blocks):
 reads and writes exactly that many bytes: the calibration of each counter),
 then runs two bench steps (medium dream rollout + NLL).  ``summarize`` scales
 the kernel's per-dispatch average by bytes / counter of the copy and writes a
-short summary, stamped with the hash of the kernel sources so that a reader
-(bench.py) can tell whether the figures still describe the current kernels.
+short summary, stamped with the names and hash of the sources the kernel is
+compiled from, so that a reader (bench.py) can tell whether the figures still
+describe the current kernel.
 """
 
 from __future__ import annotations
@@ -30,14 +31,20 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-KERNEL_SOURCES = ["wm_kernels.hip", "wm_persist.hip", "wm_device.h", "wm_kernels.h", "wm_layout.h"]
+HEADERS = ["wm_device.h", "wm_kernels.h", "wm_layout.h"]
 CALIB_BYTES = 256 << 20
 
 
-def kernel_source_hash() -> str:
-    """sha256 over the sources that define the kernels."""
+def kernel_sources(kernel: str) -> list[str]:
+    """The sources a kernel is compiled from: the persistent kernels live in
+    wm_persist.hip, every other kernel in wm_kernels.hip."""
+    return ["wm_persist.hip" if "persist" in kernel else "wm_kernels.hip", *HEADERS]
+
+
+def kernel_source_hash(sources: list[str]) -> str:
+    """sha256 over the given kernel sources."""
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in sources:
         with open(os.path.join(PKG, "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
@@ -115,8 +122,10 @@ def summarize(fetch_csv: str, write_csv: str, kernel: str, out: str, command: st
     for c, r in res.items():
         lines.append(f"| {c} | {r['kib_per_dispatch']:.1f} | {r['dispatches']} | {r['copy_kib']:.0f} | "
                      f"{r['factor']:.4f} | {r['bytes_per_launch']:.0f} |")
+    srcs = kernel_sources(kernel)
     lines += ["", f"traffic_bytes_per_launch: {total:.0f}",
-              f"kernel_source_sha256: {kernel_source_hash()}", ""]
+              f"kernel_sources: {','.join(srcs)}",
+              f"kernel_source_sha256: {kernel_source_hash(srcs)}", ""]
     os.makedirs(os.path.dirname(os.path.abspath(out)), exist_ok=True)
     with open(out, "w") as f:
         f.write("\n".join(lines))
@@ -125,13 +134,19 @@ def summarize(fetch_csv: str, write_csv: str, kernel: str, out: str, command: st
 
 def read_summary(path: str) -> float | None:
     """Bytes per launch from a summary, or None if it is missing or was taken
-    on kernels other than the current ones."""
+    on a kernel whose sources have changed since."""
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m = re.search(r"^traffic_bytes_per_launch: (\S+)$", text, re.M)
+    srcs = re.search(r"^kernel_sources: (\S+)$", text, re.M)
     h = re.search(r"^kernel_source_sha256: (\S+)$", text, re.M)
-    if not m or not h or h.group(1) != kernel_source_hash():
+    if not m or not srcs or not h:
+        return None
+    names = srcs.group(1).split(",")
+    if any(not os.path.exists(os.path.join(PKG, "csrc", n)) for n in names):
+        return None
+    if h.group(1) != kernel_source_hash(names):
         return None
     return float(m.group(1))
 
