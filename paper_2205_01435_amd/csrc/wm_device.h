@@ -112,6 +112,20 @@ __device__ __forceinline__ float ftanh(float x) {
   return copysignf(ax < 0.125f ? small : big, x);
 }
 
+// tanh as 1 - 2 / (1 + exp(2x)), without the small-|x| branch: about 2.5e-7
+// absolute error (relative accuracy is lost near 0 to the cancellation),
+// three VALU and two transcendental instructions against ten and two.  For
+// the bf16 cells, whose h is rounded to bf16 (relative step 2^-9) right away.
+__device__ __forceinline__ float ftanh_abs(float x) {
+  return 1.0f - 2.0f * frcp(1.0f + __builtin_amdgcn_exp2f(x * 2.88539008177792681f));
+}
+// the cell's tanh for activation type DT
+template <typename DT>
+__device__ __forceinline__ float ftanh_cell(float x) {
+  if constexpr (sizeof(DT) == 4) return ftanh(x);
+  else return ftanh_abs(x);
+}
+
 enum : uint32_t { STREAM_CONTROLLER = 0, STREAM_COMPONENT = 1, STREAM_GAUSS = 2, STREAM_DONE = 3 };
 
 // ---------------------------------------------------------------------------
@@ -277,9 +291,10 @@ struct MdnNoise {
   float eps;   // standard normal of dim j
 };
 
-__device__ __forceinline__ MdnNoise mixture_noise(const Rng& rng, int K, uint32_t step, uint32_t traj,
-                                                  int j) {
-  MdnNoise n;
+// Gumbel noise of components 0 .. K-1 of dim j, one Philox block per four
+// consecutive uniforms of the dim.
+__device__ __forceinline__ void component_noise(MdnNoise& n, const Rng& rng, int K, uint32_t step,
+                                                uint32_t traj, int j) {
   uint32_t cur = 0xffffffffu;
   uint4 w = make_uint4(0, 0, 0, 0);
 #pragma unroll
@@ -294,13 +309,33 @@ __device__ __forceinline__ MdnNoise mixture_noise(const Rng& rng, int K, uint32_
       n.g[k] = gumbel(word_to_uniform(word_of(w, idx & 3)));
     }
   }
-  const uint4 wg = rng.block((uint32_t)j >> 2, step, traj, STREAM_GAUSS);
-  const float u1 = word_to_uniform(word_of(wg, j & 2));
-  const float u2 = word_to_uniform(word_of(wg, (j & 2) + 1));
+}
+
+// Box-Muller on one stream-2 word pair: (cos deviate, sin deviate), which
+// belong to the pair's even and odd dim.
+__device__ __forceinline__ float2 box_muller(uint32_t w1, uint32_t w2) {
+  const float u1 = word_to_uniform(w1);
+  const float u2 = word_to_uniform(w2);
   const float r = sqrtf(-2.0f * logf(u1));
   float sn, cs;
   sincospif(2.0f * u2, &sn, &cs);
-  n.eps = (j & 1) ? r * sn : r * cs;
+  return make_float2(r * cs, r * sn);
+}
+
+// The standard normals of the four dims 4J .. 4J+3 (one stream-2 block).
+__device__ __forceinline__ float4 gauss_group(const Rng& rng, uint32_t step, uint32_t traj, int J) {
+  const uint4 wg = rng.block((uint32_t)J, step, traj, STREAM_GAUSS);
+  const float2 e01 = box_muller(wg.x, wg.y), e23 = box_muller(wg.z, wg.w);
+  return make_float4(e01.x, e01.y, e23.x, e23.y);
+}
+
+__device__ __forceinline__ MdnNoise mixture_noise(const Rng& rng, int K, uint32_t step, uint32_t traj,
+                                                  int j) {
+  MdnNoise n;
+  component_noise(n, rng, K, step, traj, j);
+  const uint4 wg = rng.block((uint32_t)j >> 2, step, traj, STREAM_GAUSS);
+  const float2 e = box_muller(word_of(wg, j & 2), word_of(wg, (j & 2) + 1));
+  n.eps = (j & 1) ? e.y : e.x;
   return n;
 }
 
@@ -309,11 +344,21 @@ __device__ __forceinline__ float mixture_pick(int K, float tau, const MdnNoise& 
                                               const float (&feat)[4 * Q]) {
   float best = -INFINITY;
   int kbest = 0;
+  if (tau == 1.0f) {  // x / 1 == x: the same scores without the divisions
 #pragma unroll
-  for (int f = 0; f < 4 * Q && f < 8; ++f) {
-    if (f < K) {
-      const float sc = feat[f] / tau + n.g[f];
-      if (sc > best) { best = sc; kbest = f; }
+    for (int f = 0; f < 4 * Q && f < 8; ++f) {
+      if (f < K) {
+        const float sc = feat[f] + n.g[f];
+        if (sc > best) { best = sc; kbest = f; }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int f = 0; f < 4 * Q && f < 8; ++f) {
+      if (f < K) {
+        const float sc = feat[f] / tau + n.g[f];
+        if (sc > best) { best = sc; kbest = f; }
+      }
     }
   }
   float mu = 0.f, ls = 0.f;

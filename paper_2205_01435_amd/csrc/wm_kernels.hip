@@ -497,8 +497,8 @@ struct GateIO {
 
   __device__ __forceinline__ void commit(int ml, int u, bool ok, const GateIn& in, float pi, float pf,
                                          float pg, float po) const {
-    const float cn = fsigmoid(pf + in.add.y) * in.c + fsigmoid(pi + in.add.x) * ftanh(pg + in.add.z);
-    const float hn = DType<DT>::round(fsigmoid(po + in.add.w) * ftanh(cn));
+    const float cn = fsigmoid(pf + in.add.y) * in.c + fsigmoid(pi + in.add.x) * ftanh_cell<DT>(pg + in.add.z);
+    const float hn = DType<DT>::round(fsigmoid(po + in.add.w) * ftanh_cell<DT>(cn));
     const float cv = in.live ? cn : in.c;
     const float hv = in.live ? hn : in.hprev;
     const uint32_t ec = ((uint32_t)ml * H + u) * 4u;
@@ -599,8 +599,8 @@ struct Gate4IO {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const float cn = fsigmoid(g[t].y + in.add[t].y) * cin[t] +
-                       fsigmoid(g[t].x + in.add[t].x) * ftanh(g[t].z + in.add[t].z);
-      const float hn = DType<DT>::round(fsigmoid(g[t].w + in.add[t].w) * ftanh(cn));
+                       fsigmoid(g[t].x + in.add[t].x) * ftanh_cell<DT>(g[t].z + in.add[t].z);
+      const float hn = DType<DT>::round(fsigmoid(g[t].w + in.add[t].w) * ftanh_cell<DT>(cn));
       cv[t] = in.live ? cn : cin[t];
       hv[t] = in.live ? hn : hin[t];
     }
@@ -844,6 +844,21 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
   if (!p.nll_mode) {
     if (!owner) return;  // no barrier below
     const Rng rng{p.k0, p.k1};
+    // The four lanes of a row (lane groups g, dims 4J + g) need the same
+    // stream-2 block.  With four row blocks per lane, lane group g draws the
+    // block and both Box-Muller pairs for row block g only, and every lane
+    // reads its deviates from the drawing lanes (shuffles, all lanes active),
+    // instead of each lane drawing all four blocks.
+    float eps[MBW];
+    if constexpr (MBW == 4) {
+      const float4 e = gauss_group(rng, p.step, p.traj0 + (uint32_t)(m0 + (wmi * MBW + g) * 16 + (lane & 15)), J);
+#pragma unroll
+      for (int jj = 0; jj < MBW; ++jj) {
+        const int src = jj * 16 + (lane & 15);
+        const float v0 = __shfl(e.x, src), v1 = __shfl(e.y, src), v2 = __shfl(e.z, src), v3 = __shfl(e.w, src);
+        eps[jj] = g == 0 ? v0 : (g == 1 ? v1 : (g == 2 ? v2 : v3));
+      }
+    }
 #pragma unroll
     for (int jj = 0; jj < MBW; ++jj) {
       const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
@@ -857,7 +872,14 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
       for (int q = 0; q < Q; ++q)
 #pragma unroll
         for (int v = 0; v < 4; ++v) feat[4 * q + v] = acc[q][jj][v] + bias[4 * q + v];
-      mdn_commit<DT>(p, m, j, mdn_draw<Q>(p, rng, m, j, feat));
+      if constexpr (MBW == 4) {
+        MdnNoise nz;
+        component_noise(nz, rng, p.K, p.step, p.traj0 + (uint32_t)m, j);
+        nz.eps = eps[jj];
+        mdn_commit<DT>(p, m, j, mdn_pick<Q>(p, nz, feat));
+      } else {
+        mdn_commit<DT>(p, m, j, mdn_draw<Q>(p, rng, m, j, feat));
+      }
     }
   } else {
 #pragma unroll
