@@ -93,7 +93,16 @@ __device__ __forceinline__ float word_to_uniform(uint32_t x) {
 __device__ __forceinline__ uint32_t word_of(uint4 w, int i) {
   return i == 0 ? w.x : (i == 1 ? w.y : (i == 2 ? w.z : w.w));
 }
-__device__ __forceinline__ float gumbel(float u) { return -logf(-logf(u)); }
+// Gumbel score -ln(-ln u) as -ln(ln 2) - ln 2 * log2(-log2 u), on the
+// hardware log2 (v_log_f32, accurate to about an ulp in relative terms also
+// near 1, where the library logf relies on it too).  The uniforms here are
+// normal numbers in [2^-24, 1), so the library's denormal and infinity
+// handling is not needed.  Over all 2^23 uniforms of word_to_uniform the
+// largest error against float64 is 2.0e-6 absolute, 2.1e-7 relative to
+// max(1, |score|) (library logf: 1.9e-6 and 2.9e-7).
+__device__ __forceinline__ float gumbel(float u) {
+  return fmaf(-0.69314718055994531f, __builtin_amdgcn_logf(-__builtin_amdgcn_logf(u)), 0.36651292058166435f);
+}
 __device__ __forceinline__ float sigmoidf(float x) { return 1.0f / (1.0f + expf(-x)); }
 
 // Fast LSTM nonlinearities on the hardware base-2 exponential and reciprocal
