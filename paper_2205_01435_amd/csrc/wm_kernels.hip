@@ -328,27 +328,25 @@ struct GemmD {
 #pragma unroll
       for (int j = 0; j < MBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // per-lane source offsets of this wave's DMA instructions (chunk 0)
-    u32x4 rs[QW];
+    // per-lane source offsets of this wave's DMA instructions (chunk 0); the
+    // two buffer resources are selected per instruction rather than held in
+    // one register quad each, which kept the scalar registers spilling
+    const u32x4 rw = rsrc_words(w.base, w.bytes), rx = rsrc_words(x.base, x.bytes);
+    bool isw[QW];
     uint32_t off[QW];
 #pragma unroll
     for (int t = 0; t < QW; ++t) {
       const int q = wave * QW + t;  // uniform
       const int row = 8 * q + (lane >> 3);
       const int c = (lane & 7) ^ ((row >> 1) & 7);
-      if (q < BN / 8) {
-        rs[t] = rsrc_words(w.base, w.bytes);
-        off[t] = w.row(row) + 16u * c;
-      } else {
-        rs[t] = rsrc_words(x.base, x.bytes);
-        off[t] = x.row(row - BN) + 16u * c;
-      }
+      isw[t] = q < BN / 8;
+      off[t] = isw[t] ? w.row(row) + 16u * c : x.row(row - BN) + 16u * c;
     }
     const int nk = Kpad / BK;
     auto issue = [&](int kc) {
       const uint32_t base = lds0 + (uint32_t)(kc % STAGES) * STAGE_BYTES + (uint32_t)wave * QW * 1024u;
 #pragma unroll
-      for (int t = 0; t < QW; ++t) dma16(rs[t], off[t] + 128u * (uint32_t)kc, base + 1024u * t);
+      for (int t = 0; t < QW; ++t) dma16(isw[t] ? rw : rx, off[t] + 128u * (uint32_t)kc, base + 1024u * t);
     };
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
@@ -731,26 +729,25 @@ struct MdnArgs {
 
 // z_{t+1,j} of row m (mixture_noise / mixture_pick with the call's step,
 // temperature and trajectory index).
-__device__ __forceinline__ MdnNoise mdn_noise(const MdnArgs& p, const Rng& rng, int m, int j) {
-  return mixture_noise(rng, p.K, p.step, p.traj0 + (uint32_t)m, j);
+__device__ __forceinline__ MdnNoise mdn_noise(const MdnArgs& p, const Rng& rng, int m, int j, int K) {
+  return mixture_noise(rng, K, p.step, p.traj0 + (uint32_t)m, j);
 }
 
 template <int Q>
 __device__ __forceinline__ float mdn_pick(const MdnArgs& p, const MdnNoise& n,
-                                          const float (&feat)[4 * Q]) {
-  return mixture_pick<Q>(p.K, p.tau, n, feat);
+                                          const float (&feat)[4 * Q], int K) {
+  return mixture_pick<Q>(K, p.tau, n, feat);
 }
 
 template <int Q>
 __device__ __forceinline__ float mdn_draw(const MdnArgs& p, const Rng& rng, int m, int j,
-                                          const float (&feat)[4 * Q]) {
-  return mdn_pick<Q>(p, mdn_noise(p, rng, m, j), feat);
+                                          const float (&feat)[4 * Q], int K) {
+  return mdn_pick<Q>(p, mdn_noise(p, rng, m, j, K), feat, K);
 }
 
 // log sum_k pi_k N(x; mu_k, sigma_k) of one latent dim (pi at tau = 1).
 template <int Q>
-__device__ __forceinline__ float mdn_loglik(const MdnArgs& p, float x, const float (&feat)[4 * Q]) {
-  const int K = p.K;
+__device__ __forceinline__ float mdn_loglik(float x, const float (&feat)[4 * Q], int K) {
   float mx = -INFINITY;
 #pragma unroll
   for (int f = 0; f < 4 * Q; ++f)
@@ -791,9 +788,12 @@ __device__ __forceinline__ void mdn_commit(const MdnArgs& p, int m, int j, float
   DType<DT>::store(reinterpret_cast<DT*>(p.x), (long)m * p.ldx + j, z);
 }
 
-template <class C>
+// KC: the number of mixture components (the call's K), a compile-time
+// constant so that the feature selections of the epilogue fold away
+template <class C, int KC>
 __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
   using DT = typename C::DT;
+  constexpr int K = KC;
   constexpr int Q = C::NBW, MBW = C::MBW, WAVES_N = C::WAVES_N, WAVES_M = C::WAVES_M;
   static_assert(WAVES_N == 2, "the NLL epilogue sums two dim groups per work-group");
   __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
@@ -874,11 +874,11 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
         for (int v = 0; v < 4; ++v) feat[4 * q + v] = acc[q][jj][v] + bias[4 * q + v];
       if constexpr (MBW == 4) {
         MdnNoise nz;
-        component_noise(nz, rng, p.K, p.step, p.traj0 + (uint32_t)m, j);
+        component_noise(nz, rng, K, p.step, p.traj0 + (uint32_t)m, j);
         nz.eps = eps[jj];
-        mdn_commit<DT>(p, m, j, mdn_pick<Q>(p, nz, feat));
+        mdn_commit<DT>(p, m, j, mdn_pick<Q>(p, nz, feat, K));
       } else {
-        mdn_commit<DT>(p, m, j, mdn_draw<Q>(p, rng, m, j, feat));
+        mdn_commit<DT>(p, m, j, mdn_draw<Q>(p, rng, m, j, feat, K));
       }
     }
   } else {
@@ -892,7 +892,7 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
         for (int q = 0; q < Q; ++q)
 #pragma unroll
           for (int v = 0; v < 4; ++v) feat[4 * q + v] = acc[q][jj][v] + bias[4 * q + v];
-        ll = mdn_loglik<Q>(p, p.z_tgt[(long)m * Z + j], feat);
+        ll = mdn_loglik<Q>(p.z_tgt[(long)m * Z + j], feat, K);
       }
       // sum over the four dims of the group (lane groups), then the two waves
       ll += __shfl_xor(ll, 16);
@@ -1431,7 +1431,7 @@ __global__ void __launch_bounds__(R::MAXT) k_mdn_rd(const MdnArgs p) {
   MdnNoise noise{};
   if (mine) {
     live = p.act[m] >= 0;
-    if (live) noise = mdn_noise(p, rng, m, j);
+    if (live) noise = mdn_noise(p, rng, m, j, p.K);
     else zprev = p.z_prev[(long)m * p.Z + j];
   }
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wm), p.ldh, p.ldh, n0, R::BN, p.Nm);
@@ -1451,7 +1451,7 @@ __global__ void __launch_bounds__(R::MAXT) k_mdn_rd(const MdnArgs p) {
       const int r = 16 * q + 4 * d + v;
       feat[4 * q + v] = E[ml * R::ELD + r] + p.bm[n0 + r];
     }
-  mdn_commit<DT>(p, m, j, mdn_pick<Q>(p, noise, feat));
+  mdn_commit<DT>(p, m, j, mdn_pick<Q>(p, noise, feat, p.K));
 }
 
 // Controller on the register-direct core: all Nc outputs x 16 rows.  Each row
@@ -1814,13 +1814,13 @@ hipError_t launch_gates(GatesArgs a, hipStream_t s) {
   return launch_gates_cfg<typename Cfgs<DT>::GatesLarge, DT>(a, s);
 }
 
-template <class C, typename DT>
+template <class C, typename DT, int KC>
 hipError_t launch_mdn_cfg(MdnArgs a, int ntiles, hipStream_t s) {
   a.map = tile_map(ntiles, (a.M + C::BM - 1) / C::BM, (size_t)a.Nm * a.ldh * sizeof(DT));
-  return launch("mdn", k_mdn<C>, dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
+  return launch("mdn", k_mdn<C, KC>, dim3(grid_of(a.map)), dim3(C::NT), 0, s, a);
 }
 
-template <typename DT, int Q>
+template <typename DT, int Q, int KC>
 hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
   if (!a.nll_mode) {
     using R = GemmRD<DT, Q, 1, 4, 640>;  // 16-row tiles: more work-groups
@@ -1835,23 +1835,26 @@ hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
       return launch("mdn", k_mdn_rd<R>, dim3(grid_of(b.map)), dim3(64 * nw), lds, s, b);
     }
   }
-  if (a.M <= kSmallRows) return launch_mdn_cfg<typename Cfgs<DT>::template MdnSmall<Q>, DT>(a, ntiles, s);
+  if (a.M <= kSmallRows) return launch_mdn_cfg<typename Cfgs<DT>::template MdnSmall<Q>, DT, KC>(a, ntiles, s);
   using XL = typename Cfgs<DT>::template MdnXL<Q>;
   if (Cfgs<DT>::kXL && (long)ntiles * ((a.M + XL::BM - 1) / XL::BM) >= kXLTiles)
-    return launch_mdn_cfg<XL, DT>(a, ntiles, s);
-  return launch_mdn_cfg<typename Cfgs<DT>::template MdnLarge<Q>, DT>(a, ntiles, s);
+    return launch_mdn_cfg<XL, DT, KC>(a, ntiles, s);
+  return launch_mdn_cfg<typename Cfgs<DT>::template MdnLarge<Q>, DT, KC>(a, ntiles, s);
 }
 
+// one instantiation per component count K (which fixes Q = ceil(3K / 4))
 template <typename DT>
 hipError_t launch_mdn(const MdnArgs& a, int Q, int ntiles, hipStream_t s) {
-  switch (Q) {
-    case 1: return launch_mdn_q<DT, 1>(a, ntiles, s);
-    case 2: return launch_mdn_q<DT, 2>(a, ntiles, s);
-    case 3: return launch_mdn_q<DT, 3>(a, ntiles, s);
-    case 4: return launch_mdn_q<DT, 4>(a, ntiles, s);
-    case 5: return launch_mdn_q<DT, 5>(a, ntiles, s);
-    case 6: return launch_mdn_q<DT, 6>(a, ntiles, s);
-    default: return hipErrorInvalidValue;
+  if (a.K < 1 || a.K > 8 || Q != (3 * a.K + 3) / 4) return hipErrorInvalidValue;
+  switch (a.K) {
+    case 1: return launch_mdn_q<DT, 1, 1>(a, ntiles, s);
+    case 2: return launch_mdn_q<DT, 2, 2>(a, ntiles, s);
+    case 3: return launch_mdn_q<DT, 3, 3>(a, ntiles, s);
+    case 4: return launch_mdn_q<DT, 3, 4>(a, ntiles, s);
+    case 5: return launch_mdn_q<DT, 4, 5>(a, ntiles, s);
+    case 6: return launch_mdn_q<DT, 5, 6>(a, ntiles, s);
+    case 7: return launch_mdn_q<DT, 6, 7>(a, ntiles, s);
+    default: return launch_mdn_q<DT, 6, 8>(a, ntiles, s);
   }
 }
 
