@@ -192,10 +192,33 @@ wm_status wm_nll(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
                  size_t workspace_bytes, wm_stream_t stream);
 
 /*
+ * Return scan over B dreamed trajectories of T steps, for the policy updates
+ * of the controller: the discounted sum of rewards that the agent maximises
+ * (section 2.2) and, with a value baseline, generalised advantage estimates
+ * (GAE(lambda), Schulman et al. 2016) for PPO (sections 2.3 and 4.1).  A
+ * done step ends its trajectory: nothing after it is discounted into it.
+ * It reads a wm_rollout's rewards and dones directly (frozen steps carry
+ * reward 0 and done 1, so they add nothing).
+ *   rewards [T, B] float32; dones [T, B] uint8 (nonzero = done).
+ *   values [T+1, B] float32, nullable.
+ *   gamma, lambda        in [0, 1]; lambda is used only with values.
+ *   returns [T, B] float32:
+ *     without values  G_t = r_t + gamma (1 - d_t) G_{t+1}, G_T = 0;
+ *     with values     A_t + V_t, where
+ *                     A_t = delta_t + gamma lambda (1 - d_t) A_{t+1}, A_T = 0,
+ *                     delta_t = r_t + gamma (1 - d_t) V_{t+1} - V_t.
+ *   advantages [T, B] float32, nullable; A_t (requires values).
+ * B = 0 or T = 0 is a no-op.  Float arrays must be 4-byte aligned.
+ */
+wm_status wm_returns(int32_t B, int32_t T, const float *rewards, const uint8_t *dones,
+                     const float *values, float gamma, float lambda, float *returns,
+                     float *advantages, wm_stream_t stream);
+
+/*
  * Measurement aid (no counterpart in the paper).  While a prefix is set, every
  * kernel launch of the library whose name starts with it is bracketed by HIP
  * events on its stream.  Kernel names: "ctrl", "gates", "mdn", "init",
- * "finish", "nll_init", "nll_reduce", "nll_means", "pack"; "" selects all,
+ * "finish", "nll_init", "nll_reduce", "nll_means", "pack", "returns"; "" selects all,
  * NULL turns timing off.  wm_profile_read waits for the recorded events and
  * returns the summed duration (ms) and count of the launches whose name
  * starts with `prefix` (NULL = all); wm_profile_reset forgets them.  Timing

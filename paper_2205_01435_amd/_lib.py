@@ -24,7 +24,7 @@ _DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
 
 # Every symbol the C header declares.
 EXPORTS = ("wm_packed_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
-           "wm_rollout", "wm_nll", "wm_profile_enable", "wm_profile_read", "wm_profile_reset",
+           "wm_rollout", "wm_nll", "wm_returns", "wm_profile_enable", "wm_profile_read", "wm_profile_reset",
            "wm_last_error", "wm_version")
 
 
@@ -72,6 +72,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_rollout.restype = I32
     lib.wm_nll.argtypes = [pd, P, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.wm_nll.restype = I32
+    lib.wm_returns.argtypes = [I32, I32, P, P, P, F32, F32, P, P, P]
+    lib.wm_returns.restype = I32
     lib.wm_profile_enable.argtypes = [ctypes.c_char_p]
     lib.wm_profile_enable.restype = I32
     lib.wm_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
@@ -222,6 +224,21 @@ def nll(m: Model, z, actions, rewards, dones, lengths=None,
                       _ptr(bufs.reward_se), _ptr(bufs.done_bce), _ptr(bufs.means),
                       _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
     return bufs
+
+
+def returns(rewards, dones, gamma: float, values=None, lam: float = 1.0, out=None, adv=None):
+    """Launch wm_returns on the current stream over device tensors
+    rewards [T, B] float32 and dones [T, B] uint8 (values [T+1, B] float32 or
+    None).  Returns (returns [T, B], advantages [T, B] or None)."""
+    lib = load()
+    T, B = rewards.shape
+    if out is None:
+        out = torch.empty((T, B), dtype=torch.float32, device=rewards.device)
+    if values is not None and adv is None:
+        adv = torch.empty((T, B), dtype=torch.float32, device=rewards.device)
+    _check(lib.wm_returns(B, T, _ptr(rewards), _ptr(dones), _ptr(values), gamma, lam, _ptr(out),
+                          _ptr(adv if values is not None else None), _stream()))
+    return out, (adv if values is not None else None)
 
 
 def profile_enable(prefix: str | None):

@@ -36,6 +36,7 @@ wm_status hip_fail(hipError_t e, const char* where) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 // Checks the model dims; returns WM_OK and fills the layout.
 wm_status check_dims(const wm_dims* d, wm::Layout* L) {
@@ -199,6 +200,29 @@ wm_status wm_nll(const wm_dims* dims, const void* packed, int32_t B, int32_t T, 
   wm::Packed P{L, packed};
   hipError_t e = wm::launch_nll(P, N, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "wm_nll");
+  return ok();
+}
+
+wm_status wm_returns(int32_t B, int32_t T, const float* rewards, const uint8_t* dones,
+                     const float* values, float gamma, float lambda, float* returns,
+                     float* advantages, wm_stream_t stream) {
+  if (B < 0 || T < 0) return fail(WM_ERR_INVALID_ARG, "B=%d and T=%d must not be negative", B, T);
+  if (!(gamma >= 0.0f && gamma <= 1.0f)) return fail(WM_ERR_INVALID_ARG, "gamma must lie in [0, 1]");
+  if (!(lambda >= 0.0f && lambda <= 1.0f)) return fail(WM_ERR_INVALID_ARG, "lambda must lie in [0, 1]");
+  if (advantages && !values) return fail(WM_ERR_INVALID_ARG, "advantages need values");
+  if ((int64_t)B * (T + 1) > (int64_t)1 << 31)
+    return fail(WM_ERR_UNSUPPORTED, "B*(T+1) too large");
+  if (B == 0 || T == 0) return ok();
+  if (!rewards || !dones || !returns)
+    return fail(WM_ERR_INVALID_ARG, "rewards, dones and returns are required");
+  if (!aligned4(rewards) || !aligned4(returns) || !aligned4(values) || !aligned4(advantages))
+    return fail(WM_ERR_INVALID_ARG, "float arrays must be 4-byte aligned");
+  wm::ReturnsBufs R{};
+  R.B = B; R.T = T; R.gamma = gamma; R.lambda = lambda;
+  R.rewards = rewards; R.dones = dones; R.values = values;
+  R.returns = returns; R.advantages = advantages;
+  hipError_t e = wm::launch_returns(R, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "wm_returns");
   return ok();
 }
 

@@ -82,4 +82,16 @@ bool persist_usable(const Layout& L, int B, bool nll);
 hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStream_t s);
 hipError_t launch_nll_persist(const Packed& P, const NllBufs& N, hipStream_t s);
 
+// Return scan over B trajectories of T steps (wm_returns.hip).
+struct ReturnsBufs {
+  int B, T;
+  float gamma, lambda;
+  const float* rewards;  // [T, B]
+  const uint8_t* dones;  // [T, B]
+  const float* values;   // [T+1, B] or null
+  float* returns;        // [T, B]
+  float* advantages;     // [T, B] or null (values given)
+};
+hipError_t launch_returns(const ReturnsBufs& R, hipStream_t s);
+
 }  // namespace wm
