@@ -272,7 +272,51 @@ def workload_table(wmlib, wl, torch, cuda) -> dict:
         res[name] = row
         del bufs, m
         torch.cuda.empty_cache()
+    res["returns_gae_xlarge"] = returns_row(wmlib, torch, cuda)
     return res
+
+
+def returns_bytes(T: int, B: int, gae: bool) -> int:
+    """Algorithmic HBM bytes of one wm_returns call: rewards (4 B) and dones
+    (1 B) read and returns (4 B) written per step, plus with GAE the values
+    [T+1, B] read and the advantages written."""
+    return T * B * (4 + 1 + 4) + ((T + 1) * B * 4 + T * B * 4 if gae else 0)
+
+
+def returns_row(wmlib, torch, cuda) -> dict:
+    """GAE scan over the xlarge rollout's shape (T = 64, B = 16384), against
+    the HBM roof (the kernel reads and writes each element once)."""
+    T, B = 64, 16384
+    rng = np.random.default_rng(5)
+    r = cuda(rng.normal(size=(T, B)).astype(np.float32))
+    d = cuda((rng.random((T, B)) < 0.05).astype(np.uint8))
+    v = cuda(rng.normal(size=(T + 1, B)).astype(np.float32))
+    out = torch.empty((T, B), dtype=torch.float32, device=r.device)
+    adv = torch.empty_like(out)
+    wmlib.returns(r, d, 0.99, values=v, lam=0.95, out=out, adv=adv)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 50
+    a.record()
+    for _ in range(reps):
+        wmlib.returns(r, d, 0.99, values=v, lam=0.95, out=out, adv=adv)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    # the kernel alone: dispatch-stamped events on every launch
+    wmlib.profile_reset()
+    wmlib.profile_enable("returns")
+    for _ in range(reps):
+        wmlib.returns(r, d, 0.99, values=v, lam=0.95, out=out, adv=adv)
+    torch.cuda.synchronize()
+    k_ms, k_n = wmlib.profile_read("returns")
+    wmlib.profile_enable(None)
+    wmlib.profile_reset()
+    kms = k_ms / max(k_n, 1)
+    nb = returns_bytes(T, B, True)
+    return {"ms": ms, "per_s": T * B / (ms / 1e3), "unit": "steps/s", "bytes": nb,
+            "GBps": nb / (ms / 1e3) / 1e9, "frac_hbm_peak": nb / (ms / 1e3) / HBM_PEAK,
+            "kernel_us": kms * 1e3, "kernel_frac_hbm_peak": nb / (kms / 1e3) / HBM_PEAK}
 
 
 def cpu_baseline(w, roll_in, nll_in, budget_s: float) -> dict:
