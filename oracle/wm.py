@@ -205,7 +205,7 @@ def softplus(x):
 
 def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: int,
                tau: float = 1.0, done_flag: bool = True, dtype: str = "fp32",
-               action=None, h_next=None) -> dict:
+               action=None, h_next=None, sigma_tau: bool = False) -> dict:
     """One dream step for a batch of live rows (sections 3.4 and 3.3.2).
 
     1. controller logits on [z_t, h_t] and a masked Gumbel-max action
@@ -215,7 +215,9 @@ def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: in
        ``h_next`` when given, to re-anchor on another implementation's h');
     4. per latent dim a Gumbel-max component pick on pi-logit / tau (stream 1);
     5. z'_j = mu_{j,k} + exp(log sigma_{j,k}) eps_j, eps from Box-Muller on
-       stream 2;
+       stream 2 (with ``sigma_tau`` the standard deviation is also scaled by
+       sqrt(tau), the temperature of Ha and Schmidhuber's World Models, whose
+       model section 3.3 builds on; the paper itself applies tau to pi only);
     6. reward = rho_r; done = sigmoid(rho_d) > u (stream 3) when enabled.
 
     ``action`` overrides the controller's choice in step 2 (re-anchoring).
@@ -246,7 +248,7 @@ def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: in
     eps = box_muller(u2)
     mu_k = np.take_along_axis(mu, k[..., None], axis=-1)[..., 0]
     ls_k = np.take_along_axis(log_sigma, k[..., None], axis=-1)[..., 0]
-    z2 = mu_k + np.exp(ls_k) * eps
+    z2 = mu_k + np.exp(ls_k) * (math.sqrt(tau) * eps if sigma_tau else eps)
 
     if done_flag:
         u3 = ph.stream_uniforms(seed, traj, step, ph.STREAM_DONE, 1)[:, 0]
@@ -270,7 +272,7 @@ def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: in
 
 def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.0,
             done_flag: bool = True, dtype: str = "fp32", traj0: int = 0, step0: int = 0,
-            h0=None, c0=None, done0=None) -> dict:
+            h0=None, c0=None, done0=None, sigma_tau: bool = False) -> dict:
     """B dream trajectories of T steps (the "hallucinated" environment of
     section 3.3 driven by the controller of section 3.4).
 
@@ -313,7 +315,7 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
         if live.size:
             r = transition(wb, dims, z[live], h[live], c[live], mask[live], seed=seed,
                            traj=traj0 + live, step=step0 + t, tau=tau,
-                           done_flag=done_flag, dtype=dtype)
+                           done_flag=done_flag, dtype=dtype, sigma_tau=sigma_tau)
             ok = r["action"] >= 0
             a_margin[t, live] = r["action_margin"]
             rows = live[ok]

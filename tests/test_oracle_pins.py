@@ -393,6 +393,38 @@ def test_tau_scales_pi_logits_only():
         np.testing.assert_array_equal(r["z"], ref)
 
 
+def test_sigma_tau_scales_the_spread_only():
+    """With sigma_tau the draw is mu + sqrt(tau) sigma eps: at tau = 1 nothing
+    changes; at tau = 2.25 the component picks, means and eps stay, and with
+    K = 1 many one-step samples standardised by 1.5 sigma are standard normal."""
+    w, d = _rollout_case(B=6, T=1)
+    wb = wm.weight_blocks(d["weights"], **w.dims, dtype="fp32")
+    z, h, c = d["z0"].astype(np.float64), np.zeros((6, w.H)), np.zeros((6, w.H))
+    kw = dict(seed=4, traj=np.arange(6), step=0, action=np.zeros(6, np.int64))
+    r0 = wm.transition(wb, w.dims, z, h, c, d["mask"], tau=1.0, **kw)
+    r1 = wm.transition(wb, w.dims, z, h, c, d["mask"], tau=1.0, sigma_tau=True, **kw)
+    np.testing.assert_array_equal(r0["z"], r1["z"])
+    a = wm.transition(wb, w.dims, z, h, c, d["mask"], tau=2.25, **kw)
+    b = wm.transition(wb, w.dims, z, h, c, d["mask"], tau=2.25, sigma_tau=True, **kw)
+    np.testing.assert_array_equal(a["component"], b["component"])
+    k = a["component"][..., None]
+    mu_k = np.take_along_axis(a["mu"], k, -1)[..., 0]
+    np.testing.assert_allclose(b["z"] - mu_k, 1.5 * (a["z"] - mu_k), rtol=1e-12, atol=1e-12)
+
+    Z, H, A, K = 4, 6, 5, 1
+    w1 = _weights(Z=Z, H=H, A=A, K=K)
+    wb1 = wm.weight_blocks(w1, Z, H, A, K, "fp32")
+    n = 20000
+    rng = np.random.default_rng(11)
+    zz = np.tile(rng.normal(size=(1, Z)), (n, 1))
+    r = wm.transition(wb1, dict(Z=Z, H=H, A=A, K=K), zz, np.zeros((n, H)), np.zeros((n, H)),
+                      np.ones((n, A), np.uint8), seed=5, traj=np.arange(n), step=0, tau=2.25,
+                      done_flag=False, action=np.zeros(n, np.int64), sigma_tau=True)
+    zs = (r["z"] - r["mu"][..., 0]) / (1.5 * np.exp(r["log_sigma"][..., 0]))
+    for j in range(Z):
+        assert stats.kstest(zs[:, j], "norm").pvalue > 1e-4
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_workload_generators_deterministic(dtype):
     w = wl.Workload("t", "rollout", B=8, T=4, Z=8, H=16, A=6, K=2, dtype=dtype, seed=3)
