@@ -64,7 +64,12 @@ typedef enum {
 
 enum {
   WM_FLAG_DONE = 1u, /* sample the done head; else dones are 0 while live */
-  WM_FLAG_TRACE = 2u /* write h_trace / c_trace                            */
+  WM_FLAG_TRACE = 2u, /* write h_trace / c_trace                           */
+  WM_FLAG_SIGMA_TAU = 4u /* also scale the mixture's standard deviation by
+                            sqrt(tau) (the temperature of Ha and
+                            Schmidhuber's World Models, on which section 3.3
+                            builds); without it tau acts on the pi-logits
+                            only, as the paper specifies                    */
 };
 
 typedef struct {
@@ -140,6 +145,7 @@ wm_status wm_controller_step(const wm_dims *dims, const void *packed, int32_t B,
  *      k_j = argmax_k (pi_logit_jk / tau + Gumbel(stream 1, j*K + k));
  *   4. z_{t+1,j} = mu_jk + exp(log_sigma_jk) * eps_j, eps from Box-Muller on
  *      the stream-2 pair (2p, 2p+1) containing j (cos for even j, sin odd);
+ *      with WM_FLAG_SIGMA_TAU, eps_j is scaled by sqrt(tau);
  *   5. reward_t = w_r.h_{t+1} + b_r; done_t = sigmoid(w_d.h_{t+1} + b_d) > u
  *      (stream 3) if WM_FLAG_DONE, else 0.
  * A done trajectory is frozen for the remaining steps: action -1, reward 0,

@@ -348,9 +348,11 @@ __device__ __forceinline__ MdnNoise mixture_noise(const Rng& rng, int K, uint32_
   return n;
 }
 
+// sig scales the normal deviate (1 = plain mixture; sqrt(tau) for the
+// sigma temperature)
 template <int Q>
 __device__ __forceinline__ float mixture_pick(int K, float tau, const MdnNoise& n,
-                                              const float (&feat)[4 * Q]) {
+                                              const float (&feat)[4 * Q], float sig = 1.0f) {
   float best = -INFINITY;
   int kbest = 0;
   if (tau == 1.0f) {  // x / 1 == x: the same scores without the divisions
@@ -376,7 +378,7 @@ __device__ __forceinline__ float mixture_pick(int K, float tau, const MdnNoise& 
     if (f == K + kbest) mu = feat[f];
     if (f == 2 * K + kbest) ls = feat[f];
   }
-  return mu + expf(ls) * n.eps;
+  return mu + expf(ls) * (n.eps * sig);
 }
 
 // ---------------------------------------------------------------------------

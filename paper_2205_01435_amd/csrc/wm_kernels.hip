@@ -718,6 +718,7 @@ struct MdnArgs {
   float* z_next;        // [M, Z]
   uint32_t k0, k1, step, traj0;
   float tau;
+  float sig;  // scale of the normal deviate: sqrt(tau) with the sigma temperature, else 1
   // nll
   const float* z_tgt;  // [M, Z]
   float* part;         // [M, ntd]
@@ -736,7 +737,7 @@ __device__ __forceinline__ MdnNoise mdn_noise(const MdnArgs& p, const Rng& rng, 
 template <int Q>
 __device__ __forceinline__ float mdn_pick(const MdnArgs& p, const MdnNoise& n,
                                           const float (&feat)[4 * Q], int K) {
-  return mixture_pick<Q>(K, p.tau, n, feat);
+  return mixture_pick<Q>(K, p.tau, n, feat, p.sig);
 }
 
 template <int Q>
@@ -1981,6 +1982,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ma.ldx = L.ldx;
   ma.H = H; ma.Z = Z; ma.K = L.K; ma.Nm = L.Nm; ma.M = B;
   ma.k0 = R.k0; ma.k1 = R.k1; ma.traj0 = R.traj0; ma.tau = R.tau;
+  ma.sig = (R.flags & 4u) ? sqrtf(R.tau) : 1.0f;
   ma.nll_mode = 0;
   const int mdn_tiles = Z / 8;
 

@@ -65,6 +65,7 @@ struct PArgs {
   int B, T, Bx;
   uint32_t k0, k1, traj0, step0;
   float tau;
+  float sig;  // scale of the normal deviate (sqrt(tau) with the sigma temperature, else 1)
   int use_done, wat_lds, wcz_lds;
   float* X;             // rollout [2, B, ldx]; NLL [T+1, B, ldx]
   float* c;             // [B, H]: initial cell state in, final state out (rollout)
@@ -464,7 +465,7 @@ __device__ __forceinline__ void mdn_phase(const PArgs& p, char* lds, int t, floa
           }
           feat[4 * q] = v[0]; feat[4 * q + 1] = v[1]; feat[4 * q + 2] = v[2]; feat[4 * q + 3] = v[3];
         }
-        z = mixture_pick<kMaxQ>(p.K, p.tau, nz, feat);
+        z = mixture_pick<kMaxQ>(p.K, p.tau, nz, feat, p.sig);
       }
       bstore4(rzn, (uint32_t)(ml * Z + j) * 4u, __float_as_uint(z));
       bstore4(rx, (uint32_t)ml * ldxb + (uint32_t)j * 4u, __float_as_uint(z));
@@ -887,6 +888,7 @@ hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStre
   PArgs a = base_args(P, pl, R.B, R.T);
   a.k0 = R.k0; a.k1 = R.k1; a.traj0 = R.traj0; a.step0 = R.step0;
   a.tau = R.tau;
+  a.sig = (R.flags & 4u) ? sqrtf(R.tau) : 1.0f;
   a.use_done = (R.flags & 1u) != 0;
   a.X = reinterpret_cast<float*>(R.x);
   a.c = R.c;

@@ -59,7 +59,7 @@ class TieCounter:
 
 
 def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, step0=0,
-               done0=None):
+               done0=None, sigma_tau=False):
     """Re-anchored comparison of a device rollout.
 
     ``g`` holds the device's z_out, actions, rewards, dones, h_trace and
@@ -89,7 +89,7 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
         sel = idx
         r = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], mask[sel], seed=seed,
                            traj=traj[sel], step=step0 + t, tau=tau, done_flag=done_flag,
-                           dtype=dtype, h_next=g["h_trace"][t + 1][sel])
+                           dtype=dtype, h_next=g["h_trace"][t + 1][sel], sigma_tau=sigma_tau)
         # actions
         ag = a_g[idx]
         ties.draws += idx.size
@@ -102,7 +102,8 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
             ties.mismatches += int(diff.sum())
             r2 = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], mask[sel], seed=seed,
                                 traj=traj[sel], step=step0 + t, tau=tau, done_flag=done_flag,
-                                dtype=dtype, h_next=g["h_trace"][t + 1][sel], action=ag)
+                                dtype=dtype, h_next=g["h_trace"][t + 1][sel], action=ag,
+                                sigma_tau=sigma_tau)
             r["h"], r["c"] = r2["h"], r2["c"]
         ok = ag >= 0
         # state
