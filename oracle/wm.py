@@ -280,7 +280,9 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
     traj0 + b for its random streams.  A trajectory that is done (input flag,
     a sampled done, or no valid action) is frozen afterwards: action -1,
     reward 0, done 1, z copied, state (z, h, c) unchanged.  A row with no
-    valid action ends at that step with the same frozen outputs.
+    valid action ends at that step with the same frozen outputs.  ``mask`` is
+    [B, A] for every step, or [T, B, A] with one mask per step (the valid
+    actions depend on the state, section 3.1.3).
 
     Returns z_out [T+1, B, Z], actions [T, B], rewards [T, B], dones [T, B],
     h_T, c_T [B, H], done_T [B], the state trace h_trace, c_trace [T+1, B, H]
@@ -313,7 +315,8 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
         h_trace[t], c_trace[t] = h, c
         live = np.nonzero(~done)[0]
         if live.size:
-            r = transition(wb, dims, z[live], h[live], c[live], mask[live], seed=seed,
+            mask_t = mask[t] if mask.ndim == 3 else mask  # per-step masks: [T, B, A]
+            r = transition(wb, dims, z[live], h[live], c[live], mask_t[live], seed=seed,
                            traj=traj0 + live, step=step0 + t, tau=tau,
                            done_flag=done_flag, dtype=dtype, sigma_tau=sigma_tau)
             ok = r["action"] >= 0

@@ -393,6 +393,31 @@ def test_tau_scales_pi_logits_only():
         np.testing.assert_array_equal(r["z"], ref)
 
 
+def test_per_step_masks():
+    """A [T, B, A] mask repeating the [B, A] one changes nothing; one-hot
+    step masks force the action of every live step; masked actions are never
+    taken under the step's own mask."""
+    w, d = _rollout_case(B=10, T=5)
+    kw = dict(T=w.T, seed=3, tau=1.0, done_flag=True, dtype="fp32")
+    ref = wm.rollout(d["weights"], w.dims, d["z0"], d["mask"], **kw)
+    rep = wm.rollout(d["weights"], w.dims, d["z0"], np.broadcast_to(d["mask"], (w.T,) + d["mask"].shape), **kw)
+    for k in ("z_out", "actions", "rewards", "dones"):
+        np.testing.assert_array_equal(ref[k], rep[k])
+    rng = np.random.default_rng(4)
+    forced = rng.integers(0, w.A, size=(w.T, w.B))
+    onehot = np.zeros((w.T, w.B, w.A), np.uint8)
+    np.put_along_axis(onehot, forced[..., None], 1, axis=-1)
+    r = wm.rollout(d["weights"], w.dims, d["z0"], onehot, **kw)
+    live = r["actions"] >= 0
+    assert live[0].all()
+    np.testing.assert_array_equal(r["actions"][live], forced[live])
+    sm = (rng.random((w.T, w.B, w.A)) < 0.5).astype(np.uint8)
+    sm[..., 0] = 1
+    r = wm.rollout(d["weights"], w.dims, d["z0"], sm, **kw)
+    tt, bb = np.nonzero(r["actions"] >= 0)
+    assert np.all(sm[tt, bb, r["actions"][tt, bb]] == 1)
+
+
 def test_sigma_tau_scales_the_spread_only():
     """With sigma_tau the draw is mu + sqrt(tau) sigma eps: at tau = 1 nothing
     changes; at tau = 2.25 the component picks, means and eps stay, and with
