@@ -65,11 +65,14 @@ typedef enum {
 enum {
   WM_FLAG_DONE = 1u, /* sample the done head; else dones are 0 while live */
   WM_FLAG_TRACE = 2u, /* write h_trace / c_trace                           */
-  WM_FLAG_SIGMA_TAU = 4u /* also scale the mixture's standard deviation by
+  WM_FLAG_SIGMA_TAU = 4u, /* also scale the mixture's standard deviation by
                             sqrt(tau) (the temperature of Ha and
                             Schmidhuber's World Models, on which section 3.3
                             builds); without it tau acts on the pi-logits
                             only, as the paper specifies                    */
+  WM_FLAG_STEP_MASK = 8u /* valid_mask is [T, B, A], one mask per step (the
+                            valid actions depend on the state, section
+                            3.1.3); else [B, A] for every step              */
 };
 
 typedef struct {
@@ -156,7 +159,9 @@ wm_status wm_controller_step(const wm_dims *dims, const void *packed, int32_t B,
  *   h0, c0 [B, H]        float32 initial state, nullable (= 0).
  *   done_io [B]          uint8, nullable: in = already done, out = done
  *                        after the last step.
- *   valid_mask [B, A]    uint8, constant over the rollout.
+ *   valid_mask [B, A]    uint8, constant over the rollout; with
+ *                        WM_FLAG_STEP_MASK [T, B, A], step t's actions
+ *                        drawn from valid_mask[t].
  *   tau                  mixture temperature, finite and > 0.
  *   z_out [T+1, B, Z]    float32; z_out[0] = z0.
  *   actions [T, B]       int32.   rewards [T, B] float32.   dones [T, B] uint8.

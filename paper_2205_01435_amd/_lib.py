@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libwm.so")
 
 WM_OK, WM_ERR_INVALID_ARG, WM_ERR_UNSUPPORTED, WM_ERR_WORKSPACE, WM_ERR_HIP = 0, -1, -2, -3, -4
 WM_FP32, WM_BF16 = 0, 1
-WM_FLAG_DONE, WM_FLAG_TRACE, WM_FLAG_SIGMA_TAU = 1, 2, 4
+WM_FLAG_DONE, WM_FLAG_TRACE, WM_FLAG_SIGMA_TAU, WM_FLAG_STEP_MASK = 1, 2, 4, 8
 _DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
 
 # Every symbol the C header declares.
@@ -187,13 +187,17 @@ def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bo
             traj0: int = 0, step0: int = 0, h0=None, c0=None, done_io=None, trace: bool = False,
             bufs: RolloutBuffers | None = None, sigma_tau: bool = False) -> RolloutBuffers:
     """Launch wm_rollout on the current stream; returns the filled buffers
-    (``sigma_tau`` sets WM_FLAG_SIGMA_TAU)."""
+    (``sigma_tau`` sets WM_FLAG_SIGMA_TAU; a [T, B, A] mask sets
+    WM_FLAG_STEP_MASK)."""
     lib = load()
     B = z0.shape[0]
+    want = (T, B, m.dims.A) if mask.dim() == 3 else (B, m.dims.A)
+    if tuple(mask.shape) != want:
+        raise ValueError(f"mask has shape {tuple(mask.shape)}, expected {want}")
     if bufs is None:
         bufs = RolloutBuffers(m, B, T, trace=trace)
     flags = (WM_FLAG_DONE if done else 0) | (WM_FLAG_TRACE if trace else 0) | \
-        (WM_FLAG_SIGMA_TAU if sigma_tau else 0)
+        (WM_FLAG_SIGMA_TAU if sigma_tau else 0) | (WM_FLAG_STEP_MASK if mask.dim() == 3 else 0)
     _check(lib.wm_rollout(
         ctypes.byref(m.dims), _ptr(m.packed), B, T, traj0, step0, _ptr(z0), _ptr(h0), _ptr(c0),
         _ptr(done_io), _ptr(mask), seed, tau, flags, _ptr(bufs.z_out), _ptr(bufs.actions),

@@ -137,7 +137,7 @@ wm_status wm_rollout(const wm_dims* dims, const void* packed, int32_t B, int32_t
   if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
   if (T < 0) return fail(WM_ERR_INVALID_ARG, "T=%d must not be negative", T);
   if (!(tau > 0.0f) || !isfinite(tau)) return fail(WM_ERR_INVALID_ARG, "tau must be finite and > 0");
-  if (flags & ~(uint32_t)(WM_FLAG_DONE | WM_FLAG_TRACE | WM_FLAG_SIGMA_TAU))
+  if (flags & ~(uint32_t)(WM_FLAG_DONE | WM_FLAG_TRACE | WM_FLAG_SIGMA_TAU | WM_FLAG_STEP_MASK))
     return fail(WM_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
   if (!z0 || !valid_mask || !z_out || !actions || !rewards || !dones)
     return fail(WM_ERR_INVALID_ARG, "z0, valid_mask, z_out, actions, rewards, dones are required");

@@ -1993,6 +1993,8 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
     ca.x = Xt;
     ca.step = step;
     ca.mode = t < T ? 1 : 2;
+    // step t's [B, A] slice of a per-step mask (the tail step draws no action)
+    ca.mask = (R.flags & 8u) ? R.mask + (long)(t < T ? t : T - 1) * B * L.A : R.mask;
     ca.act_t = t < T ? R.actions + (long)t * B : nullptr;
     ca.rew_t = t < T ? R.rewards + (long)t * B : nullptr;
     ca.done_t = t < T ? R.dones + (long)t * B : nullptr;

@@ -72,7 +72,8 @@ struct PArgs {
   int32_t* done_state;  // [B]
   float* P;             // [32, B, Nc] controller partial logits (rollout)
   unsigned* sync;       // kSyncWords words, zero at launch
-  const uint8_t* mask;  // [B, A]
+  const uint8_t* mask;  // [B, A], or [T, B, A] with step_mask
+  int step_mask;
   float* z_out;         // [T+1, B, Z]
   int32_t* actions;     // [T, B]: rollout output, NLL input
   float* rewards;
@@ -555,7 +556,8 @@ __device__ __forceinline__ void ctrl_phase(const PArgs& p, char* lds, int t, con
   // masked Gumbel-max over the valid actions, lowest index on ties
   float best = -INFINITY;
   int bidx = -1;
-  if (!tail && rowok && a < A && p.mask[(long)m * A + a]) {
+  const uint8_t* mask = p.mask + (p.step_mask && !tail ? (long)t * B * A : 0);  // [B, A] of step t
+  if (!tail && rowok && a < A && mask[(long)m * A + a]) {
     const uint4 w = rng.block((uint32_t)a >> 2, step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
     best = l + gumbel(word_to_uniform(word_of(w, a & 3)));
     bidx = a;
@@ -889,6 +891,7 @@ hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStre
   a.k0 = R.k0; a.k1 = R.k1; a.traj0 = R.traj0; a.step0 = R.step0;
   a.tau = R.tau;
   a.sig = (R.flags & 4u) ? sqrtf(R.tau) : 1.0f;
+  a.step_mask = (R.flags & 8u) != 0;
   a.use_done = (R.flags & 1u) != 0;
   a.X = reinterpret_cast<float*>(R.x);
   a.c = R.c;

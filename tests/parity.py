@@ -64,7 +64,7 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
 
     ``g`` holds the device's z_out, actions, rewards, dones, h_trace and
     c_trace for some trajectories (batch axis of length n), ``mask [n, A]``
-    their masks and ``traj [n]`` their trajectory indices (default 0..n-1).
+    (or [T, n, A] per step) their masks and ``traj [n]`` their trajectory indices (default 0..n-1).
     """
     T = g["actions"].shape[0]
     n = g["actions"].shape[1]
@@ -87,7 +87,8 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
             continue
         n_live_steps += idx.size
         sel = idx
-        r = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], mask[sel], seed=seed,
+        mask_t = mask[t] if mask.ndim == 3 else mask  # per-step masks: [T, n, A]
+        r = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], mask_t[sel], seed=seed,
                            traj=traj[sel], step=step0 + t, tau=tau, done_flag=done_flag,
                            dtype=dtype, h_next=g["h_trace"][t + 1][sel], sigma_tau=sigma_tau)
         # actions
@@ -100,7 +101,7 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
                                 f"gpu={ag[diff][~near]} ref={r['action'][diff][~near]}, "
                                 f"margin={r['action_margin'][diff][~near]}")
             ties.mismatches += int(diff.sum())
-            r2 = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], mask[sel], seed=seed,
+            r2 = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], mask_t[sel], seed=seed,
                                 traj=traj[sel], step=step0 + t, tau=tau, done_flag=done_flag,
                                 dtype=dtype, h_next=g["h_trace"][t + 1][sel], action=ag,
                                 sigma_tau=sigma_tau)
