@@ -615,6 +615,16 @@ __device__ __forceinline__ void ctrl_phase(const PArgs& p, char* lds, int t, con
 // ---------------------------------------------------------------------------
 // The kernel.
 // ---------------------------------------------------------------------------
+// The kernel's arguments read again from the kernel-argument segment through
+// a pointer the compiler cannot see through: values derived from them
+// (buffer resources, offsets) are then recomputed in each phase instead of
+// being kept across the step loop in scalar registers, which spilled.
+__device__ __forceinline__ const PArgs& fresh_args() {
+  auto a = (const __attribute__((address_space(4))) PArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(a));
+  return *(const PArgs*)a;
+}
+
 template <int RB, int NBC, bool NLL>
 __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
   // no static LDS: the dynamic region starts at LDS address 0, so that the
@@ -715,19 +725,21 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
   const long BX = (long)p.B * p.ldx;
   if constexpr (NLL) {
     for (int t = 0; t < p.T; ++t) {
-      gates_phase<RB, NBC, true>(p, st, lds, t, p.X + (long)t * BX, p.X + (long)(t + 1) * BX, r0, nrows);
+      const PArgs& q = fresh_args();
+      gates_phase<RB, NBC, true>(q, st, lds, t, q.X + (long)t * BX, q.X + (long)(t + 1) * BX, r0, nrows);
       if (t + 1 < p.T && !group_sync(gs, &s_flag)) return;
     }
   } else {
     for (int t = 0;; ++t) {
-      float* Xt = p.X + (long)(t & 1) * BX;
-      float* Xn = p.X + (long)((t + 1) & 1) * BX;
-      ctrl_phase(p, lds, t, Xt, r0, nrows);
+      const PArgs& q = fresh_args();
+      float* Xt = q.X + (long)(t & 1) * BX;
+      float* Xn = q.X + (long)((t + 1) & 1) * BX;
+      ctrl_phase(q, lds, t, Xt, r0, nrows);
       if (t == p.T) break;
       if (!group_sync(gs, &s_flag)) return;
-      gates_phase<RB, NBC, false>(p, st, lds, t, Xt, Xn, r0, nrows);
+      gates_phase<RB, NBC, false>(fresh_args(), st, lds, t, Xt, Xn, r0, nrows);
       if (!group_sync(gs, &s_flag)) return;
-      mdn_phase(p, lds, t, Xn, r0, nrows);
+      mdn_phase(fresh_args(), lds, t, Xn, r0, nrows);
       if (!group_sync(gs, &s_flag)) return;
     }
     // final cell state for k_rollout_finish
