@@ -90,7 +90,7 @@ def test_rollout_argument_checks():
     assert _rollout_call(tau=float("nan")) == wmlib.WM_ERR_INVALID_ARG
     assert _rollout_call(B=0) == wmlib.WM_ERR_INVALID_ARG
     assert _rollout_call(T=-1) == wmlib.WM_ERR_INVALID_ARG
-    assert _rollout_call(flags=8) == wmlib.WM_ERR_INVALID_ARG
+    assert _rollout_call(flags=16) == wmlib.WM_ERR_INVALID_ARG  # flags above WM_FLAG_STEP_MASK
     assert _rollout_call(flags=3) == wmlib.WM_ERR_INVALID_ARG  # trace without buffers
     assert _rollout_call(z_out=ctypes.c_void_p(4100)) == wmlib.WM_ERR_INVALID_ARG  # misaligned
     assert _rollout_call(packed=ctypes.c_void_p(4112)) == wmlib.WM_ERR_INVALID_ARG
