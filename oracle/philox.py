@@ -39,6 +39,7 @@ STREAM_CONTROLLER = 0
 STREAM_COMPONENT = 1
 STREAM_GAUSS = 2
 STREAM_DONE = 3
+STREAM_LOCATION = 4  # two-level controller: the location draw
 
 
 def philox4x32_10(counter, key) -> np.ndarray:

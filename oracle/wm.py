@@ -60,8 +60,8 @@ def weight_blocks(w: dict, Z: int, H: int, A: int, K: int, dtype: str) -> dict:
         Wz=Wg[:, :Z], Wa=Wg[:, Z:Z + A], Wh=Wg[:, Z + A:],
         b_g=np.asarray(w["b_g"], np.float64),
         W_m=q(w["W_m"], dtype), b_m=np.asarray(w["b_m"], np.float64),
-        w_r=q(w["w_r"], dtype), b_r=float(w["b_r"]),
-        w_d=q(w["w_d"], dtype), b_d=float(w["b_d"]),
+        w_r=q(w["w_r"], dtype), b_r=float(np.asarray(w["b_r"]).reshape(-1)[0]),
+        w_d=q(w["w_d"], dtype), b_d=float(np.asarray(w["b_d"]).reshape(-1)[0]),
         W_c=q(w["W_c"], dtype), b_c=np.asarray(w["b_c"], np.float64),
     )
 
@@ -106,6 +106,36 @@ def controller_logits(wb: dict, z, h, dtype: str) -> np.ndarray:
     """Section 3.4: logits = W_c [z_t, h_t] + b_c on the storage-rounded state."""
     x = np.concatenate([q(z, dtype), q(h, dtype)], axis=-1)
     return x @ wb["W_c"].T + wb["b_c"]
+
+
+def two_level_action(logits, xmask, lmask, *, seed: int, traj, step: int, N: int, L: int):
+    """The two-level action of section 3.1.3: the controller first picks a
+    graph transformation (xfer) among the valid ones, index N being the NO-OP
+    that ends the episode, then a location among those valid for that xfer.
+
+    ``logits [n, N+1+L]``: xfer logits (N+1) then location logits (L), from
+    the same controller input; ``xmask [n, N+1]``, ``lmask [n, N, L]``.
+    Each pick is a Gumbel-max (xfers on stream 0, index x; locations on
+    stream 4, index l).  Returns ``(a, margin, top)``: the flat action
+    a = x L + l of the world model's one-hot input, -2 for the NO-OP, -1 when
+    no xfer (or no location of the chosen xfer) is valid; and the margin and
+    top score of the pick with the smaller relative margin, for near-tie
+    checks.
+    """
+    logits = np.asarray(logits, np.float64)
+    n = logits.shape[0]
+    xmask = np.asarray(xmask) != 0
+    lmask = np.asarray(lmask) != 0
+    u0 = ph.stream_uniforms(seed, traj, step, ph.STREAM_CONTROLLER, N + 1)
+    x, xm, xt = argmax_fp32(logits[:, :N + 1] + gumbel(u0), xmask)
+    u4 = ph.stream_uniforms(seed, traj, step, ph.STREAM_LOCATION, L)
+    rows = lmask[np.arange(n), np.clip(x, 0, max(N - 1, 0))]
+    loc, lm, lt = argmax_fp32(logits[:, N + 1:] + gumbel(u4), rows)
+    xfer = (x >= 0) & (x < N)
+    a = np.where(x < 0, -1, np.where(x == N, -2, np.where(loc < 0, -1, x * L + loc)))
+    with np.errstate(invalid="ignore"):
+        use_l = xfer & (lm / (1 + np.abs(lt)) < xm / (1 + np.abs(xt)))
+    return a.astype(np.int64), np.where(use_l, lm, xm), np.where(use_l, lt, xt)
 
 
 def masked_softmax(logits, mask) -> np.ndarray:
@@ -205,7 +235,7 @@ def softplus(x):
 
 def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: int,
                tau: float = 1.0, done_flag: bool = True, dtype: str = "fp32",
-               action=None, h_next=None, sigma_tau: bool = False) -> dict:
+               action=None, h_next=None, sigma_tau: bool = False, two_level=None) -> dict:
     """One dream step for a batch of live rows (sections 3.4 and 3.3.2).
 
     1. controller logits on [z_t, h_t] and a masked Gumbel-max action
@@ -221,6 +251,8 @@ def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: in
     6. reward = rho_r; done = sigmoid(rho_d) > u (stream 3) when enabled.
 
     ``action`` overrides the controller's choice in step 2 (re-anchoring).
+    With ``two_level = (N, L)`` the controller is the two-level one of
+    ``two_level_action`` and ``mask`` is the pair (xfer mask, location mask).
     """
     Z, H, A, K = dims["Z"], dims["H"], dims["A"], dims["K"]
     z = np.asarray(z, np.float64)
@@ -230,8 +262,12 @@ def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: in
     n = z.shape[0]
 
     logits = controller_logits(wb, z, h, dtype)
-    u0 = ph.stream_uniforms(seed, traj, step, ph.STREAM_CONTROLLER, A)
-    a, a_margin, a_top = argmax_fp32(logits + gumbel(u0), np.asarray(mask) != 0)
+    if two_level is not None:
+        a, a_margin, a_top = two_level_action(logits, mask[0], mask[1], seed=seed, traj=traj,
+                                              step=step, N=two_level[0], L=two_level[1])
+    else:
+        u0 = ph.stream_uniforms(seed, traj, step, ph.STREAM_CONTROLLER, A)
+        a, a_margin, a_top = argmax_fp32(logits + gumbel(u0), np.asarray(mask) != 0)
     a_used = a if action is None else np.asarray(action, np.int64)
 
     g = gate_preactivations(wb, z, h, a_used, dtype)
@@ -272,7 +308,7 @@ def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: in
 
 def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.0,
             done_flag: bool = True, dtype: str = "fp32", traj0: int = 0, step0: int = 0,
-            h0=None, c0=None, done0=None, sigma_tau: bool = False) -> dict:
+            h0=None, c0=None, done0=None, sigma_tau: bool = False, two_level=None) -> dict:
     """B dream trajectories of T steps (the "hallucinated" environment of
     section 3.3 driven by the controller of section 3.4).
 
@@ -282,7 +318,10 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
     reward 0, done 1, z copied, state (z, h, c) unchanged.  A row with no
     valid action ends at that step with the same frozen outputs.  ``mask`` is
     [B, A] for every step, or [T, B, A] with one mask per step (the valid
-    actions depend on the state, section 3.1.3).
+    actions depend on the state, section 3.1.3).  With ``two_level = (N, L)``
+    the controller is two-level (``two_level_action``), ``mask`` is the pair
+    (xfer mask [B, N+1], location mask [B, N, L]) and a NO-OP ends the
+    trajectory with action -2 at that step.
 
     Returns z_out [T+1, B, Z], actions [T, B], rewards [T, B], dones [T, B],
     h_T, c_T [B, H], done_T [B], the state trace h_trace, c_trace [T+1, B, H]
@@ -294,7 +333,8 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
     wb = weight_blocks(w, Z, H, A, K, dtype)
     z0 = np.asarray(z0, np.float64)
     B = z0.shape[0]
-    mask = np.asarray(mask)
+    if two_level is None:
+        mask = np.asarray(mask)
     z = z0.copy()
     h = np.zeros((B, H)) if h0 is None else q(h0, dtype)
     c = np.zeros((B, H)) if c0 is None else np.asarray(c0, np.float64).copy()
@@ -315,10 +355,15 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
         h_trace[t], c_trace[t] = h, c
         live = np.nonzero(~done)[0]
         if live.size:
-            mask_t = mask[t] if mask.ndim == 3 else mask  # per-step masks: [T, B, A]
-            r = transition(wb, dims, z[live], h[live], c[live], mask_t[live], seed=seed,
+            if two_level is not None:
+                mask_l = (np.asarray(mask[0])[live], np.asarray(mask[1])[live])
+            else:
+                mask_t = mask[t] if mask.ndim == 3 else mask  # per-step masks: [T, B, A]
+                mask_l = mask_t[live]
+            r = transition(wb, dims, z[live], h[live], c[live], mask_l, seed=seed,
                            traj=traj0 + live, step=step0 + t, tau=tau,
-                           done_flag=done_flag, dtype=dtype, sigma_tau=sigma_tau)
+                           done_flag=done_flag, dtype=dtype, sigma_tau=sigma_tau,
+                           two_level=two_level)
             ok = r["action"] >= 0
             a_margin[t, live] = r["action_margin"]
             rows = live[ok]
@@ -332,6 +377,7 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
             c[rows] = r["c"][ok]
             done[rows] = r["done"][ok]
             done[live[~ok]] = True
+            actions[t, live[r["action"] == -2]] = -2  # the NO-OP ended these
         z_out[t + 1] = z
     h_trace[T], c_trace[T] = h, c
     return dict(z_out=z_out, actions=actions, rewards=rewards, dones=dones,

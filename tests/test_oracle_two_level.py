@@ -1,0 +1,96 @@
+"""Pins of the oracle's two-level controller (xfer, then location; NO-OP
+ends the episode) against forced choices, the masks and the softmax
+distributions the Gumbel-max draws must follow."""
+
+import numpy as np
+from scipy import stats
+
+from oracle import wm
+
+N, L = 3, 5
+
+
+def _logits(n, seed):
+    return np.random.default_rng(seed).normal(size=(n, N + 1 + L))
+
+
+def test_forced_choice_and_flat_index():
+    n = 40
+    xm = np.zeros((n, N + 1), np.uint8)
+    xm[:, 2] = 1
+    lm = np.zeros((n, N, L), np.uint8)
+    lm[:, 2, 4] = 1
+    lm[:, 0, :] = 1  # other xfers' locations do not matter
+    a, _, _ = wm.two_level_action(_logits(n, 1), xm, lm, seed=3, traj=np.arange(n), step=0, N=N, L=L)
+    np.testing.assert_array_equal(a, np.full(n, 2 * L + 4))
+
+
+def test_noop_and_empty_cases():
+    n = 20
+    lg = _logits(n, 2)
+    xm = np.zeros((n, N + 1), np.uint8)
+    xm[:, N] = 1  # only the NO-OP
+    lm = np.ones((n, N, L), np.uint8)
+    a, _, _ = wm.two_level_action(lg, xm, lm, seed=1, traj=np.arange(n), step=0, N=N, L=L)
+    assert np.all(a == -2)
+    a, _, _ = wm.two_level_action(lg, np.zeros_like(xm), lm, seed=1, traj=np.arange(n), step=0, N=N, L=L)
+    assert np.all(a == -1)
+    xm[:, N] = 0
+    xm[:, 1] = 1
+    lm[:, 1, :] = 0  # the only xfer has no valid location
+    a, _, _ = wm.two_level_action(lg, xm, lm, seed=1, traj=np.arange(n), step=0, N=N, L=L)
+    assert np.all(a == -1)
+
+
+def test_locations_valid_under_the_chosen_xfer():
+    n = 500
+    rng = np.random.default_rng(5)
+    xm = (rng.random((n, N + 1)) < 0.6).astype(np.uint8)
+    xm[:, 0] = 1
+    lm = (rng.random((n, N, L)) < 0.5).astype(np.uint8)
+    lm[:, :, 0] = 1
+    a, _, _ = wm.two_level_action(_logits(n, 6), xm, lm, seed=7, traj=np.arange(n), step=4, N=N, L=L)
+    pos = a >= 0
+    x, l = a[pos] // L, a[pos] % L
+    assert np.all(xm[pos, x] == 1) and np.all(lm[np.nonzero(pos)[0], x, l] == 1)
+    assert np.all(xm[a == -2, N] == 1)
+
+
+def test_pick_frequencies_follow_the_masked_softmaxes():
+    n = 40000
+    one = np.array([0.3, -0.5, 1.1, 0.2, 0.4, -1.0, 0.9, 0.0, 0.5])  # N+1 xfer then L location logits
+    lg = np.tile(one, (n, 1))
+    xm = np.array([1, 0, 1, 1], np.uint8)[None].repeat(n, 0)
+    lm = np.ones((n, N, L), np.uint8)
+    lm[:, 2, 1] = 0
+    a, _, _ = wm.two_level_action(lg, xm, lm, seed=11, traj=np.arange(n), step=2, N=N, L=L)
+    x = np.where(a == -2, N, a // L)
+    px = wm.masked_softmax(one[:N + 1], xm[0])
+    cnt = np.bincount(x, minlength=N + 1)
+    assert stats.chisquare(cnt[px > 0], n * px[px > 0]).pvalue > 1e-4
+    assert cnt[1] == 0
+    sel = x == 2  # locations of xfer 2 follow the softmax over its valid locations
+    pl = wm.masked_softmax(one[N + 1:], lm[0, 2])
+    cl = np.bincount(a[sel] % L, minlength=L)
+    assert stats.chisquare(cl[pl > 0], sel.sum() * pl[pl > 0]).pvalue > 1e-4
+    assert cl[1] == 0
+
+
+def test_rollout_noop_ends_the_trajectory():
+    Z, H, K, B, T = 4, 6, 2, 6, 4
+    A = N * L
+    rng = np.random.default_rng(9)
+    w = dict(W_g=rng.normal(size=(4 * H, Z + A + H)) * 0.3, b_g=np.zeros(4 * H),
+             W_m=rng.normal(size=(3 * Z * K, H)) * 0.3, b_m=np.zeros(3 * Z * K),
+             w_r=rng.normal(size=H), b_r=np.zeros(1), w_d=rng.normal(size=H), b_d=np.array([-9.0]),
+             W_c=rng.normal(size=(N + 1 + L, Z + H)), b_c=np.zeros(N + 1 + L))
+    xm = np.ones((B, N + 1), np.uint8)
+    xm[0, :N] = 0  # row 0 can only stop
+    lm = np.ones((B, N, L), np.uint8)
+    r = wm.rollout(w, dict(Z=Z, H=H, A=A, K=K), rng.normal(size=(B, Z)), (xm, lm), T=T, seed=2,
+                   two_level=(N, L))
+    assert r["actions"][0, 0] == -2 and r["rewards"][0, 0] == 0 and r["dones"][0, 0] == 1
+    assert np.all(r["actions"][1:, 0] == -1)
+    np.testing.assert_array_equal(r["z_out"][1:, 0], np.broadcast_to(r["z_out"][0, 0], (T, Z)))
+    live = r["actions"] >= 0
+    assert live[:, 1:].any() and np.all(r["actions"][live] < A)
