@@ -78,6 +78,12 @@ enum {
 typedef struct {
   int32_t Z, H, A, K;
   int32_t dtype; /* wm_dtype */
+  /* Two-level controller (section 3.1.3), 0 and 0 for the one-level one: N
+   * graph transformations (xfers) plus the NO-OP, each applied at one of L
+   * locations.  The world model's actions are the A = N * L pairs, action
+   * a = x * L + l; the controller's W_c [N+1+L, Z+H], b_c [N+1+L] hold the
+   * N+1 xfer logits (row N = NO-OP) then the L location logits.          */
+  int32_t N, L;
 } wm_dims;
 
 /*
@@ -89,7 +95,8 @@ typedef struct {
  *                    the mean (p=1) and log sigma (p=2); b_m [3ZK].
  *   w_r [H], b_r [1] reward head on h_{t+1}.
  *   w_d [H], b_d [1] done head on h_{t+1}: P(done) = sigmoid(w_d.h + b_d).
- *   W_c [A, Z+H]     controller logits on [z_t, h_t] (section 3.4); b_c [A].
+ *   W_c [Ac, Z+H]    controller logits on [z_t, h_t] (section 3.4); b_c [Ac];
+ *                    Ac = A, or N+1+L for the two-level controller.
  */
 typedef struct {
   const float *W_g, *b_g;
@@ -130,6 +137,8 @@ size_t wm_workspace_bytes(const wm_dims *dims, int32_t B, int32_t T, int32_t whi
  *   action [B]           int32; argmax over valid a of logits_a - ln(-ln u_a)
  *                        (a sample from `probs`), u_a uniform a of stream 0;
  *                        ties go to the lowest index; -1 if none is valid.
+ * The two-level controller (dims N > 0) is not served here
+ * (WM_ERR_UNSUPPORTED); it runs inside wm_rollout.
  */
 wm_status wm_controller_step(const wm_dims *dims, const void *packed, int32_t B,
                              uint32_t traj0, const float *z, const float *h,
@@ -161,7 +170,14 @@ wm_status wm_controller_step(const wm_dims *dims, const void *packed, int32_t B,
  *                        after the last step.
  *   valid_mask [B, A]    uint8, constant over the rollout; with
  *                        WM_FLAG_STEP_MASK [T, B, A], step t's actions
- *                        drawn from valid_mask[t].
+ *                        drawn from valid_mask[t].  With the two-level
+ *                        controller (dims N > 0): the xfer masks [B, N+1]
+ *                        followed by the location masks [B, N, L]; step 1
+ *                        then picks an xfer x among the valid ones (stream 0,
+ *                        index x), and for x < N a location l valid for x
+ *                        (stream 4, index l), action x * L + l; x = N (the
+ *                        NO-OP) ends the trajectory at that step with action
+ *                        -2, reward 0, done 1 (per-step masks unsupported).
  *   tau                  mixture temperature, finite and > 0.
  *   z_out [T+1, B, Z]    float32; z_out[0] = z0.
  *   actions [T, B]       int32.   rewards [T, B] float32.   dones [T, B] uint8.

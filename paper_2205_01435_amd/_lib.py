@@ -36,7 +36,8 @@ class WmError(RuntimeError):
 
 class CDims(ctypes.Structure):
     _fields_ = [("Z", ctypes.c_int32), ("H", ctypes.c_int32), ("A", ctypes.c_int32),
-                ("K", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("K", ctypes.c_int32), ("dtype", ctypes.c_int32), ("N", ctypes.c_int32),
+                ("L", ctypes.c_int32)]
 
 
 class CWeights(ctypes.Structure):
@@ -119,8 +120,9 @@ class Model:
     dtype: str
 
 
-def make_dims(Z, H, A, K, dtype="fp32") -> CDims:
-    return CDims(Z, H, A, K, _DTYPES[dtype])
+def make_dims(Z, H, A, K, dtype="fp32", N=0, L=0) -> CDims:
+    """N, L > 0: the two-level controller (N xfers + NO-OP, L locations, A = N L)."""
+    return CDims(Z, H, A, K, _DTYPES[dtype], N, L)
 
 
 def packed_bytes(dims: CDims) -> int:
@@ -132,10 +134,11 @@ def workspace_bytes(dims: CDims, B: int, T: int, which: int) -> int:
 
 
 def pack(weights: dict, Z: int, H: int, A: int, K: int, dtype: str = "fp32",
-         device="cuda") -> Model:
-    """Copy canonical float32 weights to the device and pack them."""
+         device="cuda", N: int = 0, L: int = 0) -> Model:
+    """Copy canonical float32 weights to the device and pack them (N, L > 0:
+    the two-level controller, W_c [N+1+L, Z+H])."""
     lib = load()
-    dims = make_dims(Z, H, A, K, dtype)
+    dims = make_dims(Z, H, A, K, dtype, N, L)
     n = lib.wm_packed_bytes(ctypes.byref(dims))
     if n == 0:
         raise WmError(WM_ERR_UNSUPPORTED, lib.wm_last_error().decode())
@@ -191,9 +194,19 @@ def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bo
     WM_FLAG_STEP_MASK)."""
     lib = load()
     B = z0.shape[0]
-    want = (T, B, m.dims.A) if mask.dim() == 3 else (B, m.dims.A)
-    if tuple(mask.shape) != want:
-        raise ValueError(f"mask has shape {tuple(mask.shape)}, expected {want}")
+    if m.dims.N > 0:
+        # two-level controller: (xfer mask [B, N+1], location mask [B, N, L])
+        # as one buffer, xfer masks first
+        xm, lm = mask
+        N, L = m.dims.N, m.dims.L
+        if tuple(xm.shape) != (B, N + 1) or tuple(lm.shape) != (B, N, L):
+            raise ValueError(f"two-level masks {tuple(xm.shape)}, {tuple(lm.shape)}; expected "
+                             f"{(B, N + 1)}, {(B, N, L)}")
+        mask = torch.cat([xm.reshape(-1), lm.reshape(-1)]).contiguous()
+    else:
+        want = (T, B, m.dims.A) if mask.dim() == 3 else (B, m.dims.A)
+        if tuple(mask.shape) != want:
+            raise ValueError(f"mask has shape {tuple(mask.shape)}, expected {want}")
     if bufs is None:
         bufs = RolloutBuffers(m, B, T, trace=trace)
     flags = (WM_FLAG_DONE if done else 0) | (WM_FLAG_TRACE if trace else 0) | \

@@ -52,7 +52,13 @@ wm_status check_dims(const wm_dims* d, wm::Layout* L) {
     return fail(WM_ERR_UNSUPPORTED, "H=%d: kernels need H a multiple of 16, at most 8192", d->H);
   if (d->A > 2048) return fail(WM_ERR_UNSUPPORTED, "A=%d: at most 2048 actions", d->A);
   if (d->K > 8) return fail(WM_ERR_UNSUPPORTED, "K=%d: at most 8 components", d->K);
-  *L = wm::make_layout(d->Z, d->H, d->A, d->K, d->dtype);
+  if (d->N < 0 || d->L < 0 || (d->N == 0) != (d->L == 0))
+    return fail(WM_ERR_INVALID_ARG, "N=%d and L=%d must both be 0 or both positive", d->N, d->L);
+  if (d->N > 0 && (int64_t)d->N * d->L != d->A)
+    return fail(WM_ERR_INVALID_ARG, "two-level controller: A=%d must equal N*L=%d*%d", d->A, d->N, d->L);
+  if (d->N > 0 && d->N + 1 + d->L > 318)
+    return fail(WM_ERR_UNSUPPORTED, "two-level controller: N+1+L=%d above 318 logits", d->N + 1 + d->L);
+  *L = wm::make_layout(d->Z, d->H, d->A, d->K, d->dtype, d->N, d->L);
   return WM_OK;
 }
 
@@ -112,6 +118,7 @@ wm_status wm_controller_step(const wm_dims* dims, const void* packed, int32_t B,
   wm_status st = check_dims(dims, &L);
   if (st != WM_OK) return st;
   if ((st = check_packed(L, packed)) != WM_OK) return st;
+  if (L.N > 0) return fail(WM_ERR_UNSUPPORTED, "wm_controller_step: the two-level controller runs in rollouts only");
   if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
   if (!z || !h || !valid_mask || !action)
     return fail(WM_ERR_INVALID_ARG, "z, h, valid_mask and action are required");
@@ -141,6 +148,8 @@ wm_status wm_rollout(const wm_dims* dims, const void* packed, int32_t B, int32_t
     return fail(WM_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
   if (!z0 || !valid_mask || !z_out || !actions || !rewards || !dones)
     return fail(WM_ERR_INVALID_ARG, "z0, valid_mask, z_out, actions, rewards, dones are required");
+  if (L.N > 0 && (flags & WM_FLAG_STEP_MASK))
+    return fail(WM_ERR_UNSUPPORTED, "per-step masks with the two-level controller");
   if ((flags & WM_FLAG_TRACE) && (!h_trace || !c_trace))
     return fail(WM_ERR_INVALID_ARG, "WM_FLAG_TRACE needs h_trace and c_trace");
   if (!aligned16(z0) || !aligned16(z_out))

@@ -135,7 +135,13 @@ __device__ __forceinline__ float ftanh_cell(float x) {
   else return ftanh_abs(x);
 }
 
-enum : uint32_t { STREAM_CONTROLLER = 0, STREAM_COMPONENT = 1, STREAM_GAUSS = 2, STREAM_DONE = 3 };
+enum : uint32_t {
+  STREAM_CONTROLLER = 0,  // controller Gumbel noise (action, or xfer of the two-level controller)
+  STREAM_COMPONENT = 1,
+  STREAM_GAUSS = 2,
+  STREAM_DONE = 3,
+  STREAM_LOCATION = 4     // two-level controller: location Gumbel noise
+};
 
 // ---------------------------------------------------------------------------
 // MFMA step on one 16-byte fragment per operand.

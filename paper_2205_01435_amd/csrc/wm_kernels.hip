@@ -101,15 +101,16 @@ __global__ void k_pack(const Layout L, char* base, const float* __restrict__ W_g
       const int row = (int)(idx / L.ldk), col = (int)(idx % L.ldk);
       float v = 0.f;
       if (col < Z + H) {
-        if (row < A) v = W_c[(long)row * (Z + H) + col];
-        else if (row == A && col >= Z) v = w_r[col - Z];
-        else if (row == A + 1 && col >= Z) v = w_d[col - Z];
+        const int Ac = L.Ac;
+        if (row < Ac) v = W_c[(long)row * (Z + H) + col];
+        else if (row == Ac && col >= Z) v = w_r[col - Z];
+        else if (row == Ac + 1 && col >= Z) v = w_d[col - Z];
       }
       DType<DT>::store(Wc, idx, v);
     }
   } else {
     for (long idx = i0; idx < L.Nc; idx += stride)
-      bc[idx] = idx < A ? b_c[idx] : (idx == A ? b_r[0] : (idx == A + 1 ? b_d[0] : 0.f));
+      bc[idx] = idx < L.Ac ? b_c[idx] : (idx == L.Ac ? b_r[0] : (idx == L.Ac + 1 ? b_d[0] : 0.f));
   }
 }
 
@@ -939,6 +940,10 @@ struct CtrlArgs {
   uint8_t* done_t;
   int32_t* done_state;
   int use_done;
+  // two-level controller (N > 0, rollout modes): mask holds the xfer masks
+  // [M, N+1] followed by the location masks [M, N, Lc]; the logits are the
+  // N+1 xfer rows then the Lc location rows
+  int N, Lc;
 };
 
 // Rollout bookkeeping of row m at step t (modes 1 and 2 of the controller
@@ -970,6 +975,52 @@ __device__ __forceinline__ void ctrl_row_commit(const CtrlArgs& p, const Rng& rn
     }
   }
   p.done_state[m] = ds;
+}
+
+// Two-level pick of row m (section 3.1.3) by its TPR threads (thread q of
+// the row), from its logits lg (bias not yet added): an xfer among the valid
+// ones (stream 0, index x; x = N is the NO-OP), then a location valid for
+// that xfer (stream 4, index l).  Returns the flat action x Lc + l, -2 for
+// the NO-OP, -1 when nothing is valid; the same value in every thread of the
+// row.  Ties go to the lowest index.
+template <int TPR>
+__device__ __forceinline__ int two_level_pick(const CtrlArgs& p, const Rng& rng, const float* lg,
+                                              int m, bool on, int q, uint32_t traj) {
+  const int N = p.N, NX = N + 1, Lc = p.Lc;
+  auto reduce = [](float& best, int& bidx) {
+#pragma unroll
+    for (int off = 1; off < TPR; off <<= 1) {
+      const float ob = __shfl_xor(best, off);
+      const int oi = __shfl_xor(bidx, off);
+      if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
+    }
+  };
+  float best = -INFINITY;
+  int x = -1;
+  if (on) {
+    for (int i = q; i < NX; i += TPR) {
+      if (!p.mask[(long)m * NX + i]) continue;
+      const uint4 w = rng.block((uint32_t)i >> 2, p.step, traj, STREAM_CONTROLLER);
+      const float sc = lg[i] + p.bc[i] + gumbel(word_to_uniform(word_of(w, i & 3)));
+      if (sc > best) { best = sc; x = i; }
+    }
+  }
+  reduce(best, x);
+  if (x < 0) return -1;
+  if (x == N) return -2;
+  const uint8_t* lm = p.mask + (long)p.M * NX + ((long)m * N + x) * Lc;
+  best = -INFINITY;
+  int l = -1;
+  if (on) {
+    for (int i = q; i < Lc; i += TPR) {
+      if (!lm[i]) continue;
+      const uint4 w = rng.block((uint32_t)i >> 2, p.step, traj, STREAM_LOCATION);
+      const float sc = lg[NX + i] + p.bc[NX + i] + gumbel(word_to_uniform(word_of(w, i & 3)));
+      if (sc > best) { best = sc; l = i; }
+    }
+  }
+  reduce(best, l);
+  return l < 0 ? -1 : x * Lc + l;
 }
 
 // Activation source of the controller kernels for rows m0 .. m0+rows-1.
@@ -1203,7 +1254,7 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
 #pragma unroll
   for (int b = 0; b < MAXB; ++b) {
     const int a = a0 + 4 * b;
-    const bool ok = want_action && row_ok && 4 * b < apt && a < A;
+    const bool ok = want_action && row_ok && p.N == 0 && 4 * b < apt && a < A;
     const uint32_t off = (uint32_t)(r * A + a);
     if (words) {
       mk[b] = bload4(rmask, ok ? off : kOffNone);
@@ -1236,7 +1287,7 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
   const uint32_t traj = p.traj0 + (uint32_t)m;
   float best = -INFINITY, mx = -INFINITY;
   int bidx = -1;
-  if (want_action && row_ok) {
+  if (want_action && row_ok && p.N == 0) {
 #pragma unroll
     for (int b = 0; b < MAXB; ++b) {
       if (mk[b] == 0) continue;  // no valid action in the block (or outside the range)
@@ -1289,7 +1340,9 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
     }
     return;
   }
-  if (row_ok && q == 0) ctrl_row_commit(p, rng, m, bidx, lg[A] + p.bc[A], lg[A + 1] + p.bc[A + 1]);
+  if (p.N > 0) bidx = two_level_pick<TPR>(p, rng, lg, m, want_action && row_ok, q, traj);
+  const int Ar = p.N > 0 ? p.N + 1 + p.Lc : A;  // the reward and done logit rows
+  if (row_ok && q == 0) ctrl_row_commit(p, rng, m, bidx, lg[Ar] + p.bc[Ar], lg[Ar + 1] + p.bc[Ar + 1]);
 }
 
 // ===========================================================================
@@ -1885,7 +1938,8 @@ hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
   using DT = typename S::DT;
   using Cf = Cfgs<DT>;
   const int nbtot = a.Nc / 16;
-  if (a.M <= WM_RD_CTRL_ROWS && nbtot <= 9) {
+  // (the two-level controller runs on the kernels that stage whole logit rows)
+  if (a.M <= WM_RD_CTRL_ROWS && nbtot <= 9 && a.N == 0) {
     const int nb = nbtot <= 1 ? 1 : nbtot <= 2 ? 2 : nbtot <= 3 ? 3 : nbtot <= 5 ? 5 : 9;
     const int smax = nb <= 5 ? 8 : 4;  // register budget
     const int nw = rd_waves((int)a.ldk, Mfma<DT>::KSLICE, smax, 4);
@@ -1964,6 +2018,8 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ca.k0 = R.k0; ca.k1 = R.k1; ca.traj0 = R.traj0;
   ca.done_state = R.done_state;
   ca.use_done = (R.flags & 1u) != 0;
+  ca.N = L.N;
+  ca.Lc = L.Lc;
 
   GatesArgs ga{};
   ga.Wg = base + L.off_Wg;

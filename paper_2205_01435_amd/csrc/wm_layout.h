@@ -17,9 +17,12 @@
 //                  quartet per lane then carries one dim's features.  A final
 //                  16-row block holds w_r (row 0) and w_d (row 1).
 //   bm  [Nm]       fp32, same row order (b_r, b_d in the final block).
-//   Wc  [Nc, ldk]  controller rows 0..A-1 (columns z | h), row A = [0 | w_r],
-//                  row A+1 = [0 | w_d], zero rows up to Nc = roundup(A+2, 16).
-//   bc  [Nc]       fp32: b_c, b_r, b_d, zeros.
+//   Wc  [Nc, ldk]  controller rows 0..Ac-1 (columns z | h), row Ac = [0 | w_r],
+//                  row Ac+1 = [0 | w_d], zero rows up to Nc = roundup(Ac+2, 16).
+//                  Ac = A, or N + 1 + L for the two-level controller (N+1
+//                  xfer rows, the last the NO-OP, then L location rows; the
+//                  world model's actions are then the A = N L pairs).
+//   bc  [Nc]       fp32: b_c (Ac), b_r, b_d, zeros.
 //
 // Activations live in one matrix per step, X [rows, ldx] in the same element
 // type: columns 0..Z-1 hold q(z), Z..Z+H-1 hold h, the rest zero, so that the
@@ -41,16 +44,20 @@ struct Layout {
   int ldx;             // roundup(Z + ldh, 64): row stride of the activation matrix
   int Q;               // ceil(3K / 4)
   int Nm;              // 16 Q (Z / 4) + 16
-  int Nc;              // roundup(A + 2, 16)
+  int N, Lc;           // two-level controller: xfers and locations (N = 0: one level)
+  int Ac;              // controller logit rows: A, or N + 1 + Lc
+  int Nc;              // roundup(Ac + 2, 16)
   size_t off_Wg, off_WaT, off_bg, off_Wm, off_bm, off_Wc, off_bc, total;
 };
 
 static inline size_t wm_align256(size_t x) { return (x + 255) & ~(size_t)255; }
 static inline int wm_roundup(int x, int m) { return (x + m - 1) / m * m; }
 
-static inline Layout make_layout(int Z, int H, int A, int K, int dt) {
+static inline Layout make_layout(int Z, int H, int A, int K, int dt, int N = 0, int Lc = 0) {
   Layout L;
   L.Z = Z; L.H = H; L.A = A; L.K = K; L.dt = dt;
+  L.N = N; L.Lc = Lc;
+  L.Ac = N > 0 ? N + 1 + Lc : A;
   L.esz = dt == 0 ? 4 : 2;
   L.Kx = Z + H;
   L.ldk = wm_roundup(L.Kx, 64);
@@ -58,7 +65,7 @@ static inline Layout make_layout(int Z, int H, int A, int K, int dt) {
   L.ldx = wm_roundup(Z + L.ldh, 64);
   L.Q = (3 * K + 3) / 4;
   L.Nm = 16 * L.Q * (Z / 4) + 16;
-  L.Nc = wm_roundup(A + 2, 16);
+  L.Nc = wm_roundup(L.Ac + 2, 16);
   size_t o = 0;
   L.off_Wg = o;  o = wm_align256(o + (size_t)4 * H * L.ldk * L.esz);
   L.off_WaT = o; o = wm_align256(o + (size_t)A * 4 * H * L.esz);

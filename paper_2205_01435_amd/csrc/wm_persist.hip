@@ -801,6 +801,7 @@ bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
   const int nks = L.ldk / 16;
   const int nper = (nks + 4 / nbc - 1) / (4 / nbc);
   if (nper > kMaxS || (L.H / 16 + 3) / 4 > kMaxMS || L.Q > kMaxQ) return false;
+  if (L.N > 0) return false;  // the two-level controller runs on the multi-launch path
   pl.rb = rb;
   pl.nbc = nbc;
   // the mixture-head partial sums and the controller scratch live in other

@@ -59,7 +59,7 @@ class TieCounter:
 
 
 def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, step0=0,
-               done0=None, sigma_tau=False):
+               done0=None, sigma_tau=False, two_level=None):
     """Re-anchored comparison of a device rollout.
 
     ``g`` holds the device's z_out, actions, rewards, dones, h_trace and
@@ -87,10 +87,15 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
             continue
         n_live_steps += idx.size
         sel = idx
-        mask_t = mask[t] if mask.ndim == 3 else mask  # per-step masks: [T, n, A]
-        r = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], mask_t[sel], seed=seed,
+        if two_level is not None:  # (xfer masks, location masks)
+            m_sel = (mask[0][sel], mask[1][sel])
+        else:
+            mask_t = mask[t] if mask.ndim == 3 else mask  # per-step masks: [T, n, A]
+            m_sel = mask_t[sel]
+        r = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], m_sel, seed=seed,
                            traj=traj[sel], step=step0 + t, tau=tau, done_flag=done_flag,
-                           dtype=dtype, h_next=g["h_trace"][t + 1][sel], sigma_tau=sigma_tau)
+                           dtype=dtype, h_next=g["h_trace"][t + 1][sel], sigma_tau=sigma_tau,
+                           two_level=two_level)
         # actions
         ag = a_g[idx]
         ties.draws += idx.size
@@ -101,10 +106,10 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
                                 f"gpu={ag[diff][~near]} ref={r['action'][diff][~near]}, "
                                 f"margin={r['action_margin'][diff][~near]}")
             ties.mismatches += int(diff.sum())
-            r2 = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], mask_t[sel], seed=seed,
+            r2 = owm.transition(wb, dims, za[idx], ha[idx], ca[idx], m_sel, seed=seed,
                                 traj=traj[sel], step=step0 + t, tau=tau, done_flag=done_flag,
                                 dtype=dtype, h_next=g["h_trace"][t + 1][sel], action=ag,
-                                sigma_tau=sigma_tau)
+                                sigma_tau=sigma_tau, two_level=two_level)
             r["h"], r["c"] = r2["h"], r2["c"]
         ok = ag >= 0
         # state

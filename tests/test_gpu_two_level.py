@@ -1,0 +1,105 @@
+"""GPU parity of the two-level controller (section 3.1.3: an xfer, index N
+the NO-OP, then a location valid for it) in dream rollouts, through the C
+ABI, against the oracle re-anchored per step; plus the validity of every
+action under the masks and the NO-OP ending its trajectory."""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import parity
+from paper_2205_01435_amd import _lib as wmlib
+from paper_2205_01435_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+KEYS = ("z_out", "actions", "rewards", "dones", "h_trace", "c_trace")
+
+
+def say(*a):
+    print("[gpu-test]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    wmlib.load()
+    yield
+
+
+def _t(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def _inputs(B, T, Z, H, N, L, K, seed):
+    A = N * L
+    rng = np.random.default_rng(seed)
+    w = wl.make_weights(rng, Z, H, A, K, T)
+    a = np.sqrt(6.0 / (Z + H + N + 1 + L))
+    w["W_c"] = rng.uniform(-a, a, size=(N + 1 + L, Z + H)).astype(np.float32) * 4
+    w["b_c"] = (0.3 * rng.standard_normal(N + 1 + L)).astype(np.float32)
+    z0 = rng.standard_normal((B, Z)).astype(np.float32)
+    xm = (rng.random((B, N + 1)) < 0.5).astype(np.uint8)
+    xm[:, N] = rng.random(B) < 0.3  # the NO-OP available on some rows
+    xm[np.arange(B), rng.integers(0, N, B)] = 1
+    xm[B // 4, :N] = 0  # a row that can only stop
+    xm[B // 4, N] = 1
+    lm = (rng.random((B, N, L)) < 0.3).astype(np.uint8)
+    lm[np.arange(B)[:, None], np.arange(N)[None, :], rng.integers(0, L, (B, N))] = 1
+    lm[B // 2] = 0  # a row whose xfers have no valid location
+    return w, z0, xm, lm
+
+
+# B, T, Z, H, N, L, K, dtype, rows compared
+CASES = [
+    (37, 5, 16, 128, 4, 20, 3, "fp32", None),
+    (300, 3, 32, 256, 8, 50, 5, "bf16", None),
+    (4096 + 3, 2, 64, 512, 10, 200, 5, "bf16", 40),  # 2000 actions, 211 controller logits
+]
+
+
+@pytest.mark.parametrize("B,T,Z,H,N,L,K,dtype,nrows", CASES)
+def test_two_level_rollout(B, T, Z, H, N, L, K, dtype, nrows):
+    say("two-level", B, T, Z, H, N, L, K, dtype)
+    A = N * L
+    w, z0, xm, lm = _inputs(B, T, Z, H, N, L, K, seed=B + N)
+    m = wmlib.pack(w, Z, H, A, K, dtype, N=N, L=L)
+    wmlib.profile_reset()
+    wmlib.profile_enable("")
+    try:
+        b = wmlib.rollout(m, _t(z0), (_t(xm), _t(lm)), T=T, seed=31, tau=1.0, done=True, trace=True)
+        torch.cuda.synchronize()
+        _, n_persist = wmlib.profile_read("persist")
+        _, n_ctrl = wmlib.profile_read("ctrl")
+    finally:
+        wmlib.profile_enable(None)
+        wmlib.profile_reset()
+    assert n_persist == 0 and n_ctrl == T + 1, "the two-level controller runs on the multi-launch path"
+    acts = b.actions.cpu().numpy()
+    tt, bb = np.nonzero(acts >= 0)
+    x, loc = acts[tt, bb] // L, acts[tt, bb] % L
+    assert np.all(xm[bb, x] == 1) and np.all(lm[bb, x, loc] == 1)
+    assert acts[0, B // 4] == -2 and np.all(acts[1:, B // 4] == -1)
+    assert np.all(acts[:, B // 2] < 0)
+    assert (acts >= 0).any() and (acts == -2).any()
+    rows = np.arange(B) if nrows is None else np.unique(np.concatenate(
+        [np.linspace(0, B - 1, nrows).astype(np.int64), [B // 4, B // 2, B - 1]]))
+    ri = torch.from_numpy(rows).cuda()
+    g = {k: getattr(b, k)[:, ri].cpu().numpy() for k in KEYS}
+    ties, live = parity.reanchored(dict(Z=Z, H=H, A=A, K=K), w, (xm[rows], lm[rows]), g, seed=31,
+                                   tau=1.0, done_flag=True, dtype=dtype, traj=rows, two_level=(N, L))
+    say("ties", ties.mismatches, "of", ties.draws, "live", live)
+    assert live > 0
+
+
+def test_two_level_argument_errors():
+    w, z0, xm, lm = _inputs(8, 2, 16, 128, 4, 20, 3, seed=1)
+    with pytest.raises(wmlib.WmError):
+        wmlib.pack(w, 16, 128, 81, 3, "fp32", N=4, L=20)  # A != N L
+    m = wmlib.pack(w, 16, 128, 80, 3, "fp32", N=4, L=20)
+    with pytest.raises(wmlib.WmError):  # the controller step serves the one-level controller only
+        wmlib.controller_step(m, _t(z0), torch.zeros((8, 128), device="cuda"), _t(xm), seed=1, step=0)
+    with pytest.raises(ValueError):
+        wmlib.rollout(m, _t(z0), (_t(xm), _t(lm[:, :3])), T=2, seed=1)
