@@ -273,7 +273,46 @@ def workload_table(wmlib, wl, torch, cuda) -> dict:
         del bufs, m
         torch.cuda.empty_cache()
     res["returns_gae_xlarge"] = returns_row(wmlib, torch, cuda)
+    res["two_level_rollout"] = two_level_row(wmlib, wl, torch, cuda)
     return res
+
+
+def two_level_row(wmlib, wl, torch, cuda) -> dict:
+    """A dream rollout with the two-level controller (N = 10 xfers + NO-OP,
+    L = 200 locations, A = 2000 world-model actions) at the large rollout's
+    sizes (B = 4096, Z = 64, H = 1024, K = 8, bf16), T = 20, against the bf16
+    MFMA peak; the controller has N + 1 + L logit rows."""
+    B, T, Z, H, K, N, L = 4096, 20, 64, 1024, 8, 10, 200
+    A = N * L
+    rng = np.random.default_rng(6)
+    w = wl.make_weights(rng, Z, H, A, K, T)
+    a = np.sqrt(6.0 / (Z + H + N + 1 + L))
+    w["W_c"] = rng.uniform(-a, a, size=(N + 1 + L, Z + H)).astype(np.float32)
+    w["b_c"] = np.zeros(N + 1 + L, np.float32)
+    m = wmlib.pack(w, Z, H, A, K, "bf16", N=N, L=L)
+    z0 = cuda(rng.standard_normal((B, Z)).astype(np.float32))
+    xm = (rng.random((B, N + 1)) < 0.5).astype(np.uint8)
+    xm[:, 0] = 1
+    xm[:, N] = 0
+    lm = (rng.random((B, N, L)) < 0.3).astype(np.uint8)
+    lm[:, :, 0] = 1
+    mask = (cuda(xm), cuda(lm))
+    bufs = wmlib.RolloutBuffers(m, B, T)
+    run = lambda i: wmlib.rollout(m, z0, mask, T=T, seed=7 + i, done=True, bufs=bufs)  # noqa: E731
+    run(0)
+    torch.cuda.synchronize()
+    times = []
+    for i in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run(i + 1)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = float(np.median(times))
+    fl = 2.0 * (4 * H * (Z + H) + 3 * Z * K * H + (N + 1 + L) * (Z + H) + 2 * H)
+    return {"ms": ms, "per_s": B * T / (ms / 1e3), "unit": "transitions/s",
+            "tflops": B * T * fl / (ms / 1e3) / 1e12, "frac_mfma_peak": B * T * fl / (ms / 1e3) / PEAK["bf16"]}
 
 
 def returns_bytes(T: int, B: int, gae: bool) -> int:
