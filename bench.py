@@ -274,7 +274,35 @@ def workload_table(wmlib, wl, torch, cuda) -> dict:
         torch.cuda.empty_cache()
     res["returns_gae_xlarge"] = returns_row(wmlib, torch, cuda)
     res["two_level_rollout"] = two_level_row(wmlib, wl, torch, cuda)
+    res["adam_xlarge_wm"] = adam_row(wmlib, torch)
     return res
+
+
+def adam_row(wmlib, torch) -> dict:
+    """One optimiser step over the world model's parameters at the xlarge
+    sizes (W_g 4H x (Z+A+H), W_m 3ZK x H and the biases and heads: 8.9 M fp32
+    values) against the HBM roof: 16 bytes read and 12 written per value."""
+    Z, H, A, K = 128, 1024, 256, 8
+    n = 4 * H * (Z + A + H) + 4 * H + 3 * Z * K * H + 3 * Z * K + 2 * H + 2
+    p = torch.randn(n, device="cuda")
+    g = torch.randn(n, device="cuda")
+    m = torch.zeros(n, device="cuda")
+    v = torch.zeros(n, device="cuda")
+    wmlib.adam_step(p, g, m, v, 1, 1e-4)
+    torch.cuda.synchronize()
+    reps = 20
+    wmlib.profile_reset()
+    wmlib.profile_enable("adam")
+    for i in range(reps):
+        wmlib.adam_step(p, g, m, v, 2 + i, 1e-4)
+    torch.cuda.synchronize()
+    k_ms, k_n = wmlib.profile_read("adam")
+    wmlib.profile_enable(None)
+    wmlib.profile_reset()
+    kms = k_ms / max(k_n, 1)
+    nb = 28 * n
+    return {"params": n, "kernel_us": kms * 1e3, "bytes": nb, "GBps": nb / (kms / 1e3) / 1e9,
+            "kernel_frac_hbm_peak": nb / (kms / 1e3) / HBM_PEAK}
 
 
 def two_level_row(wmlib, wl, torch, cuda) -> dict:

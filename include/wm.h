@@ -242,10 +242,29 @@ wm_status wm_returns(int32_t B, int32_t T, const float *rewards, const uint8_t *
                      float *advantages, wm_stream_t stream);
 
 /*
+ * Optimiser step of the world-model training (the model is fitted on its
+ * log-likelihood loss, section 4.7; the paper names no optimiser, Adam is
+ * this library's reading).  In place on n fp32 parameters with their first
+ * and second moments m, v (zero before step 1):
+ *   m = beta1 m + (1 - beta1) g,   v = beta2 v + (1 - beta2) g^2,
+ *   params -= lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps).
+ * step >= 1; beta1, beta2 in [0, 1); eps > 0; lr >= 0.  Arrays 16-byte
+ * aligned.  n = 0 is a no-op.
+ */
+wm_status wm_adam_step(int64_t n, float *params, const float *grads, float *m, float *v,
+                       int32_t step, float lr, float beta1, float beta2, float eps,
+                       wm_stream_t stream);
+
+/* Host function: the learning rate at `epoch` of a second-degree polynomial
+ * decay from lr0 to lr_end over `epochs` (section 4.7 decays over 5000):
+ * (lr0 - lr_end) (1 - min(epoch, epochs) / epochs)^2 + lr_end. */
+float wm_poly_lr(int32_t epoch, float lr0, float lr_end, int32_t epochs);
+
+/*
  * Measurement aid (no counterpart in the paper).  While a prefix is set, every
  * kernel launch of the library whose name starts with it is bracketed by HIP
  * events on its stream.  Kernel names: "ctrl", "gates", "mdn", "init",
- * "finish", "nll_init", "nll_reduce", "nll_means", "pack", "returns"; "" selects all,
+ * "finish", "nll_init", "nll_reduce", "nll_means", "pack", "returns", "adam"; "" selects all,
  * NULL turns timing off.  wm_profile_read waits for the recorded events and
  * returns the summed duration (ms) and count of the launches whose name
  * starts with `prefix` (NULL = all); wm_profile_reset forgets them.  Timing

@@ -24,7 +24,7 @@ _DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
 
 # Every symbol the C header declares.
 EXPORTS = ("wm_packed_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
-           "wm_rollout", "wm_nll", "wm_returns", "wm_profile_enable", "wm_profile_read", "wm_profile_reset",
+           "wm_rollout", "wm_nll", "wm_returns", "wm_adam_step", "wm_poly_lr", "wm_profile_enable", "wm_profile_read", "wm_profile_reset",
            "wm_last_error", "wm_version")
 
 
@@ -75,6 +75,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_nll.restype = I32
     lib.wm_returns.argtypes = [I32, I32, P, P, P, F32, F32, P, P, P]
     lib.wm_returns.restype = I32
+    lib.wm_adam_step.argtypes = [ctypes.c_int64, P, P, P, P, I32, F32, F32, F32, F32, P]
+    lib.wm_adam_step.restype = I32
+    lib.wm_poly_lr.argtypes = [I32, F32, F32, I32]
+    lib.wm_poly_lr.restype = F32
     lib.wm_profile_enable.argtypes = [ctypes.c_char_p]
     lib.wm_profile_enable.restype = I32
     lib.wm_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
@@ -258,6 +262,20 @@ def returns(rewards, dones, gamma: float, values=None, lam: float = 1.0, out=Non
     _check(lib.wm_returns(B, T, _ptr(rewards), _ptr(dones), _ptr(values), gamma, lam, _ptr(out),
                           _ptr(adv if values is not None else None), _stream()))
     return out, (adv if values is not None else None)
+
+
+def adam_step(params, grads, m, v, step: int, lr: float, beta1: float = 0.9, beta2: float = 0.999,
+              eps: float = 1e-8):
+    """Launch wm_adam_step on the current stream over flat float32 device
+    tensors of one size (updated in place)."""
+    n = params.numel()
+    assert grads.numel() == n and m.numel() == n and v.numel() == n
+    _check(load().wm_adam_step(n, _ptr(params), _ptr(grads), _ptr(m), _ptr(v), step, lr, beta1, beta2,
+                               eps, _stream()))
+
+
+def poly_lr(epoch: int, lr0: float, lr_end: float, epochs: int = 5000) -> float:
+    return float(load().wm_poly_lr(epoch, lr0, lr_end, epochs))
 
 
 def profile_enable(prefix: str | None):

@@ -235,6 +235,32 @@ wm_status wm_returns(int32_t B, int32_t T, const float* rewards, const uint8_t* 
   return ok();
 }
 
+wm_status wm_adam_step(int64_t n, float* params, const float* grads, float* m, float* v,
+                       int32_t step, float lr, float beta1, float beta2, float eps,
+                       wm_stream_t stream) {
+  if (n < 0) return fail(WM_ERR_INVALID_ARG, "n=%lld must not be negative", (long long)n);
+  if (step < 1) return fail(WM_ERR_INVALID_ARG, "step=%d: Adam steps count from 1", step);
+  if (!(lr >= 0.0f) || !isfinite(lr)) return fail(WM_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f))
+    return fail(WM_ERR_INVALID_ARG, "beta1 and beta2 must lie in [0, 1)");
+  if (!(eps > 0.0f)) return fail(WM_ERR_INVALID_ARG, "eps must be > 0");
+  if (n == 0) return ok();
+  if (!params || !grads || !m || !v) return fail(WM_ERR_INVALID_ARG, "params, grads, m and v are required");
+  if (!aligned16(params) || !aligned16(grads) || !aligned16(m) || !aligned16(v))
+    return fail(WM_ERR_INVALID_ARG, "params, grads, m and v must be 16-byte aligned");
+  hipError_t e = wm::launch_adam((long)n, params, grads, m, v, step, lr, beta1, beta2, eps,
+                                 reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "wm_adam_step");
+  return ok();
+}
+
+float wm_poly_lr(int32_t epoch, float lr0, float lr_end, int32_t epochs) {
+  if (epochs <= 0) return lr_end;
+  const double e = epoch < 0 ? 0.0 : (epoch > epochs ? (double)epochs : (double)epoch);
+  const double f = 1.0 - e / epochs;
+  return (float)(((double)lr0 - lr_end) * f * f + lr_end);
+}
+
 const char* wm_last_error(void) { return g_err.c_str(); }
 
 const char* wm_version(void) { return "libwm 0.1.0 (gfx950)"; }

@@ -94,4 +94,8 @@ struct ReturnsBufs {
 };
 hipError_t launch_returns(const ReturnsBufs& R, hipStream_t s);
 
+// Adam step on n fp32 parameters, in place (wm_optim.hip).
+hipError_t launch_adam(long n, float* p, const float* g, float* m, float* v, int step, float lr,
+                       float beta1, float beta2, float eps, hipStream_t s);
+
 }  // namespace wm

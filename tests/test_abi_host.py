@@ -117,3 +117,10 @@ def test_missing_library_fails_loudly(tmp_path):
             wmlib.load(str(tmp_path / "nope.so"))
     finally:
         wmlib._lib = saved
+
+
+def test_poly_lr_matches_the_oracle_schedule():
+    from oracle import train as otr
+    for e in (-3, 0, 1, 1250, 2500, 4999, 5000, 7000):
+        assert abs(wmlib.poly_lr(e, 3e-3, 1e-5) - otr.poly_lr(e, 3e-3, 1e-5)) <= 1e-9
+    assert wmlib.poly_lr(10, 1e-3, 1e-4, epochs=20) == pytest.approx(otr.poly_lr(10, 1e-3, 1e-4, 20), rel=1e-6)
