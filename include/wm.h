@@ -119,8 +119,9 @@ size_t wm_packed_bytes(const wm_dims *dims);
 wm_status wm_pack_weights(const wm_dims *dims, const wm_weights *canon, void *packed,
                           size_t packed_bytes, wm_stream_t stream);
 
-/* Workspace bytes needed by wm_rollout (which = 0) or wm_nll (which = 1)
- * for B rows and T steps; wm_controller_step needs none.  0 on bad args. */
+/* Workspace bytes needed by wm_rollout (which = 0), wm_nll (which = 1) or
+ * wm_nll_grad (which = 2) for B rows and T steps; wm_controller_step needs
+ * none.  0 on bad args. */
 size_t wm_workspace_bytes(const wm_dims *dims, int32_t B, int32_t T, int32_t which);
 
 /*
@@ -219,6 +220,31 @@ wm_status wm_nll(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
                  size_t workspace_bytes, wm_stream_t stream);
 
 /*
+ * Gradient of the world model's training loss (section 4.7): the sum of the
+ * three means of wm_nll,
+ *   L = -sum loglik / (N Z) + sum se / N + sum bce / N,
+ * with respect to every world-model weight, by backpropagation through time
+ * through the mixture, reward and done heads and the LSTM (the controller is
+ * not part of this loss).  WM_FP32 weights only (WM_ERR_UNSUPPORTED on
+ * WM_BF16).  Inputs as for wm_nll (same shapes and meanings); outputs are
+ * device float32 arrays in the canonical layout of wm_weights, written
+ * whole (not accumulated):
+ *   loss [1] nullable; grad_W_g [4H, Z+A+H]; grad_b_g [4H];
+ *   grad_W_m [3ZK, H]; grad_b_m [3ZK]; grad_w_r [H]; grad_b_r [1];
+ *   grad_w_d [H]; grad_b_d [1].
+ * N = 0 (all lengths 0) gives loss 0 and zero gradients.  T = 0 writes
+ * nothing.  T B at most 2^22.  Every reduction runs in a fixed order: the
+ * result does not depend on scheduling.
+ *   workspace: wm_workspace_bytes(dims, B, T, 2) bytes, 256-byte aligned.
+ */
+wm_status wm_nll_grad(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
+                      const float *z, const int32_t *actions, const float *rewards,
+                      const uint8_t *dones, const int32_t *lengths, float *loss,
+                      float *grad_W_g, float *grad_b_g, float *grad_W_m, float *grad_b_m,
+                      float *grad_w_r, float *grad_b_r, float *grad_w_d, float *grad_b_d,
+                      void *workspace, size_t workspace_bytes, wm_stream_t stream);
+
+/*
  * Return scan over B dreamed trajectories of T steps, for the policy updates
  * of the controller: the discounted sum of rewards that the agent maximises
  * (section 2.2) and, with a value baseline, generalised advantage estimates
@@ -264,7 +290,8 @@ float wm_poly_lr(int32_t epoch, float lr0, float lr_end, int32_t epochs);
  * Measurement aid (no counterpart in the paper).  While a prefix is set, every
  * kernel launch of the library whose name starts with it is bracketed by HIP
  * events on its stream.  Kernel names: "ctrl", "gates", "mdn", "init",
- * "finish", "nll_init", "nll_reduce", "nll_means", "pack", "returns", "adam"; "" selects all,
+ * "finish", "nll_init", "nll_reduce", "nll_means", "pack", "returns", "adam", and the
+ * "grad_" kernels of wm_nll_grad; "" selects all,
  * NULL turns timing off.  wm_profile_read waits for the recorded events and
  * returns the summed duration (ms) and count of the launches whose name
  * starts with `prefix` (NULL = all); wm_profile_reset forgets them.  Timing

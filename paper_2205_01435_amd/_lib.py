@@ -24,7 +24,7 @@ _DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
 
 # Every symbol the C header declares.
 EXPORTS = ("wm_packed_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
-           "wm_rollout", "wm_nll", "wm_returns", "wm_adam_step", "wm_poly_lr", "wm_profile_enable", "wm_profile_read", "wm_profile_reset",
+           "wm_rollout", "wm_nll", "wm_nll_grad", "wm_returns", "wm_adam_step", "wm_poly_lr", "wm_profile_enable", "wm_profile_read", "wm_profile_reset",
            "wm_last_error", "wm_version")
 
 
@@ -73,6 +73,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_rollout.restype = I32
     lib.wm_nll.argtypes = [pd, P, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.wm_nll.restype = I32
+    lib.wm_nll_grad.argtypes = [pd, P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.wm_nll_grad.restype = I32
     lib.wm_returns.argtypes = [I32, I32, P, P, P, F32, F32, P, P, P]
     lib.wm_returns.restype = I32
     lib.wm_adam_step.argtypes = [ctypes.c_int64, P, P, P, P, I32, F32, F32, F32, F32, P]
@@ -246,6 +248,42 @@ def nll(m: Model, z, actions, rewards, dones, lengths=None,
                       _ptr(rewards), _ptr(dones), _ptr(lengths), _ptr(bufs.loglik),
                       _ptr(bufs.reward_se), _ptr(bufs.done_bce), _ptr(bufs.means),
                       _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
+    return bufs
+
+
+GRAD_SHAPES = {  # canonical gradient shapes, as the weights
+    "W_g": lambda Z, H, A, K: (4 * H, Z + A + H), "b_g": lambda Z, H, A, K: (4 * H,),
+    "W_m": lambda Z, H, A, K: (3 * Z * K, H), "b_m": lambda Z, H, A, K: (3 * Z * K,),
+    "w_r": lambda Z, H, A, K: (H,), "b_r": lambda Z, H, A, K: (1,),
+    "w_d": lambda Z, H, A, K: (H,), "b_d": lambda Z, H, A, K: (1,),
+}
+
+
+class GradBuffers:
+    def __init__(self, m: Model, B: int, T: int):
+        dev = m.packed.device
+        self.loss = torch.empty(1, dtype=torch.float32, device=dev)
+        self.grads = {k: torch.empty(f(m.Z, m.H, m.A, m.K), dtype=torch.float32, device=dev)
+                      for k, f in GRAD_SHAPES.items()}
+        nws = workspace_bytes(m.dims, B, T, 2)
+        self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+        self.ws_bytes = nws
+
+
+def nll_grad(m: Model, z, actions, rewards, dones, lengths=None,
+             bufs: GradBuffers | None = None) -> GradBuffers:
+    """Launch wm_nll_grad on the current stream: the training loss (summed
+    NLL means) and its gradient in the canonical weight layout."""
+    lib = load()
+    T, B = actions.shape
+    if bufs is None:
+        bufs = GradBuffers(m, B, T)
+    g = bufs.grads
+    _check(lib.wm_nll_grad(ctypes.byref(m.dims), _ptr(m.packed), B, T, _ptr(z), _ptr(actions),
+                           _ptr(rewards), _ptr(dones), _ptr(lengths), _ptr(bufs.loss),
+                           _ptr(g["W_g"]), _ptr(g["b_g"]), _ptr(g["W_m"]), _ptr(g["b_m"]),
+                           _ptr(g["w_r"]), _ptr(g["b_r"]), _ptr(g["w_d"]), _ptr(g["b_d"]),
+                           _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
     return bufs
 
 

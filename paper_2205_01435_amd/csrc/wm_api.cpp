@@ -88,6 +88,9 @@ size_t wm_workspace_bytes(const wm_dims* dims, int32_t B, int32_t T, int32_t whi
   if (check_dims(dims, &L) != WM_OK || B <= 0 || T < 0) return 0;
   if (which == 0) return wm::rollout_workspace(L, B, nullptr, nullptr);
   if (which == 1) return wm::nll_workspace(L, B, T, nullptr, nullptr);
+  if (which == 2)
+    return wm::wm_align256(wm::nll_workspace(L, B, T, nullptr, nullptr)) +
+           wm::grad_workspace(L, B, T, nullptr, nullptr);
   return 0;
 }
 
@@ -209,6 +212,47 @@ wm_status wm_nll(const wm_dims* dims, const void* packed, int32_t B, int32_t T, 
   wm::Packed P{L, packed};
   hipError_t e = wm::launch_nll(P, N, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "wm_nll");
+  return ok();
+}
+
+wm_status wm_nll_grad(const wm_dims* dims, const void* packed, int32_t B, int32_t T, const float* z,
+                      const int32_t* actions, const float* rewards, const uint8_t* dones,
+                      const int32_t* lengths, float* loss, float* grad_W_g, float* grad_b_g,
+                      float* grad_W_m, float* grad_b_m, float* grad_w_r, float* grad_b_r,
+                      float* grad_w_d, float* grad_b_d, void* workspace, size_t workspace_bytes,
+                      wm_stream_t stream) {
+  wm::Layout L;
+  wm_status st = check_dims(dims, &L);
+  if (st != WM_OK) return st;
+  if ((st = check_packed(L, packed)) != WM_OK) return st;
+  if (L.dt != 0) return fail(WM_ERR_UNSUPPORTED, "wm_nll_grad serves fp32 weights only");
+  if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
+  if (T < 0) return fail(WM_ERR_INVALID_ARG, "T=%d must not be negative", T);
+  if (!z || !actions || !rewards || !dones)
+    return fail(WM_ERR_INVALID_ARG, "z, actions, rewards and dones are required");
+  if (!grad_W_g || !grad_b_g || !grad_W_m || !grad_b_m || !grad_w_r || !grad_b_r || !grad_w_d || !grad_b_d)
+    return fail(WM_ERR_INVALID_ARG, "every gradient output is required");
+  if (!aligned16(z)) return fail(WM_ERR_INVALID_ARG, "z must be 16-byte aligned");
+  if ((int64_t)B * T > (int64_t)1 << 22) return fail(WM_ERR_UNSUPPORTED, "T*B above 2^22");
+  if (T == 0) return ok();
+  const size_t nb = wm::wm_align256(wm::nll_workspace(L, B, T, nullptr, nullptr));
+  const size_t need = nb + wm::grad_workspace(L, B, T, nullptr, nullptr);
+  if (!workspace || workspace_bytes < need)
+    return fail(WM_ERR_WORKSPACE, "nll_grad workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(WM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+
+  char* ws = reinterpret_cast<char*>(workspace);
+  wm::NllBufs N{};
+  N.B = B; N.T = T; N.z = z; N.actions = actions; N.rewards = rewards; N.dones = dones;
+  N.lengths = lengths;
+  wm::nll_workspace(L, B, T, ws, &N);
+  wm::GradWs G{};
+  wm::grad_workspace(L, B, T, ws + nb, &G);
+  const wm::GradOut out{loss, grad_W_g, grad_b_g, grad_W_m, grad_b_m, grad_w_r, grad_b_r, grad_w_d, grad_b_d};
+  wm::Packed P{L, packed};
+  hipError_t e = wm::launch_nll_grad(P, N, G, out, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "wm_nll_grad");
   return ok();
 }
 

@@ -94,6 +94,17 @@ struct ReturnsBufs {
 };
 hipError_t launch_returns(const ReturnsBufs& R, hipStream_t s);
 
+// World-model training step: gradient of the summed NLL means (fp32).
+struct GradWs {  // workspace after the NLL pass's own
+  float *G, *Cs, *M, *dG, *dhh, *dh, *dc, *WhT, *WmT, *T1, *T2;
+  float *dWgT, *dWa, *dWm, *dbg, *dbm, *part, *apart, *nsum, *fwd;
+};
+struct GradOut {  // canonical gradients; loss (nullable): the summed means
+  float *loss, *W_g, *b_g, *W_m, *b_m, *w_r, *b_r, *w_d, *b_d;
+};
+size_t grad_workspace(const Layout& L, int B, int T, char* ws, GradWs* G);
+hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const GradOut& out, hipStream_t s);
+
 // Adam step on n fp32 parameters, in place (wm_optim.hip).
 hipError_t launch_adam(long n, float* p, const float* g, float* m, float* v, int step, float lr,
                        float beta1, float beta2, float eps, hipStream_t s);

@@ -21,6 +21,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "wm_device.h"
@@ -2226,6 +2227,470 @@ hipError_t launch_rollout(const Packed& P, const RolloutBufs& R, hipStream_t s) 
 
 hipError_t launch_nll(const Packed& P, const NllBufs& N, hipStream_t s) {
   return P.L.dt == 0 ? nll_impl<float>(P, N, s) : nll_impl<bf16_t>(P, N, s);
+}
+
+// ===========================================================================
+// World-model training step: the gradient of the summed NLL means with
+// respect to the gate, mixture, reward and done weights (fp32), by
+// backpropagation through time after the forward NLL pass.
+//
+//   forward   X (z_t | h_t) from the NLL pass; pre-activations of every step
+//             in one GEMM; a scan adds bias and one-hot column, applies the
+//             gates and records c_t
+//   heads     mixture/reward/done outputs of every h_{t+1} in one GEMM; an
+//             element-wise kernel turns them into d loss / d output (dM)
+//   back      dh_heads = dM W_m; per step (backwards) the LSTM backward gives
+//             dG_t and dc_t, and dh_t = dG_t W_h for the step before
+//   weights   dW_g = dG^T X, dW_m = dM^T H (GEMMs over all T B rows on
+//             transposed copies), bias and one-hot columns by deterministic
+//             reductions, then the canonical layout
+// Every GEMM is C[m][n] = sum_k A[m][k] B[n][k] on the direct-to-LDS core
+// (both operands K-contiguous), so the weight gradients read transposed,
+// zero-padded copies.
+// ===========================================================================
+namespace {
+
+using GradGemm = GemmD<float, 4, 2, 2, 2, 2>;  // 128 x 64 tiles
+
+// out[m][n] = sum_{k < Kpad} A[m][k] B[n][k] for m < M, n < N (Kpad a
+// multiple of 32; columns of A and B up to Kpad must be readable, zero
+// beyond the data)
+__global__ void __launch_bounds__(GradGemm::NT) k_gemm_nt(const float* A, long lda, int M, const float* Bm,
+                                                          long ldb, int N, int Kpad, float* out, long ldo,
+                                                          TileMap map) {
+  using C = GradGemm;
+  __shared__ __attribute__((aligned(16))) char lds[C::LDS_BYTES];
+  int nt, mt;
+  if (!tile_of(map, nt, mt)) return;
+  const int n0 = nt * C::BN, m0 = mt * C::BM;
+  const SrcX<float> w(Bm, ldb, Kpad, n0, C::BN, N);
+  const SrcX<float> x(A, lda, Kpad, m0, C::BM, M);
+  f32x4 acc[C::NBW][C::MBW];
+  C::run(acc, w, x, Kpad, reinterpret_cast<float*>(lds));
+  const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+  const int wn = C::wn(), wmi = C::wm();
+#pragma unroll
+  for (int j = 0; j < C::MBW; ++j) {
+    const int m = m0 + (wmi * C::MBW + j) * 16 + r16;
+    if (m >= M) continue;
+#pragma unroll
+    for (int i = 0; i < C::NBW; ++i) {
+      const int n = n0 + (wn * C::NBW + i) * 16 + 4 * g;
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (n + v < N) out[(long)m * ldo + n + v] = acc[i][j][v];
+    }
+  }
+}
+
+// dst[c][r] = src[r][c] for r < R, c < Cc; dst[c][r] = 0 for R <= r < Rp
+__global__ void __launch_bounds__(256) k_transpose(const float* src, long lds_, int R, int Cc, float* dst,
+                                                   long ldd, int Rp) {
+  __shared__ float tile[32][33];
+  const int r0 = blockIdx.x * 32, c0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  for (int k = ty; k < 32; k += 8) {
+    const int r = r0 + k, c = c0 + tx;
+    tile[k][tx] = (r < R && c < Cc) ? src[(long)r * lds_ + c] : 0.f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int c = c0 + k, r = r0 + tx;
+    if (c < Cc && r < Rp) dst[(long)c * ldd + r] = tile[tx][k];
+  }
+}
+
+// N = sum_b min(max(len_b, 0), T) (all B T without lengths)
+__global__ void k_len_sum(const int32_t* lengths, int B, int T, float* nout) {
+  __shared__ long part[256];
+  long s = 0;
+  for (int b = threadIdx.x; b < B; b += 256) s += lengths ? min(max(lengths[b], 0), T) : T;
+  part[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    long t = 0;
+    for (int i = 0; i < 256; ++i) t += part[i];
+    nout[0] = (float)t;
+  }
+}
+
+__device__ __forceinline__ float sig_(float x) { return 1.0f / (1.0f + expf(-x)); }
+
+// forward scan of one (row b, unit u): pre-activations G (packed gate
+// order, row r = t B + b, column 4u + q) plus bias and the action's column
+// -> activations i, f, tanh g, o in place; c_t into Cs [T+1, B, H]
+__global__ void __launch_bounds__(256) k_grad_fwd_scan(float* G, const float* bg, const float* WaT,
+                                                       const int32_t* actions, float* Cs, int B, int T, int H,
+                                                       int A) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)B * H) return;
+  const int b = (int)(idx / H), u = (int)(idx % H);
+  const float4 bias = reinterpret_cast<const float4*>(bg)[u];
+  float c = 0.f;
+  Cs[(long)b * H + u] = 0.f;
+  for (int t = 0; t < T; ++t) {
+    const long r = (long)t * B + b;
+    float4 g = reinterpret_cast<float4*>(G + r * 4 * H)[u];
+    const int a = actions[r];
+    float4 w = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (a >= 0 && a < A) w = reinterpret_cast<const float4*>(WaT + (long)a * 4 * H)[u];
+    const float i = sig_(g.x + bias.x + w.x), f = sig_(g.y + bias.y + w.y);
+    const float gg = tanhf(g.z + bias.z + w.z), o = sig_(g.w + bias.w + w.w);
+    c = f * c + i * gg;
+    reinterpret_cast<float4*>(G + r * 4 * H)[u] = make_float4(i, f, gg, o);
+    Cs[((long)(t + 1) * B + b) * H + u] = c;
+  }
+}
+
+// d loss / d head output of one row r = t B + b: for each latent dim j the
+// mixture features of packed rows 16 Q J + 16 q + 4 g + v (j = 4J + g,
+// feature 4q + v); thread j = Z takes the reward/done block and the padding
+// columns.  M holds the head's GEMM outputs and is overwritten with dM.
+template <int KC>
+__global__ void __launch_bounds__(256) k_grad_heads(float* M, long ldm, const float* bm, const float* z,
+                                                    const float* rewards, const uint8_t* dones,
+                                                    const int32_t* lengths, const float* nsum, int B, int T,
+                                                    int Z, int Nm, int NmP) {
+  constexpr int K = KC, Q = (3 * K + 3) / 4;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)T * B * (Z + 1)) return;
+  const long r = idx / (Z + 1);
+  const int j = (int)(idx % (Z + 1));
+  const int t = (int)(r / B), b = (int)(r % B);
+  const float N = nsum[0];
+  const bool valid = t < (lengths ? min(max(lengths[b], 0), T) : T) && N > 0.f;
+  float* row = M + r * ldm;
+  if (j == Z) {
+    const int hr = Nm - 16;
+    const float rr = row[hr] + bm[hr], rd = row[hr + 1] + bm[hr + 1];
+    row[hr] = valid ? 2.0f * (rr - rewards[r]) / N : 0.f;
+    row[hr + 1] = valid ? (sig_(rd) - (float)dones[r]) / N : 0.f;
+    for (int c = hr + 2; c < Nm; ++c) row[c] = 0.f;
+    for (int c = Nm; c < NmP; ++c) row[c] = 0.f;
+    return;
+  }
+  const int J = j >> 2, g = j & 3;
+  float f[4 * Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int c = 16 * Q * J + 16 * q + 4 * g + v;
+      f[4 * q + v] = row[c] + bm[c];
+    }
+  const float x = z[(long)(t + 1) * B * Z + (long)b * Z + j];  // target z_{t+1, j}
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < K; ++k) mx = fmaxf(mx, f[k]);
+  float se = 0.f;
+#pragma unroll
+  for (int k = 0; k < K; ++k) se += expf(f[k] - mx);
+  const float lse_pi = mx + logf(se);
+  float joint[K], uu[K], sg[K];
+  float jm = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const float mu = f[K + k], ls = f[2 * K + k];
+    sg[k] = expf(ls);
+    uu[k] = (x - mu) / sg[k];
+    joint[k] = (f[k] - lse_pi) - 0.5f * uu[k] * uu[k] - ls - kHalfLn2Pi;
+    jm = fmaxf(jm, joint[k]);
+  }
+  float sj = 0.f;
+#pragma unroll
+  for (int k = 0; k < K; ++k) sj += expf(joint[k] - jm);
+  const float ll = jm + logf(sj);
+  const float s = valid ? -1.0f / (N * (float)Z) : 0.f;  // d loss / d loglik_j
+  float d[4 * Q];
+#pragma unroll
+  for (int k = 0; k < 4 * Q; ++k) d[k] = 0.f;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const float gam = expf(joint[k] - ll), pi = expf(f[k] - lse_pi);
+    d[k] = s * (gam - pi);
+    d[K + k] = s * gam * uu[k] / sg[k];
+    d[2 * K + k] = s * gam * (uu[k] * uu[k] - 1.0f);
+  }
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) row[16 * Q * J + 16 * q + 4 * g + v] = d[4 * q + v];
+}
+
+// LSTM backward of step t for (row b, unit u): with dh = d loss / d h_{t+1}
+// (heads + the later steps) and dc = d loss / d c_{t+1} from the later steps,
+// writes dG_t (pre-activation gradients, packed gate order) and the new dc
+__global__ void __launch_bounds__(256) k_grad_lstm_back(const float* G, const float* Cs, const float* dhh,
+                                                        const float* dhr, float* dc, float* dG, int B, int H,
+                                                        int t, int last) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)B * H) return;
+  const int b = (int)(idx / H), u = (int)(idx % H);
+  const long r = (long)t * B + b;
+  const float4 a = reinterpret_cast<const float4*>(G + r * 4 * H)[u];  // i, f, g, o
+  const float c1 = Cs[((long)(t + 1) * B + b) * H + u], c0 = Cs[((long)t * B + b) * H + u];
+  const float dh = dhh[r * H + u] + (last ? 0.f : dhr[(long)b * H + u]);
+  const float dcn = last ? 0.f : dc[(long)b * H + u];
+  const float th = tanhf(c1);
+  const float d_o = dh * th;
+  const float dcc = dcn + dh * a.w * (1.0f - th * th);
+  const float d_i = dcc * a.z, d_f = dcc * c0, d_g = dcc * a.x;
+  dc[(long)b * H + u] = dcc * a.y;
+  reinterpret_cast<float4*>(dG + r * 4 * H)[u] =
+      make_float4(d_i * a.x * (1.0f - a.x), d_f * a.y * (1.0f - a.y), d_g * (1.0f - a.z * a.z),
+                  d_o * a.w * (1.0f - a.w));
+}
+
+// column sums of src [R, Cc] in a fixed order: partial sums of row chunks,
+// then their sum (two launches)
+constexpr int kSumChunks = 64;
+__global__ void __launch_bounds__(256) k_colsum_part(const float* src, long ld, long R, int Cc, float* part) {
+  const int c = blockIdx.x * 256 + threadIdx.x, ch = blockIdx.y;
+  if (c >= Cc) return;
+  const long r0 = R * ch / kSumChunks, r1 = R * (ch + 1) / kSumChunks;
+  float s = 0.f;
+  for (long r = r0; r < r1; ++r) s += src[r * ld + c];
+  part[(long)ch * Cc + c] = s;
+}
+__global__ void __launch_bounds__(256) k_colsum_final(const float* part, int Cc, float* out) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= Cc) return;
+  float s = 0.f;
+  for (int ch = 0; ch < kSumChunks; ++ch) s += part[(long)ch * Cc + c];
+  out[c] = s;
+}
+
+// one-hot columns: dWa[a][j] = sum over rows r with action a of dG[r][j].
+// Block (256-column tile, row chunk, group of 64 actions): each thread owns
+// one column and accumulates the chunk's rows in row order into an LDS slot
+// per action; partial [chunk][a][j], summed over the chunks in order.
+constexpr int kActGroup = 64;
+__global__ void __launch_bounds__(256) k_grad_actions(const float* dG, const int32_t* actions, long R, int H4,
+                                                      int A, int nchunk, float* part) {
+  __shared__ float acc[kActGroup][256];
+  __shared__ int acts[256];
+  const int j = blockIdx.x * 256 + threadIdx.x, ch = blockIdx.y, a0 = blockIdx.z * kActGroup;
+  const long r0 = R * ch / nchunk, r1 = R * (ch + 1) / nchunk;
+  for (int a = 0; a < kActGroup; ++a) acc[a][threadIdx.x] = 0.f;
+  for (long rb = r0; rb < r1; rb += 256) {
+    __syncthreads();
+    const long r = rb + threadIdx.x;
+    const int av = r < r1 ? actions[r] : -1;
+    acts[threadIdx.x] = (av >= a0 && av < A && av < a0 + kActGroup) ? av - a0 : -1;
+    __syncthreads();
+    const int n = (int)min((long)256, r1 - rb);
+    for (int k = 0; k < n; ++k) {
+      const int a = acts[k];
+      if (a >= 0 && j < H4) acc[a][threadIdx.x] += dG[(rb + k) * H4 + j];
+    }
+  }
+  if (j >= H4) return;
+  const int na = min(kActGroup, A - a0);
+  for (int a = 0; a < na; ++a) part[((long)ch * A + a0 + a) * H4 + j] = acc[a][threadIdx.x];
+}
+__global__ void __launch_bounds__(256) k_grad_actions_sum(const float* part, long n, int nchunk, float* out) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int ch = 0; ch < nchunk; ++ch) s += part[(long)ch * n + i];
+  out[i] = s;
+}
+
+// loss = sum of the three means of the forward pass
+__global__ void k_grad_loss(const float* means, float* loss) {
+  if (threadIdx.x == 0) loss[0] = means[0] + means[1] + means[2];
+}
+
+// packed-order gradients -> canonical layout
+struct UnpackArgs {
+  int Z, H, A, K, Q, Nm, ldk;
+  const float *dWgT, *dWa, *dbg, *dWm, *dbm;  // [ldk, 4H], [A, 4H], [4H], [NmP, H], [NmP]
+  float *W_g, *b_g, *W_m, *b_m, *w_r, *b_r, *w_d, *b_d;
+};
+__global__ void __launch_bounds__(256) k_grad_unpack(const UnpackArgs p) {
+  const int Z = p.Z, H = p.H, A = p.A, K = p.K, Q = p.Q;
+  const long ng = (long)4 * H * (Z + A + H), nm = (long)3 * Z * K * H;
+  const long total = ng + 4 * H + nm + 3 * Z * K + 2 * H + 2;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
+    long e = i;
+    if (e < ng) {  // W_g: canonical row q H + u <- packed row 4u + q
+      const int cr = (int)(e / (Z + A + H)), c = (int)(e % (Z + A + H));
+      const int pr = 4 * (cr % H) + cr / H;
+      float v;
+      if (c < Z) v = p.dWgT[(long)c * 4 * H + pr];
+      else if (c < Z + A) v = p.dWa[(long)(c - Z) * 4 * H + pr];
+      else v = p.dWgT[(long)(Z + c - Z - A) * 4 * H + pr];
+      p.W_g[e] = v;
+      continue;
+    }
+    e -= ng;
+    if (e < 4 * H) {
+      p.b_g[e] = p.dbg[4 * (e % H) + e / H];
+      continue;
+    }
+    e -= 4 * H;
+    auto prow = [&](long cr) {  // canonical mixture row p ZK + j K + k -> packed row
+      const int pp = (int)(cr / ((long)Z * K)), rem = (int)(cr % ((long)Z * K));
+      const int j = rem / K, k = rem % K, f = pp * K + k;
+      return 16 * Q * (j >> 2) + 16 * (f >> 2) + 4 * (j & 3) + (f & 3);
+    };
+    if (e < nm) {
+      const long cr = e / H;
+      p.W_m[e] = p.dWm[(long)prow(cr) * H + e % H];
+      continue;
+    }
+    e -= nm;
+    if (e < 3 * Z * K) {
+      p.b_m[e] = p.dbm[prow(e)];
+      continue;
+    }
+    e -= 3 * Z * K;
+    if (e < H) { p.w_r[e] = p.dWm[(long)(p.Nm - 16) * H + e]; continue; }
+    e -= H;
+    if (e < H) { p.w_d[e] = p.dWm[(long)(p.Nm - 15) * H + e]; continue; }
+    e -= H;
+    if (e == 0) p.b_r[0] = p.dbm[p.Nm - 16];
+    else p.b_d[0] = p.dbm[p.Nm - 15];
+  }
+}
+
+hipError_t gemm_nt(const float* A, long lda, int M, const float* Bm, long ldb, int N, int Kpad, float* out,
+                   long ldo, hipStream_t s) {
+  using C = GradGemm;
+  const TileMap map = tile_map((N + C::BN - 1) / C::BN, (M + C::BM - 1) / C::BM, (size_t)N * Kpad * 4);
+  return launch("grad_gemm", k_gemm_nt, dim3(grid_of(map)), dim3(C::NT), 0, s, A, lda, M, Bm, ldb, N, Kpad,
+                out, ldo, map);
+}
+
+hipError_t transpose(const float* src, long ld, int R, int Cc, float* dst, long ldd, int Rp, hipStream_t s) {
+  return launch("grad_transpose", k_transpose, dim3((unsigned)((Rp + 31) / 32), (unsigned)((Cc + 31) / 32)),
+                dim3(256), 0, s, src, ld, R, Cc, dst, ldd, Rp);
+}
+
+hipError_t colsum(const float* src, long ld, long R, int Cc, float* part, float* out, hipStream_t s) {
+  hipError_t e = launch("grad_colsum", k_colsum_part, dim3((unsigned)((Cc + 255) / 256), kSumChunks),
+                        dim3(256), 0, s, src, ld, R, Cc, part);
+  if (e != hipSuccess) return e;
+  return launch("grad_colsum", k_colsum_final, dim3((unsigned)((Cc + 255) / 256)), dim3(256), 0, s, part, Cc,
+                out);
+}
+
+template <int KC>
+hipError_t launch_heads_k(float* M, long ldm, const float* bm, const float* z, const float* rewards,
+                          const uint8_t* dones, const int32_t* lengths, const float* nsum, int B, int T, int Z,
+                          int Nm, int NmP, hipStream_t s) {
+  const long n = (long)T * B * (Z + 1);
+  return launch("grad_heads", k_grad_heads<KC>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, M, ldm,
+                bm, z, rewards, dones, lengths, nsum, B, T, Z, Nm, NmP);
+}
+
+}  // namespace
+
+// row chunks of the one-hot column reduction: about 512 work-groups
+static int act_chunks(const Layout& L) {
+  const int tiles = (4 * L.H + 255) / 256 * ((L.A + kActGroup - 1) / kActGroup);
+  return std::min(64, std::max(1, 512 / tiles));
+}
+
+size_t grad_workspace(const Layout& L, int B, int T, char* ws, GradWs* G) {
+  const long TB = (long)T * B, TBp = (TB + 31) / 32 * 32;
+  const int H = L.H, H4 = 4 * H, NmP = (L.Nm + 31) / 32 * 32;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { const size_t at = o; o = wm_align256(o + bytes); return at; };
+  const size_t oG = take((size_t)TB * H4 * 4), oC = take((size_t)(T + 1) * B * H * 4);
+  const size_t oM = take((size_t)TB * NmP * 4), odG = take((size_t)TB * H4 * 4);
+  const size_t odhh = take((size_t)TB * H * 4), odh = take((size_t)B * H * 4), odc = take((size_t)B * H * 4);
+  const size_t oWhT = take((size_t)H * H4 * 4), oWmT = take((size_t)H * NmP * 4);
+  const size_t oT1 = take((size_t)std::max(H4, NmP) * TBp * 4);   // dG^T or dM^T
+  const size_t oT2 = take((size_t)std::max(L.ldk, H) * TBp * 4);  // X^T or H^T
+  const size_t odWgT = take((size_t)L.ldk * H4 * 4), odWa = take((size_t)L.A * H4 * 4);
+  const size_t odWm = take((size_t)NmP * H * 4), odbg = take((size_t)H4 * 4), odbm = take((size_t)NmP * 4);
+  const size_t opart = take((size_t)kSumChunks * std::max(H4, NmP) * 4);
+  const size_t oapart = take((size_t)act_chunks(L) * L.A * H4 * 4);
+  const size_t on = take(16);
+  const size_t ofwd = take((size_t)TB * 3 * 4 + 16);  // loglik, reward_se, done_bce; means
+  if (ws && G) {
+    auto f = [&](size_t at) { return reinterpret_cast<float*>(ws + at); };
+    G->G = f(oG); G->Cs = f(oC); G->M = f(oM); G->dG = f(odG); G->dhh = f(odhh); G->dh = f(odh);
+    G->dc = f(odc); G->WhT = f(oWhT); G->WmT = f(oWmT); G->T1 = f(oT1); G->T2 = f(oT2);
+    G->dWgT = f(odWgT); G->dWa = f(odWa); G->dWm = f(odWm); G->dbg = f(odbg); G->dbm = f(odbm);
+    G->part = f(opart); G->apart = f(oapart); G->nsum = f(on); G->fwd = f(ofwd);
+  }
+  return o;
+}
+
+hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const GradOut& out, hipStream_t s) {
+  const Layout& L = P.L;
+  const int B = N.B, T = N.T, Z = L.Z, H = L.H, A = L.A, H4 = 4 * H;
+  const long TB = (long)T * B, TBp = (TB + 31) / 32 * 32;
+  const int NmP = (L.Nm + 31) / 32 * 32;
+  const char* base = reinterpret_cast<const char*>(P.base);
+  const float* Wg = reinterpret_cast<const float*>(base + L.off_Wg);
+  const float* WaT = reinterpret_cast<const float*>(base + L.off_WaT);
+  const float* bg = reinterpret_cast<const float*>(base + L.off_bg);
+  const float* Wm = reinterpret_cast<const float*>(base + L.off_Wm);
+  const float* bm = reinterpret_cast<const float*>(base + L.off_bm);
+  const float* X = reinterpret_cast<const float*>(N.x);
+  const float* Hn = X + (long)B * L.ldx + Z;  // h_1 .. h_T: rows of X_1 .. X_T from column Z
+  hipError_t e;
+#define WM_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
+  // forward pass: X (z_t | h_t) and the loss
+  N.loglik = G.fwd;
+  N.reward_se = G.fwd + TB;
+  N.done_bce = G.fwd + 2 * TB;
+  N.means = G.fwd + 3 * TB;
+  WM_TRY(launch_nll(P, N, s));
+  if (out.loss) WM_TRY(launch("grad_loss", k_grad_loss, dim3(1), dim3(64), 0, s, N.means, out.loss));
+  WM_TRY(launch("grad_len", k_len_sum, dim3(1), dim3(256), 0, s, N.lengths, B, T, G.nsum));
+  // pre-activations of every step, then the scan (activations, c_t)
+  WM_TRY(gemm_nt(X, L.ldx, (int)TB, Wg, L.ldk, H4, L.ldk, G.G, H4, s));
+  WM_TRY(launch("grad_scan", k_grad_fwd_scan, dim3((unsigned)(((long)B * H + 255) / 256)), dim3(256), 0, s,
+                G.G, bg, WaT, N.actions, G.Cs, B, T, H, A));
+  // head outputs of every h_{t+1}, then d loss / d output in place
+  WM_TRY(gemm_nt(Hn, L.ldx, (int)TB, Wm, L.ldh, L.Nm, L.ldh, G.M, NmP, s));
+  switch (L.K) {
+#define WM_HK(k)                                                                                       \
+  case k:                                                                                              \
+    WM_TRY(launch_heads_k<k>(G.M, NmP, bm, N.z, N.rewards, N.dones, N.lengths, G.nsum, B, T, Z, L.Nm, \
+                             NmP, s));                                                                 \
+    break;
+    WM_HK(1) WM_HK(2) WM_HK(3) WM_HK(4) WM_HK(5) WM_HK(6) WM_HK(7) WM_HK(8)
+#undef WM_HK
+    default: return hipErrorInvalidValue;
+  }
+  // d loss / d h_{t+1} through the heads: dM [TB, NmP] . W_m (W_m^T [H, NmP], zero rows padded)
+  WM_TRY(transpose(Wm, L.ldh, L.Nm, H, G.WmT, NmP, NmP, s));
+  WM_TRY(gemm_nt(G.M, NmP, (int)TB, G.WmT, NmP, H, NmP, G.dhh, H, s));
+  // back through time
+  WM_TRY(transpose(Wg + Z, L.ldk, H4, H, G.WhT, H4, H4, s));  // W_h^T [H, 4H]
+  const unsigned eg = (unsigned)(((long)B * H + 255) / 256);
+  for (int t = T - 1; t >= 0; --t) {
+    WM_TRY(launch("grad_lstm", k_grad_lstm_back, dim3(eg), dim3(256), 0, s, G.G, G.Cs, G.dhh, G.dh, G.dc, G.dG,
+                  B, H, t, t == T - 1 ? 1 : 0));
+    if (t > 0) WM_TRY(gemm_nt(G.dG + (long)t * B * H4, H4, B, G.WhT, H4, H, H4, G.dh, H, s));
+  }
+  // dW_g^T [ldk, 4H] = X^T . dG over all rows (operands X^T [ldk, TBp], dG^T [4H, TBp])
+  WM_TRY(transpose(G.dG, H4, (int)TB, H4, G.T1, TBp, (int)TBp, s));
+  WM_TRY(transpose(X, L.ldx, (int)TB, L.ldk, G.T2, TBp, (int)TBp, s));
+  WM_TRY(gemm_nt(G.T2, TBp, L.ldk, G.T1, TBp, H4, (int)TBp, G.dWgT, H4, s));
+  WM_TRY(colsum(G.dG, H4, TB, H4, G.part, G.dbg, s));
+  const int nch = act_chunks(L);
+  WM_TRY(launch("grad_actions", k_grad_actions,
+                dim3((unsigned)((H4 + 255) / 256), (unsigned)nch, (unsigned)((A + kActGroup - 1) / kActGroup)),
+                dim3(256), 0, s, G.dG, N.actions, TB, H4, A, nch, G.apart));
+  WM_TRY(launch("grad_actions", k_grad_actions_sum, dim3((unsigned)(((long)A * H4 + 255) / 256)), dim3(256), 0,
+                s, G.apart, (long)A * H4, nch, G.dWa));
+  // dW_m [NmP, H] = dM^T . H (operands dM^T [NmP, TBp], H^T [H, TBp])
+  WM_TRY(transpose(G.M, NmP, (int)TB, NmP, G.T1, TBp, (int)TBp, s));
+  WM_TRY(transpose(Hn, L.ldx, (int)TB, H, G.T2, TBp, (int)TBp, s));
+  WM_TRY(gemm_nt(G.T1, TBp, NmP, G.T2, TBp, H, (int)TBp, G.dWm, H, s));
+  WM_TRY(colsum(G.M, NmP, TB, NmP, G.part, G.dbm, s));
+  // canonical layout
+  const UnpackArgs u{Z, H, A, L.K, L.Q, L.Nm, L.ldk, G.dWgT, G.dWa, G.dbg, G.dWm, G.dbm,
+                     out.W_g, out.b_g, out.W_m, out.b_m, out.w_r, out.b_r, out.w_d, out.b_d};
+  WM_TRY(launch("grad_unpack", k_grad_unpack, dim3(1024), dim3(256), 0, s, u));
+#undef WM_TRY
+  return hipSuccess;
 }
 
 }  // namespace wm

@@ -1,0 +1,139 @@
+"""GPU parity of the world-model training gradient (wm_nll_grad, through the
+C ABI) against the oracle's hand-written backpropagation through time
+(itself pinned against finite differences of the forward oracle), on every
+gradient and the loss; shapes with ragged tails over the GEMM tiles, two
+action groups, lengths with empty and partial rows, steps without an
+action, K from 1 to 8; the full NLL workload; argument errors.
+
+Tolerance: the gradient sums over all T B rows and runs back through T
+LSTM steps in fp32, so each entry is compared with rtol GRAD_RTOL (1e-3)
+against |ref| + a scale: the RMS of its array, at least 1e-3 of the RMS
+over every gradient.  The full workload's worst error is about 3e-4 of
+the scale (W_g); the small cases stay below 1e-5."""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import parity
+from oracle import train as otr
+from paper_2205_01435_amd import _lib as wmlib
+from paper_2205_01435_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+GRAD_RTOL = 1e-3
+
+
+def say(*a):
+    print("[gpu-test]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    wmlib.load()
+    yield
+
+
+def _t(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def _case(seed, B, T, Z, H, A, K, lengths=None, no_action=0.05):
+    w = wl.Workload("grad_case", "nll", B=B, T=T, Z=Z, H=H, A=A, K=K, dtype="fp32", seed=seed, mask_p=0.3)
+    d = wl.make_nll_inputs(w)
+    a = d["actions"].copy()
+    rng = np.random.default_rng(seed + 1000)
+    a[rng.random(a.shape) < no_action] = -1  # steps without an action
+    d["actions"] = a
+    d["lengths"] = lengths
+    return w, d
+
+
+def _check(w, d, tag):
+    say("nll_grad", tag, dict(B=w.B, T=w.T, Z=w.Z, H=w.H, A=w.A, K=w.K))
+    m = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, "fp32")
+    ln = None if d["lengths"] is None else _t(np.asarray(d["lengths"], np.int32))
+    g = wmlib.nll_grad(m, _t(d["z"]), _t(d["actions"]), _t(d["rewards"]), _t(d["dones"]), ln)
+    torch.cuda.synchronize()
+    L, ref = otr.loss_and_grads(d["weights"], w.dims, d["z"], d["actions"], d["rewards"], d["dones"],
+                                d["lengths"])
+    parity.close(g.loss.cpu().numpy(), np.array([L]), parity.RTOL["fp32"], f"{tag} loss")
+    g_rms = np.sqrt(np.mean(np.concatenate([np.asarray(ref[k], np.float64).reshape(-1) for k in otr.PARAMS]) ** 2))
+    for k in otr.PARAMS:
+        got = g.grads[k].cpu().numpy().astype(np.float64)
+        want = np.asarray(ref[k], np.float64).reshape(got.shape)
+        # scale: the array's RMS, at least 1e-3 of the RMS over every gradient
+        # (an array whose entries all vanish, e.g. the done head when every
+        # label is 1 and its logit saturates, is then compared absolutely)
+        scale = max(np.sqrt(np.mean(want ** 2)), 1e-3 * g_rms)
+        err = np.abs(got - want)
+        tol = GRAD_RTOL * (np.abs(want) + scale)
+        assert (err <= tol).all(), (f"{tag} grad {k}: {(err > tol).sum()} of {err.size} beyond rtol {GRAD_RTOL}; "
+                                    f"worst err/tol {(err / tol).max():.3g}")
+        if scale > 0:
+            say(tag, k, f"max err/scale {(err / scale).max():.2e}")
+    return g
+
+
+@pytest.mark.parametrize("seed,B,T,Z,H,A,K,lengths", [
+    (11, 37, 9, 8, 48, 5, 3, "mixed"),       # one tile, ragged rows, short and empty sequences
+    (12, 130, 12, 16, 96, 70, 5, None),      # several tiles, two action groups
+    (13, 67, 7, 24, 64, 9, 1, "mixed"),      # one Gaussian
+    (14, 45, 6, 8, 32, 4, 8, None),          # eight Gaussians
+    (15, 20, 1, 8, 16, 3, 2, None),          # a single step
+])
+def test_grad_parity(seed, B, T, Z, H, A, K, lengths):
+    ln = None
+    if lengths == "mixed":
+        ln = np.random.default_rng(seed).integers(0, T + 1, size=B).astype(np.int32)
+        ln[0], ln[1] = 0, T
+    w, d = _case(seed, B, T, Z, H, A, K, ln)
+    _check(w, d, f"seed {seed}")
+
+
+def test_grad_all_lengths_zero():
+    w, d = _case(16, 9, 4, 8, 16, 3, 2, np.zeros(9, np.int32))
+    g = _check(w, d, "N = 0")
+    assert float(g.loss.cpu()[0]) == 0.0
+    for k in otr.PARAMS:
+        assert not g.grads[k].abs().max().item(), k
+
+
+def test_grad_deterministic():
+    """Every reduction runs in a fixed order: two calls agree bit for bit."""
+    w, d = _case(17, 130, 8, 16, 64, 70, 5)
+    m = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, "fp32")
+    args = (_t(d["z"]), _t(d["actions"]), _t(d["rewards"]), _t(d["dones"]))
+    g1 = wmlib.nll_grad(m, *args)
+    c1 = {k: v.clone() for k, v in g1.grads.items()}
+    g2 = wmlib.nll_grad(m, *args)
+    torch.cuda.synchronize()
+    for k in otr.PARAMS:
+        assert torch.equal(c1[k], g2.grads[k]), k
+
+
+def test_grad_nll_workload():
+    """The NLL workload at full size (B 512, T 128, Z 64, H 512, A 64, K 5)
+    against the full oracle gradient."""
+    w = wl.WORKLOADS["nll"]
+    d = wl.make_nll_inputs(w)
+    d["lengths"] = None
+    _check(w, d, "nll workload")
+
+
+def test_grad_argument_errors():
+    w, d = _case(18, 4, 2, 8, 16, 3, 2)
+    m = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, "fp32")
+    args = (_t(d["z"]), _t(d["actions"]), _t(d["rewards"]), _t(d["dones"]))
+    b = wmlib.GradBuffers(m, 4, 2)
+    b.ws_bytes -= 256
+    with pytest.raises(wmlib.WmError):
+        wmlib.nll_grad(m, *args, bufs=b)
+    mb = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, "bf16")
+    with pytest.raises(wmlib.WmError):
+        wmlib.nll_grad(mb, *args)
