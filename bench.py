@@ -90,6 +90,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--no-workloads", action="store_true", help="skip the per-workload table")
+    ap.add_argument("--rows", default="", help="comma-separated rows of the per-workload table to run "
+                    "(default: all)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle sample budget")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -222,7 +224,7 @@ def main() -> int:
     }
 
     if not args.no_workloads:
-        out["workloads"] = workload_table(wmlib, wl, torch, cuda)
+        out["workloads"] = workload_table(wmlib, wl, torch, cuda, {r for r in args.rows.split(",") if r})
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, roll_in, nll_in, args.cpu_seconds)
@@ -231,10 +233,13 @@ def main() -> int:
     return 0
 
 
-def workload_table(wmlib, wl, torch, cuda) -> dict:
-    """Whole-call timing of every workload (median of a few calls)."""
+def workload_table(wmlib, wl, torch, cuda, only=frozenset()) -> dict:
+    """Whole-call timing of every workload (median of a few calls); `only`
+    (non-empty) restricts the table to the rows it names."""
     res = {}
     for name, w in wl.WORKLOADS.items():
+        if only and name not in only:
+            continue
         if w.kind == "rollout":
             inp = wl.make_rollout_inputs(w)
             m = wmlib.pack(inp["weights"], w.Z, w.H, w.A, w.K, w.dtype)
@@ -272,10 +277,68 @@ def workload_table(wmlib, wl, torch, cuda) -> dict:
         res[name] = row
         del bufs, m
         torch.cuda.empty_cache()
-    res["returns_gae_xlarge"] = returns_row(wmlib, torch, cuda)
-    res["two_level_rollout"] = two_level_row(wmlib, wl, torch, cuda)
-    res["adam_xlarge_wm"] = adam_row(wmlib, torch)
+    extra = {"returns_gae_xlarge": lambda: returns_row(wmlib, torch, cuda),
+             "two_level_rollout": lambda: two_level_row(wmlib, wl, torch, cuda),
+             "adam_xlarge_wm": lambda: adam_row(wmlib, torch),
+             "train_step_nll": lambda: train_step_row(wmlib, wl, torch, cuda)}
+    for name, fn in extra.items():
+        if not only or name in only:
+            res[name] = fn()
     return res
+
+
+def train_step_row(wmlib, wl, torch, cuda) -> dict:
+    """One world-model training step on the NLL workload (B 512 sequences,
+    T 128, Z 64, H 512, A 64, K 5, fp32): the loss gradient by
+    backpropagation through time (wm_nll_grad), Adam on the flat canonical
+    parameters (wm_adam_step) and the re-pack for the next forward pass.
+    Algorithmic FLOPs per token: three times the forward products, 2 4H (Z+H)
+    for the gates and 2 H (3ZK+2) for the heads (the forward, the gradient
+    with respect to the inputs, the gradient with respect to the weights)."""
+    w = wl.WORKLOADS["nll"]
+    d = wl.make_nll_inputs(w)
+    m = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, "fp32")
+    args = [cuda(d[k]) for k in ("z", "actions", "rewards", "dones")]
+    gb = wmlib.GradBuffers(m, w.B, w.T)
+    params = torch.cat([cuda(np.asarray(d["weights"][k], np.float32).reshape(-1))
+                        for k in wmlib.GRAD_SHAPES])
+    canon = wmlib.flat_views(params, w.Z, w.H, w.A, w.K)
+    canon["W_c"] = cuda(np.asarray(d["weights"]["W_c"], np.float32))
+    canon["b_c"] = cuda(np.asarray(d["weights"]["b_c"], np.float32))
+    mom, vel = torch.zeros_like(params), torch.zeros_like(params)
+
+    def step(i):
+        wmlib.nll_grad(m, *args, bufs=gb)
+        wmlib.adam_step(params, gb.flat, mom, vel, i + 1, 1e-4)
+        wmlib.repack(m, canon)
+
+    step(0)
+    torch.cuda.synchronize()
+    times = []
+    for i in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        step(i + 1)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    ms = float(np.median(times))
+    wmlib.profile_reset()
+    wmlib.profile_enable("")
+    step(6)
+    torch.cuda.synchronize()
+    parts = {p: wmlib.profile_read(p)[0] for p in ("nll_persist", "mdn", "grad_gemm_bptt", "grad_gemm",
+                                                  "grad_lstm", "grad_", "adam", "pack")}
+    wmlib.profile_enable(None)
+    wmlib.profile_reset()
+    parts["grad_gemm"] -= parts["grad_gemm_bptt"]
+    parts["grad_other"] = parts.pop("grad_") - parts["grad_gemm"] - parts["grad_gemm_bptt"] - parts["grad_lstm"]
+    fwd = 2 * 4 * w.H * (w.Z + w.H) + 2 * w.H * (3 * w.Z * w.K + 2)
+    n = w.B * w.T
+    fl = 3.0 * fwd * n
+    return {"ms": ms, "tokens_per_s": n / (ms / 1e3), "flops_per_step": fl, "tflops": fl / (ms / 1e3) / 1e12,
+            "frac_fp32_peak": fl / (ms / 1e3) / PEAK["fp32"], "kernel_ms": {k: round(v, 4) for k, v in parts.items()},
+            "loss": float(gb.loss.cpu()[0])}
 
 
 def adam_row(wmlib, torch) -> dict:

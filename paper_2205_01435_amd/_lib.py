@@ -9,6 +9,7 @@ missing or fails to load, every entry point raises.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from dataclasses import dataclass
 
@@ -157,6 +158,20 @@ def pack(weights: dict, Z: int, H: int, A: int, K: int, dtype: str = "fp32",
     return Model(dims, packed, Z, H, A, K, dtype)
 
 
+def repack(m: Model, canon: dict):
+    """Re-pack canonical float32 device tensors (every weight, the
+    controller's included) into m.packed on the current stream (after an
+    optimiser step); nothing is allocated and nothing waits."""
+    lib = load()
+    for k in ("W_g", "b_g", "W_m", "b_m", "w_r", "b_r", "w_d", "b_d", "W_c", "b_c"):
+        t = canon[k]
+        assert t.is_cuda and t.dtype == torch.float32 and t.is_contiguous(), k
+    cw = CWeights(*[ctypes.c_void_p(canon[k].data_ptr()) for k in
+                    ("W_g", "b_g", "W_m", "b_m", "w_r", "b_r", "w_d", "b_d", "W_c", "b_c")])
+    _check(lib.wm_pack_weights(ctypes.byref(m.dims), ctypes.byref(cw), _ptr(m.packed), m.packed.numel(),
+                               _stream()))
+
+
 def controller_step(m: Model, z, h, mask, seed: int, step: int, traj0: int = 0,
                     want_probs: bool = True):
     """Returns (probs [B, A] or None, action [B] int32)."""
@@ -259,12 +274,28 @@ GRAD_SHAPES = {  # canonical gradient shapes, as the weights
 }
 
 
+def flat_views(flat, Z: int, H: int, A: int, K: int) -> dict:
+    """Views of a flat float32 tensor as the world-model weights, in the
+    order of GRAD_SHAPES (the layout of GradBuffers.flat)."""
+    out, o = {}, 0
+    for k, f in GRAD_SHAPES.items():
+        shp = f(Z, H, A, K)
+        n = math.prod(shp)
+        out[k] = flat[o:o + n].view(shp)
+        o += n
+    return out
+
+
 class GradBuffers:
+    """Loss, gradients (views of one flat buffer, GRAD_SHAPES order) and the
+    workspace of one wm_nll_grad shape."""
+
     def __init__(self, m: Model, B: int, T: int):
         dev = m.packed.device
         self.loss = torch.empty(1, dtype=torch.float32, device=dev)
-        self.grads = {k: torch.empty(f(m.Z, m.H, m.A, m.K), dtype=torch.float32, device=dev)
-                      for k, f in GRAD_SHAPES.items()}
+        n = sum(math.prod(f(m.Z, m.H, m.A, m.K)) for f in GRAD_SHAPES.values())
+        self.flat = torch.empty(n, dtype=torch.float32, device=dev)
+        self.grads = flat_views(self.flat, m.Z, m.H, m.A, m.K)
         nws = workspace_bytes(m.dims, B, T, 2)
         self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
         self.ws_bytes = nws

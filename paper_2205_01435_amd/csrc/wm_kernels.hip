@@ -2255,13 +2255,18 @@ using GradGemm = GemmD<float, 4, 2, 2, 2, 2>;  // 128 x 64 tiles
 // out[m][n] = sum_{k < Kpad} A[m][k] B[n][k] for m < M, n < N (Kpad a
 // multiple of 32; columns of A and B up to Kpad must be readable, zero
 // beyond the data)
+// Split K: work-group row y takes columns [y Kpad, (y + 1) Kpad) and writes
+// out + y oslice (the caller sums the slices).
 __global__ void __launch_bounds__(GradGemm::NT) k_gemm_nt(const float* A, long lda, int M, const float* Bm,
                                                           long ldb, int N, int Kpad, float* out, long ldo,
-                                                          TileMap map) {
+                                                          long oslice, TileMap map) {
   using C = GradGemm;
   __shared__ __attribute__((aligned(16))) char lds[C::LDS_BYTES];
   int nt, mt;
   if (!tile_of(map, nt, mt)) return;
+  A += (long)blockIdx.y * Kpad;
+  Bm += (long)blockIdx.y * Kpad;
+  out += (long)blockIdx.y * oslice;
   const int n0 = nt * C::BN, m0 = mt * C::BM;
   const SrcX<float> w(Bm, ldb, Kpad, n0, C::BN, N);
   const SrcX<float> x(A, lda, Kpad, m0, C::BM, M);
@@ -2420,16 +2425,22 @@ __global__ void __launch_bounds__(256) k_grad_heads(float* M, long ldm, const fl
 // LSTM backward of step t for (row b, unit u): with dh = d loss / d h_{t+1}
 // (heads + the later steps) and dc = d loss / d c_{t+1} from the later steps,
 // writes dG_t (pre-activation gradients, packed gate order) and the new dc
+// (dhr: S slices [S, B, H] of the later step's dG . W_h, summed in order)
 __global__ void __launch_bounds__(256) k_grad_lstm_back(const float* G, const float* Cs, const float* dhh,
-                                                        const float* dhr, float* dc, float* dG, int B, int H,
-                                                        int t, int last) {
+                                                        const float* dhr, int S, float* dc, float* dG, int B,
+                                                        int H, int t, int last) {
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long)B * H) return;
   const int b = (int)(idx / H), u = (int)(idx % H);
   const long r = (long)t * B + b;
   const float4 a = reinterpret_cast<const float4*>(G + r * 4 * H)[u];  // i, f, g, o
   const float c1 = Cs[((long)(t + 1) * B + b) * H + u], c0 = Cs[((long)t * B + b) * H + u];
-  const float dh = dhh[r * H + u] + (last ? 0.f : dhr[(long)b * H + u]);
+  float dh = dhh[r * H + u];
+  if (!last) {
+    float sum = 0.f;
+    for (int k = 0; k < S; ++k) sum += dhr[(long)k * B * H + (long)b * H + u];
+    dh += sum;
+  }
   const float dcn = last ? 0.f : dc[(long)b * H + u];
   const float th = tanhf(c1);
   const float d_o = dh * th;
@@ -2448,9 +2459,16 @@ __global__ void __launch_bounds__(256) k_colsum_part(const float* src, long ld, 
   const int c = blockIdx.x * 256 + threadIdx.x, ch = blockIdx.y;
   if (c >= Cc) return;
   const long r0 = R * ch / kSumChunks, r1 = R * (ch + 1) / kSumChunks;
-  float s = 0.f;
-  for (long r = r0; r < r1; ++r) s += src[r * ld + c];
-  part[(long)ch * Cc + c] = s;
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;  // rows r0 + 4i + 0..3
+  long r = r0;
+  for (; r + 4 <= r1; r += 4) {
+    s0 += src[r * ld + c];
+    s1 += src[(r + 1) * ld + c];
+    s2 += src[(r + 2) * ld + c];
+    s3 += src[(r + 3) * ld + c];
+  }
+  for (; r < r1; ++r) s0 += src[r * ld + c];
+  part[(long)ch * Cc + c] = (s0 + s1) + (s2 + s3);
 }
 __global__ void __launch_bounds__(256) k_colsum_final(const float* part, int Cc, float* out) {
   const int c = blockIdx.x * 256 + threadIdx.x;
@@ -2554,12 +2572,50 @@ __global__ void __launch_bounds__(256) k_grad_unpack(const UnpackArgs p) {
   }
 }
 
-hipError_t gemm_nt(const float* A, long lda, int M, const float* Bm, long ldb, int N, int Kpad, float* out,
-                   long ldo, hipStream_t s) {
+// K slices of an M x N x Kpad product: doubled (up to WM_GRAD_MAX_SPLIT)
+// while the tiles number under 512 and the 32-column chunks divide evenly
+#ifndef WM_GRAD_MAX_SPLIT
+#define WM_GRAD_MAX_SPLIT 8
+#endif
+int split_of(int M, int N, int Kpad) {
   using C = GradGemm;
-  const TileMap map = tile_map((N + C::BN - 1) / C::BN, (M + C::BM - 1) / C::BM, (size_t)N * Kpad * 4);
-  return launch("grad_gemm", k_gemm_nt, dim3(grid_of(map)), dim3(C::NT), 0, s, A, lda, M, Bm, ldb, N, Kpad,
-                out, ldo, map);
+  const long tiles = (long)((N + C::BN - 1) / C::BN) * ((M + C::BM - 1) / C::BM);
+  const int chunks = Kpad / 32;
+  int S = 1;
+  while (S < WM_GRAD_MAX_SPLIT && tiles * S < 512 && chunks % (2 * S) == 0 && chunks / (2 * S) >= 4) S *= 2;
+  return S;
+}
+
+// out (ldo) = A . B^T in S K-slices; S > 1 writes slice y to out + y oslice
+hipError_t gemm_nt_slices(const char* name, const float* A, long lda, int M, const float* Bm, long ldb, int N,
+                          int Kpad, int S, float* out, long ldo, long oslice, hipStream_t s) {
+  using C = GradGemm;
+  const int Ks = Kpad / S;
+  const TileMap map = tile_map((N + C::BN - 1) / C::BN, (M + C::BM - 1) / C::BM, (size_t)N * Ks * 4);
+  return launch(name, k_gemm_nt, dim3(grid_of(map), (unsigned)S), dim3(C::NT), 0, s, A, lda, M, Bm, ldb, N, Ks,
+                out, ldo, oslice, map);
+}
+
+// out[m][n] = sum_s part[s][m][n] in slice order
+__global__ void __launch_bounds__(256) k_sum_slices(const float* part, int S, int M, int N, float* out, long ldo) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long)M * N) return;
+  const long mn = (long)M * N;
+  float acc = 0.f;
+  for (int k = 0; k < S; ++k) acc += part[k * mn + i];
+  out[(i / N) * ldo + i % N] = acc;
+}
+
+// out (ldo) = A . B^T, split over K through `part` ([S, M, N]) when that
+// fills the chip better
+hipError_t gemm_nt(const float* A, long lda, int M, const float* Bm, long ldb, int N, int Kpad, float* out,
+                   long ldo, float* part, hipStream_t s) {
+  const int S = part ? split_of(M, N, Kpad) : 1;
+  if (S == 1) return gemm_nt_slices("grad_gemm", A, lda, M, Bm, ldb, N, Kpad, 1, out, ldo, 0, s);
+  const hipError_t e = gemm_nt_slices("grad_gemm", A, lda, M, Bm, ldb, N, Kpad, S, part, N, (long)M * N, s);
+  if (e != hipSuccess) return e;
+  return launch("grad_sum", k_sum_slices, dim3((unsigned)(((long)M * N + 255) / 256)), dim3(256), 0, s, part, S, M,
+                N, out, ldo);
 }
 
 hipError_t transpose(const float* src, long ld, int R, int Cc, float* dst, long ldd, int Rp, hipStream_t s) {
@@ -2607,6 +2663,16 @@ size_t grad_workspace(const Layout& L, int B, int T, char* ws, GradWs* G) {
   const size_t odWm = take((size_t)NmP * H * 4), odbg = take((size_t)H4 * 4), odbm = take((size_t)NmP * 4);
   const size_t opart = take((size_t)kSumChunks * std::max(H4, NmP) * 4);
   const size_t oapart = take((size_t)act_chunks(L) * L.A * H4 * 4);
+  // split-K partials: the largest of the products that split, and the
+  // per-step slices of dG_t . W_h (always)
+  auto split_need = [](int M, int N, int Kpad) {
+    const int S = split_of(M, N, Kpad);
+    return S > 1 ? (size_t)S * M * N : (size_t)0;
+  };
+  const size_t nsplit = std::max({(size_t)split_of(B, H, H4) * B * H, split_need((int)TB, H4, L.ldk),
+                                  split_need((int)TB, L.Nm, L.ldh), split_need((int)TB, H, NmP),
+                                  split_need(L.ldk, H4, (int)TBp), split_need(NmP, H, (int)TBp)});
+  const size_t osplit = take(nsplit * 4);
   const size_t on = take(16);
   const size_t ofwd = take((size_t)TB * 3 * 4 + 16);  // loglik, reward_se, done_bce; means
   if (ws && G) {
@@ -2614,7 +2680,7 @@ size_t grad_workspace(const Layout& L, int B, int T, char* ws, GradWs* G) {
     G->G = f(oG); G->Cs = f(oC); G->M = f(oM); G->dG = f(odG); G->dhh = f(odhh); G->dh = f(odh);
     G->dc = f(odc); G->WhT = f(oWhT); G->WmT = f(oWmT); G->T1 = f(oT1); G->T2 = f(oT2);
     G->dWgT = f(odWgT); G->dWa = f(odWa); G->dWm = f(odWm); G->dbg = f(odbg); G->dbm = f(odbm);
-    G->part = f(opart); G->apart = f(oapart); G->nsum = f(on); G->fwd = f(ofwd);
+    G->part = f(opart); G->apart = f(oapart); G->split = f(osplit); G->nsum = f(on); G->fwd = f(ofwd);
   }
   return o;
 }
@@ -2643,11 +2709,11 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   if (out.loss) WM_TRY(launch("grad_loss", k_grad_loss, dim3(1), dim3(64), 0, s, N.means, out.loss));
   WM_TRY(launch("grad_len", k_len_sum, dim3(1), dim3(256), 0, s, N.lengths, B, T, G.nsum));
   // pre-activations of every step, then the scan (activations, c_t)
-  WM_TRY(gemm_nt(X, L.ldx, (int)TB, Wg, L.ldk, H4, L.ldk, G.G, H4, s));
+  WM_TRY(gemm_nt(X, L.ldx, (int)TB, Wg, L.ldk, H4, L.ldk, G.G, H4, G.split, s));
   WM_TRY(launch("grad_scan", k_grad_fwd_scan, dim3((unsigned)(((long)B * H + 255) / 256)), dim3(256), 0, s,
                 G.G, bg, WaT, N.actions, G.Cs, B, T, H, A));
   // head outputs of every h_{t+1}, then d loss / d output in place
-  WM_TRY(gemm_nt(Hn, L.ldx, (int)TB, Wm, L.ldh, L.Nm, L.ldh, G.M, NmP, s));
+  WM_TRY(gemm_nt(Hn, L.ldx, (int)TB, Wm, L.ldh, L.Nm, L.ldh, G.M, NmP, G.split, s));
   switch (L.K) {
 #define WM_HK(k)                                                                                       \
   case k:                                                                                              \
@@ -2660,19 +2726,22 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   }
   // d loss / d h_{t+1} through the heads: dM [TB, NmP] . W_m (W_m^T [H, NmP], zero rows padded)
   WM_TRY(transpose(Wm, L.ldh, L.Nm, H, G.WmT, NmP, NmP, s));
-  WM_TRY(gemm_nt(G.M, NmP, (int)TB, G.WmT, NmP, H, NmP, G.dhh, H, s));
+  WM_TRY(gemm_nt(G.M, NmP, (int)TB, G.WmT, NmP, H, NmP, G.dhh, H, G.split, s));
   // back through time
   WM_TRY(transpose(Wg + Z, L.ldk, H4, H, G.WhT, H4, H4, s));  // W_h^T [H, 4H]
   const unsigned eg = (unsigned)(((long)B * H + 255) / 256);
+  const int Sb = split_of(B, H, H4);  // K slices of dG_t . W_h, summed by the next step's kernel
   for (int t = T - 1; t >= 0; --t) {
-    WM_TRY(launch("grad_lstm", k_grad_lstm_back, dim3(eg), dim3(256), 0, s, G.G, G.Cs, G.dhh, G.dh, G.dc, G.dG,
-                  B, H, t, t == T - 1 ? 1 : 0));
-    if (t > 0) WM_TRY(gemm_nt(G.dG + (long)t * B * H4, H4, B, G.WhT, H4, H, H4, G.dh, H, s));
+    WM_TRY(launch("grad_lstm", k_grad_lstm_back, dim3(eg), dim3(256), 0, s, G.G, G.Cs, G.dhh, G.split, Sb, G.dc,
+                  G.dG, B, H, t, t == T - 1 ? 1 : 0));
+    if (t > 0)
+      WM_TRY(gemm_nt_slices("grad_gemm_bptt", G.dG + (long)t * B * H4, H4, B, G.WhT, H4, H, H4, Sb, G.split, H,
+                            (long)B * H, s));
   }
   // dW_g^T [ldk, 4H] = X^T . dG over all rows (operands X^T [ldk, TBp], dG^T [4H, TBp])
   WM_TRY(transpose(G.dG, H4, (int)TB, H4, G.T1, TBp, (int)TBp, s));
   WM_TRY(transpose(X, L.ldx, (int)TB, L.ldk, G.T2, TBp, (int)TBp, s));
-  WM_TRY(gemm_nt(G.T2, TBp, L.ldk, G.T1, TBp, H4, (int)TBp, G.dWgT, H4, s));
+  WM_TRY(gemm_nt(G.T2, TBp, L.ldk, G.T1, TBp, H4, (int)TBp, G.dWgT, H4, G.split, s));
   WM_TRY(colsum(G.dG, H4, TB, H4, G.part, G.dbg, s));
   const int nch = act_chunks(L);
   WM_TRY(launch("grad_actions", k_grad_actions,
@@ -2683,7 +2752,7 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   // dW_m [NmP, H] = dM^T . H (operands dM^T [NmP, TBp], H^T [H, TBp])
   WM_TRY(transpose(G.M, NmP, (int)TB, NmP, G.T1, TBp, (int)TBp, s));
   WM_TRY(transpose(Hn, L.ldx, (int)TB, H, G.T2, TBp, (int)TBp, s));
-  WM_TRY(gemm_nt(G.T1, TBp, NmP, G.T2, TBp, H, (int)TBp, G.dWm, H, s));
+  WM_TRY(gemm_nt(G.T1, TBp, NmP, G.T2, TBp, H, (int)TBp, G.dWm, H, G.split, s));
   WM_TRY(colsum(G.M, NmP, TB, NmP, G.part, G.dbm, s));
   // canonical layout
   const UnpackArgs u{Z, H, A, L.K, L.Q, L.Nm, L.ldk, G.dWgT, G.dWa, G.dbg, G.dWm, G.dbm,

@@ -137,3 +137,30 @@ def test_grad_argument_errors():
     mb = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, "bf16")
     with pytest.raises(wmlib.WmError):
         wmlib.nll_grad(mb, *args)
+
+
+def test_train_step_repack():
+    """A training step's tail: Adam on the flat gradient buffer, then
+    wm_pack_weights into the model's packed buffer; the NLL pass on it must
+    equal the one on a fresh pack of the updated weights bit for bit (the
+    packed buffers themselves differ in their unwritten alignment gaps)."""
+    w, d = _case(19, 33, 5, 16, 48, 6, 3)
+    m = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, "fp32")
+    args = (_t(d["z"]), _t(d["actions"]), _t(d["rewards"]), _t(d["dones"]))
+    gb = wmlib.nll_grad(m, *args)
+    params = torch.cat([_t(np.asarray(d["weights"][k], np.float32).reshape(-1)) for k in wmlib.GRAD_SHAPES])
+    canon = wmlib.flat_views(params, w.Z, w.H, w.A, w.K)
+    canon["W_c"] = _t(np.asarray(d["weights"]["W_c"], np.float32))
+    canon["b_c"] = _t(np.asarray(d["weights"]["b_c"], np.float32))
+    mom, vel = torch.zeros_like(params), torch.zeros_like(params)
+    wmlib.adam_step(params, gb.flat, mom, vel, 1, 1e-2)
+    wmlib.repack(m, canon)
+    torch.cuda.synchronize()
+    host = {k: v.cpu().numpy() for k, v in canon.items()}
+    fresh = wmlib.pack(host, w.Z, w.H, w.A, w.K, "fp32")
+    assert not np.array_equal(host["W_g"], np.asarray(d["weights"]["W_g"], np.float32))
+    o1 = wmlib.nll(m, *args)
+    o2 = wmlib.nll(fresh, *args)
+    torch.cuda.synchronize()
+    for k in ("loglik", "reward_se", "done_bce", "means"):
+        assert torch.equal(getattr(o1, k), getattr(o2, k)), k
