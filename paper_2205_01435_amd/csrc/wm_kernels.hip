@@ -2082,8 +2082,9 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
                 X + (long)(T & 1) * BX, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
 }
 
+// heads = false: the recurrence only (X_1 .. X_T), for the training gradient
 template <typename DT>
-hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
+hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s, bool heads = true) {
   const Layout& L = P.L;
   const char* base = reinterpret_cast<const char*>(P.base);
   const int B = N.B, T = N.T, Z = L.Z, H = L.H;
@@ -2112,6 +2113,7 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s) {
     const hipError_t eg = launch_gates<DT>(ga, s);
     if (eg != hipSuccess) return eg;
   }
+  if (!heads) return hipSuccess;
 
   const int ntd = Z / 8;
   MdnArgs ma{};
@@ -2250,17 +2252,24 @@ hipError_t launch_nll(const Packed& P, const NllBufs& N, hipStream_t s) {
 // ===========================================================================
 namespace {
 
-using GradGemm = GemmD<float, 4, 2, 2, 2, 2>;  // 128 x 64 tiles
+#ifndef WM_GRAD_STAGES
+#define WM_GRAD_STAGES 2
+#endif
+#ifndef WM_BPTT_STAGES
+#define WM_BPTT_STAGES 2
+#endif
+using GradGemm = GemmD<float, 4, 2, 2, 2, WM_GRAD_STAGES>;   // 128 x 64 tiles: the products over all rows
+using GradGemmS = GemmD<float, 2, 2, 2, 2, WM_BPTT_STAGES>;  // 64 x 64 tiles: the per-step product dG_t . W_h
 
 // out[m][n] = sum_{k < Kpad} A[m][k] B[n][k] for m < M, n < N (Kpad a
 // multiple of 32; columns of A and B up to Kpad must be readable, zero
 // beyond the data)
 // Split K: work-group row y takes columns [y Kpad, (y + 1) Kpad) and writes
 // out + y oslice (the caller sums the slices).
-__global__ void __launch_bounds__(GradGemm::NT) k_gemm_nt(const float* A, long lda, int M, const float* Bm,
-                                                          long ldb, int N, int Kpad, float* out, long ldo,
-                                                          long oslice, TileMap map) {
-  using C = GradGemm;
+template <class C>
+__global__ void __launch_bounds__(C::NT) k_gemm_nt(const float* A, long lda, int M, const float* Bm, long ldb,
+                                                   int N, int Kpad, float* out, long ldo, long oslice,
+                                                   TileMap map) {
   __shared__ __attribute__((aligned(16))) char lds[C::LDS_BYTES];
   int nt, mt;
   if (!tile_of(map, nt, mt)) return;
@@ -2351,11 +2360,13 @@ __global__ void __launch_bounds__(256) k_grad_fwd_scan(float* G, const float* bg
 // mixture features of packed rows 16 Q J + 16 q + 4 g + v (j = 4J + g,
 // feature 4q + v); thread j = Z takes the reward/done block and the padding
 // columns.  M holds the head's GEMM outputs and is overwritten with dM.
+// lrow [T B, Z+1] receives each (row, dim)'s share of the loss: -loglik_j /
+// (N Z), and (se + bce) / N in column Z (0 on padded steps).
 template <int KC>
 __global__ void __launch_bounds__(256) k_grad_heads(float* M, long ldm, const float* bm, const float* z,
                                                     const float* rewards, const uint8_t* dones,
                                                     const int32_t* lengths, const float* nsum, int B, int T,
-                                                    int Z, int Nm, int NmP) {
+                                                    int Z, int Nm, int NmP, float* lrow) {
   constexpr int K = KC, Q = (3 * K + 3) / 4;
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long)T * B * (Z + 1)) return;
@@ -2368,8 +2379,12 @@ __global__ void __launch_bounds__(256) k_grad_heads(float* M, long ldm, const fl
   if (j == Z) {
     const int hr = Nm - 16;
     const float rr = row[hr] + bm[hr], rd = row[hr + 1] + bm[hr + 1];
-    row[hr] = valid ? 2.0f * (rr - rewards[r]) / N : 0.f;
-    row[hr + 1] = valid ? (sig_(rd) - (float)dones[r]) / N : 0.f;
+    const float dr = rr - rewards[r], dd = (float)dones[r];
+    // softplus(rd) - d rd, stable for either sign of rd
+    const float bce = fmaxf(rd, 0.f) + log1pf(expf(-fabsf(rd))) - dd * rd;
+    lrow[r * (Z + 1) + Z] = valid ? (dr * dr + bce) / N : 0.f;
+    row[hr] = valid ? 2.0f * dr / N : 0.f;
+    row[hr + 1] = valid ? (sig_(rd) - dd) / N : 0.f;
     for (int c = hr + 2; c < Nm; ++c) row[c] = 0.f;
     for (int c = Nm; c < NmP; ++c) row[c] = 0.f;
     return;
@@ -2406,6 +2421,7 @@ __global__ void __launch_bounds__(256) k_grad_heads(float* M, long ldm, const fl
   for (int k = 0; k < K; ++k) sj += expf(joint[k] - jm);
   const float ll = jm + logf(sj);
   const float s = valid ? -1.0f / (N * (float)Z) : 0.f;  // d loss / d loglik_j
+  lrow[r * (Z + 1) + j] = s * ll;
   float d[4 * Q];
 #pragma unroll
   for (int k = 0; k < 4 * Q; ++k) d[k] = 0.f;
@@ -2497,9 +2513,17 @@ __global__ void __launch_bounds__(256) k_grad_actions(const float* dG, const int
     acts[threadIdx.x] = (av >= a0 && av < A && av < a0 + kActGroup) ? av - a0 : -1;
     __syncthreads();
     const int n = (int)min((long)256, r1 - rb);
-    for (int k = 0; k < n; ++k) {
-      const int a = acts[k];
-      if (a >= 0 && j < H4) acc[a][threadIdx.x] += dG[(rb + k) * H4 + j];
+    for (int k = 0; k < n; k += 4) {
+      int a[4];
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        a[q] = (k + q < n && j < H4) ? acts[k + q] : -1;
+        v[q] = a[q] >= 0 ? dG[(rb + k + q) * H4 + j] : 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (a[q] >= 0) acc[a[q]][threadIdx.x] += v[q];
     }
   }
   if (j >= H4) return;
@@ -2514,9 +2538,23 @@ __global__ void __launch_bounds__(256) k_grad_actions_sum(const float* part, lon
   out[i] = s;
 }
 
-// loss = sum of the three means of the forward pass
-__global__ void k_grad_loss(const float* means, float* loss) {
-  if (threadIdx.x == 0) loss[0] = means[0] + means[1] + means[2];
+// Fixed-order sum of n floats: block b sums its contiguous piece (each
+// thread a strided share, then a tree over the block) into part[b]; one
+// block then sums part[0 .. nb) the same way.
+constexpr int kFlatBlocks = 512;
+__global__ void __launch_bounds__(256) k_flat_sum(const float* x, long n, float* part) {
+  __shared__ float red[256];
+  const long per = (n + gridDim.x - 1) / gridDim.x;
+  const long i0 = (long)blockIdx.x * per, i1 = min(n, i0 + per);
+  float acc = 0.f;
+  for (long i = i0 + threadIdx.x; i < i1; i += 256) acc += x[i];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) part[blockIdx.x] = red[0];
 }
 
 // packed-order gradients -> canonical layout
@@ -2577,23 +2615,33 @@ __global__ void __launch_bounds__(256) k_grad_unpack(const UnpackArgs p) {
 #ifndef WM_GRAD_MAX_SPLIT
 #define WM_GRAD_MAX_SPLIT 8
 #endif
-int split_of(int M, int N, int Kpad) {
-  using C = GradGemm;
+template <class C = GradGemm>
+int split_of(int M, int N, int Kpad, long target = 512) {
   const long tiles = (long)((N + C::BN - 1) / C::BN) * ((M + C::BM - 1) / C::BM);
   const int chunks = Kpad / 32;
   int S = 1;
-  while (S < WM_GRAD_MAX_SPLIT && tiles * S < 512 && chunks % (2 * S) == 0 && chunks / (2 * S) >= 4) S *= 2;
+  while (S < WM_GRAD_MAX_SPLIT && tiles * S < target && chunks % (2 * S) == 0 && chunks / (2 * S) >= 4) S *= 2;
   return S;
 }
 
+// the per-step product: its tile shape and K slices
+#ifndef WM_BPTT_TILE64
+#define WM_BPTT_TILE64 1
+#endif
+#ifndef WM_BPTT_TARGET
+#define WM_BPTT_TARGET 256
+#endif
+using BpttGemm = std::conditional_t<WM_BPTT_TILE64 != 0, GradGemmS, GradGemm>;
+int bptt_split(int B, int H) { return split_of<BpttGemm>(B, H, 4 * H, WM_BPTT_TARGET); }
+
 // out (ldo) = A . B^T in S K-slices; S > 1 writes slice y to out + y oslice
+template <class C = GradGemm>
 hipError_t gemm_nt_slices(const char* name, const float* A, long lda, int M, const float* Bm, long ldb, int N,
                           int Kpad, int S, float* out, long ldo, long oslice, hipStream_t s) {
-  using C = GradGemm;
   const int Ks = Kpad / S;
   const TileMap map = tile_map((N + C::BN - 1) / C::BN, (M + C::BM - 1) / C::BM, (size_t)N * Ks * 4);
-  return launch(name, k_gemm_nt, dim3(grid_of(map), (unsigned)S), dim3(C::NT), 0, s, A, lda, M, Bm, ldb, N, Ks,
-                out, ldo, oslice, map);
+  return launch(name, k_gemm_nt<C>, dim3(grid_of(map), (unsigned)S), dim3(C::NT), 0, s, A, lda, M, Bm, ldb, N,
+                Ks, out, ldo, oslice, map);
 }
 
 // out[m][n] = sum_s part[s][m][n] in slice order
@@ -2634,10 +2682,10 @@ hipError_t colsum(const float* src, long ld, long R, int Cc, float* part, float*
 template <int KC>
 hipError_t launch_heads_k(float* M, long ldm, const float* bm, const float* z, const float* rewards,
                           const uint8_t* dones, const int32_t* lengths, const float* nsum, int B, int T, int Z,
-                          int Nm, int NmP, hipStream_t s) {
+                          int Nm, int NmP, float* lrow, hipStream_t s) {
   const long n = (long)T * B * (Z + 1);
   return launch("grad_heads", k_grad_heads<KC>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, M, ldm,
-                bm, z, rewards, dones, lengths, nsum, B, T, Z, Nm, NmP);
+                bm, z, rewards, dones, lengths, nsum, B, T, Z, Nm, NmP, lrow);
 }
 
 }  // namespace
@@ -2669,12 +2717,12 @@ size_t grad_workspace(const Layout& L, int B, int T, char* ws, GradWs* G) {
     const int S = split_of(M, N, Kpad);
     return S > 1 ? (size_t)S * M * N : (size_t)0;
   };
-  const size_t nsplit = std::max({(size_t)split_of(B, H, H4) * B * H, split_need((int)TB, H4, L.ldk),
+  const size_t nsplit = std::max({(size_t)bptt_split(B, H) * B * H, split_need((int)TB, H4, L.ldk),
                                   split_need((int)TB, L.Nm, L.ldh), split_need((int)TB, H, NmP),
                                   split_need(L.ldk, H4, (int)TBp), split_need(NmP, H, (int)TBp)});
   const size_t osplit = take(nsplit * 4);
   const size_t on = take(16);
-  const size_t ofwd = take((size_t)TB * 3 * 4 + 16);  // loglik, reward_se, done_bce; means
+  const size_t ofwd = take((size_t)TB * (L.Z + 1) * 4);  // loss terms [TB, Z+1]
   if (ws && G) {
     auto f = [&](size_t at) { return reinterpret_cast<float*>(ws + at); };
     G->G = f(oG); G->Cs = f(oC); G->M = f(oM); G->dG = f(odG); G->dhh = f(odhh); G->dh = f(odh);
@@ -2700,13 +2748,8 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   const float* Hn = X + (long)B * L.ldx + Z;  // h_1 .. h_T: rows of X_1 .. X_T from column Z
   hipError_t e;
 #define WM_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
-  // forward pass: X (z_t | h_t) and the loss
-  N.loglik = G.fwd;
-  N.reward_se = G.fwd + TB;
-  N.done_bce = G.fwd + 2 * TB;
-  N.means = G.fwd + 3 * TB;
-  WM_TRY(launch_nll(P, N, s));
-  if (out.loss) WM_TRY(launch("grad_loss", k_grad_loss, dim3(1), dim3(64), 0, s, N.means, out.loss));
+  // forward recurrence: X (z_t | h_t) for every step
+  WM_TRY(nll_impl<float>(P, N, s, false));
   WM_TRY(launch("grad_len", k_len_sum, dim3(1), dim3(256), 0, s, N.lengths, B, T, G.nsum));
   // pre-activations of every step, then the scan (activations, c_t)
   WM_TRY(gemm_nt(X, L.ldx, (int)TB, Wg, L.ldk, H4, L.ldk, G.G, H4, G.split, s));
@@ -2718,11 +2761,17 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
 #define WM_HK(k)                                                                                       \
   case k:                                                                                              \
     WM_TRY(launch_heads_k<k>(G.M, NmP, bm, N.z, N.rewards, N.dones, N.lengths, G.nsum, B, T, Z, L.Nm, \
-                             NmP, s));                                                                 \
+                             NmP, G.fwd, s));                                                          \
     break;
     WM_HK(1) WM_HK(2) WM_HK(3) WM_HK(4) WM_HK(5) WM_HK(6) WM_HK(7) WM_HK(8)
 #undef WM_HK
     default: return hipErrorInvalidValue;
+  }
+  if (out.loss) {  // the loss: a fixed-order sum of its (row, dim) terms
+    WM_TRY(launch("grad_loss", k_flat_sum, dim3(kFlatBlocks), dim3(256), 0, s, (const float*)G.fwd,
+                  TB * (Z + 1), G.part));
+    WM_TRY(launch("grad_loss", k_flat_sum, dim3(1), dim3(256), 0, s, (const float*)G.part, (long)kFlatBlocks,
+                  out.loss));
   }
   // d loss / d h_{t+1} through the heads: dM [TB, NmP] . W_m (W_m^T [H, NmP], zero rows padded)
   WM_TRY(transpose(Wm, L.ldh, L.Nm, H, G.WmT, NmP, NmP, s));
@@ -2730,12 +2779,12 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   // back through time
   WM_TRY(transpose(Wg + Z, L.ldk, H4, H, G.WhT, H4, H4, s));  // W_h^T [H, 4H]
   const unsigned eg = (unsigned)(((long)B * H + 255) / 256);
-  const int Sb = split_of(B, H, H4);  // K slices of dG_t . W_h, summed by the next step's kernel
+  const int Sb = bptt_split(B, H);  // K slices of dG_t . W_h, summed by the next step's kernel
   for (int t = T - 1; t >= 0; --t) {
     WM_TRY(launch("grad_lstm", k_grad_lstm_back, dim3(eg), dim3(256), 0, s, G.G, G.Cs, G.dhh, G.split, Sb, G.dc,
                   G.dG, B, H, t, t == T - 1 ? 1 : 0));
     if (t > 0)
-      WM_TRY(gemm_nt_slices("grad_gemm_bptt", G.dG + (long)t * B * H4, H4, B, G.WhT, H4, H, H4, Sb, G.split, H,
+      WM_TRY(gemm_nt_slices<BpttGemm>("grad_gemm_bptt", G.dG + (long)t * B * H4, H4, B, G.WhT, H4, H, H4, Sb, G.split, H,
                             (long)B * H, s));
   }
   // dW_g^T [ldk, 4H] = X^T . dG over all rows (operands X^T [ldk, TBp], dG^T [4H, TBp])
