@@ -109,6 +109,40 @@ def test_nll_argument_checks():
     assert st == wmlib.WM_ERR_WORKSPACE
 
 
+def _grad_call(dims=None, B=4, T=3, z=4096, out=4096, ws=4096, ws_bytes=0, loss=None):
+    lib = wmlib.load()
+    d = dims or wmlib.make_dims(8, 16, 4, 2)
+    p = ctypes.c_void_p(4096)
+    zp = None if z is None else ctypes.c_void_p(z)
+    o = None if out is None else ctypes.c_void_p(out)
+    w = None if ws is None else ctypes.c_void_p(ws)
+    return lib.wm_nll_grad(ctypes.byref(d), p, B, T, zp, p, p, p, None, loss, o, p, p, p, p, p, p, p, w,
+                           ws_bytes, None)
+
+
+def test_nll_grad_argument_checks():
+    assert _grad_call(z=None) == wmlib.WM_ERR_INVALID_ARG
+    assert _grad_call(out=None) == wmlib.WM_ERR_INVALID_ARG  # every gradient output is required
+    assert _grad_call(z=4100) == wmlib.WM_ERR_INVALID_ARG  # z misaligned
+    assert _grad_call(B=0) == wmlib.WM_ERR_INVALID_ARG
+    assert _grad_call(T=-1) == wmlib.WM_ERR_INVALID_ARG
+    assert _grad_call(dims=wmlib.make_dims(8, 16, 4, 2, "bf16")) == wmlib.WM_ERR_UNSUPPORTED
+    assert _grad_call(B=1 << 12, T=1 << 11) == wmlib.WM_ERR_UNSUPPORTED  # T B above 2^22
+    assert _grad_call() == wmlib.WM_ERR_WORKSPACE
+    assert _grad_call(T=0) == wmlib.WM_OK  # no-op
+
+
+def test_nll_grad_workspace_size():
+    d = wmlib.make_dims(64, 512, 64, 5, "fp32")
+    nll = wmlib.workspace_bytes(d, 512, 128, 1)
+    g = wmlib.workspace_bytes(d, 512, 128, 2)
+    # at least the NLL pass's workspace, the gate activations and their
+    # gradient [T B, 4H], the c trace [T+1, B, H] and the head outputs
+    assert g >= nll + 4 * (2 * 512 * 128 * 4 * 512 + 129 * 512 * 512 + 512 * 128 * (3 * 64 * 5 + 2))
+    assert wmlib.workspace_bytes(d, 512, 64, 2) < g
+    assert wmlib.workspace_bytes(wmlib.make_dims(64, 512, 64, 5, "bf16"), 512, 128, 2) > 0
+
+
 def test_missing_library_fails_loudly(tmp_path):
     saved = wmlib._lib
     try:
