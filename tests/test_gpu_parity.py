@@ -61,7 +61,11 @@ def run_rollout(w, inp, *, T=None, trace=True, seed=None, tau=None, done=None, t
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("dtype,B,Z,H,A", [("fp32", 37, 64, 512, 64), ("bf16", 100, 128, 1024, 256),
-                                           ("fp32", 19, 8, 48, 37)])
+                                           ("fp32", 19, 8, 48, 37),
+                                           # wide controllers (more than 318 logit rows): 8, 24
+                                           # and 33 output blocks per wave
+                                           ("fp32", 37, 64, 512, 500), ("fp32", 21, 16, 64, 1100),
+                                           ("bf16", 70, 64, 256, 2000)])
 def test_controller_step(dtype, B, Z, H, A):
     say("controller_step", dtype, B, Z, H, A)
     w = wl.Workload("c", "rollout", B=B, T=10, Z=Z, H=H, A=A, K=2, dtype=dtype, seed=21)
@@ -106,6 +110,25 @@ def test_rollout_fp32_workloads(name):
         "live transitions", live)
     if w.done:
         assert 0 < g["dones"].sum() < g["dones"].size  # the done head is exercised
+
+
+@pytest.mark.parametrize("dtype,B,A", [("fp32", 45, 700), ("bf16", 150, 1500)])
+def test_rollout_wide_controller(dtype, B, A):
+    """Rollouts whose controller has more than 318 logit rows (the wide
+    controller kernel), free-running against the oracle and re-anchored."""
+    w = wl.Workload("wide", "rollout", B=B, T=4, Z=32, H=256, A=A, K=3, dtype=dtype, seed=31)
+    say("rollout wide controller", dtype, B, A)
+    inp = wl.make_rollout_inputs(w)
+    g = run_rollout(w, inp, trace=True)
+    if dtype == "fp32":
+        ref = owm.rollout(inp["weights"], w.dims, inp["z0"], inp["mask"], T=w.T, seed=w.seed,
+                          tau=w.tau, done_flag=w.done, dtype=w.dtype)
+        diverged = parity.free_run(ref, g, w.dtype, w.T)
+        assert diverged <= max(1, 1e-3 * w.B * w.T * (w.Z + 2))
+    ties, live = parity.reanchored(w.dims, inp["weights"], inp["mask"], g, seed=w.seed,
+                                   tau=w.tau, done_flag=w.done, dtype=w.dtype)
+    say("wide: tie mismatches", ties.mismatches, "of", ties.draws, "live", live)
+    assert live > 0
 
 
 def test_nll_workload():
