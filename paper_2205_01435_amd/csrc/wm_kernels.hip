@@ -1045,7 +1045,7 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
   __shared__ float s_rho[BM][2];
   __shared__ float s_fin[BM][2];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r16 = lane & 15;
   const int m0 = blockIdx.x * BM;
   const int nbtot = p.Nc / 16;
@@ -1068,17 +1068,37 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
 #pragma unroll
     for (int ks = 0; ks < BKC; ks += Mfma<DT>::KSLICE) {
       if (kc + ks >= (int)p.ldk) break;  // last chunk may overhang the padded K
+      // the slice's weight fragments are loaded in groups of GW, one group
+      // ahead of its MFMAs, from rows clamped into the matrix (blocks past
+      // nbtot are loaded but not used). Unguarded loads let each MFMA wait
+      // for its own fragment only; under the guard it waited for all of them.
+      constexpr int GW = 8, NG = (NBW + GW - 1) / GW;
+      uint4 a[2][GW];
+      auto load_group = [&](int gi, uint4(&dst)[GW]) {
+#pragma unroll
+        for (int q = 0; q < GW; ++q) {
+          const int i = gi * GW + q;
+          if (i < NBW) {
+            const int nb = min(wave + 4 * i, nbtot - 1);
+            dst[q] = *reinterpret_cast<const uint4*>(W + (long)(nb * 16 + r16) * p.ldk + kc + ks + g * VEC);
+          }
+        }
+      };
+      load_group(0, a[0]);
       uint4 b[MBW];
 #pragma unroll
       for (int j = 0; j < MBW; ++j)
         b[j] = *reinterpret_cast<const uint4*>(xl + (j * 16 + r16) * LDL + ks + g * VEC);
 #pragma unroll
-      for (int i = 0; i < NBW; ++i) {
-        const int nb = wave + 4 * i;
-        if (nb < nbtot) {
-          const uint4 a = *reinterpret_cast<const uint4*>(W + (long)(nb * 16 + r16) * p.ldk + kc + ks + g * VEC);
+      for (int gi = 0; gi < NG; ++gi) {
+        if (gi + 1 < NG) load_group(gi + 1, a[(gi + 1) & 1]);
 #pragma unroll
-          for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], a, b[j]);
+        for (int q = 0; q < GW; ++q) {
+          const int i = gi * GW + q;
+          if (i < NBW && wave + 4 * i < nbtot) {
+#pragma unroll
+            for (int j = 0; j < MBW; ++j) Mfma<DT>::step(acc[i][j], a[gi & 1][q], b[j]);
+          }
         }
       }
     }
