@@ -387,10 +387,11 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
 // mdn(t): mixture head on h_{t+1} (X_out columns Z ..), z_{t+1}
 // ---------------------------------------------------------------------------
 // QC > 0: the number of 16-row output blocks per latent-dim group is the
-// compile-time QC (= p.Q). Then every guard on q is resolved at compile time;
-// under a runtime Q the guarded fragment loads keep the compiler from
-// counting the loads in flight, and it waits for nearly all of them before
-// each MFMA (medium rollout 23.5 against 21.9 us per step).
+// compile-time QC (= p.Q; the rollout kernels are instantiated for every Q).
+// Then every guard on q is resolved at compile time; under a runtime Q the
+// guarded fragment loads keep the compiler from counting the loads in
+// flight, and it waits for nearly all of them before each MFMA (medium
+// rollout 23.5 against 21.9 us per step).
 template <int QC>
 __device__ __forceinline__ void mdn_phase(const PArgs& p, char* lds, int t, float* Xout, int r0, int nrows) {
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
@@ -854,14 +855,23 @@ hipError_t launch_k(const PArgs& a, size_t lds, hipStream_t s) {
   return launch(NLL ? "nll_persist" : "persist", k_persist<RB, NBC, NLL, QC>, dim3(kGrid), dim3(256), lds, s, a);
 }
 
-// the mixture head with a compile-time block count for K = 5 (Q = 4), a
-// runtime one otherwise; the NLL recurrence has no mixture phase
+// the mixture head with its block count Q = ceil(3K / 4) (1 .. 6 for
+// K <= 8) at compile time; the NLL recurrence has no mixture phase
 template <int RB, int NBC, bool NLL>
 hipError_t launch_q(const PArgs& a, size_t lds, hipStream_t s) {
-  if constexpr (!NLL) {
-    if (a.Q == 4) return launch_k<RB, NBC, false, 4>(a, lds, s);
+  if constexpr (NLL) {
+    return launch_k<RB, NBC, true, 0>(a, lds, s);
+  } else {
+    switch (a.Q) {
+      case 1: return launch_k<RB, NBC, false, 1>(a, lds, s);
+      case 2: return launch_k<RB, NBC, false, 2>(a, lds, s);
+      case 3: return launch_k<RB, NBC, false, 3>(a, lds, s);
+      case 4: return launch_k<RB, NBC, false, 4>(a, lds, s);
+      case 5: return launch_k<RB, NBC, false, 5>(a, lds, s);
+      case 6: return launch_k<RB, NBC, false, 6>(a, lds, s);
+      default: return hipErrorNotSupported;
+    }
   }
-  return launch_k<RB, NBC, NLL, 0>(a, lds, s);
 }
 
 template <bool NLL>
