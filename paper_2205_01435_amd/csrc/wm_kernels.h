@@ -51,6 +51,11 @@ struct NllBufs {
   float* head;   // [T*B, 2]
   float* wgsum;  // [nwg, 4]
   unsigned* sync;  // kSyncWords barrier words (persistent kernel)
+  // optional traces of the persistent recurrence (training gradient): gate
+  // activations (i, f, tanh g, o) [T, B, 4H] in the packed gate order, and
+  // c_{t+1} at [t+1] of [T+1, B, H]
+  float* g_trace;
+  float* c_trace;
 };
 
 // Barrier words of the persistent kernels (zeroed by the init kernels).

@@ -2334,6 +2334,12 @@ __global__ void __launch_bounds__(256) k_transpose(const float* src, long lds_, 
   }
 }
 
+// x[0 .. n) = 0
+__global__ void __launch_bounds__(256) k_zero(float* x, long n) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) x[i] = 0.f;
+}
+
 // N = sum_b min(max(len_b, 0), T) (all B T without lengths)
 __global__ void k_len_sum(const int32_t* lengths, int B, int T, float* nout) {
   __shared__ long part[256];
@@ -2768,13 +2774,24 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   const float* Hn = X + (long)B * L.ldx + Z;  // h_1 .. h_T: rows of X_1 .. X_T from column Z
   hipError_t e;
 #define WM_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
-  // forward recurrence: X (z_t | h_t) for every step
+  // forward recurrence: X (z_t | h_t) for every step. Where the persistent
+  // kernel serves it, it also leaves the gate activations and c_{t+1} of
+  // every step; otherwise they are recomputed from X (pre-activations of
+  // every step in one GEMM, then a scan that applies the gates and records
+  // c_t).
+  const bool traced = persist_usable(L, B, true);
+  N.g_trace = traced ? G.G : nullptr;
+  N.c_trace = traced ? G.Cs : nullptr;
   WM_TRY(nll_impl<float>(P, N, s, false));
   WM_TRY(launch("grad_len", k_len_sum, dim3(1), dim3(256), 0, s, N.lengths, B, T, G.nsum));
-  // pre-activations of every step, then the scan (activations, c_t)
-  WM_TRY(gemm_nt(X, L.ldx, (int)TB, Wg, L.ldk, H4, L.ldk, G.G, H4, G.split, s));
-  WM_TRY(launch("grad_scan", k_grad_fwd_scan, dim3((unsigned)(((long)B * H + 255) / 256)), dim3(256), 0, s,
-                G.G, bg, WaT, N.actions, G.Cs, B, T, H, A));
+  if (traced) {
+    WM_TRY(launch("grad_zero", k_zero, dim3((unsigned)(((long)B * H + 255) / 256)), dim3(256), 0, s, G.Cs,
+                  (long)B * H));  // c_0
+  } else {
+    WM_TRY(gemm_nt(X, L.ldx, (int)TB, Wg, L.ldk, H4, L.ldk, G.G, H4, G.split, s));
+    WM_TRY(launch("grad_scan", k_grad_fwd_scan, dim3((unsigned)(((long)B * H + 255) / 256)), dim3(256), 0, s,
+                  G.G, bg, WaT, N.actions, G.Cs, B, T, H, A));
+  }
   // head outputs of every h_{t+1}, then d loss / d output in place
   WM_TRY(gemm_nt(Hn, L.ldx, (int)TB, Wm, L.ldh, L.Nm, L.ldh, G.M, NmP, G.split, s));
   switch (L.K) {

@@ -78,7 +78,8 @@ struct PArgs {
   int32_t* actions;     // [T, B]: rollout output, NLL input
   float* rewards;
   uint8_t* dones;
-  float *h_trace, *c_trace;  // [T+1, B, H] or null
+  float *h_trace, *c_trace;  // [T+1, B, H] or null (each on its own)
+  float* g_trace;            // NLL: gate activations [T, B, 4H] or null
   // LDS carve-up (bytes)
   int off_red, off_hb, off_wat, off_wcz, off_mdn, off_ctl, off_flags;
 };
@@ -343,9 +344,9 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   if (owner) {
     const rsrc_t rxo = make_rsrc(Xout + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
     const rsrc_t rw = make_rsrc(p.WaT, (uint32_t)(A * 4 * H * 4));
-    const bool tr = p.h_trace != nullptr;
+    const bool tr = p.h_trace != nullptr, tc = p.c_trace != nullptr;
     const rsrc_t rht = make_rsrc(tr ? p.h_trace + ((long)(t + 1) * B + r0) * H : nullptr, tr ? (uint32_t)(nrows * H * 4) : 0u);
-    const rsrc_t rct = make_rsrc(tr ? p.c_trace + ((long)(t + 1) * B + r0) * H : nullptr, tr ? (uint32_t)(nrows * H * 4) : 0u);
+    const rsrc_t rct = make_rsrc(tc ? p.c_trace + ((long)(t + 1) * B + r0) * H : nullptr, tc ? (uint32_t)(nrows * H * 4) : 0u);
     const int hcol = p.Z + unit;  // X column of this lane's h
     const float* wat = reinterpret_cast<const float*>(lds + p.off_wat);
 #pragma unroll
@@ -364,8 +365,18 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
       }
       const float pi = acc[rb][0] + st.bias.x + add.x, pf = acc[rb][1] + st.bias.y + add.y;
       const float pg = acc[rb][2] + st.bias.z + add.z, po = acc[rb][3] + st.bias.w + add.w;
-      float cn = fsigmoid(pf) * st.cst[rb] + fsigmoid(pi) * ftanh(pg);
-      float hn = fsigmoid(po) * ftanh(cn);
+      const float gi = fsigmoid(pi), gf = fsigmoid(pf), gg = ftanh(pg), go = fsigmoid(po);
+      float cn = gf * st.cst[rb] + gi * gg;
+      float hn = go * ftanh(cn);
+      if constexpr (NLL) {
+        // the gate activations of row ml, unit `unit`, for the training
+        // gradient (dropped without a trace)
+        const bool tg = p.g_trace != nullptr;
+        const rsrc_t rgt = make_rsrc(tg ? p.g_trace + ((long)t * B + r0) * 4 * H : nullptr,
+                                     tg ? (uint32_t)(nrows * 4 * H * 4) : 0u);
+        bstore16(rgt, ok ? (uint32_t)(ml * 4 * H + 4 * unit) * 4u : kOffNone,
+                 make_uint4(__float_as_uint(gi), __float_as_uint(gf), __float_as_uint(gg), __float_as_uint(go)));
+      }
       if (!live) {
         cn = st.cst[rb];
         hn = *reinterpret_cast<const float*>(lds + ((hcol >> 4) * RB + rb) * 1024 + 64 * r16 + 4 * (hcol & 15));
@@ -957,6 +968,8 @@ hipError_t launch_nll_persist(const Packed& P, const NllBufs& N, hipStream_t s) 
   a.c = N.c;
   a.sync = N.sync;
   a.actions = const_cast<int32_t*>(N.actions);
+  a.g_trace = N.g_trace;
+  a.c_trace = N.c_trace;
   return launch_plan<true>(a, pl, s);
 }
 
