@@ -2334,10 +2334,14 @@ __global__ void __launch_bounds__(256) k_transpose(const float* src, long lds_, 
   }
 }
 
-// x[0 .. n) = 0
+// x[0 .. n) = 0, and = 1
 __global__ void __launch_bounds__(256) k_zero(float* x, long n) {
   const long i = (long)blockIdx.x * 256 + threadIdx.x;
   if (i < n) x[i] = 0.f;
+}
+__global__ void __launch_bounds__(256) k_ones(float* x, long n) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) x[i] = 1.f;
 }
 
 // N = sum_b min(max(len_b, 0), T) (all B T without lengths)
@@ -2827,8 +2831,14 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   // dW_g^T [ldk, 4H] = X^T . dG over all rows (operands X^T [ldk, TBp], dG^T [4H, TBp])
   WM_TRY(transpose(G.dG, H4, (int)TB, H4, G.T1, TBp, (int)TBp, s));
   WM_TRY(transpose(X, L.ldx, (int)TB, L.ldk, G.T2, TBp, (int)TBp, s));
+  // the bias gradient sum_r dG[r] comes out of the same product when X has a
+  // zero padding column to spare: a row of ones there in X^T
+  const bool ones_row = Z + H < L.ldk;
+  if (ones_row)
+    WM_TRY(launch("grad_ones", k_ones, dim3((unsigned)((TB + 255) / 256)), dim3(256), 0, s,
+                  G.T2 + (long)(Z + H) * TBp, TB));
   WM_TRY(gemm_nt(G.T2, TBp, L.ldk, G.T1, TBp, H4, (int)TBp, G.dWgT, H4, G.split, s));
-  WM_TRY(colsum(G.dG, H4, TB, H4, G.part, G.dbg, s));
+  if (!ones_row) WM_TRY(colsum(G.dG, H4, TB, H4, G.part, G.dbg, s));
   const int nch = act_chunks(L);
   WM_TRY(launch("grad_actions", k_grad_actions,
                 dim3((unsigned)((H4 + 255) / 256), (unsigned)nch, (unsigned)((A + kActGroup - 1) / kActGroup)),
@@ -2841,7 +2851,8 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   WM_TRY(gemm_nt(G.T1, TBp, NmP, G.T2, TBp, H, (int)TBp, G.dWm, H, G.split, s));
   WM_TRY(colsum(G.M, NmP, TB, NmP, G.part, G.dbm, s));
   // canonical layout
-  const UnpackArgs u{Z, H, A, L.K, L.Q, L.Nm, L.ldk, G.dWgT, G.dWa, G.dbg, G.dWm, G.dbm,
+  const UnpackArgs u{Z, H, A, L.K, L.Q, L.Nm, L.ldk, G.dWgT, G.dWa, ones_row ? G.dWgT + (long)(Z + H) * H4 : G.dbg,
+                     G.dWm, G.dbm,
                      out.W_g, out.b_g, out.W_m, out.b_m, out.w_r, out.b_r, out.w_d, out.b_d};
   WM_TRY(launch("grad_unpack", k_grad_unpack, dim3(1024), dim3(256), 0, s, u));
 #undef WM_TRY

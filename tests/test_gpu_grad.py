@@ -87,6 +87,7 @@ def _check(w, d, tag):
     (14, 45, 6, 8, 32, 4, 8, None),          # eight Gaussians
     (15, 20, 1, 8, 16, 3, 2, None),          # a single step
     (20, 100, 6, 16, 256, 9, 5, "mixed"),    # the persistent forward's gate and cell traces
+    (21, 41, 5, 16, 48, 7, 2, None),         # Z + H = 64 fills the padded K: bias by column sums
 ])
 def test_grad_parity(seed, B, T, Z, H, A, K, lengths):
     ln = None
