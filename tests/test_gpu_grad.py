@@ -88,6 +88,8 @@ def _check(w, d, tag):
     (15, 20, 1, 8, 16, 3, 2, None),          # a single step
     (20, 100, 6, 16, 256, 9, 5, "mixed"),    # the persistent forward's gate and cell traces
     (21, 41, 5, 16, 48, 7, 2, None),         # Z + H = 64 fills the padded K: bias by column sums
+    (22, 77, 5, 16, 512, 9, 3, "mixed"),     # H = 512: the persistent reverse-time kernel, ragged rows
+    (23, 40, 1, 8, 512, 5, 2, None),         # ... with a single step
 ])
 def test_grad_parity(seed, B, T, Z, H, A, K, lengths):
     ln = None
