@@ -264,7 +264,13 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
     }
     const int sl = kq * nper + 9 * c + r / rbv, rb = r % rbv;
     const uint32_t voff = (uint32_t)(16 * rb + (lane >> 2)) * ldxb + (uint32_t)sl * 64u + (uint32_t)(lane & 3) * 16u;
-    cdma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
+    // The NLL recurrence keeps every X_t (no ring), so this CU has never
+    // read these lines before and its L1 cannot hold a stale copy: the
+    // plain policy suffices there (NLL recurrence 19.7 -> 19.3 us per step
+    // at B = 512). The rollout reuses a two-matrix ring and needs the
+    // device-coherent policy.
+    if constexpr (NLL) dma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
+    else cdma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
   };
   {
     const int n0 = wave_count(0);
