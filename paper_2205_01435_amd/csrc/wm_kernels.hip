@@ -1010,14 +1010,37 @@ __device__ __forceinline__ int two_level_pick(const CtrlArgs& p, const Rng& rng,
   if (x < 0) return -1;
   if (x == N) return -2;
   const uint8_t* lm = p.mask + (long)p.M * NX + ((long)m * N + x) * Lc;
+  // thread q takes the contiguous locations [l0, l1) (a multiple of four:
+  // one Philox block each); their mask bytes are all loaded before the
+  // first is used, instead of one dependent load per location
+  // (Lc <= 316: N + 1 + Lc logits at most 318 with N >= 1)
+  constexpr int MAXW = (((316 + TPR - 1) / TPR + 3) & ~3) / 4;
+  const int cpt = ((Lc + TPR - 1) / TPR + 3) & ~3;
+  const int l0 = q * cpt, l1 = min(l0 + cpt, Lc);
+  uint32_t mw[MAXW];
+#pragma unroll
+  for (int k = 0; k < MAXW; ++k) {
+    uint32_t wv = 0;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = l0 + 4 * k + v;
+      if (on && i < l1 && lm[i]) wv |= 1u << (8 * v);
+    }
+    mw[k] = wv;
+  }
   best = -INFINITY;
   int l = -1;
-  if (on) {
-    for (int i = q; i < Lc; i += TPR) {
-      if (!lm[i]) continue;
-      const uint4 w = rng.block((uint32_t)i >> 2, p.step, traj, STREAM_LOCATION);
-      const float sc = lg[NX + i] + p.bc[NX + i] + gumbel(word_to_uniform(word_of(w, i & 3)));
-      if (sc > best) { best = sc; l = i; }
+#pragma unroll
+  for (int k = 0; k < MAXW; ++k) {
+    if (mw[k] == 0) continue;
+    const int b = l0 + 4 * k;
+    const uint4 w = rng.block((uint32_t)b >> 2, p.step, traj, STREAM_LOCATION);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      if ((mw[k] >> (8 * v)) & 1u) {
+        const float sc = lg[NX + b + v] + p.bc[NX + b + v] + gumbel(word_to_uniform(word_of(w, v)));
+        if (sc > best) { best = sc; l = b + v; }
+      }
     }
   }
   reduce(best, l);
