@@ -1131,6 +1131,22 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
   const Rng rng{p.k0, p.k1};
   const int A = p.A;
   const bool want_action = p.mode != 2;
+  // the mask bytes of this lane's actions (n .. n+3 of each block, each
+  // row), all loaded before the first is used
+  uint32_t mk[NBW][MBW];
+#pragma unroll
+  for (int j = 0; j < MBW; ++j) {
+    const int m = m0 + j * 16 + r16;
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) {
+      const int n = (wave + 4 * i) * 16 + 4 * g;
+      uint32_t wv = 0;
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (m < p.M && wave + 4 * i < nbtot && n + v < A && p.mask[(long)m * A + n + v]) wv |= 1u << (8 * v);
+      mk[i][j] = wv;
+    }
+  }
 #pragma unroll
   for (int j = 0; j < MBW; ++j) {
     const int ml = j * 16 + r16;
@@ -1155,7 +1171,7 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
           const uint4 w = rng.block((uint32_t)(n >> 2), p.step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            if (n + v < A && p.mask[(long)m * A + n + v]) {
+            if ((mk[i][j] >> (8 * v)) & 1u) {
               mx = fmaxf(mx, lg[v]);
               const float s = lg[v] + gumbel(word_to_uniform(word_of(w, v)));
               if (s > best) { best = s; bidx = n + v; }
@@ -1213,7 +1229,7 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
             const int n = nb * 16 + 4 * g;
 #pragma unroll
             for (int v = 0; v < 4; ++v)
-              if (n + v < A && p.mask[(long)m * A + n + v]) se += expf(acc[i][j][v] + p.bc[n + v] - mx);
+              if ((mk[i][j] >> (8 * v)) & 1u) se += expf(acc[i][j][v] + p.bc[n + v] - mx);
           }
         }
         se += __shfl_xor(se, 16);
@@ -1237,7 +1253,7 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             if (n + v < A) {
-              const bool ok = p.mask[(long)m * A + n + v] != 0;
+              const bool ok = (mk[i][j] >> (8 * v)) & 1u;
               p.probs[(long)m * A + n + v] = ok ? expf(acc[i][j][v] + p.bc[n + v] - mx) * inv : 0.f;
             }
           }
