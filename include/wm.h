@@ -19,8 +19,8 @@
  *     stream and the call returns; the status covers argument checks and
  *     launch errors only.
  *   - The caller owns every buffer.  The library never allocates device
- *     memory, keeps no pointer after the call returns and never
- *     synchronises the stream.
+ *     memory and keeps no pointer after the call returns.  It synchronises
+ *     the stream only in wm_workspace_status and under WM_FLAG_CHECK.
  *   - Matrices are row-major.  Time-major arrays are [T, B, ...].
  *   - Dimensions: B trajectories / sequences, T steps, Z latent size (a
  *     multiple of 8), H hidden size (a multiple of 16), A actions (1..2048),
@@ -63,16 +63,35 @@ typedef enum {
 } wm_dtype;
 
 enum {
-  WM_FLAG_DONE = 1u, /* sample the done head; else dones are 0 while live */
+  WM_FLAG_DONE = 1u,  /* sample the done head; else dones are 0 while live */
   WM_FLAG_TRACE = 2u, /* write h_trace / c_trace                           */
-  WM_FLAG_SIGMA_TAU = 4u, /* also scale the mixture's standard deviation by
-                            sqrt(tau) (the temperature of Ha and
-                            Schmidhuber's World Models, on which section 3.3
-                            builds); without it tau acts on the pi-logits
-                            only, as the paper specifies                    */
-  WM_FLAG_STEP_MASK = 8u /* valid_mask is [T, B, A], one mask per step (the
+  WM_FLAG_CHECK = 4u, /* debug mode: check the device data's preconditions
+                         (wm_rollout: every mask byte is 0 or 1; wm_nll,
+                         wm_nll_grad: every action of a step inside its
+                         sequence is in [0, A) or one of the codes -1, -2 a
+                         rollout emits, every done byte is 0 or 1) with
+                         device kernels that count violations in the
+                         workspace's status words.  The call then waits for
+                         its stream: a violation returns WM_ERR_INVALID_ARG
+                         before any output is computed, and a device-side
+                         failure of the computation (a barrier wait that
+                         timed out) returns WM_ERR_HIP.                     */
+  WM_FLAG_STEP_MASK = 8u, /* valid_mask is [T, B, A], one mask per step (the
                             valid actions depend on the state, section
                             3.1.3); else [B, A] for every step              */
+  WM_FLAG_SIGMA_TAU = 16u, /* also scale the mixture's standard deviation by
+                             sqrt(tau) (the temperature of Ha and
+                             Schmidhuber's World Models, on which section
+                             3.3 builds); without it tau acts on the
+                             pi-logits only, as the paper specifies         */
+  WM_FLAG_TEST_ABORT = 0x80000000u /* test support, never needed otherwise:
+                            the call starts with the workspace's device
+                            error word already set, as though a barrier wait
+                            of the persistent kernels had timed out.  Those
+                            kernels then leave at their first wait and exit
+                            normally, and the status (wm_workspace_status,
+                            or the return value under WM_FLAG_CHECK)
+                            reports the failure whichever path ran.         */
 };
 
 typedef struct {
@@ -108,20 +127,22 @@ typedef struct {
 
 /* Size in bytes of the packed (kernel-layout) weights for `dims`; 0 if the
  * dims are invalid or unsupported. */
-size_t wm_packed_bytes(const wm_dims *dims);
+size_t wm_packed_weights_bytes(const wm_dims *dims);
 
 /* Convert canonical weights into the kernels' layout (gate-interleaved
  * rows, one-hot block transposed for column gathers, mixture rows grouped
  * per latent dimension, controller extended with the reward and done rows),
  * rounding to bf16 (nearest, ties to even) when dims->dtype is WM_BF16.
- * `packed` is a device buffer of at least wm_packed_bytes(dims) bytes.
+ * `packed` is a device buffer of at least wm_packed_weights_bytes(dims)
+ * bytes (256-byte aligned).
  * Enqueued on `stream`; the canonical arrays may be freed once it ran. */
 wm_status wm_pack_weights(const wm_dims *dims, const wm_weights *canon, void *packed,
                           size_t packed_bytes, wm_stream_t stream);
 
-/* Workspace bytes needed by wm_rollout (which = 0), wm_nll (which = 1) or
- * wm_nll_grad (which = 2) for B rows and T steps; wm_controller_step needs
- * none.  0 on bad args. */
+/* Workspace bytes needed by wm_rollout (which = 0), wm_nll (which = 1),
+ * wm_controller_step (which = 2: it takes no workspace, so 0) or wm_nll_grad
+ * (which = 3) for B rows and T steps.  0 on bad args.  Every workspace
+ * starts with the status words that wm_workspace_status reads. */
 size_t wm_workspace_bytes(const wm_dims *dims, int32_t B, int32_t T, int32_t which);
 
 /*
@@ -208,6 +229,7 @@ wm_status wm_rollout(const wm_dims *dims, const void *packed, int32_t B, int32_t
  *   z [T+1, B, Z] float32; actions [T, B] int32 (outside [0, A) = no action,
  *   a zero one-hot); rewards [T, B] float32; dones [T, B] uint8;
  *   lengths [B] int32 nullable (= T): steps t >= lengths[b] output 0.
+ *   flags                0, or WM_FLAG_CHECK and / or WM_FLAG_TEST_ABORT.
  *   loglik, reward_se, done_bce [T, B] float32.
  *   means [3] float32 nullable: (-sum loglik / (N Z), sum se / N,
  *   sum bce / N) with N = sum of the clamped lengths (all 0 if N = 0).
@@ -215,7 +237,7 @@ wm_status wm_rollout(const wm_dims *dims, const void *packed, int32_t B, int32_t
  */
 wm_status wm_nll(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
                  const float *z, const int32_t *actions, const float *rewards,
-                 const uint8_t *dones, const int32_t *lengths, float *loglik,
+                 const uint8_t *dones, const int32_t *lengths, uint32_t flags, float *loglik,
                  float *reward_se, float *done_bce, float *means, void *workspace,
                  size_t workspace_bytes, wm_stream_t stream);
 
@@ -234,12 +256,12 @@ wm_status wm_nll(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
  *   grad_w_d [H]; grad_b_d [1].
  * N = 0 (all lengths 0) gives loss 0 and zero gradients.  T = 0 writes
  * nothing.  T B at most 2^22.  Every reduction runs in a fixed order: the
- * result does not depend on scheduling.
- *   workspace: wm_workspace_bytes(dims, B, T, 2) bytes, 256-byte aligned.
+ * result does not depend on scheduling.  flags: as for wm_nll.
+ *   workspace: wm_workspace_bytes(dims, B, T, 3) bytes, 256-byte aligned.
  */
 wm_status wm_nll_grad(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
                       const float *z, const int32_t *actions, const float *rewards,
-                      const uint8_t *dones, const int32_t *lengths, float *loss,
+                      const uint8_t *dones, const int32_t *lengths, uint32_t flags, float *loss,
                       float *grad_W_g, float *grad_b_g, float *grad_W_m, float *grad_b_m,
                       float *grad_w_r, float *grad_b_r, float *grad_w_d, float *grad_b_d,
                       void *workspace, size_t workspace_bytes, wm_stream_t stream);
@@ -300,6 +322,19 @@ float wm_poly_lr(int32_t epoch, float lr0, float lr_end, int32_t epochs);
 wm_status wm_profile_enable(const char *prefix);
 wm_status wm_profile_read(const char *prefix, double *total_ms, int64_t *launches);
 wm_status wm_profile_reset(void);
+
+/*
+ * Device-side status of the last call that used `workspace` (a workspace of
+ * wm_rollout, wm_nll or wm_nll_grad), after waiting for `stream`.  The
+ * persistent kernels wait for each other at barriers with a bounded spin; a
+ * wait that times out (for example when other work on the device keeps some
+ * of their work-groups from running) sets an error word in the workspace,
+ * and every work-group then stops at its next wait, so the outputs of that
+ * call are incomplete.  Returns WM_ERR_HIP if that word is set,
+ * WM_ERR_INVALID_ARG if the call's WM_FLAG_CHECK pass counted violations,
+ * WM_OK otherwise.  Host-side synchronisation; allocates nothing.
+ */
+wm_status wm_workspace_status(const void *workspace, wm_stream_t stream);
 
 /* Text of the last non-OK status on the calling thread ("" if none). */
 const char *wm_last_error(void);

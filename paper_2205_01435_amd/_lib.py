@@ -20,12 +20,15 @@ LIB_PATH = os.path.join(_PKG, "libwm.so")
 
 WM_OK, WM_ERR_INVALID_ARG, WM_ERR_UNSUPPORTED, WM_ERR_WORKSPACE, WM_ERR_HIP = 0, -1, -2, -3, -4
 WM_FP32, WM_BF16 = 0, 1
-WM_FLAG_DONE, WM_FLAG_TRACE, WM_FLAG_SIGMA_TAU, WM_FLAG_STEP_MASK = 1, 2, 4, 8
+WM_FLAG_DONE, WM_FLAG_TRACE, WM_FLAG_CHECK, WM_FLAG_STEP_MASK, WM_FLAG_SIGMA_TAU = 1, 2, 4, 8, 16
+WM_FLAG_TEST_ABORT = 0x80000000
+WS_ROLLOUT, WS_NLL, WS_CONTROLLER, WS_NLL_GRAD = 0, 1, 2, 3
 _DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
 
 # Every symbol the C header declares.
-EXPORTS = ("wm_packed_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
-           "wm_rollout", "wm_nll", "wm_nll_grad", "wm_returns", "wm_adam_step", "wm_poly_lr", "wm_profile_enable", "wm_profile_read", "wm_profile_reset",
+EXPORTS = ("wm_packed_weights_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
+           "wm_rollout", "wm_nll", "wm_nll_grad", "wm_returns", "wm_adam_step", "wm_poly_lr",
+           "wm_profile_enable", "wm_profile_read", "wm_profile_reset", "wm_workspace_status",
            "wm_last_error", "wm_version")
 
 
@@ -61,8 +64,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     P, I32, U32, U64, F32, SZ = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32,
                                  ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t)
     pd = ctypes.POINTER(CDims)
-    lib.wm_packed_bytes.argtypes = [pd]
-    lib.wm_packed_bytes.restype = SZ
+    lib.wm_packed_weights_bytes.argtypes = [pd]
+    lib.wm_packed_weights_bytes.restype = SZ
     lib.wm_pack_weights.argtypes = [pd, ctypes.POINTER(CWeights), P, SZ, P]
     lib.wm_pack_weights.restype = I32
     lib.wm_workspace_bytes.argtypes = [pd, I32, I32, I32]
@@ -72,9 +75,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_rollout.argtypes = [pd, P, I32, I32, U32, U32, P, P, P, P, P, U64, F32, U32,
                                P, P, P, P, P, P, P, P, P, SZ, P]
     lib.wm_rollout.restype = I32
-    lib.wm_nll.argtypes = [pd, P, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.wm_nll.argtypes = [pd, P, I32, I32, P, P, P, P, P, U32, P, P, P, P, P, SZ, P]
     lib.wm_nll.restype = I32
-    lib.wm_nll_grad.argtypes = [pd, P, I32, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.wm_nll_grad.argtypes = [pd, P, I32, I32, P, P, P, P, P, U32, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.wm_nll_grad.restype = I32
     lib.wm_returns.argtypes = [I32, I32, P, P, P, F32, F32, P, P, P]
     lib.wm_returns.restype = I32
@@ -89,6 +92,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_profile_read.restype = I32
     lib.wm_profile_reset.argtypes = []
     lib.wm_profile_reset.restype = I32
+    lib.wm_workspace_status.argtypes = [P, P]
+    lib.wm_workspace_status.restype = I32
     lib.wm_last_error.argtypes = []
     lib.wm_last_error.restype = ctypes.c_char_p
     lib.wm_version.argtypes = []
@@ -114,6 +119,35 @@ def _dev_f32(x, device):
     return torch.as_tensor(x, dtype=torch.float32).to(device).contiguous()
 
 
+def _need(name, t, dtype, shape, device=None, optional=False):
+    """Checks a tensor argument before its pointer crosses the C ABI."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the model on {device}")
+
+
+def _mask_dtype(t):
+    return t.dtype if t is not None and t.dtype in (torch.uint8, torch.bool) else torch.uint8
+
+
+def status(bufs) -> None:
+    """Wait for the current stream and raise WmError if the last call that
+    used ``bufs.workspace`` failed on the device (a timed-out barrier wait of
+    the persistent kernels, or WM_FLAG_CHECK violations)."""
+    _check(load().wm_workspace_status(_ptr(bufs.workspace), _stream()))
+
+
 @dataclass
 class Model:
     """Packed weights on a device plus their dims."""
@@ -133,7 +167,7 @@ def make_dims(Z, H, A, K, dtype="fp32", N=0, L=0) -> CDims:
 
 
 def packed_bytes(dims: CDims) -> int:
-    return load().wm_packed_bytes(ctypes.byref(dims))
+    return load().wm_packed_weights_bytes(ctypes.byref(dims))
 
 
 def workspace_bytes(dims: CDims, B: int, T: int, which: int) -> int:
@@ -146,7 +180,7 @@ def pack(weights: dict, Z: int, H: int, A: int, K: int, dtype: str = "fp32",
     the two-level controller, W_c [N+1+L, Z+H])."""
     lib = load()
     dims = make_dims(Z, H, A, K, dtype, N, L)
-    n = lib.wm_packed_bytes(ctypes.byref(dims))
+    n = lib.wm_packed_weights_bytes(ctypes.byref(dims))
     if n == 0:
         raise WmError(WM_ERR_UNSUPPORTED, lib.wm_last_error().decode())
     canon = {k: _dev_f32(np_or_t, device).reshape(-1) for k, np_or_t in weights.items()}
@@ -178,6 +212,10 @@ def controller_step(m: Model, z, h, mask, seed: int, step: int, traj0: int = 0,
     lib = load()
     B = z.shape[0]
     dev = m.packed.device
+    _need("z", z, torch.float32, (B, m.Z), dev)
+    _need("h", h, torch.float32, (B, m.H), dev)
+    if m.dims.N == 0:  # (the two-level controller is refused by the library)
+        _need("mask", mask, _mask_dtype(mask), (B, m.A), dev)
     probs = torch.empty((B, m.A), dtype=torch.float32, device=dev) if want_probs else None
     action = torch.empty(B, dtype=torch.int32, device=dev)
     _check(lib.wm_controller_step(ctypes.byref(m.dims), _ptr(m.packed), B, traj0, _ptr(z),
@@ -191,7 +229,7 @@ class RolloutBuffers:
 
     def __init__(self, m: Model, B: int, T: int, trace: bool = False, final_state: bool = True):
         dev = m.packed.device
-        self.B, self.T = B, T
+        self.B, self.T, self.Z, self.H = B, T, m.Z, m.H
         self.z_out = torch.empty((T + 1, B, m.Z), dtype=torch.float32, device=dev)
         self.actions = torch.empty((T, B), dtype=torch.int32, device=dev)
         self.rewards = torch.empty((T, B), dtype=torch.float32, device=dev)
@@ -202,19 +240,26 @@ class RolloutBuffers:
                         if trace else None)
         self.c_trace = (torch.empty((T + 1, B, m.H), dtype=torch.float32, device=dev)
                         if trace else None)
-        nws = workspace_bytes(m.dims, B, T, 0)
+        nws = workspace_bytes(m.dims, B, T, WS_ROLLOUT)
         self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
         self.ws_bytes = nws
 
 
 def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bool = True,
             traj0: int = 0, step0: int = 0, h0=None, c0=None, done_io=None, trace: bool = False,
-            bufs: RolloutBuffers | None = None, sigma_tau: bool = False) -> RolloutBuffers:
+            bufs: RolloutBuffers | None = None, sigma_tau: bool = False, check: bool = False,
+            extra_flags: int = 0) -> RolloutBuffers:
     """Launch wm_rollout on the current stream; returns the filled buffers
     (``sigma_tau`` sets WM_FLAG_SIGMA_TAU; a [T, B, A] mask sets
-    WM_FLAG_STEP_MASK)."""
+    WM_FLAG_STEP_MASK; ``check`` sets WM_FLAG_CHECK, which waits for the
+    stream)."""
     lib = load()
     B = z0.shape[0]
+    dev = m.packed.device
+    _need("z0", z0, torch.float32, (B, m.Z), dev)
+    _need("h0", h0, torch.float32, (B, m.H), dev, optional=True)
+    _need("c0", c0, torch.float32, (B, m.H), dev, optional=True)
+    _need("done_io", done_io, _mask_dtype(done_io), (B,), dev, optional=True)
     if m.dims.N > 0:
         # two-level controller: (xfer mask [B, N+1], location mask [B, N, L])
         # as one buffer, xfer masks first
@@ -223,44 +268,69 @@ def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bo
         if tuple(xm.shape) != (B, N + 1) or tuple(lm.shape) != (B, N, L):
             raise ValueError(f"two-level masks {tuple(xm.shape)}, {tuple(lm.shape)}; expected "
                              f"{(B, N + 1)}, {(B, N, L)}")
+        _need("xfer mask", xm, _mask_dtype(xm), (B, N + 1), dev)
+        _need("location mask", lm, _mask_dtype(lm), (B, N, L), dev)
         mask = torch.cat([xm.reshape(-1), lm.reshape(-1)]).contiguous()
+        step_mask = False
     else:
-        want = (T, B, m.dims.A) if mask.dim() == 3 else (B, m.dims.A)
-        if tuple(mask.shape) != want:
-            raise ValueError(f"mask has shape {tuple(mask.shape)}, expected {want}")
+        step_mask = mask is not None and mask.dim() == 3
+        want = (T, B, m.dims.A) if step_mask else (B, m.dims.A)
+        _need("mask", mask, _mask_dtype(mask), want, dev)
     if bufs is None:
         bufs = RolloutBuffers(m, B, T, trace=trace)
+    if T > 0 and ((bufs.B, bufs.T) != (B, T) or bufs.Z != m.Z or bufs.H != m.H):
+        raise ValueError(f"buffers for B={bufs.B} T={bufs.T} Z={bufs.Z} H={bufs.H}; the call has "
+                         f"B={B} T={T} Z={m.Z} H={m.H}")
+    if trace and bufs.h_trace is None:
+        raise ValueError("trace=True needs buffers made with trace=True")
     flags = (WM_FLAG_DONE if done else 0) | (WM_FLAG_TRACE if trace else 0) | \
-        (WM_FLAG_SIGMA_TAU if sigma_tau else 0) | (WM_FLAG_STEP_MASK if mask.dim() == 3 else 0)
-    _check(lib.wm_rollout(
-        ctypes.byref(m.dims), _ptr(m.packed), B, T, traj0, step0, _ptr(z0), _ptr(h0), _ptr(c0),
-        _ptr(done_io), _ptr(mask), seed, tau, flags, _ptr(bufs.z_out), _ptr(bufs.actions),
-        _ptr(bufs.rewards), _ptr(bufs.dones), _ptr(bufs.h_T), _ptr(bufs.c_T),
-        _ptr(bufs.h_trace), _ptr(bufs.c_trace), _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
+        (WM_FLAG_SIGMA_TAU if sigma_tau else 0) | (WM_FLAG_STEP_MASK if step_mask else 0) | \
+        (WM_FLAG_CHECK if check else 0) | extra_flags
+    common = (ctypes.byref(m.dims), _ptr(m.packed), B, T, traj0, step0, _ptr(z0), _ptr(h0), _ptr(c0),
+              _ptr(done_io), _ptr(mask), seed, tau, flags, _ptr(bufs.z_out), _ptr(bufs.actions),
+              _ptr(bufs.rewards), _ptr(bufs.dones), _ptr(bufs.h_T), _ptr(bufs.c_T),
+              _ptr(bufs.h_trace if trace else None), _ptr(bufs.c_trace if trace else None))
+    _check(lib.wm_rollout(*common, _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
     return bufs
 
 
 class NllBuffers:
     def __init__(self, m: Model, B: int, T: int):
         dev = m.packed.device
+        self.B, self.T = B, T
         self.loglik = torch.empty((T, B), dtype=torch.float32, device=dev)
         self.reward_se = torch.empty((T, B), dtype=torch.float32, device=dev)
         self.done_bce = torch.empty((T, B), dtype=torch.float32, device=dev)
         self.means = torch.empty(3, dtype=torch.float32, device=dev)
-        nws = workspace_bytes(m.dims, B, T, 1)
+        nws = workspace_bytes(m.dims, B, T, WS_NLL)
         self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
         self.ws_bytes = nws
 
 
-def nll(m: Model, z, actions, rewards, dones, lengths=None,
-        bufs: NllBuffers | None = None) -> NllBuffers:
-    """Launch wm_nll on the current stream; returns the filled buffers."""
-    lib = load()
+def _nll_inputs(m: Model, z, actions, rewards, dones, lengths):
     T, B = actions.shape
+    dev = m.packed.device
+    _need("actions", actions, torch.int32, (T, B), dev)
+    _need("z", z, torch.float32, (T + 1, B, m.Z), dev)
+    _need("rewards", rewards, torch.float32, (T, B), dev)
+    _need("dones", dones, _mask_dtype(dones), (T, B), dev)
+    _need("lengths", lengths, torch.int32, (B,), dev, optional=True)
+    return T, B
+
+
+def nll(m: Model, z, actions, rewards, dones, lengths=None,
+        bufs: NllBuffers | None = None, check: bool = False, extra_flags: int = 0) -> NllBuffers:
+    """Launch wm_nll on the current stream; returns the filled buffers
+    (``check`` sets WM_FLAG_CHECK, which waits for the stream)."""
+    lib = load()
+    T, B = _nll_inputs(m, z, actions, rewards, dones, lengths)
     if bufs is None:
         bufs = NllBuffers(m, B, T)
+    if (bufs.B, bufs.T) != (B, T):
+        raise ValueError(f"buffers for B={bufs.B} T={bufs.T}; the call has B={B} T={T}")
+    flags = (WM_FLAG_CHECK if check else 0) | extra_flags
     _check(lib.wm_nll(ctypes.byref(m.dims), _ptr(m.packed), B, T, _ptr(z), _ptr(actions),
-                      _ptr(rewards), _ptr(dones), _ptr(lengths), _ptr(bufs.loglik),
+                      _ptr(rewards), _ptr(dones), _ptr(lengths), flags, _ptr(bufs.loglik),
                       _ptr(bufs.reward_se), _ptr(bufs.done_bce), _ptr(bufs.means),
                       _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
     return bufs
@@ -292,26 +362,30 @@ class GradBuffers:
 
     def __init__(self, m: Model, B: int, T: int):
         dev = m.packed.device
+        self.B, self.T = B, T
         self.loss = torch.empty(1, dtype=torch.float32, device=dev)
         n = sum(math.prod(f(m.Z, m.H, m.A, m.K)) for f in GRAD_SHAPES.values())
         self.flat = torch.empty(n, dtype=torch.float32, device=dev)
         self.grads = flat_views(self.flat, m.Z, m.H, m.A, m.K)
-        nws = workspace_bytes(m.dims, B, T, 2)
+        nws = workspace_bytes(m.dims, B, T, WS_NLL_GRAD)
         self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
         self.ws_bytes = nws
 
 
 def nll_grad(m: Model, z, actions, rewards, dones, lengths=None,
-             bufs: GradBuffers | None = None) -> GradBuffers:
+             bufs: GradBuffers | None = None, check: bool = False, extra_flags: int = 0) -> GradBuffers:
     """Launch wm_nll_grad on the current stream: the training loss (summed
     NLL means) and its gradient in the canonical weight layout."""
     lib = load()
-    T, B = actions.shape
+    T, B = _nll_inputs(m, z, actions, rewards, dones, lengths)
     if bufs is None:
         bufs = GradBuffers(m, B, T)
+    if (bufs.B, bufs.T) != (B, T):
+        raise ValueError(f"buffers for B={bufs.B} T={bufs.T}; the call has B={B} T={T}")
     g = bufs.grads
+    flags = (WM_FLAG_CHECK if check else 0) | extra_flags
     _check(lib.wm_nll_grad(ctypes.byref(m.dims), _ptr(m.packed), B, T, _ptr(z), _ptr(actions),
-                           _ptr(rewards), _ptr(dones), _ptr(lengths), _ptr(bufs.loss),
+                           _ptr(rewards), _ptr(dones), _ptr(lengths), flags, _ptr(bufs.loss),
                            _ptr(g["W_g"]), _ptr(g["b_g"]), _ptr(g["W_m"]), _ptr(g["b_m"]),
                            _ptr(g["w_r"]), _ptr(g["b_r"]), _ptr(g["w_d"]), _ptr(g["b_d"]),
                            _ptr(bufs.workspace), bufs.ws_bytes, _stream()))

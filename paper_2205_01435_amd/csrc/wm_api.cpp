@@ -70,14 +70,99 @@ wm_status check_packed(const wm::Layout& L, const void* packed) {
   return WM_OK;
 }
 
+// Reads the status words at the start of a rollout / NLL workspace after the
+// stream's work has finished.
+wm_status read_status(const void* workspace, hipStream_t s) {
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "waiting for the stream");
+  unsigned w[2] = {0u, 0u};
+  e = hipMemcpy(w, reinterpret_cast<const unsigned*>(workspace) + wm::kSyncErr, sizeof w,
+                hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "reading the workspace status");
+  if (w[0]) return fail(WM_ERR_HIP, "a barrier wait of the persistent kernel timed out: the outputs are incomplete");
+  if (w[1]) return fail(WM_ERR_INVALID_ARG, "WM_FLAG_CHECK: %u precondition violations in the device data", w[1]);
+  return WM_OK;
+}
+
+// WM_FLAG_CHECK: zero the status words, run the checks `run` enqueues, wait, read.
+template <typename F>
+wm_status run_checks(void* workspace, hipStream_t s, F run) {
+  unsigned* sync = reinterpret_cast<unsigned*>(workspace);
+  hipError_t e = wm::launch_check_zero(sync, s);
+  if (e == hipSuccess) e = run(sync);
+  if (e != hipSuccess) return hip_fail(e, "WM_FLAG_CHECK");
+  return read_status(workspace, s);
+}
+
 uint32_t key_lo(uint64_t s) { return (uint32_t)(s & 0xffffffffu); }
 uint32_t key_hi(uint64_t s) { return (uint32_t)(s >> 32); }
+
+wm_status rollout_call(const wm_dims* dims, const void* packed, int32_t B, int32_t T,
+                     uint32_t traj0, uint32_t step0, const float* z0, const float* h0,
+                     const float* c0, uint8_t* done_io, const uint8_t* valid_mask, uint64_t seed,
+                     float tau, uint32_t flags, float* z_out, int32_t* actions, float* rewards,
+                     uint8_t* dones, float* h_T, float* c_T, float* h_trace, float* c_trace,
+                     void* workspace, size_t workspace_bytes, wm_stream_t stream) {
+  wm::Layout L;
+  wm_status st = check_dims(dims, &L);
+  if (st != WM_OK) return st;
+  if ((st = check_packed(L, packed)) != WM_OK) return st;
+  if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
+  if (T < 0) return fail(WM_ERR_INVALID_ARG, "T=%d must not be negative", T);
+  if (!(tau > 0.0f) || !isfinite(tau)) return fail(WM_ERR_INVALID_ARG, "tau must be finite and > 0");
+  if (flags & ~(uint32_t)(WM_FLAG_DONE | WM_FLAG_TRACE | WM_FLAG_CHECK | WM_FLAG_SIGMA_TAU |
+                          WM_FLAG_STEP_MASK | WM_FLAG_TEST_ABORT))
+    return fail(WM_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (!z0 || !valid_mask || !z_out || !actions || !rewards || !dones)
+    return fail(WM_ERR_INVALID_ARG, "z0, valid_mask, z_out, actions, rewards, dones are required");
+  if (L.N > 0 && (flags & WM_FLAG_STEP_MASK))
+    return fail(WM_ERR_UNSUPPORTED, "per-step masks with the two-level controller");
+  if ((flags & WM_FLAG_TRACE) && (!h_trace || !c_trace))
+    return fail(WM_ERR_INVALID_ARG, "WM_FLAG_TRACE needs h_trace and c_trace");
+  if (!aligned16(z0) || !aligned16(z_out))
+    return fail(WM_ERR_INVALID_ARG, "z0 and z_out must be 16-byte aligned");
+  if ((int64_t)B * (T + 1) > (int64_t)1 << 30)
+    return fail(WM_ERR_UNSUPPORTED, "B*(T+1) too large");
+  if (T == 0) return ok();
+  const size_t need = wm::rollout_workspace(L, B, nullptr, nullptr);
+  if (!workspace || workspace_bytes < need)
+    return fail(WM_ERR_WORKSPACE, "rollout workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(WM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (flags & WM_FLAG_CHECK) {
+    // mask bytes: [B, A], [T, B, A] per step, or the two-level xfer and
+    // location masks [B, N+1] + [B, N, L]
+    const long nmask = L.N > 0 ? (long)B * (L.N + 1) + (long)B * L.N * L.Lc
+                               : (long)B * L.A * ((flags & WM_FLAG_STEP_MASK) ? T : 1);
+    if ((st = run_checks(workspace, s, [&](unsigned* sync) {
+           return wm::launch_check_bytes01(valid_mask, nmask, sync, s);
+         })) != WM_OK)
+      return st;
+  }
+  char* ws = reinterpret_cast<char*>(workspace);
+  wm::RolloutBufs R{};
+  R.B = B; R.T = T; R.traj0 = traj0; R.step0 = step0;
+  R.k0 = key_lo(seed); R.k1 = key_hi(seed);
+  R.tau = tau; R.flags = flags;
+  R.z0 = z0; R.h0 = h0; R.c0 = c0; R.done_io = done_io; R.mask = valid_mask;
+  R.z_out = z_out; R.actions = actions; R.rewards = rewards; R.dones = dones;
+  R.h_T = h_T; R.c_T = c_T; R.h_trace = h_trace; R.c_trace = c_trace;
+  wm::rollout_workspace(L, B, ws, &R);
+  R.preset_err = (flags & WM_FLAG_TEST_ABORT) ? 1u : 0u;
+  wm::Packed P{L, packed};
+  hipError_t e = wm::launch_rollout(P, R, s);
+  if (e != hipSuccess) return hip_fail(e, "wm_rollout");
+  if (flags & WM_FLAG_CHECK) return (st = read_status(workspace, s)) == WM_OK ? ok() : st;
+  return ok();
+}
 
 }  // namespace
 
 extern "C" {
 
-size_t wm_packed_bytes(const wm_dims* dims) {
+size_t wm_packed_weights_bytes(const wm_dims* dims) {
   wm::Layout L;
   if (check_dims(dims, &L) != WM_OK) return 0;
   return L.total;
@@ -88,7 +173,8 @@ size_t wm_workspace_bytes(const wm_dims* dims, int32_t B, int32_t T, int32_t whi
   if (check_dims(dims, &L) != WM_OK || B <= 0 || T < 0) return 0;
   if (which == 0) return wm::rollout_workspace(L, B, nullptr, nullptr);
   if (which == 1) return wm::nll_workspace(L, B, T, nullptr, nullptr);
-  if (which == 2)
+  if (which == 2) return 0;  // wm_controller_step takes no workspace
+  if (which == 3)
     return wm::wm_align256(wm::nll_workspace(L, B, T, nullptr, nullptr)) +
            wm::grad_workspace(L, B, T, nullptr, nullptr);
   return 0;
@@ -140,57 +226,24 @@ wm_status wm_rollout(const wm_dims* dims, const void* packed, int32_t B, int32_t
                      float tau, uint32_t flags, float* z_out, int32_t* actions, float* rewards,
                      uint8_t* dones, float* h_T, float* c_T, float* h_trace, float* c_trace,
                      void* workspace, size_t workspace_bytes, wm_stream_t stream) {
-  wm::Layout L;
-  wm_status st = check_dims(dims, &L);
-  if (st != WM_OK) return st;
-  if ((st = check_packed(L, packed)) != WM_OK) return st;
-  if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
-  if (T < 0) return fail(WM_ERR_INVALID_ARG, "T=%d must not be negative", T);
-  if (!(tau > 0.0f) || !isfinite(tau)) return fail(WM_ERR_INVALID_ARG, "tau must be finite and > 0");
-  if (flags & ~(uint32_t)(WM_FLAG_DONE | WM_FLAG_TRACE | WM_FLAG_SIGMA_TAU | WM_FLAG_STEP_MASK))
-    return fail(WM_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
-  if (!z0 || !valid_mask || !z_out || !actions || !rewards || !dones)
-    return fail(WM_ERR_INVALID_ARG, "z0, valid_mask, z_out, actions, rewards, dones are required");
-  if (L.N > 0 && (flags & WM_FLAG_STEP_MASK))
-    return fail(WM_ERR_UNSUPPORTED, "per-step masks with the two-level controller");
-  if ((flags & WM_FLAG_TRACE) && (!h_trace || !c_trace))
-    return fail(WM_ERR_INVALID_ARG, "WM_FLAG_TRACE needs h_trace and c_trace");
-  if (!aligned16(z0) || !aligned16(z_out))
-    return fail(WM_ERR_INVALID_ARG, "z0 and z_out must be 16-byte aligned");
-  if ((int64_t)B * (T + 1) > (int64_t)1 << 30)
-    return fail(WM_ERR_UNSUPPORTED, "B*(T+1) too large");
-  if (T == 0) return ok();
-  const size_t need = wm::rollout_workspace(L, B, nullptr, nullptr);
-  if (!workspace || workspace_bytes < need)
-    return fail(WM_ERR_WORKSPACE, "rollout workspace needs %zu bytes, got %zu", need, workspace_bytes);
-  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
-    return fail(WM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-
-  char* ws = reinterpret_cast<char*>(workspace);
-  wm::RolloutBufs R{};
-  R.B = B; R.T = T; R.traj0 = traj0; R.step0 = step0;
-  R.k0 = key_lo(seed); R.k1 = key_hi(seed);
-  R.tau = tau; R.flags = flags;
-  R.z0 = z0; R.h0 = h0; R.c0 = c0; R.done_io = done_io; R.mask = valid_mask;
-  R.z_out = z_out; R.actions = actions; R.rewards = rewards; R.dones = dones;
-  R.h_T = h_T; R.c_T = c_T; R.h_trace = h_trace; R.c_trace = c_trace;
-  wm::rollout_workspace(L, B, ws, &R);
-  wm::Packed P{L, packed};
-  hipError_t e = wm::launch_rollout(P, R, reinterpret_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "wm_rollout");
-  return ok();
+  return rollout_call(dims, packed, B, T, traj0, step0, z0, h0, c0, done_io, valid_mask, seed, tau,
+                      flags, z_out, actions, rewards, dones, h_T, c_T, h_trace, c_trace, workspace,
+                      workspace_bytes, stream);
 }
 
 wm_status wm_nll(const wm_dims* dims, const void* packed, int32_t B, int32_t T, const float* z,
                  const int32_t* actions, const float* rewards, const uint8_t* dones,
-                 const int32_t* lengths, float* loglik, float* reward_se, float* done_bce,
-                 float* means, void* workspace, size_t workspace_bytes, wm_stream_t stream) {
+                 const int32_t* lengths, uint32_t flags, float* loglik, float* reward_se,
+                 float* done_bce, float* means, void* workspace, size_t workspace_bytes,
+                 wm_stream_t stream) {
   wm::Layout L;
   wm_status st = check_dims(dims, &L);
   if (st != WM_OK) return st;
   if ((st = check_packed(L, packed)) != WM_OK) return st;
   if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
   if (T < 0) return fail(WM_ERR_INVALID_ARG, "T=%d must not be negative", T);
+  if (flags & ~(uint32_t)(WM_FLAG_CHECK | WM_FLAG_TEST_ABORT))
+    return fail(WM_ERR_INVALID_ARG, "wm_nll: flags 0x%x (only WM_FLAG_CHECK, WM_FLAG_TEST_ABORT)", flags);
   if (!z || !actions || !rewards || !dones || !loglik || !reward_se || !done_bce)
     return fail(WM_ERR_INVALID_ARG, "z, actions, rewards, dones and the three outputs are required");
   if (!aligned16(z)) return fail(WM_ERR_INVALID_ARG, "z must be 16-byte aligned");
@@ -203,21 +256,28 @@ wm_status wm_nll(const wm_dims* dims, const void* packed, int32_t B, int32_t T, 
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(WM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
 
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if ((flags & WM_FLAG_CHECK) && (st = run_checks(workspace, s, [&](unsigned* sync) {
+                                    return wm::launch_check_nll(T, B, L.A, actions, dones, lengths, sync, s);
+                                  })) != WM_OK)
+    return st;
   char* ws = reinterpret_cast<char*>(workspace);
   wm::NllBufs N{};
   N.B = B; N.T = T; N.z = z; N.actions = actions; N.rewards = rewards; N.dones = dones;
   N.lengths = lengths; N.loglik = loglik; N.reward_se = reward_se; N.done_bce = done_bce;
   N.means = means;
   wm::nll_workspace(L, B, T, ws, &N);
+  N.preset_err = (flags & WM_FLAG_TEST_ABORT) ? 1u : 0u;
   wm::Packed P{L, packed};
-  hipError_t e = wm::launch_nll(P, N, reinterpret_cast<hipStream_t>(stream));
+  hipError_t e = wm::launch_nll(P, N, s);
   if (e != hipSuccess) return hip_fail(e, "wm_nll");
+  if (flags & WM_FLAG_CHECK) return (st = read_status(workspace, s)) == WM_OK ? ok() : st;
   return ok();
 }
 
 wm_status wm_nll_grad(const wm_dims* dims, const void* packed, int32_t B, int32_t T, const float* z,
                       const int32_t* actions, const float* rewards, const uint8_t* dones,
-                      const int32_t* lengths, float* loss, float* grad_W_g, float* grad_b_g,
+                      const int32_t* lengths, uint32_t flags, float* loss, float* grad_W_g, float* grad_b_g,
                       float* grad_W_m, float* grad_b_m, float* grad_w_r, float* grad_b_r,
                       float* grad_w_d, float* grad_b_d, void* workspace, size_t workspace_bytes,
                       wm_stream_t stream) {
@@ -228,6 +288,8 @@ wm_status wm_nll_grad(const wm_dims* dims, const void* packed, int32_t B, int32_
   if (L.dt != 0) return fail(WM_ERR_UNSUPPORTED, "wm_nll_grad serves fp32 weights only");
   if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
   if (T < 0) return fail(WM_ERR_INVALID_ARG, "T=%d must not be negative", T);
+  if (flags & ~(uint32_t)(WM_FLAG_CHECK | WM_FLAG_TEST_ABORT))
+    return fail(WM_ERR_INVALID_ARG, "wm_nll_grad: flags 0x%x (only WM_FLAG_CHECK, WM_FLAG_TEST_ABORT)", flags);
   if (!z || !actions || !rewards || !dones)
     return fail(WM_ERR_INVALID_ARG, "z, actions, rewards and dones are required");
   if (!grad_W_g || !grad_b_g || !grad_W_m || !grad_b_m || !grad_w_r || !grad_b_r || !grad_w_d || !grad_b_d)
@@ -242,17 +304,24 @@ wm_status wm_nll_grad(const wm_dims* dims, const void* packed, int32_t B, int32_
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(WM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
 
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if ((flags & WM_FLAG_CHECK) && (st = run_checks(workspace, s, [&](unsigned* sync) {
+                                    return wm::launch_check_nll(T, B, L.A, actions, dones, lengths, sync, s);
+                                  })) != WM_OK)
+    return st;
   char* ws = reinterpret_cast<char*>(workspace);
   wm::NllBufs N{};
   N.B = B; N.T = T; N.z = z; N.actions = actions; N.rewards = rewards; N.dones = dones;
   N.lengths = lengths;
   wm::nll_workspace(L, B, T, ws, &N);
+  N.preset_err = (flags & WM_FLAG_TEST_ABORT) ? 1u : 0u;
   wm::GradWs G{};
   wm::grad_workspace(L, B, T, ws + nb, &G);
   const wm::GradOut out{loss, grad_W_g, grad_b_g, grad_W_m, grad_b_m, grad_w_r, grad_b_r, grad_w_d, grad_b_d};
   wm::Packed P{L, packed};
-  hipError_t e = wm::launch_nll_grad(P, N, G, out, reinterpret_cast<hipStream_t>(stream));
+  hipError_t e = wm::launch_nll_grad(P, N, G, out, s);
   if (e != hipSuccess) return hip_fail(e, "wm_nll_grad");
+  if (flags & WM_FLAG_CHECK) return (st = read_status(workspace, s)) == WM_OK ? ok() : st;
   return ok();
 }
 
@@ -303,6 +372,12 @@ float wm_poly_lr(int32_t epoch, float lr0, float lr_end, int32_t epochs) {
   const double e = epoch < 0 ? 0.0 : (epoch > epochs ? (double)epochs : (double)epoch);
   const double f = 1.0 - e / epochs;
   return (float)(((double)lr0 - lr_end) * f * f + lr_end);
+}
+
+wm_status wm_workspace_status(const void* workspace, wm_stream_t stream) {
+  if (!workspace) return fail(WM_ERR_INVALID_ARG, "workspace is NULL");
+  const wm_status st = read_status(workspace, reinterpret_cast<hipStream_t>(stream));
+  return st == WM_OK ? ok() : st;
 }
 
 const char* wm_last_error(void) { return g_err.c_str(); }

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/wm.h"
 #include "wm_layout.h"
 
 namespace wm {
@@ -33,7 +34,8 @@ struct RolloutBufs {
   float* c;            // [B, H]
   int32_t* done_state; // [B]
   float* P;            // [32, B, Nc] controller partial logits (persistent kernel) or null
-  unsigned* sync;      // kSyncWords barrier words (persistent kernel)
+  unsigned* sync;      // kSyncWords barrier and status words, at workspace offset 0
+  unsigned preset_err; // initial value of the error word (WM_FLAG_TEST_ABORT)
 };
 
 struct NllBufs {
@@ -50,7 +52,8 @@ struct NllBufs {
   float* part;   // [T*B, NTd]
   float* head;   // [T*B, 2]
   float* wgsum;  // [nwg, 4]
-  unsigned* sync;  // kSyncWords barrier words (persistent kernel)
+  unsigned* sync;  // kSyncWords barrier and status words, at workspace offset 0
+  unsigned preset_err;  // initial value of the error word (WM_FLAG_TEST_ABORT)
   // optional traces of the persistent recurrence (training gradient): gate
   // activations (i, f, tanh g, o) [T, B, 4H] in the packed gate order, and
   // c_{t+1} at [t+1] of [T+1, B, H]
@@ -58,8 +61,13 @@ struct NllBufs {
   float* c_trace;
 };
 
-// Barrier words of the persistent kernels (zeroed by the init kernels).
+// Barrier and status words (zeroed by the init kernels) at offset 0 of the
+// rollout and NLL workspaces: the persistent kernels' group counters at
+// 64 x and placement flags at 64 (8 + x); the error word (a barrier wait
+// timed out) and the WM_FLAG_CHECK violation count.
 constexpr int kSyncWords = 64 * 17;
+constexpr int kSyncErr = 64 * 16;
+constexpr int kSyncViol = 64 * 16 + 1;
 
 // Workspace sizes; with a non-null `ws` the workspace pointers of the
 // buffer struct are also set (ws must be 256-byte aligned).
@@ -76,6 +84,15 @@ hipError_t launch_controller_step(const Packed& P, int B, uint32_t traj0, const 
                                   uint32_t step, float* probs, int32_t* action, hipStream_t s);
 
 hipError_t launch_rollout(const Packed& P, const RolloutBufs& R, hipStream_t s);
+
+// WM_FLAG_CHECK passes: zero the two status words, then count violations
+// of the device-data preconditions into sync[kSyncViol].
+hipError_t launch_check_zero(unsigned* sync, hipStream_t s);
+// bytes of p[0 .. n) other than 0 and 1
+hipError_t launch_check_bytes01(const uint8_t* p, long n, unsigned* sync, hipStream_t s);
+// actions of steps t < lengths[b] outside [0, A) u {-1, -2}; dones other than 0, 1
+hipError_t launch_check_nll(int T, int B, int A, const int32_t* actions, const uint8_t* dones,
+                            const int32_t* lengths, unsigned* sync, hipStream_t s);
 
 hipError_t launch_nll(const Packed& P, const NllBufs& N, hipStream_t s);
 

@@ -1658,11 +1658,11 @@ __global__ void k_rollout_init(int B, int Z, int H, int ldx, const float* __rest
                                const uint8_t* __restrict__ done_io, float* __restrict__ z_out,
                                DT* __restrict__ X0, DT* __restrict__ X1, float* __restrict__ c,
                                int32_t* __restrict__ done_state, float* __restrict__ h_trace,
-                               float* __restrict__ c_trace, unsigned* __restrict__ sync) {
+                               float* __restrict__ c_trace, unsigned* __restrict__ sync,
+                               unsigned preset_err) {
   const long stride = (long)gridDim.x * blockDim.x;
   const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (sync)
-    for (long i = i0; i < kSyncWords; i += stride) sync[i] = 0u;
+  for (long i = i0; i < kSyncWords; i += stride) sync[i] = i == kSyncErr ? preset_err : 0u;
   for (long i = i0; i < (long)B * ldx; i += stride) {
     const long b = i / ldx;
     const int col = (int)(i % ldx);
@@ -1702,11 +1702,11 @@ __global__ void k_rollout_finish(int B, int Z, int H, int ldx, const DT* __restr
 // X_t[:, 0:Z] = q(z_t) for t = 0..T, padding columns zero, h_0 = c_0 = 0.
 template <typename DT>
 __global__ void k_nll_init(int T, int B, int Z, int H, int ldx, const float* __restrict__ z,
-                           DT* __restrict__ X, float* __restrict__ c, unsigned* __restrict__ sync) {
+                           DT* __restrict__ X, float* __restrict__ c, unsigned* __restrict__ sync,
+                           unsigned preset_err) {
   const long stride = (long)gridDim.x * blockDim.x;
   const long i0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (sync)
-    for (long i = i0; i < kSyncWords; i += stride) sync[i] = 0u;
+  for (long i = i0; i < kSyncWords; i += stride) sync[i] = i == kSyncErr ? preset_err : 0u;
   const int ncol = ldx - H;  // z columns, then padding columns
   for (long i = i0; i < (long)(T + 1) * B * ncol; i += stride) {
     const long r = i / ncol;
@@ -2040,6 +2040,43 @@ hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+// ---------------------------------------------------------------------------
+// WM_FLAG_CHECK: device-side precondition checks.  Each thread counts the
+// violations in its grid-stride share and adds a nonzero count to the
+// status word sync[kSyncViol]; k_check_zero first clears both status words
+// (the workspace's bytes are the caller's until the call's init kernel).
+// ---------------------------------------------------------------------------
+__global__ void k_check_zero(unsigned* __restrict__ sync) {
+  if (threadIdx.x == 0) {
+    sync[kSyncErr] = 0u;
+    sync[kSyncViol] = 0u;
+  }
+}
+
+// bytes other than 0 and 1 (the masks)
+__global__ void k_check_bytes01(const uint8_t* __restrict__ p, long n, unsigned* __restrict__ sync) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  unsigned bad = 0;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) bad += p[i] > 1u;
+  if (bad) atomicAdd(sync + kSyncViol, bad);
+}
+
+// steps inside their sequence (t < lengths[b]): an action outside
+// [0, A) u {-1, -2}, or a done byte other than 0 and 1
+__global__ void k_check_nll(int T, int B, int A, const int32_t* __restrict__ actions,
+                            const uint8_t* __restrict__ dones, const int32_t* __restrict__ lengths,
+                            unsigned* __restrict__ sync) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  unsigned bad = 0;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < (long)T * B; i += stride) {
+    const int t = (int)(i / B), b = (int)(i % B);
+    if (lengths && t >= lengths[b]) continue;
+    const int32_t a = actions[i];
+    bad += (a >= A || a < -2) + (dones[i] > 1u);
+  }
+  if (bad) atomicAdd(sync + kSyncViol, bad);
+}
+
 unsigned elem_grid(long n) {
   long g = (n + 255) / 256;
   if (g < 1) g = 1;
@@ -2054,10 +2091,11 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   const int B = R.B, T = R.T, Z = L.Z, H = L.H;
   DT* X = reinterpret_cast<DT*>(R.x);
   const long BX = (long)B * L.ldx, BH = (long)B * H, BZ = (long)B * Z;
-  const bool trace = (R.flags & 2u) != 0;
+  const bool trace = (R.flags & WM_FLAG_TRACE) != 0;
   hipError_t e = launch("init", k_rollout_init<DT>, dim3(elem_grid(BX)), dim3(256), 0, s, B, Z, H,
                         L.ldx, R.z0, R.h0, R.c0, R.done_io, R.z_out, X, X + BX, R.c, R.done_state,
-                        trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr, R.sync);
+                        trace ? R.h_trace : nullptr, trace ? R.c_trace : nullptr, R.sync,
+                        R.preset_err);
   if (e != hipSuccess) return e;
   if (T > 0) {
     // one persistent launch for every step when the batch and dims allow it
@@ -2077,7 +2115,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ca.mask = R.mask;
   ca.k0 = R.k0; ca.k1 = R.k1; ca.traj0 = R.traj0;
   ca.done_state = R.done_state;
-  ca.use_done = (R.flags & 1u) != 0;
+  ca.use_done = (R.flags & WM_FLAG_DONE) != 0;
   ca.N = L.N;
   ca.Lc = L.Lc;
 
@@ -2098,7 +2136,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ma.ldx = L.ldx;
   ma.H = H; ma.Z = Z; ma.K = L.K; ma.Nm = L.Nm; ma.M = B;
   ma.k0 = R.k0; ma.k1 = R.k1; ma.traj0 = R.traj0; ma.tau = R.tau;
-  ma.sig = (R.flags & 4u) ? sqrtf(R.tau) : 1.0f;
+  ma.sig = (R.flags & WM_FLAG_SIGMA_TAU) ? sqrtf(R.tau) : 1.0f;
   ma.nll_mode = 0;
   const int mdn_tiles = Z / 8;
 
@@ -2110,7 +2148,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
     ca.step = step;
     ca.mode = t < T ? 1 : 2;
     // step t's [B, A] slice of a per-step mask (the tail step draws no action)
-    ca.mask = (R.flags & 8u) ? R.mask + (long)(t < T ? t : T - 1) * B * L.A : R.mask;
+    ca.mask = (R.flags & WM_FLAG_STEP_MASK) ? R.mask + (long)(t < T ? t : T - 1) * B * L.A : R.mask;
     ca.act_t = t < T ? R.actions + (long)t * B : nullptr;
     ca.rew_t = t < T ? R.rewards + (long)t * B : nullptr;
     ca.done_t = t < T ? R.dones + (long)t * B : nullptr;
@@ -2150,7 +2188,7 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s, bool heads
   const long BX = (long)B * L.ldx, BZ = (long)B * Z, M = (long)T * B;
   DT* X = reinterpret_cast<DT*>(N.x);
   hipError_t e = launch("nll_init", k_nll_init<DT>, dim3(elem_grid((long)(T + 1) * B * (L.ldx - H))),
-                        dim3(256), 0, s, T, B, Z, H, L.ldx, N.z, X, N.c, N.sync);
+                        dim3(256), 0, s, T, B, Z, H, L.ldx, N.z, X, N.c, N.sync, N.preset_err);
   if (e != hipSuccess) return e;
 
   GatesArgs ga{};
@@ -2201,14 +2239,14 @@ hipError_t nll_impl(const Packed& P, const NllBufs& N, hipStream_t s, bool heads
 
 size_t rollout_workspace(const Layout& L, int B, char* ws, RolloutBufs* R) {
   size_t o = 0;
+  const size_t os = o;
+  o = wm_align256(o + (size_t)kSyncWords * 4);  // barrier and status words
   const size_t ox = o;
   o = wm_align256(o + (size_t)2 * B * L.ldx * L.esz);  // X_t, X_t+1
   const size_t oc = o;
   o = wm_align256(o + (size_t)B * L.H * 4);  // c
   const size_t od = o;
   o = wm_align256(o + (size_t)B * 4);  // done state
-  const size_t os = o;
-  o = wm_align256(o + (size_t)kSyncWords * 4);  // persistent-kernel barriers
   const size_t pb = persist_partial_bytes(L, B);
   const size_t op = o;
   o = wm_align256(o + pb);  // persistent-kernel controller partials
@@ -2225,6 +2263,8 @@ size_t rollout_workspace(const Layout& L, int B, char* ws, RolloutBufs* R) {
 size_t nll_workspace(const Layout& L, int B, int T, char* ws, NllBufs* N) {
   const size_t M = (size_t)T * B;
   size_t o = 0;
+  const size_t os = o;
+  o = wm_align256(o + (size_t)kSyncWords * 4);  // barrier and status words
   const size_t ox = o;
   o = wm_align256(o + (size_t)(T + 1) * B * L.ldx * L.esz);  // X_0 .. X_T
   const size_t oc = o;
@@ -2235,8 +2275,6 @@ size_t nll_workspace(const Layout& L, int B, int T, char* ws, NllBufs* N) {
   o = wm_align256(o + M * 2 * 4);  // reward / done logits
   const size_t og = o;
   o = wm_align256(o + ((M + 255) / 256) * 4 * 4);  // block sums
-  const size_t os = o;
-  o = wm_align256(o + (size_t)kSyncWords * 4);  // persistent-kernel barriers
   if (ws && N) {
     N->sync = reinterpret_cast<unsigned*>(ws + os);
     N->x = ws + ox;
@@ -2246,6 +2284,22 @@ size_t nll_workspace(const Layout& L, int B, int T, char* ws, NllBufs* N) {
     N->wgsum = reinterpret_cast<float*>(ws + og);
   }
   return o;
+}
+
+hipError_t launch_check_zero(unsigned* sync, hipStream_t s) {
+  return launch("check", k_check_zero, dim3(1), dim3(64), 0, s, sync);
+}
+
+hipError_t launch_check_bytes01(const uint8_t* p, long n, unsigned* sync, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  return launch("check", k_check_bytes01, dim3(elem_grid(n)), dim3(256), 0, s, p, n, sync);
+}
+
+hipError_t launch_check_nll(int T, int B, int A, const int32_t* actions, const uint8_t* dones,
+                            const int32_t* lengths, unsigned* sync, hipStream_t s) {
+  if ((long)T * B <= 0) return hipSuccess;
+  return launch("check", k_check_nll, dim3(elem_grid((long)T * B)), dim3(256), 0, s, T, B, A, actions,
+                dones, lengths, sync);
 }
 
 hipError_t launch_pack(const Packed& P, void* packed, const float* W_g, const float* b_g,
@@ -2713,21 +2767,33 @@ hipError_t gemm_nt_slices(const char* name, const float* A, long lda, int M, con
                 Ks, out, ldo, oslice, map);
 }
 
-// out[m][n] = sum_s part[s][m][n] in slice order
+// The weight-gradient products reduce over all T B rows.  A K slice
+// accumulates its products in fp32, one MFMA after another, so its rounding
+// error grows with the slice's length; the slices are therefore kept to at
+// most kMaxSliceK rows and summed in fp64 (relative error of the product
+// then ~ 1e-5 of the terms' magnitude at T B = 65536).
+constexpr int kMaxSliceK = 2048;
+int split_long(int M, int N, int Kpad) {
+  int S = split_of(M, N, Kpad);
+  while (Kpad / S > kMaxSliceK && (Kpad / 32) % (2 * S) == 0) S *= 2;
+  return S;
+}
+
+// out[m][n] = sum_s part[s][m][n] in slice order, accumulated in fp64
 __global__ void __launch_bounds__(256) k_sum_slices(const float* part, int S, int M, int N, float* out, long ldo) {
   const long i = (long)blockIdx.x * 256 + threadIdx.x;
   if (i >= (long)M * N) return;
   const long mn = (long)M * N;
-  float acc = 0.f;
-  for (int k = 0; k < S; ++k) acc += part[k * mn + i];
-  out[(i / N) * ldo + i % N] = acc;
+  double acc = 0.0;
+  for (int k = 0; k < S; ++k) acc += (double)part[k * mn + i];
+  out[(i / N) * ldo + i % N] = (float)acc;
 }
 
 // out (ldo) = A . B^T, split over K through `part` ([S, M, N]) when that
-// fills the chip better
+// fills the chip better, or (long_k) to bound the fp32 accumulation chains
 hipError_t gemm_nt(const float* A, long lda, int M, const float* Bm, long ldb, int N, int Kpad, float* out,
-                   long ldo, float* part, hipStream_t s) {
-  const int S = part ? split_of(M, N, Kpad) : 1;
+                   long ldo, float* part, hipStream_t s, bool long_k = false) {
+  const int S = part ? (long_k ? split_long(M, N, Kpad) : split_of(M, N, Kpad)) : 1;
   if (S == 1) return gemm_nt_slices("grad_gemm", A, lda, M, Bm, ldb, N, Kpad, 1, out, ldo, 0, s);
   const hipError_t e = gemm_nt_slices("grad_gemm", A, lda, M, Bm, ldb, N, Kpad, S, part, N, (long)M * N, s);
   if (e != hipSuccess) return e;
@@ -2782,13 +2848,13 @@ size_t grad_workspace(const Layout& L, int B, int T, char* ws, GradWs* G) {
   const size_t oapart = take((size_t)act_chunks(L) * L.A * H4 * 4);
   // split-K partials: the largest of the products that split, and the
   // per-step slices of dG_t . W_h (always)
-  auto split_need = [](int M, int N, int Kpad) {
-    const int S = split_of(M, N, Kpad);
+  auto split_need = [](int M, int N, int Kpad, bool long_k = false) {
+    const int S = long_k ? split_long(M, N, Kpad) : split_of(M, N, Kpad);
     return S > 1 ? (size_t)S * M * N : (size_t)0;
   };
   const size_t nsplit = std::max({(size_t)bptt_split(B, H) * B * H, split_need((int)TB, H4, L.ldk),
                                   split_need((int)TB, L.Nm, L.ldh), split_need((int)TB, H, NmP),
-                                  split_need(L.ldk, H4, (int)TBp), split_need(NmP, H, (int)TBp)});
+                                  split_need(L.ldk, H4, (int)TBp, true), split_need(NmP, H, (int)TBp, true)});
   const size_t osplit = take(nsplit * 4);
   const size_t on = take(16);
   const size_t ofwd = take((size_t)TB * (L.Z + 1) * 4);  // loss terms [TB, Z+1]
@@ -2876,7 +2942,7 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   if (ones_row)
     WM_TRY(launch("grad_ones", k_ones, dim3((unsigned)((TB + 255) / 256)), dim3(256), 0, s,
                   G.T2 + (long)(Z + H) * TBp, TB));
-  WM_TRY(gemm_nt(G.T2, TBp, L.ldk, G.T1, TBp, H4, (int)TBp, G.dWgT, H4, G.split, s));
+  WM_TRY(gemm_nt(G.T2, TBp, L.ldk, G.T1, TBp, H4, (int)TBp, G.dWgT, H4, G.split, s, true));
   if (!ones_row) WM_TRY(colsum(G.dG, H4, TB, H4, G.part, G.dbg, s));
   const int nch = act_chunks(L);
   WM_TRY(launch("grad_actions", k_grad_actions,
@@ -2887,7 +2953,7 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   // dW_m [NmP, H] = dM^T . H (operands dM^T [NmP, TBp], H^T [H, TBp])
   WM_TRY(transpose(G.M, NmP, (int)TB, NmP, G.T1, TBp, (int)TBp, s));
   WM_TRY(transpose(Hn, L.ldx, (int)TB, H, G.T2, TBp, (int)TBp, s));
-  WM_TRY(gemm_nt(G.T1, TBp, NmP, G.T2, TBp, H, (int)TBp, G.dWm, H, G.split, s));
+  WM_TRY(gemm_nt(G.T1, TBp, NmP, G.T2, TBp, H, (int)TBp, G.dWm, H, G.split, s, true));
   WM_TRY(colsum(G.M, NmP, TB, NmP, G.part, G.dbm, s));
   // canonical layout
   const UnpackArgs u{Z, H, A, L.K, L.Q, L.Nm, L.ldk, G.dWgT, G.dWa, ones_row ? G.dWgT + (long)(Z + H) * H4 : G.dbg,

@@ -946,9 +946,9 @@ hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStre
   PArgs a = base_args(P, pl, R.B, R.T);
   a.k0 = R.k0; a.k1 = R.k1; a.traj0 = R.traj0; a.step0 = R.step0;
   a.tau = R.tau;
-  a.sig = (R.flags & 4u) ? sqrtf(R.tau) : 1.0f;
-  a.step_mask = (R.flags & 8u) != 0;
-  a.use_done = (R.flags & 1u) != 0;
+  a.sig = (R.flags & WM_FLAG_SIGMA_TAU) ? sqrtf(R.tau) : 1.0f;
+  a.step_mask = (R.flags & WM_FLAG_STEP_MASK) != 0;
+  a.use_done = (R.flags & WM_FLAG_DONE) != 0;
   a.X = reinterpret_cast<float*>(R.x);
   a.c = R.c;
   a.done_state = R.done_state;
@@ -959,7 +959,7 @@ hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStre
   a.actions = R.actions;
   a.rewards = R.rewards;
   a.dones = R.dones;
-  const bool trace = (R.flags & 2u) != 0;
+  const bool trace = (R.flags & WM_FLAG_TRACE) != 0;
   a.h_trace = trace ? R.h_trace : nullptr;
   a.c_trace = trace ? R.c_trace : nullptr;
   return launch_plan<false>(a, pl, s);

@@ -1,23 +1,28 @@
-"""HBM traffic per launch of one kernel class, from rocprofv3 counters.
+"""rocprofv3 counter runs and their summaries.
 
-The counters come from two rocprofv3 passes over the same program (one pass
-per counter, as the hardware collects FETCH_SIZE and WRITE_SIZE on the same
-TCC blocks):
+HBM traffic per launch of one kernel class comes from two rocprofv3 passes
+over the same program (one pass per counter, as the hardware collects
+FETCH_SIZE and WRITE_SIZE on the same TCC blocks):
 
     rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT/fetch -o run -- \
-        python3 -m paper_2205_01435_amd.traffic run
+        python3 -m paper_2205_01435_amd.traffic run --workload xlarge_rollout
     rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT/write -o run -- \
-        python3 -m paper_2205_01435_amd.traffic run
+        python3 -m paper_2205_01435_amd.traffic run --workload xlarge_rollout
     python3 -m paper_2205_01435_amd.traffic summarize OUT/fetch/run_counter_collection.csv \
-        OUT/write/run_counter_collection.csv --kernel k_gates --out profiles/<file>.md
+        OUT/write/run_counter_collection.csv --kernel k_gates --workload xlarge_rollout \
+        --out profiles/<file>.md
 
 ``run`` first copies 256 MiB device to device three times (a copy kernel that
 reads and writes exactly that many bytes: the calibration of each counter),
-then runs two bench steps (medium dream rollout + NLL).  ``summarize`` scales
-the kernel's per-dispatch average by bytes / counter of the copy and writes a
-short summary, stamped with the names and hash of the sources the kernel is
-compiled from, so that a reader (bench.py) can tell whether the figures still
-describe the current kernel.
+then runs calls of one workload (default: two of the xlarge dream rollout).
+``summarize`` scales the kernel's per-dispatch average by bytes / counter of
+the copy and writes a short summary, stamped with the names and hash of the
+sources the kernel is compiled from, so that a reader (bench.py) can tell
+whether the figures still describe the current kernel.
+
+``counters`` summarises any other counters of a ``--pmc`` pass (per-dispatch
+averages of the kernels a regex selects), and ``stats`` a
+``--kernel-trace --stats`` run's kernel_stats.csv.
 """
 
 from __future__ import annotations
@@ -50,7 +55,9 @@ def kernel_source_hash(sources: list[str]) -> str:
     return h.hexdigest()
 
 
-def run() -> None:
+def run(workload: str = "xlarge_rollout", calls: int = 2) -> None:
+    """The calibration copies, then ``calls`` calls of one workload (a dream
+    rollout or an NLL pass) on its seeded inputs."""
     import numpy as np
     import torch
 
@@ -65,20 +72,27 @@ def run() -> None:
     torch.cuda.synchronize()
     del a, b
 
-    w = wl.WORKLOADS["medium_rollout"]
-    roll = wl.make_rollout_inputs(w)
-    nll_in = wl.make_nll_inputs(w.replace(kind="nll"))
+    w = wl.WORKLOADS[workload]
     cuda = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
-    model = wmlib.pack(roll["weights"], w.Z, w.H, w.A, w.K, w.dtype)
-    z0, mask = cuda(roll["z0"]), cuda(roll["mask"])
-    nz, na, nr, nd = (cuda(nll_in[k]) for k in ("z", "actions", "rewards", "dones"))
-    rb = wmlib.RolloutBuffers(model, w.B, w.T, trace=False)
-    nb = wmlib.NllBuffers(model, w.B, w.T)
-    for i in range(2):
-        wmlib.rollout(model, z0, mask, T=w.T, seed=w.seed + i, tau=w.tau, done=w.done, bufs=rb)
-        wmlib.nll(model, nz, na, nr, nd, bufs=nb)
-    torch.cuda.synchronize()
-    print("traffic run done", flush=True)
+    if w.kind == "rollout":
+        inp = wl.make_rollout_inputs(w)
+        model = wmlib.pack(inp["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+        z0, mask = cuda(inp["z0"]), cuda(inp["mask"])
+        rb = wmlib.RolloutBuffers(model, w.B, w.T, trace=False)
+        for i in range(calls):
+            wmlib.rollout(model, z0, mask, T=w.T, seed=w.seed + i, tau=w.tau, done=w.done, bufs=rb)
+            torch.cuda.synchronize()
+            print(f"{workload}: call {i + 1} of {calls} done", flush=True)
+    else:
+        d = wl.make_nll_inputs(w)
+        model = wmlib.pack(d["weights"], w.Z, w.H, w.A, w.K, w.dtype)
+        args = [cuda(d[k]) for k in ("z", "actions", "rewards", "dones")]
+        nb = wmlib.NllBuffers(model, w.B, w.T)
+        for i in range(calls):
+            wmlib.nll(model, *args, bufs=nb)
+            torch.cuda.synchronize()
+            print(f"{workload}: call {i + 1} of {calls} done", flush=True)
+    print("counter run done", flush=True)
 
 
 def _per_dispatch(path: str, counter: str) -> list[tuple[str, int, float]]:
@@ -92,7 +106,8 @@ def _per_dispatch(path: str, counter: str) -> list[tuple[str, int, float]]:
     return rows
 
 
-def summarize(fetch_csv: str, write_csv: str, kernel: str, out: str, command: str) -> dict:
+def summarize(fetch_csv: str, write_csv: str, kernel: str, out: str, command: str,
+              workload: str = "") -> dict:
     res = {}
     for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         rows = _per_dispatch(path, counter)
@@ -108,7 +123,7 @@ def summarize(fetch_csv: str, write_csv: str, kernel: str, out: str, command: st
                         "bytes_per_launch": kib_kernel * 1024.0 * factor}
     total = res["FETCH_SIZE"]["bytes_per_launch"] + res["WRITE_SIZE"]["bytes_per_launch"]
     lines = [
-        f"# HBM traffic per launch: {kernel} (medium dream rollout + NLL, fp32)",
+        f"# HBM traffic per launch: {kernel} ({workload or 'workload not named'})",
         "",
         "Counters from two `rocprofv3 --pmc` passes (FETCH_SIZE, then WRITE_SIZE, KiB per",
         f"dispatch), each scaled by bytes / counter of a {CALIB_BYTES >> 20} MiB device copy",
@@ -151,21 +166,90 @@ def read_summary(path: str) -> float | None:
     return float(m.group(1))
 
 
+def counters(csvs: list[str], kernel: str, out: str, title: str, command: str, note: str = "") -> dict:
+    """Per-dispatch averages of every counter in the given counter-collection
+    CSVs over the dispatches whose kernel name matches ``kernel``."""
+    acc: dict[tuple[str, str], list[float]] = {}
+    for path in csvs:
+        with open(path, newline="") as f:
+            for r in csv.DictReader(f):
+                if not re.search(kernel, r["Kernel_Name"]):
+                    continue
+                acc.setdefault((r["Kernel_Name"], r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+    if not acc:
+        raise SystemExit(f"no dispatch of {kernel} in {csvs}")
+    lines = [f"# {title}", "", f"command: `{command}`", ""]
+    if note:
+        lines += [note, ""]
+    lines += ["| kernel | counter | dispatches | average per dispatch |", "|---|---|---|---|"]
+    res = {}
+    for (k, c), v in sorted(acc.items()):
+        avg = sum(v) / len(v)
+        res.setdefault(k, {})[c] = avg
+        lines.append(f"| `{_short(k)}` | {c} | {len(v)} | {avg:.6g} |")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    return res
+
+
+def _short(name: str, n: int = 90) -> str:
+    return name if len(name) <= n else name[:n - 1] + "\u2026"
+
+
+def stats(csv_path: str, out: str, title: str, command: str, note: str = "", top: int = 14) -> list:
+    """A kernel_stats.csv of `rocprofv3 --kernel-trace --stats` as a table."""
+    rows = []
+    with open(csv_path, newline="") as f:
+        for r in csv.DictReader(f):
+            rows.append((r["Name"], int(r["Calls"]), float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+                         float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+    rows.sort(key=lambda x: -x[5])
+    lines = [f"# {title}", "", f"command: `{command}`", ""]
+    if note:
+        lines += [note, ""]
+    lines += ["| kernel | calls | avg us | min us | max us | share % |", "|---|---|---|---|---|---|"]
+    for name, calls, avg, mn, mx, pct in rows[:top]:
+        lines.append(f"| `{_short(name)}` | {calls} | {avg:.2f} | {mn:.2f} | {mx:.2f} | {pct:.1f} |")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    return rows
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="cmd", required=True)
-    sub.add_parser("run")
+    r = sub.add_parser("run")
+    r.add_argument("--workload", default="xlarge_rollout")
+    r.add_argument("--calls", type=int, default=2)
     s = sub.add_parser("summarize")
     s.add_argument("fetch_csv")
     s.add_argument("write_csv")
     s.add_argument("--kernel", required=True, help="regex on the kernel name")
+    s.add_argument("--workload", default="")
     s.add_argument("--out", required=True)
     s.add_argument("--command", default="", help="command line to record in the summary")
+    c = sub.add_parser("counters")
+    c.add_argument("csvs", nargs="+")
+    c.add_argument("--kernel", required=True, help="regex on the kernel name")
+    c.add_argument("--out", required=True)
+    c.add_argument("--title", required=True)
+    c.add_argument("--command", default="")
+    c.add_argument("--note", default="")
+    t = sub.add_parser("stats")
+    t.add_argument("csv")
+    t.add_argument("--out", required=True)
+    t.add_argument("--title", required=True)
+    t.add_argument("--command", default="")
+    t.add_argument("--note", default="")
     a = ap.parse_args()
     if a.cmd == "run":
-        run()
+        run(a.workload, a.calls)
+    elif a.cmd == "summarize":
+        print(summarize(a.fetch_csv, a.write_csv, a.kernel, a.out, a.command, a.workload))
+    elif a.cmd == "counters":
+        print(counters(a.csvs, a.kernel, a.out, a.title, a.command, a.note))
     else:
-        print(summarize(a.fetch_csv, a.write_csv, a.kernel, a.out, a.command))
+        stats(a.csv, a.out, a.title, a.command, a.note)
     return 0
 
 

@@ -52,6 +52,10 @@ def test_version_and_sizes():
     assert wmlib.workspace_bytes(d, 256, 50, 0) > 0
     assert wmlib.workspace_bytes(d, 256, 50, 1) > wmlib.workspace_bytes(d, 256, 50, 0)
     assert wmlib.workspace_bytes(d, 0, 50, 0) == 0
+    # which: 0 rollout, 1 NLL, 2 controller step (no workspace), 3 training gradient
+    assert wmlib.workspace_bytes(d, 256, 50, wmlib.WS_CONTROLLER) == 0
+    assert wmlib.workspace_bytes(d, 256, 50, wmlib.WS_NLL_GRAD) > wmlib.workspace_bytes(d, 256, 50, 1)
+    assert wmlib.workspace_bytes(d, 256, 50, 4) == 0
 
 
 @pytest.mark.parametrize("dims,status", [
@@ -65,7 +69,7 @@ def test_version_and_sizes():
 def test_bad_dims_rejected(dims, status):
     lib = wmlib.load()
     d = wmlib.make_dims(*dims)
-    assert lib.wm_packed_bytes(ctypes.byref(d)) == 0
+    assert lib.wm_packed_weights_bytes(ctypes.byref(d)) == 0
     fake = ctypes.c_void_p(256)  # never dereferenced: validation fails first
     st = lib.wm_controller_step(ctypes.byref(d), fake, 4, 0, fake, fake, fake, 1, 0, None, fake, None)
     assert st == status
@@ -90,11 +94,15 @@ def test_rollout_argument_checks():
     assert _rollout_call(tau=float("nan")) == wmlib.WM_ERR_INVALID_ARG
     assert _rollout_call(B=0) == wmlib.WM_ERR_INVALID_ARG
     assert _rollout_call(T=-1) == wmlib.WM_ERR_INVALID_ARG
-    assert _rollout_call(flags=16) == wmlib.WM_ERR_INVALID_ARG  # flags above WM_FLAG_STEP_MASK
+    assert _rollout_call(flags=32) == wmlib.WM_ERR_INVALID_ARG  # an undefined flag bit
+    assert _rollout_call(flags=1 << 30) == wmlib.WM_ERR_INVALID_ARG
     assert _rollout_call(flags=3) == wmlib.WM_ERR_INVALID_ARG  # trace without buffers
     assert _rollout_call(z_out=ctypes.c_void_p(4100)) == wmlib.WM_ERR_INVALID_ARG  # misaligned
     assert _rollout_call(packed=ctypes.c_void_p(4112)) == wmlib.WM_ERR_INVALID_ARG
     assert _rollout_call() == wmlib.WM_ERR_WORKSPACE  # workspace too small
+    # every defined flag passes the flag check (and fails later on the workspace)
+    for f in (wmlib.WM_FLAG_CHECK, wmlib.WM_FLAG_STEP_MASK, wmlib.WM_FLAG_SIGMA_TAU, wmlib.WM_FLAG_TEST_ABORT):
+        assert _rollout_call(flags=1 | f) == wmlib.WM_ERR_WORKSPACE, f
     assert _rollout_call(T=0) == wmlib.WM_OK  # no-op
     assert "workspace" in wmlib.load().wm_last_error().decode() or True
 
@@ -103,20 +111,29 @@ def test_nll_argument_checks():
     lib = wmlib.load()
     d = wmlib.make_dims(8, 16, 4, 2)
     p = ctypes.c_void_p(4096)
-    st = lib.wm_nll(ctypes.byref(d), p, 4, 3, None, p, p, p, None, p, p, p, None, p, 0, None)
+    st = lib.wm_nll(ctypes.byref(d), p, 4, 3, None, p, p, p, None, 0, p, p, p, None, p, 0, None)
     assert st == wmlib.WM_ERR_INVALID_ARG
-    st = lib.wm_nll(ctypes.byref(d), p, 4, 3, p, p, p, p, None, p, p, p, None, p, 0, None)
+    st = lib.wm_nll(ctypes.byref(d), p, 4, 3, p, p, p, p, None, 0, p, p, p, None, p, 0, None)
+    assert st == wmlib.WM_ERR_WORKSPACE
+    # only WM_FLAG_CHECK and WM_FLAG_TEST_ABORT are defined for the NLL pass
+    st = lib.wm_nll(ctypes.byref(d), p, 4, 3, p, p, p, p, None, wmlib.WM_FLAG_DONE, p, p, p, None, p, 0, None)
+    assert st == wmlib.WM_ERR_INVALID_ARG
+    st = lib.wm_nll(ctypes.byref(d), p, 4, 3, p, p, p, p, None, wmlib.WM_FLAG_CHECK, p, p, p, None, p, 0, None)
     assert st == wmlib.WM_ERR_WORKSPACE
 
 
-def _grad_call(dims=None, B=4, T=3, z=4096, out=4096, ws=4096, ws_bytes=0, loss=None):
+def test_workspace_status_argument_check():
+    assert wmlib.load().wm_workspace_status(None, None) == wmlib.WM_ERR_INVALID_ARG
+
+
+def _grad_call(dims=None, B=4, T=3, z=4096, out=4096, ws=4096, ws_bytes=0, loss=None, flags=0):
     lib = wmlib.load()
     d = dims or wmlib.make_dims(8, 16, 4, 2)
     p = ctypes.c_void_p(4096)
     zp = None if z is None else ctypes.c_void_p(z)
     o = None if out is None else ctypes.c_void_p(out)
     w = None if ws is None else ctypes.c_void_p(ws)
-    return lib.wm_nll_grad(ctypes.byref(d), p, B, T, zp, p, p, p, None, loss, o, p, p, p, p, p, p, p, w,
+    return lib.wm_nll_grad(ctypes.byref(d), p, B, T, zp, p, p, p, None, flags, loss, o, p, p, p, p, p, p, p, w,
                            ws_bytes, None)
 
 
@@ -130,17 +147,18 @@ def test_nll_grad_argument_checks():
     assert _grad_call(B=1 << 12, T=1 << 11) == wmlib.WM_ERR_UNSUPPORTED  # T B above 2^22
     assert _grad_call() == wmlib.WM_ERR_WORKSPACE
     assert _grad_call(T=0) == wmlib.WM_OK  # no-op
+    assert _grad_call(flags=wmlib.WM_FLAG_TRACE) == wmlib.WM_ERR_INVALID_ARG
 
 
 def test_nll_grad_workspace_size():
     d = wmlib.make_dims(64, 512, 64, 5, "fp32")
-    nll = wmlib.workspace_bytes(d, 512, 128, 1)
-    g = wmlib.workspace_bytes(d, 512, 128, 2)
+    nll = wmlib.workspace_bytes(d, 512, 128, wmlib.WS_NLL)
+    g = wmlib.workspace_bytes(d, 512, 128, wmlib.WS_NLL_GRAD)
     # at least the NLL pass's workspace, the gate activations and their
     # gradient [T B, 4H], the c trace [T+1, B, H] and the head outputs
     assert g >= nll + 4 * (2 * 512 * 128 * 4 * 512 + 129 * 512 * 512 + 512 * 128 * (3 * 64 * 5 + 2))
-    assert wmlib.workspace_bytes(d, 512, 64, 2) < g
-    assert wmlib.workspace_bytes(wmlib.make_dims(64, 512, 64, 5, "bf16"), 512, 128, 2) > 0
+    assert wmlib.workspace_bytes(d, 512, 64, wmlib.WS_NLL_GRAD) < g
+    assert wmlib.workspace_bytes(wmlib.make_dims(64, 512, 64, 5, "bf16"), 512, 128, wmlib.WS_NLL_GRAD) > 0
 
 
 def test_missing_library_fails_loudly(tmp_path):

@@ -5,11 +5,13 @@ gradient and the loss; shapes with ragged tails over the GEMM tiles, two
 action groups, lengths with empty and partial rows, steps without an
 action, K from 1 to 8; the full NLL workload; argument errors.
 
-Tolerance: the gradient sums over all T B rows and runs back through T
-LSTM steps in fp32, so each entry is compared with rtol GRAD_RTOL (1e-3)
-against |ref| + a scale: the RMS of its array, at least 1e-3 of the RMS
-over every gradient.  The full workload's worst error is about 3e-4 of
-the scale (W_g); the small cases stay below 1e-5."""
+Tolerance: the fp32 bar of the forward outputs, rtol 1e-4, on each entry
+against |ref| + a scale: the RMS of its array, at least 1e-3 of the RMS over
+every gradient (a gradient entry is a sum over all T B rows, so an entry
+near 0 is compared against the size of its array rather than its own).
+The weight-gradient products keep their fp32 accumulation chains to at most
+2048 rows and sum them in fp64; the same algorithm run in fp32 with numpy's
+blocked sums stays within ~1e-5 of the scale at the NLL workload."""
 
 import sys
 
@@ -24,7 +26,7 @@ from paper_2205_01435_amd import workloads as wl
 
 pytestmark = pytest.mark.gpu
 
-GRAD_RTOL = 1e-3
+GRAD_RTOL = 1e-4
 
 
 def say(*a):

@@ -119,7 +119,8 @@ def test_persistent_rollout_vs_oracle_and_launch_path(B, T, Z, H, A, K):
     say("ties", ties.mismatches, "of", ties.draws, "live", live)
     ref = owm.rollout(inp["weights"], w.dims, inp["z0"], mask, T=T, seed=17, tau=1.3,
                       done_flag=True, dtype="fp32", step0=2, traj0=11)
-    assert parity.free_run(ref, g, "fp32", T) <= max(1, 1e-3 * B * T * (Z + 2))
+    assert parity.free_run(ref, g, weights=inp["weights"], dims=w.dims, mask=mask, seed=17, tau=1.3,
+                           traj=11 + np.arange(B), step0=2) <= parity.free_run_cap(B)
     assert g["actions"][0, B // 2] == -1 and np.all(g["dones"][:, B // 2] == 1)
     # the two device paths agree except where the oracle's own free run diverges
     same = np.all(g["actions"] == gl["actions"], axis=0)
@@ -189,7 +190,8 @@ def test_persistent_resume_state_inputs_and_determinism():
     np.testing.assert_array_equal(full["c_T"][pre], c0[pre])
     ref = owm.rollout(inp["weights"], w.dims, inp["z0"], inp["mask"], T=7, seed=4, done_flag=True,
                       h0=h0, c0=c0, done0=done0, step0=1, traj0=9)
-    assert parity.free_run(ref, full, "fp32", 7) <= 1
+    assert parity.free_run(ref, full, weights=inp["weights"], dims=w.dims, mask=inp["mask"], seed=4,
+                           traj=9 + np.arange(120), step0=1) <= parity.free_run_cap(120)
     # a row subset with its trajectory offset reproduces those rows
     lo, hi = 17, 83
     sub = _np(wmlib.rollout(m, _t(inp["z0"][lo:hi]), _t(inp["mask"][lo:hi]), T=7, seed=4,
@@ -212,7 +214,8 @@ def test_persistent_no_done_flag():
     assert np.all(g["dones"][:, live] == 0) and np.all(g["actions"][:, live] >= 0)
     assert np.all(g["actions"][:, ~live] == -1) and np.all(g["dones"][:, ~live] == 1)
     ref = owm.rollout(inp["weights"], w.dims, inp["z0"], mask, T=5, seed=2, done_flag=False)
-    assert parity.free_run(ref, g, "fp32", 5) <= 1
+    assert parity.free_run(ref, g, weights=inp["weights"], dims=w.dims, mask=mask, seed=2) <= \
+        parity.free_run_cap(64)
 
 
 # (B, T, Z, H, A, K)
