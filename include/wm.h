@@ -219,6 +219,26 @@ wm_status wm_rollout(const wm_dims *dims, const void *packed, int32_t B, int32_t
                      size_t workspace_bytes, wm_stream_t stream);
 
 /*
+ * wm_rollout for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same call without the workspace arguments.  Its workspace is the
+ * library's static device scratch, 64 MiB per GPU, held by every GPU the
+ * library runs on until the process ends; a call whose rollout workspace
+ * (wm_workspace_bytes(dims, B, T, 0)) is larger returns WM_ERR_UNSUPPORTED.
+ * Nothing is allocated.  Every call on one GPU shares that GPU's scratch, so
+ * calls that may overlap on one GPU (on different streams, or from several
+ * threads without ordering) race and must be serialised by the caller.
+ * wm_workspace_status does not apply (the scratch is not the caller's);
+ * under WM_FLAG_CHECK the call itself reports the device status.
+ */
+wm_status wm_rollout_noalloc(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
+                             uint32_t traj0, uint32_t step0, const float *z0, const float *h0,
+                             const float *c0, uint8_t *done_io, const uint8_t *valid_mask,
+                             uint64_t seed, float tau, uint32_t flags, float *z_out,
+                             int32_t *actions, float *rewards, uint8_t *dones, float *h_T,
+                             float *c_T, float *h_trace, float *c_trace, wm_stream_t stream);
+
+/*
  * Teacher-forced MDN-RNN loss over B logged sequences of T steps (section
  * 4.7; padding masked as in section 3.3.1).  With h_0 = c_0 = 0:
  *   h_{t+1}, c_{t+1} = LSTM(W_z q(z_t) + W_h q(h_t) + W_g[:, Z + a_t] + b_g);

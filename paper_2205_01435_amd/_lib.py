@@ -27,7 +27,7 @@ _DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
 
 # Every symbol the C header declares.
 EXPORTS = ("wm_packed_weights_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
-           "wm_rollout", "wm_nll", "wm_nll_grad", "wm_returns", "wm_adam_step", "wm_poly_lr",
+           "wm_rollout", "wm_rollout_noalloc", "wm_nll", "wm_nll_grad", "wm_returns", "wm_adam_step", "wm_poly_lr",
            "wm_profile_enable", "wm_profile_read", "wm_profile_reset", "wm_workspace_status",
            "wm_last_error", "wm_version")
 
@@ -75,6 +75,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_rollout.argtypes = [pd, P, I32, I32, U32, U32, P, P, P, P, P, U64, F32, U32,
                                P, P, P, P, P, P, P, P, P, SZ, P]
     lib.wm_rollout.restype = I32
+    lib.wm_rollout_noalloc.argtypes = [pd, P, I32, I32, U32, U32, P, P, P, P, P, U64, F32, U32,
+                                       P, P, P, P, P, P, P, P, P]
+    lib.wm_rollout_noalloc.restype = I32
     lib.wm_nll.argtypes = [pd, P, I32, I32, P, P, P, P, P, U32, P, P, P, P, P, SZ, P]
     lib.wm_nll.restype = I32
     lib.wm_nll_grad.argtypes = [pd, P, I32, I32, P, P, P, P, P, U32, P, P, P, P, P, P, P, P, P, P, SZ, P]
@@ -227,7 +230,8 @@ def controller_step(m: Model, z, h, mask, seed: int, step: int, traj0: int = 0,
 class RolloutBuffers:
     """Caller-owned device buffers of one rollout shape (reusable across calls)."""
 
-    def __init__(self, m: Model, B: int, T: int, trace: bool = False, final_state: bool = True):
+    def __init__(self, m: Model, B: int, T: int, trace: bool = False, final_state: bool = True,
+                 workspace: bool = True):
         dev = m.packed.device
         self.B, self.T, self.Z, self.H = B, T, m.Z, m.H
         self.z_out = torch.empty((T + 1, B, m.Z), dtype=torch.float32, device=dev)
@@ -240,19 +244,20 @@ class RolloutBuffers:
                         if trace else None)
         self.c_trace = (torch.empty((T + 1, B, m.H), dtype=torch.float32, device=dev)
                         if trace else None)
-        nws = workspace_bytes(m.dims, B, T, WS_ROLLOUT)
-        self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+        nws = workspace_bytes(m.dims, B, T, WS_ROLLOUT) if workspace else 0
+        self.workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev) if workspace else None
         self.ws_bytes = nws
 
 
 def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bool = True,
             traj0: int = 0, step0: int = 0, h0=None, c0=None, done_io=None, trace: bool = False,
             bufs: RolloutBuffers | None = None, sigma_tau: bool = False, check: bool = False,
-            extra_flags: int = 0) -> RolloutBuffers:
+            extra_flags: int = 0, noalloc: bool = False) -> RolloutBuffers:
     """Launch wm_rollout on the current stream; returns the filled buffers
     (``sigma_tau`` sets WM_FLAG_SIGMA_TAU; a [T, B, A] mask sets
     WM_FLAG_STEP_MASK; ``check`` sets WM_FLAG_CHECK, which waits for the
-    stream)."""
+    stream; ``noalloc`` calls wm_rollout_noalloc, whose workspace is the
+    library's static device scratch)."""
     lib = load()
     B = z0.shape[0]
     dev = m.packed.device
@@ -277,7 +282,7 @@ def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bo
         want = (T, B, m.dims.A) if step_mask else (B, m.dims.A)
         _need("mask", mask, _mask_dtype(mask), want, dev)
     if bufs is None:
-        bufs = RolloutBuffers(m, B, T, trace=trace)
+        bufs = RolloutBuffers(m, B, T, trace=trace, workspace=not noalloc)
     if T > 0 and ((bufs.B, bufs.T) != (B, T) or bufs.Z != m.Z or bufs.H != m.H):
         raise ValueError(f"buffers for B={bufs.B} T={bufs.T} Z={bufs.Z} H={bufs.H}; the call has "
                          f"B={B} T={T} Z={m.Z} H={m.H}")
@@ -290,7 +295,12 @@ def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bo
               _ptr(done_io), _ptr(mask), seed, tau, flags, _ptr(bufs.z_out), _ptr(bufs.actions),
               _ptr(bufs.rewards), _ptr(bufs.dones), _ptr(bufs.h_T), _ptr(bufs.c_T),
               _ptr(bufs.h_trace if trace else None), _ptr(bufs.c_trace if trace else None))
-    _check(lib.wm_rollout(*common, _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
+    if noalloc:
+        _check(lib.wm_rollout_noalloc(*common, _stream()))
+    else:
+        if bufs.workspace is None:
+            raise ValueError("these buffers have no workspace (made for wm_rollout_noalloc)")
+        _check(lib.wm_rollout(*common, _ptr(bufs.workspace), bufs.ws_bytes, _stream()))
     return bufs
 
 

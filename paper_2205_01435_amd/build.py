@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libwm.so")
-SOURCES = ["wm_kernels.hip", "wm_persist.hip", "wm_returns.hip", "wm_optim.hip",
+SOURCES = ["wm_kernels.hip", "wm_persist.hip", "wm_returns.hip", "wm_optim.hip", "wm_noalloc.hip",
            "wm_api.cpp", "wm_profile.cpp"]
 HEADERS = ["wm_device.h", "wm_kernels.h", "wm_layout.h", "wm_profile.h"]
 ARCH = "gfx950"

@@ -102,7 +102,7 @@ wm_status rollout_call(const wm_dims* dims, const void* packed, int32_t B, int32
                      const float* c0, uint8_t* done_io, const uint8_t* valid_mask, uint64_t seed,
                      float tau, uint32_t flags, float* z_out, int32_t* actions, float* rewards,
                      uint8_t* dones, float* h_T, float* c_T, float* h_trace, float* c_trace,
-                     void* workspace, size_t workspace_bytes, wm_stream_t stream) {
+                     void* workspace, size_t workspace_bytes, wm_stream_t stream, bool noalloc) {
   wm::Layout L;
   wm_status st = check_dims(dims, &L);
   if (st != WM_OK) return st;
@@ -125,6 +125,14 @@ wm_status rollout_call(const wm_dims* dims, const void* packed, int32_t B, int32
     return fail(WM_ERR_UNSUPPORTED, "B*(T+1) too large");
   if (T == 0) return ok();
   const size_t need = wm::rollout_workspace(L, B, nullptr, nullptr);
+  if (noalloc) {
+    if (need > wm::kStaticScratchBytes)
+      return fail(WM_ERR_UNSUPPORTED, "wm_rollout_noalloc: B=%d needs %zu bytes of workspace, above the "
+                  "%zu-byte static scratch", B, need, wm::kStaticScratchBytes);
+    const hipError_t e = wm::static_scratch(&workspace);
+    if (e != hipSuccess) return hip_fail(e, "wm_rollout_noalloc: the static scratch");
+    workspace_bytes = wm::kStaticScratchBytes;
+  }
   if (!workspace || workspace_bytes < need)
     return fail(WM_ERR_WORKSPACE, "rollout workspace needs %zu bytes, got %zu", need, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
@@ -228,7 +236,18 @@ wm_status wm_rollout(const wm_dims* dims, const void* packed, int32_t B, int32_t
                      void* workspace, size_t workspace_bytes, wm_stream_t stream) {
   return rollout_call(dims, packed, B, T, traj0, step0, z0, h0, c0, done_io, valid_mask, seed, tau,
                       flags, z_out, actions, rewards, dones, h_T, c_T, h_trace, c_trace, workspace,
-                      workspace_bytes, stream);
+                      workspace_bytes, stream, false);
+}
+
+wm_status wm_rollout_noalloc(const wm_dims* dims, const void* packed, int32_t B, int32_t T,
+                             uint32_t traj0, uint32_t step0, const float* z0, const float* h0,
+                             const float* c0, uint8_t* done_io, const uint8_t* valid_mask,
+                             uint64_t seed, float tau, uint32_t flags, float* z_out,
+                             int32_t* actions, float* rewards, uint8_t* dones, float* h_T,
+                             float* c_T, float* h_trace, float* c_trace, wm_stream_t stream) {
+  return rollout_call(dims, packed, B, T, traj0, step0, z0, h0, c0, done_io, valid_mask, seed, tau,
+                      flags, z_out, actions, rewards, dones, h_T, c_T, h_trace, c_trace, nullptr, 0,
+                      stream, true);
 }
 
 wm_status wm_nll(const wm_dims* dims, const void* packed, int32_t B, int32_t T, const float* z,

@@ -104,6 +104,11 @@ bool persist_usable(const Layout& L, int B, bool nll);
 hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStream_t s);
 hipError_t launch_nll_persist(const Packed& P, const NllBufs& N, hipStream_t s);
 
+// The static device scratch of wm_rollout_noalloc (wm_noalloc.hip): its
+// device address on the current device, looked up once per device.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+hipError_t static_scratch(void** ptr);
+
 // Return scan over B trajectories of T steps (wm_returns.hip).
 struct ReturnsBufs {
   int B, T;
