@@ -1,16 +1,16 @@
 #!/usr/bin/env python3
 """Throughput of the World-Model dream hot path on one MI355X.
 
-One step = one pass of the whole hot path over one batch of synthetic input:
-  * a dream rollout of B = 256 trajectories x T = 50 steps (Z = 64, H = 512,
-    A = 64, K = 5, fp32): controller, LSTM core, mixture sampling, reward and
-    done heads, freeze/commit;
-  * a teacher-forced mixture-NLL pass over B = 256 logged sequences of T = 50
-    steps with the same model (random-agent data: AR(1) latents, uniform valid
-    actions, N(0, 0.1^2) rewards, Bernoulli(1/T) dones).
-value = B * T / seconds per step (each transition is both dreamed and
-scored).  Inputs are resident in HBM before the timed region; weights are
-packed once, outside it.
+One step = one dream rollout of the xlarge workload, the largest of the five
+(B = 16384 trajectories x T = 64 steps, Z = 128, H = 1024, A = 256, K = 8,
+bf16 weights and GEMM operands, fp32 accumulate and mixture arithmetic, done
+head on, mask p = 0.1): per step the controller with its masked Gumbel-max
+action, the LSTM gates and cell, the mixture head with its component pick
+and Box-Muller draw, the reward and done heads, freeze/commit.
+value = B * T / seconds per step (imagined transitions/s).  Inputs are
+resident in HBM before the timed region; weights are packed once, outside
+it.  The teacher-forced NLL pass is measured on its own workload (B 512,
+T 128, fp32) in the per-workload table, as are the other four workloads.
 
 Prints ONE JSON line (rank 0, N = 1).  --gpus above 1 exits with a message:
 this build measures one GPU.
@@ -20,6 +20,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -33,6 +34,8 @@ if ROOT not in sys.path:
 METRIC = "imagined transitions/sec (B×T) + MDN-NLL tokens/sec; % of MFMA/HBM peak"
 PEAK = {"fp32": 157.3e12, "bf16": 2516.6e12}  # dense MFMA, FLOP/s
 HBM_PEAK = 8.0e12  # B/s
+HEADLINE = "xlarge_rollout"
+CPU_ROWS = 512  # trajectories of the oracle's timed sample
 
 
 def flops_per_transition(w) -> float:
@@ -47,28 +50,21 @@ def flops_per_token(w) -> float:
     return 2.0 * (4 * H * (Z + H) + 3 * Z * K * H + 2 * H)
 
 
-def kernel_flops_per_launch(name: str, w, B: int, T: int, mdn_launches_per_step: int = 1) -> float:
-    """Algorithmic flops of one launch of a kernel class in the bench step.
-    persist: one whole dream rollout (every phase of every step);
-    nll_persist: the NLL pass's recurrence (gate GEMMs of all T steps);
-    gates / ctrl: one dream step of the multi-launch path;
-    mdn: the NLL head over all T*B rows, plus, on the multi-launch path, T
-    rollout launches of B rows (averaged over the launches)."""
+def kernel_flops_per_launch(name: str, w, B: int, T: int) -> float:
+    """Algorithmic flops of one launch of a kernel class of a dream rollout.
+    persist: the whole rollout (every phase of every step, one launch);
+    gates / mdn / ctrl: one dream step of the multi-launch path (the gate
+    GEMM; the mixture head with the reward and done columns counted in the
+    controller, which computes them; the controller's logits)."""
     Z, H, A, K = w.Z, w.H, w.A, w.K
     if name == "persist":
         return B * T * flops_per_transition(w)
-    if name == "nll_persist":
-        return 2.0 * B * T * 4 * H * (Z + H)
     if name == "gates":
         return 2.0 * B * 4 * H * (Z + H)
+    if name == "mdn":
+        return 2.0 * B * 3 * Z * K * H
     if name == "ctrl":
         return 2.0 * B * (A * (Z + H) + 2 * H)
-    if name == "mdn":
-        head = 2.0 * B * T * (3 * Z * K + 2) * H
-        if mdn_launches_per_step == 1:
-            return head
-        rollout = T * 2.0 * B * 3 * Z * K * H
-        return (head + rollout) / mdn_launches_per_step
     return 0.0
 
 
@@ -83,6 +79,15 @@ def weight_stream_bytes_per_step(w) -> float:
     return mats * esz + gathered * esz + biases * 4
 
 
+def _range(torch, name):
+    """A roctx range around a region (visible to rocprofv3 --marker-trace)."""
+    try:
+        torch.cuda.nvtx.range_push(name)
+        return lambda: torch.cuda.nvtx.range_pop()
+    except Exception:  # noqa: BLE001
+        return lambda: None
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -92,7 +97,7 @@ def main() -> int:
     ap.add_argument("--no-workloads", action="store_true", help="skip the per-workload table")
     ap.add_argument("--rows", default="", help="comma-separated rows of the per-workload table to run "
                     "(default: all)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle sample budget")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="oracle sample budget")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -115,30 +120,24 @@ def main() -> int:
     def cuda(a):
         return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
-    w = wl.WORKLOADS["medium_rollout"]
+    w = wl.WORKLOADS[HEADLINE]
     B, T = w.B, w.T
     roll_in = wl.make_rollout_inputs(w)
-    nll_in = wl.make_nll_inputs(w.replace(kind="nll"))
     model = wmlib.pack(roll_in["weights"], w.Z, w.H, w.A, w.K, w.dtype)
     z0, mask = cuda(roll_in["z0"]), cuda(roll_in["mask"])
-    nz, na = cuda(nll_in["z"]), cuda(nll_in["actions"])
-    nr, nd = cuda(nll_in["rewards"]), cuda(nll_in["dones"])
     rbufs = wmlib.RolloutBuffers(model, B, T, trace=False)
-    nbufs = wmlib.NllBuffers(model, B, T)
 
     def step(i):
         wmlib.rollout(model, z0, mask, T=T, seed=w.seed + i, tau=w.tau, done=w.done, bufs=rbufs)
-        wmlib.nll(model, nz, na, nr, nd, bufs=nbufs)
 
     # warmup, with every kernel class timed to find the dominant one
+    classes = ["persist", "ctrl", "gates", "mdn", "init", "finish"]
     wmlib.profile_reset()
     wmlib.profile_enable("")
-    for i in range(max(args.warmup, 1)):
+    nwarm = max(args.warmup, 1)
+    for i in range(nwarm):
         step(i)
     torch.cuda.synchronize()
-    classes = ["persist", "nll_persist", "ctrl", "gates", "mdn", "init", "finish", "nll_init",
-               "nll_reduce", "nll_means"]
-    nwarm = max(args.warmup, 1)
     warm = {c: wmlib.profile_read(c) for c in classes}
     dominant = max(classes, key=lambda c: warm[c][0])
     wmlib.profile_enable(None)
@@ -152,6 +151,7 @@ def main() -> int:
         wmlib.profile_enable(prefix)
         torch.cuda.synchronize()
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        done = _range(torch, "timed_steps" if prefix is None else "instrumented_steps")
         t0 = time.perf_counter()
         ev0.record()
         for i in range(args.steps):
@@ -159,6 +159,7 @@ def main() -> int:
         ev1.record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        done()
         kern = wmlib.profile_read(prefix) if prefix is not None else (0.0, 0)
         wmlib.profile_enable(None)
         wmlib.profile_reset()
@@ -166,34 +167,17 @@ def main() -> int:
 
     # value: K steps with nothing but the two bracketing events; roofline: the
     # same K steps again with dispatch-stamped events on the dominant kernel
-    # (they slow the step down, so they stay out of the throughput)
+    # (they add host work per launch, so they stay out of the throughput)
     ms_total, t_wall, _ = timed(None)
     ms_inst, _, (k_ms, k_n) = timed(dominant)
     ms_step = ms_total / args.steps
     value = B * T / (ms_step / 1e3)
-
-    # per-call breakdown (clean: no per-kernel events)
-    def time_calls(fn, reps):
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for i in range(reps):
-            fn(i)
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / reps
-
-    ms_roll = time_calls(lambda i: wmlib.rollout(model, z0, mask, T=T, seed=w.seed + i, tau=w.tau,
-                                                done=w.done, bufs=rbufs), 10)
-    ms_nll = time_calls(lambda i: wmlib.nll(model, nz, na, nr, nd, bufs=nbufs), 10)
     live = int((rbufs.actions >= 0).sum().item())
 
-    # roofline of the dominant kernel
     avg_ms = k_ms / max(k_n, 1)
-    mdn_per_step = max(1, round(warm["mdn"][1] / nwarm))
-    flops_launch = kernel_flops_per_launch(dominant, w, B, T, mdn_per_step)
+    flops_launch = kernel_flops_per_launch(dominant, w, B, T)
     achieved = flops_launch / (avg_ms / 1e3) if avg_ms > 0 else 0.0
-    traffic = read_summary(os.path.join(ROOT, "profiles", f"traffic_{dominant}_medium_rollout_nll_fp32.md"))
+    traffic = read_summary(os.path.join(ROOT, "profiles", f"traffic_{dominant}_{HEADLINE}_bf16.md"))
     roofline = {"kernel": dominant, "bound": "mfma", "achieved": achieved / 1e12,
                 "peak": PEAK[w.dtype] / 1e12, "unit": "TFLOP/s",
                 "frac": achieved / PEAK[w.dtype], "traffic": traffic,
@@ -203,21 +187,21 @@ def main() -> int:
                             "second pass of the same K steps, on the launch stream",
                 "flops_per_launch": flops_launch}
 
+    per_step_kernel_ms = {c: warm[c][0] / nwarm for c in classes if warm[c][1]}
     out = {
         "metric": METRIC, "value": value, "unit": "transitions/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic (seeded; Xavier-uniform weights, N(0,1) latents, Bernoulli(0.3) masks)",
-        "config": {"workload": "medium_rollout: dream rollout B=256 T=50 Z=64 H=512 A=64 K=5 fp32 "
-                               "+ teacher-forced NLL over B=256 x T=50 logged sequences",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; Xavier-uniform weights, N(0,1) latents, Bernoulli(0.1) masks)",
+        "config": {"workload": f"{HEADLINE}: dream rollout B={B} T={T} Z={w.Z} H={w.H} A={w.A} K={w.K} "
+                               "bf16 (fp32 accumulate and mixture math), done head on, mask p 0.1",
                    "B": B, "T": T, "Z": w.Z, "H": w.H, "A": w.A, "K": w.K, "tau": w.tau},
-        "breakdown": {"rollout_ms": ms_roll, "nll_ms": ms_nll,
-                      "rollout_transitions_per_s": B * T / (ms_roll / 1e3),
-                      "nll_tokens_per_s": B * T / (ms_nll / 1e3),
+        "breakdown": {"rollout_tflops": B * T * flops_per_transition(w) / (ms_step / 1e3) / 1e12,
+                      "rollout_frac_bf16_peak": B * T * flops_per_transition(w) / (ms_step / 1e3)
+                      / PEAK[w.dtype],
                       "live_transitions_last_rollout": live,
-                      "step_tflops": (B * T * (flops_per_transition(w) + flops_per_token(w)))
-                      / (ms_step / 1e3) / 1e12,
-                      "warmup_kernel_ms": {c: round(warm[c][0], 4) for c in classes},
+                      "kernel_ms_per_rollout_warmup": {c: round(v, 4) for c, v in per_step_kernel_ms.items()},
+                      "launches_per_rollout": {c: warm[c][1] // nwarm for c in classes if warm[c][1]},
                       "wall_s_timed_region": t_wall,
                       "ms_per_step_with_kernel_events": ms_inst / args.steps},
         "roofline": roofline,
@@ -225,17 +209,45 @@ def main() -> int:
 
     if not args.no_workloads:
         out["workloads"] = workload_table(wmlib, wl, torch, cuda, {r for r in args.rows.split(",") if r})
+        nll = out["workloads"].get("nll")
+        if nll:
+            out["nll"] = {"metric": "MDN-NLL tokens/sec", "value": nll["per_s"], "unit": "tokens/s",
+                          "ms": nll["ms"], "config": "nll: teacher-forced NLL pass B=512 T=128 Z=64 H=512 "
+                          "A=64 K=5 fp32", "frac_mfma_peak": nll["frac_mfma_peak"]}
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, roll_in, nll_in, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, roll_in, args.cpu_seconds)
 
     print(json.dumps(out), flush=True)
     return 0
 
 
+def _median_ms(torch, fn, min_reps: int = 10, min_total_s: float = 1.0, max_reps: int = 2000) -> tuple:
+    """3 warm-up calls, then the median of per-call event timings over at
+    least ``min_reps`` calls and at least ``min_total_s`` seconds."""
+    for i in range(3):
+        fn(i)
+    torch.cuda.synchronize()
+    times = []
+    i = 3
+    t_start = time.perf_counter()
+    while len(times) < min_reps or (sum(times) < min_total_s * 1e3 and len(times) < max_reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn(i)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+        i += 1
+        if time.perf_counter() - t_start > 20.0 and len(times) >= min_reps:
+            break
+    return float(np.median(times)), len(times)
+
+
 def workload_table(wmlib, wl, torch, cuda, only=frozenset()) -> dict:
-    """Whole-call timing of every workload (median of a few calls); `only`
-    (non-empty) restricts the table to the rows it names."""
+    """Whole-call timing of every workload (median of at least 10 calls and
+    1 s after 3 warm-ups); `only` (non-empty) restricts the table to the rows
+    it names."""
     res = {}
     for name, w in wl.WORKLOADS.items():
         if only and name not in only:
@@ -255,21 +267,11 @@ def workload_table(wmlib, wl, torch, cuda, only=frozenset()) -> dict:
             bufs = wmlib.NllBuffers(m, w.B, w.T)
             fn = lambda i: wmlib.nll(m, *args, bufs=bufs)  # noqa: E731
             fl = flops_per_token(w)
-        fn(0)
-        torch.cuda.synchronize()
-        times = []
-        for i in range(5):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            fn(i + 1)
-            b.record()
-            torch.cuda.synchronize()
-            times.append(a.elapsed_time(b))
-        ms = float(np.median(times))
+        ms, reps = _median_ms(torch, fn)
         n = w.B * w.T
-        row = {"ms": ms, "per_s": n / (ms / 1e3), "unit": "transitions/s" if w.kind == "rollout"
-               else "tokens/s", "tflops": n * fl / (ms / 1e3) / 1e12,
-               "frac_mfma_peak": n * fl / (ms / 1e3) / PEAK[w.dtype]}
+        row = {"ms": ms, "reps": reps, "per_s": n / (ms / 1e3),
+               "unit": "transitions/s" if w.kind == "rollout" else "tokens/s",
+               "tflops": n * fl / (ms / 1e3) / 1e12, "frac_mfma_peak": n * fl / (ms / 1e3) / PEAK[w.dtype]}
         if name == "tiny_rollout":
             gb = weight_stream_bytes_per_step(w) * w.T
             row["weight_stream_GBps"] = gb / (ms / 1e3) / 1e9
@@ -312,20 +314,10 @@ def train_step_row(wmlib, wl, torch, cuda) -> dict:
         wmlib.adam_step(params, gb.flat, mom, vel, i + 1, 1e-4)
         wmlib.repack(m, canon)
 
-    step(0)
-    torch.cuda.synchronize()
-    times = []
-    for i in range(5):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        step(i + 1)
-        b.record()
-        torch.cuda.synchronize()
-        times.append(a.elapsed_time(b))
-    ms = float(np.median(times))
+    ms, reps = _median_ms(torch, step)
     wmlib.profile_reset()
     wmlib.profile_enable("")
-    step(6)
+    step(reps + 3)
     torch.cuda.synchronize()
     parts = {p: wmlib.profile_read(p)[0] for p in ("nll_persist", "mdn", "grad_gemm_bptt", "grad_gemm",
                                                   "grad_lstm", "grad_", "adam", "pack")}
@@ -336,7 +328,7 @@ def train_step_row(wmlib, wl, torch, cuda) -> dict:
     fwd = 2 * 4 * w.H * (w.Z + w.H) + 2 * w.H * (3 * w.Z * w.K + 2)
     n = w.B * w.T
     fl = 3.0 * fwd * n
-    return {"ms": ms, "tokens_per_s": n / (ms / 1e3), "flops_per_step": fl, "tflops": fl / (ms / 1e3) / 1e12,
+    return {"ms": ms, "reps": reps, "tokens_per_s": n / (ms / 1e3), "flops_per_step": fl, "tflops": fl / (ms / 1e3) / 1e12,
             "frac_fp32_peak": fl / (ms / 1e3) / PEAK["fp32"], "kernel_ms": {k: round(v, 4) for k, v in parts.items()},
             "loss": float(gb.loss.cpu()[0])}
 
@@ -390,19 +382,9 @@ def two_level_row(wmlib, wl, torch, cuda) -> dict:
     mask = (cuda(xm), cuda(lm))
     bufs = wmlib.RolloutBuffers(m, B, T)
     run = lambda i: wmlib.rollout(m, z0, mask, T=T, seed=7 + i, done=True, bufs=bufs)  # noqa: E731
-    run(0)
-    torch.cuda.synchronize()
-    times = []
-    for i in range(3):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        run(i + 1)
-        e1.record()
-        torch.cuda.synchronize()
-        times.append(e0.elapsed_time(e1))
-    ms = float(np.median(times))
+    ms, reps = _median_ms(torch, run)
     fl = 2.0 * (4 * H * (Z + H) + 3 * Z * K * H + (N + 1 + L) * (Z + H) + 2 * H)
-    return {"ms": ms, "per_s": B * T / (ms / 1e3), "unit": "transitions/s",
+    return {"ms": ms, "reps": reps, "per_s": B * T / (ms / 1e3), "unit": "transitions/s",
             "tflops": B * T * fl / (ms / 1e3) / 1e12, "frac_mfma_peak": B * T * fl / (ms / 1e3) / PEAK["bf16"]}
 
 
@@ -449,8 +431,13 @@ def returns_row(wmlib, torch, cuda) -> dict:
             "kernel_us": kms * 1e3, "kernel_frac_hbm_peak": nb / (kms / 1e3) / HBM_PEAK}
 
 
-def cpu_baseline(w, roll_in, nll_in, budget_s: float) -> dict:
-    """The oracle as it stands, timed on this host's cores on the same batch."""
+def cpu_baseline(w, roll_in, budget_s: float) -> dict:
+    """The oracle as it stands (float64 numpy with the bf16 rounding points),
+    timed on this host's cores on a subset of the same batch: the first
+    CPU_ROWS trajectories, whole rollouts of T steps, repeated while the
+    budget lasts.  A trajectory's result does not depend on the others, so
+    the per-transition rate of the subset is the oracle's rate on the
+    workload."""
     from oracle import wm as owm
 
     try:
@@ -459,21 +446,21 @@ def cpu_baseline(w, roll_in, nll_in, budget_s: float) -> dict:
         threads = int(blas[0]["num_threads"]) if blas else 1
     except Exception:  # noqa: BLE001
         threads = 1
+    rows = min(CPU_ROWS, w.B)
+    z0, mask = roll_in["z0"][:rows], roll_in["mask"][:rows]
     reps, t0 = 0, time.perf_counter()
     while True:
-        owm.rollout(roll_in["weights"], w.dims, roll_in["z0"], roll_in["mask"], T=w.T,
-                    seed=w.seed + reps, tau=w.tau, done_flag=w.done, dtype=w.dtype)
-        owm.nll(roll_in["weights"], w.dims, nll_in["z"], nll_in["actions"], nll_in["rewards"],
-                nll_in["dones"], dtype=w.dtype)
+        owm.rollout(roll_in["weights"], w.dims, z0, mask, T=w.T, seed=w.seed + reps, tau=w.tau,
+                    done_flag=w.done, dtype=w.dtype)
         reps += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 50:
+        if el >= budget_s or reps >= 20:
             break
-    return {"value": w.B * w.T * reps / el, "unit": "transitions/s", "cores": threads,
+    return {"value": rows * w.T * reps / el, "unit": "transitions/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"full step (rollout + NLL, B={w.B}, T={w.T}) x {reps} in {el:.1f} s, "
-                      f"float64 numpy, {threads} BLAS threads, "
-                      f"{len(os.sched_getaffinity(0))} cores visible"}
+            "sample": f"{reps} whole rollout(s) of the first {rows} of the {w.B} trajectories (T={w.T}, "
+                      f"{w.name}) in {el:.1f} s, float64 numpy with bf16 rounding points, "
+                      f"{threads} BLAS threads, {len(os.sched_getaffinity(0))} cores visible"}
 
 
 if __name__ == "__main__":

@@ -38,6 +38,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 HEADERS = ["wm_device.h", "wm_kernels.h", "wm_layout.h"]
 CALIB_BYTES = 256 << 20
+XCDS, SIMDS = 8, 1024  # MI355X: 8 XCDs, 256 CUs x 4 SIMDs
 
 
 def kernel_sources(kernel: str) -> list[str]:
@@ -187,6 +188,28 @@ def counters(csvs: list[str], kernel: str, out: str, title: str, command: str, n
         avg = sum(v) / len(v)
         res.setdefault(k, {})[c] = avg
         lines.append(f"| `{_short(k)}` | {c} | {len(v)} | {avg:.6g} |")
+    derived = []
+    for k, cs in res.items():
+        # GRBM_GUI_ACTIVE is summed over the 8 XCDs; the SQ counters over all 1024 SIMDs
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in cs and cs.get("GRBM_GUI_ACTIVE"):
+            cyc = cs["GRBM_GUI_ACTIVE"] / XCDS
+            derived.append((k, "MFMA busy, % of SIMD cycles", 100.0 * cs["SQ_VALU_MFMA_BUSY_CYCLES"] / SIMDS / cyc))
+            if "SQ_INSTS_VALU" in cs:
+                other = cs["SQ_INSTS_VALU"] - cs.get("SQ_INSTS_MFMA", 0.0)
+                derived.append((k, "non-MFMA VALU instructions per SIMD", other / SIMDS))
+                derived.append((k, "their issue cycles (4 per wave64 instruction), % of SIMD cycles",
+                                100.0 * 4 * other / SIMDS / cyc))
+            derived.append((k, "kernel cycles per XCD (GRBM_GUI_ACTIVE / 8)", cyc))
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in cs:
+            derived.append((k, "bf16 MFMA flops (MOPS x 512)", 512.0 * cs["SQ_INSTS_VALU_MFMA_MOPS_BF16"]))
+        if "TCC_HIT_sum" in cs and "TCC_MISS_sum" in cs:
+            tot = cs["TCC_HIT_sum"] + cs["TCC_MISS_sum"]
+            derived.append((k, "L2 hit rate, %", 100.0 * cs["TCC_HIT_sum"] / tot if tot else 0.0))
+    if derived:
+        lines += ["", "| kernel | derived | value |", "|---|---|---|"]
+        for k, name, v in derived:
+            res[k][name] = v
+            lines.append(f"| `{_short(k)}` | {name} | {v:.6g} |")
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     return res
