@@ -308,7 +308,8 @@ def transition(wb: dict, dims: dict, z, h, c, mask, *, seed: int, traj, step: in
 
 def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.0,
             done_flag: bool = True, dtype: str = "fp32", traj0: int = 0, step0: int = 0,
-            h0=None, c0=None, done0=None, sigma_tau: bool = False, two_level=None) -> dict:
+            h0=None, c0=None, done0=None, sigma_tau: bool = False, two_level=None,
+            lengths=None) -> dict:
     """B dream trajectories of T steps (the "hallucinated" environment of
     section 3.3 driven by the controller of section 3.4).
 
@@ -322,6 +323,13 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
     the controller is two-level (``two_level_action``), ``mask`` is the pair
     (xfer mask [B, N+1], location mask [B, N, L]) and a NO-OP ends the
     trajectory with action -2 at that step.
+
+    ``lengths [B]`` (optional) gives each trajectory its own horizon, as
+    variable-length sequences are zero-padded and masked (section 3.3.1):
+    trajectory b is stepped for t < lengths[b] only; a step t >= lengths[b]
+    is padding, with action -1, reward 0, done 0 and z_out[t+1] = 0, and the
+    state stays as it was after step lengths[b] - 1 (h_T, c_T, done_T are
+    that state).
 
     Returns z_out [T+1, B, Z], actions [T, B], rewards [T, B], dones [T, B],
     h_T, c_T [B, H], done_T [B], the state trace h_trace, c_trace [T+1, B, H]
@@ -351,9 +359,10 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
     k_margin = np.full((T, B, Z), np.nan)
     d_margin = np.full((T, B), np.nan)
 
+    horizon = np.full(B, T, np.int64) if lengths is None else np.clip(np.asarray(lengths, np.int64), 0, T)
     for t in range(T):
         h_trace[t], c_trace[t] = h, c
-        live = np.nonzero(~done)[0]
+        live = np.nonzero(~done & (t < horizon))[0]
         if live.size:
             if two_level is not None:
                 mask_l = (np.asarray(mask[0])[live], np.asarray(mask[1])[live])
@@ -379,6 +388,9 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
             done[live[~ok]] = True
             actions[t, live[r["action"] == -2]] = -2  # the NO-OP ended these
         z_out[t + 1] = z
+        pad = t >= horizon  # padding: zero latent, no action, reward 0, not done
+        z_out[t + 1, pad] = 0.0
+        dones[t, pad] = 0
     h_trace[T], c_trace[T] = h, c
     return dict(z_out=z_out, actions=actions, rewards=rewards, dones=dones,
                 h_T=h.copy(), c_T=c.copy(), done_T=done.astype(np.uint8),
