@@ -184,12 +184,20 @@ wm_status wm_controller_step(const wm_dims *dims, const void *packed, int32_t B,
  *      (stream 3) if WM_FLAG_DONE, else 0.
  * A done trajectory is frozen for the remaining steps: action -1, reward 0,
  * done 1, z copied, state unchanged.  A live trajectory with no valid action
- * ends at that step with the same frozen outputs.
+ * ends at that step with the same frozen outputs.  With `lengths`, variable-
+ * length trajectories are zero-padded as sequences are in section 3.3.1:
+ * trajectory b is stepped for t < lengths[b]; a step t >= lengths[b] is
+ * padding (action -1, reward 0, done 0, z_out[t+1] = 0) and its state stays
+ * as after its last real step.
  *
  *   z0 [B, Z]            float32 initial latent.
  *   h0, c0 [B, H]        float32 initial state, nullable (= 0).
  *   done_io [B]          uint8, nullable: in = already done, out = done
  *                        after the last step.
+ *   lengths [B]          int32, nullable (= T for every trajectory): the
+ *                        horizon of each trajectory (values outside [0, T]
+ *                        act as clamped); h_T, c_T and done_io then hold the
+ *                        state after step lengths[b] - 1.
  *   valid_mask [B, A]    uint8, constant over the rollout; with
  *                        WM_FLAG_STEP_MASK [T, B, A], step t's actions
  *                        drawn from valid_mask[t].  With the two-level
@@ -212,10 +220,10 @@ wm_status wm_controller_step(const wm_dims *dims, const void *packed, int32_t B,
  */
 wm_status wm_rollout(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
                      uint32_t traj0, uint32_t step0, const float *z0, const float *h0,
-                     const float *c0, uint8_t *done_io, const uint8_t *valid_mask,
-                     uint64_t seed, float tau, uint32_t flags, float *z_out,
-                     int32_t *actions, float *rewards, uint8_t *dones, float *h_T,
-                     float *c_T, float *h_trace, float *c_trace, void *workspace,
+                     const float *c0, uint8_t *done_io, const int32_t *lengths,
+                     const uint8_t *valid_mask, uint64_t seed, float tau, uint32_t flags,
+                     float *z_out, int32_t *actions, float *rewards, uint8_t *dones,
+                     float *h_T, float *c_T, float *h_trace, float *c_trace, void *workspace,
                      size_t workspace_bytes, wm_stream_t stream);
 
 /*
@@ -233,10 +241,11 @@ wm_status wm_rollout(const wm_dims *dims, const void *packed, int32_t B, int32_t
  */
 wm_status wm_rollout_noalloc(const wm_dims *dims, const void *packed, int32_t B, int32_t T,
                              uint32_t traj0, uint32_t step0, const float *z0, const float *h0,
-                             const float *c0, uint8_t *done_io, const uint8_t *valid_mask,
-                             uint64_t seed, float tau, uint32_t flags, float *z_out,
-                             int32_t *actions, float *rewards, uint8_t *dones, float *h_T,
-                             float *c_T, float *h_trace, float *c_trace, wm_stream_t stream);
+                             const float *c0, uint8_t *done_io, const int32_t *lengths,
+                             const uint8_t *valid_mask, uint64_t seed, float tau,
+                             uint32_t flags, float *z_out, int32_t *actions, float *rewards,
+                             uint8_t *dones, float *h_T, float *c_T, float *h_trace,
+                             float *c_trace, wm_stream_t stream);
 
 /*
  * Teacher-forced MDN-RNN loss over B logged sequences of T steps (section

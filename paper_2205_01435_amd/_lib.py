@@ -72,10 +72,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_workspace_bytes.restype = SZ
     lib.wm_controller_step.argtypes = [pd, P, I32, U32, P, P, P, U64, U32, P, P, P]
     lib.wm_controller_step.restype = I32
-    lib.wm_rollout.argtypes = [pd, P, I32, I32, U32, U32, P, P, P, P, P, U64, F32, U32,
+    lib.wm_rollout.argtypes = [pd, P, I32, I32, U32, U32, P, P, P, P, P, P, U64, F32, U32,
                                P, P, P, P, P, P, P, P, P, SZ, P]
     lib.wm_rollout.restype = I32
-    lib.wm_rollout_noalloc.argtypes = [pd, P, I32, I32, U32, U32, P, P, P, P, P, U64, F32, U32,
+    lib.wm_rollout_noalloc.argtypes = [pd, P, I32, I32, U32, U32, P, P, P, P, P, P, U64, F32, U32,
                                        P, P, P, P, P, P, P, P, P]
     lib.wm_rollout_noalloc.restype = I32
     lib.wm_nll.argtypes = [pd, P, I32, I32, P, P, P, P, P, U32, P, P, P, P, P, SZ, P]
@@ -250,11 +250,13 @@ class RolloutBuffers:
 
 
 def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bool = True,
-            traj0: int = 0, step0: int = 0, h0=None, c0=None, done_io=None, trace: bool = False,
+            traj0: int = 0, step0: int = 0, h0=None, c0=None, done_io=None, lengths=None,
+            trace: bool = False,
             bufs: RolloutBuffers | None = None, sigma_tau: bool = False, check: bool = False,
             extra_flags: int = 0, noalloc: bool = False) -> RolloutBuffers:
     """Launch wm_rollout on the current stream; returns the filled buffers
-    (``sigma_tau`` sets WM_FLAG_SIGMA_TAU; a [T, B, A] mask sets
+    (``lengths`` [B] int32: per-trajectory horizons, later steps padded;
+    ``sigma_tau`` sets WM_FLAG_SIGMA_TAU; a [T, B, A] mask sets
     WM_FLAG_STEP_MASK; ``check`` sets WM_FLAG_CHECK, which waits for the
     stream; ``noalloc`` calls wm_rollout_noalloc, whose workspace is the
     library's static device scratch)."""
@@ -265,6 +267,7 @@ def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bo
     _need("h0", h0, torch.float32, (B, m.H), dev, optional=True)
     _need("c0", c0, torch.float32, (B, m.H), dev, optional=True)
     _need("done_io", done_io, _mask_dtype(done_io), (B,), dev, optional=True)
+    _need("lengths", lengths, torch.int32, (B,), dev, optional=True)
     if m.dims.N > 0:
         # two-level controller: (xfer mask [B, N+1], location mask [B, N, L])
         # as one buffer, xfer masks first
@@ -292,7 +295,7 @@ def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bo
         (WM_FLAG_SIGMA_TAU if sigma_tau else 0) | (WM_FLAG_STEP_MASK if step_mask else 0) | \
         (WM_FLAG_CHECK if check else 0) | extra_flags
     common = (ctypes.byref(m.dims), _ptr(m.packed), B, T, traj0, step0, _ptr(z0), _ptr(h0), _ptr(c0),
-              _ptr(done_io), _ptr(mask), seed, tau, flags, _ptr(bufs.z_out), _ptr(bufs.actions),
+              _ptr(done_io), _ptr(lengths), _ptr(mask), seed, tau, flags, _ptr(bufs.z_out), _ptr(bufs.actions),
               _ptr(bufs.rewards), _ptr(bufs.dones), _ptr(bufs.h_T), _ptr(bufs.c_T),
               _ptr(bufs.h_trace if trace else None), _ptr(bufs.c_trace if trace else None))
     if noalloc:

@@ -99,7 +99,7 @@ uint32_t key_hi(uint64_t s) { return (uint32_t)(s >> 32); }
 
 wm_status rollout_call(const wm_dims* dims, const void* packed, int32_t B, int32_t T,
                      uint32_t traj0, uint32_t step0, const float* z0, const float* h0,
-                     const float* c0, uint8_t* done_io, const uint8_t* valid_mask, uint64_t seed,
+                     const float* c0, uint8_t* done_io, const int32_t* lengths, const uint8_t* valid_mask, uint64_t seed,
                      float tau, uint32_t flags, float* z_out, int32_t* actions, float* rewards,
                      uint8_t* dones, float* h_T, float* c_T, float* h_trace, float* c_trace,
                      void* workspace, size_t workspace_bytes, wm_stream_t stream, bool noalloc) {
@@ -154,7 +154,7 @@ wm_status rollout_call(const wm_dims* dims, const void* packed, int32_t B, int32
   R.B = B; R.T = T; R.traj0 = traj0; R.step0 = step0;
   R.k0 = key_lo(seed); R.k1 = key_hi(seed);
   R.tau = tau; R.flags = flags;
-  R.z0 = z0; R.h0 = h0; R.c0 = c0; R.done_io = done_io; R.mask = valid_mask;
+  R.z0 = z0; R.h0 = h0; R.c0 = c0; R.done_io = done_io; R.lengths = lengths; R.mask = valid_mask;
   R.z_out = z_out; R.actions = actions; R.rewards = rewards; R.dones = dones;
   R.h_T = h_T; R.c_T = c_T; R.h_trace = h_trace; R.c_trace = c_trace;
   wm::rollout_workspace(L, B, ws, &R);
@@ -230,22 +230,22 @@ wm_status wm_controller_step(const wm_dims* dims, const void* packed, int32_t B,
 
 wm_status wm_rollout(const wm_dims* dims, const void* packed, int32_t B, int32_t T,
                      uint32_t traj0, uint32_t step0, const float* z0, const float* h0,
-                     const float* c0, uint8_t* done_io, const uint8_t* valid_mask, uint64_t seed,
+                     const float* c0, uint8_t* done_io, const int32_t* lengths, const uint8_t* valid_mask, uint64_t seed,
                      float tau, uint32_t flags, float* z_out, int32_t* actions, float* rewards,
                      uint8_t* dones, float* h_T, float* c_T, float* h_trace, float* c_trace,
                      void* workspace, size_t workspace_bytes, wm_stream_t stream) {
-  return rollout_call(dims, packed, B, T, traj0, step0, z0, h0, c0, done_io, valid_mask, seed, tau,
+  return rollout_call(dims, packed, B, T, traj0, step0, z0, h0, c0, done_io, lengths, valid_mask, seed, tau,
                       flags, z_out, actions, rewards, dones, h_T, c_T, h_trace, c_trace, workspace,
                       workspace_bytes, stream, false);
 }
 
 wm_status wm_rollout_noalloc(const wm_dims* dims, const void* packed, int32_t B, int32_t T,
                              uint32_t traj0, uint32_t step0, const float* z0, const float* h0,
-                             const float* c0, uint8_t* done_io, const uint8_t* valid_mask,
+                             const float* c0, uint8_t* done_io, const int32_t* lengths, const uint8_t* valid_mask,
                              uint64_t seed, float tau, uint32_t flags, float* z_out,
                              int32_t* actions, float* rewards, uint8_t* dones, float* h_T,
                              float* c_T, float* h_trace, float* c_trace, wm_stream_t stream) {
-  return rollout_call(dims, packed, B, T, traj0, step0, z0, h0, c0, done_io, valid_mask, seed, tau,
+  return rollout_call(dims, packed, B, T, traj0, step0, z0, h0, c0, done_io, lengths, valid_mask, seed, tau,
                       flags, z_out, actions, rewards, dones, h_T, c_T, h_trace, c_trace, nullptr, 0,
                       stream, true);
 }

@@ -23,6 +23,7 @@ struct RolloutBufs {
   uint32_t flags;
   const float *z0, *h0, *c0;
   uint8_t* done_io;
+  const int32_t* lengths;  // [B] per-trajectory horizons, or null (T for all)
   const uint8_t* mask;
   float* z_out;
   int32_t* actions;

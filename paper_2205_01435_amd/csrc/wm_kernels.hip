@@ -941,6 +941,9 @@ struct CtrlArgs {
   uint8_t* done_t;
   int32_t* done_state;
   int use_done;
+  // per-trajectory horizons (null: T for all): a step t >= lengths[m] is padding
+  const int32_t* lengths;
+  int t;
   // two-level controller (N > 0, rollout modes): mask holds the xfer masks
   // [M, N+1] followed by the location masks [M, N, Lc]; the logits are the
   // N+1 xfer rows then the Lc location rows
@@ -953,6 +956,8 @@ struct CtrlArgs {
 // sigmoid(done head) exceeds the stream-3 uniform of step t-1.  Then (mode 1)
 // the row takes action `a` (the masked Gumbel-max, -1 if no action is valid)
 // or, if done, the frozen outputs; a row without a valid action ends here.
+// A step past the row's horizon is padding: no action, reward 0, done 0 (its
+// state is kept like a frozen row's; the latent is zeroed afterwards).
 __device__ __forceinline__ void ctrl_row_commit(const CtrlArgs& p, const Rng& rng, int m, int a,
                                                 float rr, float rd) {
   int ds = p.done_state[m];
@@ -967,12 +972,13 @@ __device__ __forceinline__ void ctrl_row_commit(const CtrlArgs& p, const Rng& rn
     if (d) ds = 1;
   }
   if (p.mode == 1) {
-    if (ds) a = -1;
+    const bool pad = p.lengths && p.t >= p.lengths[m];
+    if (ds || pad) a = -1;
     else if (a < 0) ds = 1;
     p.act_t[m] = a;
     if (a < 0) {
       p.rew_t[m] = 0.f;
-      p.done_t[m] = 1;
+      p.done_t[m] = pad ? 0 : 1;
     }
   }
   p.done_state[m] = ds;
@@ -1699,6 +1705,18 @@ __global__ void k_rollout_finish(int B, int Z, int H, int ldx, const DT* __restr
     for (long i = i0; i < B; i += stride) done_io[i] = (uint8_t)done_state[i];
 }
 
+// Padding of variable-length rollouts: z_out[t+1, b, :] = 0 for t >= lengths[b].
+__global__ void k_rollout_pad(int T, int B, int Z, const int32_t* __restrict__ lengths,
+                              float* __restrict__ z_out) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  const long n = (long)T * B * Z;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const long tb = i / Z;
+    const int t = (int)(tb / B), b = (int)(tb % B);
+    if (t >= lengths[b]) z_out[(long)B * Z + i] = 0.f;
+  }
+}
+
 // X_t[:, 0:Z] = q(z_t) for t = 0..T, padding columns zero, h_0 = c_0 = 0.
 template <typename DT>
 __global__ void k_nll_init(int T, int B, int Z, int H, int ldx, const float* __restrict__ z,
@@ -2084,6 +2102,18 @@ unsigned elem_grid(long n) {
   return (unsigned)g;
 }
 
+// After the last step: the final state and done flags, and the padding of
+// variable-length rollouts.
+template <typename DT>
+hipError_t rollout_tail(const Layout& L, const RolloutBufs& R, const DT* XT, hipStream_t s) {
+  const long BH = (long)R.B * L.H;
+  hipError_t e = launch("finish", k_rollout_finish<DT>, dim3(elem_grid(BH)), dim3(256), 0, s, R.B, L.Z, L.H,
+                        L.ldx, XT, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
+  if (e != hipSuccess || !R.lengths) return e;
+  return launch("finish", k_rollout_pad, dim3(elem_grid((long)R.T * R.B * L.Z)), dim3(256), 0, s, R.T, R.B,
+                L.Z, R.lengths, R.z_out);
+}
+
 template <typename DT>
 hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   const Layout& L = P.L;
@@ -2100,9 +2130,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   if (T > 0) {
     // one persistent launch for every step when the batch and dims allow it
     e = launch_rollout_persist(P, R, s);
-    if (e == hipSuccess)
-      return launch("finish", k_rollout_finish<DT>, dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, L.ldx,
-                    X + (long)(T & 1) * BX, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
+    if (e == hipSuccess) return rollout_tail<DT>(L, R, X + (long)(T & 1) * BX, s);
     if (e != hipErrorNotSupported) return e;
   }
 
@@ -2116,6 +2144,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ca.k0 = R.k0; ca.k1 = R.k1; ca.traj0 = R.traj0;
   ca.done_state = R.done_state;
   ca.use_done = (R.flags & WM_FLAG_DONE) != 0;
+  ca.lengths = R.lengths;
   ca.N = L.N;
   ca.Lc = L.Lc;
 
@@ -2146,6 +2175,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
     DT* Xn = X + (long)((t + 1) & 1) * BX;
     ca.x = Xt;
     ca.step = step;
+    ca.t = t;
     ca.mode = t < T ? 1 : 2;
     // step t's [B, A] slice of a per-step mask (the tail step draws no action)
     ca.mask = (R.flags & WM_FLAG_STEP_MASK) ? R.mask + (long)(t < T ? t : T - 1) * B * L.A : R.mask;
@@ -2175,8 +2205,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
     e = launch_mdn<DT>(ma, L.Q, mdn_tiles, s);
     if (e != hipSuccess) return e;
   }
-  return launch("finish", k_rollout_finish<DT>, dim3(elem_grid(BH)), dim3(256), 0, s, B, Z, H, L.ldx,
-                X + (long)(T & 1) * BX, R.c, R.done_state, R.h_T, R.c_T, R.done_io);
+  return rollout_tail<DT>(L, R, X + (long)(T & 1) * BX, s);
 }
 
 // heads = false: the recurrence only (X_1 .. X_T), for the training gradient

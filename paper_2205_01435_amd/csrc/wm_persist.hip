@@ -70,6 +70,7 @@ struct PArgs {
   float* X;             // rollout [2, B, ldx]; NLL [T+1, B, ldx]
   float* c;             // [B, H]: initial cell state in, final state out (rollout)
   int32_t* done_state;  // [B]
+  const int32_t* lengths;  // [B] per-trajectory horizons, or null
   float* P;             // [32, B, Nc] controller partial logits (rollout)
   unsigned* sync;       // kSyncWords words, zero at launch
   const uint8_t* mask;  // [B, A], or [T, B, A] with step_mask
@@ -623,13 +624,15 @@ __device__ __forceinline__ void ctrl_phase(const PArgs& p, char* lds, int t, con
       }
     }
     if (!tail) {
+      // past the row's horizon: padding (no action, reward 0, done 0)
+      const bool pad = p.lengths && t >= p.lengths[m];
       int act = bidx;
-      if (ds) act = -1;
+      if (ds || pad) act = -1;
       else if (act < 0) ds = 1;
       p.actions[(long)t * B + m] = act;
       if (act < 0) {
         p.rewards[(long)t * B + m] = 0.f;
-        p.dones[(long)t * B + m] = 1;
+        p.dones[(long)t * B + m] = pad ? 0 : 1;
       }
     }
     p.done_state[m] = ds;
@@ -952,6 +955,7 @@ hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStre
   a.X = reinterpret_cast<float*>(R.x);
   a.c = R.c;
   a.done_state = R.done_state;
+  a.lengths = R.lengths;
   a.P = R.P;
   a.sync = R.sync;
   a.mask = R.mask;

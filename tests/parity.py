@@ -74,13 +74,27 @@ class TieCounter:
             f"{self.mismatches} near-tie mismatches in {self.draws} draws exceed {cap:.1%}"
 
 
+def check_padding(g, t, rows):
+    """Rows past their horizon at step t show the padding pattern: action -1,
+    reward 0, done 0, zero latent, state unchanged."""
+    if rows.size == 0:
+        return
+    assert np.all(g["actions"][t][rows] == -1) and np.all(g["rewards"][t][rows] == 0)
+    assert np.all(g["dones"][t][rows] == 0)
+    assert np.all(g["z_out"][t + 1][rows] == 0)
+    if "h_trace" in g:
+        np.testing.assert_array_equal(g["h_trace"][t + 1][rows], g["h_trace"][t][rows])
+        np.testing.assert_array_equal(g["c_trace"][t + 1][rows], g["c_trace"][t][rows])
+
+
 def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, step0=0,
-               done0=None, sigma_tau=False, two_level=None):
+               done0=None, sigma_tau=False, two_level=None, lengths=None):
     """Re-anchored comparison of a device rollout.
 
     ``g`` holds the device's z_out, actions, rewards, dones, h_trace and
     c_trace for some trajectories (batch axis of length n), ``mask [n, A]``
     (or [T, n, A] per step) their masks and ``traj [n]`` their trajectory indices (default 0..n-1).
+    ``lengths [n]``: per-trajectory horizons; later steps must be padding.
     """
     T = g["actions"].shape[0]
     n = g["actions"].shape[1]
@@ -90,15 +104,18 @@ def reanchored(dims, wts, mask, g, *, seed, tau, done_flag, dtype, traj=None, st
     ties = TieCounter()
     live = np.ones(n, bool) if done0 is None else np.asarray(done0) == 0
     n_live_steps = 0
+    horizon = np.full(n, T) if lengths is None else np.asarray(lengths)
     for t in range(T):
         za, ha, ca = g["z_out"][t], g["h_trace"][t], g["c_trace"][t]
         a_g = g["actions"][t]
+        inside = t < horizon
+        check_padding(g, t, np.nonzero(~inside)[0])
         # frozen rows must show the frozen pattern
-        fr = ~live
+        fr = ~live & inside
         assert np.all(a_g[fr] == -1) and np.all(g["dones"][t][fr] == 1)
         assert np.all(g["rewards"][t][fr] == 0)
         np.testing.assert_array_equal(g["z_out"][t + 1][fr], za[fr])
-        idx = np.nonzero(live)[0]
+        idx = np.nonzero(live & inside)[0]
         if idx.size == 0:
             continue
         n_live_steps += idx.size
@@ -172,7 +189,7 @@ def free_run_cap(B: int) -> float:
 
 
 def free_run(ref, g, *, weights, dims, mask, seed, tau=1.0, dtype="fp32", traj=None, step0=0,
-             sigma_tau=False, record=None):
+             sigma_tau=False, record=None, lengths=None):
     """Free-run comparison of a device rollout ``g`` with the oracle's own
     rollout ``ref`` of the same inputs.
 
@@ -197,7 +214,8 @@ def free_run(ref, g, *, weights, dims, mask, seed, tau=1.0, dtype="fp32", traj=N
 
     Returns the number of diverged trajectories; ``record`` (a dict) gets the
     counts.  Without a device trace the drift term is 0 (the bound is the
-    re-anchored one).
+    re-anchored one).  With ``lengths`` the steps past a trajectory's horizon
+    must be padding on both sides.
     """
     from oracle import philox as ph
 
@@ -219,6 +237,10 @@ def free_run(ref, g, *, weights, dims, mask, seed, tau=1.0, dtype="fp32", traj=N
         tb = traj[b:b + 1]
         for t in range(T):
             s = step0 + t
+            if lengths is not None and t >= lengths[b]:
+                check_padding(g, t, np.array([b]))
+                check_padding(ref, t, np.array([b]))
+                continue
             zr, hr = ref["z_out"][t, b], ref["h_trace"][t, b]
             zg = g["z_out"][t, b]
             hg = g["h_trace"][t, b] if has_h else hr

@@ -81,7 +81,7 @@ def _rollout_call(**over):
     d = wmlib.make_dims(8, 16, 4, 2)
     p = ctypes.c_void_p(4096)  # aligned dummy, never dereferenced
     args = dict(dims=ctypes.byref(d), packed=p, B=4, T=3, traj0=0, step0=0, z0=p, h0=None,
-                c0=None, done_io=None, mask=p, seed=1, tau=1.0, flags=1, z_out=p, actions=p,
+                c0=None, done_io=None, lengths=None, mask=p, seed=1, tau=1.0, flags=1, z_out=p, actions=p,
                 rewards=p, dones=p, h_T=None, c_T=None, h_trace=None, c_trace=None,
                 ws=p, ws_bytes=0, stream=None)
     args.update(over)
