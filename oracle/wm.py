@@ -108,7 +108,8 @@ def controller_logits(wb: dict, z, h, dtype: str) -> np.ndarray:
     return x @ wb["W_c"].T + wb["b_c"]
 
 
-def two_level_action(logits, xmask, lmask, *, seed: int, traj, step: int, N: int, L: int):
+def two_level_action(logits, xmask, lmask, *, seed: int, traj, step: int, N: int, L: int,
+                     return_xfer: bool = False):
     """The two-level action of section 3.1.3: the controller first picks a
     graph transformation (xfer) among the valid ones, index N being the NO-OP
     that ends the episode, then a location among those valid for that xfer.
@@ -120,7 +121,8 @@ def two_level_action(logits, xmask, lmask, *, seed: int, traj, step: int, N: int
     a = x L + l of the world model's one-hot input, -2 for the NO-OP, -1 when
     no xfer (or no location of the chosen xfer) is valid; and the margin and
     top score of the pick with the smaller relative margin, for near-tie
-    checks.
+    checks (and, with ``return_xfer``, the picked xfer: N for the NO-OP, -1
+    when none is valid).
     """
     logits = np.asarray(logits, np.float64)
     n = logits.shape[0]
@@ -135,7 +137,8 @@ def two_level_action(logits, xmask, lmask, *, seed: int, traj, step: int, N: int
     a = np.where(x < 0, -1, np.where(x == N, -2, np.where(loc < 0, -1, x * L + loc)))
     with np.errstate(invalid="ignore"):
         use_l = xfer & (lm / (1 + np.abs(lt)) < xm / (1 + np.abs(xt)))
-    return a.astype(np.int64), np.where(use_l, lm, xm), np.where(use_l, lt, xt)
+    out = (a.astype(np.int64), np.where(use_l, lm, xm), np.where(use_l, lt, xt))
+    return out + (x,) if return_xfer else out
 
 
 def masked_softmax(logits, mask) -> np.ndarray:
@@ -399,16 +402,34 @@ def rollout(w: dict, dims: dict, z0, mask, *, T: int, seed: int, tau: float = 1.
 
 
 def controller_step(w: dict, dims: dict, z, h, mask, *, seed: int, step: int,
-                    traj0: int = 0, dtype: str = "fp32") -> dict:
+                    traj0: int = 0, dtype: str = "fp32", two_level=None) -> dict:
     """One controller decision (section 3.4 with the masking of section 3.1.3):
     masked softmax probabilities of the logits (tau = 1) and a Gumbel-max
-    sample from them on stream 0 of (seed, traj0 + b, step)."""
+    sample from them on stream 0 of (seed, traj0 + b, step).
+
+    With ``two_level = (N, L)`` (section 3.1.3's xfer, then location) and
+    ``mask`` the pair (xfer mask [B, N+1], location mask [B, N, L]): the
+    action of ``two_level_action`` and ``probs [B, N+1+L]``, the masked
+    softmax of the xfer logits followed by the masked softmax of the location
+    logits over the locations valid for the picked xfer (all 0 when the NO-OP
+    or nothing was picked)."""
     Z, H, A, K = dims["Z"], dims["H"], dims["A"], dims["K"]
     wb = weight_blocks(w, Z, H, A, K, dtype)
     z = np.asarray(z, np.float64)
     B = z.shape[0]
     logits = controller_logits(wb, z, h, dtype)
     traj = traj0 + np.arange(B)
+    if two_level is not None:
+        N, L = two_level
+        xm, lm = np.asarray(mask[0]) != 0, np.asarray(mask[1]) != 0
+        a, margin, top, x = two_level_action(logits, xm, lm, seed=seed, traj=traj, step=step, N=N, L=L,
+                                             return_xfer=True)
+        chosen = (x >= 0) & (x < N)
+        lrow = np.where(chosen[:, None], lm[np.arange(B), np.clip(x, 0, N - 1)], False)
+        probs = np.concatenate([masked_softmax(logits[:, :N + 1], xm),
+                                masked_softmax(logits[:, N + 1:], lrow)], axis=1)
+        return dict(probs=probs, action=a.astype(np.int32), margin=margin, top=top, logits=logits,
+                    xfer=x)
     u0 = ph.stream_uniforms(seed, traj, step, ph.STREAM_CONTROLLER, A)
     a, margin, top = argmax_fp32(logits + gumbel(u0), np.asarray(mask) != 0)
     return dict(probs=masked_softmax(logits, mask), action=a.astype(np.int32),

@@ -94,3 +94,49 @@ def test_rollout_noop_ends_the_trajectory():
     np.testing.assert_array_equal(r["z_out"][1:, 0], np.broadcast_to(r["z_out"][0, 0], (T, Z)))
     live = r["actions"] >= 0
     assert live[:, 1:].any() and np.all(r["actions"][live] < A)
+
+
+def test_controller_step_factored_probabilities():
+    """The two-level controller step's probabilities: the xfer softmax over
+    the valid xfers, then the location softmax over the locations valid for
+    the picked xfer (zero after a NO-OP or no pick); the action's parts carry
+    positive probability; against a direct float64 softmax of the logits."""
+    from paper_2205_01435_amd import workloads as wl
+    Z, H, K, n = 8, 16, 2, 300
+    rng = np.random.default_rng(9)
+    w = wl.make_weights(rng, Z, H, N * L, K, 10)
+    a_ = np.sqrt(6.0 / (Z + H + N + 1 + L))
+    w["W_c"] = rng.uniform(-a_, a_, size=(N + 1 + L, Z + H))
+    w["b_c"] = rng.normal(size=N + 1 + L)
+    dims = dict(Z=Z, H=H, A=N * L, K=K)
+    z = rng.normal(size=(n, Z))
+    h = np.tanh(rng.normal(size=(n, H)))
+    xm = (rng.random((n, N + 1)) < 0.6).astype(np.uint8)
+    xm[:5] = 0
+    xm[5:10] = 0
+    xm[5:10, N] = 1  # NO-OP only
+    lm = (rng.random((n, N, L)) < 0.5).astype(np.uint8)
+    r = wm.controller_step(w, dims, z, h, (xm, lm), seed=4, step=2, two_level=(N, L))
+    p = r["probs"]
+    assert p.shape == (n, N + 1 + L)
+    logits = np.concatenate([z, h], axis=1) @ np.asarray(w["W_c"]).T + w["b_c"]
+    for b in range(n):
+        px = p[b, :N + 1]
+        if xm[b].any():
+            e = np.where(xm[b] != 0, np.exp(logits[b, :N + 1] - logits[b, :N + 1][xm[b] != 0].max()), 0)
+            np.testing.assert_allclose(px, e / e.sum(), rtol=1e-12, atol=1e-15)
+        else:
+            assert np.all(px == 0)
+        x = r["xfer"][b]
+        pl = p[b, N + 1:]
+        if 0 <= x < N and lm[b, x].any():
+            e = np.where(lm[b, x] != 0, np.exp(logits[b, N + 1:] - logits[b, N + 1:][lm[b, x] != 0].max()), 0)
+            np.testing.assert_allclose(pl, e / e.sum(), rtol=1e-12, atol=1e-15)
+        else:
+            assert np.all(pl == 0)
+        a = r["action"][b]
+        if a >= 0:
+            assert px[a // L] > 0 and pl[a % L] > 0 and xm[b, a // L] and lm[b, a // L, a % L]
+        elif a == -2:
+            assert x == N
+    assert np.all(r["action"][:5] == -1) and np.all(r["action"][5:10] == -2)
