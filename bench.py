@@ -280,7 +280,8 @@ def workload_table(wmlib, wl, torch, cuda, only=frozenset()) -> dict:
         del bufs, m
         torch.cuda.empty_cache()
     extra = {"returns_gae_xlarge": lambda: returns_row(wmlib, torch, cuda),
-             "two_level_rollout": lambda: two_level_row(wmlib, wl, torch, cuda),
+             "two_level_rollout_n288": lambda: two_level_row(wmlib, wl, torch, cuda, 288),
+             "two_level_rollout_n80": lambda: two_level_row(wmlib, wl, torch, cuda, 80),
              "adam_xlarge_wm": lambda: adam_row(wmlib, torch),
              "train_step_nll": lambda: train_step_row(wmlib, wl, torch, cuda)}
     for name, fn in extra.items():
@@ -360,12 +361,13 @@ def adam_row(wmlib, torch) -> dict:
             "kernel_frac_hbm_peak": nb / (kms / 1e3) / HBM_PEAK}
 
 
-def two_level_row(wmlib, wl, torch, cuda) -> dict:
-    """A dream rollout with the two-level controller (N = 10 xfers + NO-OP,
-    L = 200 locations, A = 2000 world-model actions) at the large rollout's
-    sizes (B = 4096, Z = 64, H = 1024, K = 8, bf16), T = 20, against the bf16
-    MFMA peak; the controller has N + 1 + L logit rows."""
-    B, T, Z, H, K, N, L = 4096, 20, 64, 1024, 8, 10, 200
+def two_level_row(wmlib, wl, torch, cuda, N: int = 288) -> dict:
+    """A dream rollout with the two-level controller at the paper's largest
+    action space (SqueezeNet1.1's 288 substitutions + NO-OP, 200 locations:
+    A = 57600 world-model actions) at the large rollout's sizes (B = 4096,
+    Z = 64, H = 1024, K = 8, bf16), T = 20, against the bf16 MFMA peak; the
+    controller has N + 1 + L logit rows."""
+    B, T, Z, H, K, L = 4096, 20, 64, 1024, 8, 200
     A = N * L
     rng = np.random.default_rng(6)
     w = wl.make_weights(rng, Z, H, A, K, T)
@@ -379,12 +381,12 @@ def two_level_row(wmlib, wl, torch, cuda) -> dict:
     xm[:, N] = 0
     lm = (rng.random((B, N, L)) < 0.3).astype(np.uint8)
     lm[:, :, 0] = 1
-    mask = (cuda(xm), cuda(lm))
+    mask = wmlib.two_level_mask(m, cuda(xm), cuda(lm))  # the library's layout, built once
     bufs = wmlib.RolloutBuffers(m, B, T)
     run = lambda i: wmlib.rollout(m, z0, mask, T=T, seed=7 + i, done=True, bufs=bufs)  # noqa: E731
     ms, reps = _median_ms(torch, run)
     fl = 2.0 * (4 * H * (Z + H) + 3 * Z * K * H + (N + 1 + L) * (Z + H) + 2 * H)
-    return {"ms": ms, "reps": reps, "per_s": B * T / (ms / 1e3), "unit": "transitions/s",
+    return {"N": N, "L": L, "A": A, "ms": ms, "reps": reps, "per_s": B * T / (ms / 1e3), "unit": "transitions/s",
             "tflops": B * T * fl / (ms / 1e3) / 1e12, "frac_mfma_peak": B * T * fl / (ms / 1e3) / PEAK["bf16"]}
 
 

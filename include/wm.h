@@ -23,8 +23,10 @@
  *     the stream only in wm_workspace_status and under WM_FLAG_CHECK.
  *   - Matrices are row-major.  Time-major arrays are [T, B, ...].
  *   - Dimensions: B trajectories / sequences, T steps, Z latent size (a
- *     multiple of 8), H hidden size (a multiple of 16), A actions (1..2048),
- *     K Gaussians per latent dimension (1..8).  Other values return
+ *     multiple of 8), H hidden size (a multiple of 16), A actions (1..2048
+ *     with a one-level controller; A = N L with the two-level one, N + 1 and
+ *     L at most 1024, the one-hot block of A x 4H weights under 2 GiB), K
+ *     Gaussians per latent dimension (1..8).  Other values return
  *     WM_ERR_UNSUPPORTED.
  *   - Thread safety: calls may be made from several threads; calls that
  *     share output or workspace buffers must be ordered by the caller.
@@ -159,8 +161,13 @@ size_t wm_workspace_bytes(const wm_dims *dims, int32_t B, int32_t T, int32_t whi
  *   action [B]           int32; argmax over valid a of logits_a - ln(-ln u_a)
  *                        (a sample from `probs`), u_a uniform a of stream 0;
  *                        ties go to the lowest index; -1 if none is valid.
- * The two-level controller (dims N > 0) is not served here
- * (WM_ERR_UNSUPPORTED); it runs inside wm_rollout.
+ * The two-level controller (dims N > 0, section 3.1.3): valid_mask holds
+ * the xfer masks [B, N+1] followed by the location masks [B, N, L]; action
+ * is the two-level pick described under wm_rollout (x L + l, -2 for the
+ * NO-OP, -1 when nothing is valid); probs [B, N+1+L] is required and
+ * receives the softmax of the valid xfers' logits, then the softmax of the
+ * logits of the locations valid for the picked xfer (all 0 after a NO-OP or
+ * when nothing is valid).
  */
 wm_status wm_controller_step(const wm_dims *dims, const void *packed, int32_t B,
                              uint32_t traj0, const float *z, const float *h,

@@ -209,17 +209,43 @@ def repack(m: Model, canon: dict):
                                _stream()))
 
 
+def two_level_mask(m: Model, xm, lm):
+    """The one buffer the library reads for the two-level controller: the
+    xfer masks [B, N+1], then the location masks [B, N, L] (uint8)."""
+    return _two_level_mask(m, (xm, lm), xm.shape[0])
+
+
+def _two_level_mask(m: Model, mask, B: int):
+    """(xfer mask [B, N+1], location mask [B, N, L]) as the one buffer the
+    library reads, xfer masks first; a flat buffer of that layout is taken
+    as it is."""
+    N, L = m.dims.N, m.dims.L
+    dev = m.packed.device
+    if isinstance(mask, torch.Tensor):
+        _need("two-level mask", mask, _mask_dtype(mask), (B * (N + 1) + B * N * L,), dev)
+        return mask
+    xm, lm = mask
+    _need("xfer mask", xm, _mask_dtype(xm), (B, N + 1), dev)
+    _need("location mask", lm, _mask_dtype(lm), (B, N, L), dev)
+    return torch.cat([xm.reshape(-1), lm.reshape(-1)]).contiguous()
+
+
 def controller_step(m: Model, z, h, mask, seed: int, step: int, traj0: int = 0,
                     want_probs: bool = True):
-    """Returns (probs [B, A] or None, action [B] int32)."""
+    """Returns (probs or None, action [B] int32).  One-level: probs [B, A].
+    Two-level (N > 0): ``mask`` is (xfer mask [B, N+1], location mask
+    [B, N, L]) and probs [B, N+1+L] (always returned)."""
     lib = load()
     B = z.shape[0]
     dev = m.packed.device
     _need("z", z, torch.float32, (B, m.Z), dev)
     _need("h", h, torch.float32, (B, m.H), dev)
-    if m.dims.N == 0:  # (the two-level controller is refused by the library)
+    if m.dims.N > 0:
+        mask = _two_level_mask(m, mask, B)
+        probs = torch.empty((B, m.dims.N + 1 + m.dims.L), dtype=torch.float32, device=dev)
+    else:
         _need("mask", mask, _mask_dtype(mask), (B, m.A), dev)
-    probs = torch.empty((B, m.A), dtype=torch.float32, device=dev) if want_probs else None
+        probs = torch.empty((B, m.A), dtype=torch.float32, device=dev) if want_probs else None
     action = torch.empty(B, dtype=torch.int32, device=dev)
     _check(lib.wm_controller_step(ctypes.byref(m.dims), _ptr(m.packed), B, traj0, _ptr(z),
                                   _ptr(h), _ptr(mask), seed, step, _ptr(probs), _ptr(action),
@@ -269,16 +295,7 @@ def rollout(m: Model, z0, mask, *, T: int, seed: int, tau: float = 1.0, done: bo
     _need("done_io", done_io, _mask_dtype(done_io), (B,), dev, optional=True)
     _need("lengths", lengths, torch.int32, (B,), dev, optional=True)
     if m.dims.N > 0:
-        # two-level controller: (xfer mask [B, N+1], location mask [B, N, L])
-        # as one buffer, xfer masks first
-        xm, lm = mask
-        N, L = m.dims.N, m.dims.L
-        if tuple(xm.shape) != (B, N + 1) or tuple(lm.shape) != (B, N, L):
-            raise ValueError(f"two-level masks {tuple(xm.shape)}, {tuple(lm.shape)}; expected "
-                             f"{(B, N + 1)}, {(B, N, L)}")
-        _need("xfer mask", xm, _mask_dtype(xm), (B, N + 1), dev)
-        _need("location mask", lm, _mask_dtype(lm), (B, N, L), dev)
-        mask = torch.cat([xm.reshape(-1), lm.reshape(-1)]).contiguous()
+        mask = _two_level_mask(m, mask, B)
         step_mask = False
     else:
         step_mask = mask is not None and mask.dim() == 3

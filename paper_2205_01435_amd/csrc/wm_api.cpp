@@ -50,14 +50,19 @@ wm_status check_dims(const wm_dims* d, wm::Layout* L) {
     return fail(WM_ERR_UNSUPPORTED, "Z=%d: kernels need Z a multiple of 8, at most 1024", d->Z);
   if (d->H % 16 != 0 || d->H > 8192)
     return fail(WM_ERR_UNSUPPORTED, "H=%d: kernels need H a multiple of 16, at most 8192", d->H);
-  if (d->A > 2048) return fail(WM_ERR_UNSUPPORTED, "A=%d: at most 2048 actions", d->A);
   if (d->K > 8) return fail(WM_ERR_UNSUPPORTED, "K=%d: at most 8 components", d->K);
   if (d->N < 0 || d->L < 0 || (d->N == 0) != (d->L == 0))
     return fail(WM_ERR_INVALID_ARG, "N=%d and L=%d must both be 0 or both positive", d->N, d->L);
+  if (d->N == 0 && d->A > 2048)
+    return fail(WM_ERR_UNSUPPORTED, "A=%d: at most 2048 actions for a one-level controller", d->A);
   if (d->N > 0 && (int64_t)d->N * d->L != d->A)
     return fail(WM_ERR_INVALID_ARG, "two-level controller: A=%d must equal N*L=%d*%d", d->A, d->N, d->L);
-  if (d->N > 0 && d->N + 1 + d->L > 318)
-    return fail(WM_ERR_UNSUPPORTED, "two-level controller: N+1+L=%d above 318 logits", d->N + 1 + d->L);
+  if (d->N > 0 && (d->N + 1 > 1024 || d->L > 1024))
+    return fail(WM_ERR_UNSUPPORTED, "two-level controller: N+1=%d and L=%d must be at most 1024", d->N + 1,
+                d->L);
+  // the one-hot block (A rows of 4H) is addressed with 32-bit byte offsets
+  if ((int64_t)d->A * 4 * d->H * (d->dtype == WM_FP32 ? 4 : 2) >= ((int64_t)1 << 31))
+    return fail(WM_ERR_UNSUPPORTED, "A=%d, H=%d: the one-hot block exceeds 2 GiB", d->A, d->H);
   *L = wm::make_layout(d->Z, d->H, d->A, d->K, d->dtype, d->N, d->L);
   return WM_OK;
 }
@@ -215,8 +220,9 @@ wm_status wm_controller_step(const wm_dims* dims, const void* packed, int32_t B,
   wm_status st = check_dims(dims, &L);
   if (st != WM_OK) return st;
   if ((st = check_packed(L, packed)) != WM_OK) return st;
-  if (L.N > 0) return fail(WM_ERR_UNSUPPORTED, "wm_controller_step: the two-level controller runs in rollouts only");
   if (B <= 0) return fail(WM_ERR_INVALID_ARG, "B=%d must be positive", B);
+  if (L.N > 0 && !probs)
+    return fail(WM_ERR_INVALID_ARG, "the two-level controller step needs probs [B, N+1+L] (it holds the logits)");
   if (!z || !h || !valid_mask || !action)
     return fail(WM_ERR_INVALID_ARG, "z, h, valid_mask and action are required");
   if (!aligned16(z) || !aligned16(h)) return fail(WM_ERR_INVALID_ARG, "z and h must be 16-byte aligned");

@@ -35,6 +35,7 @@ struct RolloutBufs {
   float* c;            // [B, H]
   int32_t* done_state; // [B]
   float* P;            // [32, B, Nc] controller partial logits (persistent kernel) or null
+  float* lg;           // [B, Nc] logits of a wide two-level controller, or null
   unsigned* sync;      // kSyncWords barrier and status words, at workspace offset 0
   unsigned preset_err; // initial value of the error word (WM_FLAG_TEST_ABORT)
 };

@@ -944,10 +944,16 @@ struct CtrlArgs {
   // per-trajectory horizons (null: T for all): a step t >= lengths[m] is padding
   const int32_t* lengths;
   int t;
-  // two-level controller (N > 0, rollout modes): mask holds the xfer masks
-  // [M, N+1] followed by the location masks [M, N, Lc]; the logits are the
-  // N+1 xfer rows then the Lc location rows
+  // two-level controller (N > 0): mask holds the xfer masks [M, N+1]
+  // followed by the location masks [M, N, Lc]; the logits are the N+1 xfer
+  // rows then the Lc location rows
   int N, Lc;
+  // logits stored instead of picked (k_ctrl_wide): columns [0, ncol) of each
+  // row, bias not added, at logits_out + m ldl; k_ctrl_rows then picks
+  float* logits_out;
+  long ldl;
+  int ncol;
+  float* lg_ws;  // rollout workspace [M, Nc] for those logits (wide two-level controllers)
 };
 
 // Rollout bookkeeping of row m at step t (modes 1 and 2 of the controller
@@ -987,21 +993,25 @@ __device__ __forceinline__ void ctrl_row_commit(const CtrlArgs& p, const Rng& rn
 // Two-level pick of row m (section 3.1.3) by its TPR threads (thread q of
 // the row), from its logits lg (bias not yet added): an xfer among the valid
 // ones (stream 0, index x; x = N is the NO-OP), then a location valid for
-// that xfer (stream 4, index l).  Returns the flat action x Lc + l, -2 for
-// the NO-OP, -1 when nothing is valid; the same value in every thread of the
-// row.  Ties go to the lowest index.
+// that xfer (stream 4, index l).  two_level_xfer returns x (-1 when none is
+// valid), two_level_loc the location of xfer x < N (-1 when none is valid),
+// two_level_pick the flat action x Lc + l, -2 for the NO-OP, -1 when nothing
+// is valid; the same value in every thread of the row.  Ties go to the
+// lowest index.  LMAX bounds Lc.
 template <int TPR>
-__device__ __forceinline__ int two_level_pick(const CtrlArgs& p, const Rng& rng, const float* lg,
-                                              int m, bool on, int q, uint32_t traj) {
-  const int N = p.N, NX = N + 1, Lc = p.Lc;
-  auto reduce = [](float& best, int& bidx) {
+__device__ __forceinline__ void row_argmax(float& best, int& bidx) {
 #pragma unroll
-    for (int off = 1; off < TPR; off <<= 1) {
-      const float ob = __shfl_xor(best, off);
-      const int oi = __shfl_xor(bidx, off);
-      if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
-    }
-  };
+  for (int off = 1; off < TPR; off <<= 1) {
+    const float ob = __shfl_xor(best, off);
+    const int oi = __shfl_xor(bidx, off);
+    if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) { best = ob; bidx = oi; }
+  }
+}
+
+template <int TPR>
+__device__ __forceinline__ int two_level_xfer(const CtrlArgs& p, const Rng& rng, const float* lg, int m,
+                                              bool on, int q, uint32_t traj) {
+  const int NX = p.N + 1;
   float best = -INFINITY;
   int x = -1;
   if (on) {
@@ -1012,15 +1022,19 @@ __device__ __forceinline__ int two_level_pick(const CtrlArgs& p, const Rng& rng,
       if (sc > best) { best = sc; x = i; }
     }
   }
-  reduce(best, x);
-  if (x < 0) return -1;
-  if (x == N) return -2;
+  row_argmax<TPR>(best, x);
+  return x;
+}
+
+template <int TPR, int LMAX>
+__device__ __forceinline__ int two_level_loc(const CtrlArgs& p, const Rng& rng, const float* lg, int m,
+                                             bool on, int q, uint32_t traj, int x) {
+  const int N = p.N, NX = N + 1, Lc = p.Lc;
   const uint8_t* lm = p.mask + (long)p.M * NX + ((long)m * N + x) * Lc;
   // thread q takes the contiguous locations [l0, l1) (a multiple of four:
   // one Philox block each); their mask bytes are all loaded before the
   // first is used, instead of one dependent load per location
-  // (Lc <= 316: N + 1 + Lc logits at most 318 with N >= 1)
-  constexpr int MAXW = (((316 + TPR - 1) / TPR + 3) & ~3) / 4;
+  constexpr int MAXW = (((LMAX + TPR - 1) / TPR + 3) & ~3) / 4;
   const int cpt = ((Lc + TPR - 1) / TPR + 3) & ~3;
   const int l0 = q * cpt, l1 = min(l0 + cpt, Lc);
   uint32_t mw[MAXW];
@@ -1034,7 +1048,7 @@ __device__ __forceinline__ int two_level_pick(const CtrlArgs& p, const Rng& rng,
     }
     mw[k] = wv;
   }
-  best = -INFINITY;
+  float best = -INFINITY;
   int l = -1;
 #pragma unroll
   for (int k = 0; k < MAXW; ++k) {
@@ -1049,8 +1063,95 @@ __device__ __forceinline__ int two_level_pick(const CtrlArgs& p, const Rng& rng,
       }
     }
   }
-  reduce(best, l);
-  return l < 0 ? -1 : x * Lc + l;
+  row_argmax<TPR>(best, l);
+  return l;
+}
+
+template <int TPR, int LMAX = 316>
+__device__ __forceinline__ int two_level_pick(const CtrlArgs& p, const Rng& rng, const float* lg,
+                                              int m, bool on, int q, uint32_t traj) {
+  const int x = two_level_xfer<TPR>(p, rng, lg, m, on, q, traj);
+  if (x < 0) return -1;
+  if (x == p.N) return -2;
+  const int l = two_level_loc<TPR, LMAX>(p, rng, lg, m, on, q, traj, x);
+  return l < 0 ? -1 : x * p.Lc + l;
+}
+
+// The two-level controller from stored logits (k_ctrl_wide with logits_out),
+// one wave per row, for controllers too wide for the staged tiles and for
+// the controller step.  Rollout modes: the pick and the row's commit (the
+// reward and done logits are columns Ac, Ac + 1).  Mode 0: the action and,
+// over the row's logits in place, the probabilities: the softmax of the
+// valid xfers' logits [N+1], then the softmax of the valid locations of the
+// picked xfer [Lc] (0 after a NO-OP or when nothing is valid).
+constexpr int kRowsMax = 1024;  // N + 1 and Lc at most this
+__global__ void __launch_bounds__(256) k_ctrl_rows(const CtrlArgs p) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (m >= p.M) return;  // the whole wave
+  float* lg = p.logits_out + (long)m * p.ldl;
+  const Rng rng{p.k0, p.k1};
+  const uint32_t traj = p.traj0 + (uint32_t)m;
+  const int N = p.N, NX = N + 1, Lc = p.Lc;
+  if (p.mode != 0) {
+    int a = -1;
+    if (p.mode == 1) {
+      const int x = two_level_xfer<64>(p, rng, lg, m, true, lane, traj);
+      if (x == N) a = -2;
+      else if (x >= 0) {
+        const int l = two_level_loc<64, kRowsMax>(p, rng, lg, m, true, lane, traj, x);
+        a = l < 0 ? -1 : x * Lc + l;
+      }
+    }
+    const int Ar = NX + Lc;
+    if (lane == 0) ctrl_row_commit(p, rng, m, a, lg[Ar] + p.bc[Ar], lg[Ar + 1] + p.bc[Ar + 1]);
+    return;
+  }
+  const int x = two_level_xfer<64>(p, rng, lg, m, true, lane, traj);
+  const bool locs = x >= 0 && x < N;
+  const int l = locs ? two_level_loc<64, kRowsMax>(p, rng, lg, m, true, lane, traj, x) : -1;
+  const int a = x < 0 ? -1 : x == N ? -2 : l < 0 ? -1 : x * Lc + l;
+  // every logit this lane needs, read before any probability is written
+  constexpr int PER = kRowsMax / 64;
+  const uint8_t* lm = p.mask + (long)p.M * NX + ((long)m * N + (locs ? x : 0)) * Lc;
+  float vx[PER], vl[PER];
+  float mxx = -INFINITY, mxl = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int i = lane + 64 * k;
+    const bool okx = i < NX && p.mask[(long)m * NX + i];
+    vx[k] = okx ? lg[i] + p.bc[i] : -INFINITY;
+    mxx = fmaxf(mxx, vx[k]);
+    const bool okl = locs && i < Lc && lm[i];
+    vl[k] = okl ? lg[NX + i] + p.bc[NX + i] : -INFINITY;
+    mxl = fmaxf(mxl, vl[k]);
+  }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    mxx = fmaxf(mxx, __shfl_xor(mxx, off));
+    mxl = fmaxf(mxl, __shfl_xor(mxl, off));
+  }
+  float sx = 0.f, sl = 0.f;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    vx[k] = vx[k] == -INFINITY ? 0.f : expf(vx[k] - mxx);
+    vl[k] = vl[k] == -INFINITY ? 0.f : expf(vl[k] - mxl);
+    sx += vx[k];
+    sl += vl[k];
+  }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    sx += __shfl_xor(sx, off);
+    sl += __shfl_xor(sl, off);
+  }
+  const float ix = sx > 0.f ? 1.0f / sx : 0.f, il = sl > 0.f ? 1.0f / sl : 0.f;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int i = lane + 64 * k;
+    if (i < NX) lg[i] = vx[k] * ix;
+    if (i < Lc) lg[NX + i] = vl[k] * il;
+  }
+  if (lane == 0) p.action[m] = a;
 }
 
 // Activation source of the controller kernels for rows m0 .. m0+rows-1.
@@ -1134,6 +1235,23 @@ __global__ void __launch_bounds__(256) k_ctrl_wide(const CtrlArgs p) {
   }
 
   // ---- epilogue ----
+  if (p.logits_out) {  // logits only (bias not added); k_ctrl_rows picks
+#pragma unroll
+    for (int j = 0; j < MBW; ++j) {
+      const int m = m0 + j * 16 + r16;
+      if (m >= p.M) continue;
+#pragma unroll
+      for (int i = 0; i < NBW; ++i) {
+        const int nb = wave + 4 * i;
+        const int n = nb * 16 + 4 * g;
+        if (nb >= nbtot) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (n + v < p.ncol) p.logits_out[(long)m * p.ldl + n + v] = acc[i][j][v];
+      }
+    }
+    return;
+  }
   const Rng rng{p.k0, p.k1};
   const int A = p.A;
   const bool want_action = p.mode != 2;
@@ -2016,7 +2134,27 @@ hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
   using DT = typename S::DT;
   using Cf = Cfgs<DT>;
   const int nbtot = a.Nc / 16;
-  // (the two-level controller runs on the kernels that stage whole logit rows)
+  const int nbw = (nbtot + 3) / 4;  // output blocks per wave over four waves
+  // the two-level controller of the controller step, and in rollouts where
+  // its logit rows do not fit the staged tiles: the logits are stored (into
+  // probs for the step, the workspace in a rollout), then picked per row
+  if (a.N > 0 && (a.mode == 0 || nbw > 5)) {
+    CtrlArgs g = a;
+    g.logits_out = a.mode == 0 ? a.probs : a.lg_ws;
+    g.ldl = a.mode == 0 ? a.N + 1 + a.Lc : a.Nc;
+    g.ncol = a.mode == 0 ? a.N + 1 + a.Lc : a.Nc;
+    if (!g.logits_out) return hipErrorInvalidValue;
+    hipError_t e;
+    if (nbw <= 8) e = launch_ctrl_wide<S, 8, 2>(g, s);
+    else if (nbw <= 12) e = launch_ctrl_wide<S, 12, 2>(g, s);
+    else if (nbw <= 17) e = launch_ctrl_wide<S, 17, 1>(g, s);
+    else if (nbw <= 24) e = launch_ctrl_wide<S, 24, 1>(g, s);
+    else if (nbw <= 33) e = launch_ctrl_wide<S, 33, 1>(g, s);
+    else return hipErrorInvalidValue;
+    if (e != hipSuccess) return e;
+    return launch("ctrl", k_ctrl_rows, dim3((unsigned)((a.M + 3) / 4)), dim3(256), 0, s, g);
+  }
+  // (otherwise the two-level controller runs on the kernels that stage whole logit rows)
   if (a.M <= WM_RD_CTRL_ROWS && nbtot <= 9 && a.N == 0) {
     const int nb = nbtot <= 1 ? 1 : nbtot <= 2 ? 2 : nbtot <= 3 ? 3 : nbtot <= 5 ? 5 : 9;
     const int smax = nb <= 5 ? 8 : 4;  // register budget
@@ -2031,7 +2169,7 @@ hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
       }
     }
   }
-  const int nb = (nbtot + 3) / 4;  // output blocks per wave over four waves
+  const int nb = nbw;
   if constexpr (S::kTwo) {
     if (nb <= 1) return launch_ctrl_cfg<typename Cf::template CtrlLarge<1>, S>(a, s);
     if (nb <= 2) return launch_ctrl_cfg<typename Cf::template CtrlLarge<2>, S>(a, s);
@@ -2145,6 +2283,7 @@ hipError_t rollout_impl(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   ca.done_state = R.done_state;
   ca.use_done = (R.flags & WM_FLAG_DONE) != 0;
   ca.lengths = R.lengths;
+  ca.lg_ws = R.lg;
   ca.N = L.N;
   ca.Lc = L.Lc;
 
@@ -2279,7 +2418,12 @@ size_t rollout_workspace(const Layout& L, int B, char* ws, RolloutBufs* R) {
   const size_t pb = persist_partial_bytes(L, B);
   const size_t op = o;
   o = wm_align256(o + pb);  // persistent-kernel controller partials
+  // logits of a two-level controller too wide for the staged tiles
+  const bool wide2 = L.N > 0 && (L.Nc / 16 + 3) / 4 > 5;
+  const size_t og = o;
+  if (wide2) o = wm_align256(o + (size_t)B * L.Nc * 4);
   if (ws && R) {
+    R->lg = wide2 ? reinterpret_cast<float*>(ws + og) : nullptr;
     R->x = ws + ox;
     R->c = reinterpret_cast<float*>(ws + oc);
     R->done_state = reinterpret_cast<int32_t*>(ws + od);
@@ -2361,6 +2505,8 @@ hipError_t launch_controller_step(const Packed& P, int B, uint32_t traj0, const 
   ca.mode = 0;
   ca.probs = probs;
   ca.action = action;
+  ca.N = L.N;
+  ca.Lc = L.Lc;
   if (L.dt == 0) return launch_ctrl<SrcZH<float>>(ca, s);
   return launch_ctrl<SrcZH<bf16_t>>(ca, s);
 }

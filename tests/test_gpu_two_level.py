@@ -1,8 +1,13 @@
 """GPU parity of the two-level controller (section 3.1.3: an xfer, index N
-the NO-OP, then a location valid for it) in dream rollouts, through the C
-ABI, against the oracle re-anchored per step; plus the validity of every
-action under the masks and the NO-OP ending its trajectory."""
+the NO-OP, then a location valid for it) in dream rollouts and in the
+controller step, through the C ABI, against the oracle (re-anchored per step
+in rollouts); plus the validity of every action under the masks and the
+NO-OP ending its trajectory.  Sizes include the paper's action spaces
+(Table 1: 40 to 288 substitutions, at most 200 locations): N = 80 (BERT,
+A = 16000) on the staged controller tiles and N = 288 (SqueezeNet1.1,
+A = 57600, 489 controller logits) on the stored-logit path."""
 
+import ctypes
 import sys
 
 import numpy as np
@@ -10,6 +15,7 @@ import pytest
 import torch
 
 import parity
+from oracle import wm as owm
 from paper_2205_01435_amd import _lib as wmlib
 from paper_2205_01435_amd import workloads as wl
 
@@ -57,6 +63,9 @@ CASES = [
     (37, 5, 16, 128, 4, 20, 3, "fp32", None),
     (300, 3, 32, 256, 8, 50, 5, "bf16", None),
     (4096 + 3, 2, 64, 512, 10, 200, 5, "bf16", 40),  # 2000 actions, 211 controller logits
+    (70, 4, 32, 256, 80, 200, 8, "fp32", None),      # BERT's 80 xfers: A = 16000
+    (70, 4, 32, 256, 288, 200, 8, "fp32", None),     # SqueezeNet1.1's 288: A = 57600, 489 logits
+    (1027, 3, 64, 512, 288, 200, 8, "bf16", 48),
 ]
 
 
@@ -76,7 +85,8 @@ def test_two_level_rollout(B, T, Z, H, N, L, K, dtype, nrows):
     finally:
         wmlib.profile_enable(None)
         wmlib.profile_reset()
-    assert n_persist == 0 and n_ctrl == T + 1, "the two-level controller runs on the multi-launch path"
+    wide = (N + 1 + L + 2 + 15) // 16 > 20  # logits stored, then picked: two launches per step
+    assert n_persist == 0 and n_ctrl == (T + 1) * (2 if wide else 1), "the multi-launch path runs"
     acts = b.actions.cpu().numpy()
     tt, bb = np.nonzero(acts >= 0)
     x, loc = acts[tt, bb] // L, acts[tt, bb] % L
@@ -99,7 +109,49 @@ def test_two_level_argument_errors():
     with pytest.raises(wmlib.WmError):
         wmlib.pack(w, 16, 128, 81, 3, "fp32", N=4, L=20)  # A != N L
     m = wmlib.pack(w, 16, 128, 80, 3, "fp32", N=4, L=20)
-    with pytest.raises(wmlib.WmError):  # the controller step serves the one-level controller only
-        wmlib.controller_step(m, _t(z0), torch.zeros((8, 128), device="cuda"), _t(xm), seed=1, step=0)
+    with pytest.raises(ValueError):  # the two-level step takes the (xfer, location) mask pair
+        wmlib.controller_step(m, _t(z0), torch.zeros((8, 128), device="cuda"), (_t(xm), _t(lm[:, :3])),
+                              seed=1, step=0)
     with pytest.raises(ValueError):
         wmlib.rollout(m, _t(z0), (_t(xm), _t(lm[:, :3])), T=2, seed=1)
+    # the step's probs hold the logits: required through the C ABI
+    lib = wmlib.load()
+    fake = torch.zeros(64, dtype=torch.float32, device="cuda")
+    st = lib.wm_controller_step(ctypes.byref(m.dims), wmlib._ptr(m.packed), 8, 0, wmlib._ptr(fake),
+                                wmlib._ptr(fake), wmlib._ptr(fake), 1, 0, None, wmlib._ptr(fake), None)
+    assert st == wmlib.WM_ERR_INVALID_ARG
+    # limits: N + 1 and L at most 1024; the one-hot block under 2 GiB
+    for dims in ((8, 16, 1100, 2, "fp32", 1100, 1), (8, 16, 1025, 2, "fp32", 1, 1025),
+                 (8, 8192, 20000, 2, "fp32", 100, 200)):
+        assert wmlib.packed_bytes(wmlib.make_dims(*dims)) == 0
+    assert wmlib.packed_bytes(wmlib.make_dims(8, 1024, 57600, 2, "bf16", 288, 200)) > 57600 * 4096 * 2
+
+
+@pytest.mark.parametrize("B,Z,H,N,L,dtype", [(50, 16, 128, 4, 20, "fp32"), (100, 32, 256, 288, 200, "fp32"),
+                                             (333, 64, 512, 80, 200, "bf16"),
+                                             (200, 64, 512, 288, 200, "bf16")])
+def test_two_level_controller_step(B, Z, H, N, L, dtype):
+    """wm_controller_step with the two-level controller: the action (exact up
+    to near-ties) and the factored probabilities against the oracle."""
+    say("two-level controller step", B, Z, H, N, L, dtype)
+    K = 2
+    w, z0, xm, lm = _inputs(B, 3, Z, H, N, L, K, seed=B + L)
+    rng = np.random.default_rng(B)
+    h = np.tanh(rng.standard_normal((B, H))).astype(np.float32)
+    m = wmlib.pack(w, Z, H, N * L, K, dtype, N=N, L=L)
+    probs, act = wmlib.controller_step(m, _t(z0), _t(h), (_t(xm), _t(lm)), seed=5, step=7, traj0=11)
+    torch.cuda.synchronize()
+    ref = owm.controller_step(w, dict(Z=Z, H=H, A=N * L, K=K), z0, h, (xm, lm), seed=5, step=7, traj0=11,
+                              dtype=dtype, two_level=(N, L))
+    a = act.cpu().numpy()
+    p = probs.cpu().numpy()
+    diff = a != ref["action"]
+    eps = parity.EPS_TIE[dtype]
+    assert np.all(ref["margin"][diff] < eps * (1 + np.abs(ref["top"][diff]))), "non-tie mismatch"
+    assert diff.sum() <= 1e-3 * B
+    same = ~diff
+    parity.close(p[same], ref["probs"][same], parity.RTOL[dtype], "two-level probs")
+    assert np.all(p[:, :N + 1][xm == 0] == 0)
+    assert a[B // 4] == -2 and np.all(p[B // 4, N + 1:] == 0)
+    ok = a >= 0
+    assert np.all(xm[ok, a[ok] // L] == 1) and np.all(lm[ok, a[ok] // L, a[ok] % L] == 1)
