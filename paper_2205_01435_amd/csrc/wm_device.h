@@ -22,26 +22,32 @@ namespace wm {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint16_t bf16_t;  // storage type of bfloat16 values
 
 // ---------------------------------------------------------------------------
-// bfloat16 storage: round to nearest, ties to even; NaN stays NaN.
+// bfloat16 storage: round to nearest, ties to even; NaN stays NaN.  gfx950
+// converts in hardware (v_cvt_pk_bf16_f32, two values per instruction).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-  uint32_t b = __float_as_uint(f);
-  if ((b & 0x7fffffffu) > 0x7f800000u) return (b >> 16) | 0x40u;
-  b += 0x7fffu + ((b >> 16) & 1u);
-  return b >> 16;
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+// (bits of a) | (bits of b) << 16
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+  bf16x2 v;
+  v[0] = (__bf16)a;
+  v[1] = (__bf16)b;
+  return __builtin_bit_cast(uint32_t, v);
 }
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
 __device__ __forceinline__ float round_bf16(float f) { return bf16_bits_to_f32(f32_to_bf16_bits(f)); }
 
 __device__ __forceinline__ uint4 pack8_bf16(float4 a, float4 b) {
   uint4 r;
-  r.x = f32_to_bf16_bits(a.x) | (f32_to_bf16_bits(a.y) << 16);
-  r.y = f32_to_bf16_bits(a.z) | (f32_to_bf16_bits(a.w) << 16);
-  r.z = f32_to_bf16_bits(b.x) | (f32_to_bf16_bits(b.y) << 16);
-  r.w = f32_to_bf16_bits(b.z) | (f32_to_bf16_bits(b.w) << 16);
+  r.x = pack2_bf16(a.x, a.y);
+  r.y = pack2_bf16(a.z, a.w);
+  r.z = pack2_bf16(b.x, b.y);
+  r.w = pack2_bf16(b.z, b.w);
   return r;
 }
 
@@ -128,6 +134,34 @@ __device__ __forceinline__ float ftanh(float x) {
 __device__ __forceinline__ float ftanh_abs(float x) {
   return 1.0f - 2.0f * frcp(1.0f + __builtin_amdgcn_exp2f(x * 2.88539008177792681f));
 }
+// LSTM cell of the bf16 kernels: c' = sigmoid(f) c + sigmoid(i) tanh(g) and
+// h' = sigmoid(o) tanh(c'), each written over one common denominator:
+//   c' = (c (1 + Ei)(1 + G) + (1 - G)(1 + Ef)) / ((1 + Ef)(1 + Ei)(1 + G)),
+//   h' = (1 - C) / ((1 + Eo)(1 + C)),
+// with Ex = exp(-x) for the sigmoids, G = exp(-2g) and C = exp(-2c') for the
+// tanhs: five exponentials and two reciprocals instead of five and five.
+// Pre-activations and c' are clamped to +-15 first, where the sigmoid and
+// tanh are within 3.1e-7 of their limits, so that the products stay finite;
+// the result is within about 1e-6 of the separate functions (h is rounded to
+// bf16, relative step 2^-9, right after).
+constexpr float kCellClamp = 15.0f;
+__device__ __forceinline__ void lstm_cell_fused(float pi, float pf, float pg, float po, float c,
+                                                float& cn, float& hn) {
+  constexpr float L2E = 1.44269504088896341f;
+  const float xi = __builtin_amdgcn_fmed3f(pi, -kCellClamp, kCellClamp);
+  const float xf = __builtin_amdgcn_fmed3f(pf, -kCellClamp, kCellClamp);
+  const float xg = __builtin_amdgcn_fmed3f(pg, -kCellClamp, kCellClamp);
+  const float xo = __builtin_amdgcn_fmed3f(po, -kCellClamp, kCellClamp);
+  const float ai = 1.0f + __builtin_amdgcn_exp2f(xi * -L2E);
+  const float af = 1.0f + __builtin_amdgcn_exp2f(xf * -L2E);
+  const float ao = 1.0f + __builtin_amdgcn_exp2f(xo * -L2E);
+  const float G = __builtin_amdgcn_exp2f(xg * (-2.0f * L2E));
+  const float d1 = ai * (1.0f + G);
+  cn = __builtin_fmaf(c, d1, (1.0f - G) * af) * frcp(af * d1);
+  const float C = __builtin_amdgcn_exp2f(__builtin_amdgcn_fmed3f(cn, -kCellClamp, kCellClamp) * (-2.0f * L2E));
+  hn = (1.0f - C) * frcp(ao * (1.0f + C));
+}
+
 // the cell's tanh for activation type DT
 template <typename DT>
 __device__ __forceinline__ float ftanh_cell(float x) {

@@ -528,12 +528,13 @@ struct Gate4IO {
   rsrc_t rc, rxi, rxo, rw, rb, rht, rct;
   int H, A;
   uint32_t ldxb;
-  bool nll;
+  bool nll, trace;
 
   __device__ Gate4IO(const GatesArgs& p, int m0, int rows) {
     H = p.H;
     A = p.A;
     nll = p.nll_mode != 0;
+    trace = p.h_trace != nullptr;
     const long mval = max(0, min(rows, p.M - m0));
     const uint32_t hb = (uint32_t)(mval * H * 4);
     ldxb = (uint32_t)(p.ldx * (long)sizeof(DT));
@@ -598,26 +599,36 @@ struct Gate4IO {
     const float hin[4] = {in.hprev.x, in.hprev.y, in.hprev.z, in.hprev.w};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const float cn = fsigmoid(g[t].y + in.add[t].y) * cin[t] +
-                       fsigmoid(g[t].x + in.add[t].x) * ftanh_cell<DT>(g[t].z + in.add[t].z);
-      const float hn = DType<DT>::round(fsigmoid(g[t].w + in.add[t].w) * ftanh_cell<DT>(cn));
+      float cn, hn;
+      if constexpr (sizeof(DT) == 4) {
+        cn = fsigmoid(g[t].y + in.add[t].y) * cin[t] + fsigmoid(g[t].x + in.add[t].x) * ftanh(g[t].z + in.add[t].z);
+        hn = fsigmoid(g[t].w + in.add[t].w) * ftanh(cn);
+      } else {
+        lstm_cell_fused(g[t].x + in.add[t].x, g[t].y + in.add[t].y, g[t].z + in.add[t].z, g[t].w + in.add[t].w,
+                        cin[t], cn, hn);
+      }
       cv[t] = in.live ? cn : cin[t];
       hv[t] = in.live ? hn : hin[t];
     }
     const uint32_t ec = ((uint32_t)ml * H + u0) * 4u;
     const uint32_t ex = (uint32_t)ml * ldxb + (uint32_t)u0 * (uint32_t)sizeof(DT);
     const float4 c4 = make_float4(cv[0], cv[1], cv[2], cv[3]);
-    const float4 h4 = make_float4(hv[0], hv[1], hv[2], hv[3]);
     bstore16(rc, ok && in.live ? ec : kOffNone, as_uint4(c4));
+    float4 h4;
     if constexpr (sizeof(DT) == 4) {
+      h4 = make_float4(hv[0], hv[1], hv[2], hv[3]);
       bstore16(rxo, ok ? ex : kOffNone, as_uint4(h4));
     } else {
-      bstore8(rxo, ok ? ex : kOffNone,
-              make_uint2(f32_to_bf16_bits(hv[0]) | (f32_to_bf16_bits(hv[1]) << 16),
-                         f32_to_bf16_bits(hv[2]) | (f32_to_bf16_bits(hv[3]) << 16)));
+      // h is stored rounded (a frozen row's h_t is already a bf16 value)
+      const uint2 hb = make_uint2(pack2_bf16(hv[0], hv[1]), pack2_bf16(hv[2], hv[3]));
+      bstore8(rxo, ok ? ex : kOffNone, hb);
+      h4 = make_float4(bf16_bits_to_f32(hb.x & 0xffffu), bf16_bits_to_f32(hb.x >> 16),
+                       bf16_bits_to_f32(hb.y & 0xffffu), bf16_bits_to_f32(hb.y >> 16));
     }
-    bstore16(rht, ok ? ec : kOffNone, as_uint4(h4));  // dropped without traces
-    bstore16(rct, ok ? ec : kOffNone, as_uint4(c4));
+    if (trace) {
+      bstore16(rht, ok ? ec : kOffNone, as_uint4(h4));
+      bstore16(rct, ok ? ec : kOffNone, as_uint4(c4));
+    }
   }
 };
 
@@ -665,9 +676,24 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
   const bool uok = u0 < p.H;  // H % 16 == 0: the whole group is inside
   float4 b[4];
   io.bias(u0, uok, b);
+  // each pass's loads go out before its staging barrier, so that their
+  // latency passes under the staging
+  Gate4In in[IPT];
+  auto load_pass = [&](int ps) {
+    const int rp = ps * PROWS;  // first tile row of the pass
+#pragma unroll
+    for (int k = 0; k < IPT; ++k) {
+      const int r = r0 + k * RSTEP;
+      in[k] = io.load(rp + r, u0, act[ps][k], uok && r < PROWS && m0 + rp + r < p.M, b);
+    }
+  };
+  load_pass(0);
 #pragma unroll
   for (int ps = 0; ps < NPASS; ++ps) {
-    if (ps > 0) __syncthreads();  // the previous pass has read E
+    if (ps > 0) {
+      load_pass(ps);
+      __syncthreads();  // the previous pass has read E
+    }
     if (C::kw() == 0 && (NPASS == 1 || C::wm() == ps)) {
       const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
       const int wn = C::wn(), wmi = NPASS == 1 ? C::wm() : 0;
@@ -681,12 +707,6 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
     __syncthreads();
 
     const int rp = ps * PROWS;  // first tile row of the pass
-    Gate4In in[IPT];
-#pragma unroll
-    for (int k = 0; k < IPT; ++k) {
-      const int r = r0 + k * RSTEP;
-      in[k] = io.load(rp + r, u0, act[ps][k], uok && r < PROWS && m0 + rp + r < p.M, b);
-    }
 #pragma unroll
     for (int k = 0; k < IPT; ++k) {
       const int r = r0 + k * RSTEP;
