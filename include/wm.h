@@ -143,8 +143,9 @@ wm_status wm_pack_weights(const wm_dims *dims, const wm_weights *canon, void *pa
 
 /* Workspace bytes needed by wm_rollout (which = 0), wm_nll (which = 1),
  * wm_controller_step (which = 2: it takes no workspace, so 0) or wm_nll_grad
- * (which = 3) for B rows and T steps.  0 on bad args.  Every workspace
- * starts with the status words that wm_workspace_status reads. */
+ * (which = 3) for B rows and T steps.  0 on bad args and on sizes the call
+ * refuses.  Every workspace starts with the status words that
+ * wm_workspace_status reads. */
 size_t wm_workspace_bytes(const wm_dims *dims, int32_t B, int32_t T, int32_t which);
 
 /*

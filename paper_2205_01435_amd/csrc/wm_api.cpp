@@ -184,6 +184,9 @@ size_t wm_packed_weights_bytes(const wm_dims* dims) {
 size_t wm_workspace_bytes(const wm_dims* dims, int32_t B, int32_t T, int32_t which) {
   wm::Layout L;
   if (check_dims(dims, &L) != WM_OK || B <= 0 || T < 0) return 0;
+  // sizes the calls refuse need no workspace (and would overflow the sums)
+  if ((int64_t)B * (T + 1) > (int64_t)1 << 30) return 0;
+  if (which == 3 && (int64_t)B * T > (int64_t)1 << 22) return 0;
   if (which == 0) return wm::rollout_workspace(L, B, nullptr, nullptr);
   if (which == 1) return wm::nll_workspace(L, B, T, nullptr, nullptr);
   if (which == 2) return 0;  // wm_controller_step takes no workspace
