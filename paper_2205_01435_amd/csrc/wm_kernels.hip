@@ -1949,19 +1949,16 @@ namespace {
 // (MFMA-bound: more reuse per LDS byte).
 constexpr int kSmallRows = 2048;
 
-#ifndef WM_MDN_LARGE_F32_MBW
-#define WM_MDN_LARGE_F32_MBW 1
-#endif
 
 template <typename DT> struct Cfgs;
 template <> struct Cfgs<float> {
   using GatesSmall = Gemm<float, 2, 1, 2, 2, 1, 32, 4>;  // 64 x 32
   using GatesLarge = GemmD<float, 4, 2, 2, 2, 2>;  // 128 x 64
   using GatesXL = GatesLarge;
-  template <int Q> using MdnXL = GemmD<float, Q, WM_MDN_LARGE_F32_MBW, 2, 2, 2>;
+  template <int Q> using MdnXL = GemmD<float, Q, 1, 2, 2, 2>;
   static constexpr bool kXL = false;  // fp32 calls this large take the 128 x 64 tiles
   template <int Q> using MdnSmall = Gemm<float, Q, 1, 2, 1, 2, 32, 4>;  // 32Q x 16, K split 2
-  template <int Q> using MdnLarge = GemmD<float, Q, WM_MDN_LARGE_F32_MBW, 2, 2, 2>;
+  template <int Q> using MdnLarge = GemmD<float, Q, 1, 2, 2, 2>;
   template <int NB> using CtrlLarge = Gemm<float, NB, 4, 4, 1, 1, 32, 3>;  // 64NB x 64
   template <int NB> using CtrlLargeX = GemmD<float, NB, 2, 4, 1, 3>;      // 64NB x 32
   template <int NB> using CtrlXL = CtrlLargeX<NB>;
@@ -1987,22 +1984,11 @@ template <> struct Cfgs<bf16_t> {
 };
 
 // The 256-row tiles serve calls that still give every CU at least one tile.
-#ifndef WM_XL_TILES
-#define WM_XL_TILES 256
-#endif
-constexpr long kXLTiles = WM_XL_TILES;
+constexpr long kXLTiles = 256;
 
 // Register-direct kernels serve calls with at most this many rows, when the
 // K slices fit SMAX per wave on the compiled block size.
-#ifndef WM_RD_GATES_ROWS
-#define WM_RD_GATES_ROWS 256
-#endif
-#ifndef WM_RD_MDN_ROWS
-#define WM_RD_MDN_ROWS 1024
-#endif
-#ifndef WM_RD_CTRL_ROWS
-#define WM_RD_CTRL_ROWS 1024
-#endif
+constexpr int kRdGatesRows = 256, kRdMdnRows = 1024, kRdCtrlRows = 1024;
 constexpr size_t kRdLdsMax = 64 * 1024;
 
 inline int rd_waves(int Kpad, int kslice, int smax, int min_waves) {
@@ -2020,10 +2006,7 @@ hipError_t allow_lds(F* kernel, size_t bytes) {
 }
 
 // Weight bytes an XCD should keep in its L2 (4 MB) while activations stream.
-#ifndef WM_L2_BUDGET
-#define WM_L2_BUDGET (2560 * 1024)
-#endif
-constexpr size_t kL2Budget = WM_L2_BUDGET;
+constexpr size_t kL2Budget = 2560 * 1024;
 
 // Picks gn for nt x mt tiles over `wbytes` of weights: the weights' per-XCD
 // slice fits the L2 budget if possible, then the busiest XCD gets the fewest
@@ -2071,7 +2054,7 @@ hipError_t launch_gates_rd(GatesArgs a, hipStream_t s) {
 
 template <typename DT>
 hipError_t launch_gates(GatesArgs a, hipStream_t s) {
-  if (a.M <= WM_RD_GATES_ROWS) {
+  if (a.M <= kRdGatesRows) {
     // 16-row tiles for a single row block, 32-row tiles above
     const hipError_t e = a.M <= 16 ? launch_gates_rd<GemmRD<DT, 2, 1, 4, 640>, DT>(a, s)
                                    : launch_gates_rd<GemmRD<DT, 2, 2, 4, 640>, DT>(a, s);
@@ -2096,7 +2079,7 @@ hipError_t launch_mdn_q(const MdnArgs& a, int ntiles, hipStream_t s) {
     using R = GemmRD<DT, Q, 1, 4, 640>;  // 16-row tiles: more work-groups
     const int nw = rd_waves((int)a.ldh, R::KSLICE, R::SMAX, 4);
     const size_t lds = R::lds_bytes(nw);
-    if (a.M <= WM_RD_MDN_ROWS && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
+    if (a.M <= kRdMdnRows && 64 * nw <= R::MAXT && lds <= kRdLdsMax) {
       hipError_t e = allow_lds(k_mdn_rd<R>, lds);
       if (e != hipSuccess) return e;
       MdnArgs b = a;
@@ -2175,7 +2158,7 @@ hipError_t launch_ctrl(const CtrlArgs& a, hipStream_t s) {
     return launch("ctrl", k_ctrl_rows, dim3((unsigned)((a.M + 3) / 4)), dim3(256), 0, s, g);
   }
   // (otherwise the two-level controller runs on the kernels that stage whole logit rows)
-  if (a.M <= WM_RD_CTRL_ROWS && nbtot <= 9 && a.N == 0) {
+  if (a.M <= kRdCtrlRows && nbtot <= 9 && a.N == 0) {
     const int nb = nbtot <= 1 ? 1 : nbtot <= 2 ? 2 : nbtot <= 3 ? 3 : nbtot <= 5 ? 5 : 9;
     const int smax = nb <= 5 ? 8 : 4;  // register budget
     const int nw = rd_waves((int)a.ldk, Mfma<DT>::KSLICE, smax, 4);
@@ -2560,14 +2543,8 @@ hipError_t launch_nll(const Packed& P, const NllBufs& N, hipStream_t s) {
 // ===========================================================================
 namespace {
 
-#ifndef WM_GRAD_STAGES
-#define WM_GRAD_STAGES 2
-#endif
-#ifndef WM_BPTT_STAGES
-#define WM_BPTT_STAGES 2
-#endif
-using GradGemm = GemmD<float, 4, 2, 2, 2, WM_GRAD_STAGES>;   // 128 x 64 tiles: the products over all rows
-using GradGemmS = GemmD<float, 2, 2, 2, 2, WM_BPTT_STAGES>;  // 64 x 64 tiles: the per-step product dG_t . W_h
+using GradGemm = GemmD<float, 4, 2, 2, 2, 2>;   // 128 x 64 tiles: the products over all rows
+using GradGemmS = GemmD<float, 2, 2, 2, 2, 2>;  // 64 x 64 tiles: the per-step product dG_t . W_h
 
 // out[m][n] = sum_{k < Kpad} A[m][k] B[n][k] for m < M, n < N (Kpad a
 // multiple of 32; columns of A and B up to Kpad must be readable, zero
@@ -2928,29 +2905,21 @@ __global__ void __launch_bounds__(256) k_grad_unpack(const UnpackArgs p) {
   }
 }
 
-// K slices of an M x N x Kpad product: doubled (up to WM_GRAD_MAX_SPLIT)
-// while the tiles number under 512 and the 32-column chunks divide evenly
-#ifndef WM_GRAD_MAX_SPLIT
-#define WM_GRAD_MAX_SPLIT 8
-#endif
+// K slices of an M x N x Kpad product: doubled (up to kGradMaxSplit) while
+// the tiles number under 512 and the 32-column chunks divide evenly
+constexpr int kGradMaxSplit = 8;
 template <class C = GradGemm>
 int split_of(int M, int N, int Kpad, long target = 512) {
   const long tiles = (long)((N + C::BN - 1) / C::BN) * ((M + C::BM - 1) / C::BM);
   const int chunks = Kpad / 32;
   int S = 1;
-  while (S < WM_GRAD_MAX_SPLIT && tiles * S < target && chunks % (2 * S) == 0 && chunks / (2 * S) >= 4) S *= 2;
+  while (S < kGradMaxSplit && tiles * S < target && chunks % (2 * S) == 0 && chunks / (2 * S) >= 4) S *= 2;
   return S;
 }
 
 // the per-step product: its tile shape and K slices
-#ifndef WM_BPTT_TILE64
-#define WM_BPTT_TILE64 1
-#endif
-#ifndef WM_BPTT_TARGET
-#define WM_BPTT_TARGET 256
-#endif
-using BpttGemm = std::conditional_t<WM_BPTT_TILE64 != 0, GradGemmS, GradGemm>;
-int bptt_split(int B, int H) { return split_of<BpttGemm>(B, H, 4 * H, WM_BPTT_TARGET); }
+using BpttGemm = GradGemmS;
+int bptt_split(int B, int H) { return split_of<BpttGemm>(B, H, 4 * H, 256); }
 
 // out (ldo) = A . B^T in S K-slices; S > 1 writes slice y to out + y oslice
 template <class C = GradGemm>
