@@ -361,6 +361,34 @@ wm_status wm_profile_read(const char *prefix, double *total_ms, int64_t *launche
 wm_status wm_profile_reset(void);
 
 /*
+ * Phase timing of the persistent kernels (the small-batch fp32 rollout and
+ * NLL recurrence), for measurement runs: with on != 0, each later launch of
+ * those kernels stamps the device's constant-rate clock at its start, at
+ * every arrival at and release from an XCD barrier, and at its end (one
+ * lane per work-group; allocates a device buffer on first use and clears it
+ * with an asynchronous memset per launch, so leave it off under graph
+ * capture and in the no-allocation entry point; switching it on forgets the
+ * last stamped launch, switching it off keeps it readable).
+ * wm_profile_phases_read waits for the device and summarises the last
+ * stamped launch into out[0..n)
+ * (microseconds; "max" is over the 32 work-groups of an XCD, every figure
+ * is then averaged over the steps and the XCDs that hold rows):
+ *   out[0]  T (0: no stamped launch since wm_profile_phases)
+ *   out[1]  wall time per step
+ *   out[2], out[3]   ctrl(t): max work, then its barrier (last arrival to
+ *                    first release)
+ *   out[4], out[5]   gates(t): max work, barrier (NLL: the step's work and
+ *                    the barrier between steps)
+ *   out[6], out[7]   mdn(t): max work, barrier
+ *   out[8..10]       mean work of ctrl, gates, mdn
+ *   out[11], out[12] set-up before step 0 and the tail after the last step
+ *                    (max work)
+ * Rollout phases 2, 3, 6, 7 and 8, 10 are 0 for the NLL recurrence.
+ */
+wm_status wm_profile_phases(int32_t on);
+wm_status wm_profile_phases_read(double *out, int32_t n);
+
+/*
  * Device-side status of the last call that used `workspace` (a workspace of
  * wm_rollout, wm_nll or wm_nll_grad), after waiting for `stream`.  The
  * persistent kernels wait for each other at barriers with a bounded spin; a

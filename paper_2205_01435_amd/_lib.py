@@ -28,7 +28,8 @@ _DTYPES = {"fp32": WM_FP32, "bf16": WM_BF16}
 # Every symbol the C header declares.
 EXPORTS = ("wm_packed_weights_bytes", "wm_pack_weights", "wm_workspace_bytes", "wm_controller_step",
            "wm_rollout", "wm_rollout_noalloc", "wm_nll", "wm_nll_grad", "wm_returns", "wm_adam_step", "wm_poly_lr",
-           "wm_profile_enable", "wm_profile_read", "wm_profile_reset", "wm_workspace_status",
+           "wm_profile_enable", "wm_profile_read", "wm_profile_reset", "wm_profile_phases",
+           "wm_profile_phases_read", "wm_workspace_status",
            "wm_last_error", "wm_version")
 
 
@@ -95,6 +96,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wm_profile_read.restype = I32
     lib.wm_profile_reset.argtypes = []
     lib.wm_profile_reset.restype = I32
+    lib.wm_profile_phases.argtypes = [I32]
+    lib.wm_profile_phases.restype = I32
+    lib.wm_profile_phases_read.argtypes = [ctypes.POINTER(ctypes.c_double), I32]
+    lib.wm_profile_phases_read.restype = I32
     lib.wm_workspace_status.argtypes = [P, P]
     lib.wm_workspace_status.restype = I32
     lib.wm_last_error.argtypes = []
@@ -467,6 +472,22 @@ def profile_read(prefix: str | None = None) -> tuple[float, int]:
 
 def profile_reset():
     _check(load().wm_profile_reset())
+
+
+PHASE_SLOTS = ("T", "step", "ctrl", "ctrl_barrier", "gates", "gates_barrier", "mdn", "mdn_barrier",
+               "ctrl_mean", "gates_mean", "mdn_mean", "setup", "tail")
+
+
+def profile_phases(on: bool):
+    """Stamp the phase boundaries of later persistent-kernel launches."""
+    _check(load().wm_profile_phases(1 if on else 0))
+
+
+def profile_phases_read() -> dict:
+    """Per-step phase durations (us) of the last stamped launch, by slot."""
+    out = (ctypes.c_double * len(PHASE_SLOTS))()
+    _check(load().wm_profile_phases_read(out, len(PHASE_SLOTS)))
+    return dict(zip(PHASE_SLOTS, list(out)))
 
 
 def version() -> str:

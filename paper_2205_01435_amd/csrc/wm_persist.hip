@@ -83,6 +83,10 @@ struct PArgs {
   float* g_trace;            // NLL: gate activations [T, B, 4H] or null
   // LDS carve-up (bytes)
   int off_red, off_hb, off_wat, off_wcz, off_mdn, off_ctl, off_flags;
+  // phase timing (measurement runs; null otherwise): nst device-clock
+  // stamps per work-group, [blockIdx][nst]
+  unsigned long long* stamps;
+  int nst;
 };
 
 // sync words: group counters at 64*x, placement flags at 64*(8+x), error at 64*16
@@ -97,7 +101,20 @@ struct GroupSync {
   unsigned* err;
   unsigned n;  // barriers passed
   bool agent;  // members not all on one XCD: agent-scope fences
+  unsigned long long* st;  // this work-group's phase stamps, or null
+  int nst;
 };
+
+// Phase stamp i of this work-group: the constant-rate device clock, written
+// by the calling lane with a vector store.  Slot 0 is the kernel's start,
+// 2b-1 and 2b the arrival at and release from barrier b (1, 2, ...), nst-1
+// the end.
+__device__ __forceinline__ void phase_stamp(unsigned long long* st, int nst, int i) {
+  if (!st) return;
+  const unsigned long long v = __builtin_amdgcn_s_memrealtime();
+  const rsrc_t r = make_rsrc(st, (uint32_t)nst * 8u);
+  bstore8(r, (uint32_t)i * 8u, make_uint2((uint32_t)v, (uint32_t)(v >> 32)));
+}
 
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
@@ -109,6 +126,7 @@ __device__ __forceinline__ bool group_sync(GroupSync& gs, volatile int* flag) {
   __syncthreads();
   ++gs.n;
   if (threadIdx.x == 0) {
+    phase_stamp(gs.st, gs.nst, 2 * (int)gs.n - 1);
     int ok = 1;
     __hip_atomic_fetch_add(gs.ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const unsigned target = gs.n * kMembers;
@@ -128,6 +146,7 @@ __device__ __forceinline__ bool group_sync(GroupSync& gs, volatile int* flag) {
       __builtin_amdgcn_s_sleep(1);
     }
     if (gs.agent) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    phase_stamp(gs.st, gs.nst, 2 * (int)gs.n);
     *flag = ok;
   }
   __syncthreads();
@@ -667,7 +686,9 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
   const int nrows = min(p.Bx, p.B - r0);
   if (nrows <= 0) return;  // the whole group leaves
 
-  GroupSync gs{sync_ctr(p, x), sync_err(p), 0u, false};
+  GroupSync gs{sync_ctr(p, x), sync_err(p), 0u, false,
+               p.stamps && tid == 0 ? p.stamps + (long)blockIdx.x * p.nst : nullptr, p.nst};
+  phase_stamp(gs.st, gs.nst, 0);
   // placement check, settled by the first barrier
   if (tid == 0 && xcc_id() != (unsigned)x)
     __hip_atomic_fetch_or(sync_flag(p, x), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -756,6 +777,8 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
       gates_phase<RB, NBC, true>(q, st, lds, t, q.X + (long)t * BX, q.X + (long)(t + 1) * BX, r0, nrows);
       if (t + 1 < p.T && !group_sync(gs, &s_flag)) return;
     }
+    __syncthreads();
+    phase_stamp(gs.st, gs.nst, gs.nst - 1);
   } else {
     for (int t = 0;; ++t) {
       const PArgs& q = fresh_args();
@@ -777,6 +800,8 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
         if (ml < nrows) p.c[(long)(r0 + ml) * p.H + unit] = st.cst[rb];
       }
     }
+    __syncthreads();
+    phase_stamp(gs.st, gs.nst, gs.nst - 1);
   }
 }
 
@@ -942,11 +967,20 @@ bool persist_usable(const Layout& L, int B, bool nll) {
   return persist_enabled() && plan(L, B, nll, pl) && device_fits();
 }
 
+// Phase stamps for a launch with `nbar` barriers, when phase timing is on.
+void attach_stamps(PArgs& a, int nbar, bool nll, hipStream_t s) {
+  const int nst = 2 * nbar + 2;
+  a.stamps = phase_buffer((size_t)kGrid * nst, s);
+  a.nst = a.stamps ? nst : 0;
+  if (a.stamps) phase_layout(kGrid, nst, a.T, nll);
+}
+
 hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStream_t s) {
   PPlan pl;
   if (!persist_enabled() || !plan(P.L, R.B, false, pl) || !R.P || !R.sync || !device_fits())
     return hipErrorNotSupported;
   PArgs a = base_args(P, pl, R.B, R.T);
+  attach_stamps(a, 2 + 3 * R.T, false, s);
   a.k0 = R.k0; a.k1 = R.k1; a.traj0 = R.traj0; a.step0 = R.step0;
   a.tau = R.tau;
   a.sig = (R.flags & WM_FLAG_SIGMA_TAU) ? sqrtf(R.tau) : 1.0f;
@@ -974,6 +1008,7 @@ hipError_t launch_nll_persist(const Packed& P, const NllBufs& N, hipStream_t s) 
   if (!persist_enabled() || !plan(P.L, N.B, true, pl) || !N.sync || !device_fits())
     return hipErrorNotSupported;
   PArgs a = base_args(P, pl, N.B, N.T);
+  attach_stamps(a, N.T, true, s);
   a.X = reinterpret_cast<float*>(N.x);
   a.c = N.c;
   a.sync = N.sync;

@@ -34,6 +34,15 @@ void arg_ptrs(Tup& t, void** p, std::index_sequence<I...>) {
 }
 }  // namespace detail
 
+// Phase timing of the persistent kernels (wm_profile_phases): while it is
+// on, a device buffer of at least `words` zeroed 64-bit words (allocated on
+// first use, grown as needed) for the stamps of the next launch; null while
+// it is off.
+unsigned long long* phase_buffer(size_t words, hipStream_t s);
+// Layout of the launch that takes the stamps: `groups` work-groups of `nst`
+// stamps each, T steps, the NLL recurrence or the rollout.
+void phase_layout(int groups, int nst, int T, bool nll);
+
 // Launches kernel<<<grid, block, shm, s>>>(args...) and returns the launch
 // status.
 template <typename... P, typename... A>

@@ -181,6 +181,14 @@ static void others() {
   EXPECT(wm_profile_read("mdn", &ms, &n) == WM_OK && n == 0);
   EXPECT(wm_profile_reset() == WM_OK);
   EXPECT(wm_profile_enable(nullptr) == WM_OK);
+  // phase timing: nothing stamped yet, so the read touches no device
+  double ph[16];
+  for (double& v : ph) v = -1.0;
+  EXPECT(wm_profile_phases(1) == WM_OK);
+  EXPECT(wm_profile_phases_read(ph, 16) == WM_OK && ph[0] == 0.0 && ph[15] == 0.0);
+  EXPECT(wm_profile_phases_read(nullptr, 4) == WM_ERR_INVALID_ARG);
+  EXPECT(wm_profile_phases_read(ph, -1) == WM_ERR_INVALID_ARG);
+  EXPECT(wm_profile_phases(0) == WM_OK);
 }
 
 // Several threads at once: the last-error string is per thread and the
