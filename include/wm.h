@@ -375,15 +375,17 @@ wm_status wm_profile_reset(void);
  * is then averaged over the steps and the XCDs that hold rows):
  *   out[0]  T (0: no stamped launch since wm_profile_phases)
  *   out[1]  wall time per step
- *   out[2], out[3]   ctrl(t): max work, then its barrier (last arrival to
- *                    first release)
- *   out[4], out[5]   gates(t): max work, barrier (NLL: the step's work and
- *                    the barrier between steps)
+ *   out[2], out[3]   0 (reserved: the controller decisions run inside the
+ *                    gate phase)
+ *   out[4], out[5]   gates(t) with the step's controller decisions: max
+ *                    work, then its barrier (last arrival to first
+ *                    release); NLL: the step's work and the barrier between
+ *                    steps
  *   out[6], out[7]   mdn(t): max work, barrier
- *   out[8..10]       mean work of ctrl, gates, mdn
+ *   out[8..10]       0, then the mean work of gates and mdn
  *   out[11], out[12] set-up before step 0 and the tail after the last step
  *                    (max work)
- * Rollout phases 2, 3, 6, 7 and 8, 10 are 0 for the NLL recurrence.
+ * Slots 6, 7, 10 and 12 are 0 for the NLL recurrence.
  */
 wm_status wm_profile_phases(int32_t on);
 wm_status wm_profile_phases_read(double *out, int32_t n);

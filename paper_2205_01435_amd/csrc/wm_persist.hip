@@ -19,20 +19,30 @@
 // Each work-group owns NBC blocks of four hidden units (16 gate rows each).
 // The gate weights of those rows stay in registers for the whole call (the
 // A operand of the MFMAs), and each lane keeps the cell state of the
-// (unit, row) pairs it owns in registers.  Per dream step t, three phases
+// (unit, row) pairs it owns in registers.  Per dream step t, two phases
 // separated by XCD barriers:
-//   ctrl(t)   one row per work-group: logits = b_c + W_c,z q(z_t) + the sum
-//             of the 32 work-groups' h-part partials (from gates(t-1); the
-//             full product at t = 0), masked Gumbel-max action, resolution
-//             of transition t-1 (reward, done), freeze logic;
 //   gates(t)  X_t of the XCD's rows staged in LDS (LDS-DMA, four chunks so
 //             that the MFMAs start on the first), gate GEMM against the
-//             register weights, LSTM cell, h_{t+1} into X_{t+1}, and this
-//             work-group's partial W_c,h h_{t+1} of the next controller
-//             logits (rows A and A+1 of W_c are the reward and done heads);
+//             register weights; then the controller decision of every row
+//             of the XCD, which every work-group makes for itself (the same
+//             inputs and the same arithmetic give the same actions in all
+//             of them, so no barrier is needed): logits = W_c,z q(z_t) (MFMAs
+//             on the staged z columns) + the h part and the bias (from
+//             mdn(t-1)), masked Gumbel-max, resolution of transition t-1
+//             (reward, done), freeze logic; the work-group m % 32 writes
+//             row m's outputs.  LSTM cell with the chosen action's one-hot
+//             column, h_{t+1} into X_{t+1};
 //   mdn(t)    (group of four latent dims, 16-row block) tiles, K split over
 //             the four waves and summed in LDS, component pick, Box-Muller
-//             draw, z_{t+1} to z_out and X_{t+1}.
+//             draw, z_{t+1} to z_out and X_{t+1}; further tiles (or, when
+//             the tiles do not fit one round of work-groups, the first
+//             tiles themselves) compute the next step's controller h part
+//             W_c,h h_{t+1} + b_c into Lh (rows A and A+1 of W_c are the
+//             reward and done heads).
+// The barriers are split: a work-group arrives, draws the random numbers of
+// the next phase (the mixture noise of its mdn tile, the controller's
+// Gumbel noise), and then waits, so that the draws fill the barrier's
+// latency.
 // The NLL recurrence runs gates(t) only, one barrier per step; the mixture
 // head then runs once over all T*B rows (wm_kernels.hip).
 // Every wait is bounded: a wait that times out raises an error word that
@@ -71,7 +81,7 @@ struct PArgs {
   float* c;             // [B, H]: initial cell state in, final state out (rollout)
   int32_t* done_state;  // [B]
   const int32_t* lengths;  // [B] per-trajectory horizons, or null
-  float* P;             // [32, B, Nc] controller partial logits (rollout)
+  float* Lh;            // [B, Nc] controller logits' h part + bias (rollout)
   unsigned* sync;       // kSyncWords words, zero at launch
   const uint8_t* mask;  // [B, A], or [T, B, A] with step_mask
   int step_mask;
@@ -82,7 +92,10 @@ struct PArgs {
   float *h_trace, *c_trace;  // [T+1, B, H] or null (each on its own)
   float* g_trace;            // NLL: gate activations [T, B, 4H] or null
   // LDS carve-up (bytes)
-  int off_red, off_hb, off_wat, off_wcz, off_mdn, off_ctl, off_flags;
+  int off_red, off_rows, off_wat, off_wcz, off_mdn, off_cb, off_flags;
+  // controller: Nc / 16 logit blocks; the h-part blocks run as tiles of
+  // their own in mdn(t) (1) or inside the first mixture tiles (0)
+  int ncb, ctl_sep;
   // phase timing (measurement runs; null otherwise): nst device-clock
   // stamps per work-group, [blockIdx][nst]
   unsigned long long* stamps;
@@ -118,17 +131,25 @@ __device__ __forceinline__ void phase_stamp(unsigned long long* st, int nst, int
 
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-// Barrier of the 32 work-groups of one XCD.  Returns false if the group must
-// stop (a wait timed out here or elsewhere).
-__device__ __forceinline__ bool group_sync(GroupSync& gs, volatile int* flag) {
+// Barrier of the 32 work-groups of one XCD, in two halves: group_arrive
+// publishes this work-group's stores and counts it in; group_wait waits for
+// the other 31.  Work between the two may touch only registers and this
+// work-group's own LDS.  group_wait returns false if the group must stop (a
+// wait timed out here or elsewhere).
+__device__ __forceinline__ void group_arrive(GroupSync& gs) {
   if (gs.agent) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   else asm volatile("s_waitcnt vmcnt(0)" : : : "memory");  // this wave's stores reached L2
   __syncthreads();
   ++gs.n;
   if (threadIdx.x == 0) {
     phase_stamp(gs.st, gs.nst, 2 * (int)gs.n - 1);
-    int ok = 1;
     __hip_atomic_fetch_add(gs.ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+__device__ __forceinline__ bool group_wait(GroupSync& gs, volatile int* flag) {
+  if (threadIdx.x == 0) {
+    int ok = 1;
     const unsigned target = gs.n * kMembers;
     unsigned spins = 0;
     while ((int)(__hip_atomic_load(gs.ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
@@ -151,6 +172,11 @@ __device__ __forceinline__ bool group_sync(GroupSync& gs, volatile int* flag) {
   }
   __syncthreads();
   return *flag != 0;
+}
+
+__device__ __forceinline__ bool group_sync(GroupSync& gs, volatile int* flag) {
+  group_arrive(gs);
+  return group_wait(gs, flag);
 }
 #pragma clang diagnostic pop
 
@@ -192,51 +218,250 @@ template <int RB, int NBC>
 struct GateState {
   static constexpr int KSPLIT = 4 / NBC;
   uint4 wr[kMaxS];  // gate weights: rows 16 blk + r16, K slices sl0 .. sl0+nper-1
-  uint4 wc[2];      // controller h-part weights of this CU's units (rollout)
   float4 bias;      // b_g of this lane's unit (owner waves)
   float cst[RB];    // cell state of (unit, row 16 rb + r16) (owner waves)
 };
 
-// This work-group's share of the next controller logits from the h block in
-// LDS (its units, all rows of the XCD):
-// P[s][m][a] = sum over its units u of W_c[a][Z + u] h[m][u].
-template <int RB, int NBC>
-__device__ __forceinline__ void ctrl_partials(const PArgs& p, const GateState<RB, NBC>& st, char* lds,
-                                              int r0, int nrows) {
-  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+// ---------------------------------------------------------------------------
+// Controller decisions (rollout).  Every work-group of an XCD decides for all
+// of the XCD's rows, in the MFMA output layout: pair p = (cb, rb) covers
+// logits 16 cb .. 16 cb + 15 of rows 16 rb .. 16 rb + 15, and lane (g, r16)
+// of the wave that owns it (wave p % 4) holds logits 16 cb + 4 g + v,
+// v < 4, of row 16 rb + r16: one Philox block of stream 0 and one 16-byte
+// read of Lh per lane and pair.
+// ---------------------------------------------------------------------------
+// controller pairs per wave for RB row blocks: every pair of Nc <= 128
+// logits for one or two row blocks, Nc <= 80 for four
+template <int RB>
+constexpr int ctrl_cp() { return RB == 1 ? 2 : (RB == 2 ? 4 : 5); }
+constexpr int kMaxPairs = 4 * ctrl_cp<4>();
+
+template <int CP>
+struct CtrlLane {
+  float4 gum[CP];  // Gumbel noise of the lane's logits, -inf where the action is not valid
+  float4 lh[CP];   // h part + bias of the lane's logits
+  float rr, rd;    // reward and done logits of row tid (tid < rows): transition t-1
+  float ud;        // the stream-3 uniform of transition t-1 of row tid
+};
+
+// The uniform that decides whether transition t-1 of row tid ended.
+template <int CP>
+__device__ __forceinline__ void ctrl_done_uniform(const PArgs& p, CtrlLane<CP>& cl, int t, int r0, int nrows) {
+  cl.ud = 0.f;
+  if (p.use_done && t > 0 && (int)threadIdx.x < nrows) {
+    const Rng rng{p.k0, p.k1};
+    const uint4 w = rng.block(0, p.step0 + (uint32_t)t - 1u, p.traj0 + (uint32_t)(r0 + threadIdx.x), STREAM_DONE);
+    cl.ud = word_to_uniform(w.x);
+  }
+}
+
+__device__ __forceinline__ int* row_act(const PArgs& p, char* lds) { return reinterpret_cast<int*>(lds + p.off_rows); }
+__device__ __forceinline__ int* row_done(const PArgs& p, char* lds) { return row_act(p, lds) + 64; }
+__device__ __forceinline__ int* row_prev(const PArgs& p, char* lds) { return row_act(p, lds) + 128; }
+__device__ __forceinline__ int* row_len(const PArgs& p, char* lds) { return row_act(p, lds) + 192; }
+
+// The Gumbel noise of step t (drawn while the work-group waits at a barrier;
+// a valid action's score is its logit plus the noise, the argmax the action).
+template <int CP>
+__device__ __forceinline__ void ctrl_noise(const PArgs& p, CtrlLane<CP>& cl, int t, int r0, int nrows) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int g = lane >> 4, r16 = lane & 15;
-  const int s = blockIdx.x >> 3;
-  const int B = p.B;
-  const int rbv = (nrows + 15) >> 4;
-  const float* hb = reinterpret_cast<const float*>(lds + p.off_hb);
-  {
-    __syncthreads();
-    const rsrc_t rp = make_rsrc(p.P + ((long)s * B + r0) * p.Nc, (uint32_t)(nrows * p.Nc * 4));
+  const int np = p.ncb * ((nrows + 15) >> 4);
+  const Rng rng{p.k0, p.k1};
+  const uint32_t step = p.step0 + (uint32_t)t;
+  const uint8_t* mask = p.mask + (p.step_mask ? (long)t * p.B * p.A : 0);  // [B, A] of step t
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int nbk = wave + 4 * j;
-      if (16 * nbk >= p.Nc) break;
+  for (int k = 0; k < CP; ++k) {
+    float v[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    const int pi = wave + 4 * k;
+    const int cb = pi % p.ncb, rb = pi / p.ncb;
+    const int ml = 16 * rb + r16, a0 = 16 * cb + 4 * g;
+    if (pi < np && ml < nrows && a0 < p.A) {
+      const int m = r0 + ml;
+      const uint4 w = rng.block((uint32_t)a0 >> 2, step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
+      const uint8_t* mr = mask + (long)m * p.A;
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        if (rb >= rbv) break;
-        const uint4 hf = *reinterpret_cast<const uint4*>(hb + (16 * rb + r16) * 16 + 4 * g);
-        f32x4 pc = f32x4{0.f, 0.f, 0.f, 0.f};
-        Mfma<float>::step(pc, st.wc[j], hf);
-        const int ml = 16 * rb + r16;
-        const uint32_t op = ml < nrows ? (uint32_t)(ml * p.Nc + 16 * nbk + 4 * g) * 4u : kOffNone;
-        bstore16(rp, op, make_uint4(__float_as_uint(pc[0]), __float_as_uint(pc[1]), __float_as_uint(pc[2]),
-                                    __float_as_uint(pc[3])));
+      for (int i = 0; i < 4; ++i)
+        if (a0 + i < p.A && mr[a0 + i]) v[i] = gumbel(word_to_uniform(word_of(w, i)));
+    }
+    cl.gum[k] = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  ctrl_done_uniform(p, cl, t, r0, nrows);
+}
+
+// Lh of the lane's logits and the reward / done logits of row tid, written
+// by mdn(t-1) (by mdn's controller tiles over h_0 for t = 0).
+template <int CP>
+__device__ __forceinline__ void ctrl_loads(const PArgs& p, CtrlLane<CP>& cl, int r0, int nrows) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int np = p.ncb * ((nrows + 15) >> 4);
+  const rsrc_t rl = make_rsrc(p.Lh + (long)r0 * p.Nc, (uint32_t)(nrows * p.Nc * 4));
+#pragma unroll
+  for (int k = 0; k < CP; ++k) {
+    const int pi = wave + 4 * k;
+    const int cb = pi % p.ncb, rb = pi / p.ncb;
+    const int ml = 16 * rb + r16;
+    const bool ok = pi < np && ml < nrows;
+    cl.lh[k] = as_float4(cload16(rl, ok ? (uint32_t)(ml * p.Nc + 16 * cb + 4 * g) * 4u : kOffNone));
+  }
+  const int tid = threadIdx.x;
+  const bool rok = tid < nrows;
+  cl.rr = __uint_as_float(cload4(rl, rok ? (uint32_t)(tid * p.Nc + p.A) * 4u : kOffNone));
+  cl.rd = __uint_as_float(cload4(rl, rok ? (uint32_t)(tid * p.Nc + p.A + 1) * 4u : kOffNone));
+}
+
+// Best valid action of each (pair, row) into LDS: the z part of the logits
+// from the staged X_t (MFMAs against W_c's z columns; K slices that hold h
+// columns take zero weights there), plus Lh, plus the noise.  Lowest action
+// on ties.  N: this wave's pair count (its pairs' MFMA chains interleave).
+template <int RB, int CP, int N>
+__device__ __forceinline__ void ctrl_scores_n(const PArgs& p, const CtrlLane<CP>& cl, char* lds) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int zs = (p.Z + 15) >> 4;  // K slices holding z columns
+  float* cbs = reinterpret_cast<float*>(lds + p.off_cb);  // [pair][16 rows]
+  int* cbi = reinterpret_cast<int*>(cbs + kMaxPairs * 16);
+  const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(p.Nc * p.ldk * 4));
+  int cbk[N], rbk[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    const int pi = wave + 4 * k;
+    cbk[k] = pi % p.ncb;
+    rbk[k] = pi / p.ncb;
+  }
+  f32x4 acc[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int sl = 0; sl < zs; ++sl) {
+    const int col = 16 * sl + 4 * g;
+    uint4 a[N], b[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      a[k] = p.wcz_lds ? *reinterpret_cast<const uint4*>(lds + p.off_wcz + (cbk[k] * zs + sl) * 1024 + 16 * lane)
+                       : bload16(rwc, col < p.Z ? (uint32_t)((16 * cbk[k] + r16) * p.ldk + col) * 4u : kOffNone);
+      b[k] = *reinterpret_cast<const uint4*>(lds + (sl * RB + rbk[k]) * 1024 + 64 * r16 + 16 * g);
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+#pragma unroll
+      for (int k = 0; k < N; ++k) mfma4(acc[k], a[k], b[k], v);
+  }
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    const int pi = wave + 4 * k;
+    const float lv[4] = {cl.lh[k].x, cl.lh[k].y, cl.lh[k].z, cl.lh[k].w};
+    const float gv[4] = {cl.gum[k].x, cl.gum[k].y, cl.gum[k].z, cl.gum[k].w};
+    float best = -INFINITY;
+    int bi = -1;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float sc = (acc[k][v] + lv[v]) + gv[v];
+      if (gv[v] != -INFINITY && (bi < 0 || sc > best)) {
+        best = sc;
+        bi = 16 * cbk[k] + 4 * g + v;
       }
+    }
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float ob = __shfl_xor(best, off);
+      const int oi = __shfl_xor(bi, off);
+      if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
+        best = ob;
+        bi = oi;
+      }
+    }
+    if (g == 0) {
+      cbs[pi * 16 + r16] = best;
+      cbi[pi * 16 + r16] = bi;
     }
   }
 }
 
+template <int RB, int CP>
+__device__ __forceinline__ void ctrl_scores(const PArgs& p, const CtrlLane<CP>& cl, char* lds, int nrows) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int np = p.ncb * ((nrows + 15) >> 4);
+  const int npw = np > wave ? (np - wave + 3) >> 2 : 0;  // this wave's pairs (<= CP)
+  switch (npw) {
+    case 1: ctrl_scores_n<RB, CP, 1>(p, cl, lds); break;
+    case 2: if constexpr (CP >= 2) ctrl_scores_n<RB, CP, 2>(p, cl, lds); break;
+    case 3: if constexpr (CP >= 3) ctrl_scores_n<RB, CP, 3>(p, cl, lds); break;
+    case 4: if constexpr (CP >= 4) ctrl_scores_n<RB, CP, 4>(p, cl, lds); break;
+    case 5: if constexpr (CP >= 5) ctrl_scores_n<RB, CP, 5>(p, cl, lds); break;
+    default: break;
+  }
+}
+
+// The action of row tid (tid < rows) from its pairs, then the bookkeeping:
+// transition t-1 is resolved if the row was live then (its reward is the
+// reward head on h_t, it is done when sigmoid(done head) exceeds the
+// stream-3 uniform of step t-1); then (t < T) the row takes its action or,
+// if done, the frozen outputs; a row without a valid action ends here; a
+// step past the row's horizon is padding (no action, reward 0, done 0).
+// Every work-group keeps the same row state in LDS; work-group m % 32
+// writes row m's outputs.
+template <int CP>
+__device__ __forceinline__ void ctrl_resolve(const PArgs& p, const CtrlLane<CP>& cl, char* lds, int t, int r0,
+                                             int nrows) {
+  const int ml = threadIdx.x;
+  if (ml >= nrows) return;
+  const int s = blockIdx.x >> 3;
+  const bool owner = (ml & (kMembers - 1)) == s;
+  const int m = r0 + ml, B = p.B;
+  int* act_l = row_act(p, lds);
+  int* ds_l = row_done(p, lds);
+  int* pv_l = row_prev(p, lds);
+  int ds = ds_l[ml];
+  if (pv_l[ml] >= 0) {
+    const int d = p.use_done ? sigmoidf(cl.rd) > cl.ud : 0;
+    if (owner) {
+      p.rewards[(long)(t - 1) * B + m] = cl.rr;
+      p.dones[(long)(t - 1) * B + m] = (uint8_t)d;
+    }
+    if (d) ds = 1;
+  }
+  if (t < p.T) {
+    const float* cbs = reinterpret_cast<const float*>(lds + p.off_cb);
+    const int* cbi = reinterpret_cast<const int*>(cbs + kMaxPairs * 16);
+    const int rb = ml >> 4, r16 = ml & 15;
+    float best = -INFINITY;
+    int bi = -1;
+    for (int cb = 0; cb < p.ncb; ++cb) {
+      const int pi = rb * p.ncb + cb;
+      const float ob = cbs[pi * 16 + r16];
+      const int oi = cbi[pi * 16 + r16];
+      if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
+        best = ob;
+        bi = oi;
+      }
+    }
+    const bool pad = t >= row_len(p, lds)[ml];
+    int act = bi;
+    if (ds || pad) act = -1;
+    else if (act < 0) ds = 1;
+    if (owner) {
+      p.actions[(long)t * B + m] = act;
+      if (act < 0) {
+        p.rewards[(long)t * B + m] = 0.f;
+        p.dones[(long)t * B + m] = pad ? 0 : 1;
+      }
+    }
+    act_l[ml] = act;
+    pv_l[ml] = act;
+  } else if (owner) {
+    p.done_state[m] = ds;  // for the finishing kernel
+  }
+  ds_l[ml] = ds;
+}
+
 // ---------------------------------------------------------------------------
-// gates(t): X_in -> h_{t+1} into X_out (+ the controller partials)
+// gates(t): X_in -> h_{t+1} into X_out (rollout: with the step's actions)
 // ---------------------------------------------------------------------------
 template <int RB, int NBC, bool NLL>
-__device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& st, char* lds, int t,
-                                            const float* Xin, float* Xout, int r0, int nrows) {
+__device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& st, CtrlLane<ctrl_cp<RB>()>& cl,
+                                            char* lds,
+                                            int t, const float* Xin, float* Xout, int r0, int nrows) {
   constexpr int KSPLIT = GateState<RB, NBC>::KSPLIT;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
   const int s = blockIdx.x >> 3;
@@ -249,13 +474,18 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   const int sl0 = kp * nper;
   const int B = p.B, H = p.H, A = p.A;
 
-  // epilogue inputs issued first (older than the staging loads)
-  const rsrc_t ra = make_rsrc(p.actions + (long)t * B + r0, (uint32_t)nrows * 4u);
+  // epilogue inputs issued first (older than the staging loads): the NLL
+  // pass's actions, the rollout controller's Lh
   int act[RB];
+  if constexpr (NLL) {
+    const rsrc_t ra = make_rsrc(p.actions + (long)t * B + r0, (uint32_t)nrows * 4u);
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int ml = 16 * rb + r16;
-    act[rb] = owner && ml < nrows ? (int)cload4(ra, (uint32_t)ml * 4u) : -1;
+    for (int rb = 0; rb < RB; ++rb) {
+      const int ml = 16 * rb + r16;
+      act[rb] = owner && ml < nrows ? (int)cload4(ra, (uint32_t)ml * 4u) : -1;
+    }
+  } else {
+    ctrl_loads(p, cl, r0, nrows);
   }
 
   // stage X_in rows [r0, r0 + nrows), columns [0, ldk) into LDS as
@@ -292,9 +522,18 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
     if constexpr (NLL) dma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
     else cdma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
   };
+  // few loads per wave (small batches): every chunk goes out at once and
+  // one wait covers them all; else chunk 0 now and the rest under the MFMAs
+  const bool eager = wave_count(0) + wave_count(1) + wave_count(2) + wave_count(3) <= 12;
   {
     const int n0 = wave_count(0);
     for (int k = 0; k < n0; ++k) issue(0, k);
+    if (eager) {
+      for (int c = 1; c < 4; ++c) {
+        const int nc = wave_count(c);
+        for (int k = 0; k < nc; ++k) issue(c, k);
+      }
+    }
   }
 
   // two accumulator sets (even and odd K slices) and RB row blocks give
@@ -305,10 +544,21 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   const int nval = min(nper, nks - sl0);  // this wave's valid K slices (uniform)
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
-    vm_wait<0>();  // this wave's loads of chunk c (the only ones in flight)
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" : : : "memory");
-    const int nn = c < 3 ? wave_count(c + 1) : 0;
+    if (!NLL && c == 1) asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory");  // pair bests written
+    if (c == 0 || !eager) {
+      vm_wait<0>();  // this wave's loads of chunk c (the only ones in flight)
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" : : : "memory");
+    } else if (!NLL && c == 1) {
+      __builtin_amdgcn_s_barrier();  // the controller's pair bests are in LDS
+      asm volatile("" : : : "memory");
+    }
+    // rollout: the rows' actions (wave 0) from the pair bests of chunk 0's
+    // controller MFMAs, while chunk 1's loads land
+    if constexpr (!NLL) {
+      if (c == 1 && wave == 0) ctrl_resolve(p, cl, lds, t, r0, nrows);
+    }
+    const int nn = c < 3 && !eager ? wave_count(c + 1) : 0;
     int kk = 0;  // next load of chunk c+1 to issue
     const char* sb0 = lds + sl0 * RB * 1024 + 64 * r16 + 16 * g;
     if (9 * c + 9 <= nval && rbv == RB) {
@@ -345,19 +595,26 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
         for (; kk < upto; ++kk) issue(c + 1, kk);
       }
     }
+    // rollout: the controller's (pair, row) bests from the staged z columns
+    // (chunk 0 holds them), under chunk 1's loads
+    if constexpr (!NLL) {
+      if (c == 0) ctrl_scores<RB>(p, cl, lds, nrows);
+    }
   }
   f32x4 acc[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) acc[rb] = acc2[0][rb] + acc2[1][rb];
 
   // K-split partials meet in LDS (waves of the same gate block)
+  f32x4* red = reinterpret_cast<f32x4*>(lds + p.off_red);
   if constexpr (KSPLIT > 1) {
-    f32x4* red = reinterpret_cast<f32x4*>(lds + p.off_red);
     if (!owner) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) red[(((kp - 1) * NBC + wb) * RB + rb) * 64 + lane] = acc[rb];
     }
-    __syncthreads();
+  }
+  if constexpr (KSPLIT > 1 || !NLL) __syncthreads();
+  if constexpr (KSPLIT > 1) {
     if (owner) {
 #pragma unroll
       for (int k2 = 1; k2 < KSPLIT; ++k2)
@@ -365,8 +622,17 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
         for (int rb = 0; rb < RB; ++rb) acc[rb] += red[(((k2 - 1) * NBC + wb) * RB + rb) * 64 + lane];
     }
   }
+  if constexpr (!NLL) {
+    // the rows' actions (resolved in chunk 1), seen by every wave after the
+    // barrier above
+    const int* act_l = row_act(p, lds);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int ml = 16 * rb + r16;
+      act[rb] = owner && ml < nrows ? act_l[ml] : -1;
+    }
+  }
 
-  float* hb = reinterpret_cast<float*>(lds + p.off_hb);  // [16 RB rows][16 units]
   if (owner) {
     const rsrc_t rxo = make_rsrc(Xout + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
     const rsrc_t rw = make_rsrc(p.WaT, (uint32_t)(A * 4 * H * 4));
@@ -413,249 +679,168 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
       const uint32_t oh = ok ? (uint32_t)(ml * H + unit) * 4u : kOffNone;
       bstore4(rht, oh, __float_as_uint(hn));  // dropped without traces
       bstore4(rct, oh, __float_as_uint(cn));
-      if constexpr (!NLL) hb[ml * 16 + 4 * wb + g] = hn;
     }
   }
-
-  if constexpr (!NLL) ctrl_partials<RB, NBC>(p, st, lds, r0, nrows);
 }
 
 // ---------------------------------------------------------------------------
-// mdn(t): mixture head on h_{t+1} (X_out columns Z ..), z_{t+1}
+// mdn(t): mixture head on h_{t+1} (X_out columns Z ..), z_{t+1}, and the
+// controller's h part of step t+1
 // ---------------------------------------------------------------------------
-// QC > 0: the number of 16-row output blocks per latent-dim group is the
-// compile-time QC (= p.Q; the rollout kernels are instantiated for every Q).
-// Then every guard on q is resolved at compile time; under a runtime Q the
-// guarded fragment loads keep the compiler from counting the loads in
-// flight, and it waits for nearly all of them before each MFMA (medium
-// rollout 23.5 against 21.9 us per step).
-template <int QC>
-__device__ __forceinline__ void mdn_phase(const PArgs& p, char* lds, int t, float* Xout, int r0, int nrows) {
+// One tile: rows 16 rb .. 16 rb + 15 against HZ ? QC mixture blocks of dim
+// group J (output rows 16 Q J ..) : none, plus HC ? controller block cb
+// (W_c rows 16 cb .., h columns) : none; K (= H) split over the four waves,
+// partial sums met in LDS.  QC (= p.Q) is compile-time: every guard on q is
+// then resolved at compile time; under a runtime Q the guarded fragment
+// loads keep the compiler from counting the loads in flight, and it waits
+// for nearly all of them before each MFMA (medium rollout 23.5 against 21.9
+// us per step).  `pre` is the lane's mixture noise drawn at the barrier
+// (null: draw it here).
+template <int QC, bool HZ, bool HC>
+__device__ __forceinline__ void mdn_tile(const PArgs& p, char* lds, int t, float* Xout, int r0, int nrows,
+                                         int J, int rb, int cb, const MdnNoise* pre) {
+  constexpr int NB = (HZ ? QC : 0) + (HC ? 1 : 0);  // A blocks of the tile
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
-  const int s = blockIdx.x >> 3;
-  const int B = p.B, Z = p.Z, H = p.H, Q = QC > 0 ? QC : p.Q;
-  const int rbv = (nrows + 15) >> 4;
-  const int ntiles = (Z >> 2) * rbv;
+  const int B = p.B, Z = p.Z, H = p.H;
   const int nsl = H >> 4;
   const int per = (nsl + 3) >> 2;  // K slices per wave (<= kMaxMS)
   const int s0 = wave * per;
-  const Rng rng{p.k0, p.k1};
   const uint32_t step = p.step0 + (uint32_t)t;
   const uint32_t ldxb = (uint32_t)p.ldx * 4u;
-  const rsrc_t rwm = make_rsrc(p.Wm, (uint32_t)((16 * Q * (Z >> 2) + 16) * p.ldh * 4));
+  const rsrc_t rwm = make_rsrc(p.Wm, (uint32_t)((16 * QC * (Z >> 2) + 16) * p.ldh * 4));
+  const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(p.Nc * p.ldk * 4));
   const rsrc_t rx = make_rsrc(Xout + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
-  const rsrc_t ra = make_rsrc(p.actions + (long)t * B + r0, (uint32_t)nrows * 4u);
   const rsrc_t rzp = make_rsrc(p.z_out + ((long)t * B + r0) * Z, (uint32_t)(nrows * Z * 4));
   const rsrc_t rzn = make_rsrc(p.z_out + ((long)(t + 1) * B + r0) * Z, (uint32_t)(nrows * Z * 4));
-  f32x4* red = reinterpret_cast<f32x4*>(lds + p.off_mdn);  // [4 waves][Q][64 lanes]
+  f32x4* red = reinterpret_cast<f32x4*>(lds + p.off_mdn);  // [4 waves][NB][64 lanes]
 
-  for (int ti = s; ti < ntiles; ti += kMembers) {
-    const int J = ti / rbv, rb = ti % rbv;
-    const int ml = 16 * rb + r16, j = 4 * J + g;
-    const bool ok = ml < nrows;
-    // wave 0 owns the epilogue: liveness, noise or the frozen latent
-    bool live = false;
-    float zprev = 0.f;
-    MdnNoise nz{};
-    if (wave == 0) {
-      const int a = (int)cload4(ra, ok ? (uint32_t)ml * 4u : kOffNone);
-      live = ok && a >= 0;
-      if (live) nz = mixture_noise(rng, p.K, step, p.traj0 + (uint32_t)(r0 + ml), j);
-      zprev = __uint_as_float(cload4(rzp, ok && !live ? (uint32_t)(ml * Z + j) * 4u : kOffNone));
+  const int ml = 16 * rb + r16, j = 4 * J + g;
+  const bool ok = ml < nrows;
+  // wave 0 owns the epilogue: liveness, noise or the frozen latent
+  bool live = false;
+  float zprev = 0.f;
+  MdnNoise nz{};
+  if (HZ && wave == 0) {
+    live = ok && row_act(p, lds)[ml] >= 0;
+    if (pre) nz = *pre;
+    else if (live) nz = mixture_noise(Rng{p.k0, p.k1}, p.K, step, p.traj0 + (uint32_t)(r0 + ml), j);
+    zprev = __uint_as_float(cload4(rzp, ok && !live ? (uint32_t)(ml * Z + j) * 4u : kOffNone));
+  }
+  // the epilogue's biases, fetched before the MFMAs
+  float4 bz[HZ ? QC : 1], bcv = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (wave == 0) {
+    if constexpr (HZ) {
+#pragma unroll
+      for (int q = 0; q < QC; ++q) bz[q] = *reinterpret_cast<const float4*>(p.bm + 16 * QC * J + 16 * q + 4 * g);
     }
-    f32x4 acc[kMaxQ];
+    if constexpr (HC) bcv = *reinterpret_cast<const float4*>(p.bc + 16 * cb + 4 * g);
+  }
+  f32x4 acc[NB];
 #pragma unroll
-    for (int q = 0; q < kMaxQ; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // slice i's fragments are fetched three slices ahead of their MFMAs; the
-    // scheduling barriers keep the compiler from hoisting every fetch (which
-    // would not fit the registers next to the resident gate weights)
-    uint4 af[kMaxMS][kMaxQ], bf[kMaxMS];
+  for (int q = 0; q < NB; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // slice i's fragments are fetched three slices ahead of their MFMAs; the
+  // scheduling barriers keep the compiler from hoisting every fetch (which
+  // would not fit the registers next to the resident gate weights)
+  uint4 af[kMaxMS][NB], bf[kMaxMS];
 #pragma unroll
-    for (int i = 0; i < kMaxMS + 3; ++i) {
-      if (i < kMaxMS) {
-        const int sl = s0 + i;
-        const bool kin = i < per && sl < nsl;
-        const uint32_t kb = (uint32_t)(sl * 16 + 4 * g) * 4u;
-        bf[i] = cload16(rx, kin && ok ? (uint32_t)ml * ldxb + (uint32_t)Z * 4u + kb : kOffNone);
+  for (int i = 0; i < kMaxMS + 3; ++i) {
+    if (i < kMaxMS) {
+      const int sl = s0 + i;
+      const bool kin = i < per && sl < nsl;
+      const uint32_t kb = (uint32_t)(sl * 16 + 4 * g) * 4u;
+      bf[i] = cload16(rx, kin && ok ? (uint32_t)ml * ldxb + (uint32_t)Z * 4u + kb : kOffNone);
 #pragma unroll
-        for (int q = 0; q < kMaxQ; ++q)
-          if (q < Q)
-            af[i][q] = bload16(rwm, kin ? (uint32_t)((16 * Q * J + 16 * q + r16) * p.ldh) * 4u + kb : kOffNone);
+      for (int q = 0; q < NB; ++q) {
+        if (HZ && q < QC)
+          af[i][q] = bload16(rwm, kin ? (uint32_t)((16 * QC * J + 16 * q + r16) * p.ldh) * 4u + kb : kOffNone);
+        else
+          af[i][q] = bload16(rwc, kin ? (uint32_t)((16 * cb + r16) * p.ldk + Z) * 4u + kb : kOffNone);
       }
-      if (i >= 3 && i - 3 < per && s0 + i - 3 < nsl) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-#pragma unroll
-          for (int q = 0; q < kMaxQ; ++q)
-            if (q < Q) mfma4(acc[q], af[i - 3][q], bf[i - 3], v);
-      }
-      __builtin_amdgcn_sched_barrier(0);
     }
+    if (i >= 3 && i - 3 < per && s0 + i - 3 < nsl) {
 #pragma unroll
-    for (int q = 0; q < kMaxQ; ++q)
-      if (q < Q) red[(wave * Q + q) * 64 + lane] = acc[q];
-    __syncthreads();
-    if (wave == 0 && ok) {
+      for (int v = 0; v < 4; ++v)
+#pragma unroll
+        for (int q = 0; q < NB; ++q) mfma4(acc[q], af[i - 3][q], bf[i - 3], v);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int q = 0; q < NB; ++q) red[(wave * NB + q) * 64 + lane] = acc[q];
+  __syncthreads();
+  if (wave == 0 && ok) {
+    if constexpr (HZ) {
       float z = zprev;
       if (live) {
-        float feat[4 * kMaxQ];
+        float feat[4 * QC];
 #pragma unroll
-        for (int q = 0; q < kMaxQ; ++q) {
-          f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (q < Q) {
-            v = red[q * 64 + lane] + red[(Q + q) * 64 + lane] + red[(2 * Q + q) * 64 + lane] +
-                red[(3 * Q + q) * 64 + lane];
-            const float4 b4 = *reinterpret_cast<const float4*>(p.bm + 16 * Q * J + 16 * q + 4 * g);
-            v += f32x4{b4.x, b4.y, b4.z, b4.w};
-          }
+        for (int q = 0; q < QC; ++q) {
+          f32x4 v = red[q * 64 + lane] + red[(NB + q) * 64 + lane] + red[(2 * NB + q) * 64 + lane] +
+                    red[(3 * NB + q) * 64 + lane];
+          v += f32x4{bz[q].x, bz[q].y, bz[q].z, bz[q].w};
           feat[4 * q] = v[0]; feat[4 * q + 1] = v[1]; feat[4 * q + 2] = v[2]; feat[4 * q + 3] = v[3];
         }
-        z = mixture_pick<kMaxQ>(p.K, p.tau, nz, feat, p.sig);
+        z = mixture_pick<QC>(p.K, p.tau, nz, feat, p.sig);
       }
       bstore4(rzn, (uint32_t)(ml * Z + j) * 4u, __float_as_uint(z));
       bstore4(rx, (uint32_t)ml * ldxb + (uint32_t)j * 4u, __float_as_uint(z));
     }
-    __syncthreads();
+    if constexpr (HC) {
+      constexpr int q = NB - 1;
+      f32x4 v = red[q * 64 + lane] + red[(NB + q) * 64 + lane] + red[(2 * NB + q) * 64 + lane] +
+                red[(3 * NB + q) * 64 + lane];
+      v += f32x4{bcv.x, bcv.y, bcv.z, bcv.w};
+      const rsrc_t rl = make_rsrc(p.Lh + (long)r0 * p.Nc, (uint32_t)(nrows * p.Nc * 4));
+      bstore16(rl, (uint32_t)(ml * p.Nc + 16 * cb + 4 * g) * 4u,
+               make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])));
+    }
+  }
+  __syncthreads();
+}
+
+// The tiles of one XCD: ZT = (Z/4) rbv mixture tiles, then (ctl_sep) the
+// ncb rbv controller tiles; without ctl_sep the mixture tiles of dim groups
+// J < ncb carry controller block J.  Work-group s takes tiles s, s + 32, ...
+// `pre` holds the noise of tile s when it is a mixture tile.
+template <int QC>
+__device__ __forceinline__ void mdn_phase(const PArgs& p, char* lds, int t, float* Xout, int r0, int nrows,
+                                          const MdnNoise& pre) {
+  const int s = blockIdx.x >> 3;
+  const int rbv = (nrows + 15) >> 4;
+  const int zt = (p.Z >> 2) * rbv;
+  const int nt = zt + (p.ctl_sep ? p.ncb * rbv : 0);
+  for (int ti = s; ti < nt; ti += kMembers) {
+    const MdnNoise* pn = ti == s ? &pre : nullptr;
+    if (ti < zt) {
+      const int J = ti / rbv, rb = ti % rbv;
+      if (!p.ctl_sep && J < p.ncb) mdn_tile<QC, true, true>(p, lds, t, Xout, r0, nrows, J, rb, J, pn);
+      else mdn_tile<QC, true, false>(p, lds, t, Xout, r0, nrows, J, rb, 0, pn);
+    } else {
+      const int c = ti - zt;
+      mdn_tile<QC, false, true>(p, lds, t, Xout, r0, nrows, 0, c / p.ncb, c % p.ncb, nullptr);
+    }
   }
 }
 
-// ---------------------------------------------------------------------------
-// ctrl(t): action a_t of each row (mode 1) and resolution of transition t-1
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void ctrl_phase(const PArgs& p, char* lds, int t, const float* Xt, int r0,
-                                           int nrows) {
-  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+// The controller tiles alone, over h_0 (X_0): Lh of step 0.
+template <int QC>
+__device__ __forceinline__ void ctrl_h0(const PArgs& p, char* lds, float* X0, int r0, int nrows) {
   const int s = blockIdx.x >> 3;
-  const int B = p.B, Z = p.Z, A = p.A, Nc = p.Nc;
-  const int k = __builtin_amdgcn_readfirstlane(tid >> 7), a = tid & 127;  // k: wave-uniform
-  const int ml = s + kMembers * k;
-  const bool rowok = ml < nrows;
-  const int m = r0 + ml;
-  const bool tail = t == p.T;
-  const uint32_t step = p.step0 + (uint32_t)t;
-  const Rng rng{p.k0, p.k1};
-  float* lg = reinterpret_cast<float*>(lds + p.off_ctl);  // [2][128] logits
-  float* wbest = lg + 256;                                // [4] best score per wave
-  int* widx = reinterpret_cast<int*>(wbest + 4);           // [4] its action
-  float* xz = lg + 272;                                   // [2][Z] q(z_t) of the two rows
+  const int rbv = (nrows + 15) >> 4;
+  for (int c = s; c < p.ncb * rbv; c += kMembers)
+    mdn_tile<QC, false, true>(p, lds, 0, X0, r0, nrows, 0, c / p.ncb, c % p.ncb, nullptr);
+}
 
-  // z_t of this work-group's rows (written by mdn(t-1) elsewhere on the XCD)
-  {
-    const int zq = Z >> 2;  // 16-byte pieces per row
-    for (int e = tid; e < 2 * zq; e += 256) {
-      const int kk = e / zq, pc = e % zq;
-      const int mr = s + kMembers * kk;
-      const rsrc_t rxt = make_rsrc(Xt + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
-      const uint4 v = cload16(rxt, mr < nrows ? (uint32_t)(mr * p.ldx + 4 * pc) * 4u : kOffNone);
-      *reinterpret_cast<uint4*>(xz + kk * Z + 4 * pc) = v;
-    }
-  }
-  // this lane's share of the partial logits (issued before the barrier)
-  float ps = 0.f;
-  if (rowok && a < Nc) {
-    const rsrc_t rp = make_rsrc(p.P, (uint32_t)((long)kMembers * B * Nc * 4));
-    float pv[kMembers];
-#pragma unroll
-    for (int s2 = 0; s2 < kMembers; ++s2)
-      pv[s2] = __uint_as_float(cload4(rp, (uint32_t)(((long)s2 * B + m) * Nc + a) * 4u));
-#pragma unroll
-    for (int s2 = 0; s2 < kMembers; ++s2) ps += pv[s2];
-  }
-  __syncthreads();
-
-  float l = 0.f;
-  if (rowok && a < Nc) {
-    // logit a = b_c + W_c[a, 0:Z] . q(z_t) + (the h part, summed above)
-    const float* zr = xz + k * Z;
-    float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (p.wcz_lds) {
-      // W_c[:, 0:Z] resident in LDS as [Z/4][Nc][4]
-      const float4* wz = reinterpret_cast<const float4*>(lds + p.off_wcz);
-#pragma unroll 8
-      for (int kk = 0; kk < Z; kk += 4) {
-        const float4 w = wz[(kk >> 2) * Nc + a];
-        const float4 xv = *reinterpret_cast<const float4*>(zr + kk);
-        s4.x = fmaf(w.x, xv.x, s4.x);
-        s4.y = fmaf(w.y, xv.y, s4.y);
-        s4.z = fmaf(w.z, xv.z, s4.z);
-        s4.w = fmaf(w.w, xv.w, s4.w);
-      }
-    } else {
-      const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(Nc * p.ldk * 4));  // uniform resource
-      const uint32_t wrow = (uint32_t)(a * p.ldk) * 4u;
-#pragma unroll 8
-      for (int kk = 0; kk < Z; kk += 4) {
-        const float4 w = as_float4(bload16(rwc, wrow + (uint32_t)kk * 4u));
-        const float4 xv = *reinterpret_cast<const float4*>(zr + kk);
-        s4.x = fmaf(w.x, xv.x, s4.x);
-        s4.y = fmaf(w.y, xv.y, s4.y);
-        s4.z = fmaf(w.z, xv.z, s4.z);
-        s4.w = fmaf(w.w, xv.w, s4.w);
-      }
-    }
-    l = (s4.x + s4.y) + (s4.z + s4.w) + ps + p.bc[a];
-  }
-  lg[k * 128 + a] = l;
-
-  // masked Gumbel-max over the valid actions, lowest index on ties
-  float best = -INFINITY;
-  int bidx = -1;
-  const uint8_t* mask = p.mask + (p.step_mask && !tail ? (long)t * B * A : 0);  // [B, A] of step t
-  if (!tail && rowok && a < A && mask[(long)m * A + a]) {
-    const uint4 w = rng.block((uint32_t)a >> 2, step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
-    best = l + gumbel(word_to_uniform(word_of(w, a & 3)));
-    bidx = a;
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float ob = __shfl_xor(best, off);
-    const int oi = __shfl_xor(bidx, off);
-    if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) {
-      best = ob;
-      bidx = oi;
-    }
-  }
-  if (lane == 0) {
-    wbest[wave] = best;
-    widx[wave] = bidx;
-  }
-  __syncthreads();
-  if (a == 0 && rowok) {
-    const float ob = wbest[2 * k + 1];
-    const int oi = widx[2 * k + 1];
-    best = wbest[2 * k];
-    bidx = widx[2 * k];
-    if (oi >= 0 && (bidx < 0 || ob > best || (ob == best && oi < bidx))) bidx = oi;
-    // commit (rows are owned by this work-group for the whole call)
-    const rsrc_t rds = make_rsrc(p.done_state, (uint32_t)B * 4u);
-    int ds = (int)cload4(rds, (uint32_t)m * 4u);
-    if (t > 0) {
-      const rsrc_t rap = make_rsrc(p.actions + (long)(t - 1) * B, (uint32_t)B * 4u);
-      if ((int)cload4(rap, (uint32_t)m * 4u) >= 0) {
-        p.rewards[(long)(t - 1) * B + m] = lg[k * 128 + A];
-        int d = 0;
-        if (p.use_done) {
-          const uint4 w = rng.block(0, step - 1u, p.traj0 + (uint32_t)m, STREAM_DONE);
-          d = sigmoidf(lg[k * 128 + A + 1]) > word_to_uniform(w.x);
-        }
-        p.dones[(long)(t - 1) * B + m] = (uint8_t)d;
-        if (d) ds = 1;
-      }
-    }
-    if (!tail) {
-      // past the row's horizon: padding (no action, reward 0, done 0)
-      const bool pad = p.lengths && t >= p.lengths[m];
-      int act = bidx;
-      if (ds || pad) act = -1;
-      else if (act < 0) ds = 1;
-      p.actions[(long)t * B + m] = act;
-      if (act < 0) {
-        p.rewards[(long)t * B + m] = 0.f;
-        p.dones[(long)t * B + m] = pad ? 0 : 1;
-      }
-    }
-    p.done_state[m] = ds;
-  }
+// The mixture noise of tile s of mdn(t) (wave 0's lanes), drawn at the
+// barrier before it.
+__device__ __forceinline__ void mdn_noise_pre(const PArgs& p, MdnNoise& nz, int t, int r0, int nrows) {
+  const int s = blockIdx.x >> 3, lane = threadIdx.x & 63;
+  const int rbv = (nrows + 15) >> 4;
+  if ((threadIdx.x >> 6) != 0 || s >= (p.Z >> 2) * rbv) return;
+  const int J = s / rbv, rb = s % rbv;
+  const int ml = 16 * rb + (lane & 15), j = 4 * J + (lane >> 4);
+  if (ml < nrows)
+    nz = mixture_noise(Rng{p.k0, p.k1}, p.K, p.step0 + (uint32_t)t, p.traj0 + (uint32_t)(r0 + ml), j);
 }
 
 // ---------------------------------------------------------------------------
@@ -718,25 +903,30 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
       const int ml = 16 * rb + r16;
       st.cst[rb] = __uint_as_float(bload4(rc, owner && ml < nrows ? (uint32_t)(ml * p.H + unit) * 4u : kOffNone));
     }
-    const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(p.Nc * p.ldk * 4));
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int nbk = wave + 4 * j;
-      const bool ok = !NLL && 16 * nbk < p.Nc && g < NBC;
-      st.wc[j] = bload16(rwc, ok ? (uint32_t)((16 * nbk + r16) * p.ldk + p.Z + 4 * NBC * s + 4 * g) * 4u : kOffNone);
-    }
   }
   if constexpr (!NLL) {
-    // unused units of the h block read as zero in the partial-logit MFMA
-    float* hb = reinterpret_cast<float*>(lds + p.off_hb);
-    for (int i = tid; i < 16 * RB * 16; i += 256) hb[i] = 0.f;
-  }
-  if (!NLL && p.wcz_lds) {
-    // the controller's z columns, W_c[:, 0:Z], as [Z/4][Nc][4]
-    float4* wz = reinterpret_cast<float4*>(lds + p.off_wcz);
-    for (int i = tid; i < (p.Z >> 2) * p.Nc; i += 256) {
-      const int q4 = i / p.Nc, aa = i % p.Nc;
-      wz[i] = *reinterpret_cast<const float4*>(p.Wc + (long)aa * p.ldk + 4 * q4);
+    // row state: the actions of step t, the done state, the previous action
+    int* rows = row_act(p, lds);
+    for (int i = tid; i < 4 * 64; i += 256) {
+      const int ml = i & 63;
+      int v = -1;
+      if (i >= 64 && i < 128) v = ml < nrows ? p.done_state[r0 + ml] : 0;
+      if (i >= 192) v = p.lengths && ml < nrows ? p.lengths[r0 + ml] : 0x7fffffff;
+      rows[i] = v;
+    }
+    if (p.wcz_lds) {
+      // the controller's z columns as MFMA A fragments: fragment (cb, sl),
+      // lane (g, r16) holds W_c[16 cb + r16][16 sl + 4 g .. + 3] (zero
+      // where those columns are h columns)
+      const int zs = (p.Z + 15) >> 4;
+      uint4* wz = reinterpret_cast<uint4*>(lds + p.off_wcz);
+      for (int i = tid; i < p.ncb * zs * 64; i += 256) {
+        const int f = i >> 6, l = i & 63;
+        const int cb = f / zs, sl = f % zs;
+        const int col = 16 * sl + 4 * (l >> 4);
+        wz[i] = col < p.Z ? *reinterpret_cast<const uint4*>(p.Wc + (long)(16 * cb + (l & 15)) * p.ldk + col)
+                          : make_uint4(0u, 0u, 0u, 0u);
+      }
     }
   }
   if (p.wat_lds) {
@@ -754,43 +944,46 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
   __syncthreads();
   gs.agent = s_agent != 0;
 
+  CtrlLane<ctrl_cp<RB>()> cl;
+  MdnNoise nz{};
   if constexpr (!NLL) {
     // the h part of the step-0 controller logits, from h_0 (X_0, written
-    // before the launch), like every later step's from gates(t-1)
-    if (owner) {
-      float* hb = reinterpret_cast<float*>(lds + p.off_hb);
-      const rsrc_t rx0 = make_rsrc(p.X + (long)r0 * p.ldx, (uint32_t)(nrows * p.ldx * 4));
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const int ml = 16 * rb + r16;
-        if (ml < nrows) hb[ml * 16 + 4 * wb + g] = __uint_as_float(bload4(rx0, (uint32_t)(ml * p.ldx + p.Z + unit) * 4u));
-      }
-    }
-    ctrl_partials<RB, NBC>(p, st, lds, r0, nrows);
-    if (!group_sync(gs, &s_flag)) return;
+    // before the launch), like every later step's from mdn(t-1)
+    ctrl_h0<QC>(p, lds, p.X, r0, nrows);
+    group_arrive(gs);
+    ctrl_noise(p, cl, 0, r0, nrows);
+    if (!group_wait(gs, &s_flag)) return;
   }
 
   const long BX = (long)p.B * p.ldx;
   if constexpr (NLL) {
     for (int t = 0; t < p.T; ++t) {
       const PArgs& q = fresh_args();
-      gates_phase<RB, NBC, true>(q, st, lds, t, q.X + (long)t * BX, q.X + (long)(t + 1) * BX, r0, nrows);
+      gates_phase<RB, NBC, true>(q, st, cl, lds, t, q.X + (long)t * BX, q.X + (long)(t + 1) * BX, r0, nrows);
       if (t + 1 < p.T && !group_sync(gs, &s_flag)) return;
     }
     __syncthreads();
     phase_stamp(gs.st, gs.nst, gs.nst - 1);
   } else {
-    for (int t = 0;; ++t) {
+    for (int t = 0; t < p.T; ++t) {
       const PArgs& q = fresh_args();
       float* Xt = q.X + (long)(t & 1) * BX;
       float* Xn = q.X + (long)((t + 1) & 1) * BX;
-      ctrl_phase(q, lds, t, Xt, r0, nrows);
-      if (t == p.T) break;
-      if (!group_sync(gs, &s_flag)) return;
-      gates_phase<RB, NBC, false>(fresh_args(), st, lds, t, Xt, Xn, r0, nrows);
-      if (!group_sync(gs, &s_flag)) return;
-      mdn_phase<QC>(fresh_args(), lds, t, Xn, r0, nrows);
-      if (!group_sync(gs, &s_flag)) return;
+      gates_phase<RB, NBC, false>(q, st, cl, lds, t, Xt, Xn, r0, nrows);
+      group_arrive(gs);
+      mdn_noise_pre(fresh_args(), nz, t, r0, nrows);
+      if (!group_wait(gs, &s_flag)) return;
+      mdn_phase<QC>(fresh_args(), lds, t, Xn, r0, nrows, nz);
+      group_arrive(gs);
+      if (t + 1 < p.T) ctrl_noise(fresh_args(), cl, t + 1, r0, nrows);
+      if (!group_wait(gs, &s_flag)) return;
+    }
+    // transition T-1 (its reward and done from mdn(T-1)'s Lh), the done state
+    {
+      const PArgs& q = fresh_args();
+      ctrl_loads(q, cl, r0, nrows);
+      ctrl_done_uniform(q, cl, q.T, r0, nrows);
+      if (wave == 0) ctrl_resolve(q, cl, lds, q.T, r0, nrows);
     }
     // final cell state for k_rollout_finish
     if (owner) {
@@ -825,8 +1018,9 @@ int persist_rb(int B) {
 struct PPlan {
   int rb = 0, nbc = 0;
   size_t lds = 0;
-  int off_red = 0, off_hb = 0, off_wat = 0, off_wcz = 0, off_mdn = 0, off_ctl = 0, off_flags = 0;
+  int off_red = 0, off_rows = 0, off_wat = 0, off_wcz = 0, off_mdn = 0, off_cb = 0, off_flags = 0;
   int wat_lds = 0, wcz_lds = 0;
+  int ncb = 0, ctl_sep = 0;
 };
 
 // The grid must be co-resident with one work-group per CU: 8 XCDs x 32 CUs.
@@ -856,21 +1050,32 @@ bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
   if (L.N > 0) return false;  // the two-level controller runs on the multi-launch path
   pl.rb = rb;
   pl.nbc = nbc;
-  // the mixture-head partial sums and the controller scratch live in other
-  // phases than the gate staging and share its bytes; the h block (zero
-  // padded once) and the one-hot columns persist
+  if (!nll) {
+    // controller pairs (logit block, row block) per wave, and the tiles of
+    // mdn(t): the controller blocks as tiles of their own when all tiles fit
+    // one round of the 32 work-groups, else inside the first mixture tiles
+    const int rbv = (((B + kGroups - 1) / kGroups) + 15) / 16;
+    pl.ncb = L.Nc / 16;
+    if (pl.ncb * rbv > 4 * (rb == 1 ? ctrl_cp<1>() : rb == 2 ? ctrl_cp<2>() : ctrl_cp<4>())) return false;
+    const int zt = (L.Z / 4) * rbv;
+    pl.ctl_sep = zt + pl.ncb * rbv <= kMembers ? 1 : 0;
+    if (!pl.ctl_sep && pl.ncb > L.Z / 4) return false;
+    if ((L.Z + 15) / 16 > 9) return false;  // the z columns lie in the first staged chunk
+  }
+  // the mixture-head partial sums share the gate staging's bytes (another
+  // phase); the controller's pair bests, the row state and the one-hot
+  // columns persist
   size_t o = (size_t)nks * rb * 1024;  // staging
   pl.off_red = (int)o;
   o += (size_t)(4 - nbc) * rb * 1024;   // K-split partial sums
   pl.off_mdn = 0;
-  pl.off_ctl = 0;
   if (!nll) {
-    o = o > (size_t)4 * L.Q * 1024 ? o : (size_t)4 * L.Q * 1024;
-    const size_t ctl = 1088 + (size_t)8 * L.Z;  // logits, wave bests, two latent rows
-    o = o > ctl ? o : ctl;
+    o = o > (size_t)4 * (L.Q + 1) * 1024 ? o : (size_t)4 * (L.Q + 1) * 1024;
+    pl.off_cb = (int)o;
+    o += (size_t)kMaxPairs * 16 * 8;  // best score and action per (pair, row)
+    pl.off_rows = (int)o;
+    o += (size_t)4 * 64 * 4;          // actions, done state, previous actions, horizons
   }
-  pl.off_hb = (int)o;
-  if (!nll) o += (size_t)rb * 1024;
   o = (o + 15) & ~(size_t)15;
   pl.off_wat = (int)o;
   const size_t wat = (size_t)L.A * 64 * nbc;
@@ -878,9 +1083,9 @@ bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
     pl.wat_lds = 1;
     o += wat;
   }
-  o = (o + 15) & ~(size_t)15;
+  o = (o + 1023) & ~(size_t)1023;
   pl.off_wcz = (int)o;
-  const size_t wcz = (size_t)L.Nc * L.Z * 4;
+  const size_t wcz = (size_t)pl.ncb * ((L.Z + 15) / 16) * 1024;  // A fragments of W_c's z columns
   if (!nll && o + wcz <= kLdsMax) {
     pl.wcz_lds = 1;
     o += wcz;
@@ -949,8 +1154,10 @@ PArgs base_args(const Packed& P, const PPlan& pl, int B, int T) {
   a.wat_lds = pl.wat_lds;
   a.wcz_lds = pl.wcz_lds;
   a.off_wcz = pl.off_wcz;
-  a.off_red = pl.off_red; a.off_hb = pl.off_hb; a.off_wat = pl.off_wat;
-  a.off_mdn = pl.off_mdn; a.off_ctl = pl.off_ctl; a.off_flags = pl.off_flags;
+  a.off_red = pl.off_red; a.off_rows = pl.off_rows; a.off_wat = pl.off_wat;
+  a.off_mdn = pl.off_mdn; a.off_cb = pl.off_cb; a.off_flags = pl.off_flags;
+  a.ncb = pl.ncb;
+  a.ctl_sep = pl.ctl_sep;
   return a;
 }
 
@@ -959,7 +1166,7 @@ PArgs base_args(const Packed& P, const PPlan& pl, int B, int T) {
 size_t persist_partial_bytes(const Layout& L, int B) {
   PPlan pl;
   if (!plan(L, B, false, pl)) return 0;
-  return (size_t)kMembers * B * L.Nc * 4;
+  return (size_t)B * L.Nc * 4;  // Lh
 }
 
 bool persist_usable(const Layout& L, int B, bool nll) {
@@ -980,7 +1187,7 @@ hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStre
   if (!persist_enabled() || !plan(P.L, R.B, false, pl) || !R.P || !R.sync || !device_fits())
     return hipErrorNotSupported;
   PArgs a = base_args(P, pl, R.B, R.T);
-  attach_stamps(a, 2 + 3 * R.T, false, s);
+  attach_stamps(a, 2 + 2 * R.T, false, s);
   a.k0 = R.k0; a.k1 = R.k1; a.traj0 = R.traj0; a.step0 = R.step0;
   a.tau = R.tau;
   a.sig = (R.flags & WM_FLAG_SIGMA_TAU) ? sqrtf(R.tau) : 1.0f;
@@ -990,7 +1197,7 @@ hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStre
   a.c = R.c;
   a.done_state = R.done_state;
   a.lengths = R.lengths;
-  a.P = R.P;
+  a.Lh = R.P;
   a.sync = R.sync;
   a.mask = R.mask;
   a.z_out = R.z_out;

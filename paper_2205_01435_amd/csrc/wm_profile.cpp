@@ -170,20 +170,18 @@ void phase_summary(const std::vector<unsigned long long>& st, int groups, int ns
       acc[1] += (double)(last_end() - first_release(1)) * tick_us / T;
       work(0, 1, pro, dummy);
     } else {
-      // barriers 1, 2 end the set-up; 3 + 3t, 4 + 3t, 5 + 3t follow ctrl(t),
-      // gates(t), mdn(t)
+      // barriers 1, 2 end the set-up; 3 + 2t and 4 + 2t follow gates(t)
+      // (which makes the step's controller decisions) and mdn(t)
       for (int t = 0; t < T; ++t) {
-        const int b = 3 + 3 * t;
-        work(b - 1, b, acc[2], acc[8]);
-        acc[3] += latency(b);
-        work(b, b + 1, acc[4], acc[9]);
-        acc[5] += latency(b + 1);
-        work(b + 1, b + 2, acc[6], acc[10]);
-        acc[7] += latency(b + 2);
+        const int b = 3 + 2 * t;
+        work(b - 1, b, acc[4], acc[9]);
+        acc[5] += latency(b);
+        work(b, b + 1, acc[6], acc[10]);
+        acc[7] += latency(b + 1);
       }
-      acc[1] += (double)(first_release(2 + 3 * T) - first_release(2)) * tick_us / T;
+      acc[1] += (double)(first_release(2 + 2 * T) - first_release(2)) * tick_us / T;
       work(0, 2, pro, dummy);
-      work(2 + 3 * T, 0, epi, dummy);
+      work(2 + 2 * T, 0, epi, dummy);
     }
     acc[11] += pro;
     acc[12] += epi;

@@ -25,17 +25,15 @@ from . import workloads as wl
 
 DESCR = {
     "step": "wall time per step (first release of the set-up barrier to that of the last step's)",
-    "ctrl": "ctrl(t): controller logits, masked Gumbel-max, transition t-1 (max over an XCD's work-groups)",
-    "ctrl_barrier": "barrier after ctrl(t): last arrival to first release",
-    "gates": "gates(t): staging, gate MFMAs, LSTM cell, controller partials (max); NLL: the step",
-    "gates_barrier": "barrier after gates(t)",
-    "mdn": "mdn(t): mixture head, component pick, Box-Muller, z commit (max)",
-    "mdn_barrier": "barrier after mdn(t)",
-    "ctrl_mean": "ctrl(t), mean over the work-groups",
+    "gates": "gates(t): staging, gate MFMAs, controller decisions, LSTM cell (max over an XCD's "
+             "work-groups); NLL: the step",
+    "gates_barrier": "barrier after gates(t): last arrival to first release (the mixture noise is drawn in it)",
+    "mdn": "mdn(t): mixture head, component pick, Box-Muller, z commit, next controller h part (max)",
+    "mdn_barrier": "barrier after mdn(t) (the controller's Gumbel noise is drawn in it)",
     "gates_mean": "gates(t), mean",
     "mdn_mean": "mdn(t), mean",
-    "setup": "set-up: register weights, LDS tables, step-0 partials (max, once per call)",
-    "tail": "tail: ctrl(T) resolves the last transition, final cell state (max, once per call)",
+    "setup": "set-up: register weights, LDS tables, step-0 controller h part (max, once per call)",
+    "tail": "tail: the last transition's reward and done, final cell state (max, once per call)",
 }
 
 
@@ -83,10 +81,12 @@ def summary(name: str, res: dict, calls: int) -> str:
              f"Median over {calls} stamped calls of each slot, microseconds per step (set-up and tail: per call).",
              "", "| slot | us | what |", "|---|---:|---|"]
     for k in wmlib.PHASE_SLOTS[1:]:
-        if w.kind == "nll" and k in ("ctrl", "ctrl_barrier", "mdn", "mdn_barrier", "ctrl_mean", "mdn_mean", "tail"):
+        if k in ("ctrl", "ctrl_barrier", "ctrl_mean"):
+            continue  # the controller decisions run inside gates(t)
+        if w.kind == "nll" and k in ("mdn", "mdn_barrier", "mdn_mean", "tail"):
             continue
         lines.append(f"| {k} | {res[k]:.3f} | {DESCR[k]} |")
-    parts = ("ctrl", "ctrl_barrier", "gates", "gates_barrier", "mdn", "mdn_barrier")
+    parts = ("gates", "gates_barrier", "mdn", "mdn_barrier")
     acc = sum(res[k] for k in parts)
     lines += ["", f"Sum of the max-work and barrier slots: {acc:.3f} us of the {res['step']:.3f} us step "
               "(the rest is skew: work-groups leave a barrier at different times).", ""]
