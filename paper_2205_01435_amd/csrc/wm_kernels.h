@@ -125,7 +125,7 @@ hipError_t launch_returns(const ReturnsBufs& R, hipStream_t s);
 
 // World-model training step: gradient of the summed NLL means (fp32).
 struct GradWs {  // workspace after the NLL pass's own
-  float *G, *Cs, *M, *dG, *dhh, *dh, *dc, *WhT, *WmT, *T1, *T2;
+  float *G, *Cs, *M, *dG, *dhh, *dh, *dc;
   float *dWgT, *dWa, *dWm, *dbg, *dbm, *part, *apart, *split, *nsum, *fwd;
 };
 struct GradOut {  // canonical gradients; loss (nullable): the summed means

@@ -109,9 +109,37 @@ __global__ void k_pack(const Layout L, char* base, const float* __restrict__ W_g
       }
       DType<DT>::store(Wc, idx, v);
     }
-  } else {
+  } else if (section == 6) {
     for (long idx = i0; idx < L.Nc; idx += stride)
       bc[idx] = idx < L.Ac ? b_c[idx] : (idx == L.Ac ? b_r[0] : (idx == L.Ac + 1 ? b_d[0] : 0.f));
+  } else if constexpr (sizeof(DT) == 4) {
+    if (section == 7) {  // WhT[i][r] = Wg[r][Z + i]
+      float* WhT = reinterpret_cast<float*>(base + L.off_WhT);
+      for (long idx = i0; idx < (long)H * 4 * H; idx += stride) {
+        const int i = (int)(idx / (4 * H)), r = (int)(idx % (4 * H));
+        WhT[idx] = W_g[((long)(r % 4) * H + r / 4) * cg + A + Z + i];
+      }
+    } else if (section == 8) {  // WmT[i][r] = Wm[r][i], zero past Nm
+      float* WmT = reinterpret_cast<float*>(base + L.off_WmT);
+      for (long idx = i0; idx < (long)H * L.NmP; idx += stride) {
+        const int i = (int)(idx / L.NmP), row = (int)(idx % L.NmP);
+        float v = 0.f;
+        if (row >= head0 && row < L.Nm) {
+          const int hr = row - head0;
+          v = hr == 0 ? w_r[i] : (hr == 1 ? w_d[i] : 0.f);
+        } else if (row < head0) {
+          const int J = row / (16 * Q), rem = row % (16 * Q);
+          const int q = rem / 16, g = (rem % 16) / 4, vv = rem % 4;
+          const int j = 4 * J + g, f = 4 * q + vv;
+          long canon = -1;
+          if (f < K) canon = (long)j * K + f;
+          else if (f < 2 * K) canon = (long)Z * K + (long)j * K + (f - K);
+          else if (f < 3 * K) canon = 2L * Z * K + (long)j * K + (f - 2 * K);
+          if (canon >= 0) v = W_m[canon * H + i];
+        }
+        WmT[idx] = v;
+      }
+    }
   }
 }
 
@@ -2482,12 +2510,11 @@ hipError_t launch_pack(const Packed& P, void* packed, const float* W_g, const fl
                        const float* W_m, const float* b_m, const float* w_r, const float* b_r,
                        const float* w_d, const float* b_d, const float* W_c, const float* b_c,
                        hipStream_t s) {
-  dim3 grid(1024, 7);
   char* out = reinterpret_cast<char*>(packed);
-  if (P.L.dt == 0)
-    return launch("pack", k_pack<float>, grid, dim3(256), 0, s, P.L, out, W_g, b_g, W_m, b_m, w_r, b_r,
-                  w_d, b_d, W_c, b_c);
-  return launch("pack", k_pack<bf16_t>, grid, dim3(256), 0, s, P.L, out, W_g, b_g, W_m, b_m, w_r, b_r,
+  if (P.L.dt == 0)  // two more sections: the transposed copies
+    return launch("pack", k_pack<float>, dim3(1024, 9), dim3(256), 0, s, P.L, out, W_g, b_g, W_m, b_m, w_r,
+                  b_r, w_d, b_d, W_c, b_c);
+  return launch("pack", k_pack<bf16_t>, dim3(1024, 7), dim3(256), 0, s, P.L, out, W_g, b_g, W_m, b_m, w_r, b_r,
                 w_d, b_d, W_c, b_c);
 }
 
@@ -2580,33 +2607,6 @@ __global__ void __launch_bounds__(C::NT) k_gemm_nt(const float* A, long lda, int
         if (n + v < N) out[(long)m * ldo + n + v] = acc[i][j][v];
     }
   }
-}
-
-// dst[c][r] = src[r][c] for r < R, c < Cc; dst[c][r] = 0 for R <= r < Rp
-__global__ void __launch_bounds__(256) k_transpose(const float* src, long lds_, int R, int Cc, float* dst,
-                                                   long ldd, int Rp) {
-  __shared__ float tile[32][33];
-  const int r0 = blockIdx.x * 32, c0 = blockIdx.y * 32;
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
-  for (int k = ty; k < 32; k += 8) {
-    const int r = r0 + k, c = c0 + tx;
-    tile[k][tx] = (r < R && c < Cc) ? src[(long)r * lds_ + c] : 0.f;
-  }
-  __syncthreads();
-  for (int k = ty; k < 32; k += 8) {
-    const int c = c0 + k, r = r0 + tx;
-    if (c < Cc && r < Rp) dst[(long)c * ldd + r] = tile[tx][k];
-  }
-}
-
-// x[0 .. n) = 0, and = 1
-__global__ void __launch_bounds__(256) k_zero(float* x, long n) {
-  const long i = (long)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) x[i] = 0.f;
-}
-__global__ void __launch_bounds__(256) k_ones(float* x, long n) {
-  const long i = (long)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) x[i] = 1.f;
 }
 
 // N = sum_b min(max(len_b, 0), T) (all B T without lengths)
@@ -2763,32 +2763,6 @@ __global__ void __launch_bounds__(256) k_grad_lstm_back(const float* G, const fl
                   d_o * a.w * (1.0f - a.w));
 }
 
-// column sums of src [R, Cc] in a fixed order: partial sums of row chunks,
-// then their sum (two launches)
-constexpr int kSumChunks = 64;
-__global__ void __launch_bounds__(256) k_colsum_part(const float* src, long ld, long R, int Cc, float* part) {
-  const int c = blockIdx.x * 256 + threadIdx.x, ch = blockIdx.y;
-  if (c >= Cc) return;
-  const long r0 = R * ch / kSumChunks, r1 = R * (ch + 1) / kSumChunks;
-  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;  // rows r0 + 4i + 0..3
-  long r = r0;
-  for (; r + 4 <= r1; r += 4) {
-    s0 += src[r * ld + c];
-    s1 += src[(r + 1) * ld + c];
-    s2 += src[(r + 2) * ld + c];
-    s3 += src[(r + 3) * ld + c];
-  }
-  for (; r < r1; ++r) s0 += src[r * ld + c];
-  part[(long)ch * Cc + c] = (s0 + s1) + (s2 + s3);
-}
-__global__ void __launch_bounds__(256) k_colsum_final(const float* part, int Cc, float* out) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= Cc) return;
-  float s = 0.f;
-  for (int ch = 0; ch < kSumChunks; ++ch) s += part[(long)ch * Cc + c];
-  out[c] = s;
-}
-
 // one-hot columns: dWa[a][j] = sum over rows r with action a of dG[r][j].
 // Block (256-column tile, row chunk, group of 64 actions): each thread owns
 // one column and accumulates the chunk's rows in row order into an LDS slot
@@ -2931,6 +2905,161 @@ hipError_t gemm_nt_slices(const char* name, const float* A, long lda, int M, con
                 Ks, out, ldo, oslice, map);
 }
 
+// x[0 .. n) = 0
+__global__ void __launch_bounds__(256) k_zero(float* x, long n) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) x[i] = 0.f;
+}
+
+// ===========================================================================
+// k_gemm_tn: out[m][n] = sum over rows k of A[k][m] B[k][n], both operands
+// row-major with the reduction over their rows (the weight-gradient products
+// over the T B rows read their activation and gradient matrices as stored,
+// no transposed copies).  K slice s covers rows [s Ks, (s+1) Ks) and writes
+// its own partial [M, N] (summed in fp64 afterwards).  128 x 64 tiles, four
+// waves of 64 x 32; chunks of 16 rows reach LDS by LDS-DMA in a ring of four
+// stages.  A fragment read takes rows 4g + j, j < 4, of a chunk (one MFMA
+// each): the 16-byte pieces of staged row k are XOR-permuted by ((k/4) mod 4)
+// * 4, so that the four lane groups g read four distinct 64-byte bank
+// windows.  SUMA / SUMB: the work-groups of the first tile column / row also
+// sum A's / B's columns over their rows (an extra MFMA block against ones)
+// into colsum partials [S, M] / [S, N].  Work-group -> tile: XCD x takes
+// the slices s = x mod 8, each slice's tiles m fastest, so that a slice's
+// rows are shared in one L2.
+// ===========================================================================
+constexpr int kTnBM = 128, kTnBN = 64, kTnBK = 16, kTnStages = 4;
+constexpr int kTnStageBytes = (kTnBM + kTnBN) * kTnBK * 4;  // 12 KB: A rows, then B rows
+
+struct TnArgs {
+  const float* A;
+  const float* Bm;
+  long lda, ldb, K;
+  int Ks, S, M, N, ntm, ntn;
+  float* part;  // [S, M, N] partials (ldp = N)
+  float* csA;   // [S, M] or null
+  float* csB;   // [S, N] or null
+};
+
+__global__ void __launch_bounds__(256) k_gemm_tn(const TnArgs p) {
+  __shared__ __attribute__((aligned(1024))) char lds[kTnStages * kTnStageBytes];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, r16 = lane & 15;
+  const int x = blockIdx.x & 7, r = blockIdx.x >> 3;
+  const int per = p.ntm * p.ntn;
+  const int sl = x + 8 * (r / per);
+  if (sl >= p.S) return;
+  const int nt = (r % per) / p.ntm, mt = (r % per) % p.ntm;
+  const int m0 = mt * kTnBM, n0 = nt * kTnBN;
+  const long k0 = (long)sl * p.Ks;
+  const long k1 = min(p.K, k0 + (long)p.Ks);
+  const int nk = (int)((k1 - k0 + kTnBK - 1) / kTnBK);
+  // the slice's rows only: rows past k1 (and the tail of the last row) read zero
+  const u32x4 ra = rsrc_words(p.A + k0 * p.lda, (uint32_t)((k1 - k0) * p.lda * 4));
+  const u32x4 rb = rsrc_words(p.Bm + k0 * p.ldb, (uint32_t)((k1 - k0) * p.ldb * 4));
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) char*)lds);
+  // this wave's three DMA instructions per chunk: q < 8 stage A rows 2q, 2q+1
+  // (32 pieces each), q >= 8 B rows 4(q-8) .. +3 (16 pieces each)
+  bool isa[3];
+  uint32_t off[3];
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const int q = wave * 3 + t;
+    isa[t] = q < 8;
+    if (isa[t]) {
+      const int row = 2 * q + (lane >> 5), pc = (lane & 31) ^ (((row >> 2) & 3) << 2);
+      off[t] = (uint32_t)(row * p.lda + m0) * 4u + 16u * (uint32_t)pc;
+    } else {
+      const int row = 4 * (q - 8) + (lane >> 4), pc = (lane & 15) ^ (((row >> 2) & 3) << 2);
+      off[t] = (uint32_t)(row * p.ldb + n0) * 4u + 16u * (uint32_t)pc;
+    }
+  }
+  const uint32_t stepa = (uint32_t)(kTnBK * p.lda) * 4u, stepb = (uint32_t)(kTnBK * p.ldb) * 4u;
+  auto issue = [&](int kc) {
+    const uint32_t base = lds0 + (uint32_t)(kc % kTnStages) * kTnStageBytes + (uint32_t)wave * 3u * 1024u;
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+      dma16(isa[t] ? ra : rb, off[t] + (uint32_t)kc * (isa[t] ? stepa : stepb), base + 1024u * t);
+  };
+#pragma unroll
+  for (int c = 0; c < kTnStages - 1; ++c)
+    if (c < nk) issue(c);
+
+  const int wm = wave >> 1, wn = wave & 1;
+  const bool suma = p.csA && nt == 0 && wn == 0;  // wave-uniform
+  const bool sumb = p.csB && mt == 0 && wm == 0;
+  f32x4 acc[4][2], cs[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    acc[i][0] = acc[i][1] = cs[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  // lane byte offsets inside a stage: A element (4g + j, (wm 4 + i) 16 + r16),
+  // B element (4g + j, (wn 2 + jb) 16 + r16)
+  uint32_t oa[4], ob[2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) oa[i] = (uint32_t)(4 * g * 512 + (((wm * 4 + i) ^ g) & 7) * 64 + r16 * 4);
+#pragma unroll
+  for (int jb = 0; jb < 2; ++jb) ob[jb] = (uint32_t)(kTnBM * kTnBK * 4 + 4 * g * 256 + (((wn * 2 + jb) ^ g) & 3) * 64 + r16 * 4);
+  for (int kc = 0; kc < nk; ++kc) {
+    const int young = min(kTnStages - 2, nk - 1 - kc);
+    if (young >= 2) vm_wait<6>();
+    else if (young == 1) vm_wait<3>();
+    else vm_wait<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" : : : "memory");
+    if (kc + kTnStages - 1 < nk) issue(kc + kTnStages - 1);
+    const char* buf = lds + (kc % kTnStages) * kTnStageBytes;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float a[4], b[2];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const float*>(buf + oa[i] + j * 512);
+#pragma unroll
+      for (int jb = 0; jb < 2; ++jb) b[jb] = *reinterpret_cast<const float*>(buf + ob[jb] + j * 256);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int jb = 0; jb < 2; ++jb) acc[i][jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[jb], acc[i][jb], 0, 0, 0);
+      if (suma) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cs[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], 1.0f, cs[i], 0, 0, 0);
+      }
+      if (sumb) {
+#pragma unroll
+        for (int jb = 0; jb < 2; ++jb) cs[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(1.0f, b[jb], cs[jb], 0, 0, 0);
+      }
+    }
+  }
+  // lane (g, r16) holds C[4g + v][r16]: rows m, columns n
+  float* part = p.part + (long)sl * p.M * p.N;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int jb = 0; jb < 2; ++jb) {
+      const int n = n0 + (wn * 2 + jb) * 16 + r16;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = m0 + (wm * 4 + i) * 16 + 4 * g + v;
+        if (m < p.M && n < p.N) part[(long)m * p.N + n] = acc[i][jb][v];
+      }
+    }
+  if (suma && r16 == 0) {  // every column of C holds A's column sums
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = m0 + (wm * 4 + i) * 16 + 4 * g + v;
+        if (m < p.M) p.csA[(long)sl * p.M + m] = cs[i][v];
+      }
+  }
+  if (sumb && g == 0) {  // every row of C holds B's column sums
+#pragma unroll
+    for (int jb = 0; jb < 2; ++jb) {
+      const int n = n0 + (wn * 2 + jb) * 16 + r16;
+      if (n < p.N) p.csB[(long)sl * p.N + n] = cs[jb][0];
+    }
+  }
+}
+
 // The weight-gradient products reduce over all T B rows.  A K slice
 // accumulates its products in fp32, one MFMA after another, so its rounding
 // error grows with the slice's length; the slices are therefore kept to at
@@ -2965,17 +3094,35 @@ hipError_t gemm_nt(const float* A, long lda, int M, const float* Bm, long ldb, i
                 N, out, ldo);
 }
 
-hipError_t transpose(const float* src, long ld, int R, int Cc, float* dst, long ldd, int Rp, hipStream_t s) {
-  return launch("grad_transpose", k_transpose, dim3((unsigned)((Rp + 31) / 32), (unsigned)((Cc + 31) / 32)),
-                dim3(256), 0, s, src, ld, R, Cc, dst, ldd, Rp);
-}
+// K slices of a product over K rows (kMaxSliceK rows each)
+inline int tn_slices(long K) { return (int)((K + kMaxSliceK - 1) / kMaxSliceK); }
 
-hipError_t colsum(const float* src, long ld, long R, int Cc, float* part, float* out, hipStream_t s) {
-  hipError_t e = launch("grad_colsum", k_colsum_part, dim3((unsigned)((Cc + 255) / 256), kSumChunks),
-                        dim3(256), 0, s, src, ld, R, Cc, part);
+// out (ldo) = A^T B over the K rows of both (A [K, lda] with M used columns,
+// B [K, ldb] with N), through the slice partials `part` ([S, M, N]) summed in
+// fp64; with csA (csB) also the column sums of A (B) into colsum ([M] or [N],
+// slice partials in cpart [S, M or N]).
+hipError_t gemm_tn(const float* A, long lda, int M, const float* Bm, long ldb, int N, long K, float* part,
+                   float* out, long ldo, bool sum_a, bool sum_b, float* cpart, float* colsum, hipStream_t s) {
+  if (sum_a && sum_b) return hipErrorInvalidValue;  // one colsum register set per wave
+  TnArgs a{};
+  a.A = A; a.Bm = Bm; a.lda = lda; a.ldb = ldb; a.K = K;
+  a.Ks = kMaxSliceK;
+  a.S = tn_slices(K);
+  a.M = M; a.N = N;
+  a.ntm = (M + kTnBM - 1) / kTnBM;
+  a.ntn = (N + kTnBN - 1) / kTnBN;
+  a.part = part;
+  a.csA = sum_a ? cpart : nullptr;
+  a.csB = sum_b ? cpart : nullptr;
+  const long nwg = (long)((a.S + 7) / 8) * 8 * a.ntm * a.ntn;
+  hipError_t e = launch("grad_gemm_tn", k_gemm_tn, dim3((unsigned)nwg), dim3(256), 0, s, a);
   if (e != hipSuccess) return e;
-  return launch("grad_colsum", k_colsum_final, dim3((unsigned)((Cc + 255) / 256)), dim3(256), 0, s, part, Cc,
-                out);
+  e = launch("grad_sum", k_sum_slices, dim3((unsigned)(((long)M * N + 255) / 256)), dim3(256), 0, s,
+             (const float*)part, a.S, M, N, out, ldo);
+  if (e != hipSuccess || !(sum_a || sum_b)) return e;
+  const int nc = sum_a ? M : N;
+  return launch("grad_sum", k_sum_slices, dim3((unsigned)((nc + 255) / 256)), dim3(256), 0, s, (const float*)cpart,
+                a.S, 1, nc, colsum, (long)nc);
 }
 
 template <int KC>
@@ -3003,12 +3150,9 @@ size_t grad_workspace(const Layout& L, int B, int T, char* ws, GradWs* G) {
   const size_t oG = take((size_t)TB * H4 * 4), oC = take((size_t)(T + 1) * B * H * 4);
   const size_t oM = take((size_t)TB * NmP * 4), odG = take((size_t)TB * H4 * 4);
   const size_t odhh = take((size_t)TB * H * 4), odh = take((size_t)B * H * 4), odc = take((size_t)B * H * 4);
-  const size_t oWhT = take((size_t)H * H4 * 4), oWmT = take((size_t)H * NmP * 4);
-  const size_t oT1 = take((size_t)std::max(H4, NmP) * TBp * 4);   // dG^T or dM^T
-  const size_t oT2 = take((size_t)std::max(L.ldk, H) * TBp * 4);  // X^T or H^T
   const size_t odWgT = take((size_t)L.ldk * H4 * 4), odWa = take((size_t)L.A * H4 * 4);
   const size_t odWm = take((size_t)NmP * H * 4), odbg = take((size_t)H4 * 4), odbm = take((size_t)NmP * 4);
-  const size_t opart = take((size_t)kSumChunks * std::max(H4, NmP) * 4);
+  const size_t opart = take((size_t)std::max(kFlatBlocks, tn_slices(TB)) * std::max(H4, NmP) * 4);
   const size_t oapart = take((size_t)act_chunks(L) * L.A * H4 * 4);
   // split-K partials: the largest of the products that split, and the
   // per-step slices of dG_t . W_h (always)
@@ -3018,14 +3162,14 @@ size_t grad_workspace(const Layout& L, int B, int T, char* ws, GradWs* G) {
   };
   const size_t nsplit = std::max({(size_t)bptt_split(B, H) * B * H, split_need((int)TB, H4, L.ldk),
                                   split_need((int)TB, L.Nm, L.ldh), split_need((int)TB, H, NmP),
-                                  split_need(L.ldk, H4, (int)TBp, true), split_need(NmP, H, (int)TBp, true)});
+                                  (size_t)tn_slices(TB) * L.ldk * H4, (size_t)tn_slices(TB) * NmP * H});
   const size_t osplit = take(nsplit * 4);
   const size_t on = take(16);
   const size_t ofwd = take((size_t)TB * (L.Z + 1) * 4);  // loss terms [TB, Z+1]
   if (ws && G) {
     auto f = [&](size_t at) { return reinterpret_cast<float*>(ws + at); };
     G->G = f(oG); G->Cs = f(oC); G->M = f(oM); G->dG = f(odG); G->dhh = f(odhh); G->dh = f(odh);
-    G->dc = f(odc); G->WhT = f(oWhT); G->WmT = f(oWmT); G->T1 = f(oT1); G->T2 = f(oT2);
+    G->dc = f(odc);
     G->dWgT = f(odWgT); G->dWa = f(odWa); G->dWm = f(odWm); G->dbg = f(odbg); G->dbm = f(odbm);
     G->part = f(opart); G->apart = f(oapart); G->split = f(osplit); G->nsum = f(on); G->fwd = f(ofwd);
   }
@@ -3043,6 +3187,8 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
   const float* bg = reinterpret_cast<const float*>(base + L.off_bg);
   const float* Wm = reinterpret_cast<const float*>(base + L.off_Wm);
   const float* bm = reinterpret_cast<const float*>(base + L.off_bm);
+  const float* WhT = reinterpret_cast<const float*>(base + L.off_WhT);  // [H, 4H]
+  const float* WmT = reinterpret_cast<const float*>(base + L.off_WmT);  // [H, NmP]
   const float* X = reinterpret_cast<const float*>(N.x);
   const float* Hn = X + (long)B * L.ldx + Z;  // h_1 .. h_T: rows of X_1 .. X_T from column Z
   hipError_t e;
@@ -3083,45 +3229,33 @@ hipError_t launch_nll_grad(const Packed& P, NllBufs N, const GradWs& G, const Gr
     WM_TRY(launch("grad_loss", k_flat_sum, dim3(1), dim3(256), 0, s, (const float*)G.part, (long)kFlatBlocks,
                   out.loss));
   }
-  // d loss / d h_{t+1} through the heads: dM [TB, NmP] . W_m (W_m^T [H, NmP], zero rows padded)
-  WM_TRY(transpose(Wm, L.ldh, L.Nm, H, G.WmT, NmP, NmP, s));
-  WM_TRY(gemm_nt(G.M, NmP, (int)TB, G.WmT, NmP, H, NmP, G.dhh, H, G.split, s));
-  // back through time
-  WM_TRY(transpose(Wg + Z, L.ldk, H4, H, G.WhT, H4, H4, s));  // W_h^T [H, 4H]
+  // d loss / d h_{t+1} through the heads: dM [TB, NmP] . W_m (the packed
+  // W_m^T [H, NmP], zero columns past Nm)
+  WM_TRY(gemm_nt(G.M, NmP, (int)TB, WmT, NmP, H, NmP, G.dhh, H, G.split, s));
+  // back through time (the packed W_h^T [H, 4H])
   const unsigned eg = (unsigned)(((long)B * H + 255) / 256);
   const int Sb = bptt_split(B, H);  // K slices of dG_t . W_h, summed by the next step's kernel
   for (int t = T - 1; t >= 0; --t) {
     WM_TRY(launch("grad_lstm", k_grad_lstm_back, dim3(eg), dim3(256), 0, s, G.G, G.Cs, G.dhh, G.split, Sb, G.dc,
                   G.dG, B, H, t, t == T - 1 ? 1 : 0));
     if (t > 0)
-      WM_TRY(gemm_nt_slices<BpttGemm>("grad_gemm_bptt", G.dG + (long)t * B * H4, H4, B, G.WhT, H4, H, H4, Sb, G.split, H,
+      WM_TRY(gemm_nt_slices<BpttGemm>("grad_gemm_bptt", G.dG + (long)t * B * H4, H4, B, WhT, H4, H, H4, Sb, G.split, H,
                             (long)B * H, s));
   }
-  // dW_g^T [ldk, 4H] = X^T . dG over all rows (operands X^T [ldk, TBp], dG^T [4H, TBp])
-  WM_TRY(transpose(G.dG, H4, (int)TB, H4, G.T1, TBp, (int)TBp, s));
-  WM_TRY(transpose(X, L.ldx, (int)TB, L.ldk, G.T2, TBp, (int)TBp, s));
-  // the bias gradient sum_r dG[r] comes out of the same product when X has a
-  // zero padding column to spare: a row of ones there in X^T
-  const bool ones_row = Z + H < L.ldk;
-  if (ones_row)
-    WM_TRY(launch("grad_ones", k_ones, dim3((unsigned)((TB + 255) / 256)), dim3(256), 0, s,
-                  G.T2 + (long)(Z + H) * TBp, TB));
-  WM_TRY(gemm_nt(G.T2, TBp, L.ldk, G.T1, TBp, H4, (int)TBp, G.dWgT, H4, G.split, s, true));
-  if (!ones_row) WM_TRY(colsum(G.dG, H4, TB, H4, G.part, G.dbg, s));
+  // dW_g^T [ldk, 4H] = X^T . dG over all rows, read as stored; the bias
+  // gradient (dG's column sums) from the same pass
+  WM_TRY(gemm_tn(X, L.ldx, L.ldk, G.dG, H4, H4, TB, G.split, G.dWgT, H4, false, true, G.part, G.dbg, s));
   const int nch = act_chunks(L);
   WM_TRY(launch("grad_actions", k_grad_actions,
                 dim3((unsigned)((H4 + 255) / 256), (unsigned)nch, (unsigned)((A + kActGroup - 1) / kActGroup)),
                 dim3(256), 0, s, G.dG, N.actions, TB, H4, A, nch, G.apart));
   WM_TRY(launch("grad_actions", k_grad_actions_sum, dim3((unsigned)(((long)A * H4 + 255) / 256)), dim3(256), 0,
                 s, G.apart, (long)A * H4, nch, G.dWa));
-  // dW_m [NmP, H] = dM^T . H (operands dM^T [NmP, TBp], H^T [H, TBp])
-  WM_TRY(transpose(G.M, NmP, (int)TB, NmP, G.T1, TBp, (int)TBp, s));
-  WM_TRY(transpose(Hn, L.ldx, (int)TB, H, G.T2, TBp, (int)TBp, s));
-  WM_TRY(gemm_nt(G.T1, TBp, NmP, G.T2, TBp, H, (int)TBp, G.dWm, H, G.split, s, true));
-  WM_TRY(colsum(G.M, NmP, TB, NmP, G.part, G.dbm, s));
+  // dW_m [NmP, H] = dM^T . H over all rows, and the head bias gradient
+  // (dM's column sums)
+  WM_TRY(gemm_tn(G.M, NmP, NmP, Hn, L.ldx, H, TB, G.split, G.dWm, H, true, false, G.part, G.dbm, s));
   // canonical layout
-  const UnpackArgs u{Z, H, A, L.K, L.Q, L.Nm, L.ldk, G.dWgT, G.dWa, ones_row ? G.dWgT + (long)(Z + H) * H4 : G.dbg,
-                     G.dWm, G.dbm,
+  const UnpackArgs u{Z, H, A, L.K, L.Q, L.Nm, L.ldk, G.dWgT, G.dWa, G.dbg, G.dWm, G.dbm,
                      out.W_g, out.b_g, out.W_m, out.b_m, out.w_r, out.b_r, out.w_d, out.b_d};
   WM_TRY(launch("grad_unpack", k_grad_unpack, dim3(1024), dim3(256), 0, s, u));
 #undef WM_TRY

@@ -23,6 +23,11 @@
 //                  xfer rows, the last the NO-OP, then L location rows; the
 //                  world model's actions are then the A = N L pairs).
 //   bc  [Nc]       fp32: b_c (Ac), b_r, b_d, zeros.
+//   fp32 only, for the training gradient's products against transposed
+//   weights (written by the same packing pass):
+//   WhT [H, 4H]    Wg's h columns transposed: WhT[i][r] = Wg[r][Z + i].
+//   WmT [H, NmP]   Wm transposed, NmP = roundup(Nm, 32) (zero columns past
+//                  Nm): WmT[i][r] = Wm[r][i].
 //
 // Activations live in one matrix per step, X [rows, ldx] in the same element
 // type: columns 0..Z-1 hold q(z), Z..Z+H-1 hold h, the rest zero, so that the
@@ -47,7 +52,10 @@ struct Layout {
   int N, Lc;           // two-level controller: xfers and locations (N = 0: one level)
   int Ac;              // controller logit rows: A, or N + 1 + Lc
   int Nc;              // roundup(Ac + 2, 16)
-  size_t off_Wg, off_WaT, off_bg, off_Wm, off_bm, off_Wc, off_bc, total;
+  int NmP;             // roundup(Nm, 32)
+  size_t off_Wg, off_WaT, off_bg, off_Wm, off_bm, off_Wc, off_bc;
+  size_t off_WhT, off_WmT;  // fp32 layouts only (else equal to total)
+  size_t total;
 };
 
 static inline size_t wm_align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -74,6 +82,11 @@ static inline Layout make_layout(int Z, int H, int A, int K, int dt, int N = 0, 
   L.off_bm = o;  o = wm_align256(o + (size_t)L.Nm * 4);
   L.off_Wc = o;  o = wm_align256(o + (size_t)L.Nc * L.ldk * L.esz);
   L.off_bc = o;  o = wm_align256(o + (size_t)L.Nc * 4);
+  L.NmP = wm_roundup(L.Nm, 32);
+  L.off_WhT = o;
+  if (dt == 0) o = wm_align256(o + (size_t)H * 4 * H * 4);
+  L.off_WmT = o;
+  if (dt == 0) o = wm_align256(o + (size_t)H * L.NmP * 4);
   L.total = o;
   return L;
 }
