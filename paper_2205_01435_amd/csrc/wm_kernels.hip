@@ -344,10 +344,16 @@ struct GemmD {
     vm_wait<0>();
   }
 
-  template <class S>
+  // GPERM: tile row 64 w + 16 i + 4 g + v of the weights is packed row
+  // 64 w + 16 g + 4 v + i, so that with four 16-row blocks per wave, block i
+  // of a wave holds gate i of 16 consecutive hidden units and lane (g, r16)
+  // gets all four gates of units 4 g .. 4 g + 3 (the packed rows interleave
+  // the gates per unit: row 4 u + q)
+  template <class S, bool GPERM = false>
   __device__ __forceinline__ static void run(f32x4 (&acc)[NBW][MBW], const SrcX<DT>& w, const S& x,
                                              int Kpad, DT* lds) {
     static_assert(!S::kTwo, "the direct core reads one activation matrix");
+    static_assert(!GPERM || NBW == 4, "the gate permutation needs four blocks per wave");
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 4, r16 = lane & 15;
@@ -370,7 +376,8 @@ struct GemmD {
       const int row = 8 * q + (lane >> 3);
       const int c = (lane & 7) ^ ((row >> 1) & 7);
       isw[t] = q < BN / 8;
-      off[t] = isw[t] ? w.row(row) + 16u * c : x.row(row - BN) + 16u * c;
+      const int wr = GPERM ? (row & ~63) | (((row >> 2) & 3) << 4) | ((row & 3) << 2) | ((row >> 4) & 3) : row;
+      off[t] = isw[t] ? w.row(wr) + 16u * c : x.row(row - BN) + 16u * c;
     }
     const int nk = Kpad / BK;
     auto issue = [&](int kc) {
@@ -744,6 +751,56 @@ __global__ void __launch_bounds__(C::NT) k_gates(const GatesArgs p) {
       for (int t = 0; t < 4; ++t) gsum[t] = *reinterpret_cast<const float4*>(E + r * ELD + 16 * grp + 4 * t);
       io.commit(rp + r, u0, uok && m0 + rp + r < p.M, in[k], gsum);
     }
+  }
+}
+
+// Gate kernel with the epilogue straight from the MFMA accumulators (four
+// 16-row blocks per wave, no split K): the weight tile is loaded with the
+// gate permutation of GemmD::run, so lane (g, r16) holds, in acc[q][j][v],
+// gate q of unit n0/4 + 16 wn + 4 g + v for row (wm MBW + j) 16 + r16 of the
+// tile.  Each lane then runs the LSTM cell of four consecutive units of its
+// MBW rows, with the next row's loads in flight under the current row's
+// cell; no LDS staging, no barrier after the GEMM.
+template <class C>
+__global__ void __launch_bounds__(C::NT) k_gates_direct(const GatesArgs p) {
+  using DT = typename C::DT;
+  constexpr int MBW = C::MBW;
+  static_assert(C::NBW == 4 && C::KSPLIT == 1, "four gate blocks per wave");
+  __shared__ __attribute__((aligned(16))) char lds_raw[C::LDS_BYTES];
+  int nt, mt;
+  if (!tile_of(p.map, nt, mt)) return;
+  const int n0 = nt * C::BN, m0 = mt * C::BM;
+  const int lane = threadIdx.x & 63, g = lane >> 4, r16 = lane & 15;
+  const int wn = C::wn(), wmi = C::wm();
+  const int u0 = n0 / 4 + 16 * wn + 4 * g;  // this lane's four units
+  // the lane's rows and their actions, fetched ahead of the GEMM
+  int act[MBW];
+#pragma unroll
+  for (int j = 0; j < MBW; ++j) {
+    const int m = m0 + (wmi * MBW + j) * 16 + r16;
+    act[j] = m < p.M ? p.act[m] : -1;
+  }
+  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wg), p.ldk, p.ldk, n0, C::BN, 4 * p.H);
+  const SrcX<DT> x(reinterpret_cast<const DT*>(p.x_in), p.ldx, p.ldx, m0, C::BM, p.M);
+  f32x4 acc[4][MBW];
+  C::template run<SrcX<DT>, true>(acc, w, x, (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
+
+  const Gate4IO<DT> io(p, m0, C::BM);
+  const bool uok = u0 < p.H;  // H % 16 == 0: the four units are inside together
+  float4 b[4];
+  io.bias(u0, uok, b);
+  auto row_of = [&](int j) { return (wmi * MBW + j) * 16 + r16; };
+  auto ok_of = [&](int j) { return uok && m0 + row_of(j) < p.M; };
+  Gate4In cur = io.load(row_of(0), u0, act[0], ok_of(0), b);
+#pragma unroll
+  for (int j = 0; j < MBW; ++j) {
+    Gate4In nxt;
+    if (j + 1 < MBW) nxt = io.load(row_of(j + 1), u0, act[j + 1], ok_of(j + 1), b);
+    float4 gs[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) gs[t] = make_float4(acc[0][j][t], acc[1][j][t], acc[2][j][t], acc[3][j][t]);
+    io.commit(row_of(j), u0, ok_of(j), cur, gs);
+    if (j + 1 < MBW) cur = nxt;
   }
 }
 
@@ -2090,8 +2147,15 @@ hipError_t launch_gates(GatesArgs a, hipStream_t s) {
   }
   if (a.M <= kSmallRows) return launch_gates_cfg<typename Cfgs<DT>::GatesSmall, DT>(a, s);
   using XL = typename Cfgs<DT>::GatesXL;
-  if (Cfgs<DT>::kXL && (long)((4 * a.H + XL::BN - 1) / XL::BN) * ((a.M + XL::BM - 1) / XL::BM) >= kXLTiles)
-    return launch_gates_cfg<XL, DT>(a, s);
+  if (Cfgs<DT>::kXL && (long)((4 * a.H + XL::BN - 1) / XL::BN) * ((a.M + XL::BM - 1) / XL::BM) >= kXLTiles) {
+    if constexpr (sizeof(DT) == 2 && XL::NBW == 4 && XL::KSPLIT == 1) {
+      a.map = tile_map((4 * a.H + XL::BN - 1) / XL::BN, (a.M + XL::BM - 1) / XL::BM,
+                       (size_t)4 * a.H * a.ldk * sizeof(DT));
+      return launch("gates", k_gates_direct<XL>, dim3(grid_of(a.map)), dim3(XL::NT), 0, s, a);
+    } else {
+      return launch_gates_cfg<XL, DT>(a, s);
+    }
+  }
   return launch_gates_cfg<typename Cfgs<DT>::GatesLarge, DT>(a, s);
 }
 
