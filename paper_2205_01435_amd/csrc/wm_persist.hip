@@ -505,14 +505,21 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
     if (KSPLIT > 1) n += valid_in(c, 1) * rbv;
     return n > wave ? (n - wave + 3) >> 2 : 0;
   };
-  auto issue = [&](int c, int k) {
+  // the (slice, row block) of load k of chunk c of this wave
+  auto piece = [&](int c, int k, int& sl, int& rb) {
     int r = wave + 4 * k, kq = 0;
     const int n0 = valid_in(c, 0) * rbv;
     if (KSPLIT > 1 && r >= n0) {
       kq = 1;
       r -= n0;
     }
-    const int sl = kq * nper + 9 * c + r / rbv, rb = r % rbv;
+    const int q = RB == 1 ? r : (rbv == RB ? r / RB : r / rbv);
+    sl = kq * nper + 9 * c + q;
+    rb = r - q * (RB == 1 ? 1 : rbv);
+  };
+  auto issue = [&](int c, int k) {
+    int sl, rb;
+    piece(c, k, sl, rb);
     const uint32_t voff = (uint32_t)(16 * rb + (lane >> 2)) * ldxb + (uint32_t)sl * 64u + (uint32_t)(lane & 3) * 16u;
     // The NLL recurrence keeps every X_t (no ring), so this CU has never
     // read these lines before and its L1 cannot hold a stale copy: the
@@ -523,8 +530,13 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
     else cdma16(rsx, voff, lds0 + (uint32_t)(sl * RB + rb) * 1024u);
   };
   // few loads per wave (small batches): every chunk goes out at once and
-  // one wait covers them all; else chunk 0 now and the rest under the MFMAs
-  const bool eager = wave_count(0) + wave_count(1) + wave_count(2) + wave_count(3) <= 12;
+  // one wait covers them all; else chunk 0 now and the rest under the MFMAs.
+  // Decided for the whole work-group, so that the waves' barriers pair up:
+  // at most 48 loads in all, so at most 12 per wave.
+  int nall = 0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) nall += (valid_in(c, 0) + (KSPLIT > 1 ? valid_in(c, 1) : 0)) * rbv;
+  const bool eager = nall <= 48;
   {
     const int n0 = wave_count(0);
     for (int k = 0; k < n0; ++k) issue(0, k);
