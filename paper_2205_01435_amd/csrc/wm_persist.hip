@@ -76,12 +76,13 @@ struct PArgs {
   uint32_t k0, k1, traj0, step0;
   float tau;
   float sig;  // scale of the normal deviate (sqrt(tau) with the sigma temperature, else 1)
-  int use_done, wat_lds, wcz_lds;
+  int use_done, wat_lds;
   float* X;             // rollout [2, B, ldx]; NLL [T+1, B, ldx]
   float* c;             // [B, H]: initial cell state in, final state out (rollout)
   int32_t* done_state;  // [B]
   const int32_t* lengths;  // [B] per-trajectory horizons, or null
   float* Lh;            // [B, Nc] controller logits' h part + bias (rollout)
+  unsigned* flags;      // [B] step t's action of row m is written once flags[m] > t (rollout)
   unsigned* sync;       // kSyncWords words, zero at launch
   const uint8_t* mask;  // [B, A], or [T, B, A] with step_mask
   int step_mask;
@@ -92,7 +93,7 @@ struct PArgs {
   float *h_trace, *c_trace;  // [T+1, B, H] or null (each on its own)
   float* g_trace;            // NLL: gate activations [T, B, 4H] or null
   // LDS carve-up (bytes)
-  int off_red, off_rows, off_wat, off_wcz, off_mdn, off_cb, off_flags;
+  int off_red, off_rows, off_wat, off_mdn, off_ctl, off_flags;
   // controller: Nc / 16 logit blocks; the h-part blocks run as tiles of
   // their own in mdn(t) (1) or inside the first mixture tiles (0)
   int ncb, ctl_sep;
@@ -223,243 +224,189 @@ struct GateState {
 };
 
 // ---------------------------------------------------------------------------
-// Controller decisions (rollout).  Every work-group of an XCD decides for all
-// of the XCD's rows, in the MFMA output layout: pair p = (cb, rb) covers
-// logits 16 cb .. 16 cb + 15 of rows 16 rb .. 16 rb + 15, and lane (g, r16)
-// of the wave that owns it (wave p % 4) holds logits 16 cb + 4 g + v,
-// v < 4, of row 16 rb + r16: one Philox block of stream 0 and one 16-byte
-// read of Lh per lane and pair.
+// Controller decisions (rollout).  Row m of an XCD (m < 64) is owned by
+// work-group m % 32 of the XCD, which decides its action at the start of
+// gates(t), while its staging loads are in flight: logits = W_c,z q(z_t) (one
+// thread per action, W_c's z columns from L2) + Lh (the h part and the bias,
+// written by mdn(t-1)), plus the Gumbel noise drawn at the barrier; the best
+// valid action, lowest index on ties; then the bookkeeping of transition t-1
+// and step t.  The owner writes the action and then the row's flag (t + 1);
+// every work-group waits for the flags of the XCD's rows only before its
+// cell epilogue, which needs the actions.
 // ---------------------------------------------------------------------------
-// controller pairs per wave for RB row blocks: every pair of Nc <= 128
-// logits for one or two row blocks, Nc <= 80 for four
-template <int RB>
-constexpr int ctrl_cp() { return RB == 1 ? 2 : (RB == 2 ? 4 : 5); }
-constexpr int kMaxPairs = 4 * ctrl_cp<4>();
+constexpr int kMaxOwn = 2;  // rows per work-group: 64 rows per XCD at most
 
-template <int CP>
 struct CtrlLane {
-  float4 gum[CP];  // Gumbel noise of the lane's logits, -inf where the action is not valid
-  float4 lh[CP];   // h part + bias of the lane's logits
-  float rr, rd;    // reward and done logits of row tid (tid < rows): transition t-1
-  float ud;        // the stream-3 uniform of transition t-1 of row tid
+  float gum[kMaxOwn];  // thread a's Gumbel noise for action a of each owned row; -inf: not valid
+  float ud[kMaxOwn];   // the stream-3 uniform of transition t-1 of each owned row
 };
-
-// The uniform that decides whether transition t-1 of row tid ended.
-template <int CP>
-__device__ __forceinline__ void ctrl_done_uniform(const PArgs& p, CtrlLane<CP>& cl, int t, int r0, int nrows) {
-  cl.ud = 0.f;
-  if (p.use_done && t > 0 && (int)threadIdx.x < nrows) {
-    const Rng rng{p.k0, p.k1};
-    const uint4 w = rng.block(0, p.step0 + (uint32_t)t - 1u, p.traj0 + (uint32_t)(r0 + threadIdx.x), STREAM_DONE);
-    cl.ud = word_to_uniform(w.x);
-  }
-}
 
 __device__ __forceinline__ int* row_act(const PArgs& p, char* lds) { return reinterpret_cast<int*>(lds + p.off_rows); }
 __device__ __forceinline__ int* row_done(const PArgs& p, char* lds) { return row_act(p, lds) + 64; }
 __device__ __forceinline__ int* row_prev(const PArgs& p, char* lds) { return row_act(p, lds) + 128; }
 __device__ __forceinline__ int* row_len(const PArgs& p, char* lds) { return row_act(p, lds) + 192; }
 
-// The Gumbel noise of step t (drawn while the work-group waits at a barrier;
-// a valid action's score is its logit plus the noise, the argmax the action).
-template <int CP>
-__device__ __forceinline__ void ctrl_noise(const PArgs& p, CtrlLane<CP>& cl, int t, int r0, int nrows) {
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int g = lane >> 4, r16 = lane & 15;
-  const int np = p.ncb * ((nrows + 15) >> 4);
+// The random numbers of step t for this work-group's rows (drawn while it
+// waits at a barrier): thread a takes action a's Gumbel score (-inf where
+// the action is not valid), and the done uniforms of transition t-1.
+// t == T: the done uniforms only.
+__device__ __forceinline__ void ctrl_noise(const PArgs& p, CtrlLane& cl, int t, int r0, int nrows) {
+  const int a = threadIdx.x, s = blockIdx.x >> 3;
   const Rng rng{p.k0, p.k1};
   const uint32_t step = p.step0 + (uint32_t)t;
-  const uint8_t* mask = p.mask + (p.step_mask ? (long)t * p.B * p.A : 0);  // [B, A] of step t
 #pragma unroll
-  for (int k = 0; k < CP; ++k) {
-    float v[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-    const int pi = wave + 4 * k;
-    const int cb = pi % p.ncb, rb = pi / p.ncb;
-    const int ml = 16 * rb + r16, a0 = 16 * cb + 4 * g;
-    if (pi < np && ml < nrows && a0 < p.A) {
-      const int m = r0 + ml;
-      const uint4 w = rng.block((uint32_t)a0 >> 2, step, p.traj0 + (uint32_t)m, STREAM_CONTROLLER);
-      const uint8_t* mr = mask + (long)m * p.A;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (a0 + i < p.A && mr[a0 + i]) v[i] = gumbel(word_to_uniform(word_of(w, i)));
+  for (int o = 0; o < kMaxOwn; ++o) {
+    const int ml = s + kMembers * o;
+    cl.gum[o] = -INFINITY;
+    cl.ud[o] = 0.f;
+    if (ml >= nrows) continue;
+    const uint32_t traj = p.traj0 + (uint32_t)(r0 + ml);
+    if (t < p.T && a < p.A) {
+      const uint8_t* mask = p.mask + (p.step_mask ? (long)t * p.B * p.A : 0) + (long)(r0 + ml) * p.A;
+      if (mask[a]) {
+        const uint4 w = rng.block((uint32_t)a >> 2, step, traj, STREAM_CONTROLLER);
+        cl.gum[o] = gumbel(word_to_uniform(word_of(w, a & 3)));
+      }
     }
-    cl.gum[k] = make_float4(v[0], v[1], v[2], v[3]);
+    if (p.use_done && t > 0) cl.ud[o] = word_to_uniform(rng.block(0, step - 1u, traj, STREAM_DONE).x);
   }
-  ctrl_done_uniform(p, cl, t, r0, nrows);
 }
 
-// Lh of the lane's logits and the reward / done logits of row tid, written
-// by mdn(t-1) (by mdn's controller tiles over h_0 for t = 0).
-template <int CP>
-__device__ __forceinline__ void ctrl_loads(const PArgs& p, CtrlLane<CP>& cl, int r0, int nrows) {
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int g = lane >> 4, r16 = lane & 15;
-  const int np = p.ncb * ((nrows + 15) >> 4);
-  const rsrc_t rl = make_rsrc(p.Lh + (long)r0 * p.Nc, (uint32_t)(nrows * p.Nc * 4));
-#pragma unroll
-  for (int k = 0; k < CP; ++k) {
-    const int pi = wave + 4 * k;
-    const int cb = pi % p.ncb, rb = pi / p.ncb;
-    const int ml = 16 * rb + r16;
-    const bool ok = pi < np && ml < nrows;
-    cl.lh[k] = as_float4(cload16(rl, ok ? (uint32_t)(ml * p.Nc + 16 * cb + 4 * g) * 4u : kOffNone));
-  }
-  const int tid = threadIdx.x;
-  const bool rok = tid < nrows;
-  cl.rr = __uint_as_float(cload4(rl, rok ? (uint32_t)(tid * p.Nc + p.A) * 4u : kOffNone));
-  cl.rd = __uint_as_float(cload4(rl, rok ? (uint32_t)(tid * p.Nc + p.A + 1) * 4u : kOffNone));
+// LDS barrier that does not wait for the vector memory loads in flight
+// (the gate phase's staging).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" : : : "memory");
 }
 
-// Best valid action of each (pair, row) into LDS: the z part of the logits
-// from the staged X_t (MFMAs against W_c's z columns; K slices that hold h
-// columns take zero weights there), plus Lh, plus the noise.  Lowest action
-// on ties.  N: this wave's pair count (its pairs' MFMA chains interleave).
-template <int RB, int CP, int N>
-__device__ __forceinline__ void ctrl_scores_n(const PArgs& p, const CtrlLane<CP>& cl, char* lds) {
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int g = lane >> 4, r16 = lane & 15;
-  const int zs = (p.Z + 15) >> 4;  // K slices holding z columns
-  float* cbs = reinterpret_cast<float*>(lds + p.off_cb);  // [pair][16 rows]
-  int* cbi = reinterpret_cast<int*>(cbs + kMaxPairs * 16);
+// The owner's decisions for its rows at step t (t == T: only transition
+// T-1 and the final done state).  All threads take part.
+__device__ __forceinline__ void ctrl_owner(const PArgs& p, const CtrlLane& cl, char* lds, int t, int r0, int nrows) {
+  const int tid = threadIdx.x, s = blockIdx.x >> 3, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int B = p.B, Z = p.Z, A = p.A;
+  float* zrow = reinterpret_cast<float*>(lds + p.off_ctl);  // [Z]
+  float* wbest = zrow + 160;                                // [4] best score per wave
+  int* widx = reinterpret_cast<int*>(wbest + 4);             // [4] its action
   const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(p.Nc * p.ldk * 4));
-  int cbk[N], rbk[N];
 #pragma unroll
-  for (int k = 0; k < N; ++k) {
-    const int pi = wave + 4 * k;
-    cbk[k] = pi % p.ncb;
-    rbk[k] = pi / p.ncb;
-  }
-  f32x4 acc[N];
-#pragma unroll
-  for (int k = 0; k < N; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int sl = 0; sl < zs; ++sl) {
-    const int col = 16 * sl + 4 * g;
-    uint4 a[N], b[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      a[k] = p.wcz_lds ? *reinterpret_cast<const uint4*>(lds + p.off_wcz + (cbk[k] * zs + sl) * 1024 + 16 * lane)
-                       : bload16(rwc, col < p.Z ? (uint32_t)((16 * cbk[k] + r16) * p.ldk + col) * 4u : kOffNone);
-      b[k] = *reinterpret_cast<const uint4*>(lds + (sl * RB + rbk[k]) * 1024 + 64 * r16 + 16 * g);
-    }
-#pragma unroll
-    for (int v = 0; v < 4; ++v)
-#pragma unroll
-      for (int k = 0; k < N; ++k) mfma4(acc[k], a[k], b[k], v);
-  }
-#pragma unroll
-  for (int k = 0; k < N; ++k) {
-    const int pi = wave + 4 * k;
-    const float lv[4] = {cl.lh[k].x, cl.lh[k].y, cl.lh[k].z, cl.lh[k].w};
-    const float gv[4] = {cl.gum[k].x, cl.gum[k].y, cl.gum[k].z, cl.gum[k].w};
+  for (int o = 0; o < kMaxOwn; ++o) {
+    const int ml = s + kMembers * o;
+    if (ml >= nrows) break;  // uniform
+    const int m = r0 + ml;
+    const rsrc_t rl = make_rsrc(p.Lh + (long)m * p.Nc, (uint32_t)(p.Nc * 4));
     float best = -INFINITY;
     int bi = -1;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const float sc = (acc[k][v] + lv[v]) + gv[v];
-      if (gv[v] != -INFINITY && (bi < 0 || sc > best)) {
-        best = sc;
-        bi = 16 * cbk[k] + 4 * g + v;
+    if (t < p.T) {
+      // z_t of the row (written by mdn(t-1), or before the launch for t = 0)
+      const rsrc_t rz = make_rsrc(p.z_out + ((long)t * B + m) * Z, (uint32_t)(Z * 4));
+      if (tid < Z) zrow[tid] = __uint_as_float(cload4(rz, (uint32_t)tid * 4u));
+      const float lh = __uint_as_float(cload4(rl, tid < A ? (uint32_t)tid * 4u : kOffNone));
+      lds_barrier();
+      if (tid < A && cl.gum[o] != -INFINITY) {
+        float4 acc4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        const uint32_t wrow = (uint32_t)(tid * p.ldk) * 4u;
+        for (int j = 0; j < Z; j += 4) {
+          const float4 wv = as_float4(bload16(rwc, wrow + (uint32_t)j * 4u));
+          const float4 zv = *reinterpret_cast<const float4*>(zrow + j);
+          acc4.x = fmaf(wv.x, zv.x, acc4.x);
+          acc4.y = fmaf(wv.y, zv.y, acc4.y);
+          acc4.z = fmaf(wv.z, zv.z, acc4.z);
+          acc4.w = fmaf(wv.w, zv.w, acc4.w);
+        }
+        best = (((acc4.x + acc4.y) + (acc4.z + acc4.w)) + lh) + cl.gum[o];
+        bi = tid;
       }
-    }
+      // best valid action, lowest index on ties
 #pragma unroll
-    for (int off = 16; off <= 32; off <<= 1) {
-      const float ob = __shfl_xor(best, off);
-      const int oi = __shfl_xor(bi, off);
-      if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
-        best = ob;
-        bi = oi;
+      for (int off = 32; off >= 1; off >>= 1) {
+        const float ob = __shfl_xor(best, off);
+        const int oi = __shfl_xor(bi, off);
+        if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
+          best = ob;
+          bi = oi;
+        }
       }
+      if (lane == 0) {
+        wbest[wave] = best;
+        widx[wave] = bi;
+      }
+      lds_barrier();
     }
-    if (g == 0) {
-      cbs[pi * 16 + r16] = best;
-      cbi[pi * 16 + r16] = bi;
+    if (tid == 0) {
+      if (t < p.T) {  // thread 0 holds wave 0's best; the other waves'
+        for (int w = 1; w < 4; ++w) {
+          const float ob = wbest[w];
+          const int oi = widx[w];
+          if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
+            best = ob;
+            bi = oi;
+          }
+        }
+      }
+      int* ds_l = row_done(p, lds);
+      int* pv_l = row_prev(p, lds);
+      int ds = ds_l[ml];
+      if (pv_l[ml] >= 0) {  // transition t-1 was live: its reward and done
+        const float rr = __uint_as_float(cload4(rl, (uint32_t)A * 4u));
+        const float rd = __uint_as_float(cload4(rl, (uint32_t)(A + 1) * 4u));
+        const int d = p.use_done ? sigmoidf(rd) > cl.ud[o] : 0;
+        p.rewards[(long)(t - 1) * B + m] = rr;
+        p.dones[(long)(t - 1) * B + m] = (uint8_t)d;
+        if (d) ds = 1;
+      }
+      if (t < p.T) {
+        const bool pad = t >= row_len(p, lds)[ml];
+        int act = bi;
+        if (ds || pad) act = -1;
+        else if (act < 0) ds = 1;
+        p.actions[(long)t * B + m] = act;
+        if (act < 0) {
+          p.rewards[(long)t * B + m] = 0.f;
+          p.dones[(long)t * B + m] = pad ? 0 : 1;
+        }
+        pv_l[ml] = act;
+        // the action reaches the L2 before the flag that announces it
+        asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
+        const rsrc_t rf = make_rsrc(p.flags + r0, (uint32_t)nrows * 4u);
+        bstore4(rf, (uint32_t)ml * 4u, (uint32_t)(t + 1));
+      } else {
+        p.done_state[m] = ds;  // for the finishing kernel
+      }
+      ds_l[ml] = ds;
     }
   }
 }
 
-template <int RB, int CP>
-__device__ __forceinline__ void ctrl_scores(const PArgs& p, const CtrlLane<CP>& cl, char* lds, int nrows) {
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int np = p.ncb * ((nrows + 15) >> 4);
-  const int npw = np > wave ? (np - wave + 3) >> 2 : 0;  // this wave's pairs (<= CP)
-  switch (npw) {
-    case 1: ctrl_scores_n<RB, CP, 1>(p, cl, lds); break;
-    case 2: if constexpr (CP >= 2) ctrl_scores_n<RB, CP, 2>(p, cl, lds); break;
-    case 3: if constexpr (CP >= 3) ctrl_scores_n<RB, CP, 3>(p, cl, lds); break;
-    case 4: if constexpr (CP >= 4) ctrl_scores_n<RB, CP, 4>(p, cl, lds); break;
-    case 5: if constexpr (CP >= 5) ctrl_scores_n<RB, CP, 5>(p, cl, lds); break;
-    default: break;
-  }
-}
-
-// The action of row tid (tid < rows) from its pairs, then the bookkeeping:
-// transition t-1 is resolved if the row was live then (its reward is the
-// reward head on h_t, it is done when sigmoid(done head) exceeds the
-// stream-3 uniform of step t-1); then (t < T) the row takes its action or,
-// if done, the frozen outputs; a row without a valid action ends here; a
-// step past the row's horizon is padding (no action, reward 0, done 0).
-// Every work-group keeps the same row state in LDS; work-group m % 32
-// writes row m's outputs.
-template <int CP>
-__device__ __forceinline__ void ctrl_resolve(const PArgs& p, const CtrlLane<CP>& cl, char* lds, int t, int r0,
-                                             int nrows) {
-  const int ml = threadIdx.x;
-  if (ml >= nrows) return;
-  const int s = blockIdx.x >> 3;
-  const bool owner = (ml & (kMembers - 1)) == s;
-  const int m = r0 + ml, B = p.B;
-  int* act_l = row_act(p, lds);
-  int* ds_l = row_done(p, lds);
-  int* pv_l = row_prev(p, lds);
-  int ds = ds_l[ml];
-  if (pv_l[ml] >= 0) {
-    const int d = p.use_done ? sigmoidf(cl.rd) > cl.ud : 0;
-    if (owner) {
-      p.rewards[(long)(t - 1) * B + m] = cl.rr;
-      p.dones[(long)(t - 1) * B + m] = (uint8_t)d;
-    }
-    if (d) ds = 1;
-  }
-  if (t < p.T) {
-    const float* cbs = reinterpret_cast<const float*>(lds + p.off_cb);
-    const int* cbi = reinterpret_cast<const int*>(cbs + kMaxPairs * 16);
-    const int rb = ml >> 4, r16 = ml & 15;
-    float best = -INFINITY;
-    int bi = -1;
-    for (int cb = 0; cb < p.ncb; ++cb) {
-      const int pi = rb * p.ncb + cb;
-      const float ob = cbs[pi * 16 + r16];
-      const int oi = cbi[pi * 16 + r16];
-      if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
-        best = ob;
-        bi = oi;
+// The actions of step t of all of the XCD's rows into LDS, once their owners'
+// flags show them.  The wait is bounded: on timeout (or another work-group's)
+// the error word is set and the work-group leaves at its next barrier.
+__device__ __forceinline__ void ctrl_gather(const PArgs& p, char* lds, int t, int r0, int nrows, unsigned* err) {
+  const int tid = threadIdx.x;
+  if (tid < nrows) {
+    const rsrc_t rf = make_rsrc(p.flags + r0, (uint32_t)nrows * 4u);
+    unsigned spins = 0;
+    while ((int)(cload4(rf, (uint32_t)tid * 4u) - (uint32_t)(t + 1)) < 0) {
+      if ((++spins & 63u) == 0) {
+        if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
+        if (spins >= kSpinLimit) {
+          __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
       }
+      __builtin_amdgcn_s_sleep(1);
     }
-    const bool pad = t >= row_len(p, lds)[ml];
-    int act = bi;
-    if (ds || pad) act = -1;
-    else if (act < 0) ds = 1;
-    if (owner) {
-      p.actions[(long)t * B + m] = act;
-      if (act < 0) {
-        p.rewards[(long)t * B + m] = 0.f;
-        p.dones[(long)t * B + m] = pad ? 0 : 1;
-      }
-    }
-    act_l[ml] = act;
-    pv_l[ml] = act;
-  } else if (owner) {
-    p.done_state[m] = ds;  // for the finishing kernel
+    const rsrc_t ra = make_rsrc(p.actions + (long)t * p.B + r0, (uint32_t)nrows * 4u);
+    row_act(p, lds)[tid] = (int)cload4(ra, (uint32_t)tid * 4u);
   }
-  ds_l[ml] = ds;
 }
 
 // ---------------------------------------------------------------------------
 // gates(t): X_in -> h_{t+1} into X_out (rollout: with the step's actions)
 // ---------------------------------------------------------------------------
 template <int RB, int NBC, bool NLL>
-__device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& st, CtrlLane<ctrl_cp<RB>()>& cl,
+__device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& st, const CtrlLane& cl,
                                             char* lds,
                                             int t, const float* Xin, float* Xout, int r0, int nrows) {
   constexpr int KSPLIT = GateState<RB, NBC>::KSPLIT;
@@ -475,7 +422,7 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   const int B = p.B, H = p.H, A = p.A;
 
   // epilogue inputs issued first (older than the staging loads): the NLL
-  // pass's actions, the rollout controller's Lh
+  // pass's actions
   int act[RB];
   if constexpr (NLL) {
     const rsrc_t ra = make_rsrc(p.actions + (long)t * B + r0, (uint32_t)nrows * 4u);
@@ -484,8 +431,6 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
       const int ml = 16 * rb + r16;
       act[rb] = owner && ml < nrows ? (int)cload4(ra, (uint32_t)ml * 4u) : -1;
     }
-  } else {
-    ctrl_loads(p, cl, r0, nrows);
   }
 
   // stage X_in rows [r0, r0 + nrows), columns [0, ldk) into LDS as
@@ -547,6 +492,8 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
       }
     }
   }
+  // rollout: this work-group's rows' decisions, under the staging loads
+  if constexpr (!NLL) ctrl_owner(p, cl, lds, t, r0, nrows);
 
   // two accumulator sets (even and odd K slices) and RB row blocks give
   // 2 RB independent MFMA chains, issued interleaved
@@ -556,19 +503,10 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   const int nval = min(nper, nks - sl0);  // this wave's valid K slices (uniform)
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
-    if (!NLL && c == 1) asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory");  // pair bests written
     if (c == 0 || !eager) {
       vm_wait<0>();  // this wave's loads of chunk c (the only ones in flight)
       __builtin_amdgcn_s_barrier();
       asm volatile("" : : : "memory");
-    } else if (!NLL && c == 1) {
-      __builtin_amdgcn_s_barrier();  // the controller's pair bests are in LDS
-      asm volatile("" : : : "memory");
-    }
-    // rollout: the rows' actions (wave 0) from the pair bests of chunk 0's
-    // controller MFMAs, while chunk 1's loads land
-    if constexpr (!NLL) {
-      if (c == 1 && wave == 0) ctrl_resolve(p, cl, lds, t, r0, nrows);
     }
     const int nn = c < 3 && !eager ? wave_count(c + 1) : 0;
     int kk = 0;  // next load of chunk c+1 to issue
@@ -607,11 +545,6 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
         for (; kk < upto; ++kk) issue(c + 1, kk);
       }
     }
-    // rollout: the controller's (pair, row) bests from the staged z columns
-    // (chunk 0 holds them), under chunk 1's loads
-    if constexpr (!NLL) {
-      if (c == 0) ctrl_scores<RB>(p, cl, lds, nrows);
-    }
   }
   f32x4 acc[RB];
 #pragma unroll
@@ -635,8 +568,9 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
     }
   }
   if constexpr (!NLL) {
-    // the rows' actions (resolved in chunk 1), seen by every wave after the
-    // barrier above
+    // the rows' actions, from their owners
+    if (wave == 0) ctrl_gather(p, lds, t, r0, nrows, sync_err(p));
+    __syncthreads();
     const int* act_l = row_act(p, lds);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -926,19 +860,11 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
       if (i >= 192) v = p.lengths && ml < nrows ? p.lengths[r0 + ml] : 0x7fffffff;
       rows[i] = v;
     }
-    if (p.wcz_lds) {
-      // the controller's z columns as MFMA A fragments: fragment (cb, sl),
-      // lane (g, r16) holds W_c[16 cb + r16][16 sl + 4 g .. + 3] (zero
-      // where those columns are h columns)
-      const int zs = (p.Z + 15) >> 4;
-      uint4* wz = reinterpret_cast<uint4*>(lds + p.off_wcz);
-      for (int i = tid; i < p.ncb * zs * 64; i += 256) {
-        const int f = i >> 6, l = i & 63;
-        const int cb = f / zs, sl = f % zs;
-        const int col = 16 * sl + 4 * (l >> 4);
-        wz[i] = col < p.Z ? *reinterpret_cast<const uint4*>(p.Wc + (long)(16 * cb + (l & 15)) * p.ldk + col)
-                          : make_uint4(0u, 0u, 0u, 0u);
-      }
+    // the flags of this work-group's rows start at 0 (before barrier 1)
+#pragma unroll
+    for (int o = 0; o < kMaxOwn; ++o) {
+      const int ml = s + kMembers * o;
+      if (tid == 0 && ml < nrows) p.flags[r0 + ml] = 0u;
     }
   }
   if (p.wat_lds) {
@@ -956,7 +882,7 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
   __syncthreads();
   gs.agent = s_agent != 0;
 
-  CtrlLane<ctrl_cp<RB>()> cl;
+  CtrlLane cl;
   MdnNoise nz{};
   if constexpr (!NLL) {
     // the h part of the step-0 controller logits, from h_0 (X_0, written
@@ -993,9 +919,8 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
     // transition T-1 (its reward and done from mdn(T-1)'s Lh), the done state
     {
       const PArgs& q = fresh_args();
-      ctrl_loads(q, cl, r0, nrows);
-      ctrl_done_uniform(q, cl, q.T, r0, nrows);
-      if (wave == 0) ctrl_resolve(q, cl, lds, q.T, r0, nrows);
+      ctrl_noise(q, cl, q.T, r0, nrows);
+      ctrl_owner(q, cl, lds, q.T, r0, nrows);
     }
     // final cell state for k_rollout_finish
     if (owner) {
@@ -1030,8 +955,8 @@ int persist_rb(int B) {
 struct PPlan {
   int rb = 0, nbc = 0;
   size_t lds = 0;
-  int off_red = 0, off_rows = 0, off_wat = 0, off_wcz = 0, off_mdn = 0, off_cb = 0, off_flags = 0;
-  int wat_lds = 0, wcz_lds = 0;
+  int off_red = 0, off_rows = 0, off_wat = 0, off_mdn = 0, off_ctl = 0, off_flags = 0;
+  int wat_lds = 0;
   int ncb = 0, ctl_sep = 0;
 };
 
@@ -1063,28 +988,27 @@ bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
   pl.rb = rb;
   pl.nbc = nbc;
   if (!nll) {
-    // controller pairs (logit block, row block) per wave, and the tiles of
-    // mdn(t): the controller blocks as tiles of their own when all tiles fit
-    // one round of the 32 work-groups, else inside the first mixture tiles
+    // the tiles of mdn(t): the controller's h-part blocks as tiles of their
+    // own when all tiles fit one round of the 32 work-groups, else inside
+    // the first mixture tiles; one thread per action in the owner decisions
     const int rbv = (((B + kGroups - 1) / kGroups) + 15) / 16;
     pl.ncb = L.Nc / 16;
-    if (pl.ncb * rbv > 4 * (rb == 1 ? ctrl_cp<1>() : rb == 2 ? ctrl_cp<2>() : ctrl_cp<4>())) return false;
     const int zt = (L.Z / 4) * rbv;
     pl.ctl_sep = zt + pl.ncb * rbv <= kMembers ? 1 : 0;
     if (!pl.ctl_sep && pl.ncb > L.Z / 4) return false;
-    if ((L.Z + 15) / 16 > 9) return false;  // the z columns lie in the first staged chunk
+    if (L.Z > 160 || L.A > 256) return false;
   }
   // the mixture-head partial sums share the gate staging's bytes (another
-  // phase); the controller's pair bests, the row state and the one-hot
-  // columns persist
+  // phase); the controller's scratch, the row state and the one-hot columns
+  // persist
   size_t o = (size_t)nks * rb * 1024;  // staging
   pl.off_red = (int)o;
   o += (size_t)(4 - nbc) * rb * 1024;   // K-split partial sums
   pl.off_mdn = 0;
   if (!nll) {
     o = o > (size_t)4 * (L.Q + 1) * 1024 ? o : (size_t)4 * (L.Q + 1) * 1024;
-    pl.off_cb = (int)o;
-    o += (size_t)kMaxPairs * 16 * 8;  // best score and action per (pair, row)
+    pl.off_ctl = (int)o;
+    o += 1024;                        // a row's z_t, wave bests
     pl.off_rows = (int)o;
     o += (size_t)4 * 64 * 4;          // actions, done state, previous actions, horizons
   }
@@ -1094,13 +1018,6 @@ bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
   if (o + wat <= kLdsMax) {
     pl.wat_lds = 1;
     o += wat;
-  }
-  o = (o + 1023) & ~(size_t)1023;
-  pl.off_wcz = (int)o;
-  const size_t wcz = (size_t)pl.ncb * ((L.Z + 15) / 16) * 1024;  // A fragments of W_c's z columns
-  if (!nll && o + wcz <= kLdsMax) {
-    pl.wcz_lds = 1;
-    o += wcz;
   }
   if (o > kLdsMax) return false;
   o = o < kLdsMin ? kLdsMin : o;
@@ -1164,10 +1081,8 @@ PArgs base_args(const Packed& P, const PPlan& pl, int B, int T) {
   a.ldk = L.ldk; a.ldh = L.ldh; a.ldx = L.ldx;
   a.B = B; a.T = T; a.Bx = (B + kGroups - 1) / kGroups;
   a.wat_lds = pl.wat_lds;
-  a.wcz_lds = pl.wcz_lds;
-  a.off_wcz = pl.off_wcz;
   a.off_red = pl.off_red; a.off_rows = pl.off_rows; a.off_wat = pl.off_wat;
-  a.off_mdn = pl.off_mdn; a.off_cb = pl.off_cb; a.off_flags = pl.off_flags;
+  a.off_mdn = pl.off_mdn; a.off_ctl = pl.off_ctl; a.off_flags = pl.off_flags;
   a.ncb = pl.ncb;
   a.ctl_sep = pl.ctl_sep;
   return a;
@@ -1178,7 +1093,7 @@ PArgs base_args(const Packed& P, const PPlan& pl, int B, int T) {
 size_t persist_partial_bytes(const Layout& L, int B) {
   PPlan pl;
   if (!plan(L, B, false, pl)) return 0;
-  return (size_t)B * L.Nc * 4;  // Lh
+  return (size_t)B * L.Nc * 4 + (size_t)B * 4;  // Lh, then the row flags
 }
 
 bool persist_usable(const Layout& L, int B, bool nll) {
@@ -1210,6 +1125,7 @@ hipError_t launch_rollout_persist(const Packed& P, const RolloutBufs& R, hipStre
   a.done_state = R.done_state;
   a.lengths = R.lengths;
   a.Lh = R.P;
+  a.flags = reinterpret_cast<unsigned*>(R.P + (size_t)R.B * P.L.Nc);
   a.sync = R.sync;
   a.mask = R.mask;
   a.z_out = R.z_out;
