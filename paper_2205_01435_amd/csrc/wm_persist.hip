@@ -416,7 +416,7 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   const int blk = s * NBC + wb;
   const int unit = 4 * blk + g;
   const bool owner = kp == 0;
-  const int nks = p.ldk >> 4;
+  const int nks = (p.Z + p.H + 15) >> 4;  // K slices holding z, h (the padding columns are zero)
   const int nper = (nks + KSPLIT - 1) / KSPLIT;
   const int sl0 = kp * nper;
   const int B = p.B, H = p.H, A = p.A;
@@ -830,7 +830,7 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
   const int blk = s * NBC + wb;
   const int unit = 4 * blk + g;
   const bool owner = kp == 0;
-  const int nks = p.ldk >> 4;
+  const int nks = (p.Z + p.H + 15) >> 4;  // K slices holding z, h (the padding columns are zero)
   const int nper = (nks + KSPLIT - 1) / KSPLIT;
   const int sl0 = kp * nper;
   {
@@ -981,7 +981,7 @@ bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
   const int rb = persist_rb(B);
   if (rb == 0) return false;
   const int nbc = L.H / 128;
-  const int nks = L.ldk / 16;
+  const int nks = (L.Z + L.H + 15) / 16;
   const int nper = (nks + 4 / nbc - 1) / (4 / nbc);
   if (nper > kMaxS || (L.H / 16 + 3) / 4 > kMaxMS || L.Q > kMaxQ) return false;
   if (L.N > 0) return false;  // the two-level controller runs on the multi-launch path
