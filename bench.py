@@ -283,6 +283,7 @@ def workload_table(wmlib, wl, torch, cuda, only=frozenset()) -> dict:
              "two_level_rollout_n288": lambda: two_level_row(wmlib, wl, torch, cuda, 288),
              "two_level_rollout_n80": lambda: two_level_row(wmlib, wl, torch, cuda, 80),
              "adam_xlarge_wm": lambda: adam_row(wmlib, torch),
+             "library_gemm_xlarge": lambda: library_gemm_row(torch),
              "train_step_nll": lambda: train_step_row(wmlib, wl, torch, cuda)}
     for name, fn in extra.items():
         if not only or name in only:
@@ -332,6 +333,43 @@ def train_step_row(wmlib, wl, torch, cuda) -> dict:
     return {"ms": ms, "reps": reps, "tokens_per_s": n / (ms / 1e3), "flops_per_step": fl, "tflops": fl / (ms / 1e3) / 1e12,
             "frac_fp32_peak": fl / (ms / 1e3) / PEAK["fp32"], "kernel_ms": {k: round(v, 4) for k, v in parts.items()},
             "loss": float(gb.loss.cpu()[0])}
+
+
+def library_gemm_row(torch) -> dict:
+    """The library's bf16 GEMM (torch.matmul, hipBLASLt) at the three products
+    of one xlarge rollout step (B 16384 rows; gates K = Z + H = 1152 by
+    N = 4H = 4096, mixture head K = H = 1024 by N = 3ZK = 3072, controller
+    K = 1152 by N = A + 2 = 258), weights stored [N, K] as the packed layout
+    holds them. A comparison for the fused kernels, which also run their
+    epilogues: the GEMM alone, median over 10 batches of 20 calls."""
+    res = {}
+    total = 0.0
+    for name, (M, K, N) in {"gates": (16384, 1152, 4096), "mixture_head": (16384, 1024, 3072),
+                            "controller": (16384, 1152, 258)}.items():
+        g = torch.Generator(device="cuda").manual_seed(0)
+        a = torch.randn(M, K, dtype=torch.bfloat16, device="cuda", generator=g)
+        w = torch.randn(N, K, dtype=torch.bfloat16, device="cuda", generator=g)
+        wt = w.t()
+        for _ in range(5):
+            c = a @ wt
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(10):
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            for _ in range(20):
+                c = a @ wt
+            e.record()
+            e.synchronize()
+            times.append(s.elapsed_time(e) * 1e3 / 20)
+        us = float(np.median(times))
+        total += us
+        res[name] = {"M": M, "K": K, "N": N, "us": us,
+                     "frac_bf16_peak": 2.0 * M * N * K / (us * 1e-6) / PEAK["bf16"]}
+        del a, w, wt, c
+    res["step_gemms_us"] = total
+    torch.cuda.empty_cache()
+    return res
 
 
 def adam_row(wmlib, torch) -> dict:
