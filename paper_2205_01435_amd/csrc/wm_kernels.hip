@@ -912,12 +912,6 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
   int ntile, mt;
   if (!tile_of(p.map, ntile, mt)) return;
   const int n0 = ntile * C::BN, m0 = mt * C::BM;
-  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wm), p.ldh, p.ldh, n0, C::BN, p.Nm);
-  const SrcX<DT> x(reinterpret_cast<const DT*>(p.x) + p.Z, p.ldx, p.ldx - p.Z, m0, C::BM, p.M);
-  f32x4 acc[Q][MBW];
-  C::run(acc, w, x, (int)p.ldh, reinterpret_cast<DT*>(lds_raw));
-  const bool owner = C::kw() == 0;  // holds the summed tile
-
   const int lane = threadIdx.x & 63;
   const int wn = C::wn(), wmi = C::wm();
   const int g = lane >> 4;
@@ -925,6 +919,27 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
   const int J = ntile * WAVES_N + wn;  // dim group of this wave
   const int j = 4 * J + g;             // latent dim of this lane
   const bool head_tile = p.nll_mode && ntile == p.ntd;
+  // rollout: the actions of this lane's rows and their previous latents
+  // (kept by frozen rows), fetched ahead of the GEMM
+  int actp[MBW];
+  float zpv[MBW];
+  if (!p.nll_mode) {
+    const long mval = max(0, min(C::BM, p.M - m0));
+    const rsrc_t ra = make_rsrc(p.act + m0, (uint32_t)(mval * 4));
+    const rsrc_t rz = make_rsrc(p.z_prev + (long)m0 * Z, (uint32_t)(mval * Z * 4));
+#pragma unroll
+    for (int jj = 0; jj < MBW; ++jj) {
+      const int ml = (wmi * MBW + jj) * 16 + (lane & 15);
+      const bool ok = m0 + ml < p.M && j < Z;
+      actp[jj] = (int)bload4(ra, ok ? (uint32_t)ml * 4u : kOffNone);
+      zpv[jj] = __uint_as_float(bload4(rz, ok ? (uint32_t)(ml * Z + j) * 4u : kOffNone));
+    }
+  }
+  const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wm), p.ldh, p.ldh, n0, C::BN, p.Nm);
+  const SrcX<DT> x(reinterpret_cast<const DT*>(p.x) + p.Z, p.ldx, p.ldx - p.Z, m0, C::BM, p.M);
+  f32x4 acc[Q][MBW];
+  C::run(acc, w, x, (int)p.ldh, reinterpret_cast<DT*>(lds_raw));
+  const bool owner = C::kw() == 0;  // holds the summed tile
 
   if (head_tile) {
     // Rows 0 and 1 of the block are the reward and done logits.
@@ -971,8 +986,8 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
     for (int jj = 0; jj < MBW; ++jj) {
       const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
       if (m >= p.M || j >= Z) continue;
-      if (p.act[m] < 0) {
-        mdn_commit<DT>(p, m, j, p.z_prev[(long)m * Z + j]);
+      if (actp[jj] < 0) {
+        mdn_commit<DT>(p, m, j, zpv[jj]);
         continue;
       }
       float feat[4 * Q];

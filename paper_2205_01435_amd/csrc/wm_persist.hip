@@ -23,15 +23,16 @@
 // separated by XCD barriers:
 //   gates(t)  X_t of the XCD's rows staged in LDS (LDS-DMA, four chunks so
 //             that the MFMAs start on the first), gate GEMM against the
-//             register weights; then the controller decision of every row
-//             of the XCD, which every work-group makes for itself (the same
-//             inputs and the same arithmetic give the same actions in all
-//             of them, so no barrier is needed): logits = W_c,z q(z_t) (MFMAs
-//             on the staged z columns) + the h part and the bias (from
-//             mdn(t-1)), masked Gumbel-max, resolution of transition t-1
-//             (reward, done), freeze logic; the work-group m % 32 writes
-//             row m's outputs.  LSTM cell with the chosen action's one-hot
-//             column, h_{t+1} into X_{t+1};
+//             register weights.  Under the staging loads, the owner of each
+//             row (work-group m % 32 for row m) makes that row's controller
+//             decision: logits = W_c,z z_t (vector FMAs against W_c in the
+//             L2) + the h part and the bias (from mdn(t-1)), masked
+//             Gumbel-max, the reward and done of transition t-1, freeze
+//             logic; it writes the row's outputs, then a per-row flag
+//             (t + 1) once they have reached the L2.  Before the LSTM cell
+//             every work-group waits (bounded) for the flags of the XCD's
+//             rows and reads their actions.  LSTM cell with the chosen
+//             action's one-hot column, h_{t+1} into X_{t+1};
 //   mdn(t)    (group of four latent dims, 16-row block) tiles, K split over
 //             the four waves and summed in LDS, component pick, Box-Muller
 //             draw, z_{t+1} to z_out and X_{t+1}; further tiles (or, when
