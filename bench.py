@@ -13,7 +13,7 @@ it.  The teacher-forced NLL pass is measured on its own workload (B 512,
 T 128, fp32) in the per-workload table, as are the other four workloads.
 
 Prints ONE JSON line (rank 0, N = 1).  --gpus above 1 exits with a message:
-this build measures one GPU.
+the benchmark measures one GPU.
 """
 
 from __future__ import annotations
