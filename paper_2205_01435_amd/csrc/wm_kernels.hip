@@ -2633,19 +2633,22 @@ hipError_t launch_nll(const Packed& P, const NllBufs& N, hipStream_t s) {
 // respect to the gate, mixture, reward and done weights (fp32), by
 // backpropagation through time after the forward NLL pass.
 //
-//   forward   X (z_t | h_t) from the NLL pass; pre-activations of every step
-//             in one GEMM; a scan adds bias and one-hot column, applies the
+//   forward   X (z_t | h_t) from the NLL pass; where the persistent kernel
+//             runs it, the gate activations and c_{t+1} of every step come
+//             with it; otherwise the pre-activations of every step in one
+//             GEMM and a scan that adds bias and one-hot column, applies the
 //             gates and records c_t
 //   heads     mixture/reward/done outputs of every h_{t+1} in one GEMM; an
 //             element-wise kernel turns them into d loss / d output (dM)
 //   back      dh_heads = dM W_m; per step (backwards) the LSTM backward gives
 //             dG_t and dc_t, and dh_t = dG_t W_h for the step before
-//   weights   dW_g = dG^T X, dW_m = dM^T H (GEMMs over all T B rows on
-//             transposed copies), bias and one-hot columns by deterministic
-//             reductions, then the canonical layout
-// Every GEMM is C[m][n] = sum_k A[m][k] B[n][k] on the direct-to-LDS core
-// (both operands K-contiguous), so the weight gradients read transposed,
-// zero-padded copies.
+//   weights   dW_g^T = X^T dG and dW_m = dM^T H over all T B rows, with the
+//             bias gradients summed in the same pass (k_gemm_tn reads X, dG,
+//             dM and H as stored, K outer), the one-hot columns by a
+//             deterministic reduction, then the canonical layout
+// The forward and per-step products are C[m][n] = sum_k A[m][k] B[n][k] on
+// the direct-to-LDS core (both operands K-contiguous: the packing kernel
+// also writes W_h^T and W_m^T for them).
 // ===========================================================================
 namespace {
 

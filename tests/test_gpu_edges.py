@@ -56,6 +56,10 @@ RAGGED = [
     (33, 3, 16, 64, 1000, 2, "fp32"),
     (17, 2, 8, 32, 2048, 4, "bf16"),
     (129, 3, 40, 112, 7, 6, "fp32"),
+    (20, 2, 1024, 64, 8, 2, "fp32"),   # the widest latent the library takes
+    (20, 2, 1024, 64, 8, 2, "bf16"),
+    (9, 2, 8, 2048, 3, 1, "fp32"),     # a wide hidden state: 8192 gate rows
+    (9, 2, 8, 2048, 3, 1, "bf16"),
 ]
 
 
