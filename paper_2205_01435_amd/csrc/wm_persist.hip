@@ -236,6 +236,45 @@ struct GateState {
 // cell epilogue, which needs the actions.
 // ---------------------------------------------------------------------------
 constexpr int kMaxOwn = 2;  // rows per work-group: 64 rows per XCD at most
+// Row m's flag after its decision of step t: (t + 1) << kFlagShift |
+// (action + 1), so that the action travels in the word that announces it
+// and no ordering between two stores is needed (actions are below 1023).
+constexpr int kFlagShift = 10;
+__device__ __forceinline__ uint32_t row_flag(int t, int act) {
+  return ((uint32_t)(t + 1) << kFlagShift) | (uint32_t)(act + 1);
+}
+
+// One step of the wave's (score, action) argmax: merge with the pair that
+// the DPP pattern CTRL brings in (none: an empty pair).  The merge keeps the
+// higher score, the lower action on equal scores, and ignores empty pairs
+// (action < 0), so it is idempotent and any covering order gives the same
+// result as a butterfly.
+template <int CTRL, int ROWM>
+__device__ __forceinline__ void argmax_dpp(float& best, int& bi) {
+  const float ob = __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(-INFINITY), __float_as_int(best), CTRL, ROWM, 0xf, false));
+  const int oi = __builtin_amdgcn_update_dpp(-1, bi, CTRL, ROWM, 0xf, false);
+  if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
+    best = ob;
+    bi = oi;
+  }
+}
+
+// Argmax of (best, bi) over the 64 lanes, lowest action on ties, in every
+// lane: row shifts by 1, 2, 4 and 8 leave each row's result in its lane 15,
+// the row broadcasts 15 and 31 carry them to lane 63, which is read out.
+// (Cross-lane moves on the DPP path instead of 12 dependent LDS-crossbar
+// shuffles.)
+__device__ __forceinline__ void wave_argmax(float& best, int& bi) {
+  argmax_dpp<0x111, 0xf>(best, bi);  // row_shr:1
+  argmax_dpp<0x112, 0xf>(best, bi);  // row_shr:2
+  argmax_dpp<0x114, 0xf>(best, bi);  // row_shr:4
+  argmax_dpp<0x118, 0xf>(best, bi);  // row_shr:8
+  argmax_dpp<0x142, 0xa>(best, bi);  // row_bcast:15 into rows 1 and 3
+  argmax_dpp<0x143, 0xc>(best, bi);  // row_bcast:31 into rows 2 and 3
+  best = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(best), 63));
+  bi = __builtin_amdgcn_readlane(bi, 63);
+}
 
 struct CtrlLane {
   float gum[kMaxOwn];  // thread a's Gumbel noise for action a of each owned row; -inf: not valid
@@ -320,15 +359,7 @@ __device__ __forceinline__ void ctrl_owner(const PArgs& p, const CtrlLane& cl, c
         bi = tid;
       }
       // best valid action, lowest index on ties
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) {
-        const float ob = __shfl_xor(best, off);
-        const int oi = __shfl_xor(bi, off);
-        if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
-          best = ob;
-          bi = oi;
-        }
-      }
+      wave_argmax(best, bi);
       if (lane == 0) {
         wbest[wave] = best;
         widx[wave] = bi;
@@ -368,10 +399,85 @@ __device__ __forceinline__ void ctrl_owner(const PArgs& p, const CtrlLane& cl, c
           p.dones[(long)t * B + m] = pad ? 0 : 1;
         }
         pv_l[ml] = act;
-        // the action reaches the L2 before the flag that announces it
-        asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
         const rsrc_t rf = make_rsrc(p.flags + r0, (uint32_t)nrows * 4u);
-        bstore4(rf, (uint32_t)ml * 4u, (uint32_t)(t + 1));
+        bstore4(rf, (uint32_t)ml * 4u, row_flag(t, act));
+      } else {
+        p.done_state[m] = ds;  // for the finishing kernel
+      }
+      ds_l[ml] = ds;
+    }
+  }
+}
+
+// The owner's decisions with one wave (A <= 64: lane a takes action a), so
+// that the work-group's other three waves issue the gate phase's staging
+// loads meanwhile and this wave's loads wait for nothing else.  Same
+// arithmetic and tie rule as ctrl_owner.  Wave 0 only.
+__device__ __forceinline__ void ctrl_owner_w0(const PArgs& p, const CtrlLane& cl, char* lds, int t, int r0,
+                                              int nrows) {
+  const int lane = threadIdx.x & 63, s = blockIdx.x >> 3;
+  const int B = p.B, Z = p.Z, A = p.A;
+  float* zrow = reinterpret_cast<float*>(lds + p.off_ctl);  // [Z]
+  const rsrc_t rwc = make_rsrc(p.Wc, (uint32_t)(p.Nc * p.ldk * 4));
+#pragma unroll
+  for (int o = 0; o < kMaxOwn; ++o) {
+    const int ml = s + kMembers * o;
+    if (ml >= nrows) break;  // uniform
+    const int m = r0 + ml;
+    const rsrc_t rl = make_rsrc(p.Lh + (long)m * p.Nc, (uint32_t)(p.Nc * 4));
+    // transition t-1's reward and done logits, loaded with the row's inputs
+    const float rr = __uint_as_float(cload4(rl, (uint32_t)A * 4u));
+    const float rd = __uint_as_float(cload4(rl, (uint32_t)(A + 1) * 4u));
+    float best = -INFINITY;
+    int bi = -1;
+    if (t < p.T) {
+      // z_t of the row (written by mdn(t-1), or before the launch for t = 0)
+      const rsrc_t rz = make_rsrc(p.z_out + ((long)t * B + m) * Z, (uint32_t)(Z * 4));
+      for (int j = lane; j < Z; j += 64) zrow[j] = __uint_as_float(cload4(rz, (uint32_t)j * 4u));
+      const float lh = __uint_as_float(cload4(rl, lane < A ? (uint32_t)lane * 4u : kOffNone));
+      // one wave: its LDS writes and reads are processed in order
+      __builtin_amdgcn_wave_barrier();
+      if (lane < A && cl.gum[o] != -INFINITY) {
+        float4 acc4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        const uint32_t wrow = (uint32_t)(lane * p.ldk) * 4u;
+        for (int j = 0; j < Z; j += 4) {
+          const float4 wv = as_float4(bload16(rwc, wrow + (uint32_t)j * 4u));
+          const float4 zv = *reinterpret_cast<const float4*>(zrow + j);
+          acc4.x = fmaf(wv.x, zv.x, acc4.x);
+          acc4.y = fmaf(wv.y, zv.y, acc4.y);
+          acc4.z = fmaf(wv.z, zv.z, acc4.z);
+          acc4.w = fmaf(wv.w, zv.w, acc4.w);
+        }
+        best = (((acc4.x + acc4.y) + (acc4.z + acc4.w)) + lh) + cl.gum[o];
+        bi = lane;
+      }
+      // best valid action, lowest index on ties
+      wave_argmax(best, bi);
+      __builtin_amdgcn_wave_barrier();  // zrow is read out before the next row's z
+    }
+    if (lane == 0) {
+      int* ds_l = row_done(p, lds);
+      int* pv_l = row_prev(p, lds);
+      int ds = ds_l[ml];
+      if (pv_l[ml] >= 0) {  // transition t-1 was live: its reward and done
+        const int d = p.use_done ? sigmoidf(rd) > cl.ud[o] : 0;
+        p.rewards[(long)(t - 1) * B + m] = rr;
+        p.dones[(long)(t - 1) * B + m] = (uint8_t)d;
+        if (d) ds = 1;
+      }
+      if (t < p.T) {
+        const bool pad = t >= row_len(p, lds)[ml];
+        int act = bi;
+        if (ds || pad) act = -1;
+        else if (act < 0) ds = 1;
+        p.actions[(long)t * B + m] = act;
+        if (act < 0) {
+          p.rewards[(long)t * B + m] = 0.f;
+          p.dones[(long)t * B + m] = pad ? 0 : 1;
+        }
+        pv_l[ml] = act;
+        const rsrc_t rf = make_rsrc(p.flags + r0, (uint32_t)nrows * 4u);
+        bstore4(rf, (uint32_t)ml * 4u, row_flag(t, act));
       } else {
         p.done_state[m] = ds;  // for the finishing kernel
       }
@@ -388,7 +494,8 @@ __device__ __forceinline__ void ctrl_gather(const PArgs& p, char* lds, int t, in
   if (tid < nrows) {
     const rsrc_t rf = make_rsrc(p.flags + r0, (uint32_t)nrows * 4u);
     unsigned spins = 0;
-    while ((int)(cload4(rf, (uint32_t)tid * 4u) - (uint32_t)(t + 1)) < 0) {
+    uint32_t f = cload4(rf, (uint32_t)tid * 4u);
+    while ((int)((f >> kFlagShift) - (uint32_t)(t + 1)) < 0) {
       if ((++spins & 63u) == 0) {
         if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
         if (spins >= kSpinLimit) {
@@ -397,9 +504,9 @@ __device__ __forceinline__ void ctrl_gather(const PArgs& p, char* lds, int t, in
         }
       }
       __builtin_amdgcn_s_sleep(1);
+      f = cload4(rf, (uint32_t)tid * 4u);
     }
-    const rsrc_t ra = make_rsrc(p.actions + (long)t * p.B + r0, (uint32_t)nrows * 4u);
-    row_act(p, lds)[tid] = (int)cload4(ra, (uint32_t)tid * 4u);
+    row_act(p, lds)[tid] = (int)(f & ((1u << kFlagShift) - 1u)) - 1;
   }
 }
 
@@ -445,15 +552,20 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
   const uint32_t lds0 = lds_addr(lds);
   const uint32_t ldxb = (uint32_t)p.ldx * 4u;
   const int rbv = (nrows + 15) >> 4;  // row blocks holding valid rows
+  // A work-group that owns rows of a rollout with at most 64 actions makes
+  // their decisions in wave 0 (ctrl_owner_w0) and deals the staging loads
+  // to waves 1..3 only; every other work-group deals them to all four.
+  const bool w0ctl = !NLL && p.A <= 64 && s < nrows;  // uniform
+  const int nwi = w0ctl ? 3 : 4, wi = w0ctl ? wave - 1 : wave;
   auto valid_in = [&](int c, int kq) { return max(0, min(min(9, nper - 9 * c), nks - kq * nper - 9 * c)); };
   auto wave_count = [&](int c) {
     int n = valid_in(c, 0) * rbv;
     if (KSPLIT > 1) n += valid_in(c, 1) * rbv;
-    return n > wave ? (n - wave + 3) >> 2 : 0;
+    return wi >= 0 && n > wi ? (n - wi + nwi - 1) / nwi : 0;
   };
   // the (slice, row block) of load k of chunk c of this wave
   auto piece = [&](int c, int k, int& sl, int& rb) {
-    int r = wave + 4 * k, kq = 0;
+    int r = wi + nwi * k, kq = 0;
     const int n0 = valid_in(c, 0) * rbv;
     if (KSPLIT > 1 && r >= n0) {
       kq = 1;
@@ -494,7 +606,13 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
     }
   }
   // rollout: this work-group's rows' decisions, under the staging loads
-  if constexpr (!NLL) ctrl_owner(p, cl, lds, t, r0, nrows);
+  if constexpr (!NLL) {
+    if (p.A <= 64) {
+      if (w0ctl && wave == 0) ctrl_owner_w0(p, cl, lds, t, r0, nrows);
+    } else {
+      ctrl_owner(p, cl, lds, t, r0, nrows);
+    }
+  }
 
   // two accumulator sets (even and odd K slices) and RB row blocks give
   // 2 RB independent MFMA chains, issued interleaved
@@ -921,7 +1039,11 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
     {
       const PArgs& q = fresh_args();
       ctrl_noise(q, cl, q.T, r0, nrows);
-      ctrl_owner(q, cl, lds, q.T, r0, nrows);
+      if (q.A <= 64) {
+        if ((threadIdx.x >> 6) == 0) ctrl_owner_w0(q, cl, lds, q.T, r0, nrows);
+      } else {
+        ctrl_owner(q, cl, lds, q.T, r0, nrows);
+      }
     }
     // final cell state for k_rollout_finish
     if (owner) {
