@@ -77,7 +77,7 @@ struct PArgs {
   uint32_t k0, k1, traj0, step0;
   float tau;
   float sig;  // scale of the normal deviate (sqrt(tau) with the sigma temperature, else 1)
-  int use_done, wat_lds;
+  int use_done, wat_lds, mres;
   float* X;             // rollout [2, B, ldx]; NLL [T+1, B, ldx]
   float* c;             // [B, H]: initial cell state in, final state out (rollout)
   int32_t* done_state;  // [B]
@@ -94,7 +94,7 @@ struct PArgs {
   float *h_trace, *c_trace;  // [T+1, B, H] or null (each on its own)
   float* g_trace;            // NLL: gate activations [T, B, 4H] or null
   // LDS carve-up (bytes)
-  int off_red, off_rows, off_wat, off_mdn, off_ctl, off_flags;
+  int off_red, off_rows, off_wat, off_mdn, off_ctl, off_flags, off_mres;
   // controller: Nc / 16 logit blocks; the h-part blocks run as tiles of
   // their own in mdn(t) (1) or inside the first mixture tiles (0)
   int ncb, ctl_sep;
@@ -761,9 +761,9 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
 // for nearly all of them before each MFMA (medium rollout 23.5 against 21.9
 // us per step).  `pre` is the lane's mixture noise drawn at the barrier
 // (null: draw it here).
-template <int QC, bool HZ, bool HC>
+template <int QC, bool HZ, bool HC, bool RES = false>
 __device__ __forceinline__ void mdn_tile(const PArgs& p, char* lds, int t, float* Xout, int r0, int nrows,
-                                         int J, int rb, int cb, const MdnNoise* pre) {
+                                         int J, int rb, int cb, const MdnNoise* pre, const uint4* res = nullptr) {
   constexpr int NB = (HZ ? QC : 0) + (HC ? 1 : 0);  // A blocks of the tile
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
   const int B = p.B, Z = p.Z, H = p.H;
@@ -816,7 +816,9 @@ __device__ __forceinline__ void mdn_tile(const PArgs& p, char* lds, int t, float
       bf[i] = cload16(rx, kin && ok ? (uint32_t)ml * ldxb + (uint32_t)Z * 4u + kb : kOffNone);
 #pragma unroll
       for (int q = 0; q < NB; ++q) {
-        if (HZ && q < QC)
+        if constexpr (RES)
+          af[i][q] = kin ? res[(sl * NB + q) * 64 + lane] : make_uint4(0u, 0u, 0u, 0u);
+        else if (HZ && q < QC)
           af[i][q] = bload16(rwm, kin ? (uint32_t)((16 * QC * J + 16 * q + r16) * p.ldh) * 4u + kb : kOffNone);
         else
           af[i][q] = bload16(rwc, kin ? (uint32_t)((16 * cb + r16) * p.ldk + Z) * 4u + kb : kOffNone);
@@ -874,6 +876,19 @@ __device__ __forceinline__ void mdn_phase(const PArgs& p, char* lds, int t, floa
   const int rbv = (nrows + 15) >> 4;
   const int zt = (p.Z >> 2) * rbv;
   const int nt = zt + (p.ctl_sep ? p.ncb * rbv : 0);
+  if (p.mres) {
+    // at most one tile per work-group, its weight fragments in LDS
+    const uint4* res = reinterpret_cast<const uint4*>(lds + p.off_mres);
+    if (s < zt) {
+      const int J = s / rbv, rb = s % rbv;
+      if (!p.ctl_sep && J < p.ncb) mdn_tile<QC, true, true, true>(p, lds, t, Xout, r0, nrows, J, rb, J, &pre, res);
+      else mdn_tile<QC, true, false, true>(p, lds, t, Xout, r0, nrows, J, rb, 0, &pre, res);
+    } else if (s < nt) {
+      const int c = s - zt;
+      mdn_tile<QC, false, true, true>(p, lds, t, Xout, r0, nrows, 0, c / p.ncb, c % p.ncb, nullptr, res);
+    }
+    return;
+  }
   for (int ti = s; ti < nt; ti += kMembers) {
     const MdnNoise* pn = ti == s ? &pre : nullptr;
     if (ti < zt) {
@@ -986,6 +1001,29 @@ __global__ void __launch_bounds__(256, 1) k_persist(const PArgs p) {
       if (tid == 0 && ml < nrows) p.flags[r0 + ml] = 0u;
     }
   }
+  if constexpr (!NLL) {
+    if (p.mres) {
+      // the weight fragments of this work-group's mdn tile (the same for
+      // every step), laid out as mdn_tile reads them
+      const int rbv = (nrows + 15) >> 4, zt = (p.Z >> 2) * rbv;
+      const int nt = zt + (p.ctl_sep ? p.ncb * rbv : 0);
+      if (s < nt) {
+        const bool hz = s < zt;
+        const int J = hz ? s / rbv : 0;
+        const bool hc = hz ? (!p.ctl_sep && J < p.ncb) : true;
+        const int cb = hz ? J : (s - zt) % p.ncb;
+        const int nb = (hz ? p.Q : 0) + (hc ? 1 : 0);
+        uint4* res = reinterpret_cast<uint4*>(lds + p.off_mres);
+        for (int idx = tid; idx < (p.H >> 4) * nb * 64; idx += 256) {
+          const int ln = idx & 63, q = (idx >> 6) % nb, sl = (idx >> 6) / nb;
+          const int kcol = sl * 16 + 4 * (ln >> 4);
+          const float* src = hz && q < p.Q ? p.Wm + (long)(16 * p.Q * J + 16 * q + (ln & 15)) * p.ldh + kcol
+                                           : p.Wc + (long)(16 * cb + (ln & 15)) * p.ldk + p.Z + kcol;
+          res[idx] = *reinterpret_cast<const uint4*>(src);
+        }
+      }
+    }
+  }
   if (p.wat_lds) {
     // this work-group's columns of the one-hot block: [A][NBC blocks][4 units][4 gates]
     float* wat = reinterpret_cast<float*>(lds + p.off_wat);
@@ -1078,8 +1116,8 @@ int persist_rb(int B) {
 struct PPlan {
   int rb = 0, nbc = 0;
   size_t lds = 0;
-  int off_red = 0, off_rows = 0, off_wat = 0, off_mdn = 0, off_ctl = 0, off_flags = 0;
-  int wat_lds = 0;
+  int off_red = 0, off_rows = 0, off_wat = 0, off_mdn = 0, off_ctl = 0, off_flags = 0, off_mres = 0;
+  int wat_lds = 0, mres = 0;
   int ncb = 0, ctl_sep = 0;
 };
 
@@ -1141,6 +1179,18 @@ bool plan(const Layout& L, int B, bool nll, PPlan& pl) {
   if (o + wat <= kLdsMax) {
     pl.wat_lds = 1;
     o += wat;
+  }
+  if (!nll) {
+    // with at most one mdn tile per work-group, its weight fragments stay in
+    // LDS for the whole call: [K slice][block][64 lanes] 16-byte pieces
+    const int rbv = (((B + kGroups - 1) / kGroups) + 15) / 16;
+    const int nt = (L.Z / 4) * rbv + (pl.ctl_sep ? pl.ncb * rbv : 0);
+    const size_t res = (size_t)(L.H / 16) * (L.Q + 1) * 1024;
+    if (nt <= kMembers && o + res <= kLdsMax) {
+      pl.off_mres = (int)o;
+      pl.mres = 1;
+      o += res;
+    }
   }
   if (o > kLdsMax) return false;
   o = o < kLdsMin ? kLdsMin : o;
@@ -1204,6 +1254,8 @@ PArgs base_args(const Packed& P, const PPlan& pl, int B, int T) {
   a.ldk = L.ldk; a.ldh = L.ldh; a.ldx = L.ldx;
   a.B = B; a.T = T; a.Bx = (B + kGroups - 1) / kGroups;
   a.wat_lds = pl.wat_lds;
+  a.mres = pl.mres;
+  a.off_mres = pl.off_mres;
   a.off_red = pl.off_red; a.off_rows = pl.off_rows; a.off_wat = pl.off_wat;
   a.off_mdn = pl.off_mdn; a.off_ctl = pl.off_ctl; a.off_flags = pl.off_flags;
   a.ncb = pl.ncb;
