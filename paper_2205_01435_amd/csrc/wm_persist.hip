@@ -780,14 +780,16 @@ __device__ __forceinline__ void gates_phase(const PArgs& p, GateState<RB, NBC>& 
 // for nearly all of them before each MFMA (medium rollout 23.5 against 21.9
 // us per step).  `pre` is the lane's mixture noise drawn at the barrier
 // (null: draw it here).
-template <int QC, bool HZ, bool HC, bool RES = false>
+// MS: the K loop's slices per wave at most (kMaxMS, or fewer where the
+// caller knows the call's H needs fewer)
+template <int QC, bool HZ, bool HC, bool RES = false, int MS = kMaxMS>
 __device__ __forceinline__ void mdn_tile(const PArgs& p, char* lds, int t, float* Xout, int r0, int nrows,
                                          int J, int rb, int cb, const MdnNoise* pre, const uint4* res = nullptr) {
   constexpr int NB = (HZ ? QC : 0) + (HC ? 1 : 0);  // A blocks of the tile
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, r16 = lane & 15;
   const int B = p.B, Z = p.Z, H = p.H;
   const int nsl = H >> 4;
-  const int per = (nsl + 3) >> 2;  // K slices per wave (<= kMaxMS)
+  const int per = (nsl + 3) >> 2;  // K slices per wave (<= MS)
   const int s0 = wave * per;
   const uint32_t step = p.step0 + (uint32_t)t;
   const uint32_t ldxb = (uint32_t)p.ldx * 4u;
@@ -825,10 +827,10 @@ __device__ __forceinline__ void mdn_tile(const PArgs& p, char* lds, int t, float
   // slice i's fragments are fetched three slices ahead of their MFMAs; the
   // scheduling barriers keep the compiler from hoisting every fetch (which
   // would not fit the registers next to the resident gate weights)
-  uint4 af[kMaxMS][NB], bf[kMaxMS];
+  uint4 af[MS][NB], bf[MS];
 #pragma unroll
-  for (int i = 0; i < kMaxMS + 3; ++i) {
-    if (i < kMaxMS) {
+  for (int i = 0; i < MS + 3; ++i) {
+    if (i < MS) {
       const int sl = s0 + i;
       const bool kin = i < per && sl < nsl;
       const uint32_t kb = (uint32_t)(sl * 16 + 4 * g) * 4u;
@@ -884,6 +886,21 @@ __device__ __forceinline__ void mdn_tile(const PArgs& p, char* lds, int t, float
   __syncthreads();
 }
 
+// Work-group s's single mdn tile, its weight fragments resident in LDS.
+template <int QC, int MS>
+__device__ __forceinline__ void mdn_phase_res(const PArgs& p, char* lds, int t, float* Xout, int r0, int nrows,
+                                              const MdnNoise& pre, const uint4* res, int zt, int nt, int rbv) {
+  const int s = blockIdx.x >> 3;
+  if (s < zt) {
+    const int J = s / rbv, rb = s % rbv;
+    if (!p.ctl_sep && J < p.ncb) mdn_tile<QC, true, true, true, MS>(p, lds, t, Xout, r0, nrows, J, rb, J, &pre, res);
+    else mdn_tile<QC, true, false, true, MS>(p, lds, t, Xout, r0, nrows, J, rb, 0, &pre, res);
+  } else if (s < nt) {
+    const int c = s - zt;
+    mdn_tile<QC, false, true, true, MS>(p, lds, t, Xout, r0, nrows, 0, c / p.ncb, c % p.ncb, nullptr, res);
+  }
+}
+
 // The tiles of one XCD: ZT = (Z/4) rbv mixture tiles, then (ctl_sep) the
 // ncb rbv controller tiles; without ctl_sep the mixture tiles of dim groups
 // J < ncb carry controller block J.  Work-group s takes tiles s, s + 32, ...
@@ -896,16 +913,12 @@ __device__ __forceinline__ void mdn_phase(const PArgs& p, char* lds, int t, floa
   const int zt = (p.Z >> 2) * rbv;
   const int nt = zt + (p.ctl_sep ? p.ncb * rbv : 0);
   if (p.mres) {
-    // at most one tile per work-group, its weight fragments in LDS
+    // at most one tile per work-group, its weight fragments in LDS; with
+    // H <= 256 the K loop is instantiated for its four slices per wave, so
+    // that no iteration is spent on slices the call does not have
     const uint4* res = reinterpret_cast<const uint4*>(lds + p.off_mres);
-    if (s < zt) {
-      const int J = s / rbv, rb = s % rbv;
-      if (!p.ctl_sep && J < p.ncb) mdn_tile<QC, true, true, true>(p, lds, t, Xout, r0, nrows, J, rb, J, &pre, res);
-      else mdn_tile<QC, true, false, true>(p, lds, t, Xout, r0, nrows, J, rb, 0, &pre, res);
-    } else if (s < nt) {
-      const int c = s - zt;
-      mdn_tile<QC, false, true, true>(p, lds, t, Xout, r0, nrows, 0, c / p.ncb, c % p.ncb, nullptr, res);
-    }
+    if (((p.H >> 4) + 3) >> 2 <= 4) mdn_phase_res<QC, 4>(p, lds, t, Xout, r0, nrows, pre, res, zt, nt, rbv);
+    else mdn_phase_res<QC, kMaxMS>(p, lds, t, Xout, r0, nrows, pre, res, zt, nt, rbv);
     return;
   }
   for (int ti = s; ti < nt; ti += kMembers) {
