@@ -2077,9 +2077,13 @@ template <> struct Cfgs<bf16_t> {
   static constexpr bool kXL = true;
   template <int NB> using CtrlLarge = Gemm<bf16_t, NB, 4, 4, 1, 1, 64, 2>;
   template <int NB> using CtrlLargeX = GemmD<bf16_t, NB, 2, 4, 1, 3>;
-  // 64-row controller tiles on eight waves, three stages: half the
-  // weight re-reads of the 32-row tiles
-  template <int NB> using CtrlXL = GemmD<bf16_t, NB, 2, 4, 2, 3>;
+  // 64-row controller tiles, three stages: half the weight re-reads of the
+  // 32-row tiles.  With five 64-output blocks (A up to 318) sixteen waves of
+  // one 16-row block each, which hide more of the chunk loads' latency than
+  // eight waves of two (xlarge controller 23.9 -> 22.6 us per step; four
+  // waves of four blocks: 32 us)
+  template <int NB> using CtrlXL = std::conditional_t<NB == 5, GemmD<bf16_t, NB, 1, 4, 4, 3>,
+                                                      GemmD<bf16_t, NB, 2, 4, 2, 3>>;
   static constexpr int WIDE_BKC = 128;
 };
 
