@@ -309,6 +309,10 @@ struct Gemm {
 // Same interface as Gemm (without a K split); Kpad must be a multiple of
 // the chunk.
 // ===========================================================================
+struct NoWork {
+  __device__ __forceinline__ void operator()() const {}
+};
+
 template <typename DT_, int NBW_, int MBW_, int WAVES_N_, int WAVES_M_, int STAGES_>
 struct GemmD {
   using DT = DT_;
@@ -349,9 +353,11 @@ struct GemmD {
   // of a wave holds gate i of 16 consecutive hidden units and lane (g, r16)
   // gets all four gates of units 4 g .. 4 g + 3 (the packed rows interleave
   // the gates per unit: row 4 u + q)
-  template <class S, bool GPERM = false>
+  // pre(): caller work that does not depend on the product, run once the
+  // first chunks' loads are issued, so that it fills their latency
+  template <class S, bool GPERM = false, class Pre = NoWork>
   __device__ __forceinline__ static void run(f32x4 (&acc)[NBW][MBW], const SrcX<DT>& w, const S& x,
-                                             int Kpad, DT* lds) {
+                                             int Kpad, DT* lds, Pre&& pre = Pre{}) {
     static_assert(!S::kTwo, "the direct core reads one activation matrix");
     static_assert(!GPERM || NBW == 4, "the gate permutation needs four blocks per wave");
     const int lane = threadIdx.x & 63;
@@ -388,6 +394,7 @@ struct GemmD {
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
       if (s < nk) issue(s);
+    pre();
 
     const int wni = wn(), wmi = wm();
     const int sw = (r16 >> 1) & 7;
@@ -417,6 +424,10 @@ struct GemmD {
     __syncthreads();  // LDS free for the caller's epilogue
   }
 };
+
+template <class C> struct IsGemmD : std::false_type {};
+template <typename DT, int NBW, int MBW, int WN, int WM, int ST>
+struct IsGemmD<GemmD<DT, NBW, MBW, WN, WM, ST>> : std::true_type {};
 
 // Static LDS a work-group may hold on gfx950 (160 KB per CU).
 constexpr int kLdsStatic = 160 * 1024;
@@ -1570,9 +1581,35 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
     }
   }
 
+  const Rng rng{p.k0, p.k1};
+  const uint32_t traj = p.traj0 + (uint32_t)m;
+  const bool flat_pick = want_action && row_ok && p.N == 0;
+  // With at most five Philox blocks per thread on the direct core, the
+  // Gumbel noise of all of the thread's actions is drawn while the GEMM's
+  // first chunks load (it does not depend on the logits).  It is drawn
+  // whatever the mask: the mask words are still in flight there, and
+  // waiting for them would wait for the chunks too.
+  constexpr bool kPre = IsGemmD<C>::value && MAXB <= 5;
+  float gq[kPre ? MAXB : 1][4];
+  auto draw = [&]() {
+    if constexpr (kPre) {
+#pragma unroll
+      for (int b = 0; b < MAXB; ++b) {
+        if (flat_pick && 4 * b < apt && a0 + 4 * b < A) {
+          const uint4 wd = rng.block((uint32_t)((a0 + 4 * b) >> 2), p.step, traj, STREAM_CONTROLLER);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) gq[b][v] = gumbel(word_to_uniform(word_of(wd, v)));
+        }
+      }
+    }
+  };
+
   f32x4 acc[NBW][MBW];
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wc), p.ldk, p.ldk, 0, p.Nc, p.Nc);
-  C::run(acc, w, ctrl_src<S>(p, m0, BM), (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
+  if constexpr (kPre)
+    C::run(acc, w, ctrl_src<S>(p, m0, BM), (int)p.ldk, reinterpret_cast<DT*>(lds_raw), draw);
+  else
+    C::run(acc, w, ctrl_src<S>(p, m0, BM), (int)p.ldk, reinterpret_cast<DT*>(lds_raw));
   float* E = reinterpret_cast<float*>(lds_raw);
   if (C::kw() == 0) {
     const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
@@ -1587,16 +1624,15 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
   __syncthreads();
 
   const float* lg = E + r * ELD;
-  const Rng rng{p.k0, p.k1};
-  const uint32_t traj = p.traj0 + (uint32_t)m;
   float best = -INFINITY, mx = -INFINITY;
   int bidx = -1;
-  if (want_action && row_ok && p.N == 0) {
+  if (flat_pick) {
 #pragma unroll
     for (int b = 0; b < MAXB; ++b) {
       if (mk[b] == 0) continue;  // no valid action in the block (or outside the range)
       const int a = a0 + 4 * b;
-      const uint4 wd = rng.block((uint32_t)(a >> 2), p.step, traj, STREAM_CONTROLLER);
+      uint4 wd = make_uint4(0u, 0u, 0u, 0u);
+      if constexpr (!kPre) wd = rng.block((uint32_t)(a >> 2), p.step, traj, STREAM_CONTROLLER);
       const float4 l4 = *reinterpret_cast<const float4*>(lg + a);
       const float4 b4 = *reinterpret_cast<const float4*>(p.bc + a);
       const float lv[4] = {l4.x + b4.x, l4.y + b4.y, l4.z + b4.z, l4.w + b4.w};
@@ -1604,7 +1640,10 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
       for (int v = 0; v < 4; ++v) {
         if ((mk[b] >> (8 * v)) & 0xffu) {
           mx = fmaxf(mx, lv[v]);
-          const float sc = lv[v] + gumbel(word_to_uniform(word_of(wd, v)));
+          float gv;
+          if constexpr (kPre) gv = gq[b][v];
+          else gv = gumbel(word_to_uniform(word_of(wd, v)));
+          const float sc = lv[v] + gv;
           if (sc > best) { best = sc; bidx = a + v; }
         }
       }
