@@ -948,8 +948,36 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
   }
   const SrcX<DT> w(reinterpret_cast<const DT*>(p.Wm), p.ldh, p.ldh, n0, C::BN, p.Nm);
   const SrcX<DT> x(reinterpret_cast<const DT*>(p.x) + p.Z, p.ldx, p.ldx - p.Z, m0, C::BM, p.M);
+  const Rng rng{p.k0, p.k1};
+  // The four lanes of a row (lane groups g, dims 4J + g) need the same
+  // stream-2 block.  With four row blocks per lane, lane group g draws the
+  // block and both Box-Muller pairs for row block g only, and every lane
+  // reads its deviates from the drawing lanes (shuffles, all lanes active),
+  // instead of each lane drawing all four blocks.  On the direct core these
+  // draws run while the GEMM's first chunks load: they do not depend on the
+  // product.  (Drawing the component noise there too, for every row, frozen
+  // or not, made the xlarge mixture kernel slower: 108.7 against 107.3 us.)
+  constexpr bool kPre = IsGemmD<C>::value && MBW == 4;
+  float eps[MBW];
+  auto draw_eps = [&]() {
+    if constexpr (MBW == 4) {
+      const float4 e = gauss_group(rng, p.step, p.traj0 + (uint32_t)(m0 + (wmi * MBW + g) * 16 + (lane & 15)), J);
+#pragma unroll
+      for (int jj = 0; jj < MBW; ++jj) {
+        const int src = jj * 16 + (lane & 15);
+        const float v0 = __shfl(e.x, src), v1 = __shfl(e.y, src), v2 = __shfl(e.z, src), v3 = __shfl(e.w, src);
+        eps[jj] = g == 0 ? v0 : (g == 1 ? v1 : (g == 2 ? v2 : v3));
+      }
+    }
+  };
+  auto pre = [&]() {
+    if (!p.nll_mode) draw_eps();
+  };
   f32x4 acc[Q][MBW];
-  C::run(acc, w, x, (int)p.ldh, reinterpret_cast<DT*>(lds_raw));
+  if constexpr (kPre)
+    C::run(acc, w, x, (int)p.ldh, reinterpret_cast<DT*>(lds_raw), pre);
+  else
+    C::run(acc, w, x, (int)p.ldh, reinterpret_cast<DT*>(lds_raw));
   const bool owner = C::kw() == 0;  // holds the summed tile
 
   if (head_tile) {
@@ -977,22 +1005,7 @@ __global__ void __launch_bounds__(C::NT) k_mdn(const MdnArgs p) {
 
   if (!p.nll_mode) {
     if (!owner) return;  // no barrier below
-    const Rng rng{p.k0, p.k1};
-    // The four lanes of a row (lane groups g, dims 4J + g) need the same
-    // stream-2 block.  With four row blocks per lane, lane group g draws the
-    // block and both Box-Muller pairs for row block g only, and every lane
-    // reads its deviates from the drawing lanes (shuffles, all lanes active),
-    // instead of each lane drawing all four blocks.
-    float eps[MBW];
-    if constexpr (MBW == 4) {
-      const float4 e = gauss_group(rng, p.step, p.traj0 + (uint32_t)(m0 + (wmi * MBW + g) * 16 + (lane & 15)), J);
-#pragma unroll
-      for (int jj = 0; jj < MBW; ++jj) {
-        const int src = jj * 16 + (lane & 15);
-        const float v0 = __shfl(e.x, src), v1 = __shfl(e.y, src), v2 = __shfl(e.z, src), v3 = __shfl(e.w, src);
-        eps[jj] = g == 0 ? v0 : (g == 1 ? v1 : (g == 2 ? v2 : v3));
-      }
-    }
+    if constexpr (!kPre) draw_eps();
 #pragma unroll
     for (int jj = 0; jj < MBW; ++jj) {
       const int m = m0 + (wmi * MBW + jj) * 16 + (lane & 15);
