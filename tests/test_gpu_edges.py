@@ -83,6 +83,42 @@ def test_ragged_shapes_reanchored(B, T, Z, H, A, K, dtype):
                                tau=1.3, dtype=dtype) <= parity.free_run_cap(B)
 
 
+# Staged controller tiles with one or two 64-output blocks (more than 1024
+# rows, at most 126 actions), where each thread's Gumbel noise is drawn while
+# the GEMM's first chunks load; the last row tile is ragged.  nrows: rows
+# re-anchored against the oracle (None: all).
+FEW_ACTIONS = [
+    (2048 + 7, 3, 32, 256, 60, 3, "bf16", None),   # 32-row tiles, one output block
+    (2048 + 7, 3, 32, 256, 100, 3, "bf16", None),  # 32-row tiles, two output blocks
+    (2048 + 7, 3, 32, 256, 100, 3, "fp32", None),  # the same on the fp32 core
+    (16384 + 3, 2, 32, 128, 60, 2, "bf16", 48),    # 64-row tiles
+]
+
+
+@pytest.mark.parametrize("B,T,Z,H,A,K,dtype,nrows", FEW_ACTIONS)
+def test_few_action_controller_tiles(B, T, Z, H, A, K, dtype, nrows, monkeypatch):
+    say("few-action controller tiles", B, T, Z, H, A, K, dtype)
+    monkeypatch.setenv("WM_PERSISTENT", "0")  # the multi-launch kernels
+    w, inp = _case(B, T, Z, H, A, K, dtype)
+    mask = inp["mask"].copy()
+    mask[B - 2] = 0  # a row without a valid action, in the ragged tile
+    m = wmlib.pack(inp["weights"], Z, H, A, K, dtype)
+    b = wmlib.rollout(m, _t(inp["z0"]), _t(mask), T=T, seed=37, tau=1.0, done=True, trace=True)
+    torch.cuda.synchronize()
+    rows = np.arange(B) if nrows is None else np.unique(
+        np.concatenate([np.linspace(0, B - 1, nrows).astype(np.int64), np.arange(B - 6, B)]))
+    ri = torch.from_numpy(rows).cuda()
+    keys = ("z_out", "actions", "rewards", "dones", "h_trace", "c_trace")
+    g = {k: getattr(b, k)[:, ri].cpu().numpy() for k in keys}
+    del b
+    ties, live = parity.reanchored(w.dims, inp["weights"], mask[rows], g, seed=37, tau=1.0,
+                                   done_flag=True, dtype=dtype, traj=rows)
+    say("ties", ties.mismatches, "of", ties.draws, "live", live)
+    assert live > 0
+    k = int(np.searchsorted(rows, B - 2))
+    assert g["actions"][0, k] == -1 and np.all(g["dones"][:, k] == 1)
+
+
 def test_resume_and_state_inputs_bit_exact():
     """rollout(T1) then rollout(T2, step0=T1, state) equals rollout(T1+T2)."""
     w, inp = _case(48, 7, 16, 64, 9, 3, "fp32")
