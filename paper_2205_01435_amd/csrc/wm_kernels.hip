@@ -1597,12 +1597,13 @@ __global__ void __launch_bounds__(C::NT) k_ctrl(const CtrlArgs p) {
   const Rng rng{p.k0, p.k1};
   const uint32_t traj = p.traj0 + (uint32_t)m;
   const bool flat_pick = want_action && row_ok && p.N == 0;
-  // With at most five Philox blocks per thread on the direct core, the
-  // Gumbel noise of all of the thread's actions is drawn while the GEMM's
-  // first chunks load (it does not depend on the logits).  It is drawn
-  // whatever the mask: the mask words are still in flight there, and
-  // waiting for them would wait for the chunks too.
-  constexpr bool kPre = IsGemmD<C>::value && MAXB <= 5;
+  // On the sixteen-wave direct tile, the Gumbel noise of all of the thread's
+  // actions is drawn while the GEMM's first chunks load (it does not depend
+  // on the logits).  It is drawn whatever the mask: the mask words are still
+  // in flight there, and waiting for them would wait for the chunks too.
+  // (On the four-wave 32-row tiles of the large rollout the same draw made
+  // the controller slower, 12.0 -> 12.8 us per step.)
+  constexpr bool kPre = IsGemmD<C>::value && C::NT >= 1024 && MAXB <= 5;
   float gq[kPre ? MAXB : 1][4];
   auto draw = [&]() {
     if constexpr (kPre) {

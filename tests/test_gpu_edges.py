@@ -84,9 +84,8 @@ def test_ragged_shapes_reanchored(B, T, Z, H, A, K, dtype):
 
 
 # Staged controller tiles with one or two 64-output blocks (more than 1024
-# rows, at most 126 actions), where each thread's Gumbel noise is drawn while
-# the GEMM's first chunks load; the last row tile is ragged.  nrows: rows
-# re-anchored against the oracle (None: all).
+# rows, at most 126 actions), on four and eight waves; the last row tile is
+# ragged.  nrows: rows re-anchored against the oracle (None: all).
 FEW_ACTIONS = [
     (2048 + 7, 3, 32, 256, 60, 3, "bf16", None),   # 32-row tiles, one output block
     (2048 + 7, 3, 32, 256, 100, 3, "bf16", None),  # 32-row tiles, two output blocks
